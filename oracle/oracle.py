@@ -1,0 +1,420 @@
+"""TemporalGS CPU oracle driver -- TEST INFRASTRUCTURE ONLY.
+
+Composes the single-threaded C stages of ``tgs_oracle.c`` in the order the
+paper gives them:
+
+* a full 3DGS frame (Sec. III-A): per-Gaussian preprocess, per-tile lists
+  sorted front to back, alpha blending;
+* a temporal sequence (Sec. III-B): reference frames build the temporal
+  priors (Sec. III-C: TGB by Eq. 1/2, TAB, temporal Gaussian buffer, adaptive
+  frustum), the frames in between use them through temporal dynamic culling
+  (Sec. III-D) and selective rendering (Sec. III-E, Eq. 3/4), and pseudo
+  reference frames are inserted by the interval and eta rules (Sec. III-E,
+  Sec. IV-B).
+
+Only tests, the package smoke check and the benchmark's CPU-baseline leg may
+import this module.  It shares no code with the HIP library; the only common
+inputs are the seeded arrays of ``paper_2607_03390_amd.synth``, passed in by
+the caller.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle.so")
+SRC_PATH = os.path.join(HERE, "tgs_oracle.c")
+GCC_CMD = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", LIB_PATH, SRC_PATH, "-lm"]
+
+NOHIT = np.float32(1001.0)          # z_far + epsilon (Sec. III-C)
+NEAR_CULLED, AFC_CULLED, TOC_CULLED, DEGENERATE, NO_TILES, VISIBLE = range(6)
+TRUE_REF, PSEUDO_REF, TGS_FRAME = 0, 1, 2
+
+
+class _Cam(C.Structure):
+    _fields_ = [("w2c", C.c_float * 16), ("fx", C.c_float), ("fy", C.c_float),
+                ("cx", C.c_float), ("cy", C.c_float), ("width", C.c_int32),
+                ("height", C.c_int32)]
+
+
+class _Cull(C.Structure):
+    _fields_ = [("afc", C.c_int32), ("fbox", C.c_float * 4), ("toc", C.c_int32),
+                ("dmin", C.c_void_p), ("smax", C.c_void_p), ("g_rendered", C.c_void_p),
+                ("lambda1", C.c_float), ("lambda2", C.c_float)]
+
+
+_LIB = None
+
+
+def build():
+    import subprocess
+    subprocess.check_call(GCC_CMD)
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = C.CDLL(LIB_PATH)
+        L.or_gaussians.restype = C.c_int32
+        L.or_tile_counts.restype = C.c_int64
+        L.or_blend.restype = C.c_int64
+        L.or_afc_bounds.restype = C.c_int32
+        _LIB = L
+    return _LIB
+
+
+def _p(a):
+    return C.c_void_p(0) if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _cam(cam) -> _Cam:
+    c = _Cam()
+    w = np.ascontiguousarray(cam.w2c, np.float32).ravel()
+    for i in range(16):
+        c.w2c[i] = float(w[i])
+    c.fx, c.fy, c.cx, c.cy = cam.fx, cam.fy, cam.cx, cam.cy
+    c.width, c.height = cam.width, cam.height
+    return c
+
+
+def _intr(cam):
+    return np.array([cam.fx, cam.fy, cam.cx, cam.cy], np.float32)
+
+
+@dataclass
+class Params:
+    """Method parameters (Sec. III-C..E, Sec. IV-B)."""
+    lambda_tdc: int = 50
+    lambda_sr: int = 5
+    eta: float = 0.40
+    lambda1: float = 3.0
+    lambda2: float = 0.0
+    z_near: float = 0.2
+    enable_afc: bool = True
+    enable_toc: bool = True
+    enable_sr: bool = True
+    force_all_dirty: bool = False
+
+
+# --------------------------------------------------------------------------
+# stages
+# --------------------------------------------------------------------------
+
+def relative_pose(w2c_ref, w2c_cur):
+    """M = W_cur W_ref^-1 and its inverse as fp32 3x4 (Eq. 3)."""
+    m = np.zeros(12, np.float32)
+    mi = np.zeros(12, np.float32)
+    lib().or_relative_pose(_p(np.ascontiguousarray(w2c_ref, np.float32).ravel()),
+                           _p(np.ascontiguousarray(w2c_cur, np.float32).ravel()), _p(m), _p(mi))
+    return m, mi
+
+
+def camera_centre(w2c):
+    c = np.zeros(3, np.float32)
+    lib().or_camera_centre(_p(np.ascontiguousarray(w2c, np.float32).ravel()), _p(c))
+    return c
+
+
+def quat_to_rot(q):
+    R = np.zeros(9, np.float32)
+    lib().or_quat_to_rot(_p(np.ascontiguousarray(q, np.float32)), _p(R))
+    return R.reshape(3, 3)
+
+
+def cov3d(scale, q):
+    S = np.zeros(9, np.float32)
+    lib().or_cov3d(_p(np.ascontiguousarray(scale, np.float32)),
+                   _p(np.ascontiguousarray(q, np.float32)), _p(S))
+    return S.reshape(3, 3)
+
+
+def sh_basis(deg, d):
+    out = np.zeros(16, np.float64)
+    lib().or_sh_basis(C.c_int(deg), C.c_double(d[0]), C.c_double(d[1]), C.c_double(d[2]), _p(out))
+    return out[:(deg + 1) ** 2]
+
+
+def gaussians(scene, cam, z_near=0.2, cull=None):
+    """Per-Gaussian stage: near cull, projection, AFC/TOC (if ``cull``), 2D
+    covariance, radius, tile rectangle, SH colour."""
+    n = scene.n
+    out = dict(status=np.zeros(n, np.int32), newly_visible=np.zeros(n, np.uint8),
+               mean2d=np.zeros((n, 2), np.float32), ndc=np.zeros((n, 2), np.float32),
+               depth=np.zeros(n, np.float32), conic=np.zeros((n, 3), np.float32),
+               radius=np.zeros(n, np.float32), rect=np.zeros((n, 4), np.int32),
+               rgb=np.zeros((n, 3), np.float64))
+    means = np.ascontiguousarray(scene.means, np.float32)
+    scales = np.ascontiguousarray(scene.scales, np.float32)
+    rots = np.ascontiguousarray(scene.rotations, np.float32)
+    sh = np.ascontiguousarray(scene.sh, np.float32)
+    cs = None
+    keep = []
+    if cull is not None:
+        cs = _Cull()
+        cs.afc = int(bool(cull.get("afc", False)))
+        fb = cull.get("fbox", np.zeros(4, np.float32))
+        for k in range(4):
+            cs.fbox[k] = float(fb[k])
+        cs.toc = int(bool(cull.get("toc", False)))
+        if cs.toc:
+            dmin = np.ascontiguousarray(cull["dmin"], np.float32)
+            smax = np.ascontiguousarray(cull["smax"], np.float32)
+            gr = np.ascontiguousarray(cull["g_rendered"], np.uint8)
+            keep += [dmin, smax, gr]
+            cs.dmin, cs.smax, cs.g_rendered = _p(dmin), _p(smax), _p(gr)
+        cs.lambda1 = float(cull.get("lambda1", 3.0))
+        cs.lambda2 = float(cull.get("lambda2", 0.0))
+    cam_s = _cam(cam)
+    out["n_survivors"] = int(lib().or_gaussians(
+        C.c_int32(n), C.c_int32(scene.sh_degree), _p(means), _p(scales), _p(rots), _p(sh),
+        C.byref(cam_s), C.c_float(z_near), C.byref(cs) if cs is not None else None,
+        _p(out["status"]), _p(out["newly_visible"]), _p(out["mean2d"]), _p(out["ndc"]),
+        _p(out["depth"]), _p(out["conic"]), _p(out["radius"]), _p(out["rect"]), _p(out["rgb"])))
+    out["opacity"] = np.ascontiguousarray(scene.opacities, np.float32)
+    return out
+
+
+def tile_lists(g, TX, TY, tile_sel=None):
+    """Per-tile front-to-back lists: (tile_start[TX*TY+1], items[K])."""
+    n = g["status"].shape[0]
+    ts = np.zeros(TX * TY + 1, np.int64)
+    sel = None if tile_sel is None else np.ascontiguousarray(tile_sel, np.uint8).ravel()
+    K = lib().or_tile_counts(C.c_int32(n), _p(g["status"]), _p(g["rect"]), C.c_int32(TX),
+                             C.c_int32(TY), _p(sel), _p(ts))
+    items = np.zeros(max(K, 1), np.int32)
+    lib().or_tile_lists(C.c_int32(n), _p(g["status"]), _p(g["rect"]), _p(g["depth"]),
+                        C.c_int32(TX), C.c_int32(TY), _p(sel), _p(ts), _p(items))
+    return ts, items[:K]
+
+
+def blend(W, H, ts, items, g, render_tiles=None):
+    """Alpha blending of the listed tiles (all if None)."""
+    n = g["status"].shape[0]
+    rgb = np.zeros((3, H, W), np.float64)
+    D = np.full((H, W), float(NOHIT), np.float64)
+    S = np.zeros((H, W), np.float64)
+    A = np.zeros((H, W), np.float64)
+    mpos = np.full((H, W), -1, np.int32)
+    maxw = np.zeros(n, np.float32)
+    gc = np.zeros(n, np.uint8)
+    gu = np.zeros(n, np.uint8)
+    rt = None if render_tiles is None else np.ascontiguousarray(render_tiles, np.int32)
+    items_c = np.ascontiguousarray(items if items.size else np.zeros(1, np.int32), np.int32)
+    E = lib().or_blend(C.c_int32(W), C.c_int32(H), _p(ts), _p(items_c), _p(rt),
+                       C.c_int32(0 if rt is None else rt.size), _p(g["mean2d"]), _p(g["conic"]),
+                       _p(g["opacity"]), _p(g["depth"]), _p(g["rgb"]), _p(rgb), _p(D), _p(S),
+                       _p(A), _p(mpos), _p(maxw), _p(gc), _p(gu))
+    return dict(rgb=rgb, D=D, sigma=S, alpha=A, margin_pos=mpos, maxw=maxw,
+                g_certain=gc, g_uncertain=gu, pairs=int(E))
+
+
+def blend_bruteforce(W, H, g):
+    rgb = np.zeros((3, H, W), np.float64)
+    D = np.zeros((H, W), np.float64)
+    S = np.zeros((H, W), np.float64)
+    A = np.zeros((H, W), np.float64)
+    n = g["status"].shape[0]
+    lib().or_blend_bruteforce(C.c_int32(W), C.c_int32(H), C.c_int32(n), _p(g["status"]),
+                              _p(g["rect"]), _p(g["mean2d"]), _p(g["conic"]), _p(g["opacity"]),
+                              _p(g["depth"]), _p(g["rgb"]), _p(rgb), _p(D), _p(S), _p(A))
+    return dict(rgb=rgb, D=D, sigma=S, alpha=A)
+
+
+def afc_bounds(g_rendered, ndc):
+    fb = np.zeros(4, np.float32)
+    cnt = lib().or_afc_bounds(C.c_int32(g_rendered.size),
+                              _p(np.ascontiguousarray(g_rendered, np.uint8)),
+                              _p(np.ascontiguousarray(ndc, np.float32)), _p(fb))
+    return fb, int(cnt)
+
+
+def forward_warp(D, S, kref, kcur, M, z_near=0.2):
+    H, W = D.shape
+    dmin = np.zeros((H, W), np.float32)
+    smax = np.zeros((H, W), np.float32)
+    lib().or_forward_warp(C.c_int32(W), C.c_int32(H), _p(np.ascontiguousarray(D, np.float32)),
+                          _p(np.ascontiguousarray(S, np.float32)), _p(kref), _p(kcur),
+                          _p(np.ascontiguousarray(M, np.float32)), C.c_float(z_near),
+                          _p(dmin), _p(smax))
+    return dmin, smax
+
+
+def depth_fill(dmin):
+    H, W = dmin.shape
+    out = np.zeros((H, W), np.float32)
+    lib().or_depth_fill(C.c_int32(W), C.c_int32(H), _p(np.ascontiguousarray(dmin, np.float32)),
+                        _p(out))
+    return out
+
+
+def backward_query(dfill, kcur, kref, Minv, z_near=0.2):
+    H, W = dfill.shape
+    TX, TY = (W + 15) // 16, (H + 15) // 16
+    uv = np.zeros((H, W, 2), np.float32)
+    matched = np.zeros((H, W), np.uint8)
+    um = np.zeros((TY, TX), np.uint8)
+    lib().or_backward_query(C.c_int32(W), C.c_int32(H),
+                            _p(np.ascontiguousarray(dfill, np.float32)), _p(kcur), _p(kref),
+                            _p(np.ascontiguousarray(Minv, np.float32)), C.c_float(z_near),
+                            _p(uv), _p(matched), _p(um))
+    return uv, matched, um
+
+
+def occluded_tiles(W, H, g):
+    TX, TY = (W + 15) // 16, (H + 15) // 16
+    oc = np.zeros((TY, TX), np.uint8)
+    ocm = np.zeros((TY, TX), np.uint8)
+    n = g["status"].shape[0]
+    lib().or_occluded_tiles(C.c_int32(W), C.c_int32(H), C.c_int32(n), _p(g["newly_visible"]),
+                            _p(g["status"]), _p(g["rect"]), _p(g["mean2d"]), _p(g["conic"]),
+                            _p(g["opacity"]), _p(oc), _p(ocm))
+    return oc, ocm
+
+
+def stitch(tab, uv, tile_sel, out_rgb):
+    _, H, W = tab.shape
+    lib().or_stitch(C.c_int32(W), C.c_int32(H), _p(np.ascontiguousarray(tab, np.float32)),
+                    _p(np.ascontiguousarray(uv, np.float32)),
+                    _p(np.ascontiguousarray(tile_sel, np.uint8)), _p(out_rgb))
+    return out_rgb
+
+
+# --------------------------------------------------------------------------
+# a full 3DGS frame
+# --------------------------------------------------------------------------
+
+def render_full(scene, cam, z_near=0.2, cull=None):
+    W, H = cam.width, cam.height
+    TX, TY = (W + 15) // 16, (H + 15) // 16
+    g = gaussians(scene, cam, z_near, cull)
+    ts, items = tile_lists(g, TX, TY)
+    b = blend(W, H, ts, items, g)
+    b.update(g=g, tile_start=ts, items=items, K=int(items.size),
+             n_survivors=g["n_survivors"])
+    return b
+
+
+# --------------------------------------------------------------------------
+# the temporal sequence
+# --------------------------------------------------------------------------
+
+class TemporalOracle:
+    """Reference / pseudo-reference / TemporalGS frames over a camera stream."""
+
+    def __init__(self, scene, width, height, params: Params | None = None):
+        self.scene = scene
+        self.W, self.H = width, height
+        self.TX, self.TY = (width + 15) // 16, (height + 15) // 16
+        self.p = params or Params()
+        self.reset()
+
+    def reset(self):
+        self.frame_index = 0
+        self.since_true = 0
+        self.since_ref = 0
+        self.force_pseudo = False
+        self.D = self.S = self.tab = self.g_rendered = None
+        self.fbox = np.zeros(4, np.float32)
+        self.ref_w2c = None
+        self.ref_intr = None
+
+    # schedule (Sec. III-B, III-E, IV-B)
+    def next_kind(self):
+        if self.frame_index == 0 or self.since_true >= self.p.lambda_tdc:
+            return TRUE_REF
+        if self.force_pseudo or self.since_ref >= self.p.lambda_sr:
+            return PSEUDO_REF
+        return TGS_FRAME
+
+    def import_state(self, D, S, tab, g_rendered, fbox, ref_w2c, ref_intr, frame_index,
+                     since_true, since_ref, force_pseudo):
+        self.D = np.array(D, np.float32)
+        self.S = np.array(S, np.float32)
+        self.tab = np.array(tab, np.float32)
+        self.g_rendered = np.array(g_rendered, np.uint8)
+        self.fbox = np.array(fbox, np.float32)
+        self.ref_w2c = np.array(ref_w2c, np.float32).reshape(4, 4)
+        self.ref_intr = np.array(ref_intr, np.float32)
+        self.frame_index = int(frame_index)
+        self.since_true = int(since_true)
+        self.since_ref = int(since_ref)
+        self.force_pseudo = bool(force_pseudo)
+
+    def render(self, cam, kind=None):
+        kind = self.next_kind() if kind is None else kind
+        if kind == TGS_FRAME:
+            out = self._tgs_frame(cam)
+        else:
+            out = self._reference(cam, kind)
+        out["kind"] = kind
+        self.advance(kind, out["n_selected"])
+        return out
+
+    def advance(self, kind, n_selected):
+        """Counter update after a frame of ``kind`` (Sec. III-B, III-E)."""
+        self.frame_index += 1
+        if kind == TRUE_REF:
+            self.since_true = 1
+            self.since_ref = 1
+            self.force_pseudo = False
+        elif kind == PSEUDO_REF:
+            self.since_true += 1
+            self.since_ref = 1
+            self.force_pseudo = False
+        else:
+            self.since_true += 1
+            self.since_ref += 1
+            if self.p.enable_sr:
+                # adaptive reference insertion: "exceeds" eta of all tiles
+                self.force_pseudo = n_selected > self.p.eta * self.TX * self.TY
+
+    def _reference(self, cam, kind):
+        cull = None
+        if kind == PSEUDO_REF and self.p.enable_afc:
+            cull = dict(afc=True, fbox=self.fbox)
+        out = render_full(self.scene, cam, self.p.z_near, cull)
+        # temporal priors (Sec. III-C)
+        self.D = out["D"].astype(np.float32)
+        self.S = out["sigma"].astype(np.float32)
+        self.tab = out["rgb"].astype(np.float32)
+        self.g_rendered = (out["maxw"] > 0).astype(np.uint8)
+        if kind == TRUE_REF:
+            self.fbox, _ = afc_bounds(self.g_rendered, out["g"]["ndc"])
+        self.ref_w2c = np.array(cam.w2c, np.float32)
+        self.ref_intr = _intr(cam)
+        out["tile_sel"] = np.ones((self.TY, self.TX), np.uint8)
+        out["n_selected"] = self.TX * self.TY
+        return out
+
+    def _tgs_frame(self, cam):
+        p = self.p
+        W, H = self.W, self.H
+        kcur = _intr(cam)
+        M, Minv = relative_pose(self.ref_w2c, cam.w2c)
+        dmin, smax = forward_warp(self.D, self.S, self.ref_intr, kcur, M, p.z_near)
+        dfill = depth_fill(dmin)
+        uv, matched, um = backward_query(dfill, kcur, self.ref_intr, Minv, p.z_near)
+        cull = dict(afc=p.enable_afc, fbox=self.fbox, toc=p.enable_toc, dmin=dmin, smax=smax,
+                    g_rendered=self.g_rendered, lambda1=p.lambda1, lambda2=p.lambda2)
+        g = gaussians(self.scene, cam, p.z_near, cull)
+        oc, oc_margin = occluded_tiles(W, H, g)
+        if p.enable_sr and not p.force_all_dirty:
+            sel = (oc | um).astype(np.uint8)
+        else:
+            sel = np.ones((self.TY, self.TX), np.uint8)
+        render_tiles = np.flatnonzero(sel.ravel()).astype(np.int32)
+        ts, items = tile_lists(g, self.TX, self.TY, sel)
+        b = blend(W, H, ts, items, g, render_tiles)
+        stitch(self.tab, uv, sel, b["rgb"])
+        b.update(g=g, tile_start=ts, items=items, K=int(items.size), tile_sel=sel,
+                 oc=oc, oc_margin=oc_margin, um=um, dmin=dmin, smax=smax, dfill=dfill, uv=uv,
+                 matched=matched, n_selected=int(render_tiles.size),
+                 n_survivors=g["n_survivors"], M=M, Minv=Minv)
+        return b

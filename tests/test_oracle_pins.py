@@ -1,0 +1,557 @@
+"""Pins of the CPU oracle against closed forms, brute force, invariants and
+the paper's printed schedule numbers.  None of these calls the HIP library.
+
+Each test targets a plausible mistake: a dropped low-pass term, a transposed
+rotation, a wrong SH sign or constant, a flipped sort order, a wrong warp
+direction, an off-by-one fill rule, a mis-counted schedule interval.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_03390_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _cam(w2c, W, H, f=None):
+    f = synth.focal_for_height(H) if f is None else f
+    return synth.Camera(np.asarray(w2c, np.float32), float(np.float32(f)), float(np.float32(f)),
+                        (W - 1) / 2.0, (H - 1) / 2.0, W, H)
+
+
+def _scene(means, scales, rots=None, opac=None, dc=None, deg=0):
+    n = len(means)
+    means = np.asarray(means, np.float32).reshape(n, 3)
+    scales = np.asarray(scales, np.float32).reshape(n, 3)
+    rots = np.tile(np.array([1, 0, 0, 0], np.float32), (n, 1)) if rots is None else np.asarray(rots, np.float32)
+    opac = np.full(n, 0.9, np.float32) if opac is None else np.asarray(opac, np.float32)
+    k = (deg + 1) ** 2
+    sh = np.zeros((n, k, 3), np.float32)
+    if dc is not None:
+        sh[:, 0, :] = np.asarray(dc, np.float32).reshape(n, 3)
+    return synth.Scene(means, scales, rots, opac, sh, deg)
+
+
+C0 = 1.0 / (2.0 * math.sqrt(math.pi))
+
+
+# --------------------------------------------------------------------------
+# projection and covariance (Sec. III-A)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("s,Z", [(0.01, 2.0), (0.05, 4.0), (0.2, 9.0)])
+def test_cov2d_isotropic_on_axis(s, Z):
+    W = H = 64
+    cam = _cam(np.eye(4), W, H)
+    f = cam.fx
+    g = O.gaussians(_scene([[0, 0, Z]], [[s, s, s]]), cam)
+    var = (f * s / Z) ** 2 + 0.3
+    np.testing.assert_allclose(g["conic"][0], [1 / var, 0.0, 1 / var], rtol=2e-6, atol=1e-12)
+    assert g["radius"][0] == math.ceil(3 * math.sqrt(var) - 1e-6) or abs(3 * math.sqrt(var) - round(3 * math.sqrt(var))) < 1e-4
+    np.testing.assert_allclose(g["mean2d"][0], [cam.cx, cam.cy], atol=1e-5)
+    assert g["depth"][0] == np.float32(Z)
+
+
+def test_cov2d_off_axis():
+    W, H = 128, 96
+    cam = _cam(np.eye(4), W, H)
+    f = cam.fx
+    s, X, Z = 0.03, 0.6, 3.0
+    g = O.gaussians(_scene([[X, 0, Z]], [[s, s, s]]), cam)
+    a = s * s * f * f * (1 / Z ** 2 + X ** 2 / Z ** 4) + 0.3
+    c = s * s * f * f / Z ** 2 + 0.3
+    np.testing.assert_allclose(g["conic"][0], [1 / a, 0.0, 1 / c], rtol=5e-6, atol=1e-9)
+    np.testing.assert_allclose(g["mean2d"][0], [f * X / Z + cam.cx, cam.cy], rtol=1e-6)
+
+
+def test_cov2d_anisotropic_rotated():
+    """An x-elongated Gaussian rotated 90 deg about the optical axis becomes
+    y-elongated on screen (a transposed rotation would leave it along x)."""
+    W = H = 64
+    cam = _cam(np.eye(4), W, H)
+    q = np.array([[math.cos(math.pi / 4), 0, 0, math.sin(math.pi / 4)]], np.float32)
+    g0 = O.gaussians(_scene([[0, 0, 3]], [[0.1, 0.01, 0.01]]), cam)
+    g1 = O.gaussians(_scene([[0, 0, 3]], [[0.1, 0.01, 0.01]], rots=q), cam)
+    f = cam.fx
+    big = (f * 0.1 / 3) ** 2 + 0.3
+    small = (f * 0.01 / 3) ** 2 + 0.3
+    np.testing.assert_allclose(g0["conic"][0], [1 / big, 0, 1 / small], rtol=1e-5, atol=1e-7)
+    np.testing.assert_allclose(g1["conic"][0], [1 / small, 0, 1 / big], rtol=1e-5, atol=1e-6)
+
+
+def test_rotation_invariants():
+    rng = np.random.default_rng(5)
+    for q in rng.standard_normal((50, 4)).astype(np.float32):
+        R = O.quat_to_rot(q).astype(np.float64)
+        np.testing.assert_allclose(R.T @ R, np.eye(3), atol=2e-6)
+        assert abs(np.linalg.det(R) - 1.0) < 3e-6
+    h = math.sqrt(0.5)
+    np.testing.assert_allclose(O.quat_to_rot([h, 0, 0, h]), [[0, -1, 0], [1, 0, 0], [0, 0, 1]], atol=2e-7)
+    np.testing.assert_allclose(O.quat_to_rot([h, h, 0, 0]), [[1, 0, 0], [0, 0, -1], [0, 1, 0]], atol=2e-7)
+    # unnormalised input gives the same rotation
+    np.testing.assert_allclose(O.quat_to_rot([2 * h, 0, 0, 2 * h]), O.quat_to_rot([h, 0, 0, h]), atol=2e-7)
+    S = O.cov3d([0.1, 0.2, 0.3], [h, 0, 0, h])
+    np.testing.assert_allclose(np.diag(S), [0.04, 0.01, 0.09], rtol=1e-5)
+
+
+def test_near_plane_and_view_transform():
+    W = H = 32
+    eye = np.array([1.0, -4.0, 0.5])
+    w2c = synth.look_at(eye, (1.0, 0.0, 0.5))
+    cam = _cam(w2c, W, H)
+    g = O.gaussians(_scene([[1, 0, 0.5], [1, -3.85, 0.5], [1, -5, 0.5]], [[.01] * 3] * 3), cam)
+    assert g["status"][0] == O.VISIBLE and abs(g["depth"][0] - 4.0) < 1e-5
+    assert g["status"][1] == O.NEAR_CULLED   # depth 0.15 <= 0.2
+    assert g["status"][2] == O.NEAR_CULLED   # behind the camera
+    np.testing.assert_allclose(O.camera_centre(w2c), eye, atol=1e-6)
+
+
+def test_tile_rect_closed_form():
+    """The rectangle holds exactly the tiles with a pixel centre in [u-r, u+r]."""
+    W, H = 100, 70
+    cam = _cam(np.eye(4), W, H)
+    rng = np.random.default_rng(1)
+    pts = np.column_stack([rng.uniform(-1.2, 1.2, 300), rng.uniform(-0.8, 0.8, 300), rng.uniform(1, 4, 300)])
+    g = O.gaussians(_scene(pts, np.full((300, 3), 0.02)), cam)
+    TX, TY = 7, 5
+    for i in range(300):
+        u, v = g["mean2d"][i]
+        r = g["radius"][i]
+        tx = [k for k in range(TX) if 16 * k <= u + r and 16 * k + 15 >= u - r]
+        ty = [k for k in range(TY) if 16 * k <= v + r and 16 * k + 15 >= v - r]
+        if tx and ty:
+            assert g["status"][i] == O.VISIBLE
+            assert list(g["rect"][i]) == [tx[0], ty[0], tx[-1], ty[-1]]
+        else:
+            assert g["status"][i] == O.NO_TILES
+
+
+# --------------------------------------------------------------------------
+# SH colour (3DGS colour model)
+# --------------------------------------------------------------------------
+
+def test_sh_degree0_closed_form():
+    W = H = 32
+    cam = _cam(np.eye(4), W, H)
+    g = O.gaussians(_scene([[0, 0, 2]], [[.01] * 3], dc=[[0.3, -0.2, -3.0]]), cam)
+    dc = np.float32([0.3, -0.2]).astype(np.float64)
+    np.testing.assert_allclose(g["rgb"][0], [C0 * dc[0] + 0.5, C0 * dc[1] + 0.5, 0.0], rtol=1e-12)
+
+
+def _sphere_quadrature(n_theta=48, n_phi=96):
+    x, w = np.polynomial.legendre.leggauss(n_theta)
+    phi = np.arange(n_phi) * 2 * np.pi / n_phi
+    ct, ph = np.meshgrid(x, phi, indexing="ij")
+    st = np.sqrt(1 - ct ** 2)
+    dirs = np.stack([st * np.cos(ph), st * np.sin(ph), ct], -1).reshape(-1, 3)
+    wts = (w[:, None] * np.full(n_phi, 2 * np.pi / n_phi)[None, :]).ravel()
+    return dirs, wts
+
+
+def test_sh_orthonormal():
+    dirs, wts = _sphere_quadrature()
+    Y = np.array([O.sh_basis(3, d) for d in dirs])
+    G = (Y * wts[:, None]).T @ Y
+    np.testing.assert_allclose(G, np.eye(16), atol=1e-12)
+
+
+def test_sh_matches_textbook_real_harmonics():
+    """Each basis function equals +/- a real spherical harmonic of the same
+    degree built from scipy's complex harmonics; the map is one-to-one."""
+    from scipy.special import sph_harm_y
+    dirs, _ = _sphere_quadrature(8, 16)
+    theta = np.arccos(np.clip(dirs[:, 2], -1, 1))
+    phi = np.arctan2(dirs[:, 1], dirs[:, 0])
+    Y = np.array([O.sh_basis(3, d) for d in dirs])
+    for l in range(4):
+        ref = []
+        for m in range(-l, l + 1):
+            c = sph_harm_y(l, abs(m), theta, phi)
+            if m > 0:
+                ref.append(math.sqrt(2) * (-1) ** m * c.real)
+            elif m < 0:
+                ref.append(math.sqrt(2) * (-1) ** m * c.imag)
+            else:
+                ref.append(c.real)
+        used = set()
+        for k in range(l * l, (l + 1) ** 2):
+            hit = [j for j, r in enumerate(ref) if np.allclose(Y[:, k], r, atol=1e-10) or np.allclose(Y[:, k], -r, atol=1e-10)]
+            assert len(hit) == 1 and hit[0] not in used, (l, k)
+            used.add(hit[0])
+
+
+# --------------------------------------------------------------------------
+# blending (Sec. III-A), depth moments (Eq. 1, Eq. 2)
+# --------------------------------------------------------------------------
+
+def test_blend_single_gaussian_closed_form():
+    W, H = 48, 40
+    cam = _cam(np.eye(4), W, H)
+    s, Z, o = 0.05, 3.0, 0.8
+    sc = _scene([[0, 0, Z]], [[s, s, s]], opac=[o], dc=[[0.4, 0.1, -0.3]])
+    r = O.render_full(sc, cam)
+    var = (cam.fx * s / Z) ** 2 + 0.3
+    col = np.array([C0 * 0.4 + 0.5, C0 * 0.1 + 0.5, max(0.0, C0 * -0.3 + 0.5)])
+    ys, xs = np.mgrid[0:H, 0:W]
+    rho2 = ((xs - cam.cx) ** 2 + (ys - cam.cy) ** 2) / var
+    a = np.minimum(0.99, o * np.exp(-0.5 * rho2))
+    rad = math.ceil(3 * math.sqrt(var))
+    in_rect = (np.abs(xs // 16 * 16 + 7.5 - cam.cx) >= 0)  # every tile meeting the 3-sigma box
+    tx = [k for k in range((W + 15) // 16) if 16 * k <= cam.cx + rad and 16 * k + 15 >= cam.cx - rad]
+    ty = [k for k in range((H + 15) // 16) if 16 * k <= cam.cy + rad and 16 * k + 15 >= cam.cy - rad]
+    in_rect = np.isin(xs // 16, tx) & np.isin(ys // 16, ty)
+    a = np.where((a >= 1 / 255) & in_rect, a, 0.0)
+    ok = np.abs(a - 1 / 255) > 1e-6
+    for ch in range(3):
+        np.testing.assert_allclose(r["rgb"][ch][ok], (col[ch] * a)[ok], atol=2e-6)
+    np.testing.assert_allclose(r["alpha"][ok], a[ok], atol=2e-6)
+    hit = (a > 0) & ok
+    np.testing.assert_allclose(r["D"][hit], Z, rtol=1e-7)
+    assert np.all(r["sigma"][hit] == 0.0)
+    assert np.all(r["D"][(a == 0) & ok] == float(O.NOHIT))
+
+
+def test_blend_two_gaussians_on_one_ray():
+    W = H = 32
+    cam = _cam(np.eye(4), W, H)
+    d1, d2, o1, o2 = 2.0, 3.5, 0.6, 0.7
+    sc = _scene([[0, 0, d1], [0, 0, d2]], [[0.02] * 3, [0.05] * 3], opac=[o1, o2],
+                dc=[[1.0, 0.0, 0.0], [0.0, 1.0, 0.0]])
+    r = O.render_full(sc, cam)
+    # probe a pixel next to the principal point (centres are at .5 offsets)
+    x, y = 15, 15
+    dd = (x - cam.cx) ** 2 + (y - cam.cy) ** 2
+    v1 = (cam.fx * 0.02 / d1) ** 2 + 0.3
+    v2 = (cam.fx * 0.05 / d2) ** 2 + 0.3
+    a1 = o1 * math.exp(-0.5 * dd / v1)
+    a2 = o2 * math.exp(-0.5 * dd / v2)
+    w1, w2 = a1, a2 * (1 - a1)
+    D = (w1 * d1 + w2 * d2) / (w1 + w2)
+    sig = math.sqrt(w1 * w2) * abs(d2 - d1) / (w1 + w2)
+    assert abs(r["D"][y, x] - D) < 1e-6
+    assert abs(r["sigma"][y, x] - sig) < 1e-6
+    c1 = np.array([C0 + 0.5, 0.5, 0.5])
+    c2 = np.array([0.5, C0 + 0.5, 0.5])
+    np.testing.assert_allclose(r["rgb"][:, y, x], w1 * c1 + w2 * c2, atol=1e-6)
+    assert abs(r["alpha"][y, x] - (1 - (1 - a1) * (1 - a2))) < 1e-6
+
+
+@pytest.mark.parametrize("seed,W,H", [(0, 64, 48), (1, 50, 37), (2, 33, 70)])
+def test_bruteforce_equals_tiled(seed, W, H):
+    sc = synth.small_scene(600, seed, degree=3, log_scale_mean=-3.2)
+    cam = _cam(synth.look_at((0.3, -3.0, 0.8), (0, 0, 0)), W, H)
+    r = O.render_full(sc, cam)
+    bf = O.blend_bruteforce(W, H, r["g"])
+    for k in ("rgb", "D", "sigma", "alpha"):
+        assert np.array_equal(r[k], bf[k]), k
+    assert r["K"] > 0
+
+
+def test_lists_sorted_and_complete():
+    W, H = 80, 64
+    sc = synth.small_scene(800, 3, degree=1)
+    cam = _cam(synth.look_at((0, -3.2, 0.5), (0, 0, 0)), W, H)
+    g = O.gaussians(sc, cam)
+    TX, TY = 5, 4
+    ts, items = O.tile_lists(g, TX, TY)
+    vis = np.flatnonzero(g["status"] == O.VISIBLE)
+    for t in range(TX * TY):
+        lst = items[ts[t]:ts[t + 1]]
+        tx, ty = t % TX, t // TX
+        want = [i for i in vis if g["rect"][i][0] <= tx <= g["rect"][i][2] and g["rect"][i][1] <= ty <= g["rect"][i][3]]
+        assert sorted(lst.tolist()) == sorted(want)
+        keys = [(g["depth"][i].view(np.uint32), i) for i in lst]
+        assert keys == sorted(keys)
+
+
+def test_blend_invariants():
+    w = synth.workload("tiny", n_frames=1)
+    r = O.render_full(w.scene, w.cameras[0])
+    assert np.all(r["alpha"] >= 0) and np.all(r["alpha"] <= 1 - 1e-4 + 1e-7)
+    assert np.all(r["rgb"] >= 0) and np.all(np.isfinite(r["rgb"]))
+    hit = r["D"] != float(O.NOHIT)
+    assert np.all(r["sigma"] >= 0)
+    d = r["g"]["depth"][r["g"]["status"] == O.VISIBLE]
+    assert r["D"][hit].min() >= d.min() - 1e-6 and r["D"][hit].max() <= d.max() + 1e-6
+    # temporal Gaussian buffer = Gaussians with a positive weight somewhere
+    assert np.array_equal(r["maxw"] > 0, (r["g_certain"] > 0) | ((r["maxw"] > 0) & (r["g_uncertain"] > 0)))
+    assert (r["margin_pos"] >= 0).mean() < 0.01
+
+
+# --------------------------------------------------------------------------
+# warping, fill, correspondence, stitch (Eq. 3, Sec. III-E, Eq. 4)
+# --------------------------------------------------------------------------
+
+def _intr(cam):
+    return np.array([cam.fx, cam.fy, cam.cx, cam.cy], np.float32)
+
+
+def test_warp_identity_and_stitch():
+    W, H = 40, 36
+    cam = _cam(np.eye(4), W, H)
+    rng = np.random.default_rng(2)
+    D = rng.uniform(2, 6, (H, W)).astype(np.float32)
+    D[rng.uniform(size=(H, W)) < 0.1] = O.NOHIT
+    S = rng.uniform(0, 0.3, (H, W)).astype(np.float32)
+    M, Mi = O.relative_pose(cam.w2c, cam.w2c)
+    np.testing.assert_array_equal(M, np.eye(4, dtype=np.float32)[:3].ravel())
+    dmin, smax = O.forward_warp(D, S, _intr(cam), _intr(cam), M)
+    assert np.array_equal(dmin, D)
+    assert np.array_equal(smax, np.where(D == O.NOHIT, 0, S))
+    dfill = O.depth_fill(dmin)
+    uv, matched, um = O.backward_query(dfill, _intr(cam), _intr(cam), Mi)
+    assert np.array_equal(matched.astype(bool), dfill != O.NOHIT)
+    tab = rng.uniform(0, 1, (3, H, W)).astype(np.float32)
+    out = np.zeros((3, H, W))
+    O.stitch(tab, uv, np.zeros(((H + 15) // 16, (W + 15) // 16), np.uint8), out)
+    np.testing.assert_allclose(out[:, matched > 0], tab[:, matched > 0], atol=1e-5)
+
+
+def test_warp_roll90_is_permutation():
+    W = H = 64
+    cam = _cam(np.eye(4), W, H)
+    roll = np.array([[0, -1, 0, 0], [1, 0, 0, 0], [0, 0, 1, 0], [0, 0, 0, 1]], np.float32)
+    M, _ = O.relative_pose(np.eye(4, dtype=np.float32), roll)
+    D = np.full((H, W), 5.0, np.float32)
+    label = np.arange(W * H, dtype=np.float32).reshape(H, W) / 8.0
+    dmin, smax = O.forward_warp(D, label, _intr(cam), _intr(cam), M)
+    assert np.all(dmin == 5.0)
+    ys, xs = np.mgrid[0:H, 0:W]
+    # (x, y) -> (63 - y, x)
+    expect = np.zeros((H, W), np.float32)
+    expect[xs, 63 - ys] = label[ys, xs]
+    assert np.array_equal(smax, expect)
+
+
+def test_warp_dolly_magnification():
+    W, H = 96, 64
+    cam = _cam(np.eye(4), W, H)
+    Z, dz = 4.0, 0.5
+    fwd = np.eye(4, dtype=np.float32)
+    fwd[2, 3] = -dz                      # camera moved forward by dz
+    M, _ = O.relative_pose(np.eye(4, dtype=np.float32), fwd)
+    D = np.full((H, W), Z, np.float32)
+    dmin, _ = O.forward_warp(D, np.zeros_like(D), _intr(cam), _intr(cam), M)
+    ys, xs = np.mgrid[0:H, 0:W]
+    u = cam.cx + (xs - cam.cx) * Z / (Z - dz)
+    v = cam.cy + (ys - cam.cy) * Z / (Z - dz)
+    frac_ok = (np.abs(u - np.floor(u) - 0.5) > 1e-3) & (np.abs(v - np.floor(v) - 0.5) > 1e-3)
+    xi, yi = np.floor(u + 0.5).astype(int), np.floor(v + 0.5).astype(int)
+    inside = (xi >= 0) & (xi < W) & (yi >= 0) & (yi < H) & frac_ok
+    hit = np.zeros((H, W), bool)
+    hit[yi[inside], xi[inside]] = True
+    got = dmin != O.NOHIT
+    assert np.all(got[hit])
+    assert np.all(dmin[got] == np.float32(Z - dz))
+    # magnification leaves holes: about (1 - ((Z-dz)/Z)^2) of the image
+    assert 0.15 < 1 - got.mean() < 0.30
+
+
+def test_lateral_translation_unmatched_strip():
+    W, H = 160, 48
+    cam = _cam(np.eye(4), W, H)
+    Z, dx = 5.0, 0.1
+    cur = np.eye(4, dtype=np.float32)
+    cur[0, 3] = -dx                      # camera moved right by dx
+    M, Mi = O.relative_pose(np.eye(4, dtype=np.float32), cur)
+    D = np.full((H, W), Z, np.float32)
+    dmin, smax = O.forward_warp(D, np.zeros_like(D), _intr(cam), _intr(cam), M)
+    dfill = O.depth_fill(dmin)
+    uv, matched, um = O.backward_query(dfill, _intr(cam), _intr(cam), Mi)
+    shift = cam.fx * dx / Z              # pixels
+    xs = np.arange(W)
+    expect_cols = xs > (W - 1) - shift + 0.5
+    strip = ~matched.astype(bool)
+    assert np.array_equal(strip.any(0), expect_cols)
+    assert np.array_equal(um.any(0), np.array([expect_cols[16 * k:16 * k + 16].any() for k in range(W // 16)]))
+
+
+def test_depth_fill_examples():
+    N = O.NOHIT
+    a = np.full((5, 5), 3.0, np.float32)
+    a[2, 2] = N
+    a[1, 1] = 1.0
+    f = O.depth_fill(a)
+    assert f[2, 2] == np.float32((1.0 + 3.0 * 7) / 8)
+    b = np.full((5, 5), 3.0, np.float32)
+    b[2, 2] = N
+    b[2, 3] = N
+    f = O.depth_fill(b)
+    assert f[2, 2] == N and f[2, 3] == N
+    c = np.full((5, 5), 3.0, np.float32)
+    c[0, 2] = N
+    c[2, 4] = N
+    f = O.depth_fill(c)
+    assert f[0, 2] == N and f[2, 4] == N
+    assert np.all(f[c != N] == 3.0)
+
+
+# --------------------------------------------------------------------------
+# culling and occluded tiles (Sec. III-D, III-E)
+# --------------------------------------------------------------------------
+
+def test_toc_and_newly_visible_rules():
+    W, H = 64, 48
+    cam = _cam(np.eye(4), W, H)
+    # four Gaussians on the optical axis region at different depths
+    pts = [[0, 0, 2.0], [0, 0, 3.9], [0, 0, 4.05], [0.3, 0.2, 6.0]]
+    sc = _scene(pts, [[0.02] * 3] * 4, opac=[0.9] * 4)
+    dmin = np.full((H, W), 4.0, np.float32)
+    smax = np.full((H, W), 0.1, np.float32)
+    g_rendered = np.array([0, 0, 0, 1], np.uint8)
+    cull = dict(afc=False, toc=True, dmin=dmin, smax=smax, g_rendered=g_rendered, lambda1=3.0, lambda2=0.0)
+    g = O.gaussians(sc, cam, cull=cull)
+    assert g["status"][0] == O.VISIBLE and g["newly_visible"][0] == 1    # 2.0 <= 4 - 0.3
+    assert g["status"][1] == O.VISIBLE and g["newly_visible"][1] == 0    # inside the surface band
+    assert g["status"][2] == O.TOC_CULLED                                 # 4.05 > 4 + 0
+    assert g["status"][3] == O.VISIBLE and g["newly_visible"][3] == 0    # in G_rendered: never culled
+    # off-screen means are never tested
+    sc2 = _scene([[5.0, 0, 4.5]], [[0.5] * 3])
+    g2 = O.gaussians(sc2, cam, cull=dict(cull, g_rendered=np.zeros(1, np.uint8)))
+    assert g2["status"][0] != O.TOC_CULLED
+
+
+def test_afc_rule():
+    W, H = 64, 48
+    cam = _cam(np.eye(4), W, H)
+    sc = _scene([[0, 0, 3], [1.2, 0, 3], [-0.5, 0.5, 3]], [[0.02] * 3] * 3)
+    g = O.gaussians(sc, cam)
+    fb, cnt = O.afc_bounds(np.array([1, 0, 1], np.uint8), g["ndc"])
+    assert cnt == 2 and fb[0] <= fb[2] and fb[1] <= fb[3]
+    g2 = O.gaussians(sc, cam, cull=dict(afc=True, fbox=fb))
+    assert list(g2["status"]) == [O.VISIBLE, O.AFC_CULLED, O.VISIBLE]
+    # Pix2NDC maps pixel centres -0.5 .. W-0.5 onto [-1, 1]
+    np.testing.assert_allclose(g["ndc"][0], [(2 * cam.cx + 1) / W - 1, (2 * cam.cy + 1) / H - 1], atol=1e-6)
+
+
+def test_occluded_tiles_closed_form():
+    W, H = 96, 80
+    cam = _cam(np.eye(4), W, H)
+    s, Z, o = 0.06, 3.0, 0.7
+    sc = _scene([[0.13, -0.07, Z]], [[s, s, s]], opac=[o])
+    cull = dict(afc=False, toc=True, dmin=np.full((H, W), O.NOHIT, np.float32),
+                smax=np.zeros((H, W), np.float32), g_rendered=np.zeros(1, np.uint8))
+    g = O.gaussians(sc, cam, cull=cull)
+    assert g["newly_visible"][0] == 1
+    oc, ocm = O.occluded_tiles(W, H, g)
+    var = (cam.fx * s / Z) ** 2 + 0.3   # off-axis terms change Sigma' by < 1e-3 here
+    u, v = g["mean2d"][0]
+    R2 = 2 * var * math.log(255 * o)
+    ys, xs = np.mgrid[0:H, 0:W]
+    d2 = (xs - u) ** 2 + (ys - v) ** 2
+    rad = g["radius"][0]
+    TX, TY = W // 16, H // 16
+    expect = np.zeros((TY, TX), np.uint8)
+    for ty in range(TY):
+        for tx in range(TX):
+            if not (16 * tx <= u + rad and 16 * tx + 15 >= u - rad and 16 * ty <= v + rad and 16 * ty + 15 >= v - rad):
+                continue
+            expect[ty, tx] = (d2[16 * ty:16 * ty + 16, 16 * tx:16 * tx + 16] <= R2).any()
+    assert expect.sum() >= 2
+    assert np.array_equal(oc, expect)
+
+
+# --------------------------------------------------------------------------
+# selection, schedule (Sec. III-B, III-E, IV-B, Table VI)
+# --------------------------------------------------------------------------
+
+def test_all_dirty_no_cull_equals_full():
+    w = synth.workload("tiny", n_frames=6)
+    p = O.Params(enable_afc=False, enable_toc=False, force_all_dirty=True)
+    T = O.TemporalOracle(w.scene, 256, 256, p)
+    for cam in w.cameras:
+        o = T.render(cam)
+        f = O.render_full(w.scene, cam)
+        assert np.array_equal(o["rgb"], f["rgb"])
+        assert o["K"] == f["K"]
+
+
+def test_lambda_tdc_one_equals_full():
+    w = synth.workload("tiny", n_frames=3)
+    T = O.TemporalOracle(w.scene, 256, 256, O.Params(lambda_tdc=1))
+    for cam in w.cameras:
+        o = T.render(cam)
+        assert o["kind"] == O.TRUE_REF
+        assert np.array_equal(o["rgb"], O.render_full(w.scene, cam)["rgb"])
+
+
+def test_static_camera_reuses_tab():
+    w = synth.workload("tiny", n_frames=1)
+    T = O.TemporalOracle(w.scene, 256, 256)
+    ref = T.render(w.cameras[0])
+    o = T.render(w.cameras[0])
+    assert o["kind"] == O.TGS_FRAME
+    # every covered pixel finds itself; selected tiles = occluded or uncovered
+    covered = ref["D"] != float(O.NOHIT)
+    assert np.array_equal(o["matched"].astype(bool), o["dfill"] != O.NOHIT)
+    assert np.all(o["matched"][covered])
+    assert np.array_equal(o["tile_sel"], (o["oc"] | o["um"]))
+    keep = np.repeat(np.repeat(o["tile_sel"] == 0, 16, 0), 16, 1)[:256, :256]
+    np.testing.assert_allclose(o["rgb"][:, keep], ref["rgb"][:, keep], atol=1e-5)
+
+
+def _tgsf(lambda_tdc, lambda_sr, eta, n_frames):
+    T = O.TemporalOracle.__new__(O.TemporalOracle)
+    T.p = O.Params(lambda_tdc=lambda_tdc, lambda_sr=lambda_sr, eta=eta)
+    T.TX, T.TY = 10, 10
+    T.reset()
+    kinds = []
+    for _ in range(n_frames):
+        k = T.next_kind()
+        kinds.append(k)
+        T.advance(k, 0)
+    return kinds
+
+
+def test_schedule_table6_tgsf():
+    rows = json.load(open(os.path.join(GOLDEN, "table6_tgsf.json")))["rows"]
+    for r in rows:
+        n = 150   # a common multiple of the lambda_TDC values in the table
+        kinds = _tgsf(r["lambda_tdc"], r["lambda_sr"], r["eta"], n)
+        tgsf = 100.0 * sum(k == O.TGS_FRAME for k in kinds) / n
+        assert round(tgsf, 2) == r["tgsf_percent"], r
+
+
+def test_schedule_pattern_and_eta():
+    kinds = _tgsf(50, 5, 0.4, 101)
+    assert kinds[0] == O.TRUE_REF and kinds[50] == O.TRUE_REF and kinds[100] == O.TRUE_REF
+    assert all(kinds[i] == O.PSEUDO_REF for i in (5, 10, 45, 55))
+    assert all(kinds[i] == O.TGS_FRAME for i in (1, 4, 6, 49, 51))
+    T = O.TemporalOracle.__new__(O.TemporalOracle)
+    T.p = O.Params()
+    T.TX, T.TY = 10, 10
+    T.reset()
+    T.advance(T.next_kind(), 100)           # true reference
+    T.advance(T.next_kind(), 40)            # TGS frame at exactly eta: no insertion
+    assert T.next_kind() == O.TGS_FRAME
+    T.advance(O.TGS_FRAME, 41)              # exceeds eta
+    assert T.next_kind() == O.PSEUDO_REF
+
+
+def test_temporal_culls_respect_buffers():
+    """No member of the temporal Gaussian buffer is ever culled by TOC; each
+    TOC-culled Gaussian lies behind the warped surface at its pixel; at the
+    reference camera AFC keeps every buffer member."""
+    sc = synth.scene_uniform_cube(20000, 7, degree=1, log_scale_mean=-3.3)
+    cams = synth.orbit_path(4, 3.0, 15.0, 1.0, 128, 128)
+    T = O.TemporalOracle(sc, 128, 128, O.Params(eta=1.0))
+    ref = T.render(cams[0])
+    g0 = ref["g"]
+    keep = O.gaussians(sc, cams[0], cull=dict(afc=True, fbox=T.fbox))
+    assert np.all(keep["status"][T.g_rendered > 0] != O.AFC_CULLED)
+    for cam in cams[1:]:
+        o = T.render(cam)
+        if o["kind"] != O.TGS_FRAME:
+            continue
+        st = o["g"]["status"]
+        assert not np.any((st == O.TOC_CULLED) & (T.g_rendered > 0))
+        idx = np.flatnonzero(st == O.TOC_CULLED)
+        assert idx.size > 0
+        u = np.floor(o["g"]["mean2d"][idx] + 0.5).astype(int)
+        assert np.all(o["g"]["depth"][idx] > o["dmin"][u[:, 1], u[:, 0]])
+    assert g0["n_survivors"] == sc.n
