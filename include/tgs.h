@@ -1,0 +1,216 @@
+/*
+ * tgs.h -- C-ABI of the TemporalGS hot path on MI355X (gfx950).
+ *
+ * TemporalGS (arxiv 2607.03390) renders a stream of camera views of a 3D
+ * Gaussian Splatting scene.  Reference frames are rendered by the full
+ * tile-based 3DGS pipeline (Sec. III-A: preprocess, Gaussian-tile key
+ * duplication, per-tile depth sort, front-to-back alpha blending) and build
+ * temporal priors (Sec. III-C: the temporal geometry buffer of Eq. 1/2, the
+ * temporal appearance buffer, the temporal Gaussian buffer).  The frames in
+ * between use them to drop Gaussians (temporal dynamic culling, Sec. III-D)
+ * and to re-render only the tiles the warped priors cannot supply (selective
+ * rendering, Sec. III-E, Eq. 3/4), with pseudo reference frames inserted by
+ * interval and by the eta rule (Sec. III-E, Sec. IV-B).
+ *
+ * Conventions shared by every entry point:
+ *  - Status codes only; nothing is thrown across the ABI.  On error the
+ *    caller's outputs are left untouched (unless stated) and tgs_last_error()
+ *    returns a message (thread-local, valid until the next call on the thread).
+ *  - "host" pointers are read during the call only; "device" pointers are
+ *    HIP device memory owned by the caller (for example torch tensors) and
+ *    must stay valid until the enqueued work completes.
+ *  - Work is enqueued on the caller's HIP stream (hipStream_t passed as
+ *    void*, NULL = the null stream).  Every render call synchronises that
+ *    stream once per frame to read the key and tile counts back, so the
+ *    scalar fields of tgs_frame_out are valid on return and the device
+ *    outputs are complete once the stream is synchronised.
+ *  - Camera: world_to_cam is a row-major rigid 4x4 matrix (camera x right, y
+ *    down, z forward); pinhole intrinsics fx, fy, cx, cy in pixels with pixel
+ *    centres at integer coordinates.  Images are planar float32: rgb is
+ *    [3][H][W], single-channel maps are [H][W].  Tiles are 16x16 pixels,
+ *    TX = ceil(W/16), TY = ceil(H/16), numbered row-major.
+ *  - A scene or a state is not thread-safe; distinct states may share a scene
+ *    but calls on one scene or state must not overlap.
+ */
+#ifndef TGS_H
+#define TGS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TGS_OK = 0,
+    TGS_ERR_INVALID_ARG = 1,     /* bad pointer, size, NaN, non-rigid pose ... */
+    TGS_ERR_OUT_OF_MEMORY = 2,   /* a device or host allocation failed        */
+    TGS_ERR_DEVICE = 3,          /* a HIP call or kernel launch failed        */
+    TGS_ERR_STATE_MISMATCH = 4,  /* camera size differs from the state's      */
+    TGS_ERR_CAPACITY = 5         /* more than 2^30-1 keys in one frame        */
+} tgs_status;
+
+/* Frame kinds reported in tgs_frame_out.frame_kind (Sec. III-B, III-E). */
+enum {
+    TGS_FRAME_TRUE_REF = 0,   /* full render, no culling; refreshes all priors  */
+    TGS_FRAME_PSEUDO_REF = 1, /* full render with adaptive frustum culling      */
+    TGS_FRAME_TGS = 2,        /* AFC + TOC + selective rendering + stitching    */
+    TGS_FRAME_FULL = 3        /* tgs_render_full (no temporal state)            */
+};
+
+/* Opaque device-resident scene (structure-of-arrays copy) and temporal state. */
+typedef struct tgs_scene tgs_scene;
+typedef struct tgs_state tgs_state;
+
+/* Scene description (Sec. III-A: mean, covariance from scale and rotation,
+ * opacity, SH colour).  All arrays are HOST memory in array-of-structs order,
+ * already activated: scales are linear, opacities in [0,1], rotations are
+ * quaternions (w,x,y,z) that need not be normalised (they must not be zero),
+ * sh holds (sh_degree+1)^2 coefficients x 3 channels per Gaussian,
+ * coefficient-major. */
+typedef struct {
+    int32_t n;            /* number of Gaussians, >= 0 (0 renders background) */
+    int32_t sh_degree;    /* 0..3                                             */
+    const float *means;   /* [n][3]                                           */
+    const float *scales;  /* [n][3]                                           */
+    const float *rotations; /* [n][4]                                         */
+    const float *opacities; /* [n]                                            */
+    const float *sh;      /* [n][(sh_degree+1)^2][3]                          */
+} tgs_scene_desc;
+
+typedef struct {
+    float world_to_cam[16];   /* row-major rigid transform                    */
+    float fx, fy, cx, cy;     /* pinhole intrinsics (pixels), fx, fy > 0      */
+    int32_t width, height;    /* image size, 1..16384                         */
+} tgs_camera;
+
+/* Method parameters: lambda_TDC, lambda_SR (Sec. III-B, IV-B), eta
+ * (Sec. III-E), lambda1/lambda2 of the surface range (Sec. III-C), the near
+ * plane of the 3DGS preprocess, and the ablation switches of Table IV. */
+typedef struct {
+    int32_t lambda_tdc;       /* 50: interval between true references          */
+    int32_t lambda_sr;        /* 5: interval between references of any kind    */
+    float eta;                /* 0.40: selected-tile share that forces a pseudo reference */
+    float lambda1;            /* 3: surface range below the warped depth       */
+    float lambda2;            /* 0: surface range above the warped depth       */
+    float z_near;             /* 0.2                                           */
+    int32_t enable_afc;       /* 1: adaptive frustum culling                   */
+    int32_t enable_toc;       /* 1: temporal occlusion culling                 */
+    int32_t enable_sr;        /* 1: selective rendering (0 = render every tile)*/
+    int32_t force_all_dirty;  /* 0: select every tile in TGS frames (testing)  */
+} tgs_params;
+
+/* Outputs of one rendered frame.  rgb is required; the other pointers may be
+ * NULL.  depth/sigma/alpha are written on reference frames and by
+ * tgs_render_full only (Eq. 1, Eq. 2 and 1-T; depth is 1001 = z_far+eps and
+ * sigma 0 where no Gaussian was composited); contrib (per Gaussian, the
+ * largest blending weight over the image, Sec. III-C) likewise.  tile_mask
+ * receives 1 for every tile that was rasterised this frame. */
+typedef struct {
+    float *rgb;               /* device [3][H][W]                              */
+    float *depth;             /* device [H][W] or NULL                         */
+    float *sigma;             /* device [H][W] or NULL                         */
+    float *alpha;             /* device [H][W] or NULL                         */
+    float *contrib;           /* device [n] or NULL                            */
+    uint8_t *tile_mask;       /* device [TY][TX] or NULL                       */
+    /* scalars written by the library on success */
+    int32_t frame_kind;       /* TGS_FRAME_*                                   */
+    int32_t n_selected;       /* tiles rasterised                              */
+    int32_t n_survivors;      /* Gaussians past the near plane and the culls   */
+    int32_t n_newly_visible;  /* newly visible Gaussians (TGS frames)          */
+    int64_t n_keys;           /* Gaussian-tile keys sorted                     */
+} tgs_frame_out;
+
+/* Fills *p with the paper's defaults (lambda_TDC 50, lambda_SR 5, eta 0.40,
+ * lambda1 3, lambda2 0, near 0.2, all accelerations on). */
+void tgs_params_default(tgs_params *p);
+
+/* Copies a host scene to the device (Sec. III-A parameters) as
+ * structure-of-arrays, on `stream`; synchronous on return.  *out is owned by
+ * the caller and released with tgs_scene_free.  Errors: INVALID_ARG for NULL
+ * arrays with n > 0, sh_degree outside 0..3, non-finite values or zero
+ * quaternions; OUT_OF_MEMORY; DEVICE. */
+tgs_status tgs_scene_upload(const tgs_scene_desc *desc, void *stream, tgs_scene **out);
+void tgs_scene_free(tgs_scene *scene);
+int32_t tgs_scene_count(const tgs_scene *scene);
+
+/* Renders one frame with the full 3DGS pipeline (Sec. III-A), no temporal
+ * state.  frame_kind = TGS_FRAME_FULL.  The scene holds the frame's
+ * workspace, so calls on one scene must not overlap. */
+tgs_status tgs_render_full(tgs_scene *scene, const tgs_camera *cam, tgs_frame_out *out,
+                           void *stream);
+
+/* Creates the temporal state for `scene` at width x height (Sec. III-B..E):
+ * priors, warp buffers and the frame schedule.  params may be NULL
+ * (defaults).  The scene must outlive the state. */
+tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
+                            const tgs_params *params, tgs_state **out);
+/* Forgets all priors: the next tgs_render_temporal renders a true reference. */
+tgs_status tgs_state_reset(tgs_state *state);
+void tgs_state_free(tgs_state *state);
+
+/* Renders the next frame of the stream (Sec. III-B..E).  The schedule picks
+ * the kind: a true reference on the first frame and every lambda_tdc frames;
+ * a pseudo reference every lambda_sr frames or after a TGS frame whose
+ * selected tiles exceeded eta of all tiles; otherwise a TGS frame (adaptive
+ * frustum + occlusion culling, selected tiles rasterised, the others stitched
+ * from the reference image warped by Eq. 3/4).  cam->width/height must equal
+ * the state's (STATE_MISMATCH otherwise). */
+tgs_status tgs_render_temporal(tgs_state *state, const tgs_camera *cam, tgs_frame_out *out,
+                               void *stream);
+
+/* Host layout of an exported state: this header followed by
+ *   float depth[H*W], float sigma[H*W]   (temporal geometry buffer, Eq. 1/2)
+ *   float tab[3*H*W]                     (temporal appearance buffer)
+ *   uint8_t g_rendered[n]                (temporal Gaussian buffer)        */
+typedef struct {
+    uint32_t magic;           /* 0x54475331 'TGS1'                             */
+    int32_t width, height, n;
+    int32_t frame_index;      /* frames rendered since the last reset          */
+    int32_t since_true_ref;   /* frames since the last true reference          */
+    int32_t since_ref;        /* frames since the last reference of any kind   */
+    int32_t force_pseudo;     /* the eta rule fired on the last frame          */
+    int32_t has_reference;    /* priors are valid                              */
+    float fbox[4];            /* adaptive frustum F_min.xy, F_max.xy (NDC)     */
+    float ref_world_to_cam[16];
+    float ref_intrinsics[4];  /* fx, fy, cx, cy of the reference frame         */
+} tgs_state_header;
+
+/* Export: with host == NULL, *nbytes receives the blob size; otherwise the
+ * blob is written (synchronous) if *nbytes is large enough (INVALID_ARG
+ * otherwise).  Import: replaces the priors and counters (INVALID_ARG on a
+ * size or magic mismatch, STATE_MISMATCH on other sizes).  Used for
+ * checkpoint / resume and state-injection testing. */
+tgs_status tgs_state_export(const tgs_state *state, void *host, size_t *nbytes);
+tgs_status tgs_state_import(tgs_state *state, const void *host, size_t nbytes);
+
+/* Intermediate buffers of the last frame rendered through `scene`
+ * (tgs_render_full, state == NULL) or through `state`, copied to host
+ * memory (synchronous).  host == NULL queries the size into *nbytes. */
+enum {
+    TGS_DUMP_SORTED_VALUES = 0,  /* uint32 [n_keys] Gaussian index per sorted key   */
+    TGS_DUMP_SORTED_KEYS = 1,    /* uint64 [n_keys] (tile << 32) | depth bits        */
+    TGS_DUMP_TILE_RANGES = 2,    /* uint32 [TX*TY][2] start, end into the sorted keys */
+    TGS_DUMP_RECORDS = 3,        /* float [n][12]: u, v, conic a, b | conic c, opacity, depth, 0 | r, g, b, 0 */
+    TGS_DUMP_RECTS = 4,          /* uint16 [n][4] tile rectangle x0,y0,x1,y1 (x0 > x1: none) */
+    TGS_DUMP_STATUS = 5,         /* uint8 [n] bit0 survivor, bit1 newly visible     */
+    TGS_DUMP_WARP_DEPTH = 6,     /* float [H*W] warped min depth (Eq. 3)            */
+    TGS_DUMP_WARP_SIGMA = 7,     /* float [H*W] warped max sigma                    */
+    TGS_DUMP_FILLED_DEPTH = 8,   /* float [H*W] repaired depth                       */
+    TGS_DUMP_CORRESPONDENCE = 9, /* float [H*W][2] reference (u,v), -1 if unmatched  */
+    TGS_DUMP_UNMATCHED = 10,     /* uint8 [TX*TY] unmatched tiles                    */
+    TGS_DUMP_OCCLUDED = 11,      /* uint8 [TX*TY] occluded tiles                     */
+    TGS_DUMP_SELECTED = 12       /* uint8 [TX*TY] selected tiles                     */
+};
+tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_t what,
+                          void *host, size_t *nbytes);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *tgs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TGS_H */

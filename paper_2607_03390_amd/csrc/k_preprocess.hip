@@ -1,0 +1,203 @@
+// Per-Gaussian stage of a frame (3DGS preprocess, Sec. III-A) with the
+// temporal dynamic culling of Sec. III-D and the newly-visible test of the
+// occluded-tile detection (Sec. III-E) folded in.
+//
+// One thread per Gaussian over the structure-of-arrays scene: every load is a
+// coalesced 256-byte wave access, and the SH coefficients (192 of the 236
+// bytes per Gaussian at degree 3) are read only by survivors.  The kernel is
+// HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
+// and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
+// fixed order with contraction disabled for the whole library, so they are
+// reproducible by any implementation that follows the same order.
+#include "tgs_internal.h"
+
+namespace tgs {
+
+namespace {
+
+template <int DEG>
+__device__ inline void sh_colour(const SceneDev &s, int i, float dx, float dy, float dz,
+                                 float &r, float &g, float &b) {
+    constexpr int K = (DEG + 1) * (DEG + 1);
+    float basis[K];
+    basis[0] = 0.28209479177387814f;
+    if constexpr (DEG >= 1) {
+        const float C1 = 0.4886025119029199f;
+        float inv = 1.0f / sqrtf(dx * dx + dy * dy + dz * dz);
+        float x = dx * inv, y = dy * inv, z = dz * inv;
+        basis[1] = -C1 * y;
+        basis[2] = C1 * z;
+        basis[3] = -C1 * x;
+        if constexpr (DEG >= 2) {
+            float xx = x * x, yy = y * y, zz = z * z, xy = x * y, yz = y * z, xz = x * z;
+            basis[4] = 1.0925484305920792f * xy;
+            basis[5] = -1.0925484305920792f * yz;
+            basis[6] = 0.31539156525252005f * (2.0f * zz - xx - yy);
+            basis[7] = -1.0925484305920792f * xz;
+            basis[8] = 0.5462742152960396f * (xx - yy);
+            if constexpr (DEG >= 3) {
+                basis[9] = -0.5900435899266435f * y * (3.0f * xx - yy);
+                basis[10] = 2.890611442640554f * xy * z;
+                basis[11] = -0.4570457994644658f * y * (4.0f * zz - xx - yy);
+                basis[12] = 0.3731763325901154f * z * (2.0f * zz - 3.0f * xx - 3.0f * yy);
+                basis[13] = -0.4570457994644658f * x * (4.0f * zz - xx - yy);
+                basis[14] = 1.445305721320277f * z * (xx - yy);
+                basis[15] = -0.5900435899266435f * x * (xx - 3.0f * yy);
+            }
+        }
+    }
+    float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f;
+    const size_t n = (size_t)s.n;
+    const float *p = s.sh + i;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        acc0 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 0) * n], acc0);
+        acc1 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 1) * n], acc1);
+        acc2 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 2) * n], acc2);
+    }
+    r = fmaxf(acc0 + 0.5f, 0.0f);
+    g = fmaxf(acc1 + 0.5f, 0.0f);
+    b = fmaxf(acc2 + 0.5f, 0.0f);
+}
+
+template <int DEG>
+__global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, CullK cull,
+                                                         Records rec, Counters *cnt) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    bool survivor = false, newly = false;
+    ushort4 rect = make_ushort4(1, 1, 0, 0);
+
+    if (i < s.n) {
+        const float mx = s.mx[i], my = s.my[i], mz = s.mz[i];
+        const float *V = cam.V;
+        const float tx = ((V[0] * mx + V[1] * my) + V[2] * mz) + V[3];
+        const float ty = ((V[4] * mx + V[5] * my) + V[6] * mz) + V[7];
+        const float tz = ((V[8] * mx + V[9] * my) + V[10] * mz) + V[11];
+        bool alive = tz > cull.z_near;                      // near-plane culling
+        float u = 0.0f, v = 0.0f;
+        if (alive) {
+            u = cam.fx * (tx / tz) + cam.cx;
+            v = cam.fy * (ty / tz) + cam.cy;
+            if (cull.afc) {                                 // adaptive frustum culling
+                const float nx = (2.0f * u + 1.0f) / (float)cam.W - 1.0f;
+                const float ny = (2.0f * v + 1.0f) / (float)cam.H - 1.0f;
+                alive = ordered_to_float(cull.fbox[0]) <= nx && nx <= ordered_to_float(cull.fbox[2]) &&
+                        ordered_to_float(cull.fbox[1]) <= ny && ny <= ordered_to_float(cull.fbox[3]);
+            }
+        }
+        if (alive && cull.toc) {                            // occlusion culling, newly visible
+            const float pxf = floorf(u + 0.5f), pyf = floorf(v + 0.5f);
+            if (pxf >= 0.0f && pxf <= (float)(cam.W - 1) && pyf >= 0.0f &&
+                pyf <= (float)(cam.H - 1) && !cull.g_rendered[i]) {
+                const int p = (int)pyf * cam.W + (int)pxf;
+                const float dm = cull.dmin[p], sm = cull.smax[p];
+                if (tz > dm + cull.lambda2 * sm) alive = false;
+                else if (tz <= dm - cull.lambda1 * sm) newly = true;
+            }
+        }
+        survivor = alive;
+        if (alive) {
+            // 3D covariance R S S^T R^T from the normalised quaternion
+            const float q0 = s.qw[i], q1 = s.qx[i], q2 = s.qy[i], q3 = s.qz[i];
+            const float qn = sqrtf(((q0 * q0 + q1 * q1) + q2 * q2) + q3 * q3);
+            const float r = q0 / qn, x = q1 / qn, y = q2 / qn, z = q3 / qn;
+            float R[9];
+            R[0] = 1.0f - 2.0f * (y * y + z * z);
+            R[1] = 2.0f * (x * y - r * z);
+            R[2] = 2.0f * (x * z + r * y);
+            R[3] = 2.0f * (x * y + r * z);
+            R[4] = 1.0f - 2.0f * (x * x + z * z);
+            R[5] = 2.0f * (y * z - r * x);
+            R[6] = 2.0f * (x * z - r * y);
+            R[7] = 2.0f * (y * z + r * x);
+            R[8] = 1.0f - 2.0f * (x * x + y * y);
+            const float sc[3] = {s.sx[i], s.sy[i], s.sz[i]};
+            float M[9];
+#pragma unroll
+            for (int a = 0; a < 3; ++a)
+#pragma unroll
+                for (int c = 0; c < 3; ++c) M[a * 3 + c] = R[a * 3 + c] * sc[c];
+            float S[9];
+#pragma unroll
+            for (int a = 0; a < 3; ++a)
+#pragma unroll
+                for (int c = 0; c < 3; ++c)
+                    S[a * 3 + c] = (M[a * 3 + 0] * M[c * 3 + 0] + M[a * 3 + 1] * M[c * 3 + 1]) +
+                                   M[a * 3 + 2] * M[c * 3 + 2];
+            // EWA projection: J W Sigma W^T J^T + 0.3 I
+            const float txc = fminf(cam.limx, fmaxf(-cam.limx, tx / tz)) * tz;
+            const float tyc = fminf(cam.limy, fmaxf(-cam.limy, ty / tz)) * tz;
+            const float j00 = cam.fx / tz, j02 = -(cam.fx * txc) / (tz * tz);
+            const float j11 = cam.fy / tz, j12 = -(cam.fy * tyc) / (tz * tz);
+            float A[6];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                A[c] = j00 * V[c] + j02 * V[8 + c];
+                A[3 + c] = j11 * V[4 + c] + j12 * V[8 + c];
+            }
+            float B[6];
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int c = 0; c < 3; ++c)
+                    B[a * 3 + c] = (A[a * 3 + 0] * S[c] + A[a * 3 + 1] * S[3 + c]) + A[a * 3 + 2] * S[6 + c];
+            const float ca = ((B[0] * A[0] + B[1] * A[1]) + B[2] * A[2]) + 0.3f;
+            const float cb = (B[0] * A[3] + B[1] * A[4]) + B[2] * A[5];
+            const float cc = ((B[3] * A[3] + B[4] * A[4]) + B[5] * A[5]) + 0.3f;
+            const float det = ca * cc - cb * cb;
+            if (det > 0.0f) {
+                const float dinv = 1.0f / det;
+                const float mid = 0.5f * (ca + cc);
+                const float lam = mid + sqrtf(fmaxf(0.0f, mid * mid - det));
+                const float rad = ceilf(3.0f * sqrtf(lam));
+                const float x0 = fmaxf(0.0f, ceilf(((u - rad) - 15.0f) / 16.0f));
+                const float x1 = fminf((float)(cam.TX - 1), floorf((u + rad) / 16.0f));
+                const float y0 = fmaxf(0.0f, ceilf(((v - rad) - 15.0f) / 16.0f));
+                const float y1 = fminf((float)(cam.TY - 1), floorf((v + rad) / 16.0f));
+                if (x0 <= x1 && y0 <= y1) {
+                    rect = make_ushort4((unsigned short)x0, (unsigned short)y0,
+                                        (unsigned short)x1, (unsigned short)y1);
+                    float cr, cg, cbl;
+                    sh_colour<DEG>(s, i, mx - cam.campos[0], my - cam.campos[1],
+                                   mz - cam.campos[2], cr, cg, cbl);
+                    rec.g0[i] = make_float4(u, v, cc * dinv, -cb * dinv);
+                    rec.g1[i] = make_float4(ca * dinv, s.opac[i], tz, 0.0f);
+                    rec.col[i] = make_float4(cr, cg, cbl, 0.0f);
+                }
+            }
+        }
+        rec.rect[i] = rect;
+        rec.status[i] = (uint8_t)((survivor ? 1 : 0) | (newly ? 2 : 0));
+    }
+
+    // wave-aggregated counters and the newly-visible list
+    const uint64_t surv_mask = __ballot(survivor);
+    const uint64_t newly_mask = __ballot(newly);
+    const int lane = threadIdx.x & 63;
+    if (lane == 0 && surv_mask) atomicAdd(&cnt->n_survivors, (uint32_t)__popcll(surv_mask));
+    if (newly_mask) {
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(&cnt->n_newly, (uint32_t)__popcll(newly_mask));
+        base = __shfl(base, 0);
+        if (newly) {
+            const uint32_t below = (uint32_t)__popcll(newly_mask & ((1ull << lane) - 1ull));
+            cull.newly_list[base + below] = i;
+        }
+    }
+}
+
+}  // namespace
+
+void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
+                       Counters *cnt, hipStream_t st) {
+    if (s.n <= 0) return;
+    const dim3 grid((s.n + 255) / 256), block(256);
+    switch (s.deg) {
+        case 0: preprocess_kernel<0><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
+        case 1: preprocess_kernel<1><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
+        case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
+        default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
+    }
+}
+
+}  // namespace tgs

@@ -1,0 +1,815 @@
+// Host side of libtgs: the C-ABI of include/tgs.h, device memory, the frame
+// schedule of TemporalGS (Sec. III-B, III-E last paragraph, Sec. IV-B) and
+// the launch sequences of full, reference and TemporalGS frames.
+//
+// Every frame is enqueued on the caller's stream; the only host round trip
+// is one read-back of four counters after the key scan (the key count sizes
+// the sort and the selected-tile count drives the eta rule).
+#include <math.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/tgs.h"
+#include "tgs_internal.h"
+
+using namespace tgs;
+
+namespace {
+
+thread_local std::string g_err;
+
+tgs_status fail(tgs_status s, const std::string &msg) {
+    g_err = msg;
+    return s;
+}
+
+#define TGS_HIP(call)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (call);                                                              \
+        if (e_ != hipSuccess)                                                                \
+            return fail(e_ == hipErrorOutOfMemory ? TGS_ERR_OUT_OF_MEMORY : TGS_ERR_DEVICE, \
+                        std::string(#call) + ": " + hipGetErrorString(e_));                  \
+    } while (0)
+
+#define TGS_LAUNCHED(what)                                                                   \
+    do {                                                                                     \
+        hipError_t e_ = hipGetLastError();                                                   \
+        if (e_ != hipSuccess)                                                                \
+            return fail(TGS_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e_));   \
+    } while (0)
+
+#define TGS_TRY(expr)                   \
+    do {                                \
+        tgs_status s_ = (expr);         \
+        if (s_ != TGS_OK) return s_;    \
+    } while (0)
+
+// A growable device allocation.
+struct DevBuf {
+    void *p = nullptr;
+    size_t bytes = 0;
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+    tgs_status ensure(size_t want) {
+        if (want <= bytes && p) return TGS_OK;
+        if (p) {
+            (void)hipFree(p);
+            p = nullptr;
+            bytes = 0;
+        }
+        const size_t alloc = want > 0 ? want : 16;
+        hipError_t e = hipMalloc(&p, alloc);
+        if (e != hipSuccess) {
+            p = nullptr;
+            return fail(TGS_ERR_OUT_OF_MEMORY, "hipMalloc of " + std::to_string(alloc) + " bytes failed");
+        }
+        bytes = alloc;
+        return TGS_OK;
+    }
+    template <typename T>
+    T *as() const { return static_cast<T *>(p); }
+};
+
+// Per-frame scratch of one render path (a scene's tgs_render_full, or a state).
+struct Workspace {
+    DevBuf g0, g1, col, rect, status, offsets, newly, scan;
+    DevBuf keys, keys_alt, vals, vals_alt, sort;
+    DevBuf ranges, sel, sel_list, rowpre, cnt;
+    Counters *host_cnt = nullptr;
+    int n = -1, W = 0, H = 0;
+    size_t key_cap = 0;
+    // last frame, for tgs_debug_dump
+    uint32_t last_K = 0;
+    int last_alt = 0;
+    bool has_frame = false;
+
+    ~Workspace() {
+        if (host_cnt) (void)hipHostFree(host_cnt);
+    }
+
+    tgs_status prepare(int n_, int W_, int H_) {
+        const int TX = (W_ + 15) / 16, TY = (H_ + 15) / 16;
+        const size_t nn = (size_t)(n_ > 0 ? n_ : 1);
+        if (!host_cnt) TGS_HIP(hipHostMalloc((void **)&host_cnt, sizeof(Counters), 0));
+        if (n_ != n) {
+            TGS_TRY(g0.ensure(nn * sizeof(float4)));
+            TGS_TRY(g1.ensure(nn * sizeof(float4)));
+            TGS_TRY(col.ensure(nn * sizeof(float4)));
+            TGS_TRY(rect.ensure(nn * sizeof(ushort4)));
+            TGS_TRY(status.ensure(nn));
+            TGS_TRY(offsets.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(newly.ensure(nn * sizeof(int)));
+            TGS_TRY(scan.ensure(scan_scratch_words(n_) * sizeof(uint32_t)));
+            n = n_;
+        }
+        if (W_ != W || H_ != H) {
+            const size_t nt = (size_t)TX * TY;
+            TGS_TRY(ranges.ensure(nt * sizeof(uint2)));
+            TGS_TRY(sel.ensure(nt));
+            TGS_TRY(sel_list.ensure(nt * sizeof(int)));
+            TGS_TRY(rowpre.ensure((size_t)TY * (TX + 1) * sizeof(uint32_t)));
+            W = W_;
+            H = H_;
+        }
+        TGS_TRY(cnt.ensure(sizeof(Counters)));
+        return TGS_OK;
+    }
+
+    tgs_status ensure_keys(uint32_t K, int passes) {
+        if (K > key_cap || !keys.p) {
+            const size_t cap = (size_t)K + K / 2 + 1024;
+            TGS_TRY(keys.ensure(cap * sizeof(uint64_t)));
+            TGS_TRY(keys_alt.ensure(cap * sizeof(uint64_t)));
+            TGS_TRY(vals.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(vals_alt.ensure(cap * sizeof(uint32_t)));
+            key_cap = cap;
+        }
+        TGS_TRY(sort.ensure(sort_scratch_words((uint32_t)key_cap, passes) * sizeof(uint32_t)));
+        return TGS_OK;
+    }
+
+    Records records() const {
+        return Records{g0.as<float4>(), g1.as<float4>(), col.as<float4>(), rect.as<ushort4>(),
+                       status.as<uint8_t>()};
+    }
+};
+
+bool finite(float x) { return isfinite(x) != 0; }
+
+tgs_status check_camera(const tgs_camera *c) {
+    if (!c) return fail(TGS_ERR_INVALID_ARG, "camera is NULL");
+    if (c->width < 1 || c->height < 1 || c->width > 16384 || c->height > 16384)
+        return fail(TGS_ERR_INVALID_ARG, "image size must be within 1..16384");
+    if (!(finite(c->fx) && finite(c->fy) && c->fx > 0.0f && c->fy > 0.0f && finite(c->cx) &&
+          finite(c->cy)))
+        return fail(TGS_ERR_INVALID_ARG, "intrinsics must be finite with fx, fy > 0");
+    const float *m = c->world_to_cam;
+    for (int i = 0; i < 16; ++i)
+        if (!finite(m[i])) return fail(TGS_ERR_INVALID_ARG, "world_to_cam has a non-finite entry");
+    if (fabsf(m[12]) > 1e-6f || fabsf(m[13]) > 1e-6f || fabsf(m[14]) > 1e-6f ||
+        fabsf(m[15] - 1.0f) > 1e-6f)
+        return fail(TGS_ERR_INVALID_ARG, "world_to_cam last row must be (0,0,0,1)");
+    double R[3][3];
+    for (int i = 0; i < 3; ++i)
+        for (int j = 0; j < 3; ++j) R[i][j] = m[i * 4 + j];
+    for (int i = 0; i < 3; ++i)
+        for (int j = 0; j < 3; ++j) {
+            double s = R[0][i] * R[0][j] + R[1][i] * R[1][j] + R[2][i] * R[2][j];
+            if (fabs(s - (i == j ? 1.0 : 0.0)) > 1e-4)
+                return fail(TGS_ERR_INVALID_ARG, "world_to_cam rotation is not orthonormal");
+        }
+    const double det = R[0][0] * (R[1][1] * R[2][2] - R[1][2] * R[2][1]) -
+                       R[0][1] * (R[1][0] * R[2][2] - R[1][2] * R[2][0]) +
+                       R[0][2] * (R[1][0] * R[2][1] - R[1][1] * R[2][0]);
+    if (fabs(det - 1.0) > 1e-4) return fail(TGS_ERR_INVALID_ARG, "world_to_cam is not a rotation");
+    return TGS_OK;
+}
+
+CamK make_camk(const tgs_camera *c) {
+    CamK k;
+    for (int i = 0; i < 12; ++i) k.V[i] = c->world_to_cam[i];
+    k.fx = c->fx;
+    k.fy = c->fy;
+    k.cx = c->cx;
+    k.cy = c->cy;
+    k.W = c->width;
+    k.H = c->height;
+    k.TX = (c->width + 15) / 16;
+    k.TY = (c->height + 15) / 16;
+    const float tanfx = (0.5f * (float)c->width) / c->fx;
+    const float tanfy = (0.5f * (float)c->height) / c->fy;
+    k.limx = 1.3f * tanfx;
+    k.limy = 1.3f * tanfy;
+    // camera centre -R^T t, formed in double
+    const float *m = c->world_to_cam;
+    for (int i = 0; i < 3; ++i) {
+        const double s = (double)m[0 * 4 + i] * (double)m[3] + (double)m[1 * 4 + i] * (double)m[7] +
+                         (double)m[2 * 4 + i] * (double)m[11];
+        k.campos[i] = (float)(-s);
+    }
+    return k;
+}
+
+// Relative pose of Eq. 3 in double: M = W_cur W_ref^-1 and its inverse,
+// both rounded to fp32 3x4 row-major.
+void relative_pose(const float *ref, const float *cur, float *M, float *Minv) {
+    double a[16], b[16], ainv[16], binv[16];
+    for (int i = 0; i < 16; ++i) {
+        a[i] = ref[i];
+        b[i] = cur[i];
+    }
+    a[12] = a[13] = a[14] = 0.0;
+    a[15] = 1.0;
+    b[12] = b[13] = b[14] = 0.0;
+    b[15] = 1.0;
+    auto rigid_inv = [](const double *x, double *xi) {
+        for (int i = 0; i < 3; ++i) {
+            for (int j = 0; j < 3; ++j) xi[i * 4 + j] = x[j * 4 + i];
+            xi[i * 4 + 3] = -(x[0 * 4 + i] * x[3] + x[1 * 4 + i] * x[7] + x[2 * 4 + i] * x[11]);
+        }
+        xi[12] = xi[13] = xi[14] = 0.0;
+        xi[15] = 1.0;
+    };
+    auto mul = [](const double *x, const double *y, float *out) {
+        for (int i = 0; i < 3; ++i)
+            for (int j = 0; j < 4; ++j) {
+                double s = 0.0;
+                for (int k = 0; k < 4; ++k) s += x[i * 4 + k] * y[k * 4 + j];
+                out[i * 4 + j] = (float)s;
+            }
+    };
+    rigid_inv(a, ainv);
+    rigid_inv(b, binv);
+    mul(b, ainv, M);
+    mul(a, binv, Minv);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// opaque objects
+// ---------------------------------------------------------------------------
+
+struct tgs_scene {
+    int n = 0, deg = 0, ncoef = 1;
+    DevBuf data;
+    SceneDev view{};
+    Workspace ws;
+    int last_W = 0, last_H = 0;
+};
+
+struct tgs_state {
+    tgs_scene *scene = nullptr;
+    int W = 0, H = 0, TX = 0, TY = 0;
+    tgs_params p{};
+    Workspace ws;
+    DevBuf tgb_d, tgb_s, tab, g_flag, fbox, dmin, smax, dfill, uv, um, oc;
+    int frame_index = 0, since_true = 0, since_ref = 0, force_pseudo = 0, has_ref = 0;
+    float fbox_host[4] = {0, 0, 0, 0};
+    float ref_w2c[16] = {0};
+    float ref_intr[4] = {0};
+};
+
+// ---------------------------------------------------------------------------
+// shared frame steps
+// ---------------------------------------------------------------------------
+
+namespace {
+
+struct FrameResult {
+    uint32_t K = 0, n_surv = 0, n_newly = 0, n_sel = 0;
+};
+
+// Zero the counters and run the per-Gaussian stage.
+tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
+                           hipStream_t st) {
+    launch_fill_i32(ws.cnt.as<int>(), sizeof(Counters) / sizeof(int), 0, st);
+    launch_preprocess(sc->view, cam, cull, ws.records(), ws.cnt.as<Counters>(), st);
+    TGS_LAUNCHED("preprocess");
+    return TGS_OK;
+}
+
+// Scan the key counts and read the counters back (the one sync of a frame).
+tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
+                          FrameResult &fr) {
+    launch_scan(n, ws.rect.as<ushort4>(), rowpre, TX, ws.offsets.as<uint32_t>(),
+                ws.scan.as<uint32_t>(), ws.cnt.as<Counters>(), st);
+    TGS_LAUNCHED("scan");
+    TGS_HIP(hipMemcpyAsync(ws.host_cnt, ws.cnt.p, sizeof(Counters), hipMemcpyDeviceToHost, st));
+    TGS_HIP(hipStreamSynchronize(st));
+    fr.K = ws.host_cnt->n_keys;
+    fr.n_surv = ws.host_cnt->n_survivors;
+    fr.n_newly = ws.host_cnt->n_newly;
+    fr.n_sel = ws.host_cnt->n_selected;
+    if (fr.K > kMaxKeys)
+        return fail(TGS_ERR_CAPACITY, "frame needs " + std::to_string(fr.K) +
+                                          " Gaussian-tile keys; the limit is 2^30-1");
+    return TGS_OK;
+}
+
+// Duplicate, sort and find tile ranges; returns the sorted values buffer.
+tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint8_t *sel, uint32_t K,
+                     hipStream_t st, const uint32_t **sorted_vals) {
+    const int passes = sort_passes(TX * TY);
+    TGS_TRY(ws.ensure_keys(K, passes));
+    launch_duplicate(n, ws.rect.as<ushort4>(), ws.g1.as<float4>(), ws.offsets.as<uint32_t>(), sel,
+                     TX, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(), st);
+    TGS_LAUNCHED("duplicate");
+    const int alt = launch_sort(K, passes, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(),
+                                ws.keys_alt.as<uint64_t>(), ws.vals_alt.as<uint32_t>(),
+                                ws.sort.as<uint32_t>(), st);
+    TGS_LAUNCHED("sort");
+    const uint64_t *skeys = alt ? ws.keys_alt.as<uint64_t>() : ws.keys.as<uint64_t>();
+    launch_ranges(K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
+    TGS_LAUNCHED("ranges");
+    *sorted_vals = alt ? ws.vals_alt.as<uint32_t>() : ws.vals.as<uint32_t>();
+    ws.last_K = K;
+    ws.last_alt = alt;
+    ws.has_frame = true;
+    return TGS_OK;
+}
+
+BlendArgs blend_args(const Workspace &ws, int W, int H, const uint32_t *vals) {
+    BlendArgs a{};
+    a.W = W;
+    a.H = H;
+    a.TX = (W + 15) / 16;
+    a.TY = (H + 15) / 16;
+    a.ranges = ws.ranges.as<uint2>();
+    a.vals = vals;
+    a.g0 = ws.g0.as<float4>();
+    a.g1 = ws.g1.as<float4>();
+    a.col = ws.col.as<float4>();
+    return a;
+}
+
+CullK no_cull(float z_near, Workspace &ws) {
+    CullK c{};
+    c.z_near = z_near;
+    c.newly_list = ws.newly.as<int>();
+    c.lambda1 = 3.0f;
+    return c;
+}
+
+tgs_status check_params(const tgs_params *p) {
+    if (p->lambda_tdc < 1 || p->lambda_sr < 1)
+        return fail(TGS_ERR_INVALID_ARG, "lambda_tdc and lambda_sr must be >= 1");
+    if (!(finite(p->eta) && p->eta >= 0.0f))
+        return fail(TGS_ERR_INVALID_ARG, "eta must be finite and >= 0");
+    if (!(finite(p->lambda1) && finite(p->lambda2)))
+        return fail(TGS_ERR_INVALID_ARG, "lambda1, lambda2 must be finite");
+    if (!(finite(p->z_near) && p->z_near > 0.0f))
+        return fail(TGS_ERR_INVALID_ARG, "z_near must be finite and > 0");
+    return TGS_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C-ABI
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char *tgs_last_error(void) { return g_err.c_str(); }
+
+void tgs_params_default(tgs_params *p) {
+    if (!p) return;
+    p->lambda_tdc = 50;
+    p->lambda_sr = 5;
+    p->eta = 0.40f;
+    p->lambda1 = 3.0f;
+    p->lambda2 = 0.0f;
+    p->z_near = 0.2f;
+    p->enable_afc = 1;
+    p->enable_toc = 1;
+    p->enable_sr = 1;
+    p->force_all_dirty = 0;
+}
+
+tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **out) {
+    g_err.clear();
+    if (!d || !out) return fail(TGS_ERR_INVALID_ARG, "desc and out must not be NULL");
+    if (d->n < 0) return fail(TGS_ERR_INVALID_ARG, "n must be >= 0");
+    if (d->sh_degree < 0 || d->sh_degree > 3)
+        return fail(TGS_ERR_INVALID_ARG, "sh_degree must be within 0..3");
+    const int n = d->n, ncoef = (d->sh_degree + 1) * (d->sh_degree + 1);
+    if (n > 0 && (!d->means || !d->scales || !d->rotations || !d->opacities || !d->sh))
+        return fail(TGS_ERR_INVALID_ARG, "scene arrays must not be NULL when n > 0");
+    for (size_t k = 0; k < (size_t)n * 3; ++k)
+        if (!finite(d->means[k]) || !finite(d->scales[k]))
+            return fail(TGS_ERR_INVALID_ARG, "non-finite mean or scale");
+    for (int i = 0; i < n; ++i) {
+        const float *q = d->rotations + 4 * (size_t)i;
+        if (!(finite(q[0]) && finite(q[1]) && finite(q[2]) && finite(q[3])))
+            return fail(TGS_ERR_INVALID_ARG, "non-finite rotation");
+        if (q[0] == 0.0f && q[1] == 0.0f && q[2] == 0.0f && q[3] == 0.0f)
+            return fail(TGS_ERR_INVALID_ARG, "zero quaternion at Gaussian " + std::to_string(i));
+        if (!finite(d->opacities[i])) return fail(TGS_ERR_INVALID_ARG, "non-finite opacity");
+    }
+    for (size_t k = 0; k < (size_t)n * ncoef * 3; ++k)
+        if (!finite(d->sh[k])) return fail(TGS_ERR_INVALID_ARG, "non-finite SH coefficient");
+
+    tgs_scene *sc = new (std::nothrow) tgs_scene();
+    if (!sc) return fail(TGS_ERR_OUT_OF_MEMORY, "host allocation failed");
+    sc->n = n;
+    sc->deg = d->sh_degree;
+    sc->ncoef = ncoef;
+    const size_t nn = (size_t)(n > 0 ? n : 1);
+    const size_t n_arrays = 11 + (size_t)ncoef * 3;
+    tgs_status s = sc->data.ensure(n_arrays * nn * sizeof(float));
+    if (s != TGS_OK) {
+        delete sc;
+        return s;
+    }
+    float *base = sc->data.as<float>();
+    hipStream_t st = (hipStream_t)stream;
+    std::vector<float> stage(nn);
+    auto upload = [&](int slot, auto getter) -> hipError_t {
+        for (int i = 0; i < n; ++i) stage[i] = getter(i);
+        hipError_t e = hipMemcpyAsync(base + slot * nn, stage.data(), (size_t)n * sizeof(float),
+                                      hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return e;
+        return hipStreamSynchronize(st);
+    };
+    hipError_t e = hipSuccess;
+    for (int c = 0; c < 3 && e == hipSuccess && n > 0; ++c)
+        e = upload(c, [&](int i) { return d->means[3 * (size_t)i + c]; });
+    for (int c = 0; c < 3 && e == hipSuccess && n > 0; ++c)
+        e = upload(3 + c, [&](int i) { return d->scales[3 * (size_t)i + c]; });
+    for (int c = 0; c < 4 && e == hipSuccess && n > 0; ++c)
+        e = upload(6 + c, [&](int i) { return d->rotations[4 * (size_t)i + c]; });
+    if (e == hipSuccess && n > 0) e = upload(10, [&](int i) { return d->opacities[i]; });
+    for (int c = 0; c < ncoef * 3 && e == hipSuccess && n > 0; ++c)
+        e = upload(11 + c, [&](int i) { return d->sh[(size_t)i * ncoef * 3 + c]; });
+    if (e != hipSuccess) {
+        delete sc;
+        return fail(TGS_ERR_DEVICE, std::string("scene upload: ") + hipGetErrorString(e));
+    }
+    SceneDev &v = sc->view;
+    v.n = n;
+    v.deg = sc->deg;
+    v.ncoef = ncoef;
+    v.mx = base + 0 * nn;
+    v.my = base + 1 * nn;
+    v.mz = base + 2 * nn;
+    v.sx = base + 3 * nn;
+    v.sy = base + 4 * nn;
+    v.sz = base + 5 * nn;
+    v.qw = base + 6 * nn;
+    v.qx = base + 7 * nn;
+    v.qy = base + 8 * nn;
+    v.qz = base + 9 * nn;
+    v.opac = base + 10 * nn;
+    v.sh = base + 11 * nn;
+    // The SH block uses stride nn == n for n > 0 (see SceneDev::sh).
+    *out = sc;
+    return TGS_OK;
+}
+
+void tgs_scene_free(tgs_scene *scene) { delete scene; }
+
+int32_t tgs_scene_count(const tgs_scene *scene) { return scene ? scene->n : 0; }
+
+tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *out,
+                           void *stream) {
+    g_err.clear();
+    if (!sc || !out || !out->rgb) return fail(TGS_ERR_INVALID_ARG, "scene, out and out->rgb are required");
+    TGS_TRY(check_camera(cam));
+    hipStream_t st = (hipStream_t)stream;
+    const int W = cam->width, H = cam->height, TX = (W + 15) / 16, TY = (H + 15) / 16;
+    Workspace &ws = sc->ws;
+    TGS_TRY(ws.prepare(sc->n, W, H));
+    const CamK ck = make_camk(cam);
+    TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
+    FrameResult fr;
+    TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr));
+    const uint32_t *vals = nullptr;
+    TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, fr.K, st, &vals));
+    if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
+    BlendArgs a = blend_args(ws, W, H, vals);
+    a.rgb = out->rgb;
+    a.depth = out->depth;
+    a.sigma = out->sigma;
+    a.alpha = out->alpha;
+    a.contrib = out->contrib;
+    launch_blend(a, TX * TY, st);
+    TGS_LAUNCHED("blend");
+    if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)TX * TY, 1, st);
+    TGS_LAUNCHED("tile mask");
+    sc->last_W = W;
+    sc->last_H = H;
+    out->frame_kind = TGS_FRAME_FULL;
+    out->n_selected = TX * TY;
+    out->n_survivors = (int32_t)fr.n_surv;
+    out->n_newly_visible = 0;
+    out->n_keys = fr.K;
+    return TGS_OK;
+}
+
+tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
+                            const tgs_params *params, tgs_state **out) {
+    g_err.clear();
+    if (!scene || !out) return fail(TGS_ERR_INVALID_ARG, "scene and out must not be NULL");
+    if (width < 1 || height < 1 || width > 16384 || height > 16384)
+        return fail(TGS_ERR_INVALID_ARG, "image size must be within 1..16384");
+    tgs_params p;
+    tgs_params_default(&p);
+    if (params) p = *params;
+    TGS_TRY(check_params(&p));
+    tgs_state *s = new (std::nothrow) tgs_state();
+    if (!s) return fail(TGS_ERR_OUT_OF_MEMORY, "host allocation failed");
+    s->scene = scene;
+    s->W = width;
+    s->H = height;
+    s->TX = (width + 15) / 16;
+    s->TY = (height + 15) / 16;
+    s->p = p;
+    const size_t px = (size_t)width * height, nt = (size_t)s->TX * s->TY;
+    const size_t nn = (size_t)(scene->n > 0 ? scene->n : 1);
+    tgs_status st = TGS_OK;
+    if (st == TGS_OK) st = s->tgb_d.ensure(px * 4);
+    if (st == TGS_OK) st = s->tgb_s.ensure(px * 4);
+    if (st == TGS_OK) st = s->tab.ensure(3 * px * 4);
+    if (st == TGS_OK) st = s->g_flag.ensure(nn);
+    if (st == TGS_OK) st = s->fbox.ensure(16);
+    if (st == TGS_OK) st = s->dmin.ensure(px * 4);
+    if (st == TGS_OK) st = s->smax.ensure(px * 4);
+    if (st == TGS_OK) st = s->dfill.ensure(px * 4);
+    if (st == TGS_OK) st = s->uv.ensure(px * 8);
+    if (st == TGS_OK) st = s->um.ensure(nt);
+    if (st == TGS_OK) st = s->oc.ensure(nt);
+    if (st == TGS_OK) st = s->ws.prepare(scene->n, width, height);
+    if (st != TGS_OK) {
+        delete s;
+        return st;
+    }
+    *out = s;
+    return TGS_OK;
+}
+
+tgs_status tgs_state_reset(tgs_state *s) {
+    g_err.clear();
+    if (!s) return fail(TGS_ERR_INVALID_ARG, "state is NULL");
+    s->frame_index = s->since_true = s->since_ref = s->force_pseudo = s->has_ref = 0;
+    return TGS_OK;
+}
+
+void tgs_state_free(tgs_state *s) { delete s; }
+
+tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_out *out,
+                               void *stream) {
+    g_err.clear();
+    if (!s || !out || !out->rgb) return fail(TGS_ERR_INVALID_ARG, "state, out and out->rgb are required");
+    TGS_TRY(check_camera(cam));
+    if (cam->width != s->W || cam->height != s->H)
+        return fail(TGS_ERR_STATE_MISMATCH, "camera size differs from the state's");
+    hipStream_t st = (hipStream_t)stream;
+    tgs_scene *sc = s->scene;
+    const int W = s->W, H = s->H, TX = s->TX, TY = s->TY, nt = TX * TY;
+    Workspace &ws = s->ws;
+    TGS_TRY(ws.prepare(sc->n, W, H));
+    const CamK ck = make_camk(cam);
+    const tgs_params &p = s->p;
+
+    // schedule (Sec. III-B, III-E, IV-B)
+    int kind;
+    if (!s->has_ref || s->frame_index == 0 || s->since_true >= p.lambda_tdc)
+        kind = TGS_FRAME_TRUE_REF;
+    else if (s->force_pseudo || s->since_ref >= p.lambda_sr)
+        kind = TGS_FRAME_PSEUDO_REF;
+    else
+        kind = TGS_FRAME_TGS;
+
+    FrameResult fr;
+    const uint32_t *vals = nullptr;
+    if (kind == TGS_FRAME_TGS) {
+        WarpK w{};
+        relative_pose(s->ref_w2c, cam->world_to_cam, w.M, w.Minv);
+        for (int k = 0; k < 4; ++k) w.kref[k] = s->ref_intr[k];
+        w.kcur[0] = cam->fx;
+        w.kcur[1] = cam->fy;
+        w.kcur[2] = cam->cx;
+        w.kcur[3] = cam->cy;
+        w.z_near = p.z_near;
+        w.W = W;
+        w.H = H;
+        w.TX = TX;
+        w.TY = TY;
+        launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
+                             s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
+        launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
+                            s->smax.as<float>(), st);
+        launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
+                          s->um.as<uint8_t>(), st);
+        TGS_LAUNCHED("warp");
+        CullK cull = no_cull(p.z_near, ws);
+        cull.afc = p.enable_afc;
+        cull.fbox = s->fbox.as<int>();
+        cull.toc = p.enable_toc;
+        cull.dmin = s->dmin.as<float>();
+        cull.smax = s->smax.as<float>();
+        cull.g_rendered = s->g_flag.as<uint8_t>();
+        cull.lambda1 = p.lambda1;
+        cull.lambda2 = p.lambda2;
+        TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
+        launch_occluded(w, ws.newly.as<int>(), ws.cnt.as<Counters>(), ws.g0.as<float4>(),
+                        ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
+        const int mode = (!p.enable_sr || p.force_all_dirty) ? 1 : 0;
+        launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(), ws.sel.as<uint8_t>(),
+                      ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(), out->tile_mask,
+                      ws.cnt.as<Counters>(), st);
+        TGS_LAUNCHED("tile selection");
+        TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr));
+        TGS_TRY(step_keys(ws, sc->n, TX, TY, ws.sel.as<uint8_t>(), fr.K, st, &vals));
+        BlendArgs a = blend_args(ws, W, H, vals);
+        a.tile_list = ws.sel_list.as<int>();
+        a.rgb = out->rgb;
+        launch_blend(a, (int)fr.n_sel, st);
+        TGS_LAUNCHED("blend");
+        launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(), out->rgb, st);
+        TGS_LAUNCHED("stitch");
+    } else {
+        CullK cull = no_cull(p.z_near, ws);
+        cull.afc = (kind == TGS_FRAME_PSEUDO_REF && p.enable_afc) ? 1 : 0;
+        cull.fbox = s->fbox.as<int>();
+        launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
+        TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
+        TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr));
+        TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, fr.K, st, &vals));
+        if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
+        BlendArgs a = blend_args(ws, W, H, vals);
+        a.rgb = out->rgb;
+        a.tab = s->tab.as<float>();
+        a.depth = out->depth;
+        a.sigma = out->sigma;
+        a.alpha = out->alpha;
+        a.tgb_depth = s->tgb_d.as<float>();
+        a.tgb_sigma = s->tgb_s.as<float>();
+        a.g_flag = s->g_flag.as<uint8_t>();
+        a.contrib = out->contrib;
+        launch_blend(a, nt, st);
+        TGS_LAUNCHED("blend");
+        if (kind == TGS_FRAME_TRUE_REF) {
+            launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
+                              s->fbox.as<int>(), st);
+            TGS_LAUNCHED("adaptive frustum");
+        }
+        if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
+        launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
+        TGS_LAUNCHED("tile mask");
+        memcpy(s->ref_w2c, cam->world_to_cam, sizeof(s->ref_w2c));
+        s->ref_intr[0] = cam->fx;
+        s->ref_intr[1] = cam->fy;
+        s->ref_intr[2] = cam->cx;
+        s->ref_intr[3] = cam->cy;
+        s->has_ref = 1;
+        fr.n_sel = (uint32_t)nt;
+    }
+
+    // counters (Sec. III-B) and adaptive reference insertion (Sec. III-E)
+    s->frame_index += 1;
+    if (kind == TGS_FRAME_TRUE_REF) {
+        s->since_true = 1;
+        s->since_ref = 1;
+        s->force_pseudo = 0;
+    } else if (kind == TGS_FRAME_PSEUDO_REF) {
+        s->since_true += 1;
+        s->since_ref = 1;
+        s->force_pseudo = 0;
+    } else {
+        s->since_true += 1;
+        s->since_ref += 1;
+        if (p.enable_sr) s->force_pseudo = (double)fr.n_sel > (double)p.eta * (double)nt ? 1 : 0;
+    }
+    out->frame_kind = kind;
+    out->n_selected = (int32_t)fr.n_sel;
+    out->n_survivors = (int32_t)fr.n_surv;
+    out->n_newly_visible = kind == TGS_FRAME_TGS ? (int32_t)fr.n_newly : 0;
+    out->n_keys = fr.K;
+    return TGS_OK;
+}
+
+tgs_status tgs_state_export(const tgs_state *s, void *host, size_t *nbytes) {
+    g_err.clear();
+    if (!s || !nbytes) return fail(TGS_ERR_INVALID_ARG, "state and nbytes must not be NULL");
+    const size_t px = (size_t)s->W * s->H, n = (size_t)s->scene->n;
+    const size_t need = sizeof(tgs_state_header) + (5 * px) * sizeof(float) + n;
+    if (!host) {
+        *nbytes = need;
+        return TGS_OK;
+    }
+    if (*nbytes < need) return fail(TGS_ERR_INVALID_ARG, "export buffer too small");
+    TGS_HIP(hipDeviceSynchronize());
+    tgs_state_header h{};
+    h.magic = 0x54475331u;
+    h.width = s->W;
+    h.height = s->H;
+    h.n = s->scene->n;
+    h.frame_index = s->frame_index;
+    h.since_true_ref = s->since_true;
+    h.since_ref = s->since_ref;
+    h.force_pseudo = s->force_pseudo;
+    h.has_reference = s->has_ref;
+    int fb[4];
+    TGS_HIP(hipMemcpy(fb, s->fbox.p, sizeof(fb), hipMemcpyDeviceToHost));
+    for (int k = 0; k < 4; ++k) {
+        const int i = fb[k] >= 0 ? fb[k] : fb[k] ^ 0x7fffffff;
+        memcpy(&h.fbox[k], &i, 4);
+    }
+    memcpy(h.ref_world_to_cam, s->ref_w2c, sizeof(h.ref_world_to_cam));
+    memcpy(h.ref_intrinsics, s->ref_intr, sizeof(h.ref_intrinsics));
+    char *dst = static_cast<char *>(host);
+    memcpy(dst, &h, sizeof(h));
+    dst += sizeof(h);
+    TGS_HIP(hipMemcpy(dst, s->tgb_d.p, px * 4, hipMemcpyDeviceToHost));
+    dst += px * 4;
+    TGS_HIP(hipMemcpy(dst, s->tgb_s.p, px * 4, hipMemcpyDeviceToHost));
+    dst += px * 4;
+    TGS_HIP(hipMemcpy(dst, s->tab.p, 3 * px * 4, hipMemcpyDeviceToHost));
+    dst += 3 * px * 4;
+    if (n) TGS_HIP(hipMemcpy(dst, s->g_flag.p, n, hipMemcpyDeviceToHost));
+    *nbytes = need;
+    return TGS_OK;
+}
+
+tgs_status tgs_state_import(tgs_state *s, const void *host, size_t nbytes) {
+    g_err.clear();
+    if (!s || !host) return fail(TGS_ERR_INVALID_ARG, "state and host must not be NULL");
+    const size_t px = (size_t)s->W * s->H, n = (size_t)s->scene->n;
+    const size_t need = sizeof(tgs_state_header) + (5 * px) * sizeof(float) + n;
+    if (nbytes != need) return fail(TGS_ERR_INVALID_ARG, "blob size does not match the state");
+    tgs_state_header h;
+    memcpy(&h, host, sizeof(h));
+    if (h.magic != 0x54475331u) return fail(TGS_ERR_INVALID_ARG, "bad blob magic");
+    if (h.width != s->W || h.height != s->H || h.n != s->scene->n)
+        return fail(TGS_ERR_STATE_MISMATCH, "blob sizes differ from the state's");
+    TGS_HIP(hipDeviceSynchronize());
+    const char *src = static_cast<const char *>(host) + sizeof(h);
+    TGS_HIP(hipMemcpy(s->tgb_d.p, src, px * 4, hipMemcpyHostToDevice));
+    src += px * 4;
+    TGS_HIP(hipMemcpy(s->tgb_s.p, src, px * 4, hipMemcpyHostToDevice));
+    src += px * 4;
+    TGS_HIP(hipMemcpy(s->tab.p, src, 3 * px * 4, hipMemcpyHostToDevice));
+    src += 3 * px * 4;
+    if (n) TGS_HIP(hipMemcpy(s->g_flag.p, src, n, hipMemcpyHostToDevice));
+    int fb[4];
+    for (int k = 0; k < 4; ++k) {
+        int i;
+        memcpy(&i, &h.fbox[k], 4);
+        fb[k] = i >= 0 ? i : i ^ 0x7fffffff;
+    }
+    TGS_HIP(hipMemcpy(s->fbox.p, fb, sizeof(fb), hipMemcpyHostToDevice));
+    s->frame_index = h.frame_index;
+    s->since_true = h.since_true_ref;
+    s->since_ref = h.since_ref;
+    s->force_pseudo = h.force_pseudo;
+    s->has_ref = h.has_reference;
+    memcpy(s->ref_w2c, h.ref_world_to_cam, sizeof(s->ref_w2c));
+    memcpy(s->ref_intr, h.ref_intrinsics, sizeof(s->ref_intr));
+    return TGS_OK;
+}
+
+tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_t what, void *host,
+                          size_t *nbytes) {
+    g_err.clear();
+    if (!nbytes || (!scene && !state))
+        return fail(TGS_ERR_INVALID_ARG, "nbytes and one of scene/state are required");
+    const Workspace &ws = state ? state->ws : scene->ws;
+    const int n = state ? state->scene->n : scene->n;
+    const int W = state ? state->W : scene->last_W, H = state ? state->H : scene->last_H;
+    const size_t px = (size_t)W * H, nt = (size_t)((W + 15) / 16) * ((H + 15) / 16);
+    const void *src = nullptr;
+    size_t size = 0;
+    if (!ws.has_frame) return fail(TGS_ERR_INVALID_ARG, "no frame has been rendered yet");
+    switch (what) {
+        case TGS_DUMP_SORTED_VALUES:
+            src = ws.last_alt ? ws.vals_alt.p : ws.vals.p;
+            size = (size_t)ws.last_K * 4;
+            break;
+        case TGS_DUMP_SORTED_KEYS:
+            src = ws.last_alt ? ws.keys_alt.p : ws.keys.p;
+            size = (size_t)ws.last_K * 8;
+            break;
+        case TGS_DUMP_TILE_RANGES: src = ws.ranges.p; size = nt * 8; break;
+        case TGS_DUMP_RECTS: src = ws.rect.p; size = (size_t)n * 8; break;
+        case TGS_DUMP_STATUS: src = ws.status.p; size = (size_t)n; break;
+        case TGS_DUMP_SELECTED: src = ws.sel.p; size = nt; break;
+        case TGS_DUMP_RECORDS: size = (size_t)n * 48; break;
+        default:
+            if (!state) return fail(TGS_ERR_INVALID_ARG, "this buffer exists only for a state");
+            switch (what) {
+                case TGS_DUMP_WARP_DEPTH: src = state->dmin.p; size = px * 4; break;
+                case TGS_DUMP_WARP_SIGMA: src = state->smax.p; size = px * 4; break;
+                case TGS_DUMP_FILLED_DEPTH: src = state->dfill.p; size = px * 4; break;
+                case TGS_DUMP_CORRESPONDENCE: src = state->uv.p; size = px * 8; break;
+                case TGS_DUMP_UNMATCHED: src = state->um.p; size = nt; break;
+                case TGS_DUMP_OCCLUDED: src = state->oc.p; size = nt; break;
+                default: return fail(TGS_ERR_INVALID_ARG, "unknown dump id");
+            }
+    }
+    if (!host) {
+        *nbytes = size;
+        return TGS_OK;
+    }
+    if (*nbytes < size) return fail(TGS_ERR_INVALID_ARG, "dump buffer too small");
+    TGS_HIP(hipDeviceSynchronize());
+    if (what == TGS_DUMP_RECORDS) {
+        float *dst = static_cast<float *>(host);
+        std::vector<float4> tmp((size_t)n);
+        const DevBuf *parts[3] = {&ws.g0, &ws.g1, &ws.col};
+        for (int k = 0; k < 3; ++k) {
+            if (n) TGS_HIP(hipMemcpy(tmp.data(), parts[k]->p, (size_t)n * 16, hipMemcpyDeviceToHost));
+            for (int i = 0; i < n; ++i) memcpy(dst + (size_t)i * 12 + 4 * k, &tmp[i], 16);
+        }
+    } else if (size) {
+        TGS_HIP(hipMemcpy(host, src, size, hipMemcpyDeviceToHost));
+    }
+    *nbytes = size;
+    return TGS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,137 @@
+// Internal declarations shared by the HIP translation units of libtgs.
+// Kernel argument structs and the host-side launchers each .hip file exports.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tgs {
+
+constexpr float kNoHit = 1001.0f;           // z_far (1000) + epsilon (1)
+constexpr float kAlphaMin = 1.0f / 255.0f;
+constexpr float kAlphaMax = 0.99f;
+constexpr float kTMin = 1e-4f;
+constexpr int kTile = 16;
+constexpr uint32_t kMaxKeys = (1u << 30) - 1;
+
+// Camera constants as the kernels consume them.
+struct CamK {
+    float V[12];              // rows 0..2 of world->camera
+    float fx, fy, cx, cy;
+    int W, H, TX, TY;
+    float limx, limy;         // 1.3 * tan(half fov) guards of the Jacobian
+    float campos[3];          // camera centre in world space
+};
+
+// Device scene, structure of arrays.
+struct SceneDev {
+    int n, deg, ncoef;
+    const float *mx, *my, *mz;
+    const float *sx, *sy, *sz;
+    const float *qw, *qx, *qy, *qz;
+    const float *opac;
+    const float *sh;          // [(k*3 + ch) * n + i]
+};
+
+// Per-Gaussian records written by the preprocess.
+struct Records {
+    float4 *g0;               // u, v, conic a, conic b
+    float4 *g1;               // conic c, opacity, depth, 0
+    float4 *col;              // r, g, b, 0
+    ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
+    uint8_t *status;          // bit0 survivor, bit1 newly visible
+};
+
+// Temporal dynamic culling inputs of the preprocess.
+struct CullK {
+    float z_near;
+    int afc, toc;
+    const int *fbox;          // ordered-int encoded F_min.x, F_min.y, F_max.x, F_max.y
+    const float *dmin, *smax; // warped TGB
+    const uint8_t *g_rendered;
+    float lambda1, lambda2;
+    int *newly_list;          // appended indices of newly visible Gaussians
+};
+
+// Frame counters on the device (read back once per frame).
+struct Counters {
+    uint32_t n_keys;
+    uint32_t n_survivors;
+    uint32_t n_newly;
+    uint32_t n_selected;
+};
+
+// Ordered-int encoding of a float: signed-int order equals float order, so
+// integer atomic min/max give exact float min/max.
+__device__ inline int float_to_ordered(float f) {
+    int i = __float_as_int(f);
+    return i >= 0 ? i : i ^ 0x7fffffff;
+}
+__device__ inline float ordered_to_float(int i) {
+    return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff);
+}
+
+// ---- launchers (k_preprocess.hip) ----
+void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
+                       Counters *cnt, hipStream_t st);
+
+// ---- launchers (k_keys.hip) ----
+size_t scan_scratch_words(int n);
+void launch_scan(int n, const ushort4 *rect, const uint32_t *rowpre, int TX, uint32_t *offsets,
+                 uint32_t *scratch, Counters *cnt, hipStream_t st);
+void launch_duplicate(int n, const ushort4 *rect, const float4 *g1, const uint32_t *offsets,
+                      const uint8_t *sel, int TX, uint64_t *keys, uint32_t *vals, hipStream_t st);
+void launch_ranges(uint32_t K, int n_tiles, const uint64_t *keys, uint2 *ranges, hipStream_t st);
+
+// ---- launchers (k_sort.hip) ----
+size_t sort_scratch_words(uint32_t K, int passes);
+int sort_passes(int n_tiles);
+// Sorts (keys, vals) in place by key; alt buffers of the same size are used
+// as ping-pong storage.  Returns 1 if the result ended in the alt buffers.
+int launch_sort(uint32_t K, int passes, uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
+                uint32_t *vals_alt, uint32_t *scratch, hipStream_t st);
+
+// ---- launchers (k_blend.hip) ----
+struct BlendArgs {
+    int W, H, TX, TY;
+    const int *tile_list;     // NULL: blockIdx = tile
+    const uint2 *ranges;
+    const uint32_t *vals;
+    const float4 *g0, *g1, *col;
+    float *rgb;               // [3][H][W]
+    float *tab;               // optional second copy of rgb
+    float *depth, *sigma, *alpha;       // optional outputs
+    float *tgb_depth, *tgb_sigma;       // optional second copies
+    uint8_t *g_flag;          // optional: Gaussian composited somewhere
+    float *contrib;           // optional: max weight per Gaussian
+};
+void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st);
+void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
+                       hipStream_t st);
+
+// ---- launchers (k_temporal.hip) ----
+struct WarpK {
+    float M[12];              // reference camera -> current camera
+    float Minv[12];           // current camera -> reference camera
+    float kref[4], kcur[4];   // fx, fy, cx, cy
+    float z_near;
+    int W, H, TX, TY;
+};
+void launch_temporal_init(int n_px, int n_tiles, float *dmin, float *smax, uint8_t *oc,
+                          Counters *cnt, hipStream_t st);
+void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *dmin, float *smax,
+                         hipStream_t st);
+void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
+                       hipStream_t st);
+void launch_occluded(const WarpK &w, const int *newly_list, const Counters *cnt, const float4 *g0,
+                     const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st);
+void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
+                   int *sel_list, uint32_t *rowpre, uint8_t *mask_out, Counters *cnt,
+                   hipStream_t st);
+void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,
+                   float *rgb, hipStream_t st);
+void launch_fill_u8(uint8_t *p, size_t n, uint8_t v, hipStream_t st);
+void launch_fill_f32(float *p, size_t n, float v, hipStream_t st);
+void launch_fill_i32(int *p, size_t n, int v, hipStream_t st);
+
+}  // namespace tgs

@@ -1,0 +1,119 @@
+"""CPU checks of the C-ABI library: it loads, exports every function that
+include/tgs.h declares, and rejects bad arguments before touching a GPU."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2607_03390_amd import synth, tgs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tgs.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = set(re.findall(r"\b(tgs_[a-z_]+)\s*\(", src))
+    return sorted(names)
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for must in ("tgs_scene_upload", "tgs_render_full", "tgs_state_create", "tgs_render_temporal"):
+        assert must in names
+    assert sorted(tgs.EXPORTED) == names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", tgs.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (tgs_[a-z_]+)$", out, flags=re.M))
+    missing = [n for n in _declared() if n not in exported]
+    assert not missing, missing
+    L = tgs.lib()
+    for n in _declared():
+        assert hasattr(L, n)
+
+
+def test_struct_layouts_match_header():
+    # sizes follow from the C declarations with natural alignment
+    assert C.sizeof(tgs.tgs_camera) == 16 * 4 + 4 * 4 + 2 * 4
+    assert C.sizeof(tgs.tgs_params) == 10 * 4
+    assert C.sizeof(tgs.tgs_frame_out) == 6 * 8 + 4 * 4 + 8
+    assert C.sizeof(tgs.tgs_scene_desc) == 8 + 5 * 8
+    assert C.sizeof(tgs.tgs_state_header) == 9 * 4 + 4 * 4 + 16 * 4 + 4 * 4
+
+
+def test_params_default_are_the_papers():
+    p = tgs.params()
+    assert (p.lambda_tdc, p.lambda_sr) == (50, 5)
+    assert abs(p.eta - 0.40) < 1e-7 and p.lambda1 == 3.0 and p.lambda2 == 0.0
+    assert abs(p.z_near - 0.2) < 1e-7
+    assert p.enable_afc == p.enable_toc == p.enable_sr == 1 and p.force_all_dirty == 0
+
+
+def _bad_upload(**kw):
+    sc = synth.small_scene(4, 0, degree=1)
+    d = tgs.tgs_scene_desc()
+    arrs = [np.ascontiguousarray(a, np.float32) for a in
+            (sc.means, sc.scales, sc.rotations, sc.opacities, sc.sh)]
+    d.n, d.sh_degree = 4, 1
+    d.means, d.scales, d.rotations, d.opacities, d.sh = [a.ctypes.data for a in arrs]
+    for k, v in kw.items():
+        if k in ("nan_mean", "zero_quat"):
+            if k == "nan_mean":
+                arrs[0][1, 2] = np.nan
+            else:
+                arrs[2][3] = 0.0
+        else:
+            setattr(d, k, v)
+    h = C.c_void_p()
+    st = tgs.lib().tgs_scene_upload(C.byref(d), None, C.byref(h))
+    return st, tgs.lib().tgs_last_error().decode()
+
+
+@pytest.mark.parametrize("kw", [dict(n=-1), dict(sh_degree=4), dict(sh_degree=-1),
+                                dict(means=None), dict(nan_mean=True), dict(zero_quat=True)])
+def test_scene_upload_rejects_bad_input_on_host(kw):
+    st, msg = _bad_upload(**kw)
+    assert st == tgs.TGS_ERR_INVALID_ARG and msg
+
+
+def test_render_rejects_bad_camera_on_host():
+    L = tgs.lib()
+    o = tgs.tgs_frame_out()
+    o.rgb = 1  # never dereferenced: validation fails first
+    cam = tgs.camera(synth.make_camera(np.eye(4), 32, 32))
+    cam.world_to_cam[0] = 2.0                  # not a rotation
+    dummy = C.c_void_p(1)
+    assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    assert "orthonormal" in L.tgs_last_error().decode()
+    cam = tgs.camera(synth.make_camera(np.eye(4), 32, 32))
+    cam.fx = 0.0
+    assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    cam = tgs.camera(synth.make_camera(np.eye(4), 0, 32))
+    assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    o.rgb = None
+    cam = tgs.camera(synth.make_camera(np.eye(4), 32, 32))
+    assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+
+
+def test_state_create_rejects_bad_params_on_host():
+    L = tgs.lib()
+    h = C.c_void_p()
+    dummy = C.c_void_p(1)
+    for kw in (dict(lambda_sr=0), dict(lambda_tdc=0), dict(eta=float("nan")), dict(z_near=0.0)):
+        p = tgs.params(**kw)
+        assert L.tgs_state_create(dummy, 64, 64, C.byref(p), C.byref(h)) == tgs.TGS_ERR_INVALID_ARG
+    assert L.tgs_state_create(dummy, 0, 64, None, C.byref(h)) == tgs.TGS_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(tgs, "_LIB", None)
+    monkeypatch.setattr(tgs, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        tgs.lib()

@@ -1,0 +1,277 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle on the
+same seeded inputs.
+
+Bit-exact: survivors, newly-visible flags, projected means, conics, depths,
+tile rectangles, key counts, every per-tile sorted list, the warped depth and
+sigma buffers, the repaired depth, correspondences, unmatched / occluded /
+selected tile masks.  Within tolerance: colour (2e-4), Eq. 1/2 moments,
+alpha, stitched pixels.  Pixels (and occluded tiles) whose blending takes a
+decision within the oracle's margin of a threshold are excluded and counted.
+Temporal frames use state injection: the GPU's priors after frame t are
+imported into the oracle before both render frame t+1.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_03390_amd import synth, tgs
+from tests.parity_util import (RGB_TOL, STITCH_TOL, check_gaussian_buffer, check_image, check_lists,
+                               check_moments, check_records, dumps, gpu_full, import_into_oracle,
+                               log, tile_pixels)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    torch.cuda.set_device(0)
+    tgs.lib()
+
+
+class Uploaded:
+    def __init__(self, scene):
+        self.scene = scene
+
+    def __enter__(self):
+        self.h = tgs.tgs_scene_upload(self.scene)
+        return self.h
+
+    def __exit__(self, *a):
+        tgs.tgs_scene_free(self.h)
+
+
+def _full_parity(scene, cams, sample_tiles=None, label=""):
+    n = scene.n
+    with Uploaded(scene) as h:
+        for k, cam in enumerate(cams):
+            W, H = cam.width, cam.height
+            TX, TY = cam.tiles
+            log(f"[full parity {label}] cam {k} {W}x{H} n={n}")
+            res = gpu_full(h, cam, n)
+            d = dumps(h, None, n)
+            g = O.gaussians(scene, cam)
+            ts, items = O.tile_lists(g, TX, TY)
+            check_records(d, g)
+            check_lists(d, ts, items)
+            assert res["n_keys"] == items.size and res["n_survivors"] == g["n_survivors"]
+            assert res["frame_kind"] == tgs.TGS_FRAME_FULL and np.all(res["tile_mask"] == 1)
+            b = O.blend(W, H, ts, items, g, None if sample_tiles is None else np.asarray(sample_tiles, np.int32))
+            rendered = np.ones((TY, TX), bool)
+            if sample_tiles is not None:
+                rendered = np.zeros(TX * TY, bool)
+                rendered[np.asarray(sample_tiles)] = True
+                rendered = rendered.reshape(TY, TX)
+            ok = tile_pixels(rendered, W, H) & (b["margin_pos"] < 0)
+            worst = check_image(res["rgb"], b["rgb"], ok, where=f"cam {k}")
+            check_moments(res, b, ok)
+            if sample_tiles is None:
+                check_gaussian_buffer(res["contrib"][:n] > 0, b)
+            log(f"    keys {items.size} pairs {b['pairs']} max|drgb| {worst:.2e} "
+                f"margin px {(b['margin_pos'] >= 0).sum()}")
+
+
+def test_full_parity_tiny_orbit():
+    w = synth.workload("tiny")
+    _full_parity(w.scene, w.cameras, label="tiny")
+
+
+@pytest.mark.parametrize("n,seed,deg,W,H", [(3000, 1, 3, 200, 136), (500, 2, 2, 37, 53),
+                                            (50, 3, 1, 1, 1), (2000, 4, 0, 300, 17),
+                                            (4000, 5, 3, 64, 64)])
+def test_full_parity_ragged(n, seed, deg, W, H):
+    sc = synth.small_scene(n, seed, degree=deg)
+    cams = [synth.make_camera(synth.look_at(e, (0, 0, 0)), W, H)
+            for e in ((0.2, -3.0, 0.7), (2.5, 1.0, -0.4), (0.0, -1.2, 0.1))]
+    _full_parity(sc, cams, label=f"ragged {W}x{H}")
+
+
+def test_full_parity_object_subset():
+    w = synth.workload("object", n_gaussians=40_000)
+    _full_parity(w.scene, [w.cameras[0], w.cameras[37]], label="object 40k")
+
+
+def test_empty_and_invisible_scenes():
+    import torch
+    sc = synth.small_scene(0, 0, degree=0)
+    cam = synth.make_camera(synth.look_at((0, -3, 0), (0, 0, 0)), 48, 40)
+    with Uploaded(sc) as h:
+        res = gpu_full(h, cam, 0)
+        assert res["n_keys"] == 0 and np.all(res["rgb"] == 0) and np.all(res["depth"] == O.NOHIT)
+        assert np.all(res["alpha"] == 0) and np.all(res["sigma"] == 0)
+    sc = synth.small_scene(300, 1, degree=1)
+    back = synth.make_camera(synth.look_at((0, -3, 0), (0, -6, 0)), 48, 40)   # looks away
+    with Uploaded(sc) as h:
+        res = gpu_full(h, back, sc.n)
+        assert res["n_keys"] == 0 and res["n_survivors"] == 0 and np.all(res["rgb"] == 0)
+        s = tgs.tgs_state_create(h, 48, 40, tgs.params())
+        out = tgs.alloc_frame(48, 40, sc.n)
+        for _ in range(3):
+            info = tgs.tgs_render_temporal(s, back, **out)
+            torch.cuda.synchronize()
+            assert info["n_keys"] == 0 and torch.all(out["rgb"] == 0)
+        tgs.tgs_state_free(s)
+
+
+def _temporal_parity(scene, cams, W, H, label, **pkw):
+    import torch
+    n = scene.n
+    stats = dict(frames=0, tgs=0, margin_tiles=0, margin_px=0)
+    with Uploaded(scene) as h:
+        s = tgs.tgs_state_create(h, W, H, tgs.params(**pkw))
+        ora = O.TemporalOracle(scene, W, H, O.Params(**pkw))
+        try:
+            for k, cam in enumerate(cams):
+                blob = tgs.tgs_state_export(s)
+                if k > 0:
+                    import_into_oracle(ora, blob)
+                out = tgs.alloc_frame(W, H, n, depth=True, contrib=True, tile_mask=True)
+                log(f"[temporal parity {label}] frame {k}")
+                info = tgs.tgs_render_temporal(s, cam, **out)
+                torch.cuda.synchronize()
+                res = {kk: v.cpu().numpy() for kk, v in out.items()}
+                ref = ora.render(cam)
+                assert info["frame_kind"] == ref["kind"], (k, info["frame_kind"], ref["kind"])
+                d = dumps(None, s, n)
+                check_records(d, ref["g"])
+                stats["frames"] += 1
+                sel_tiles = res["tile_mask"].astype(bool)
+                if ref["kind"] == O.TGS_FRAME:
+                    stats["tgs"] += 1
+                    TX, TY = cam.tiles
+                    dm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_DEPTH).reshape(H, W)
+                    sm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_SIGMA).reshape(H, W)
+                    df = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_FILLED_DEPTH).reshape(H, W)
+                    uv = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_CORRESPONDENCE).reshape(H, W, 2)
+                    um = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_UNMATCHED).reshape(TY, TX)
+                    oc = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_OCCLUDED).reshape(TY, TX)
+                    assert np.array_equal(dm.view(np.uint32), ref["dmin"].view(np.uint32)), "warped depth"
+                    assert np.array_equal(sm, ref["smax"]), "warped sigma"
+                    assert np.array_equal(df.view(np.uint32), ref["dfill"].view(np.uint32)), "filled depth"
+                    assert np.array_equal(uv.view(np.uint32), ref["uv"].view(np.uint32)), "correspondences"
+                    assert np.array_equal(um, ref["um"]), "unmatched tiles"
+                    differ = oc != ref["oc"]
+                    assert not np.any(differ & (ref["oc_margin"] == 0)), "occluded tiles"
+                    stats["margin_tiles"] += int(differ.sum())
+                    sel_ref = ref["tile_sel"].astype(bool)
+                    if np.array_equal(sel_tiles, sel_ref):
+                        check_lists(d, ref["tile_start"], ref["items"],
+                                    tiles=np.flatnonzero(sel_ref.ravel()))
+                        assert info["n_keys"] == ref["K"]
+                    else:
+                        log(f"    selection differs only at margin tiles {np.flatnonzero(differ.ravel())}")
+                    assert info["n_selected"] == int(sel_tiles.sum())
+                    assert info["n_survivors"] == ref["n_survivors"]
+                    assert info["n_newly_visible"] == int(ref["g"]["newly_visible"].sum())
+                    rend = tile_pixels(sel_tiles & sel_ref, W, H)
+                    stitched = tile_pixels(~sel_tiles & ~sel_ref, W, H)
+                    ok = rend & (ref["margin_pos"] < 0)
+                    check_image(res["rgb"], ref["rgb"], ok, RGB_TOL, f"frame {k} rendered tiles")
+                    check_image(res["rgb"], ref["rgb"], stitched, STITCH_TOL, f"frame {k} stitched tiles")
+                    stats["margin_px"] += int((rend & (ref["margin_pos"] >= 0)).sum())
+                else:
+                    assert np.all(sel_tiles)
+                    check_lists(d, ref["tile_start"], ref["items"])
+                    assert info["n_keys"] == ref["K"] and info["n_survivors"] == ref["n_survivors"]
+                    ok = ref["margin_pos"] < 0
+                    check_image(res["rgb"], ref["rgb"], ok, RGB_TOL, f"frame {k} reference")
+                    check_moments(res, ref, ok)
+                    check_gaussian_buffer(res["contrib"][:n] > 0, ref)
+                    stats["margin_px"] += int((~ok).sum())
+                log(f"    kind {info['frame_kind']} sel {info['n_selected']} keys {info['n_keys']} "
+                    f"surv {info['n_survivors']} newly {info['n_newly_visible']}")
+        finally:
+            tgs.tgs_state_free(s)
+    log(f"[temporal parity {label}] {stats}")
+    return stats
+
+
+def test_temporal_parity_tiny():
+    w = synth.workload("tiny")
+    st = _temporal_parity(w.scene, w.cameras, 256, 256, "tiny")
+    assert st["tgs"] >= 1
+
+
+@pytest.mark.parametrize("pkw", [dict(), dict(lambda_sr=2), dict(enable_toc=0),
+                                 dict(enable_afc=0, eta=1.0), dict(enable_sr=0)])
+def test_temporal_parity_room_subset(pkw):
+    sc = synth.scene_room(60_000, 2)
+    cams = synth.handheld_path(12, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 400, 232)
+    st = _temporal_parity(sc, cams, 400, 232, f"room60k {pkw}", **pkw)
+    assert st["tgs"] >= 3
+
+
+def test_temporal_parity_cube_occlusion():
+    sc = synth.scene_uniform_cube(20_000, 7, degree=1, log_scale_mean=-3.3)
+    cams = synth.orbit_path(10, 3.0, 15.0, 1.0, 144, 120)
+    st = _temporal_parity(sc, cams, 144, 120, "cube20k", eta=1.0)
+    assert st["tgs"] >= 5
+
+
+def test_force_all_dirty_no_cull_equals_full():
+    import torch
+    w = synth.workload("tiny", n_frames=5)
+    with Uploaded(w.scene) as h:
+        s = tgs.tgs_state_create(h, 256, 256, tgs.params(enable_afc=0, enable_toc=0, force_all_dirty=1))
+        for cam in w.cameras:
+            a = tgs.alloc_frame(256, 256)
+            tgs.tgs_render_temporal(s, cam, **a)
+            b = gpu_full(h, cam, w.scene.n, depth=False, contrib=False)
+            torch.cuda.synchronize()
+            assert np.array_equal(a["rgb"].cpu().numpy(), b["rgb"])
+        tgs.tgs_state_free(s)
+
+
+def test_determinism():
+    import torch
+    w = synth.workload("tiny", n_frames=6)
+    with Uploaded(w.scene) as h:
+        s = tgs.tgs_state_create(h, 256, 256, tgs.params())
+        runs = []
+        for rep in range(2):
+            tgs.tgs_state_reset(s)
+            frames = []
+            for cam in w.cameras:
+                o = tgs.alloc_frame(256, 256)
+                tgs.tgs_render_temporal(s, cam, **o)
+                torch.cuda.synchronize()
+                frames.append((o["rgb"].cpu().numpy(), tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_SORTED_KEYS).copy()))
+            runs.append(frames)
+        for (a, ka), (b, kb) in zip(*runs):
+            assert np.array_equal(a, b) and np.array_equal(ka, kb)
+        tgs.tgs_state_free(s)
+
+
+def test_state_errors_on_device():
+    w = synth.workload("tiny", n_frames=1)
+    with Uploaded(w.scene) as h:
+        s = tgs.tgs_state_create(h, 256, 256)
+        other = synth.make_camera(w.cameras[0].w2c, 128, 256)
+        with pytest.raises(tgs.TgsError) as e:
+            tgs.tgs_render_temporal(s, other, **tgs.alloc_frame(128, 256))
+        assert e.value.status == tgs.TGS_ERR_STATE_MISMATCH
+        blob = tgs.tgs_state_export(s)
+        with pytest.raises(tgs.TgsError):
+            tgs.tgs_state_import(s, blob[:-1])
+        tgs.tgs_state_import(s, blob)
+        tgs.tgs_state_free(s)
+
+
+def test_full_size_room_frame():
+    """The 1.5M-Gaussian 1920x1080 workload in the benchmark's launch
+    configuration: every list bit-exact, colour and moments on sampled tiles,
+    then one TemporalGS frame by state injection."""
+    import torch
+    w = synth.workload("room", n_frames=2)
+    sc, cams = w.scene, w.cameras
+    TX, TY = cams[0].tiles
+    rng = np.random.default_rng(0)
+    g = O.gaussians(sc, cams[0])
+    ts, _ = O.tile_lists(g, TX, TY)
+    heavy = np.argsort(np.diff(ts))[-12:]
+    sample = np.unique(np.concatenate([heavy, rng.choice(TX * TY, 40, replace=False),
+                                       np.arange((TY - 1) * TX, TY * TX, 13)]))
+    _full_parity(sc, cams[:1], sample_tiles=sample, label="room 1.5M")
+    _temporal_parity(sc, cams[:2], 1920, 1080, "room 1.5M")
+    torch.cuda.synchronize()
