@@ -1,0 +1,243 @@
+"""Benchmark of the TemporalGS hot path on one MI355X.
+
+One step = one pass of the whole hot path over the 120-frame camera path of
+the room workload (1.5M Gaussians, SH degree 3, 1920x1080): the frame
+schedule renders true references, pseudo references and TemporalGS frames
+(adaptive frustum + occlusion culling, selective rendering, stitching), every
+one through the HIP kernels of libtgs.  The scene is resident in HBM before
+the timed region starts.
+
+Printed (one JSON line): temporal-mode FPS (value), full-render FPS over the
+same path, PSNR of temporal vs full, per-stage kernel times (HIP events on the
+launch stream, inside the timed region), the roofline of the dominant kernel
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms/frame & FPS (full vs temporal) at 1080p, 1.5M Gaussians; PSNR temporal-vs-full"
+# lane-operations per evaluated (pixel, Gaussian) pair of the blend (derivation in the design doc)
+BLEND_OPS_PER_PAIR = 25
+# non-packed fp32 VALU issue rate: 256 CUs x 64 lanes x 2.4 GHz
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "blend_traffic_room.json")
+BLEND_SRC = os.path.join(ROOT, "paper_2607_03390_amd", "csrc", "k_blend.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="room")
+    ap.add_argument("--frames", type=int, default=None, help="truncate the camera path")
+    ap.add_argument("--cpu-frames", type=int, default=3,
+                    help="frames of the path the CPU oracle renders for its baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-psnr", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run one device copy of this size (for HBM counter calibration)")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    return hashlib.sha256(open(BLEND_SRC, "rb").read()).hexdigest()[:16]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build targets one GPU: the TemporalGS hot path runs "
+                                   "on a single MI355X; run with --gpus 1"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2607_03390_amd import synth, tgs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    log(f"[bench] generating workload {args.workload}")
+    wl = synth.workload(args.workload, n_frames=args.frames)
+    cams = wl.cameras
+    W, H = cams[0].width, cams[0].height
+    TX, TY = cams[0].tiles
+    n = wl.scene.n
+    scene_h = tgs.tgs_scene_upload(wl.scene)
+    state_h = tgs.tgs_state_create(scene_h, W, H, tgs.params())
+    out_t = tgs.alloc_frame(W, H)
+    out_f = tgs.alloc_frame(W, H)
+    torch.cuda.synchronize()
+    log(f"[bench] {n} Gaussians, {W}x{H}, {len(cams)} frames uploaded")
+
+    def temporal_step(record=None):
+        tgs.tgs_state_reset(state_h)
+        for cam in cams:
+            info = tgs.tgs_render_temporal(state_h, cam, **out_t)
+            if record is not None:
+                record.append(info)
+
+    def full_step():
+        for cam in cams:
+            tgs.tgs_render_full(scene_h, cam, **out_f)
+
+    if args.copy_calibration_mb:
+        nb = args.copy_calibration_mb << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {nb} bytes done")
+        del src, dst
+
+    for w in range(args.warmup):
+        temporal_step()
+        full_step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {w + 1}/{args.warmup} done")
+
+    # untimed: evaluated pixel-Gaussian pairs per blend stage (deterministic)
+    tgs.tgs_profile_start(count_pairs=True)
+    kinds = []
+    temporal_step(kinds)
+    full_step()
+    counted = tgs.tgs_profile_stop()
+    log("[bench] pair counts done")
+
+    # timed: temporal mode, kernel events on
+    torch.cuda.synchronize()
+    tgs.tgs_profile_start(count_pairs=False)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        temporal_step()
+    torch.cuda.synchronize()
+    t_temporal = time.perf_counter() - t0
+    prof = tgs.tgs_profile_stop()
+    log(f"[bench] temporal timed: {t_temporal:.3f}s for {args.steps} steps")
+
+    # timed: full render of the same path
+    torch.cuda.synchronize()
+    tgs.tgs_profile_start(count_pairs=False)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        full_step()
+    torch.cuda.synchronize()
+    t_full = time.perf_counter() - t0
+    prof_full = tgs.tgs_profile_stop()
+    log(f"[bench] full timed: {t_full:.3f}s for {args.steps} steps")
+
+    n_frames = len(cams)
+    fps_t = n_frames * args.steps / t_temporal
+    fps_f = n_frames * args.steps / t_full
+
+    # per-kind frame times (untimed pass, events around each frame)
+    per_kind = {0: [], 1: [], 2: []}
+    tgs.tgs_state_reset(state_h)
+    for cam in cams:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        info = tgs.tgs_render_temporal(state_h, cam, **out_t)
+        e1.record()
+        torch.cuda.synchronize()
+        per_kind[info["frame_kind"]].append(e0.elapsed_time(e1))
+
+    # PSNR temporal vs full (images clamped to [0,1]); identical frames excluded
+    psnr = None
+    if not args.no_psnr:
+        vals = []
+        tgs.tgs_state_reset(state_h)
+        for cam in cams:
+            tgs.tgs_render_temporal(state_h, cam, **out_t)
+            tgs.tgs_render_full(scene_h, cam, **out_f)
+            mse = torch.mean((out_t["rgb"].clamp(0, 1) - out_f["rgb"].clamp(0, 1)) ** 2).item()
+            if mse > 0:
+                vals.append(-10.0 * math.log10(mse))
+        psnr = dict(mean_db=float(np.mean(vals)) if vals else None,
+                    min_db=float(np.min(vals)) if vals else None,
+                    frames_compared=len(vals), identical_frames=n_frames - len(vals))
+
+    n_tgs = sum(1 for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS)
+    sr_pct = [100.0 * i["n_selected"] / (TX * TY) for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS]
+
+    # roofline of the dominant kernel (largest summed time in the timed region)
+    stage_ms = {k: v["ms"] for k, v in prof.items()}
+    dom = max(("blend_ref", "blend_tgs"), key=lambda s: stage_ms[s])
+    launches = prof[dom]["launches"]
+    avg_s = stage_ms[dom] / launches * 1e-3
+    pairs_per_launch = counted[dom]["pairs"] / max(1, counted[dom]["launches"])
+    achieved = BLEND_OPS_PER_PAIR * pairs_per_launch / avg_s / 1e12
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("kernel_source_sha") == kernel_source_hash() and dom in tr.get("bytes_per_launch", {}):
+            traffic = tr["bytes_per_launch"][dom]
+    roofline = {"bound": "alu", "kernel": f"blend ({dom})", "achieved": round(achieved, 3),
+                "peak": round(VALU_PEAK_TOPS, 2), "unit": "Tlane-op/s",
+                "frac": round(achieved / VALU_PEAK_TOPS, 4), "traffic": traffic,
+                "avg_launch_ms": round(avg_s * 1e3, 4), "pairs_per_launch": int(pairs_per_launch),
+                "ops_per_pair": BLEND_OPS_PER_PAIR}
+
+    # CPU oracle on a bounded sample of the same workload
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        nf = min(args.cpu_frames, n_frames)
+        ora = O.TemporalOracle(wl.scene, W, H)
+        t0 = time.perf_counter()
+        for cam in cams[:nf]:
+            ora.render(cam)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(nf / dt, 5), "unit": "frames/s", "cores": 1, "kind": "oracle",
+               "sample": f"frames 0-{nf - 1} of the {n_frames}-frame temporal sequence "
+                         f"(1 true reference + {nf - 1} TemporalGS frames), single-threaded C "
+                         f"oracle, {dt:.1f} s on {os.cpu_count()} host cores"}
+        log(f"[bench] cpu oracle: {nf} frames in {dt:.1f}s")
+
+    per_frame = lambda s: round(stage_ms[s] / (args.steps * n_frames), 4)
+    res = {
+        "metric": METRIC, "value": round(fps_t, 2), "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * t_temporal / args.steps, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": synth.WORKLOADS.get(args.workload, args.workload),
+                   "frames_per_step": n_frames, "gaussians": n, "width": W, "height": H,
+                   "lambda_tdc": 50, "lambda_sr": 5, "eta": 0.4},
+        "temporal": {"fps": round(fps_t, 2), "ms_per_frame": round(1e3 * t_temporal / (args.steps * n_frames), 4),
+                     "ms_per_kind": {name: round(float(np.mean(v)), 4) if v else None
+                                     for name, v in zip(("true_ref", "pseudo_ref", "tgs"),
+                                                        (per_kind[0], per_kind[1], per_kind[2]))},
+                     "tgsf_pct": round(100.0 * n_tgs / n_frames, 2),
+                     "sr_tile_pct": round(float(np.mean(sr_pct)), 2) if sr_pct else None},
+        "full": {"fps": round(fps_f, 2), "ms_per_frame": round(1e3 * t_full / (args.steps * n_frames), 4)},
+        "speedup_temporal_vs_full": round(fps_t / fps_f, 3),
+        "psnr_temporal_vs_full": psnr,
+        "kernels_ms_per_frame": {s: per_frame(s) for s in tgs.PROF_STAGES if stage_ms[s] > 0},
+        "kernels_full_ms_per_frame": {s: round(v["ms"] / (args.steps * n_frames), 4)
+                                      for s, v in prof_full.items() if v["ms"] > 0},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    tgs.tgs_state_free(state_h)
+    tgs.tgs_scene_free(scene_h)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -206,6 +206,39 @@ enum {
 tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_t what,
                           void *host, size_t *nbytes);
 
+/* Kernel timing for benchmarking.  Between tgs_profile_start and
+ * tgs_profile_stop every launch of the library is bracketed by HIP events on
+ * the stream it is enqueued on; stop synchronises the device and returns, per
+ * stage, the summed event time and the number of launches.  With
+ * count_pairs != 0 the blend kernels also count the (pixel, Gaussian) pairs
+ * they evaluate (the blend's unit of work), which costs one add per pair.
+ * Process-wide, not thread-safe; renders must not overlap with start/stop. */
+enum {
+    TGS_PROF_PREPROCESS = 0,  /* per-Gaussian stage (incl. counter reset)     */
+    TGS_PROF_SCAN = 1,        /* key counts + exclusive scan                  */
+    TGS_PROF_READBACK = 2,    /* counter copy to the host (event-timed)       */
+    TGS_PROF_DUPLICATE = 3,
+    TGS_PROF_SORT = 4,        /* clear + histogram + all digit passes         */
+    TGS_PROF_RANGES = 5,
+    TGS_PROF_BLEND_FULL = 6,  /* tgs_render_full                              */
+    TGS_PROF_BLEND_REF = 7,   /* reference frames (with prior capture)        */
+    TGS_PROF_BLEND_TGS = 8,   /* selected tiles of TemporalGS frames          */
+    TGS_PROF_WARP = 9,        /* buffer init + forward warp                   */
+    TGS_PROF_FILL_QUERY = 10,
+    TGS_PROF_OCCLUDED = 11,
+    TGS_PROF_SELECT = 12,
+    TGS_PROF_STITCH = 13,
+    TGS_PROF_CAPTURE = 14,    /* adaptive frustum, flag/mask resets           */
+    TGS_PROF_STAGES = 16
+};
+typedef struct {
+    double ms[TGS_PROF_STAGES];
+    int64_t launches[TGS_PROF_STAGES];
+    int64_t pairs[TGS_PROF_STAGES];   /* blend stages only, if counted        */
+} tgs_profile;
+tgs_status tgs_profile_start(int32_t count_pairs);
+tgs_status tgs_profile_stop(tgs_profile *out);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *tgs_last_error(void);
 

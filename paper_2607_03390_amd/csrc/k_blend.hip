@@ -23,7 +23,7 @@ namespace tgs {
 
 namespace {
 
-template <bool CAPTURE, bool CONTRIB>
+template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     __shared__ float4 s_g0[256];
     __shared__ float4 s_g1[256];
@@ -43,6 +43,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
     bool pivot = false;
     bool done = !inside;
+    uint32_t evaluated = 0;
 
     for (uint32_t b = range.x; b < range.y; b += 256) {
         if (__syncthreads_count(done) == 256) break;
@@ -61,6 +62,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             bool inc = false;
             float w = 0.0f;
             if (!done) {
+                if (COUNT) ++evaluated;
                 const float4 g0 = s_g0[j];
                 const float4 g1 = s_g1[j];
                 const float dx = g0.x - fpx, dy = g0.y - fpy;
@@ -107,6 +109,12 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
         if (CAPTURE && a.g_flag && k < range.y && s_flag[tid]) a.g_flag[s_idx[tid]] = 1u;
     }
 
+    if (COUNT) {
+        unsigned long long e = evaluated;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) e += __shfl_xor(e, o);
+        if (lane == 0 && e) atomicAdd(a.pairs, e);
+    }
     if (!inside) return;
     const size_t HW = (size_t)a.W * a.H;
     const size_t q = (size_t)py * a.W + px;
@@ -170,16 +178,24 @@ __global__ __launch_bounds__(256) void afc_bounds_kernel(int n, const uint8_t *g
 
 }  // namespace
 
+template <bool CAPTURE, bool CONTRIB>
+void launch_blend_v(const BlendArgs &a, int n_blocks, hipStream_t st) {
+    if (a.pairs)
+        blend_kernel<CAPTURE, CONTRIB, true><<<n_blocks, 256, 0, st>>>(a);
+    else
+        blend_kernel<CAPTURE, CONTRIB, false><<<n_blocks, 256, 0, st>>>(a);
+}
+
 void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st) {
     if (n_blocks <= 0) return;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma || a.g_flag ||
                          a.contrib;
     if (a.contrib)
-        blend_kernel<true, true><<<n_blocks, 256, 0, st>>>(a);
+        launch_blend_v<true, true>(a, n_blocks, st);
     else if (capture)
-        blend_kernel<true, false><<<n_blocks, 256, 0, st>>>(a);
+        launch_blend_v<true, false>(a, n_blocks, st);
     else
-        blend_kernel<false, false><<<n_blocks, 256, 0, st>>>(a);
+        launch_blend_v<false, false>(a, n_blocks, st);
 }
 
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,

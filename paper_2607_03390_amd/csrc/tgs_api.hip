@@ -227,6 +227,48 @@ void relative_pose(const float *ref, const float *cur, float *M, float *Minv) {
     mul(a, binv, Minv);
 }
 
+
+// Event timing of every launch while profiling is on (tgs_profile_start/stop).
+struct Profiler {
+    bool on = false, count = false;
+    std::vector<hipEvent_t> pool;
+    size_t used = 0;
+    struct Rec {
+        int stage;
+        hipEvent_t a, b;
+    };
+    std::vector<Rec> recs;
+    unsigned long long *d_pairs = nullptr;
+
+    hipEvent_t event() {
+        if (used == pool.size()) {
+            hipEvent_t e = nullptr;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            pool.push_back(e);
+        }
+        return pool[used++];
+    }
+    unsigned long long *pairs(int stage) { return on && count ? d_pairs + stage : nullptr; }
+};
+Profiler g_prof;
+
+// Brackets the launches of one stage with events on their stream.
+struct ProfScope {
+    int stage;
+    hipStream_t st;
+    hipEvent_t a = nullptr;
+    ProfScope(int stage_, hipStream_t st_) : stage(stage_), st(st_) {
+        if (g_prof.on && (a = g_prof.event()) != nullptr) (void)hipEventRecord(a, st);
+    }
+    ~ProfScope() {
+        if (!a) return;
+        hipEvent_t b = g_prof.event();
+        if (!b) return;
+        (void)hipEventRecord(b, st);
+        g_prof.recs.push_back({stage, a, b});
+    }
+};
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -266,6 +308,7 @@ struct FrameResult {
 // Zero the counters and run the per-Gaussian stage.
 tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
                            hipStream_t st) {
+    ProfScope ps(TGS_PROF_PREPROCESS, st);
     launch_fill_i32(ws.cnt.as<int>(), sizeof(Counters) / sizeof(int), 0, st);
     launch_preprocess(sc->view, cam, cull, ws.records(), ws.cnt.as<Counters>(), st);
     TGS_LAUNCHED("preprocess");
@@ -275,10 +318,16 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
 // Scan the key counts and read the counters back (the one sync of a frame).
 tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
                           FrameResult &fr) {
-    launch_scan(n, ws.rect.as<ushort4>(), rowpre, TX, ws.offsets.as<uint32_t>(),
-                ws.scan.as<uint32_t>(), ws.cnt.as<Counters>(), st);
-    TGS_LAUNCHED("scan");
-    TGS_HIP(hipMemcpyAsync(ws.host_cnt, ws.cnt.p, sizeof(Counters), hipMemcpyDeviceToHost, st));
+    {
+        ProfScope ps(TGS_PROF_SCAN, st);
+        launch_scan(n, ws.rect.as<ushort4>(), rowpre, TX, ws.offsets.as<uint32_t>(),
+                    ws.scan.as<uint32_t>(), ws.cnt.as<Counters>(), st);
+        TGS_LAUNCHED("scan");
+    }
+    {
+        ProfScope ps(TGS_PROF_READBACK, st);
+        TGS_HIP(hipMemcpyAsync(ws.host_cnt, ws.cnt.p, sizeof(Counters), hipMemcpyDeviceToHost, st));
+    }
     TGS_HIP(hipStreamSynchronize(st));
     fr.K = ws.host_cnt->n_keys;
     fr.n_surv = ws.host_cnt->n_survivors;
@@ -295,16 +344,26 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint8_t *sel, u
                      hipStream_t st, const uint32_t **sorted_vals) {
     const int passes = sort_passes(TX * TY);
     TGS_TRY(ws.ensure_keys(K, passes));
-    launch_duplicate(n, ws.rect.as<ushort4>(), ws.g1.as<float4>(), ws.offsets.as<uint32_t>(), sel,
-                     TX, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(), st);
-    TGS_LAUNCHED("duplicate");
-    const int alt = launch_sort(K, passes, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(),
-                                ws.keys_alt.as<uint64_t>(), ws.vals_alt.as<uint32_t>(),
-                                ws.sort.as<uint32_t>(), st);
-    TGS_LAUNCHED("sort");
+    {
+        ProfScope ps(TGS_PROF_DUPLICATE, st);
+        launch_duplicate(n, ws.rect.as<ushort4>(), ws.g1.as<float4>(), ws.offsets.as<uint32_t>(),
+                         sel, TX, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(), st);
+        TGS_LAUNCHED("duplicate");
+    }
+    int alt = 0;
+    {
+        ProfScope ps(TGS_PROF_SORT, st);
+        alt = launch_sort(K, passes, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(),
+                          ws.keys_alt.as<uint64_t>(), ws.vals_alt.as<uint32_t>(),
+                          ws.sort.as<uint32_t>(), st);
+        TGS_LAUNCHED("sort");
+    }
     const uint64_t *skeys = alt ? ws.keys_alt.as<uint64_t>() : ws.keys.as<uint64_t>();
-    launch_ranges(K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
-    TGS_LAUNCHED("ranges");
+    {
+        ProfScope ps(TGS_PROF_RANGES, st);
+        launch_ranges(K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
+        TGS_LAUNCHED("ranges");
+    }
     *sorted_vals = alt ? ws.vals_alt.as<uint32_t>() : ws.vals.as<uint32_t>();
     ws.last_K = K;
     ws.last_alt = alt;
@@ -355,6 +414,40 @@ tgs_status check_params(const tgs_params *p) {
 extern "C" {
 
 const char *tgs_last_error(void) { return g_err.c_str(); }
+
+tgs_status tgs_profile_start(int32_t count_pairs) {
+    g_err.clear();
+    if (!g_prof.d_pairs)
+        TGS_HIP(hipMalloc((void **)&g_prof.d_pairs, TGS_PROF_STAGES * sizeof(unsigned long long)));
+    TGS_HIP(hipDeviceSynchronize());
+    TGS_HIP(hipMemset(g_prof.d_pairs, 0, TGS_PROF_STAGES * sizeof(unsigned long long)));
+    g_prof.used = 0;
+    g_prof.recs.clear();
+    g_prof.count = count_pairs != 0;
+    g_prof.on = true;
+    return TGS_OK;
+}
+
+tgs_status tgs_profile_stop(tgs_profile *out) {
+    g_err.clear();
+    if (!g_prof.on) return fail(TGS_ERR_INVALID_ARG, "profiling was not started");
+    g_prof.on = false;
+    TGS_HIP(hipDeviceSynchronize());
+    tgs_profile r{};
+    for (const auto &rec : g_prof.recs) {
+        float ms = 0.0f;
+        TGS_HIP(hipEventElapsedTime(&ms, rec.a, rec.b));
+        r.ms[rec.stage] += ms;
+        r.launches[rec.stage] += 1;
+    }
+    unsigned long long pairs[TGS_PROF_STAGES];
+    TGS_HIP(hipMemcpy(pairs, g_prof.d_pairs, sizeof(pairs), hipMemcpyDeviceToHost));
+    for (int k = 0; k < TGS_PROF_STAGES; ++k) r.pairs[k] = g_prof.count ? (int64_t)pairs[k] : 0;
+    g_prof.recs.clear();
+    g_prof.used = 0;
+    if (out) *out = r;
+    return TGS_OK;
+}
 
 void tgs_params_default(tgs_params *p) {
     if (!p) return;
@@ -476,8 +569,12 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     a.sigma = out->sigma;
     a.alpha = out->alpha;
     a.contrib = out->contrib;
-    launch_blend(a, TX * TY, st);
-    TGS_LAUNCHED("blend");
+    a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
+    {
+        ProfScope ps(TGS_PROF_BLEND_FULL, st);
+        launch_blend(a, TX * TY, st);
+        TGS_LAUNCHED("blend");
+    }
     if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)TX * TY, 1, st);
     TGS_LAUNCHED("tile mask");
     sc->last_W = W;
@@ -579,13 +676,20 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         w.H = H;
         w.TX = TX;
         w.TY = TY;
-        launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
-                             s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
-        launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
-                            s->smax.as<float>(), st);
-        launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
-                          s->um.as<uint8_t>(), st);
-        TGS_LAUNCHED("warp");
+        {
+            ProfScope ps(TGS_PROF_WARP, st);
+            launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
+                                 s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
+            launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
+                                s->smax.as<float>(), st);
+            TGS_LAUNCHED("warp");
+        }
+        {
+            ProfScope ps(TGS_PROF_FILL_QUERY, st);
+            launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
+                              s->um.as<uint8_t>(), st);
+            TGS_LAUNCHED("fill query");
+        }
         CullK cull = no_cull(p.z_near, ws);
         cull.afc = p.enable_afc;
         cull.fbox = s->fbox.as<int>();
@@ -596,27 +700,45 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         cull.lambda1 = p.lambda1;
         cull.lambda2 = p.lambda2;
         TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
-        launch_occluded(w, ws.newly.as<int>(), ws.cnt.as<Counters>(), ws.g0.as<float4>(),
-                        ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
+        {
+            ProfScope ps(TGS_PROF_OCCLUDED, st);
+            launch_occluded(w, ws.newly.as<int>(), ws.cnt.as<Counters>(), ws.g0.as<float4>(),
+                            ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
+            TGS_LAUNCHED("occluded tiles");
+        }
         const int mode = (!p.enable_sr || p.force_all_dirty) ? 1 : 0;
-        launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(), ws.sel.as<uint8_t>(),
-                      ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(), out->tile_mask,
-                      ws.cnt.as<Counters>(), st);
-        TGS_LAUNCHED("tile selection");
+        {
+            ProfScope ps(TGS_PROF_SELECT, st);
+            launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(),
+                          ws.sel.as<uint8_t>(), ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(),
+                          out->tile_mask, ws.cnt.as<Counters>(), st);
+            TGS_LAUNCHED("tile selection");
+        }
         TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr));
         TGS_TRY(step_keys(ws, sc->n, TX, TY, ws.sel.as<uint8_t>(), fr.K, st, &vals));
         BlendArgs a = blend_args(ws, W, H, vals);
         a.tile_list = ws.sel_list.as<int>();
         a.rgb = out->rgb;
-        launch_blend(a, (int)fr.n_sel, st);
-        TGS_LAUNCHED("blend");
-        launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(), out->rgb, st);
-        TGS_LAUNCHED("stitch");
+        a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
+        {
+            ProfScope ps(TGS_PROF_BLEND_TGS, st);
+            launch_blend(a, (int)fr.n_sel, st);
+            TGS_LAUNCHED("blend");
+        }
+        {
+            ProfScope ps(TGS_PROF_STITCH, st);
+            launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
+                          out->rgb, st);
+            TGS_LAUNCHED("stitch");
+        }
     } else {
         CullK cull = no_cull(p.z_near, ws);
         cull.afc = (kind == TGS_FRAME_PSEUDO_REF && p.enable_afc) ? 1 : 0;
         cull.fbox = s->fbox.as<int>();
-        launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
+        {
+            ProfScope ps(TGS_PROF_CAPTURE, st);
+            launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
+        }
         TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
         TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr));
         TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, fr.K, st, &vals));
@@ -631,16 +753,23 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         a.tgb_sigma = s->tgb_s.as<float>();
         a.g_flag = s->g_flag.as<uint8_t>();
         a.contrib = out->contrib;
-        launch_blend(a, nt, st);
-        TGS_LAUNCHED("blend");
-        if (kind == TGS_FRAME_TRUE_REF) {
-            launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
-                              s->fbox.as<int>(), st);
-            TGS_LAUNCHED("adaptive frustum");
+        a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
+        {
+            ProfScope ps(TGS_PROF_BLEND_REF, st);
+            launch_blend(a, nt, st);
+            TGS_LAUNCHED("blend");
         }
-        if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
-        launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
-        TGS_LAUNCHED("tile mask");
+        {
+            ProfScope ps(TGS_PROF_CAPTURE, st);
+            if (kind == TGS_FRAME_TRUE_REF) {
+                launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
+                                  s->fbox.as<int>(), st);
+                TGS_LAUNCHED("adaptive frustum");
+            }
+            if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
+            launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
+            TGS_LAUNCHED("tile mask");
+        }
         memcpy(s->ref_w2c, cam->world_to_cam, sizeof(s->ref_w2c));
         s->ref_intr[0] = cam->fx;
         s->ref_intr[1] = cam->fy;

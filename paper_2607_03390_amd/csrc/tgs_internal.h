@@ -104,6 +104,7 @@ struct BlendArgs {
     float *tgb_depth, *tgb_sigma;       // optional second copies
     uint8_t *g_flag;          // optional: Gaussian composited somewhere
     float *contrib;           // optional: max weight per Gaussian
+    unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
 };
 void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st);
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,

@@ -26,7 +26,11 @@ TGS_FRAME_TRUE_REF, TGS_FRAME_PSEUDO_REF, TGS_FRAME_TGS, TGS_FRAME_FULL = range(
 EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_scene_count",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
-            "tgs_last_error"]
+            "tgs_profile_start", "tgs_profile_stop", "tgs_last_error"]
+
+PROF_STAGES = ["preprocess", "scan", "readback", "duplicate", "sort", "ranges", "blend_full",
+               "blend_ref", "blend_tgs", "warp", "fill_query", "occluded", "select", "stitch",
+               "capture"]
 
 
 class TgsError(RuntimeError):
@@ -58,6 +62,10 @@ class tgs_frame_out(C.Structure):
                 ("alpha", C.c_void_p), ("contrib", C.c_void_p), ("tile_mask", C.c_void_p),
                 ("frame_kind", C.c_int32), ("n_selected", C.c_int32), ("n_survivors", C.c_int32),
                 ("n_newly_visible", C.c_int32), ("n_keys", C.c_int64)]
+
+
+class tgs_profile(C.Structure):
+    _fields_ = [("ms", C.c_double * 16), ("launches", C.c_int64 * 16), ("pairs", C.c_int64 * 16)]
 
 
 class tgs_state_header(C.Structure):
@@ -92,6 +100,8 @@ def lib():
         L.tgs_state_export.argtypes = [vp, vp, C.POINTER(sz)]
         L.tgs_state_import.argtypes = [vp, vp, sz]
         L.tgs_debug_dump.argtypes = [vp, vp, i32, vp, C.POINTER(sz)]
+        L.tgs_profile_start.argtypes = [i32]
+        L.tgs_profile_stop.argtypes = [C.POINTER(tgs_profile)]
         for name in EXPORTED:
             if name not in ("tgs_last_error", "tgs_params_default", "tgs_scene_free",
                             "tgs_state_free", "tgs_scene_count"):
@@ -246,6 +256,18 @@ def tgs_debug_dump(scene_h, state_h, what) -> np.ndarray:
     out = np.zeros(n.value, np.uint8)
     _check(lib().tgs_debug_dump(scene_h, state_h, int(what), out.ctypes.data, C.byref(n)))
     return out.view(_DUMP_DTYPE[what])
+
+
+def tgs_profile_start(count_pairs=False):
+    _check(lib().tgs_profile_start(1 if count_pairs else 0))
+
+
+def tgs_profile_stop():
+    """Per stage: summed event ms, launches, counted pairs."""
+    p = tgs_profile()
+    _check(lib().tgs_profile_stop(C.byref(p)))
+    return {name: dict(ms=p.ms[k], launches=p.launches[k], pairs=p.pairs[k])
+            for k, name in enumerate(PROF_STAGES)}
 
 
 def alloc_frame(width, height, n=0, depth=False, contrib=False, tile_mask=False, device="cuda"):

@@ -46,6 +46,7 @@ def test_struct_layouts_match_header():
     assert C.sizeof(tgs.tgs_frame_out) == 6 * 8 + 4 * 4 + 8
     assert C.sizeof(tgs.tgs_scene_desc) == 8 + 5 * 8
     assert C.sizeof(tgs.tgs_state_header) == 9 * 4 + 4 * 4 + 16 * 4 + 4 * 4
+    assert C.sizeof(tgs.tgs_profile) == 16 * 8 * 3
 
 
 def test_params_default_are_the_papers():

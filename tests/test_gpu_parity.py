@@ -275,3 +275,19 @@ def test_full_size_room_frame():
     _full_parity(sc, cams[:1], sample_tiles=sample, label="room 1.5M")
     _temporal_parity(sc, cams[:2], 1920, 1080, "room 1.5M")
     torch.cuda.synchronize()
+
+
+def test_pair_count_matches_oracle():
+    """The blend's evaluated (pixel, Gaussian) pairs, the unit of the blend
+    roofline, equal the oracle's count up to margin pixels."""
+    w = synth.workload("tiny", n_frames=2)
+    with Uploaded(w.scene) as h:
+        for cam in w.cameras:
+            tgs.tgs_profile_start(count_pairs=True)
+            gpu_full(h, cam, w.scene.n, depth=False, contrib=False)
+            prof = tgs.tgs_profile_stop()
+            r = O.render_full(w.scene, cam)
+            got = prof["blend_full"]["pairs"]
+            log(f"    pairs gpu {got} oracle {r['pairs']}")
+            assert prof["blend_full"]["launches"] == 1
+            assert abs(got - r["pairs"]) <= 1e-3 * r["pairs"]
