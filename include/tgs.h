@@ -190,7 +190,7 @@ tgs_status tgs_state_import(tgs_state *state, const void *host, size_t nbytes);
  * memory (synchronous).  host == NULL queries the size into *nbytes. */
 enum {
     TGS_DUMP_SORTED_VALUES = 0,  /* uint32 [n_keys] Gaussian index per sorted key   */
-    TGS_DUMP_SORTED_KEYS = 1,    /* uint64 [n_keys] (tile << 32) | depth bits        */
+    TGS_DUMP_SORTED_KEYS = 1,    /* uint32 [n_keys] tile id per sorted entry         */
     TGS_DUMP_TILE_RANGES = 2,    /* uint32 [TX*TY][2] start, end into the sorted keys */
     TGS_DUMP_RECORDS = 3,        /* float [n][12]: u, v, conic a, b | conic c, opacity, depth, 0 | r, g, b, 0 */
     TGS_DUMP_RECTS = 4,          /* uint16 [n][4] tile rectangle x0,y0,x1,y1 (x0 > x1: none) */

@@ -25,6 +25,10 @@ namespace {
 
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
+    // Per staged Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
+    // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares)
+    // so that log2 of the Gaussian falloff is a three-FMA quadratic form and
+    // the opacity is one v_exp_f32.
     __shared__ float4 s_g0[256];
     __shared__ float4 s_g1[256];
     __shared__ float4 s_col[256];
@@ -38,6 +42,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     const bool inside = px < a.W && py < a.H;
     const float fpx = (float)px, fpy = (float)py;
     const uint2 range = a.ranges[tile];
+    constexpr float kLog2e = 1.4426950408889634f;
 
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
@@ -50,49 +55,45 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
         const uint32_t k = b + tid;
         if (k < range.y) {
             const int idx = (int)a.vals[k];
+            const float4 g0 = a.g0[idx];
+            const float4 g1 = a.g1[idx];
             s_idx[tid] = idx;
-            s_g0[tid] = a.g0[idx];
-            s_g1[tid] = a.g1[idx];
+            s_g0[tid] = make_float4(g0.x, g0.y, -0.5f * kLog2e * g0.z, -kLog2e * g0.w);
+            s_g1[tid] = make_float4(-0.5f * kLog2e * g1.x, g1.y, g1.z, 0.0f);
             s_col[tid] = a.col[idx];
         }
         if (CAPTURE) s_flag[tid] = 0u;
         __syncthreads();
         const int cnt = (int)min(256u, range.y - b);
         for (int j = 0; j < cnt; ++j) {
-            bool inc = false;
-            float w = 0.0f;
-            if (!done) {
-                if (COUNT) ++evaluated;
-                const float4 g0 = s_g0[j];
-                const float4 g1 = s_g1[j];
-                const float dx = g0.x - fpx, dy = g0.y - fpy;
-                const float power = -0.5f * (g0.z * dx * dx + g1.x * dy * dy) - g0.w * dx * dy;
-                if (!(power > 0.0f)) {
-                    const float alpha = fminf(kAlphaMax, g1.y * __expf(power));
-                    if (!(alpha < kAlphaMin)) {
-                        const float Tn = T * (1.0f - alpha);
-                        if (Tn < kTMin) {
-                            done = true;
-                        } else {
-                            w = alpha * T;
-                            const float4 c = s_col[j];
-                            cr = __builtin_fmaf(w, c.x, cr);
-                            cg = __builtin_fmaf(w, c.y, cg);
-                            cb = __builtin_fmaf(w, c.z, cb);
-                            if (CAPTURE) {
-                                if (!pivot) { d0 = g1.z; pivot = true; }
-                                const float dd = g1.z - d0;
-                                sw += w;
-                                s1 = __builtin_fmaf(w, dd, s1);
-                                s2 = __builtin_fmaf(w * dd, dd, s2);
-                            }
-                            T = Tn;
-                            inc = true;
-                        }
-                    }
-                }
-            }
+            if (__all(done)) break;
+            if (COUNT) evaluated += done ? 0u : 1u;
+            const float4 g0 = s_g0[j];
+            const float4 g1 = s_g1[j];
+            const float dx = g0.x - fpx, dy = g0.y - fpy;
+            // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
+            const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
+            const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
+            const bool hit = !done && !(p2 > 0.0f) && !(alpha < kAlphaMin);
+            if (!__any(hit)) continue;
+            const float Tn = T * (1.0f - alpha);
+            const bool stop = hit && Tn < kTMin;
+            const bool inc = hit && !stop;
+            const float w = inc ? alpha * T : 0.0f;
+            const float4 c = s_col[j];
+            cr = __builtin_fmaf(w, c.x, cr);
+            cg = __builtin_fmaf(w, c.y, cg);
+            cb = __builtin_fmaf(w, c.z, cb);
+            T = inc ? Tn : T;
+            done = done || stop;
             if (CAPTURE) {
+                const float dep = g1.z;
+                d0 = (inc && !pivot) ? dep : d0;
+                pivot = pivot || inc;
+                const float dd = dep - d0;
+                sw += w;
+                s1 = __builtin_fmaf(w, dd, s1);
+                s2 = __builtin_fmaf(w * dd, dd, s2);
                 const uint64_t m = __ballot(inc);
                 if (m != 0ull && lane == 0) s_flag[j] = 1u;
                 if (CONTRIB && m != 0ull) {
@@ -141,39 +142,66 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     }
 }
 
-__global__ __launch_bounds__(64) void afc_init_kernel(int *fbox) {
-    if (threadIdx.x < 4) {
-        const float v = threadIdx.x < 2 ? __builtin_inff() : -__builtin_inff();
-        fbox[threadIdx.x] = float_to_ordered(v);
-    }
-}
+// Adaptive frustum (Sec. III-D): min / max NDC of the projected means of the
+// temporal Gaussian buffer.  Two levels: a fixed grid of blocks reduces
+// grid-strided slices into partials, one block reduces the partials (no
+// contended atomics; min / max are exact, so the result is deterministic).
+constexpr int kAfcBlocks = kAfcPartials;
 
-__global__ __launch_bounds__(256) void afc_bounds_kernel(int n, const uint8_t *g_flag,
-                                                         const float4 *g0, int W, int H,
-                                                         int *fbox) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    int mnx = float_to_ordered(__builtin_inff()), mny = mnx;
-    int mxx = float_to_ordered(-__builtin_inff()), mxy = mxx;
-    if (i < n && g_flag[i]) {
+__global__ __launch_bounds__(256) void afc_partial_kernel(int n, const uint8_t *g_flag,
+                                                          const float4 *g0, int W, int H,
+                                                          int *partial) {
+    __shared__ int s_red[4][4];
+    int v[4] = {float_to_ordered(__builtin_inff()), float_to_ordered(__builtin_inff()),
+                float_to_ordered(-__builtin_inff()), float_to_ordered(-__builtin_inff())};
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        if (!g_flag[i]) continue;
         const float4 r = g0[i];
-        const float nx = (2.0f * r.x + 1.0f) / (float)W - 1.0f;
-        const float ny = (2.0f * r.y + 1.0f) / (float)H - 1.0f;
-        mnx = mxx = float_to_ordered(nx);
-        mny = mxy = float_to_ordered(ny);
+        const int nx = float_to_ordered((2.0f * r.x + 1.0f) / (float)W - 1.0f);
+        const int ny = float_to_ordered((2.0f * r.y + 1.0f) / (float)H - 1.0f);
+        v[0] = min(v[0], nx);
+        v[1] = min(v[1], ny);
+        v[2] = max(v[2], nx);
+        v[3] = max(v[3], ny);
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
-        mnx = min(mnx, __shfl_xor(mnx, o));
-        mny = min(mny, __shfl_xor(mny, o));
-        mxx = max(mxx, __shfl_xor(mxx, o));
-        mxy = max(mxy, __shfl_xor(mxy, o));
+        v[0] = min(v[0], __shfl_xor(v[0], o));
+        v[1] = min(v[1], __shfl_xor(v[1], o));
+        v[2] = max(v[2], __shfl_xor(v[2], o));
+        v[3] = max(v[3], __shfl_xor(v[3], o));
     }
-    if ((threadIdx.x & 63) == 0) {
-        atomicMin(&fbox[0], mnx);
-        atomicMin(&fbox[1], mny);
-        atomicMax(&fbox[2], mxx);
-        atomicMax(&fbox[3], mxy);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0)
+        for (int k = 0; k < 4; ++k) s_red[wave][k] = v[k];
+    __syncthreads();
+    if (threadIdx.x < 4) {
+        const int k = threadIdx.x;
+        int r = s_red[0][k];
+        for (int w = 1; w < 4; ++w) r = k < 2 ? min(r, s_red[w][k]) : max(r, s_red[w][k]);
+        partial[blockIdx.x * 4 + k] = r;
     }
+}
+
+__global__ __launch_bounds__(64) void afc_final_kernel(const int *partial, int n_partial,
+                                                       int *fbox) {
+    int v[4] = {float_to_ordered(__builtin_inff()), float_to_ordered(__builtin_inff()),
+                float_to_ordered(-__builtin_inff()), float_to_ordered(-__builtin_inff())};
+    for (int b = threadIdx.x; b < n_partial; b += 64) {
+        v[0] = min(v[0], partial[b * 4 + 0]);
+        v[1] = min(v[1], partial[b * 4 + 1]);
+        v[2] = max(v[2], partial[b * 4 + 2]);
+        v[3] = max(v[3], partial[b * 4 + 3]);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        v[0] = min(v[0], __shfl_xor(v[0], o));
+        v[1] = min(v[1], __shfl_xor(v[1], o));
+        v[2] = max(v[2], __shfl_xor(v[2], o));
+        v[3] = max(v[3], __shfl_xor(v[3], o));
+    }
+    if (threadIdx.x == 0)
+        for (int k = 0; k < 4; ++k) fbox[k] = v[k];
 }
 
 }  // namespace
@@ -200,8 +228,10 @@ void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st) {
 
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
                        hipStream_t st) {
-    afc_init_kernel<<<1, 64, 0, st>>>(fbox);
-    if (n > 0) afc_bounds_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, g_flag, g0, W, H, fbox);
+    // fbox[0..3] is the result; fbox[4..] holds kAfcBlocks x 4 partials
+    int *partial = fbox + 4;
+    afc_partial_kernel<<<kAfcBlocks, 256, 0, st>>>(n, g_flag, g0, W, H, partial);
+    afc_final_kernel<<<1, 64, 0, st>>>(partial, kAfcBlocks, fbox);
 }
 
 }  // namespace tgs

@@ -2,10 +2,11 @@
 // temporal dynamic culling of Sec. III-D and the newly-visible test of the
 // occluded-tile detection (Sec. III-E) folded in.
 //
-// One thread per Gaussian over the structure-of-arrays scene: every load is a
-// coalesced 256-byte wave access, and the SH coefficients (192 of the 236
-// bytes per Gaussian at degree 3) are read only by survivors.  The kernel is
-// HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
+// One thread per Gaussian.  The scene is stored as 16-byte attribute groups
+// and wave-tiled SH blocks, so every wave load is one contiguous 1 KB request;
+// only the mean (16 bytes) is read for a culled Gaussian, and the SH
+// coefficients (192 of the 240 bytes per Gaussian at degree 3) only for
+// survivors that touch a tile.  The kernel is HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
 // and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.
@@ -19,6 +20,7 @@ template <int DEG>
 __device__ inline void sh_colour(const SceneDev &s, int i, float dx, float dy, float dz,
                                  float &r, float &g, float &b) {
     constexpr int K = (DEG + 1) * (DEG + 1);
+    constexpr int SLOTS = (3 * K + 3) / 4;
     float basis[K];
     basis[0] = 0.28209479177387814f;
     if constexpr (DEG >= 1) {
@@ -46,14 +48,22 @@ __device__ inline void sh_colour(const SceneDev &s, int i, float dx, float dy, f
             }
         }
     }
+    float f[4 * SLOTS];
+    const float4 *p = s.sh + (size_t)(i >> 6) * SLOTS * 64 + (i & 63);
+#pragma unroll
+    for (int j = 0; j < SLOTS; ++j) {
+        const float4 v = p[j * 64];
+        f[4 * j + 0] = v.x;
+        f[4 * j + 1] = v.y;
+        f[4 * j + 2] = v.z;
+        f[4 * j + 3] = v.w;
+    }
     float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f;
-    const size_t n = (size_t)s.n;
-    const float *p = s.sh + i;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-        acc0 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 0) * n], acc0);
-        acc1 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 1) * n], acc1);
-        acc2 = __builtin_fmaf(basis[k], p[(size_t)(3 * k + 2) * n], acc2);
+        acc0 = __builtin_fmaf(basis[k], f[3 * k + 0], acc0);
+        acc1 = __builtin_fmaf(basis[k], f[3 * k + 1], acc1);
+        acc2 = __builtin_fmaf(basis[k], f[3 * k + 2], acc2);
     }
     r = fmaxf(acc0 + 0.5f, 0.0f);
     g = fmaxf(acc1 + 0.5f, 0.0f);
@@ -66,9 +76,11 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     bool survivor = false, newly = false;
     ushort4 rect = make_ushort4(1, 1, 0, 0);
+    uint32_t keys = 0;
 
     if (i < s.n) {
-        const float mx = s.mx[i], my = s.my[i], mz = s.mz[i];
+        const float4 mo = s.mean_op[i];
+        const float mx = mo.x, my = mo.y, mz = mo.z;
         const float *V = cam.V;
         const float tx = ((V[0] * mx + V[1] * my) + V[2] * mz) + V[3];
         const float ty = ((V[4] * mx + V[5] * my) + V[6] * mz) + V[7];
@@ -98,7 +110,9 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
         survivor = alive;
         if (alive) {
             // 3D covariance R S S^T R^T from the normalised quaternion
-            const float q0 = s.qw[i], q1 = s.qx[i], q2 = s.qy[i], q3 = s.qz[i];
+            const float4 sq = s.scale_qw[i];
+            const float4 qv = s.qxyz[i];
+            const float q0 = sq.w, q1 = qv.x, q2 = qv.y, q3 = qv.z;
             const float qn = sqrtf(((q0 * q0 + q1 * q1) + q2 * q2) + q3 * q3);
             const float r = q0 / qn, x = q1 / qn, y = q2 / qn, z = q3 / qn;
             float R[9];
@@ -111,7 +125,7 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
             R[6] = 2.0f * (x * z - r * y);
             R[7] = 2.0f * (y * z + r * x);
             R[8] = 1.0f - 2.0f * (x * x + y * y);
-            const float sc[3] = {s.sx[i], s.sy[i], s.sz[i]};
+            const float sc[3] = {sq.x, sq.y, sq.z};
             float M[9];
 #pragma unroll
             for (int a = 0; a < 3; ++a)
@@ -157,16 +171,18 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
                 if (x0 <= x1 && y0 <= y1) {
                     rect = make_ushort4((unsigned short)x0, (unsigned short)y0,
                                         (unsigned short)x1, (unsigned short)y1);
+                    keys = (uint32_t)(rect.z - rect.x + 1) * (uint32_t)(rect.w - rect.y + 1);
                     float cr, cg, cbl;
                     sh_colour<DEG>(s, i, mx - cam.campos[0], my - cam.campos[1],
                                    mz - cam.campos[2], cr, cg, cbl);
                     rec.g0[i] = make_float4(u, v, cc * dinv, -cb * dinv);
-                    rec.g1[i] = make_float4(ca * dinv, s.opac[i], tz, 0.0f);
+                    rec.g1[i] = make_float4(ca * dinv, mo.w, tz, 0.0f);
                     rec.col[i] = make_float4(cr, cg, cbl, 0.0f);
                 }
             }
         }
         rec.rect[i] = rect;
+        rec.count[i] = keys;
         rec.status[i] = (uint8_t)((survivor ? 1 : 0) | (newly ? 2 : 0));
     }
 

@@ -1,16 +1,23 @@
-// Per-tile depth sort (Sec. III-A) as one LSD radix sort of the 64-bit keys
-// (tile << 32) | depth bits, 8-bit digits, only over the significant bits
-// (32 depth bits + ceil(log2 tiles) tile bits).
+// LSD radix sort of (uint32 key, uint32 value) pairs, 8-bit digits, for the
+// two sorts of a frame (Sec. III-A, per-tile depth order):
+//  1. the visible Gaussians by depth (float bits of a positive depth are
+//     ordered like the depths), input in Gaussian index order;
+//  2. the Gaussian-tile keys by tile id, input in depth order.
+// Both sorts are stable, so each tile's list ends up ordered by
+// (depth bits, Gaussian index): deterministic and identical to a direct sort
+// of the 64-bit (tile, depth) keys, at a third of the HBM traffic (the depth
+// passes run over the Gaussians, not over their tile copies).
 //
 // Onesweep structure for gfx950: one histogram kernel counts every pass's
-// digits at once, then one kernel per pass ranks a 3840-key partition in LDS
+// digits at once; then one kernel per pass ranks a 3840-key partition in LDS
 // and resolves its global digit offsets by decoupled look-back over the
 // preceding partitions.  Partitions are numbered by an atomic ticket taken on
-// entry, so a block only ever waits on partitions that are already running.
+// entry, so a block only waits on partitions that are already running.
 // Ranking is stable (a wave's 64-lane match over the digit bits plus per-wave
-// digit counters in input order), so equal depths keep Gaussian index order:
-// the sort is deterministic.  Keys are staged in LDS in digit order before
-// the global scatter so that writes of one digit run are contiguous.
+// digit counters in input order).  Keys are staged in LDS in digit order
+// before the scatter so that writes of one digit run are contiguous.
+// The key count may live on the device (grid sized for an upper bound;
+// partitions past the count leave at once), so no host round trip is needed.
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -22,16 +29,20 @@ constexpr int kSortIpt = 15;
 constexpr int kSortWaveItems = 64 * kSortIpt;
 constexpr int kSortTile = kSortThreads * kSortIpt;   // 3840 keys per partition
 constexpr int kRadix = 256;
-constexpr int kMaxPasses = 8;
+constexpr int kMaxPasses = 4;
 constexpr uint32_t kFlagAgg = 1u << 30;
 constexpr uint32_t kFlagInc = 2u << 30;
 constexpr uint32_t kValMask = (1u << 30) - 1;
 
-__device__ inline uint32_t ld_acquire(const uint32_t *p) {
+__device__ inline uint32_t ld_agent(const uint32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline void st_release(uint32_t *p, uint32_t v) {
+__device__ inline void st_agent(uint32_t *p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint32_t key_count(const uint32_t *n_dev, uint32_t n_host) {
+    return n_dev ? *n_dev : n_host;
 }
 
 __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave) {
@@ -58,17 +69,18 @@ __global__ __launch_bounds__(256) void sort_clear_kernel(uint32_t *p, size_t n) 
         p[k] = 0u;
 }
 
-__global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *keys, uint32_t K,
-                                                        int passes, uint32_t *hist) {
+__global__ __launch_bounds__(256) void sort_hist_kernel(const uint32_t *keys, const uint32_t *n_dev,
+                                                        uint32_t n_host, int begin_bit, int passes,
+                                                        uint32_t *hist) {
     __shared__ uint32_t s_h[4][kMaxPasses * kRadix];
     const int wave = threadIdx.x >> 6;
-    for (int k = threadIdx.x; k < 4 * kMaxPasses * kRadix; k += blockDim.x)
-        (&s_h[0][0])[k] = 0u;
+    for (int k = threadIdx.x; k < 4 * kMaxPasses * kRadix; k += blockDim.x) (&s_h[0][0])[k] = 0u;
     __syncthreads();
+    const uint32_t K = key_count(n_dev, n_host);
     for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
-        const uint64_t key = keys[k];
+        const uint32_t key = keys[k];
         for (int p = 0; p < passes; ++p)
-            atomicAdd(&s_h[wave][p * kRadix + (int)((key >> (8 * p)) & 255u)], 1u);
+            atomicAdd(&s_h[wave][p * kRadix + ((key >> (begin_bit + 8 * p)) & 255u)], 1u);
     }
     __syncthreads();
     for (int b = threadIdx.x; b < passes * kRadix; b += blockDim.x) {
@@ -78,10 +90,10 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *keys, ui
 }
 
 __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
-    const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint64_t *__restrict__ kout,
-    uint32_t *__restrict__ vout, uint32_t K, int shift, const uint32_t *hist, uint32_t *status,
-    uint32_t *ticket) {
-    __shared__ uint64_t s_keys[kSortTile];
+    const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
+    uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift,
+    const uint32_t *hist, uint32_t *status, uint32_t *ticket) {
+    __shared__ uint32_t s_keys[kSortTile];
     __shared__ uint32_t s_vals[kSortTile];
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
     __shared__ uint32_t s_dstart[kRadix];     // block-local start of each digit
@@ -93,26 +105,26 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
     if (tid == 0) s_part = atomicAdd(ticket, 1u);
     for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
     __syncthreads();
+    const uint32_t K = key_count(n_dev, n_host);
     const uint32_t part = s_part;
     const uint32_t base = part * (uint32_t)kSortTile;
+    if (base >= K) return;   // past the keys: later partitions leave as well
     const uint32_t wbase = base + (uint32_t)wave * kSortWaveItems;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
 
-    uint64_t key[kSortIpt];
-    uint32_t val[kSortIpt];
-    uint32_t rank[kSortIpt];
+    uint32_t key[kSortIpt], val[kSortIpt], rank[kSortIpt];
 #pragma unroll
     for (int j = 0; j < kSortIpt; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
         const bool valid = idx < K;
-        key[j] = valid ? kin[idx] : ~0ull;
+        key[j] = valid ? kin[idx] : 0xffffffffu;
         val[j] = valid ? vin[idx] : 0u;
     }
 #pragma unroll
     for (int j = 0; j < kSortIpt; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
         const bool valid = idx < K;
-        const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+        const uint32_t d = (key[j] >> shift) & 255u;
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
@@ -130,7 +142,6 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
     }
     __syncthreads();
 
-    // per digit: block total, wave prefixes, block-local start, global base
     const int d = tid;
     const uint32_t c0 = s_wh[d], c1 = s_wh[kRadix + d], c2 = s_wh[2 * kRadix + d],
                    c3 = s_wh[3 * kRadix + d];
@@ -146,12 +157,12 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
     uint32_t excl = 0;
     uint32_t *mine = status + (size_t)part * kRadix + d;
     if (part == 0) {
-        st_release(mine, kFlagInc | total);
+        st_agent(mine, kFlagInc | total);
     } else {
-        st_release(mine, kFlagAgg | total);
+        st_agent(mine, kFlagAgg | total);
         int p = (int)part - 1;
         while (true) {
-            const uint32_t w = ld_acquire(status + (size_t)p * kRadix + d);
+            const uint32_t w = ld_agent(status + (size_t)p * kRadix + d);
             const uint32_t flag = w & ~kValMask;
             if (flag == 0u) {
                 __builtin_amdgcn_s_sleep(1);
@@ -161,17 +172,16 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
             if (flag == kFlagInc) break;
             --p;
         }
-        st_release(mine, kFlagInc | (excl + total));
+        st_agent(mine, kFlagInc | (excl + total));
     }
     s_gbase[d] = hex + excl;
     __syncthreads();
 
-    // stage in digit order
 #pragma unroll
     for (int j = 0; j < kSortIpt; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
         if (idx < K) {
-            const uint32_t dj = (uint32_t)(key[j] >> shift) & 255u;
+            const uint32_t dj = (key[j] >> shift) & 255u;
             const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rank[j];
             s_keys[pos] = key[j];
             s_vals[pos] = val[j];
@@ -181,8 +191,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
 
     const uint32_t n_valid = K - base < (uint32_t)kSortTile ? K - base : (uint32_t)kSortTile;
     for (uint32_t i = tid; i < n_valid; i += kSortThreads) {
-        const uint64_t kk = s_keys[i];
-        const uint32_t dj = (uint32_t)(kk >> shift) & 255u;
+        const uint32_t kk = s_keys[i];
+        const uint32_t dj = (kk >> shift) & 255u;
         const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
         kout[out] = kk;
         vout[out] = s_vals[i];
@@ -193,36 +203,33 @@ inline uint32_t n_partitions(uint32_t K) { return (K + kSortTile - 1) / kSortTil
 
 }  // namespace
 
-int sort_passes(int n_tiles) {
-    int bits = 0;
-    while ((1 << bits) < n_tiles) ++bits;
-    return (32 + bits + 7) / 8;
+int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
+
+size_t sort_scratch_words(uint32_t max_keys, int passes) {
+    return (size_t)kMaxPasses * kRadix + kMaxPasses +
+           (size_t)passes * (n_partitions(max_keys) + 1) * kRadix;
 }
 
-size_t sort_scratch_words(uint32_t K, int passes) {
-    return (size_t)kMaxPasses * kRadix + kMaxPasses + (size_t)passes * n_partitions(K) * kRadix;
-}
-
-int launch_sort(uint32_t K, int passes, uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
-                uint32_t *vals_alt, uint32_t *scratch, hipStream_t st) {
-    if (K <= 1) return 0;
-    const uint32_t np = n_partitions(K);
+int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
+                    uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt,
+                    uint32_t *scratch, hipStream_t st) {
+    if (n_max <= 1 || passes <= 0) return 0;
+    const uint32_t np = n_partitions(n_max);
     uint32_t *hist = scratch;
     uint32_t *tickets = scratch + kMaxPasses * kRadix;
     uint32_t *status = tickets + kMaxPasses;
-    const size_t words = sort_scratch_words(K, passes);
-    const int clear_blocks = (int)((words + 255) / 256 < 2048 ? (words + 255) / 256 : 2048);
+    const size_t words = sort_scratch_words(n_max, passes);
+    const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
     sort_clear_kernel<<<clear_blocks, 256, 0, st>>>(scratch, words);
     const int hist_blocks = (int)(np < 1024 ? np : 1024);
-    sort_hist_kernel<<<hist_blocks, 256, 0, st>>>(keys, K, passes, hist);
-    uint64_t *ki = keys, *ko = keys_alt;
-    uint32_t *vi = vals, *vo = vals_alt;
+    sort_hist_kernel<<<hist_blocks, 256, 0, st>>>(keys, n_dev, n_max, begin_bit, passes, hist);
+    uint32_t *ki = keys, *ko = keys_alt, *vi = vals, *vo = vals_alt;
     for (int p = 0; p < passes; ++p) {
-        sort_pass_kernel<<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, K, 8 * p, hist + p * kRadix,
-                                                      status + (size_t)p * np * kRadix,
-                                                      tickets + p);
-        uint64_t *tk = ki; ki = ko; ko = tk;
-        uint32_t *tv = vi; vi = vo; vo = tv;
+        sort_pass_kernel<<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, n_dev, n_max,
+                                                      begin_bit + 8 * p, hist + p * kRadix,
+                                                      status + (size_t)p * np * kRadix, tickets + p);
+        uint32_t *t = ki; ki = ko; ko = t;
+        t = vi; vi = vo; vo = t;
     }
     return passes & 1;
 }

@@ -75,15 +75,16 @@ struct DevBuf {
 
 // Per-frame scratch of one render path (a scene's tgs_render_full, or a state).
 struct Workspace {
-    DevBuf g0, g1, col, rect, status, offsets, newly, scan;
-    DevBuf keys, keys_alt, vals, vals_alt, sort;
+    DevBuf g0, g1, col, rect, status, count, newly;
+    DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
+    DevBuf tkey, tval, tkey_alt, tval_alt, sort;
     DevBuf ranges, sel, sel_list, rowpre, cnt;
     Counters *host_cnt = nullptr;
     int n = -1, W = 0, H = 0;
     size_t key_cap = 0;
     // last frame, for tgs_debug_dump
     uint32_t last_K = 0;
-    int last_alt = 0;
+    const uint32_t *last_keys = nullptr, *last_vals = nullptr;
     bool has_frame = false;
 
     ~Workspace() {
@@ -100,9 +101,16 @@ struct Workspace {
             TGS_TRY(col.ensure(nn * sizeof(float4)));
             TGS_TRY(rect.ensure(nn * sizeof(ushort4)));
             TGS_TRY(status.ensure(nn));
-            TGS_TRY(offsets.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(count.ensure((nn + 4) * sizeof(uint32_t)));
             TGS_TRY(newly.ensure(nn * sizeof(int)));
-            TGS_TRY(scan.ensure(scan_scratch_words(n_) * sizeof(uint32_t)));
+            TGS_TRY(dkey.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(didx.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(dkey_alt.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(didx_alt.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(offs.ensure(nn * sizeof(uint32_t)));
+            TGS_TRY(scan.ensure(scan_scratch_bytes(n_)));
+            // the depth sort runs over at most n keys, four passes
+            TGS_TRY(sort.ensure(sort_scratch_words((uint32_t)nn, 4) * sizeof(uint32_t)));
             n = n_;
         }
         if (W_ != W || H_ != H) {
@@ -118,22 +126,27 @@ struct Workspace {
         return TGS_OK;
     }
 
+    // Called after the frame's read-back (the stream is idle): grow the key
+    // buffers and the sort scratch for K keys.
     tgs_status ensure_keys(uint32_t K, int passes) {
-        if (K > key_cap || !keys.p) {
+        if (K > key_cap || !tkey.p) {
             const size_t cap = (size_t)K + K / 2 + 1024;
-            TGS_TRY(keys.ensure(cap * sizeof(uint64_t)));
-            TGS_TRY(keys_alt.ensure(cap * sizeof(uint64_t)));
-            TGS_TRY(vals.ensure(cap * sizeof(uint32_t)));
-            TGS_TRY(vals_alt.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(tkey.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(tval.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(tkey_alt.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(tval_alt.ensure(cap * sizeof(uint32_t)));
             key_cap = cap;
         }
-        TGS_TRY(sort.ensure(sort_scratch_words((uint32_t)key_cap, passes) * sizeof(uint32_t)));
+        const size_t nn = (size_t)(n > 0 ? n : 1);
+        const size_t words = sort_scratch_words((uint32_t)key_cap, passes);
+        const size_t words_depth = sort_scratch_words((uint32_t)nn, 4);
+        TGS_TRY(sort.ensure((words > words_depth ? words : words_depth) * sizeof(uint32_t)));
         return TGS_OK;
     }
 
     Records records() const {
-        return Records{g0.as<float4>(), g1.as<float4>(), col.as<float4>(), rect.as<ushort4>(),
-                       status.as<uint8_t>()};
+        return Records{g0.as<float4>(),    g1.as<float4>(),   col.as<float4>(),
+                       rect.as<ushort4>(), status.as<uint8_t>(), count.as<uint32_t>()};
     }
 };
 
@@ -302,7 +315,7 @@ struct tgs_state {
 namespace {
 
 struct FrameResult {
-    uint32_t K = 0, n_surv = 0, n_newly = 0, n_sel = 0;
+    uint32_t K = 0, V = 0, n_surv = 0, n_newly = 0, n_sel = 0;
 };
 
 // Zero the counters and run the per-Gaussian stage.
@@ -315,14 +328,33 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
     return TGS_OK;
 }
 
-// Scan the key counts and read the counters back (the one sync of a frame).
+// Depth-order the Gaussians that have keys, scan their key counts in that
+// order, and read the counters back (the one host round trip of a frame).
 tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
-                          FrameResult &fr) {
+                          FrameResult &fr, const uint32_t **sorted_didx) {
+    const uint32_t nn = (uint32_t)(n > 0 ? n : 0);
+    int alt = 0;
     {
         ProfScope ps(TGS_PROF_SCAN, st);
-        launch_scan(n, ws.rect.as<ushort4>(), rowpre, TX, ws.offsets.as<uint32_t>(),
-                    ws.scan.as<uint32_t>(), ws.cnt.as<Counters>(), st);
-        TGS_LAUNCHED("scan");
+        if (rowpre) launch_count_masked(n, ws.rect.as<ushort4>(), rowpre, TX, ws.count.as<uint32_t>(), st);
+        launch_visible_scans(n, ws.count.as<uint32_t>(), ws.g1.as<float4>(), ws.dkey.as<uint32_t>(),
+                             ws.didx.as<uint32_t>(), ws.scan.p, ws.cnt.as<Counters>(), st);
+        TGS_LAUNCHED("visible scan");
+    }
+    {
+        ProfScope ps(TGS_PROF_SORT, st);
+        const uint32_t *n_dev = &ws.cnt.as<Counters>()->n_visible;
+        alt = launch_sort_u32(n_dev, nn, 0, 4, ws.dkey.as<uint32_t>(), ws.didx.as<uint32_t>(),
+                              ws.dkey_alt.as<uint32_t>(), ws.didx_alt.as<uint32_t>(),
+                              ws.sort.as<uint32_t>(), st);
+        TGS_LAUNCHED("depth sort");
+    }
+    const uint32_t *didx = alt ? ws.didx_alt.as<uint32_t>() : ws.didx.as<uint32_t>();
+    {
+        ProfScope ps(TGS_PROF_SCAN, st);
+        launch_sorted_count_scan(n, didx, ws.count.as<uint32_t>(), ws.offs.as<uint32_t>(), ws.scan.p,
+                                 ws.cnt.as<Counters>(), st);
+        TGS_LAUNCHED("key scan");
     }
     {
         ProfScope ps(TGS_PROF_READBACK, st);
@@ -330,43 +362,49 @@ tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, 
     }
     TGS_HIP(hipStreamSynchronize(st));
     fr.K = ws.host_cnt->n_keys;
+    fr.V = ws.host_cnt->n_visible;
     fr.n_surv = ws.host_cnt->n_survivors;
     fr.n_newly = ws.host_cnt->n_newly;
     fr.n_sel = ws.host_cnt->n_selected;
+    *sorted_didx = didx;
     if (fr.K > kMaxKeys)
         return fail(TGS_ERR_CAPACITY, "frame needs " + std::to_string(fr.K) +
                                           " Gaussian-tile keys; the limit is 2^30-1");
     return TGS_OK;
 }
 
-// Duplicate, sort and find tile ranges; returns the sorted values buffer.
-tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint8_t *sel, uint32_t K,
-                     hipStream_t st, const uint32_t **sorted_vals) {
-    const int passes = sort_passes(TX * TY);
-    TGS_TRY(ws.ensure_keys(K, passes));
+// Emit the keys in depth order, sort them by tile (stable), find tile ranges;
+// returns the per-tile lists of Gaussian indices.
+tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, const uint32_t *didx,
+                     const FrameResult &fr, hipStream_t st, const uint32_t **sorted_vals) {
+    int bits = 0;
+    while ((1 << bits) < TX * TY) ++bits;
+    const int passes = sort_passes_for_bits(bits);
+    TGS_TRY(ws.ensure_keys(fr.K, passes));
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
-        launch_duplicate(n, ws.rect.as<ushort4>(), ws.g1.as<float4>(), ws.offsets.as<uint32_t>(),
-                         sel, TX, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(), st);
+        launch_duplicate(fr.V, fr.K, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX,
+                         ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(), st);
         TGS_LAUNCHED("duplicate");
     }
     int alt = 0;
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        alt = launch_sort(K, passes, ws.keys.as<uint64_t>(), ws.vals.as<uint32_t>(),
-                          ws.keys_alt.as<uint64_t>(), ws.vals_alt.as<uint32_t>(),
-                          ws.sort.as<uint32_t>(), st);
-        TGS_LAUNCHED("sort");
+        alt = launch_sort_u32(nullptr, fr.K, 0, passes, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
+                              ws.tkey_alt.as<uint32_t>(), ws.tval_alt.as<uint32_t>(),
+                              ws.sort.as<uint32_t>(), st);
+        TGS_LAUNCHED("tile sort");
     }
-    const uint64_t *skeys = alt ? ws.keys_alt.as<uint64_t>() : ws.keys.as<uint64_t>();
+    const uint32_t *skeys = alt ? ws.tkey_alt.as<uint32_t>() : ws.tkey.as<uint32_t>();
     {
         ProfScope ps(TGS_PROF_RANGES, st);
-        launch_ranges(K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
+        launch_ranges(fr.K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
     }
-    *sorted_vals = alt ? ws.vals_alt.as<uint32_t>() : ws.vals.as<uint32_t>();
-    ws.last_K = K;
-    ws.last_alt = alt;
+    *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
+    ws.last_K = fr.K;
+    ws.last_keys = skeys;
+    ws.last_vals = *sorted_vals;
     ws.has_frame = true;
     return TGS_OK;
 }
@@ -491,33 +529,71 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
     sc->n = n;
     sc->deg = d->sh_degree;
     sc->ncoef = ncoef;
-    const size_t nn = (size_t)(n > 0 ? n : 1);
-    const size_t n_arrays = 11 + (size_t)ncoef * 3;
-    tgs_status s = sc->data.ensure(n_arrays * nn * sizeof(float));
+    const int slots = (3 * ncoef + 3) / 4;
+    const size_t n_pad = ((size_t)(n > 0 ? n : 1) + 63) / 64 * 64;
+    const size_t n_vec = n_pad * (3 + (size_t)slots);   // float4 count
+    tgs_status s = sc->data.ensure(n_vec * sizeof(float4));
     if (s != TGS_OK) {
         delete sc;
         return s;
     }
-    float *base = sc->data.as<float>();
+    float4 *base = sc->data.as<float4>();
     hipStream_t st = (hipStream_t)stream;
-    std::vector<float> stage(nn);
-    auto upload = [&](int slot, auto getter) -> hipError_t {
-        for (int i = 0; i < n; ++i) stage[i] = getter(i);
-        hipError_t e = hipMemcpyAsync(base + slot * nn, stage.data(), (size_t)n * sizeof(float),
-                                      hipMemcpyHostToDevice, st);
-        if (e != hipSuccess) return e;
+    std::vector<float4> stage;
+    hipError_t e = hipSuccess;
+    try {
+        stage.assign(n_pad, make_float4(0.0f, 0.0f, 0.0f, 0.0f));
+    } catch (...) {
+        delete sc;
+        return fail(TGS_ERR_OUT_OF_MEMORY, "host staging allocation failed");
+    }
+    auto put = [&](float4 *dst) -> hipError_t {
+        hipError_t err = hipMemcpyAsync(dst, stage.data(), n_pad * sizeof(float4),
+                                        hipMemcpyHostToDevice, st);
+        if (err != hipSuccess) return err;
         return hipStreamSynchronize(st);
     };
-    hipError_t e = hipSuccess;
-    for (int c = 0; c < 3 && e == hipSuccess && n > 0; ++c)
-        e = upload(c, [&](int i) { return d->means[3 * (size_t)i + c]; });
-    for (int c = 0; c < 3 && e == hipSuccess && n > 0; ++c)
-        e = upload(3 + c, [&](int i) { return d->scales[3 * (size_t)i + c]; });
-    for (int c = 0; c < 4 && e == hipSuccess && n > 0; ++c)
-        e = upload(6 + c, [&](int i) { return d->rotations[4 * (size_t)i + c]; });
-    if (e == hipSuccess && n > 0) e = upload(10, [&](int i) { return d->opacities[i]; });
-    for (int c = 0; c < ncoef * 3 && e == hipSuccess && n > 0; ++c)
-        e = upload(11 + c, [&](int i) { return d->sh[(size_t)i * ncoef * 3 + c]; });
+    for (int i = 0; i < n; ++i)
+        stage[i] = make_float4(d->means[3 * (size_t)i], d->means[3 * (size_t)i + 1],
+                               d->means[3 * (size_t)i + 2], d->opacities[i]);
+    e = put(base);
+    if (e == hipSuccess) {
+        for (int i = 0; i < n; ++i)
+            stage[i] = make_float4(d->scales[3 * (size_t)i], d->scales[3 * (size_t)i + 1],
+                                   d->scales[3 * (size_t)i + 2], d->rotations[4 * (size_t)i]);
+        e = put(base + n_pad);
+    }
+    if (e == hipSuccess) {
+        for (int i = 0; i < n; ++i)
+            stage[i] = make_float4(d->rotations[4 * (size_t)i + 1], d->rotations[4 * (size_t)i + 2],
+                                   d->rotations[4 * (size_t)i + 3], 0.0f);
+        e = put(base + 2 * n_pad);
+    }
+    // SH: wave-tiled, one staging pass per 64-Gaussian block row of slots
+    if (e == hipSuccess) {
+        const size_t per = (size_t)ncoef * 3;
+        std::vector<float4> sh;
+        try {
+            sh.assign(n_pad * slots, make_float4(0.0f, 0.0f, 0.0f, 0.0f));
+        } catch (...) {
+            delete sc;
+            return fail(TGS_ERR_OUT_OF_MEMORY, "host staging allocation failed");
+        }
+        for (int i = 0; i < n; ++i) {
+            const float *src = d->sh + (size_t)i * per;
+            for (int j = 0; j < slots; ++j) {
+                float v[4];
+                for (int c = 0; c < 4; ++c) {
+                    const size_t f = 4 * (size_t)j + c;
+                    v[c] = f < per ? src[f] : 0.0f;
+                }
+                sh[((size_t)(i >> 6) * slots + j) * 64 + (i & 63)] = make_float4(v[0], v[1], v[2], v[3]);
+            }
+        }
+        e = hipMemcpyAsync(base + 3 * n_pad, sh.data(), sh.size() * sizeof(float4),
+                           hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+    }
     if (e != hipSuccess) {
         delete sc;
         return fail(TGS_ERR_DEVICE, std::string("scene upload: ") + hipGetErrorString(e));
@@ -526,19 +602,11 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
     v.n = n;
     v.deg = sc->deg;
     v.ncoef = ncoef;
-    v.mx = base + 0 * nn;
-    v.my = base + 1 * nn;
-    v.mz = base + 2 * nn;
-    v.sx = base + 3 * nn;
-    v.sy = base + 4 * nn;
-    v.sz = base + 5 * nn;
-    v.qw = base + 6 * nn;
-    v.qx = base + 7 * nn;
-    v.qy = base + 8 * nn;
-    v.qz = base + 9 * nn;
-    v.opac = base + 10 * nn;
-    v.sh = base + 11 * nn;
-    // The SH block uses stride nn == n for n > 0 (see SceneDev::sh).
+    v.sh_slots = slots;
+    v.mean_op = base;
+    v.scale_qw = base + n_pad;
+    v.qxyz = base + 2 * n_pad;
+    v.sh = base + 3 * n_pad;
     *out = sc;
     return TGS_OK;
 }
@@ -559,9 +627,9 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     const CamK ck = make_camk(cam);
     TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
     FrameResult fr;
-    TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr));
-    const uint32_t *vals = nullptr;
-    TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, fr.K, st, &vals));
+    const uint32_t *didx = nullptr, *vals = nullptr;
+    TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
+    TGS_TRY(step_keys(ws, TX, TY, nullptr, didx, fr, st, &vals));
     if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
     BlendArgs a = blend_args(ws, W, H, vals);
     a.rgb = out->rgb;
@@ -612,7 +680,7 @@ tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
     if (st == TGS_OK) st = s->tgb_s.ensure(px * 4);
     if (st == TGS_OK) st = s->tab.ensure(3 * px * 4);
     if (st == TGS_OK) st = s->g_flag.ensure(nn);
-    if (st == TGS_OK) st = s->fbox.ensure(16);
+    if (st == TGS_OK) st = s->fbox.ensure((4 + 4 * kAfcPartials) * sizeof(int));
     if (st == TGS_OK) st = s->dmin.ensure(px * 4);
     if (st == TGS_OK) st = s->smax.ensure(px * 4);
     if (st == TGS_OK) st = s->dfill.ensure(px * 4);
@@ -714,8 +782,9 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                           out->tile_mask, ws.cnt.as<Counters>(), st);
             TGS_LAUNCHED("tile selection");
         }
-        TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr));
-        TGS_TRY(step_keys(ws, sc->n, TX, TY, ws.sel.as<uint8_t>(), fr.K, st, &vals));
+        const uint32_t *didx = nullptr;
+        TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr, &didx));
+        TGS_TRY(step_keys(ws, TX, TY, ws.rowpre.as<uint32_t>(), didx, fr, st, &vals));
         BlendArgs a = blend_args(ws, W, H, vals);
         a.tile_list = ws.sel_list.as<int>();
         a.rgb = out->rgb;
@@ -740,8 +809,9 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
         }
         TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
-        TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr));
-        TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, fr.K, st, &vals));
+        const uint32_t *didx = nullptr;
+        TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
+        TGS_TRY(step_keys(ws, TX, TY, nullptr, didx, fr, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, W, H, vals);
         a.rgb = out->rgb;
@@ -895,14 +965,8 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
     size_t size = 0;
     if (!ws.has_frame) return fail(TGS_ERR_INVALID_ARG, "no frame has been rendered yet");
     switch (what) {
-        case TGS_DUMP_SORTED_VALUES:
-            src = ws.last_alt ? ws.vals_alt.p : ws.vals.p;
-            size = (size_t)ws.last_K * 4;
-            break;
-        case TGS_DUMP_SORTED_KEYS:
-            src = ws.last_alt ? ws.keys_alt.p : ws.keys.p;
-            size = (size_t)ws.last_K * 8;
-            break;
+        case TGS_DUMP_SORTED_VALUES: src = ws.last_vals; size = (size_t)ws.last_K * 4; break;
+        case TGS_DUMP_SORTED_KEYS: src = ws.last_keys; size = (size_t)ws.last_K * 4; break;
         case TGS_DUMP_TILE_RANGES: src = ws.ranges.p; size = nt * 8; break;
         case TGS_DUMP_RECTS: src = ws.rect.p; size = (size_t)n * 8; break;
         case TGS_DUMP_STATUS: src = ws.status.p; size = (size_t)n; break;

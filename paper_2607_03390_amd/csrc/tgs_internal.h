@@ -23,14 +23,16 @@ struct CamK {
     float campos[3];          // camera centre in world space
 };
 
-// Device scene, structure of arrays.
+// Device scene.  Attributes are grouped in 16-byte vectors so a wave loads
+// each group as one contiguous 1 KB request; the SH coefficients (the bulk of
+// the bytes) are stored wave-tiled: for Gaussian i, float4 slot j lives at
+// ((i / 64) * sh_slots + j) * 64 + i % 64.
 struct SceneDev {
-    int n, deg, ncoef;
-    const float *mx, *my, *mz;
-    const float *sx, *sy, *sz;
-    const float *qw, *qx, *qy, *qz;
-    const float *opac;
-    const float *sh;          // [(k*3 + ch) * n + i]
+    int n, deg, ncoef, sh_slots;
+    const float4 *mean_op;    // x, y, z, opacity
+    const float4 *scale_qw;   // sx, sy, sz, qw
+    const float4 *qxyz;       // qx, qy, qz, 0
+    const float4 *sh;         // wave-tiled coefficient-major (k*3 + channel) floats
 };
 
 // Per-Gaussian records written by the preprocess.
@@ -40,6 +42,7 @@ struct Records {
     float4 *col;              // r, g, b, 0
     ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
     uint8_t *status;          // bit0 survivor, bit1 newly visible
+    uint32_t *count;          // keys of the Gaussian (tiles of its rectangle)
 };
 
 // Temporal dynamic culling inputs of the preprocess.
@@ -59,6 +62,8 @@ struct Counters {
     uint32_t n_survivors;
     uint32_t n_newly;
     uint32_t n_selected;
+    uint32_t n_visible;       // Gaussians with at least one key
+    uint32_t pad[3];
 };
 
 // Ordered-int encoding of a float: signed-int order equals float order, so
@@ -76,20 +81,27 @@ void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Re
                        Counters *cnt, hipStream_t st);
 
 // ---- launchers (k_keys.hip) ----
-size_t scan_scratch_words(int n);
-void launch_scan(int n, const ushort4 *rect, const uint32_t *rowpre, int TX, uint32_t *offsets,
-                 uint32_t *scratch, Counters *cnt, hipStream_t st);
-void launch_duplicate(int n, const ushort4 *rect, const float4 *g1, const uint32_t *offsets,
-                      const uint8_t *sel, int TX, uint64_t *keys, uint32_t *vals, hipStream_t st);
-void launch_ranges(uint32_t K, int n_tiles, const uint64_t *keys, uint2 *ranges, hipStream_t st);
+size_t scan_scratch_bytes(int n);
+void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
+                         uint32_t *count, hipStream_t st);
+void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
+                          uint32_t *didx, void *scratch, Counters *cnt, hipStream_t st);
+void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
+                              void *scratch, Counters *cnt, hipStream_t st);
+void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,
+                      const ushort4 *rect, const uint32_t *rowpre, int TX, uint32_t *tkey,
+                      uint32_t *tval, hipStream_t st);
+void launch_ranges(uint32_t K, int n_tiles, const uint32_t *keys, uint2 *ranges, hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
-size_t sort_scratch_words(uint32_t K, int passes);
-int sort_passes(int n_tiles);
-// Sorts (keys, vals) in place by key; alt buffers of the same size are used
-// as ping-pong storage.  Returns 1 if the result ended in the alt buffers.
-int launch_sort(uint32_t K, int passes, uint64_t *keys, uint32_t *vals, uint64_t *keys_alt,
-                uint32_t *vals_alt, uint32_t *scratch, hipStream_t st);
+int sort_passes_for_bits(int bits);
+size_t sort_scratch_words(uint32_t max_keys, int passes);
+// Stable LSD sort of (key, value) pairs on key bits [begin_bit, begin_bit +
+// 8*passes).  The key count is *n_dev if n_dev is not NULL (n_max bounds it),
+// else n_max.  Returns 1 if the result is in the alt buffers.
+int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
+                    uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt,
+                    uint32_t *scratch, hipStream_t st);
 
 // ---- launchers (k_blend.hip) ----
 struct BlendArgs {
@@ -107,6 +119,8 @@ struct BlendArgs {
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
 };
 void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st);
+// fbox must hold 4 + 4 * kAfcPartials ints (result, then partials).
+constexpr int kAfcPartials = 256;
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
                        hipStream_t st);
 

@@ -241,7 +241,7 @@ def parse_state(blob: bytes):
                 g_rendered=g)
 
 
-_DUMP_DTYPE = {TGS_DUMP_SORTED_VALUES: np.uint32, TGS_DUMP_SORTED_KEYS: np.uint64,
+_DUMP_DTYPE = {TGS_DUMP_SORTED_VALUES: np.uint32, TGS_DUMP_SORTED_KEYS: np.uint32,
                TGS_DUMP_TILE_RANGES: np.uint32, TGS_DUMP_RECORDS: np.float32,
                TGS_DUMP_RECTS: np.uint16, TGS_DUMP_STATUS: np.uint8,
                TGS_DUMP_WARP_DEPTH: np.float32, TGS_DUMP_WARP_SIGMA: np.float32,
