@@ -25,7 +25,7 @@ namespace {
 
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
-    // Per staged Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
+    // Staged per Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
     // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares)
     // so that log2 of the Gaussian falloff is a three-FMA quadratic form and
     // the opacity is one v_exp_f32.
@@ -34,25 +34,33 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     __shared__ float4 s_col[256];
     __shared__ int s_idx[256];
     __shared__ uint32_t s_flag[256];
+    // Wave w (pixel rows 4w..4w+3 of the tile) visits only the staged
+    // Gaussians whose alpha >= 1/255 ellipse, conservatively enlarged, meets
+    // its 16x4 strip, in staging (= depth) order.
+    __shared__ uint8_t s_list[4][256];
+    __shared__ uint32_t s_cnt[4][4];
 
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;
     const int px = tx * kTile + (tid & 15), py = ty * kTile + (tid >> 4);
     const bool inside = px < a.W && py < a.H;
     const float fpx = (float)px, fpy = (float)py;
+    const float tile_x0 = (float)(tx * kTile), tile_y0 = (float)(ty * kTile);
     const uint2 range = a.ranges[tile];
     constexpr float kLog2e = 1.4426950408889634f;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
 
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
     bool pivot = false;
     bool done = !inside;
-    uint32_t evaluated = 0;
+    uint32_t stop_pos = range.y;   // list position of the stopping Gaussian (+1 below)
 
     for (uint32_t b = range.x; b < range.y; b += 256) {
         if (__syncthreads_count(done) == 256) break;
         const uint32_t k = b + tid;
+        uint32_t strips = 0;
         if (k < range.y) {
             const int idx = (int)a.vals[k];
             const float4 g0 = a.g0[idx];
@@ -61,13 +69,46 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             s_g0[tid] = make_float4(g0.x, g0.y, -0.5f * kLog2e * g0.z, -kLog2e * g0.w);
             s_g1[tid] = make_float4(-0.5f * kLog2e * g1.x, g1.y, g1.z, 0.0f);
             s_col[tid] = a.col[idx];
+            // alpha >= 1/255  <=>  d^T conic d <= 2 ln(255 o): an ellipse with
+            // half extents sqrt(k Sigma'_xx), sqrt(k Sigma'_yy); enlarged by
+            // 0.2% + 0.05 px so that every pixel left out has alpha well below
+            // the threshold.
+            if (g1.y >= 0.999f * kAlphaMin) {
+                const float kq = 2.0f * __logf(fmaxf(255.0f * g1.y, 1.0f)) + 1e-3f;
+                const float det = g0.z * g1.x - g0.w * g0.w;
+                const float hx = sqrtf(kq * g1.x / det) * 1.002f + 0.05f;
+                const float hy = sqrtf(kq * g0.z / det) * 1.002f + 0.05f;
+                if (g0.x + hx >= tile_x0 && g0.x - hx <= tile_x0 + 15.0f) {
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const float ylo = tile_y0 + 4.0f * w;
+                        if (g0.y + hy >= ylo && g0.y - hy <= ylo + 3.0f) strips |= 1u << w;
+                    }
+                }
+            }
         }
         if (CAPTURE) s_flag[tid] = 0u;
+        // order-preserving compaction of each strip's Gaussians
+        uint64_t bal[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            bal[w] = __ballot((strips >> w) & 1u);
+            if (lane == 0) s_cnt[wave][w] = (uint32_t)__popcll(bal[w]);
+        }
         __syncthreads();
-        const int cnt = (int)min(256u, range.y - b);
-        for (int j = 0; j < cnt; ++j) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            if ((strips >> w) & 1u) {
+                uint32_t pos = (uint32_t)__popcll(bal[w] & lt_mask);
+                for (int sw2 = 0; sw2 < wave; ++sw2) pos += s_cnt[sw2][w];
+                s_list[w][pos] = (uint8_t)tid;
+            }
+        }
+        const uint32_t n_mine = s_cnt[0][wave] + s_cnt[1][wave] + s_cnt[2][wave] + s_cnt[3][wave];
+        __syncthreads();
+        for (uint32_t e = 0; e < n_mine; ++e) {
             if (__all(done)) break;
-            if (COUNT) evaluated += done ? 0u : 1u;
+            const int j = s_list[wave][e];
             const float4 g0 = s_g0[j];
             const float4 g1 = s_g1[j];
             const float dx = g0.x - fpx, dy = g0.y - fpy;
@@ -85,6 +126,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             cg = __builtin_fmaf(w, c.y, cg);
             cb = __builtin_fmaf(w, c.z, cb);
             T = inc ? Tn : T;
+            if (COUNT && stop) stop_pos = b + (uint32_t)j;
             done = done || stop;
             if (CAPTURE) {
                 const float dep = g1.z;
@@ -111,7 +153,8 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     }
 
     if (COUNT) {
-        unsigned long long e = evaluated;
+        // evaluated list entries: up to and including the stopping one
+        unsigned long long e = inside ? (unsigned long long)(stop_pos < range.y ? stop_pos + 1 : range.y) - range.x : 0ull;
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) e += __shfl_xor(e, o);
         if (lane == 0 && e) atomicAdd(a.pairs, e);

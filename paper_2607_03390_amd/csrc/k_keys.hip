@@ -9,9 +9,9 @@
 //    coalesced (the owning Gaussian is found by a binary search over the
 //    wave's 64 offsets held in LDS);
 //  - per-tile [start, end) ranges of the tile-sorted keys.
-// The scans are single-pass chained scans (decoupled look-back over
-// 4096-element partitions numbered by an atomic ticket); their totals stay on
-// the device, so the sorts need no host round trip.
+// The scans are reduce-then-scan over 4096-element blocks (no block waits on
+// another, no contended atomics); their totals stay on the device, so the
+// depth sort needs no host round trip.
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -21,9 +21,6 @@ namespace {
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanTile = kScanThreads * kScanItems;   // 4096
-constexpr uint64_t kSFlagAgg = 1ull << 62;
-constexpr uint64_t kSFlagInc = 2ull << 62;
-constexpr uint64_t kSValMask = (1ull << 62) - 1;
 
 __device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int TX) {
     if (r.x > r.z || r.y > r.w) return 0u;
@@ -40,13 +37,6 @@ __global__ __launch_bounds__(256) void count_masked_kernel(int n, const ushort4 
                                                            uint32_t *count) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) count[i] = masked_count(rect[i], rowpre, TX);
-}
-
-__device__ inline uint64_t ld_agent64(const uint64_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void st_agent64(uint64_t *p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Exclusive block scan of 64-bit values over 256 threads.
@@ -72,126 +62,104 @@ __device__ inline uint64_t block_exclusive_scan64(uint64_t v, uint64_t *s_wave, 
     return off + inc - v;
 }
 
-// Partition prefix by decoupled look-back (one lane per block does the walk).
-__device__ inline uint64_t chained_prefix(uint64_t *status, uint32_t part, uint64_t block_total,
-                                          uint64_t *s_prefix) {
+// The two scans of a frame are reduce-then-scan: per-block sums, one block
+// scanning the sums, then a downsweep that recomputes the local values.
+// Item j of block b is element b*4096 + j*256 + threadIdx.x (coalesced).
+
+// MODE 0: flags (count[i] > 0) over Gaussians i < n (n on the host).
+// MODE 1: key counts count[didx[s]] over sorted positions s < cnt->n_visible.
+template <int MODE>
+__device__ inline uint32_t scan_value(uint32_t e, int n, const uint32_t *count, const uint32_t *didx,
+                                      const Counters *cnt) {
+    if (MODE == 0) return (e < (uint32_t)n && count[e] > 0u) ? 1u : 0u;
+    return e < cnt->n_visible ? count[didx[e]] : 0u;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(int n, const uint32_t *count,
+                                                                   const uint32_t *didx,
+                                                                   const Counters *cnt,
+                                                                   uint64_t *block_sums) {
+    const uint32_t base = blockIdx.x * (uint32_t)kScanTile;
+    uint64_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j)
+        sum += scan_value<MODE>(base + j * kScanThreads + threadIdx.x, n, count, didx, cnt);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    __shared__ uint64_t s_sum[4];
+    if ((threadIdx.x & 63) == 0) s_sum[threadIdx.x >> 6] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) block_sums[blockIdx.x] = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
+}
+
+// One block: exclusive scan of the block sums in place; the total goes to
+// cnt->n_visible (MODE 0) or cnt->n_keys (MODE 1, saturated).
+template <int MODE>
+__global__ __launch_bounds__(1024) void scan_top_kernel(int nb, uint64_t *block_sums,
+                                                        Counters *cnt) {
+    __shared__ uint64_t s_wave[16];
+    __shared__ uint64_t s_carry;
+    if (threadIdx.x == 0) s_carry = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int c = 0; c < nb; c += 1024) {
+        const int i = c + threadIdx.x;
+        const uint64_t v = i < nb ? block_sums[i] : 0;
+        uint64_t inc = v;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint64_t o = __shfl_up(inc, d);
+            if (lane >= d) inc += o;
+        }
+        if (lane == 63) s_wave[wave] = inc;
+        __syncthreads();
+        uint64_t off = 0, tot = 0;
+        for (int w = 0; w < 16; ++w) {
+            const uint64_t x = s_wave[w];
+            if (w < wave) off += x;
+            tot += x;
+        }
+        const uint64_t carry = s_carry;
+        if (i < nb) block_sums[i] = carry + off + inc - v;
+        __syncthreads();
+        if (threadIdx.x == 0) s_carry = carry + tot;
+        __syncthreads();
+    }
     if (threadIdx.x == 0) {
-        uint64_t excl = 0;
-        if (part == 0) {
-            st_agent64(status, kSFlagInc | block_total);
-        } else {
-            st_agent64(status + part, kSFlagAgg | block_total);
-            int p = (int)part - 1;
-            while (true) {
-                const uint64_t w = ld_agent64(status + p);
-                const uint64_t flag = w & ~kSValMask;
-                if (flag == 0) {
-                    __builtin_amdgcn_s_sleep(1);
-                    continue;
-                }
-                excl += w & kSValMask;
-                if (flag == kSFlagInc) break;
-                --p;
+        const uint64_t total = s_carry;
+        const uint32_t t32 = total > 0xffffffffull ? 0xffffffffu : (uint32_t)total;
+        if (MODE == 0) cnt->n_visible = t32;
+        else cnt->n_keys = t32;
+    }
+}
+
+// MODE 0: compaction of the Gaussians with keys into (depth bits, index).
+// MODE 1: offs[s] = exclusive prefix of the key counts in depth order.
+template <int MODE>
+__global__ __launch_bounds__(kScanThreads) void scan_down_kernel(int n, const uint32_t *count,
+                                                                 const uint32_t *didx,
+                                                                 const Counters *cnt,
+                                                                 const uint64_t *block_sums,
+                                                                 const float4 *g1, uint32_t *out_a,
+                                                                 uint32_t *out_b) {
+    __shared__ uint64_t s_wave[4];
+    const uint32_t base = blockIdx.x * (uint32_t)kScanTile;
+    uint64_t run = block_sums[blockIdx.x];
+    for (int j = 0; j < kScanItems; ++j) {
+        const uint32_t e = base + j * kScanThreads + threadIdx.x;
+        const uint32_t v = scan_value<MODE>(e, n, count, didx, cnt);
+        uint64_t tot;
+        const uint64_t ex = block_exclusive_scan64(v, s_wave, &tot);
+        if (MODE == 0) {
+            if (v) {
+                out_a[run + ex] = __float_as_uint(g1[e].z);
+                out_b[run + ex] = e;
             }
-            st_agent64(status + part, kSFlagInc | (excl + block_total));
+        } else if (e < cnt->n_visible) {
+            out_a[e] = (uint32_t)(run + ex);
         }
-        *s_prefix = excl;
-    }
-    __syncthreads();
-    return *s_prefix;
-}
-
-// Compacts the Gaussians with count > 0, in index order, into
-// (depth bits, index) pairs; the number of such Gaussians goes to
-// cnt->n_visible.
-__global__ __launch_bounds__(kScanThreads) void compact_visible_kernel(
-    int n, const uint32_t *__restrict__ count, const float4 *__restrict__ g1, uint32_t *dkey,
-    uint32_t *didx, uint64_t *status, uint32_t *ticket, Counters *cnt) {
-    __shared__ uint64_t s_wave[4];
-    __shared__ uint64_t s_prefix;
-    __shared__ uint32_t s_part;
-    if (threadIdx.x == 0) s_part = atomicAdd(ticket, 1u);
-    __syncthreads();
-    const uint32_t part = s_part;
-    const uint32_t base = part * (uint32_t)kScanTile;
-    if (base >= (uint32_t)n) {
-        if (part == 0 && threadIdx.x == 0) cnt->n_visible = 0u;
-        return;
-    }
-    const uint32_t first = base + threadIdx.x * kScanItems;
-    uint32_t flags = 0, local = 0;
-#pragma unroll
-    for (int j = 0; j < kScanItems; j += 4) {
-        const uint32_t i = first + j;
-        uint4 c = make_uint4(0u, 0u, 0u, 0u);
-        if (i + 3 < (uint32_t)n) {
-            c = *reinterpret_cast<const uint4 *>(count + i);
-        } else {
-            if (i < (uint32_t)n) c.x = count[i];
-            if (i + 1 < (uint32_t)n) c.y = count[i + 1];
-            if (i + 2 < (uint32_t)n) c.z = count[i + 2];
-        }
-        const uint32_t f = (c.x > 0u ? 1u : 0u) | (c.y > 0u ? 2u : 0u) | (c.z > 0u ? 4u : 0u) |
-                           (c.w > 0u ? 8u : 0u);
-        flags |= f << j;
-    }
-    local = (uint32_t)__popc(flags);
-    uint64_t block_total;
-    const uint64_t texcl = block_exclusive_scan64(local, s_wave, &block_total);
-    const uint64_t prefix = chained_prefix(status, part, block_total, &s_prefix);
-    uint32_t pos = (uint32_t)(prefix + texcl);
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        if (flags & (1u << j)) {
-            const uint32_t i = first + j;
-            dkey[pos] = __float_as_uint(g1[i].z);
-            didx[pos] = i;
-            ++pos;
-        }
-    }
-    if (base + kScanTile >= (uint32_t)n && threadIdx.x == 0)
-        cnt->n_visible = (uint32_t)(prefix + block_total);
-}
-
-// Exclusive scan of the key counts in depth order: offs[s] for the sorted
-// position s of Gaussian didx[s]; total -> cnt->n_keys (saturated).
-__global__ __launch_bounds__(kScanThreads) void scan_sorted_counts_kernel(
-    const uint32_t *__restrict__ didx, const uint32_t *__restrict__ count, uint32_t *offs,
-    uint64_t *status, uint32_t *ticket, Counters *cnt) {
-    __shared__ uint64_t s_wave[4];
-    __shared__ uint64_t s_prefix;
-    __shared__ uint32_t s_part;
-    if (threadIdx.x == 0) s_part = atomicAdd(ticket, 1u);
-    __syncthreads();
-    const uint32_t n = cnt->n_visible;
-    const uint32_t part = s_part;
-    const uint32_t base = part * (uint32_t)kScanTile;
-    if (base >= n) {
-        if (part == 0 && threadIdx.x == 0) cnt->n_keys = 0u;
-        return;
-    }
-    const uint32_t first = base + threadIdx.x * kScanItems;
-    uint32_t c[kScanItems];
-    uint64_t local = 0;
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        const uint32_t s = first + j;
-        c[j] = s < n ? count[didx[s]] : 0u;
-        local += c[j];
-    }
-    uint64_t block_total;
-    const uint64_t texcl = block_exclusive_scan64(local, s_wave, &block_total);
-    const uint64_t prefix = chained_prefix(status, part, block_total, &s_prefix);
-    uint64_t run = prefix + texcl;
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        const uint32_t s = first + j;
-        if (s < n) offs[s] = (uint32_t)run;
-        run += c[j];
-    }
-    if (base + kScanTile >= n && threadIdx.x == 0) {
-        const uint64_t K = prefix + block_total;
-        cnt->n_keys = K > 0xffffffffull ? 0xffffffffu : (uint32_t)K;
+        run += tot;
     }
 }
 
@@ -272,20 +240,12 @@ __global__ __launch_bounds__(256) void ranges_kernel(uint32_t K, const uint32_t 
     if (k == K - 1 || keys[k + 1] != t) ranges[t].y = k + 1;
 }
 
-__global__ __launch_bounds__(256) void clear64_kernel(uint64_t *p, size_t n) {
-    for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n;
-         k += (size_t)gridDim.x * blockDim.x)
-        p[k] = 0ull;
-}
-
 inline uint32_t scan_parts(uint32_t n) { return (n + kScanTile - 1) / kScanTile; }
 
 }  // namespace
 
 size_t scan_scratch_bytes(int n) {
-    // two chained scans: status words + tickets for each
-    const size_t parts = scan_parts((uint32_t)(n > 0 ? n : 1)) + 1;
-    return 2 * (parts + 1) * sizeof(uint64_t);
+    return (size_t)(scan_parts((uint32_t)(n > 0 ? n : 1)) + 1) * sizeof(uint64_t);
 }
 
 void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
@@ -296,21 +256,21 @@ void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int
 
 void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
                           uint32_t *didx, void *scratch, Counters *cnt, hipStream_t st) {
-    const uint32_t parts = scan_parts((uint32_t)(n > 0 ? n : 1));
-    uint64_t *status = static_cast<uint64_t *>(scratch);
-    const size_t words = 2 * ((size_t)parts + 2);
-    clear64_kernel<<<(unsigned)((words + 255) / 256), 256, 0, st>>>(status, words);
-    uint32_t *ticket = reinterpret_cast<uint32_t *>(status + parts + 1);
-    compact_visible_kernel<<<parts, kScanThreads, 0, st>>>(n, count, g1, dkey, didx, status,
-                                                           ticket, cnt);
+    const uint32_t nb = scan_parts((uint32_t)(n > 0 ? n : 1));
+    uint64_t *sums = static_cast<uint64_t *>(scratch);
+    scan_reduce_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums);
+    scan_top_kernel<0><<<1, 1024, 0, st>>>((int)nb, sums, cnt);
+    scan_down_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums, g1, dkey, didx);
 }
 
 void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
                               void *scratch, Counters *cnt, hipStream_t st) {
-    const uint32_t parts = scan_parts((uint32_t)(n > 0 ? n : 1));
-    uint64_t *status = static_cast<uint64_t *>(scratch) + parts + 2;
-    uint32_t *ticket = reinterpret_cast<uint32_t *>(status + parts + 1);
-    scan_sorted_counts_kernel<<<parts, kScanThreads, 0, st>>>(didx, count, offs, status, ticket, cnt);
+    const uint32_t nb = scan_parts((uint32_t)(n > 0 ? n : 1));
+    uint64_t *sums = static_cast<uint64_t *>(scratch);
+    scan_reduce_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums);
+    scan_top_kernel<1><<<1, 1024, 0, st>>>((int)nb, sums, cnt);
+    scan_down_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums, nullptr, offs,
+                                                     nullptr);
 }
 
 void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,

@@ -186,19 +186,49 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
         rec.status[i] = (uint8_t)((survivor ? 1 : 0) | (newly ? 2 : 0));
     }
 
-    // wave-aggregated counters and the newly-visible list
+    // per-block counts (no contended device-wide atomics)
+    __shared__ uint32_t s_cnt[4][2];
     const uint64_t surv_mask = __ballot(survivor);
     const uint64_t newly_mask = __ballot(newly);
-    const int lane = threadIdx.x & 63;
-    if (lane == 0 && surv_mask) atomicAdd(&cnt->n_survivors, (uint32_t)__popcll(surv_mask));
-    if (newly_mask) {
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(&cnt->n_newly, (uint32_t)__popcll(newly_mask));
-        base = __shfl(base, 0);
-        if (newly) {
-            const uint32_t below = (uint32_t)__popcll(newly_mask & ((1ull << lane) - 1ull));
-            cull.newly_list[base + below] = i;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        s_cnt[wave][0] = (uint32_t)__popcll(surv_mask);
+        s_cnt[wave][1] = (uint32_t)__popcll(newly_mask);
+    }
+    __syncthreads();
+    if (threadIdx.x < 2)
+        rec.partial[2 * blockIdx.x + threadIdx.x] = s_cnt[0][threadIdx.x] + s_cnt[1][threadIdx.x] +
+                                                    s_cnt[2][threadIdx.x] + s_cnt[3][threadIdx.x];
+    (void)cnt;
+}
+
+__global__ __launch_bounds__(1024) void sum_partials_kernel(int n_blocks, const uint32_t *partial,
+                                                            Counters *cnt) {
+    __shared__ uint32_t s_sum[16][2];
+    uint32_t a = 0, b = 0;
+    for (int k = threadIdx.x; k < n_blocks; k += 1024) {
+        a += partial[2 * k];
+        b += partial[2 * k + 1];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        a += __shfl_xor(a, o);
+        b += __shfl_xor(b, o);
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        s_sum[wave][0] = a;
+        s_sum[wave][1] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t sa = 0, sb = 0;
+        for (int w = 0; w < 16; ++w) {
+            sa += s_sum[w][0];
+            sb += s_sum[w][1];
         }
+        cnt->n_survivors = sa;
+        cnt->n_newly = sb;
     }
 }
 
@@ -207,13 +237,14 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
                        Counters *cnt, hipStream_t st) {
     if (s.n <= 0) return;
-    const dim3 grid((s.n + 255) / 256), block(256);
+    const dim3 grid(preprocess_blocks(s.n)), block(256);
     switch (s.deg) {
         case 0: preprocess_kernel<0><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
         case 1: preprocess_kernel<1><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
         case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
         default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
     }
+    sum_partials_kernel<<<1, 1024, 0, st>>>((int)grid.x, rec.partial, cnt);
 }
 
 }  // namespace tgs

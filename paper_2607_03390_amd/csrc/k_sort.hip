@@ -8,16 +8,19 @@
 // of the 64-bit (tile, depth) keys, at a third of the HBM traffic (the depth
 // passes run over the Gaussians, not over their tile copies).
 //
-// Onesweep structure for gfx950: one histogram kernel counts every pass's
-// digits at once; then one kernel per pass ranks a 3840-key partition in LDS
-// and resolves its global digit offsets by decoupled look-back over the
-// preceding partitions.  Partitions are numbered by an atomic ticket taken on
-// entry, so a block only waits on partitions that are already running.
-// Ranking is stable (a wave's 64-lane match over the digit bits plus per-wave
-// digit counters in input order).  Keys are staged in LDS in digit order
-// before the scatter so that writes of one digit run are contiguous.
-// The key count may live on the device (grid sized for an upper bound;
-// partitions past the count leave at once), so no host round trip is needed.
+// Structure for gfx950: one histogram kernel counts every pass's digits at
+// once (the global digit bases); then, per pass, an upsweep kernel counts
+// each 3840-key partition's digits, a column scan turns those counts into
+// per-(digit, partition) output offsets, and a downsweep kernel ranks each
+// partition in LDS and scatters it.  No block ever waits on another and no
+// device-wide atomic is contended (same-address atomics serialise across the
+// eight XCDs), so the sort is deterministic and needs no forward-progress
+// assumption.  Ranking is stable (a wave's 64-lane match over the digit bits
+// plus per-wave digit counters in input order).  Keys are staged in LDS in
+// digit order before the scatter so that writes of one digit run are
+// contiguous.  The key count may live on the device (grids sized for an upper
+// bound; partitions past the count do no work), so no host round trip is
+// needed.
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -30,16 +33,6 @@ constexpr int kSortWaveItems = 64 * kSortIpt;
 constexpr int kSortTile = kSortThreads * kSortIpt;   // 3840 keys per partition
 constexpr int kRadix = 256;
 constexpr int kMaxPasses = 4;
-constexpr uint32_t kFlagAgg = 1u << 30;
-constexpr uint32_t kFlagInc = 2u << 30;
-constexpr uint32_t kValMask = (1u << 30) - 1;
-
-__device__ inline uint32_t ld_agent(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void st_agent(uint32_t *p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 __device__ inline uint32_t key_count(const uint32_t *n_dev, uint32_t n_host) {
     return n_dev ? *n_dev : n_host;
@@ -89,26 +82,76 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const uint32_t *keys, co
     }
 }
 
-__global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
+// Digit counts of one partition: counts[d * np + part].
+__global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(const uint32_t *__restrict__ kin,
+                                                                    const uint32_t *n_dev,
+                                                                    uint32_t n_host, int shift,
+                                                                    uint32_t np, uint32_t *counts) {
+    __shared__ uint32_t s_h[4][kRadix];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int k = tid; k < 4 * kRadix; k += kSortThreads) (&s_h[0][0])[k] = 0u;
+    __syncthreads();
+    const uint32_t K = key_count(n_dev, n_host);
+    const uint32_t part = blockIdx.x;
+    const uint32_t wbase = part * (uint32_t)kSortTile + (uint32_t)wave * kSortWaveItems;
+#pragma unroll
+    for (int j = 0; j < kSortIpt; ++j) {
+        const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
+        if (idx < K) atomicAdd(&s_h[wave][(kin[idx] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    counts[(size_t)tid * np + part] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
+}
+
+// One block per digit: exclusive scan of the digit's counts over partitions,
+// offset by the digit's global base (exclusive prefix of the histogram).
+__global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *hist, uint32_t np,
+                                                           uint32_t *counts) {
+    __shared__ uint32_t s_scan[4];
+    __shared__ uint32_t s_base;
+    const int d = blockIdx.x;
+    const uint32_t hv = threadIdx.x < d ? hist[threadIdx.x] : 0u;
+    uint32_t base = hv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) base += __shfl_xor(base, o);
+    if ((threadIdx.x & 63) == 0) s_scan[threadIdx.x >> 6] = base;
+    __syncthreads();
+    if (threadIdx.x == 0) s_base = s_scan[0] + s_scan[1] + s_scan[2] + s_scan[3];
+    __syncthreads();
+    uint32_t run = s_base;
+    uint32_t *col = counts + (size_t)d * np;
+    for (uint32_t c = 0; c < np; c += 256) {
+        const uint32_t p = c + threadIdx.x;
+        const uint32_t v = p < np ? col[p] : 0u;
+        __syncthreads();
+        const uint32_t ex = block_exclusive_scan256(v, s_scan);
+        if (p < np) col[p] = run + ex;
+        // block total = last exclusive + last value, broadcast through LDS
+        if (threadIdx.x == 255) s_base = run + ex + v;
+        __syncthreads();
+        run = s_base;
+    }
+}
+
+__global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
-    uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift,
-    const uint32_t *hist, uint32_t *status, uint32_t *ticket) {
+    uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
+    const uint32_t *__restrict__ offsets) {
     __shared__ uint32_t s_keys[kSortTile];
     __shared__ uint32_t s_vals[kSortTile];
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
     __shared__ uint32_t s_dstart[kRadix];     // block-local start of each digit
     __shared__ uint32_t s_gbase[kRadix];      // global start of this block's digit run
     __shared__ uint32_t s_scan[4];
-    __shared__ uint32_t s_part;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) s_part = atomicAdd(ticket, 1u);
-    for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
-    __syncthreads();
     const uint32_t K = key_count(n_dev, n_host);
-    const uint32_t part = s_part;
+    const uint32_t part = blockIdx.x;
     const uint32_t base = part * (uint32_t)kSortTile;
-    if (base >= K) return;   // past the keys: later partitions leave as well
+    if (base >= K) return;   // block-uniform
+    for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
+    s_gbase[tid] = offsets[(size_t)tid * np + part];
+    __syncthreads();
     const uint32_t wbase = base + (uint32_t)wave * kSortWaveItems;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
 
@@ -152,29 +195,6 @@ __global__ __launch_bounds__(kSortThreads) void sort_pass_kernel(
     s_wh[2 * kRadix + d] = c0 + c1;
     s_wh[3 * kRadix + d] = c0 + c1 + c2;
     s_dstart[d] = block_exclusive_scan256(total, s_scan);
-    const uint32_t hex = block_exclusive_scan256(hist[d], s_scan);
-
-    uint32_t excl = 0;
-    uint32_t *mine = status + (size_t)part * kRadix + d;
-    if (part == 0) {
-        st_agent(mine, kFlagInc | total);
-    } else {
-        st_agent(mine, kFlagAgg | total);
-        int p = (int)part - 1;
-        while (true) {
-            const uint32_t w = ld_agent(status + (size_t)p * kRadix + d);
-            const uint32_t flag = w & ~kValMask;
-            if (flag == 0u) {
-                __builtin_amdgcn_s_sleep(1);
-                continue;
-            }
-            excl += w & kValMask;
-            if (flag == kFlagInc) break;
-            --p;
-        }
-        st_agent(mine, kFlagInc | (excl + total));
-    }
-    s_gbase[d] = hex + excl;
     __syncthreads();
 
 #pragma unroll
@@ -206,8 +226,9 @@ inline uint32_t n_partitions(uint32_t K) { return (K + kSortTile - 1) / kSortTil
 int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
 
 size_t sort_scratch_words(uint32_t max_keys, int passes) {
-    return (size_t)kMaxPasses * kRadix + kMaxPasses +
-           (size_t)passes * (n_partitions(max_keys) + 1) * kRadix;
+    // histogram of every pass + one (digit x partition) offset table
+    (void)passes;
+    return (size_t)kMaxPasses * kRadix + (size_t)kRadix * (n_partitions(max_keys) + 1);
 }
 
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
@@ -216,18 +237,17 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
     if (n_max <= 1 || passes <= 0) return 0;
     const uint32_t np = n_partitions(n_max);
     uint32_t *hist = scratch;
-    uint32_t *tickets = scratch + kMaxPasses * kRadix;
-    uint32_t *status = tickets + kMaxPasses;
-    const size_t words = sort_scratch_words(n_max, passes);
-    const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
-    sort_clear_kernel<<<clear_blocks, 256, 0, st>>>(scratch, words);
-    const int hist_blocks = (int)(np < 1024 ? np : 1024);
+    uint32_t *table = scratch + kMaxPasses * kRadix;
+    sort_clear_kernel<<<1, 256, 0, st>>>(hist, (size_t)kMaxPasses * kRadix);
+    const int hist_blocks = (int)(np < 128 ? np : 128);   // few blocks: few atomics per bin
     sort_hist_kernel<<<hist_blocks, 256, 0, st>>>(keys, n_dev, n_max, begin_bit, passes, hist);
     uint32_t *ki = keys, *ko = keys_alt, *vi = vals, *vo = vals_alt;
     for (int p = 0; p < passes; ++p) {
-        sort_pass_kernel<<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, n_dev, n_max,
-                                                      begin_bit + 8 * p, hist + p * kRadix,
-                                                      status + (size_t)p * np * kRadix, tickets + p);
+        const int shift = begin_bit + 8 * p;
+        sort_upsweep_kernel<<<np, kSortThreads, 0, st>>>(ki, n_dev, n_max, shift, np, table);
+        sort_colscan_kernel<<<kRadix, 256, 0, st>>>(hist + p * kRadix, np, table);
+        sort_downsweep_kernel<<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, n_dev, n_max, shift, np,
+                                                           table);
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }

@@ -7,8 +7,8 @@
 //    block per tile with a block-wide OR;
 //  - occluded tiles of the newly visible Gaussians, one wave per
 //    (Gaussian, tile) pair with a wave ballot over the tile's 256 pixels;
-//  - tile selection and compaction (one block), including per-row prefix
-//    sums of the mask used by the key counts;
+//  - tile selection and compaction, one block per tile row, including the
+//    per-row prefix sums of the mask used by the key counts;
 //  - stitching of the warped reference image into the tiles that are not
 //    re-rendered (Eq. 4, bilinear).
 // All of these are HBM- or latency-bound; none is a dense contraction.
@@ -104,41 +104,50 @@ __global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *_
     if (threadIdx.x == 0) um[tile] = (uint8_t)(any ? 1 : 0);
 }
 
-__global__ __launch_bounds__(256) void occluded_kernel(WarpK w, const int *__restrict__ newly_list,
-                                                       const Counters *cnt, const float4 *g0,
-                                                       const float4 *g1, const ushort4 *rect,
-                                                       uint8_t *oc) {
+// Each wave scans 64 status bytes at a time; for every newly visible
+// Gaussian among them the whole wave tests its rectangle's tiles, four pixel
+// centres per lane, with a ballot per tile.
+__global__ __launch_bounds__(256) void occluded_kernel(WarpK w, int n,
+                                                       const uint8_t *__restrict__ status,
+                                                       const float4 *g0, const float4 *g1,
+                                                       const ushort4 *rect, uint8_t *oc) {
     const int lane = threadIdx.x & 63;
-    const uint32_t wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-    const uint32_t n_waves = (gridDim.x * blockDim.x) >> 6;
-    const uint32_t n_newly = cnt->n_newly;
-    for (uint32_t e = wave; e < n_newly; e += n_waves) {
-        const int i = newly_list[e];
-        const ushort4 r = rect[i];
-        if (r.x > r.z || r.y > r.w) continue;
-        const float4 a = g0[i];
-        const float4 b = g1[i];
-        for (int ty = r.y; ty <= r.w; ++ty)
-            for (int tx = r.x; tx <= r.z; ++tx) {
-                float amax = 0.0f;
+    const int wave = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+    const int n_waves = (int)((gridDim.x * blockDim.x) >> 6);
+    for (int base = wave * 64; base < n; base += n_waves * 64) {
+        const int me = base + lane;
+        const bool nv = me < n && (status[me] & 2u);
+        uint64_t todo = __ballot(nv);
+        while (todo) {
+            const int l = __ffsll((unsigned long long)todo) - 1;
+            todo &= todo - 1ull;
+            const int i = base + l;
+            const ushort4 r = rect[i];
+            if (r.x > r.z || r.y > r.w) continue;
+            const float4 a = g0[i];
+            const float4 b = g1[i];
+            for (int ty = r.y; ty <= r.w; ++ty)
+                for (int tx = r.x; tx <= r.z; ++tx) {
+                    float amax = 0.0f;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int p = lane + 64 * k;
-                    const int x = tx * kTile + (p & 15), y = ty * kTile + (p >> 4);
-                    if (x < w.W && y < w.H) {
-                        const float dx = a.x - (float)x, dy = a.y - (float)y;
-                        const float power = -0.5f * (a.z * dx * dx + b.x * dy * dy) - a.w * dx * dy;
-                        if (!(power > 0.0f))
-                            amax = fmaxf(amax, fminf(kAlphaMax, b.y * __expf(power)));
+                    for (int k = 0; k < 4; ++k) {
+                        const int p = lane + 64 * k;
+                        const int x = tx * kTile + (p & 15), y = ty * kTile + (p >> 4);
+                        if (x < w.W && y < w.H) {
+                            const float dx = a.x - (float)x, dy = a.y - (float)y;
+                            const float power = -0.5f * (a.z * dx * dx + b.x * dy * dy) - a.w * dx * dy;
+                            if (!(power > 0.0f))
+                                amax = fmaxf(amax, fminf(kAlphaMax, b.y * __expf(power)));
+                        }
                     }
+                    const uint64_t hit = __ballot(!(amax < kAlphaMin));
+                    if (hit != 0ull && lane == 0) oc[ty * w.TX + tx] = 1;
                 }
-                const uint64_t hit = __ballot(!(amax < kAlphaMin));
-                if (hit != 0ull && lane == 0) oc[ty * w.TX + tx] = 1;
-            }
+        }
     }
 }
 
-__device__ inline uint32_t block_exclusive_scan1024(uint32_t v, uint32_t *s_wave, uint32_t *total) {
+__device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave, uint32_t *total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t inc = v;
 #pragma unroll
@@ -149,7 +158,8 @@ __device__ inline uint32_t block_exclusive_scan1024(uint32_t v, uint32_t *s_wave
     if (lane == 63) s_wave[wave] = inc;
     __syncthreads();
     uint32_t off = 0, tot = 0;
-    for (int x = 0; x < 16; ++x) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
         const uint32_t c = s_wave[x];
         if (x < wave) off += c;
         tot += c;
@@ -159,37 +169,53 @@ __device__ inline uint32_t block_exclusive_scan1024(uint32_t v, uint32_t *s_wave
     return off + inc - v;
 }
 
-__global__ __launch_bounds__(1024) void select_kernel(int TX, int TY, int mode, const uint8_t *oc,
-                                                      const uint8_t *um, uint8_t *sel,
-                                                      int *sel_list, uint32_t *rowpre,
-                                                      uint8_t *mask_out, Counters *cnt) {
-    __shared__ uint32_t s_wave[16];
-    const int n_tiles = TX * TY;
-    uint32_t running = 0;
-    for (int c = 0; c < n_tiles; c += 1024) {
-        const int t = c + threadIdx.x;
+// One block per tile row: selected = occluded | unmatched (or every tile),
+// and the row's exclusive prefix sums rowpre[ty][0..TX] (rowpre[ty][TX] is the
+// row's count).
+__global__ __launch_bounds__(256) void select_rows_kernel(int TX, int mode, const uint8_t *oc,
+                                                          const uint8_t *um, uint8_t *sel,
+                                                          uint32_t *rowpre, uint8_t *mask_out) {
+    __shared__ uint32_t s_wave[4];
+    const int ty = blockIdx.x;
+    uint32_t *row = rowpre + (size_t)ty * (TX + 1);
+    uint32_t run = 0;
+    for (int c = 0; c < TX; c += 256) {
+        const int x = c + threadIdx.x;
+        const int t = ty * TX + x;
         uint32_t s = 0;
-        if (t < n_tiles) {
+        if (x < TX) {
             s = mode ? 1u : (uint32_t)(oc[t] | um[t]);
             sel[t] = (uint8_t)s;
             if (mask_out) mask_out[t] = (uint8_t)s;
         }
         uint32_t tot;
-        const uint32_t ex = block_exclusive_scan1024(s, s_wave, &tot);
-        if (s) sel_list[running + ex] = t;
-        running += tot;
+        const uint32_t ex = block_exclusive_scan256(s, s_wave, &tot);
+        if (x < TX) row[x] = run + ex;
+        run += tot;
     }
-    if (threadIdx.x == 0) cnt->n_selected = running;
-    for (int ty = threadIdx.x; ty < TY; ty += 1024) {
-        uint32_t acc = 0;
-        uint32_t *row = rowpre + (size_t)ty * (TX + 1);
-        for (int x = 0; x < TX; ++x) {
-            row[x] = acc;
-            const int t = ty * TX + x;
-            acc += mode ? 1u : (uint32_t)(oc[t] | um[t]);
-        }
-        row[TX] = acc;
+    if (threadIdx.x == 0) row[TX] = run;
+}
+
+// One block per tile row: the ascending list of selected tiles; the last row
+// also stores the total.
+__global__ __launch_bounds__(256) void select_list_kernel(int TX, int TY, const uint8_t *sel,
+                                                          const uint32_t *rowpre, int *sel_list,
+                                                          Counters *cnt) {
+    __shared__ uint32_t s_sum[4];
+    const int ty = blockIdx.x;
+    uint32_t part = 0;
+    for (int r = threadIdx.x; r < ty; r += 256) part += rowpre[(size_t)r * (TX + 1) + TX];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
+    if ((threadIdx.x & 63) == 0) s_sum[threadIdx.x >> 6] = part;
+    __syncthreads();
+    const uint32_t off = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
+    const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
+    for (int x = threadIdx.x; x < TX; x += 256) {
+        const int t = ty * TX + x;
+        if (sel[t]) sel_list[off + row[x]] = t;
     }
+    if (ty == TY - 1 && threadIdx.x == 0) cnt->n_selected = off + row[TX];
 }
 
 __global__ __launch_bounds__(256) void stitch_kernel(WarpK w, const uint8_t *sel,
@@ -256,15 +282,19 @@ void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *
     fill_query_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, dmin, dfill, uv, um);
 }
 
-void launch_occluded(const WarpK &w, const int *newly_list, const Counters *cnt, const float4 *g0,
+void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g0,
                      const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st) {
-    occluded_kernel<<<512, 256, 0, st>>>(w, newly_list, cnt, g0, g1, rect, oc);
+    if (n <= 0) return;
+    int blocks = (n + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    occluded_kernel<<<blocks, 256, 0, st>>>(w, n, status, g0, g1, rect, oc);
 }
 
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
                    int *sel_list, uint32_t *rowpre, uint8_t *mask_out, Counters *cnt,
                    hipStream_t st) {
-    select_kernel<<<1, 1024, 0, st>>>(TX, TY, mode, oc, um, sel, sel_list, rowpre, mask_out, cnt);
+    select_rows_kernel<<<TY, 256, 0, st>>>(TX, mode, oc, um, sel, rowpre, mask_out);
+    select_list_kernel<<<TY, 256, 0, st>>>(TX, TY, sel, rowpre, sel_list, cnt);
 }
 
 void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,

@@ -75,7 +75,7 @@ struct DevBuf {
 
 // Per-frame scratch of one render path (a scene's tgs_render_full, or a state).
 struct Workspace {
-    DevBuf g0, g1, col, rect, status, count, newly;
+    DevBuf g0, g1, col, rect, status, count, partial;
     DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
     DevBuf ranges, sel, sel_list, rowpre, cnt;
@@ -102,7 +102,7 @@ struct Workspace {
             TGS_TRY(rect.ensure(nn * sizeof(ushort4)));
             TGS_TRY(status.ensure(nn));
             TGS_TRY(count.ensure((nn + 4) * sizeof(uint32_t)));
-            TGS_TRY(newly.ensure(nn * sizeof(int)));
+            TGS_TRY(partial.ensure((size_t)(2 * preprocess_blocks(n_ > 0 ? n_ : 1)) * sizeof(uint32_t)));
             TGS_TRY(dkey.ensure(nn * sizeof(uint32_t)));
             TGS_TRY(didx.ensure(nn * sizeof(uint32_t)));
             TGS_TRY(dkey_alt.ensure(nn * sizeof(uint32_t)));
@@ -145,8 +145,9 @@ struct Workspace {
     }
 
     Records records() const {
-        return Records{g0.as<float4>(),    g1.as<float4>(),   col.as<float4>(),
-                       rect.as<ushort4>(), status.as<uint8_t>(), count.as<uint32_t>()};
+        return Records{g0.as<float4>(),      g1.as<float4>(),       col.as<float4>(),
+                       rect.as<ushort4>(),   status.as<uint8_t>(),  count.as<uint32_t>(),
+                       partial.as<uint32_t>()};
     }
 };
 
@@ -426,7 +427,6 @@ BlendArgs blend_args(const Workspace &ws, int W, int H, const uint32_t *vals) {
 CullK no_cull(float z_near, Workspace &ws) {
     CullK c{};
     c.z_near = z_near;
-    c.newly_list = ws.newly.as<int>();
     c.lambda1 = 3.0f;
     return c;
 }
@@ -770,7 +770,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
         {
             ProfScope ps(TGS_PROF_OCCLUDED, st);
-            launch_occluded(w, ws.newly.as<int>(), ws.cnt.as<Counters>(), ws.g0.as<float4>(),
+            launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g0.as<float4>(),
                             ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
             TGS_LAUNCHED("occluded tiles");
         }

@@ -43,6 +43,7 @@ struct Records {
     ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
     uint8_t *status;          // bit0 survivor, bit1 newly visible
     uint32_t *count;          // keys of the Gaussian (tiles of its rectangle)
+    uint32_t *partial;        // per 256-Gaussian block: survivors, newly visible
 };
 
 // Temporal dynamic culling inputs of the preprocess.
@@ -53,7 +54,6 @@ struct CullK {
     const float *dmin, *smax; // warped TGB
     const uint8_t *g_rendered;
     float lambda1, lambda2;
-    int *newly_list;          // appended indices of newly visible Gaussians
 };
 
 // Frame counters on the device (read back once per frame).
@@ -77,8 +77,11 @@ __device__ inline float ordered_to_float(int i) {
 }
 
 // ---- launchers (k_preprocess.hip) ----
+// Writes the records and, per 256-Gaussian block, the survivor and
+// newly-visible counts; a second small kernel sums those into cnt.
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
                        Counters *cnt, hipStream_t st);
+inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
 // ---- launchers (k_keys.hip) ----
 size_t scan_scratch_bytes(int n);
@@ -138,7 +141,7 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
                          hipStream_t st);
 void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
                        hipStream_t st);
-void launch_occluded(const WarpK &w, const int *newly_list, const Counters *cnt, const float4 *g0,
+void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g0,
                      const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st);
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
                    int *sel_list, uint32_t *rowpre, uint8_t *mask_out, Counters *cnt,
