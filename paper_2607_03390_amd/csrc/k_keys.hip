@@ -64,15 +64,32 @@ __device__ inline uint64_t block_exclusive_scan64(uint64_t v, uint64_t *s_wave, 
 
 // The two scans of a frame are reduce-then-scan: per-block sums, one block
 // scanning the sums, then a downsweep that recomputes the local values.
-// Item j of block b is element b*4096 + j*256 + threadIdx.x (coalesced).
+// Thread t of block b owns the 16 consecutive elements b*4096 + 16t + j, read
+// with 16-byte loads; one block scan per block.
 
 // MODE 0: flags (count[i] > 0) over Gaussians i < n (n on the host).
 // MODE 1: key counts count[didx[s]] over sorted positions s < cnt->n_visible.
 template <int MODE>
-__device__ inline uint32_t scan_value(uint32_t e, int n, const uint32_t *count, const uint32_t *didx,
-                                      const Counters *cnt) {
-    if (MODE == 0) return (e < (uint32_t)n && count[e] > 0u) ? 1u : 0u;
-    return e < cnt->n_visible ? count[didx[e]] : 0u;
+__device__ inline void load16(uint32_t first, int n, const uint32_t *count, const uint32_t *didx,
+                              const Counters *cnt, uint32_t v[kScanItems]) {
+    const uint32_t lim = MODE == 0 ? (uint32_t)n : cnt->n_visible;
+    const uint32_t *src = MODE == 0 ? count : didx;
+    if (first + kScanItems <= lim) {
+#pragma unroll
+        for (int j = 0; j < kScanItems; j += 4) {
+            const uint4 q = *reinterpret_cast<const uint4 *>(src + first + j);
+            v[j] = q.x; v[j + 1] = q.y; v[j + 2] = q.z; v[j + 3] = q.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) v[j] = first + j < lim ? src[first + j] : 0xffffffffu;
+    }
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        if (first + j >= lim) v[j] = 0u;
+        else if (MODE == 0) v[j] = v[j] > 0u ? 1u : 0u;
+        else v[j] = count[v[j]];
+    }
 }
 
 template <int MODE>
@@ -80,11 +97,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(int n, const 
                                                                    const uint32_t *didx,
                                                                    const Counters *cnt,
                                                                    uint64_t *block_sums) {
-    const uint32_t base = blockIdx.x * (uint32_t)kScanTile;
+    uint32_t v[kScanItems];
+    load16<MODE>(blockIdx.x * (uint32_t)kScanTile + threadIdx.x * kScanItems, n, count, didx, cnt, v);
     uint64_t sum = 0;
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j)
-        sum += scan_value<MODE>(base + j * kScanThreads + threadIdx.x, n, count, didx, cnt);
+    for (int j = 0; j < kScanItems; ++j) sum += v[j];
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
     __shared__ uint64_t s_sum[4];
@@ -144,22 +161,40 @@ __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(int n, const ui
                                                                  const float4 *g1, uint32_t *out_a,
                                                                  uint32_t *out_b) {
     __shared__ uint64_t s_wave[4];
-    const uint32_t base = blockIdx.x * (uint32_t)kScanTile;
-    uint64_t run = block_sums[blockIdx.x];
-    for (int j = 0; j < kScanItems; ++j) {
-        const uint32_t e = base + j * kScanThreads + threadIdx.x;
-        const uint32_t v = scan_value<MODE>(e, n, count, didx, cnt);
-        uint64_t tot;
-        const uint64_t ex = block_exclusive_scan64(v, s_wave, &tot);
-        if (MODE == 0) {
-            if (v) {
-                out_a[run + ex] = __float_as_uint(g1[e].z);
-                out_b[run + ex] = e;
+    const uint32_t first = blockIdx.x * (uint32_t)kScanTile + threadIdx.x * kScanItems;
+    uint32_t v[kScanItems];
+    load16<MODE>(first, n, count, didx, cnt, v);
+    uint64_t local = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) local += v[j];
+    uint64_t tot;
+    uint64_t run = block_sums[blockIdx.x] + block_exclusive_scan64(local, s_wave, &tot);
+    if (MODE == 0) {
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            if (v[j]) {
+                out_a[run] = __float_as_uint(g1[first + j].z);
+                out_b[run] = first + j;
+                ++run;
             }
-        } else if (e < cnt->n_visible) {
-            out_a[e] = (uint32_t)(run + ex);
         }
-        run += tot;
+    } else {
+        const uint32_t lim = cnt->n_visible;
+        uint32_t o[kScanItems];
+#pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            o[j] = (uint32_t)run;
+            run += v[j];
+        }
+        if (first + kScanItems <= lim) {
+#pragma unroll
+            for (int j = 0; j < kScanItems; j += 4)
+                *reinterpret_cast<uint4 *>(out_a + first + j) = make_uint4(o[j], o[j + 1], o[j + 2], o[j + 3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < kScanItems; ++j)
+                if (first + j < lim) out_a[first + j] = o[j];
+        }
     }
 }
 

@@ -8,11 +8,11 @@
 // of the 64-bit (tile, depth) keys, at a third of the HBM traffic (the depth
 // passes run over the Gaussians, not over their tile copies).
 //
-// Structure for gfx950: one histogram kernel counts every pass's digits at
-// once (the global digit bases); then, per pass, an upsweep kernel counts
-// each 3840-key partition's digits, a column scan turns those counts into
-// per-(digit, partition) output offsets, and a downsweep kernel ranks each
-// partition in LDS and scatters it.  No block ever waits on another and no
+// Structure for gfx950, per 8-bit pass: an upsweep kernel counts each
+// 3840-key partition's digits, a column scan turns those counts into
+// per-(digit, partition) offsets and digit totals, and a downsweep kernel
+// ranks each partition in LDS and scatters it (the digit bases are a block
+// scan of the 256 totals).  No block ever waits on another and no
 // device-wide atomic is contended (same-address atomics serialise across the
 // eight XCDs), so the sort is deterministic and needs no forward-progress
 // assumption.  Ranking is stable (a wave's 64-lane match over the digit bits
@@ -32,7 +32,6 @@ constexpr int kSortIpt = 15;
 constexpr int kSortWaveItems = 64 * kSortIpt;
 constexpr int kSortTile = kSortThreads * kSortIpt;   // 3840 keys per partition
 constexpr int kRadix = 256;
-constexpr int kMaxPasses = 4;
 
 __device__ inline uint32_t key_count(const uint32_t *n_dev, uint32_t n_host) {
     return n_dev ? *n_dev : n_host;
@@ -56,32 +55,6 @@ __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave)
     return off + inc - v;
 }
 
-__global__ __launch_bounds__(256) void sort_clear_kernel(uint32_t *p, size_t n) {
-    for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n;
-         k += (size_t)gridDim.x * blockDim.x)
-        p[k] = 0u;
-}
-
-__global__ __launch_bounds__(256) void sort_hist_kernel(const uint32_t *keys, const uint32_t *n_dev,
-                                                        uint32_t n_host, int begin_bit, int passes,
-                                                        uint32_t *hist) {
-    __shared__ uint32_t s_h[4][kMaxPasses * kRadix];
-    const int wave = threadIdx.x >> 6;
-    for (int k = threadIdx.x; k < 4 * kMaxPasses * kRadix; k += blockDim.x) (&s_h[0][0])[k] = 0u;
-    __syncthreads();
-    const uint32_t K = key_count(n_dev, n_host);
-    for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
-        const uint32_t key = keys[k];
-        for (int p = 0; p < passes; ++p)
-            atomicAdd(&s_h[wave][p * kRadix + ((key >> (begin_bit + 8 * p)) & 255u)], 1u);
-    }
-    __syncthreads();
-    for (int b = threadIdx.x; b < passes * kRadix; b += blockDim.x) {
-        const uint32_t c = s_h[0][b] + s_h[1][b] + s_h[2][b] + s_h[3][b];
-        if (c) atomicAdd(&hist[b], c);
-    }
-}
-
 // Digit counts of one partition: counts[d * np + part].
 __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(const uint32_t *__restrict__ kin,
                                                                     const uint32_t *n_dev,
@@ -103,40 +76,32 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(const uint32
     counts[(size_t)tid * np + part] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
 }
 
-// One block per digit: exclusive scan of the digit's counts over partitions,
-// offset by the digit's global base (exclusive prefix of the histogram).
-__global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *hist, uint32_t np,
-                                                           uint32_t *counts) {
+// One block per digit: exclusive scan of the digit's counts over partitions
+// (in place) and the digit's total.
+__global__ __launch_bounds__(256) void sort_colscan_kernel(uint32_t np, uint32_t *counts,
+                                                           uint32_t *totals) {
     __shared__ uint32_t s_scan[4];
-    __shared__ uint32_t s_base;
+    __shared__ uint32_t s_run;
     const int d = blockIdx.x;
-    const uint32_t hv = threadIdx.x < d ? hist[threadIdx.x] : 0u;
-    uint32_t base = hv;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) base += __shfl_xor(base, o);
-    if ((threadIdx.x & 63) == 0) s_scan[threadIdx.x >> 6] = base;
-    __syncthreads();
-    if (threadIdx.x == 0) s_base = s_scan[0] + s_scan[1] + s_scan[2] + s_scan[3];
-    __syncthreads();
-    uint32_t run = s_base;
+    uint32_t run = 0;
     uint32_t *col = counts + (size_t)d * np;
     for (uint32_t c = 0; c < np; c += 256) {
         const uint32_t p = c + threadIdx.x;
         const uint32_t v = p < np ? col[p] : 0u;
-        __syncthreads();
         const uint32_t ex = block_exclusive_scan256(v, s_scan);
         if (p < np) col[p] = run + ex;
-        // block total = last exclusive + last value, broadcast through LDS
-        if (threadIdx.x == 255) s_base = run + ex + v;
+        if (threadIdx.x == 255) s_run = run + ex + v;
         __syncthreads();
-        run = s_base;
+        run = s_run;
+        __syncthreads();
     }
+    if (threadIdx.x == 0) totals[d] = run;
 }
 
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
     uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
-    const uint32_t *__restrict__ offsets) {
+    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ totals) {
     __shared__ uint32_t s_keys[kSortTile];
     __shared__ uint32_t s_vals[kSortTile];
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
@@ -150,7 +115,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t base = part * (uint32_t)kSortTile;
     if (base >= K) return;   // block-uniform
     for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
-    s_gbase[tid] = offsets[(size_t)tid * np + part];
+    // global start of digit tid: digits below it, then partitions before this one
+    s_gbase[tid] = block_exclusive_scan256(totals[tid], s_scan) + offsets[(size_t)tid * np + part];
     __syncthreads();
     const uint32_t wbase = base + (uint32_t)wave * kSortWaveItems;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
@@ -226,9 +192,9 @@ inline uint32_t n_partitions(uint32_t K) { return (K + kSortTile - 1) / kSortTil
 int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
 
 size_t sort_scratch_words(uint32_t max_keys, int passes) {
-    // histogram of every pass + one (digit x partition) offset table
+    // digit totals + one (digit x partition) offset table, reused by every pass
     (void)passes;
-    return (size_t)kMaxPasses * kRadix + (size_t)kRadix * (n_partitions(max_keys) + 1);
+    return (size_t)kRadix + (size_t)kRadix * (n_partitions(max_keys) + 1);
 }
 
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
@@ -236,18 +202,15 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
                     uint32_t *scratch, hipStream_t st) {
     if (n_max <= 1 || passes <= 0) return 0;
     const uint32_t np = n_partitions(n_max);
-    uint32_t *hist = scratch;
-    uint32_t *table = scratch + kMaxPasses * kRadix;
-    sort_clear_kernel<<<1, 256, 0, st>>>(hist, (size_t)kMaxPasses * kRadix);
-    const int hist_blocks = (int)(np < 128 ? np : 128);   // few blocks: few atomics per bin
-    sort_hist_kernel<<<hist_blocks, 256, 0, st>>>(keys, n_dev, n_max, begin_bit, passes, hist);
+    uint32_t *totals = scratch;
+    uint32_t *table = scratch + kRadix;
     uint32_t *ki = keys, *ko = keys_alt, *vi = vals, *vo = vals_alt;
     for (int p = 0; p < passes; ++p) {
         const int shift = begin_bit + 8 * p;
         sort_upsweep_kernel<<<np, kSortThreads, 0, st>>>(ki, n_dev, n_max, shift, np, table);
-        sort_colscan_kernel<<<kRadix, 256, 0, st>>>(hist + p * kRadix, np, table);
+        sort_colscan_kernel<<<kRadix, 256, 0, st>>>(np, table, totals);
         sort_downsweep_kernel<<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, n_dev, n_max, shift, np,
-                                                           table);
+                                                           table, totals);
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }
