@@ -207,12 +207,17 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
                           void *host, size_t *nbytes);
 
 /* Kernel timing for benchmarking.  Between tgs_profile_start and
- * tgs_profile_stop every launch of the library is bracketed by HIP events on
- * the stream it is enqueued on; stop synchronises the device and returns, per
- * stage, the summed event time and the number of launches.  With
- * count_pairs != 0 the blend kernels also count the (pixel, Gaussian) pairs
- * they evaluate (the blend's unit of work), which costs one add per pair.
- * Process-wide, not thread-safe; renders must not overlap with start/stop. */
+ * tgs_profile_stop the blend dispatches carry HIP start/stop events attached
+ * to the dispatch itself (no extra queue packets, so timing does not perturb
+ * the frame); with TGS_PROFILE_STAGES every other stage is also bracketed by
+ * separately recorded events on its stream (each such record adds a queue
+ * barrier of several microseconds: use it in untimed passes).  With
+ * TGS_PROFILE_COUNT_PAIRS the blend kernels also count the (pixel, Gaussian)
+ * list entries their pixels evaluate up to termination (the blend's unit of
+ * work).  tgs_profile_stop synchronises the device and returns, per stage,
+ * the summed event time and the number of timed launches.  Process-wide,
+ * not thread-safe; renders must not overlap with start/stop. */
+enum { TGS_PROFILE_COUNT_PAIRS = 1, TGS_PROFILE_STAGES = 2 };
 enum {
     TGS_PROF_PREPROCESS = 0,  /* per-Gaussian stage (incl. counter reset)     */
     TGS_PROF_SCAN = 1,        /* key counts + exclusive scan                  */
@@ -236,7 +241,7 @@ typedef struct {
     int64_t launches[TGS_PROF_STAGES];
     int64_t pairs[TGS_PROF_STAGES];   /* blend stages only, if counted        */
 } tgs_profile;
-tgs_status tgs_profile_start(int32_t count_pairs);
+tgs_status tgs_profile_start(int32_t flags);
 tgs_status tgs_profile_stop(tgs_profile *out);
 
 /* Message of the last failed call on this thread ("" if none). */

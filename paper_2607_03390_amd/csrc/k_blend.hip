@@ -17,6 +17,8 @@
 // cancellation of the unshifted form at large depths.  Gaussians that a wave
 // composites are flagged through a wave ballot, so the temporal Gaussian
 // buffer costs one scalar test per record and wave.
+#include <hip/hip_ext.h>
+
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -250,23 +252,26 @@ __global__ __launch_bounds__(64) void afc_final_kernel(const int *partial, int n
 }  // namespace
 
 template <bool CAPTURE, bool CONTRIB>
-void launch_blend_v(const BlendArgs &a, int n_blocks, hipStream_t st) {
+void launch_blend_v(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     if (a.pairs)
-        blend_kernel<CAPTURE, CONTRIB, true><<<n_blocks, 256, 0, st>>>(a);
+        hipExtLaunchKernelGGL(blend_kernel<CAPTURE, CONTRIB, true>, dim3(n_blocks), dim3(256), 0, st,
+                              e0, e1, 0, a);
     else
-        blend_kernel<CAPTURE, CONTRIB, false><<<n_blocks, 256, 0, st>>>(a);
+        hipExtLaunchKernelGGL(blend_kernel<CAPTURE, CONTRIB, false>, dim3(n_blocks), dim3(256), 0, st,
+                              e0, e1, 0, a);
 }
 
-void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st) {
+void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t start,
+                  hipEvent_t stop) {
     if (n_blocks <= 0) return;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma || a.g_flag ||
                          a.contrib;
     if (a.contrib)
-        launch_blend_v<true, true>(a, n_blocks, st);
+        launch_blend_v<true, true>(a, n_blocks, st, start, stop);
     else if (capture)
-        launch_blend_v<true, false>(a, n_blocks, st);
+        launch_blend_v<true, false>(a, n_blocks, st, start, stop);
     else
-        launch_blend_v<false, false>(a, n_blocks, st);
+        launch_blend_v<false, false>(a, n_blocks, st, start, stop);
 }
 
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,

@@ -114,12 +114,40 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(int n, const 
 // cnt->n_visible (MODE 0) or cnt->n_keys (MODE 1, saturated).
 template <int MODE>
 __global__ __launch_bounds__(1024) void scan_top_kernel(int nb, uint64_t *block_sums,
+                                                        const uint32_t *pre_partial, int n_pre,
                                                         Counters *cnt) {
     __shared__ uint64_t s_wave[16];
     __shared__ uint64_t s_carry;
+    __shared__ uint32_t s_pre[16][2];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (MODE == 0) {
+        // survivor and newly-visible counts of the preprocess blocks
+        uint32_t a = 0, b = 0;
+        for (int k = threadIdx.x; k < n_pre; k += 1024) {
+            a += pre_partial[2 * k];
+            b += pre_partial[2 * k + 1];
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            a += __shfl_xor(a, o);
+            b += __shfl_xor(b, o);
+        }
+        if (lane == 0) {
+            s_pre[wave][0] = a;
+            s_pre[wave][1] = b;
+        }
+    }
     if (threadIdx.x == 0) s_carry = 0;
     __syncthreads();
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (MODE == 0 && threadIdx.x == 0) {
+        uint32_t a = 0, b = 0;
+        for (int w = 0; w < 16; ++w) {
+            a += s_pre[w][0];
+            b += s_pre[w][1];
+        }
+        cnt->n_survivors = a;
+        cnt->n_newly = b;
+    }
     for (int c = 0; c < nb; c += 1024) {
         const int i = c + threadIdx.x;
         const uint64_t v = i < nb ? block_sums[i] : 0;
@@ -203,12 +231,15 @@ __global__ __launch_bounds__(256) void duplicate_kernel(uint32_t V, uint32_t K,
                                                         const uint32_t *__restrict__ didx,
                                                         const uint32_t *__restrict__ offs,
                                                         const ushort4 *__restrict__ rect,
-                                                        const uint32_t *rowpre, int TX,
-                                                        uint32_t *tkey, uint32_t *tval) {
+                                                        const uint32_t *rowpre, const int *sel_cols,
+                                                        int TX, int n_tiles, uint32_t *tkey,
+                                                        uint32_t *tval, uint2 *ranges) {
     __shared__ uint32_t s_off[4][64];
     __shared__ uint32_t s_g[4][64];
     __shared__ ushort4 s_rect[4][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < n_tiles; t += gridDim.x * blockDim.x)
+        ranges[t] = make_uint2(0u, 0u);
     const uint32_t w0 = (blockIdx.x * 4u + (uint32_t)wave) * 64u;
     if (w0 >= V) return;
     const uint32_t s = w0 + lane;
@@ -239,22 +270,15 @@ __global__ __launch_bounds__(256) void duplicate_kernel(uint32_t V, uint32_t K,
             ty = rc.y + (int)(r / w);
             tx = rc.x + (int)(r % w);
         } else {
+            // r-th selected tile of the rectangle, rows first: O(1) per row
             ty = rc.y;
-            for (;; ++ty) {
-                const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
+            const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
+            for (;; ++ty, row += TX + 1) {
                 const uint32_t c = row[rc.z + 1] - row[rc.x];
                 if (r < c) break;
                 r -= c;
             }
-            const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
-            const uint32_t b = row[rc.x];
-            int xl = rc.x, xh = rc.z;   // smallest x with row[x+1] - b > r
-            while (xl < xh) {
-                const int mid = (xl + xh) >> 1;
-                if (row[mid + 1] - b > r) xh = mid;
-                else xl = mid + 1;
-            }
-            tx = xl;
+            tx = sel_cols[(size_t)ty * TX + row[rc.x] + r];
         }
         tkey[p] = (uint32_t)(ty * TX + tx);
         tval[p] = s_g[wave][lo];
@@ -290,11 +314,13 @@ void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int
 }
 
 void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
-                          uint32_t *didx, void *scratch, Counters *cnt, hipStream_t st) {
+                          uint32_t *didx, void *scratch, const uint32_t *pre_partial,
+                          Counters *cnt, hipStream_t st) {
     const uint32_t nb = scan_parts((uint32_t)(n > 0 ? n : 1));
     uint64_t *sums = static_cast<uint64_t *>(scratch);
     scan_reduce_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums);
-    scan_top_kernel<0><<<1, 1024, 0, st>>>((int)nb, sums, cnt);
+    scan_top_kernel<0><<<1, 1024, 0, st>>>((int)nb, sums, pre_partial,
+                                           n > 0 ? preprocess_blocks(n) : 0, cnt);
     scan_down_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums, g1, dkey, didx);
 }
 
@@ -303,21 +329,24 @@ void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count
     const uint32_t nb = scan_parts((uint32_t)(n > 0 ? n : 1));
     uint64_t *sums = static_cast<uint64_t *>(scratch);
     scan_reduce_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums);
-    scan_top_kernel<1><<<1, 1024, 0, st>>>((int)nb, sums, cnt);
+    scan_top_kernel<1><<<1, 1024, 0, st>>>((int)nb, sums, nullptr, 0, cnt);
     scan_down_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums, nullptr, offs,
                                                      nullptr);
 }
 
 void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,
-                      const ushort4 *rect, const uint32_t *rowpre, int TX, uint32_t *tkey,
-                      uint32_t *tval, hipStream_t st) {
-    if (V == 0 || K == 0) return;
+                      const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
+                      int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st) {
+    if (V == 0 || K == 0) {
+        ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
+        return;
+    }
     const uint32_t waves = (V + 63) / 64;
-    duplicate_kernel<<<(waves + 3) / 4, 256, 0, st>>>(V, K, didx, offs, rect, rowpre, TX, tkey, tval);
+    duplicate_kernel<<<(waves + 3) / 4, 256, 0, st>>>(V, K, didx, offs, rect, rowpre, sel_cols, TX,
+                                                      n_tiles, tkey, tval, ranges);
 }
 
-void launch_ranges(uint32_t K, int n_tiles, const uint32_t *keys, uint2 *ranges, hipStream_t st) {
-    ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
+void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st) {
     if (K > 0) ranges_kernel<<<(K + 255) / 256, 256, 0, st>>>(K, keys, ranges);
 }
 

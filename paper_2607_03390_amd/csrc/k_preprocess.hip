@@ -202,36 +202,6 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
     (void)cnt;
 }
 
-__global__ __launch_bounds__(1024) void sum_partials_kernel(int n_blocks, const uint32_t *partial,
-                                                            Counters *cnt) {
-    __shared__ uint32_t s_sum[16][2];
-    uint32_t a = 0, b = 0;
-    for (int k = threadIdx.x; k < n_blocks; k += 1024) {
-        a += partial[2 * k];
-        b += partial[2 * k + 1];
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        a += __shfl_xor(a, o);
-        b += __shfl_xor(b, o);
-    }
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0) {
-        s_sum[wave][0] = a;
-        s_sum[wave][1] = b;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t sa = 0, sb = 0;
-        for (int w = 0; w < 16; ++w) {
-            sa += s_sum[w][0];
-            sb += s_sum[w][1];
-        }
-        cnt->n_survivors = sa;
-        cnt->n_newly = sb;
-    }
-}
-
 }  // namespace
 
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
@@ -244,7 +214,6 @@ void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Re
         case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
         default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
     }
-    sum_partials_kernel<<<1, 1024, 0, st>>>((int)grid.x, rec.partial, cnt);
 }
 
 }  // namespace tgs

@@ -126,8 +126,19 @@ __global__ __launch_bounds__(256) void occluded_kernel(WarpK w, int n,
             if (r.x > r.z || r.y > r.w) continue;
             const float4 a = g0[i];
             const float4 b = g1[i];
-            for (int ty = r.y; ty <= r.w; ++ty)
-                for (int tx = r.x; tx <= r.z; ++tx) {
+            if (!(b.y >= 0.999f * kAlphaMin)) continue;   // alpha < 1/255 everywhere
+            // tiles meeting the box of the alpha >= 1/255 ellipse (enlarged
+            // by 0.2% + 0.05 px): no pixel outside it can reach the threshold
+            const float kq = 2.0f * __logf(fmaxf(255.0f * b.y, 1.0f)) + 1e-3f;
+            const float det = a.z * b.x - a.w * a.w;
+            const float hx = sqrtf(kq * b.x / det) * 1.002f + 0.05f;
+            const float hy = sqrtf(kq * a.z / det) * 1.002f + 0.05f;
+            const int ex0 = max((int)r.x, (int)ceilf((a.x - hx - 15.0f) * 0.0625f));
+            const int ex1 = min((int)r.z, (int)floorf((a.x + hx) * 0.0625f));
+            const int ey0 = max((int)r.y, (int)ceilf((a.y - hy - 15.0f) * 0.0625f));
+            const int ey1 = min((int)r.w, (int)floorf((a.y + hy) * 0.0625f));
+            for (int ty = ey0; ty <= ey1; ++ty)
+                for (int tx = ex0; tx <= ex1; ++tx) {
                     float amax = 0.0f;
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
@@ -200,7 +211,7 @@ __global__ __launch_bounds__(256) void select_rows_kernel(int TX, int mode, cons
 // also stores the total.
 __global__ __launch_bounds__(256) void select_list_kernel(int TX, int TY, const uint8_t *sel,
                                                           const uint32_t *rowpre, int *sel_list,
-                                                          Counters *cnt) {
+                                                          int *sel_cols, Counters *cnt) {
     __shared__ uint32_t s_sum[4];
     const int ty = blockIdx.x;
     uint32_t part = 0;
@@ -213,7 +224,10 @@ __global__ __launch_bounds__(256) void select_list_kernel(int TX, int TY, const 
     const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
     for (int x = threadIdx.x; x < TX; x += 256) {
         const int t = ty * TX + x;
-        if (sel[t]) sel_list[off + row[x]] = t;
+        if (sel[t]) {
+            sel_list[off + row[x]] = t;
+            sel_cols[(size_t)ty * TX + row[x]] = x;
+        }
     }
     if (ty == TY - 1 && threadIdx.x == 0) cnt->n_selected = off + row[TX];
 }
@@ -291,10 +305,10 @@ void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 
 }
 
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
-                   int *sel_list, uint32_t *rowpre, uint8_t *mask_out, Counters *cnt,
-                   hipStream_t st) {
+                   int *sel_list, uint32_t *rowpre, int *sel_cols, uint8_t *mask_out,
+                   Counters *cnt, hipStream_t st) {
     select_rows_kernel<<<TY, 256, 0, st>>>(TX, mode, oc, um, sel, rowpre, mask_out);
-    select_list_kernel<<<TY, 256, 0, st>>>(TX, TY, sel, rowpre, sel_list, cnt);
+    select_list_kernel<<<TY, 256, 0, st>>>(TX, TY, sel, rowpre, sel_list, sel_cols, cnt);
 }
 
 void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,

@@ -78,7 +78,7 @@ struct Workspace {
     DevBuf g0, g1, col, rect, status, count, partial;
     DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
-    DevBuf ranges, sel, sel_list, rowpre, cnt;
+    DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt;
     Counters *host_cnt = nullptr;
     int n = -1, W = 0, H = 0;
     size_t key_cap = 0;
@@ -118,6 +118,7 @@ struct Workspace {
             TGS_TRY(ranges.ensure(nt * sizeof(uint2)));
             TGS_TRY(sel.ensure(nt));
             TGS_TRY(sel_list.ensure(nt * sizeof(int)));
+            TGS_TRY(sel_cols.ensure(nt * sizeof(int)));
             TGS_TRY(rowpre.ensure((size_t)TY * (TX + 1) * sizeof(uint32_t)));
             W = W_;
             H = H_;
@@ -244,7 +245,7 @@ void relative_pose(const float *ref, const float *cur, float *M, float *Minv) {
 
 // Event timing of every launch while profiling is on (tgs_profile_start/stop).
 struct Profiler {
-    bool on = false, count = false;
+    bool on = false, count = false, stages = false;
     std::vector<hipEvent_t> pool;
     size_t used = 0;
     struct Rec {
@@ -263,16 +264,26 @@ struct Profiler {
         return pool[used++];
     }
     unsigned long long *pairs(int stage) { return on && count ? d_pairs + stage : nullptr; }
+    // events attached to one kernel dispatch (no extra packets)
+    void kernel_events(int stage, hipEvent_t *a, hipEvent_t *b) {
+        *a = *b = nullptr;
+        if (!on) return;
+        *a = event();
+        *b = event();
+        if (*a && *b) recs.push_back({stage, *a, *b});
+        else *a = *b = nullptr;
+    }
 };
 Profiler g_prof;
 
-// Brackets the launches of one stage with events on their stream.
+// Brackets the launches of one stage with events recorded on their stream
+// (detail mode only: each separate event record costs a barrier packet).
 struct ProfScope {
     int stage;
     hipStream_t st;
     hipEvent_t a = nullptr;
     ProfScope(int stage_, hipStream_t st_) : stage(stage_), st(st_) {
-        if (g_prof.on && (a = g_prof.event()) != nullptr) (void)hipEventRecord(a, st);
+        if (g_prof.on && g_prof.stages && (a = g_prof.event()) != nullptr) (void)hipEventRecord(a, st);
     }
     ~ProfScope() {
         if (!a) return;
@@ -323,7 +334,6 @@ struct FrameResult {
 tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
                            hipStream_t st) {
     ProfScope ps(TGS_PROF_PREPROCESS, st);
-    launch_fill_i32(ws.cnt.as<int>(), sizeof(Counters) / sizeof(int), 0, st);
     launch_preprocess(sc->view, cam, cull, ws.records(), ws.cnt.as<Counters>(), st);
     TGS_LAUNCHED("preprocess");
     return TGS_OK;
@@ -339,7 +349,8 @@ tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, 
         ProfScope ps(TGS_PROF_SCAN, st);
         if (rowpre) launch_count_masked(n, ws.rect.as<ushort4>(), rowpre, TX, ws.count.as<uint32_t>(), st);
         launch_visible_scans(n, ws.count.as<uint32_t>(), ws.g1.as<float4>(), ws.dkey.as<uint32_t>(),
-                             ws.didx.as<uint32_t>(), ws.scan.p, ws.cnt.as<Counters>(), st);
+                             ws.didx.as<uint32_t>(), ws.scan.p, ws.partial.as<uint32_t>(),
+                             ws.cnt.as<Counters>(), st);
         TGS_LAUNCHED("visible scan");
     }
     {
@@ -361,7 +372,11 @@ tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, 
         ProfScope ps(TGS_PROF_READBACK, st);
         TGS_HIP(hipMemcpyAsync(ws.host_cnt, ws.cnt.p, sizeof(Counters), hipMemcpyDeviceToHost, st));
     }
-    TGS_HIP(hipStreamSynchronize(st));
+    // spin on the stream: a blocking wait adds tens of microseconds of wake-up
+    hipError_t q;
+    while ((q = hipStreamQuery(st)) == hipErrorNotReady) {
+    }
+    if (q != hipSuccess) return fail(TGS_ERR_DEVICE, std::string("frame read-back: ") + hipGetErrorString(q));
     fr.K = ws.host_cnt->n_keys;
     fr.V = ws.host_cnt->n_visible;
     fr.n_surv = ws.host_cnt->n_survivors;
@@ -376,16 +391,18 @@ tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, 
 
 // Emit the keys in depth order, sort them by tile (stable), find tile ranges;
 // returns the per-tile lists of Gaussian indices.
-tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, const uint32_t *didx,
-                     const FrameResult &fr, hipStream_t st, const uint32_t **sorted_vals) {
+tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, const int *sel_cols,
+                     const uint32_t *didx, const FrameResult &fr, hipStream_t st,
+                     const uint32_t **sorted_vals) {
     int bits = 0;
     while ((1 << bits) < TX * TY) ++bits;
     const int passes = sort_passes_for_bits(bits);
     TGS_TRY(ws.ensure_keys(fr.K, passes));
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
-        launch_duplicate(fr.V, fr.K, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX,
-                         ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(), st);
+        launch_duplicate(fr.V, fr.K, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
+                         sel_cols, TX, TX * TY, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
+                         ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("duplicate");
     }
     int alt = 0;
@@ -399,7 +416,7 @@ tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, cons
     const uint32_t *skeys = alt ? ws.tkey_alt.as<uint32_t>() : ws.tkey.as<uint32_t>();
     {
         ProfScope ps(TGS_PROF_RANGES, st);
-        launch_ranges(fr.K, TX * TY, skeys, ws.ranges.as<uint2>(), st);
+        launch_ranges(fr.K, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
@@ -453,7 +470,7 @@ extern "C" {
 
 const char *tgs_last_error(void) { return g_err.c_str(); }
 
-tgs_status tgs_profile_start(int32_t count_pairs) {
+tgs_status tgs_profile_start(int32_t flags) {
     g_err.clear();
     if (!g_prof.d_pairs)
         TGS_HIP(hipMalloc((void **)&g_prof.d_pairs, TGS_PROF_STAGES * sizeof(unsigned long long)));
@@ -461,7 +478,8 @@ tgs_status tgs_profile_start(int32_t count_pairs) {
     TGS_HIP(hipMemset(g_prof.d_pairs, 0, TGS_PROF_STAGES * sizeof(unsigned long long)));
     g_prof.used = 0;
     g_prof.recs.clear();
-    g_prof.count = count_pairs != 0;
+    g_prof.count = (flags & TGS_PROFILE_COUNT_PAIRS) != 0;
+    g_prof.stages = (flags & TGS_PROFILE_STAGES) != 0;
     g_prof.on = true;
     return TGS_OK;
 }
@@ -629,7 +647,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     FrameResult fr;
     const uint32_t *didx = nullptr, *vals = nullptr;
     TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
-    TGS_TRY(step_keys(ws, TX, TY, nullptr, didx, fr, st, &vals));
+    TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
     if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
     BlendArgs a = blend_args(ws, W, H, vals);
     a.rgb = out->rgb;
@@ -639,8 +657,9 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     a.contrib = out->contrib;
     a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
     {
-        ProfScope ps(TGS_PROF_BLEND_FULL, st);
-        launch_blend(a, TX * TY, st);
+        hipEvent_t ev0, ev1;
+        g_prof.kernel_events(TGS_PROF_BLEND_FULL, &ev0, &ev1);
+        launch_blend(a, TX * TY, st, ev0, ev1);
         TGS_LAUNCHED("blend");
     }
     if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)TX * TY, 1, st);
@@ -779,19 +798,21 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             ProfScope ps(TGS_PROF_SELECT, st);
             launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(),
                           ws.sel.as<uint8_t>(), ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(),
-                          out->tile_mask, ws.cnt.as<Counters>(), st);
+                          ws.sel_cols.as<int>(), out->tile_mask, ws.cnt.as<Counters>(), st);
             TGS_LAUNCHED("tile selection");
         }
         const uint32_t *didx = nullptr;
         TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr, &didx));
-        TGS_TRY(step_keys(ws, TX, TY, ws.rowpre.as<uint32_t>(), didx, fr, st, &vals));
+        TGS_TRY(step_keys(ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx, fr, st,
+                          &vals));
         BlendArgs a = blend_args(ws, W, H, vals);
         a.tile_list = ws.sel_list.as<int>();
         a.rgb = out->rgb;
         a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
         {
-            ProfScope ps(TGS_PROF_BLEND_TGS, st);
-            launch_blend(a, (int)fr.n_sel, st);
+            hipEvent_t ev0, ev1;
+            g_prof.kernel_events(TGS_PROF_BLEND_TGS, &ev0, &ev1);
+            launch_blend(a, (int)fr.n_sel, st, ev0, ev1);
             TGS_LAUNCHED("blend");
         }
         {
@@ -811,7 +832,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
         const uint32_t *didx = nullptr;
         TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
-        TGS_TRY(step_keys(ws, TX, TY, nullptr, didx, fr, st, &vals));
+        TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, W, H, vals);
         a.rgb = out->rgb;
@@ -825,8 +846,9 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         a.contrib = out->contrib;
         a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
         {
-            ProfScope ps(TGS_PROF_BLEND_REF, st);
-            launch_blend(a, nt, st);
+            hipEvent_t ev0, ev1;
+            g_prof.kernel_events(TGS_PROF_BLEND_REF, &ev0, &ev1);
+            launch_blend(a, nt, st, ev0, ev1);
             TGS_LAUNCHED("blend");
         }
         {

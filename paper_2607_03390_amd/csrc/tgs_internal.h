@@ -78,7 +78,7 @@ __device__ inline float ordered_to_float(int i) {
 
 // ---- launchers (k_preprocess.hip) ----
 // Writes the records and, per 256-Gaussian block, the survivor and
-// newly-visible counts; a second small kernel sums those into cnt.
+// newly-visible counts (summed into cnt by the visible-compaction scan).
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
                        Counters *cnt, hipStream_t st);
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
@@ -88,13 +88,16 @@ size_t scan_scratch_bytes(int n);
 void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
                          uint32_t *count, hipStream_t st);
 void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
-                          uint32_t *didx, void *scratch, Counters *cnt, hipStream_t st);
+                          uint32_t *didx, void *scratch, const uint32_t *pre_partial,
+                          Counters *cnt, hipStream_t st);
 void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
                               void *scratch, Counters *cnt, hipStream_t st);
+// Also clears the tile ranges (filled by launch_ranges after the tile sort).
+// rowpre / sel_cols are NULL in frames that render every tile.
 void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,
-                      const ushort4 *rect, const uint32_t *rowpre, int TX, uint32_t *tkey,
-                      uint32_t *tval, hipStream_t st);
-void launch_ranges(uint32_t K, int n_tiles, const uint32_t *keys, uint2 *ranges, hipStream_t st);
+                      const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
+                      int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
+void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
@@ -121,7 +124,10 @@ struct BlendArgs {
     float *contrib;           // optional: max weight per Gaussian
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
 };
-void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st);
+// start/stop (may be NULL) are attached to the dispatch itself
+// (hipExtLaunchKernelGGL): kernel timing without extra barrier packets.
+void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t start = nullptr,
+                  hipEvent_t stop = nullptr);
 // fbox must hold 4 + 4 * kAfcPartials ints (result, then partials).
 constexpr int kAfcPartials = 256;
 void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
@@ -143,9 +149,10 @@ void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *
                        hipStream_t st);
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g0,
                      const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st);
+// sel_cols[ty * TX + k] = column of the k-th selected tile of row ty
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
-                   int *sel_list, uint32_t *rowpre, uint8_t *mask_out, Counters *cnt,
-                   hipStream_t st);
+                   int *sel_list, uint32_t *rowpre, int *sel_cols, uint8_t *mask_out,
+                   Counters *cnt, hipStream_t st);
 void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,
                    float *rgb, hipStream_t st);
 void launch_fill_u8(uint8_t *p, size_t n, uint8_t v, hipStream_t st);

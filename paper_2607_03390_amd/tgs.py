@@ -258,8 +258,14 @@ def tgs_debug_dump(scene_h, state_h, what) -> np.ndarray:
     return out.view(_DUMP_DTYPE[what])
 
 
-def tgs_profile_start(count_pairs=False):
-    _check(lib().tgs_profile_start(1 if count_pairs else 0))
+TGS_PROFILE_COUNT_PAIRS, TGS_PROFILE_STAGES = 1, 2
+
+
+def tgs_profile_start(count_pairs=False, stages=False):
+    """Blend dispatches are always timed; ``stages`` also brackets every other
+    stage with separately recorded events (adds queue barriers)."""
+    flags = (TGS_PROFILE_COUNT_PAIRS if count_pairs else 0) | (TGS_PROFILE_STAGES if stages else 0)
+    _check(lib().tgs_profile_start(flags))
 
 
 def tgs_profile_stop():
