@@ -143,17 +143,18 @@ def sh_basis(deg, d):
 
 def gaussians(scene, cam, z_near=0.2, cull=None):
     """Per-Gaussian stage: near cull, projection, AFC/TOC (if ``cull``), 2D
-    covariance, radius, tile rectangle, SH colour."""
+    covariance, footprint half extents, tile rectangle, SH colour."""
     n = scene.n
     out = dict(status=np.zeros(n, np.int32), newly_visible=np.zeros(n, np.uint8),
                mean2d=np.zeros((n, 2), np.float32), ndc=np.zeros((n, 2), np.float32),
                depth=np.zeros(n, np.float32), conic=np.zeros((n, 3), np.float32),
-               radius=np.zeros(n, np.float32), rect=np.zeros((n, 4), np.int32),
+               extent=np.zeros((n, 2), np.float32), rect=np.zeros((n, 4), np.int32),
                rgb=np.zeros((n, 3), np.float64))
     means = np.ascontiguousarray(scene.means, np.float32)
     scales = np.ascontiguousarray(scene.scales, np.float32)
     rots = np.ascontiguousarray(scene.rotations, np.float32)
     sh = np.ascontiguousarray(scene.sh, np.float32)
+    opac = np.ascontiguousarray(scene.opacities, np.float32)
     cs = None
     keep = []
     if cull is not None:
@@ -173,11 +174,11 @@ def gaussians(scene, cam, z_near=0.2, cull=None):
         cs.lambda2 = float(cull.get("lambda2", 0.0))
     cam_s = _cam(cam)
     out["n_survivors"] = int(lib().or_gaussians(
-        C.c_int32(n), C.c_int32(scene.sh_degree), _p(means), _p(scales), _p(rots), _p(sh),
-        C.byref(cam_s), C.c_float(z_near), C.byref(cs) if cs is not None else None,
+        C.c_int32(n), C.c_int32(scene.sh_degree), _p(means), _p(scales), _p(rots), _p(opac),
+        _p(sh), C.byref(cam_s), C.c_float(z_near), C.byref(cs) if cs is not None else None,
         _p(out["status"]), _p(out["newly_visible"]), _p(out["mean2d"]), _p(out["ndc"]),
-        _p(out["depth"]), _p(out["conic"]), _p(out["radius"]), _p(out["rect"]), _p(out["rgb"])))
-    out["opacity"] = np.ascontiguousarray(scene.opacities, np.float32)
+        _p(out["depth"]), _p(out["conic"]), _p(out["extent"]), _p(out["rect"]), _p(out["rgb"])))
+    out["opacity"] = opac
     return out
 
 
@@ -215,7 +216,10 @@ def blend(W, H, ts, items, g, render_tiles=None):
                 g_certain=gc, g_uncertain=gu, pairs=int(E))
 
 
-def blend_bruteforce(W, H, g):
+def blend_bruteforce(W, H, g, every_gaussian=False):
+    """Per-pixel blend without tiles.  ``every_gaussian``: every Gaussian with
+    a 2D footprint at every pixel (tests the tile rectangles); otherwise the
+    Gaussians whose rectangle contains the pixel's tile."""
     rgb = np.zeros((3, H, W), np.float64)
     D = np.zeros((H, W), np.float64)
     S = np.zeros((H, W), np.float64)
@@ -223,7 +227,8 @@ def blend_bruteforce(W, H, g):
     n = g["status"].shape[0]
     lib().or_blend_bruteforce(C.c_int32(W), C.c_int32(H), C.c_int32(n), _p(g["status"]),
                               _p(g["rect"]), _p(g["mean2d"]), _p(g["conic"]), _p(g["opacity"]),
-                              _p(g["depth"]), _p(g["rgb"]), _p(rgb), _p(D), _p(S), _p(A))
+                              _p(g["depth"]), _p(g["rgb"]), C.c_int32(int(every_gaussian)),
+                              _p(rgb), _p(D), _p(S), _p(A))
     return dict(rgb=rgb, D=D, sigma=S, alpha=A)
 
 

@@ -176,10 +176,10 @@ typedef struct {
 } or_cull;
 
 int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const float *scales,
-                     const float *rots, const float *sh, const or_camera *cam, float z_near,
-                     const or_cull *cull,
+                     const float *rots, const float *opac, const float *sh, const or_camera *cam,
+                     float z_near, const or_cull *cull,
                      int32_t *status, uint8_t *newly_visible, float *mean2d, float *ndc,
-                     float *depth, float *conic, float *radius, int32_t *rect, double *rgb)
+                     float *depth, float *conic, float *extent, int32_t *rect, double *rgb)
 {
     const float *V = cam->w2c;
     const int W = cam->width, H = cam->height;
@@ -200,7 +200,8 @@ int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const flo
         ndc[2 * i] = ndc[2 * i + 1] = 0.0f;
         depth[i] = 0.0f;
         conic[3 * i] = conic[3 * i + 1] = conic[3 * i + 2] = 0.0f;
-        radius[i] = 0.0f;
+        extent[2 * i] = extent[2 * i + 1] = 0.0f;
+        float x0 = 1.0f, x1 = 0.0f, y0 = 1.0f, y1 = 0.0f;
         rgb[3 * i] = rgb[3 * i + 1] = rgb[3 * i + 2] = 0.0;
 
         /* view-space position */
@@ -262,33 +263,57 @@ int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const flo
         conic[3 * i + 1] = -cb * dinv;
         conic[3 * i + 2] = ca * dinv;
 
-        /* radius from the larger eigenvalue (3 sigma) and the tile rectangle:
-         * tiles whose pixel-centre span [16k, 16k+15] meets [u-r, u+r] */
-        float mid = 0.5f * (ca + cc);
-        float lam = mid + sqrtf(fmaxf(0.0f, mid * mid - det));
-        float r = ceilf(3.0f * sqrtf(lam));
-        radius[i] = r;
-        float x0 = fmaxf(0.0f, ceilf(((u - r) - 15.0f) / 16.0f));
-        float x1 = fminf((float)(TX - 1), floorf((u + r) / 16.0f));
-        float y0 = fmaxf(0.0f, ceilf(((v - r) - 15.0f) / 16.0f));
-        float y1 = fminf((float)(TY - 1), floorf((v + r) / 16.0f));
-
-        /* colour from SH along the viewing direction, +0.5, clamped at 0 */
-        double dx = (double)mx - campos[0], dy = (double)my - campos[1], dz = (double)mz - campos[2];
-        double dn = sqrt(dx * dx + dy * dy + dz * dz);
-        double basis[16];
-        or_sh_basis(sh_degree, dx / dn, dy / dn, dz / dn, basis);
-        for (int ch = 0; ch < 3; ++ch) {
-            double s = 0.0;
-            for (int k = 0; k < ncoef; ++k) s += basis[k] * (double)sh[((size_t)i * ncoef + k) * 3 + ch];
-            s += 0.5;
-            rgb[3 * i + ch] = s > 0.0 ? s : 0.0;
+        /* Footprint and tile rectangle.  A pixel at offset d can reach
+         * alpha >= 1/255 only if o exp(-q/2) >= 1/255 with q = d^T Sigma'^-1 d,
+         * i.e. q <= 2 ln(255 o); the tiles are those whose pixel-centre span
+         * [16k, 16k+15] meets the bounding box of that ellipse, half extents
+         * sqrt(kq Sigma'_xx), sqrt(kq Sigma'_yy).  kq bounds 2 ln(255 o) from
+         * above without a transcendental: log2 x = e + log2 m (x = m 2^e,
+         * m in [1,2)), and log2 m lies below its tangent at sqrt(2).  The box
+         * is enlarged by 0.1% + 0.01 px, so every pixel left out has alpha
+         * well below 1/255.  Opacity below 1/255 reaches no pixel. */
+        if (!(opac[i] >= OR_ALPHA_MIN)) { status[i] = OR_NO_TILES; goto colour; }
+        {
+            float x = fmaxf(255.0f * opac[i], 1.0f);
+            uint32_t xb = f2u(x);
+            int e = (int)((xb >> 23) & 255u) - 127;
+            uint32_t mb = (xb & 0x007fffffu) | 0x3f800000u;
+            float m;
+            memcpy(&m, &mb, 4);
+            float t = m - 1.4142135f;
+            t = 1.0201394f * t;
+            t = 0.5f + t;
+            float L = (float)e + t;
+            L = L + 1e-4f;
+            float kq = 1.3862944f * L;
+            float hx = sqrtf(kq * ca) * 1.001f + 0.01f;
+            float hy = sqrtf(kq * cc) * 1.001f + 0.01f;
+            extent[2 * i] = hx;
+            extent[2 * i + 1] = hy;
+            x0 = fmaxf(0.0f, ceilf(((u - hx) - 15.0f) / 16.0f));
+            x1 = fminf((float)(TX - 1), floorf((u + hx) / 16.0f));
+            y0 = fmaxf(0.0f, ceilf(((v - hy) - 15.0f) / 16.0f));
+            y1 = fminf((float)(TY - 1), floorf((v + hy) / 16.0f));
+            status[i] = (x0 <= x1 && y0 <= y1) ? OR_VISIBLE : OR_NO_TILES;
         }
-
-        if (!(x0 <= x1 && y0 <= y1)) { status[i] = OR_NO_TILES; continue; }
-        rect[4 * i + 0] = (int)x0; rect[4 * i + 1] = (int)y0;
-        rect[4 * i + 2] = (int)x1; rect[4 * i + 3] = (int)y1;
-        status[i] = OR_VISIBLE;
+    colour:
+        /* colour from SH along the viewing direction, +0.5, clamped at 0 */
+        {
+            double dx = (double)mx - campos[0], dy = (double)my - campos[1], dz = (double)mz - campos[2];
+            double dn = sqrt(dx * dx + dy * dy + dz * dz);
+            double basis[16];
+            or_sh_basis(sh_degree, dx / dn, dy / dn, dz / dn, basis);
+            for (int ch = 0; ch < 3; ++ch) {
+                double sacc = 0.0;
+                for (int k = 0; k < ncoef; ++k) sacc += basis[k] * (double)sh[((size_t)i * ncoef + k) * 3 + ch];
+                sacc += 0.5;
+                rgb[3 * i + ch] = sacc > 0.0 ? sacc : 0.0;
+            }
+        }
+        if (status[i] == OR_VISIBLE) {
+            rect[4 * i + 0] = (int)x0; rect[4 * i + 1] = (int)y0;
+            rect[4 * i + 2] = (int)x1; rect[4 * i + 3] = (int)y1;
+        }
     }
     return survivors;
 }
@@ -481,13 +506,19 @@ int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t 
  * per-tile lists, no keys.  Must reproduce or_blend bit for bit. */
 void or_blend_bruteforce(int32_t W, int32_t H, int32_t n, const int32_t *status, const int32_t *rect,
                          const float *mean2d, const float *conic, const float *opac,
-                         const float *depth, const double *rgb, double *out_rgb, double *out_D,
-                         double *out_sigma, double *out_alpha)
+                         const float *depth, const double *rgb, int32_t every_gaussian,
+                         double *out_rgb, double *out_D, double *out_sigma, double *out_alpha)
 {
+    /* every_gaussian != 0: each pixel blends every Gaussian that has a 2D
+     * footprint (tile rectangle or not), so the tile rectangles themselves
+     * are under test; otherwise each pixel takes the Gaussians whose
+     * rectangle contains its tile, in depth order. */
     or_item *order = (or_item *)malloc(sizeof(or_item) * (size_t)(n > 0 ? n : 1));
     int m = 0;
     for (int i = 0; i < n; ++i)
-        if (status[i] == OR_VISIBLE) { order[m].dbits = f2u(depth[i]); order[m].idx = i; ++m; }
+        if (status[i] == OR_VISIBLE || (every_gaussian && status[i] == OR_NO_TILES)) {
+            order[m].dbits = f2u(depth[i]); order[m].idx = i; ++m;
+        }
     qsort(order, (size_t)m, sizeof(or_item), item_cmp);
     int32_t *list = (int32_t *)malloc(sizeof(int32_t) * (size_t)(m > 0 ? m : 1));
     or_blend_ctx c = {mean2d, conic, opac, depth, rgb, NULL, NULL, NULL,
@@ -498,7 +529,8 @@ void or_blend_bruteforce(int32_t W, int32_t H, int32_t n, const int32_t *status,
             int tx = x / 16, ty = y / 16, len = 0;
             for (int k = 0; k < m; ++k) {
                 const int32_t *r = &rect[4 * order[k].idx];
-                if (tx >= r[0] && tx <= r[2] && ty >= r[1] && ty <= r[3]) list[len++] = order[k].idx;
+                if (every_gaussian || (tx >= r[0] && tx <= r[2] && ty >= r[1] && ty <= r[3]))
+                    list[len++] = order[k].idx;
             }
             or_pixel p;
             blend_pixel(&c, list, len, (float)x, (float)y, &p);

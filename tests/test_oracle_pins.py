@@ -52,7 +52,12 @@ def test_cov2d_isotropic_on_axis(s, Z):
     g = O.gaussians(_scene([[0, 0, Z]], [[s, s, s]]), cam)
     var = (f * s / Z) ** 2 + 0.3
     np.testing.assert_allclose(g["conic"][0], [1 / var, 0.0, 1 / var], rtol=2e-6, atol=1e-12)
-    assert g["radius"][0] == math.ceil(3 * math.sqrt(var) - 1e-6) or abs(3 * math.sqrt(var) - round(3 * math.sqrt(var))) < 1e-4
+    # footprint half extent: sqrt(2 ln(255 o) var), bounded above by the
+    # tangent bound of log2 (at most 0.1 over) and the 0.1% + 0.01 px margin
+    lo = math.sqrt(2 * math.log(255 * 0.9) * var)
+    hi = math.sqrt((2 * math.log(255 * 0.9) + 0.14) * var) * 1.0011 + 0.0101
+    for h in g["extent"][0]:
+        assert lo < h < hi
     np.testing.assert_allclose(g["mean2d"][0], [cam.cx, cam.cy], atol=1e-5)
     assert g["depth"][0] == np.float32(Z)
 
@@ -111,24 +116,79 @@ def test_near_plane_and_view_transform():
     np.testing.assert_allclose(O.camera_centre(w2c), eye, atol=1e-6)
 
 
+def _footprint_ok(g, i):
+    """The half extents bound the alpha >= 1/255 ellipse of Gaussian i from
+    above, and not by much: closed form from the inverse of its conic."""
+    a, b, c = (float(x) for x in g["conic"][i])
+    det = a * c - b * b
+    sxx, syy = c / det, a / det
+    o = float(g["opacity"][i])
+    k = max(0.0, 2 * math.log(255 * o))
+    hx, hy = (float(x) for x in g["extent"][i])
+    assert hx >= math.sqrt(k * sxx) * 1.0005 and hy >= math.sqrt(k * syy) * 1.0005
+    assert hx <= math.sqrt((k + 0.14) * sxx) * 1.0011 + 0.0101
+    assert hy <= math.sqrt((k + 0.14) * syy) * 1.0011 + 0.0101
+    return hx, hy
+
+
 def test_tile_rect_closed_form():
-    """The rectangle holds exactly the tiles with a pixel centre in [u-r, u+r]."""
+    """The rectangle holds exactly the tiles with a pixel centre inside the
+    footprint's bounding box [u-hx, u+hx] x [v-hy, v+hy]."""
     W, H = 100, 70
     cam = _cam(np.eye(4), W, H)
     rng = np.random.default_rng(1)
-    pts = np.column_stack([rng.uniform(-1.2, 1.2, 300), rng.uniform(-0.8, 0.8, 300), rng.uniform(1, 4, 300)])
-    g = O.gaussians(_scene(pts, np.full((300, 3), 0.02)), cam)
+    n = 300
+    pts = np.column_stack([rng.uniform(-1.2, 1.2, n), rng.uniform(-0.8, 0.8, n), rng.uniform(1, 4, n)])
+    scales = np.exp(rng.normal(-3.5, 0.6, (n, 3)))
+    q = rng.normal(size=(n, 4))
+    q /= np.linalg.norm(q, axis=1, keepdims=True)
+    opac = np.concatenate([rng.uniform(0.0, 0.012, 60), rng.uniform(0.004, 1.0, n - 60)])
+    g = O.gaussians(_scene(pts, scales, rots=q, opac=opac), cam)
     TX, TY = 7, 5
-    for i in range(300):
+    n_tiles = 0
+    for i in range(n):
+        if g["status"][i] == O.NEAR_CULLED:
+            continue
+        if opac[i] < np.float32(1 / 255):
+            assert g["status"][i] == O.NO_TILES
+            continue
         u, v = g["mean2d"][i]
-        r = g["radius"][i]
-        tx = [k for k in range(TX) if 16 * k <= u + r and 16 * k + 15 >= u - r]
-        ty = [k for k in range(TY) if 16 * k <= v + r and 16 * k + 15 >= v - r]
+        hx, hy = _footprint_ok(g, i)
+        tx = [k for k in range(TX) if 16 * k <= u + hx and 16 * k + 15 >= u - hx]
+        ty = [k for k in range(TY) if 16 * k <= v + hy and 16 * k + 15 >= v - hy]
         if tx and ty:
             assert g["status"][i] == O.VISIBLE
             assert list(g["rect"][i]) == [tx[0], ty[0], tx[-1], ty[-1]]
+            n_tiles += len(tx) * len(ty)
         else:
             assert g["status"][i] == O.NO_TILES
+    assert n_tiles > n
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_no_contribution_outside_rect(seed):
+    """At every pixel outside a Gaussian's tile rectangle its alpha, in fp64
+    from the conic, is below 1/255, so dropping it there changes nothing."""
+    W, H = 90, 61
+    sc = synth.small_scene(400, seed, degree=0, log_scale_mean=-2.8)
+    rng = np.random.default_rng(seed)
+    sc.opacities[:] = np.where(rng.random(sc.n) < 0.3, rng.uniform(0.0039, 0.02, sc.n),
+                               sc.opacities).astype(np.float32)
+    cam = _cam(synth.look_at((0.4, -2.6, 0.9), (0, 0, 0)), W, H)
+    g = O.gaussians(sc, cam)
+    ys, xs = np.mgrid[0:H, 0:W]
+    tile_x, tile_y = xs // 16, ys // 16
+    checked = 0
+    for i in np.nonzero((g["status"] == O.VISIBLE) | (g["status"] == O.NO_TILES))[0]:
+        a, b, c = (float(x) for x in g["conic"][i])
+        u, v = (float(x) for x in g["mean2d"][i])
+        dx, dy = u - xs, v - ys
+        alpha = float(g["opacity"][i]) * np.exp(-0.5 * (a * dx * dx + c * dy * dy) - b * dx * dy)
+        x0, y0, x1, y1 = g["rect"][i]
+        inside = (tile_x >= x0) & (tile_x <= x1) & (tile_y >= y0) & (tile_y <= y1)
+        assert alpha[~inside].max(initial=0.0) < (1 / 255) * (1 - 1e-4)
+        checked += 1
+    assert checked > 100
 
 
 # --------------------------------------------------------------------------
@@ -247,8 +307,10 @@ def test_bruteforce_equals_tiled(seed, W, H):
     cam = _cam(synth.look_at((0.3, -3.0, 0.8), (0, 0, 0)), W, H)
     r = O.render_full(sc, cam)
     bf = O.blend_bruteforce(W, H, r["g"])
+    every = O.blend_bruteforce(W, H, r["g"], every_gaussian=True)
     for k in ("rgb", "D", "sigma", "alpha"):
         assert np.array_equal(r[k], bf[k]), k
+        assert np.array_equal(r[k], every[k]), k
     assert r["K"] > 0
 
 
@@ -444,13 +506,10 @@ def test_occluded_tiles_closed_form():
     R2 = 2 * var * math.log(255 * o)
     ys, xs = np.mgrid[0:H, 0:W]
     d2 = (xs - u) ** 2 + (ys - v) ** 2
-    rad = g["radius"][0]
     TX, TY = W // 16, H // 16
     expect = np.zeros((TY, TX), np.uint8)
     for ty in range(TY):
         for tx in range(TX):
-            if not (16 * tx <= u + rad and 16 * tx + 15 >= u - rad and 16 * ty <= v + rad and 16 * ty + 15 >= v - rad):
-                continue
             expect[ty, tx] = (d2[16 * ty:16 * ty + 16, 16 * tx:16 * tx + 16] <= R2).any()
     assert expect.sum() >= 2
     assert np.array_equal(oc, expect)
