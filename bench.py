@@ -8,7 +8,8 @@ one through the HIP kernels of libtgs.  The scene is resident in HBM before
 the timed region starts.
 
 Printed (one JSON line): temporal-mode FPS (value), full-render FPS over the
-same path, PSNR of temporal vs full, the roofline of the dominant kernel (its
+same path (both with the 3DGS 3-sigma tile rule; the same two timings with
+the alpha-footprint tile rule alongside), PSNR of temporal vs full, the roofline of the dominant kernel (its
 launch durations from HIP events attached to its dispatches inside the timed
 region), a per-stage breakdown from an untimed pass, and the CPU oracle timed
 on a bounded sample of the same workload.
@@ -50,6 +51,8 @@ def parse():
                     help="frames of the path the CPU oracle renders for its baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-psnr", action="store_true")
+    ap.add_argument("--no-footprint", action="store_true",
+                    help="skip the timing of the footprint tile rule")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
     return ap.parse_args()
@@ -182,6 +185,32 @@ def main():
                     min_db=float(np.min(vals)) if vals else None,
                     frames_compared=len(vals), identical_frames=n_frames - len(vals))
 
+    # the same path with the alpha-footprint tile rule (same contributions
+    # up to the 3-sigma clipping, fewer Gaussian-tile keys)
+    fp = None
+    if not args.no_footprint:
+        tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_FOOTPRINT)
+        temporal_step()
+        full_step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            temporal_step()
+        torch.cuda.synchronize()
+        fp_t = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            full_step()
+        torch.cuda.synchronize()
+        fp_f = time.perf_counter() - t0
+        tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_3SIGMA)
+        fp = {"tile_rule": "alpha >= 1/255 footprint box",
+              "temporal_fps": round(n_frames * args.steps / fp_t, 2),
+              "full_fps": round(n_frames * args.steps / fp_f, 2),
+              "temporal_ms_per_frame": round(1e3 * fp_t / (args.steps * n_frames), 4),
+              "full_ms_per_frame": round(1e3 * fp_f / (args.steps * n_frames), 4)}
+        log(f"[bench] footprint tile rule timed: {fp}")
+
     n_tgs = sum(1 for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS)
     sr_pct = [100.0 * i["n_selected"] / (TX * TY) for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS]
 
@@ -237,6 +266,8 @@ def main():
                      "sr_tile_pct": round(float(np.mean(sr_pct)), 2) if sr_pct else None},
         "full": {"fps": round(fps_f, 2), "ms_per_frame": round(1e3 * t_full / (args.steps * n_frames), 4)},
         "speedup_temporal_vs_full": round(fps_t / fps_f, 3),
+        "tile_rule": "3DGS 3-sigma square",
+        "footprint_tile_rule": fp,
         "psnr_temporal_vs_full": psnr,
         "stage_ms_per_frame": {s: per_frame(s) for s in tgs.PROF_STAGES if detail[s]["ms"] > 0},
         "stage_full_ms_per_frame": {s: round(v["ms"] / n_frames, 4)

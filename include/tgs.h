@@ -135,6 +135,21 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *desc, void *stream, tgs_scene 
 void tgs_scene_free(tgs_scene *scene);
 int32_t tgs_scene_count(const tgs_scene *scene);
 
+/* Which tiles a Gaussian is duplicated into (Sec. III-A: the tiles it
+ * intersects), for every later render of `scene` (full and temporal):
+ *  TGS_TILES_3SIGMA (default, the 3DGS rule): the tiles whose pixel-centre
+ *    span meets the square of half side ceil(3 sqrt(lambda_max(Sigma'))).
+ *  TGS_TILES_FOOTPRINT: the tiles meeting the bounding box of the ellipse
+ *    where the Gaussian can reach alpha >= 1/255 (an upper bound of
+ *    2 ln(255 o) computed without transcendentals, enlarged 0.1% + 0.01 px);
+ *    opacity below 1/255 gives no tiles.  Every pixel it leaves out has
+ *    alpha < 1/255, so the image equals a tile-free blend of all Gaussians;
+ *    it differs from the 3-sigma rule only where 3 sigma clips a Gaussian
+ *    that still reaches 1/255.
+ * Errors: INVALID_ARG for a NULL scene or an unknown rule. */
+enum { TGS_TILES_3SIGMA = 0, TGS_TILES_FOOTPRINT = 1 };
+tgs_status tgs_scene_set_tile_bound(tgs_scene *scene, int32_t bound);
+
 /* Renders one frame with the full 3DGS pipeline (Sec. III-A), no temporal
  * state.  frame_kind = TGS_FRAME_FULL.  The scene holds the frame's
  * workspace, so calls on one scene must not overlap. */

@@ -33,6 +33,7 @@ GCC_CMD = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fno-fast-ma
 
 NOHIT = np.float32(1001.0)          # z_far + epsilon (Sec. III-C)
 NEAR_CULLED, AFC_CULLED, TOC_CULLED, DEGENERATE, NO_TILES, VISIBLE = range(6)
+TILES_3SIGMA, TILES_FOOTPRINT = 0, 1   # tile rectangle rules (Sec. III-A intersection)
 TRUE_REF, PSEUDO_REF, TGS_FRAME = 0, 1, 2
 
 
@@ -101,6 +102,7 @@ class Params:
     enable_toc: bool = True
     enable_sr: bool = True
     force_all_dirty: bool = False
+    tile_bound: int = 0          # TILES_3SIGMA or TILES_FOOTPRINT
 
 
 # --------------------------------------------------------------------------
@@ -141,7 +143,7 @@ def sh_basis(deg, d):
     return out[:(deg + 1) ** 2]
 
 
-def gaussians(scene, cam, z_near=0.2, cull=None):
+def gaussians(scene, cam, z_near=0.2, cull=None, tile_bound=0):
     """Per-Gaussian stage: near cull, projection, AFC/TOC (if ``cull``), 2D
     covariance, footprint half extents, tile rectangle, SH colour."""
     n = scene.n
@@ -176,6 +178,7 @@ def gaussians(scene, cam, z_near=0.2, cull=None):
     out["n_survivors"] = int(lib().or_gaussians(
         C.c_int32(n), C.c_int32(scene.sh_degree), _p(means), _p(scales), _p(rots), _p(opac),
         _p(sh), C.byref(cam_s), C.c_float(z_near), C.byref(cs) if cs is not None else None,
+        C.c_int32(tile_bound),
         _p(out["status"]), _p(out["newly_visible"]), _p(out["mean2d"]), _p(out["ndc"]),
         _p(out["depth"]), _p(out["conic"]), _p(out["extent"]), _p(out["rect"]), _p(out["rgb"])))
     out["opacity"] = opac
@@ -295,10 +298,10 @@ def stitch(tab, uv, tile_sel, out_rgb):
 # a full 3DGS frame
 # --------------------------------------------------------------------------
 
-def render_full(scene, cam, z_near=0.2, cull=None):
+def render_full(scene, cam, z_near=0.2, cull=None, tile_bound=0):
     W, H = cam.width, cam.height
     TX, TY = (W + 15) // 16, (H + 15) // 16
-    g = gaussians(scene, cam, z_near, cull)
+    g = gaussians(scene, cam, z_near, cull, tile_bound)
     ts, items = tile_lists(g, TX, TY)
     b = blend(W, H, ts, items, g)
     b.update(g=g, tile_start=ts, items=items, K=int(items.size),
@@ -384,7 +387,7 @@ class TemporalOracle:
         cull = None
         if kind == PSEUDO_REF and self.p.enable_afc:
             cull = dict(afc=True, fbox=self.fbox)
-        out = render_full(self.scene, cam, self.p.z_near, cull)
+        out = render_full(self.scene, cam, self.p.z_near, cull, self.p.tile_bound)
         # temporal priors (Sec. III-C)
         self.D = out["D"].astype(np.float32)
         self.S = out["sigma"].astype(np.float32)
@@ -408,7 +411,7 @@ class TemporalOracle:
         uv, matched, um = backward_query(dfill, kcur, self.ref_intr, Minv, p.z_near)
         cull = dict(afc=p.enable_afc, fbox=self.fbox, toc=p.enable_toc, dmin=dmin, smax=smax,
                     g_rendered=self.g_rendered, lambda1=p.lambda1, lambda2=p.lambda2)
-        g = gaussians(self.scene, cam, p.z_near, cull)
+        g = gaussians(self.scene, cam, p.z_near, cull, p.tile_bound)
         oc, oc_margin = occluded_tiles(W, H, g)
         if p.enable_sr and not p.force_all_dirty:
             sel = (oc | um).astype(np.uint8)

@@ -34,6 +34,7 @@
 #define OR_MARGIN_T (1e-4 * 1e-4)
 #define OR_MARGIN_POWER 1e-6
 
+enum { OR_TILES_3SIGMA = 0, OR_TILES_FOOTPRINT = 1 };
 enum { OR_NEAR_CULLED = 0, OR_AFC_CULLED = 1, OR_TOC_CULLED = 2, OR_DEGENERATE = 3,
        OR_NO_TILES = 4, OR_VISIBLE = 5 };
 
@@ -161,7 +162,7 @@ void or_sh_basis(int deg, double x, double y, double z, double *basis)
 /* ------------------------------------------------------------------------ */
 /* Per-Gaussian stage: near-plane cull, projection, adaptive frustum culling */
 /* (Sec. III-D), temporal occlusion culling and the newly-visible test       */
-/* (Sec. III-D/III-E), then 2D covariance, radius, tile rectangle and colour */
+/* (Sec. III-D/III-E), then 2D covariance, extent, tile rectangle, colour    */
 /* for the survivors (Sec. III-A).                                           */
 /* ------------------------------------------------------------------------ */
 
@@ -177,7 +178,7 @@ typedef struct {
 
 int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const float *scales,
                      const float *rots, const float *opac, const float *sh, const or_camera *cam,
-                     float z_near, const or_cull *cull,
+                     float z_near, const or_cull *cull, int32_t tile_bound,
                      int32_t *status, uint8_t *newly_visible, float *mean2d, float *ndc,
                      float *depth, float *conic, float *extent, int32_t *rect, double *rgb)
 {
@@ -263,31 +264,42 @@ int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const flo
         conic[3 * i + 1] = -cb * dinv;
         conic[3 * i + 2] = ca * dinv;
 
-        /* Footprint and tile rectangle.  A pixel at offset d can reach
-         * alpha >= 1/255 only if o exp(-q/2) >= 1/255 with q = d^T Sigma'^-1 d,
-         * i.e. q <= 2 ln(255 o); the tiles are those whose pixel-centre span
-         * [16k, 16k+15] meets the bounding box of that ellipse, half extents
-         * sqrt(kq Sigma'_xx), sqrt(kq Sigma'_yy).  kq bounds 2 ln(255 o) from
-         * above without a transcendental: log2 x = e + log2 m (x = m 2^e,
-         * m in [1,2)), and log2 m lies below its tangent at sqrt(2).  The box
-         * is enlarged by 0.1% + 0.01 px, so every pixel left out has alpha
-         * well below 1/255.  Opacity below 1/255 reaches no pixel. */
-        if (!(opac[i] >= OR_ALPHA_MIN)) { status[i] = OR_NO_TILES; goto colour; }
+        /* Tile rectangle: the tiles whose pixel-centre span [16k, 16k+15]
+         * meets the box [u-hx, u+hx] x [v-hy, v+hy] (Sec. III-A duplicates a
+         * Gaussian into every tile it intersects).
+         * OR_TILES_3SIGMA (3DGS): hx = hy = ceil(3 sqrt(lambda_max(Sigma'))).
+         * OR_TILES_FOOTPRINT: the bounding box of the ellipse where the
+         * Gaussian can reach alpha >= 1/255.  A pixel at offset d does so
+         * only if o exp(-q/2) >= 1/255 with q = d^T Sigma'^-1 d, i.e.
+         * q <= 2 ln(255 o); the box has half extents sqrt(kq Sigma'_xx),
+         * sqrt(kq Sigma'_yy).  kq bounds 2 ln(255 o) from above without a
+         * transcendental: log2 x = e + log2 m (x = m 2^e, m in [1,2)), and
+         * log2 m lies below its tangent at sqrt(2).  The box is enlarged by
+         * 0.1% + 0.01 px, so every pixel left out has alpha well below
+         * 1/255; opacity below 1/255 reaches no pixel. */
         {
-            float x = fmaxf(255.0f * opac[i], 1.0f);
-            uint32_t xb = f2u(x);
-            int e = (int)((xb >> 23) & 255u) - 127;
-            uint32_t mb = (xb & 0x007fffffu) | 0x3f800000u;
-            float m;
-            memcpy(&m, &mb, 4);
-            float t = m - 1.4142135f;
-            t = 1.0201394f * t;
-            t = 0.5f + t;
-            float L = (float)e + t;
-            L = L + 1e-4f;
-            float kq = 1.3862944f * L;
-            float hx = sqrtf(kq * ca) * 1.001f + 0.01f;
-            float hy = sqrtf(kq * cc) * 1.001f + 0.01f;
+            float hx, hy;
+            if (tile_bound == OR_TILES_FOOTPRINT) {
+                if (!(opac[i] >= OR_ALPHA_MIN)) { status[i] = OR_NO_TILES; goto colour; }
+                float x = fmaxf(255.0f * opac[i], 1.0f);
+                uint32_t xb = f2u(x);
+                int e = (int)((xb >> 23) & 255u) - 127;
+                uint32_t mb = (xb & 0x007fffffu) | 0x3f800000u;
+                float m;
+                memcpy(&m, &mb, 4);
+                float t = m - 1.4142135f;
+                t = 1.0201394f * t;
+                t = 0.5f + t;
+                float L = (float)e + t;
+                L = L + 1e-4f;
+                float kq = 1.3862944f * L;
+                hx = sqrtf(kq * ca) * 1.001f + 0.01f;
+                hy = sqrtf(kq * cc) * 1.001f + 0.01f;
+            } else {
+                float mid = 0.5f * (ca + cc);
+                float lam = mid + sqrtf(fmaxf(0.0f, mid * mid - det));
+                hx = hy = ceilf(3.0f * sqrtf(lam));
+            }
             extent[2 * i] = hx;
             extent[2 * i + 1] = hy;
             x0 = fmaxf(0.0f, ceilf(((u - hx) - 15.0f) / 16.0f));

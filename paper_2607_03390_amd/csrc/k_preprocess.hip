@@ -159,27 +159,36 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
             const float cb = (B[0] * A[3] + B[1] * A[4]) + B[2] * A[5];
             const float cc = ((B[3] * A[3] + B[4] * A[4]) + B[5] * A[5]) + 0.3f;
             const float det = ca * cc - cb * cb;
-            if (det > 0.0f && mo.w >= kAlphaMin) {
+            if (det > 0.0f && (!cull.footprint || mo.w >= kAlphaMin)) {
                 const float dinv = 1.0f / det;
-                // Footprint: a pixel at offset d reaches alpha >= 1/255 only if
-                // d^T Sigma'^-1 d <= 2 ln(255 o).  kq bounds that from above
-                // without a transcendental (exact exponent plus the tangent of
-                // log2 at sqrt 2 for the mantissa, which lies above log2 on
-                // [1, 2)), so the rectangle is exactly reproducible.  The tiles
-                // are those whose pixel-centre span meets the bounding box of
-                // the ellipse, half extents sqrt(kq Sigma'_xx), sqrt(kq Sigma'_yy),
-                // enlarged by 0.1% + 0.01 px.
-                const uint32_t xb = __float_as_uint(fmaxf(255.0f * mo.w, 1.0f));
-                const int e = (int)((xb >> 23) & 255u) - 127;
-                const float m = __uint_as_float((xb & 0x007fffffu) | 0x3f800000u);
-                float t = m - 1.4142135f;
-                t = 1.0201394f * t;
-                t = 0.5f + t;
-                float L = (float)e + t;
-                L = L + 1e-4f;
-                const float kq = 1.3862944f * L;
-                const float hx = sqrtf(kq * ca) * 1.001f + 0.01f;
-                const float hy = sqrtf(kq * cc) * 1.001f + 0.01f;
+                // Tile rectangle: tiles whose pixel-centre span meets the box
+                // [u-hx, u+hx] x [v-hy, v+hy].
+                float hx, hy;
+                if (cull.footprint) {
+                    // Bounding box of the ellipse where the Gaussian can reach
+                    // alpha >= 1/255: d^T Sigma'^-1 d <= 2 ln(255 o).  kq bounds
+                    // that from above without a transcendental (exact exponent
+                    // plus the tangent of log2 at sqrt 2 for the mantissa, which
+                    // lies above log2 on [1, 2)), so the rectangle is exactly
+                    // reproducible; half extents sqrt(kq Sigma'_xx),
+                    // sqrt(kq Sigma'_yy), enlarged by 0.1% + 0.01 px.
+                    const uint32_t xb = __float_as_uint(fmaxf(255.0f * mo.w, 1.0f));
+                    const int e = (int)((xb >> 23) & 255u) - 127;
+                    const float m = __uint_as_float((xb & 0x007fffffu) | 0x3f800000u);
+                    float t = m - 1.4142135f;
+                    t = 1.0201394f * t;
+                    t = 0.5f + t;
+                    float L = (float)e + t;
+                    L = L + 1e-4f;
+                    const float kq = 1.3862944f * L;
+                    hx = sqrtf(kq * ca) * 1.001f + 0.01f;
+                    hy = sqrtf(kq * cc) * 1.001f + 0.01f;
+                } else {
+                    // 3DGS: 3 sigma of the larger eigenvalue of Sigma', rounded up
+                    const float mid = 0.5f * (ca + cc);
+                    const float lam = mid + sqrtf(fmaxf(0.0f, mid * mid - det));
+                    hx = hy = ceilf(3.0f * sqrtf(lam));
+                }
                 const float x0 = fmaxf(0.0f, ceilf(((u - hx) - 15.0f) / 16.0f));
                 const float x1 = fminf((float)(cam.TX - 1), floorf((u + hx) / 16.0f));
                 const float y0 = fmaxf(0.0f, ceilf(((v - hy) - 15.0f) / 16.0f));

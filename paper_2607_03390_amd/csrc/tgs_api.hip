@@ -302,6 +302,7 @@ struct ProfScope {
 
 struct tgs_scene {
     int n = 0, deg = 0, ncoef = 1;
+    int tile_bound = TGS_TILES_3SIGMA;
     DevBuf data;
     SceneDev view{};
     Workspace ws;
@@ -334,7 +335,9 @@ struct FrameResult {
 tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
                            hipStream_t st) {
     ProfScope ps(TGS_PROF_PREPROCESS, st);
-    launch_preprocess(sc->view, cam, cull, ws.records(), ws.cnt.as<Counters>(), st);
+    CullK c = cull;
+    c.footprint = sc->tile_bound == TGS_TILES_FOOTPRINT ? 1 : 0;
+    launch_preprocess(sc->view, cam, c, ws.records(), ws.cnt.as<Counters>(), st);
     TGS_LAUNCHED("preprocess");
     return TGS_OK;
 }
@@ -632,6 +635,15 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
 void tgs_scene_free(tgs_scene *scene) { delete scene; }
 
 int32_t tgs_scene_count(const tgs_scene *scene) { return scene ? scene->n : 0; }
+
+tgs_status tgs_scene_set_tile_bound(tgs_scene *scene, int32_t bound) {
+    g_err.clear();
+    if (!scene) return fail(TGS_ERR_INVALID_ARG, "scene is NULL");
+    if (bound != TGS_TILES_3SIGMA && bound != TGS_TILES_FOOTPRINT)
+        return fail(TGS_ERR_INVALID_ARG, "tile bound must be TGS_TILES_3SIGMA or TGS_TILES_FOOTPRINT");
+    scene->tile_bound = bound;
+    return TGS_OK;
+}
 
 tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *out,
                            void *stream) {

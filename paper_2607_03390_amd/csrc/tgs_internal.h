@@ -54,6 +54,7 @@ struct CullK {
     const float *dmin, *smax; // warped TGB
     const uint8_t *g_rendered;
     float lambda1, lambda2;
+    int footprint;            // tile rectangle: 0 = 3-sigma square, 1 = alpha footprint box
 };
 
 // Frame counters on the device (read back once per frame).

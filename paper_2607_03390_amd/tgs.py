@@ -18,12 +18,14 @@ LIB_PATH = os.path.join(HERE, "libtgs.so")
 TGS_OK, TGS_ERR_INVALID_ARG, TGS_ERR_OUT_OF_MEMORY, TGS_ERR_DEVICE, TGS_ERR_STATE_MISMATCH, \
     TGS_ERR_CAPACITY = range(6)
 TGS_FRAME_TRUE_REF, TGS_FRAME_PSEUDO_REF, TGS_FRAME_TGS, TGS_FRAME_FULL = range(4)
+TGS_TILES_3SIGMA, TGS_TILES_FOOTPRINT = 0, 1
 (TGS_DUMP_SORTED_VALUES, TGS_DUMP_SORTED_KEYS, TGS_DUMP_TILE_RANGES, TGS_DUMP_RECORDS,
  TGS_DUMP_RECTS, TGS_DUMP_STATUS, TGS_DUMP_WARP_DEPTH, TGS_DUMP_WARP_SIGMA,
  TGS_DUMP_FILLED_DEPTH, TGS_DUMP_CORRESPONDENCE, TGS_DUMP_UNMATCHED, TGS_DUMP_OCCLUDED,
  TGS_DUMP_SELECTED) = range(13)
 
 EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_scene_count",
+            "tgs_scene_set_tile_bound",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
             "tgs_profile_start", "tgs_profile_stop", "tgs_last_error"]
@@ -92,6 +94,7 @@ def lib():
         L.tgs_scene_upload.argtypes = [C.POINTER(tgs_scene_desc), vp, C.POINTER(vp)]
         L.tgs_scene_free.argtypes = [vp]
         L.tgs_scene_count.argtypes = [vp]
+        L.tgs_scene_set_tile_bound.argtypes = [vp, C.c_int32]
         L.tgs_render_full.argtypes = [vp, C.POINTER(tgs_camera), C.POINTER(tgs_frame_out), vp]
         L.tgs_state_create.argtypes = [vp, i32, i32, C.POINTER(tgs_params), C.POINTER(vp)]
         L.tgs_state_reset.argtypes = [vp]
@@ -176,6 +179,11 @@ def tgs_scene_free(h):
 
 def tgs_scene_count(h):
     return int(lib().tgs_scene_count(h))
+
+
+def tgs_scene_set_tile_bound(h, bound):
+    """TGS_TILES_3SIGMA (default) or TGS_TILES_FOOTPRINT for later renders."""
+    _check(lib().tgs_scene_set_tile_bound(h, int(bound)))
 
 
 def tgs_render_full(scene_h, cam, rgb, depth=None, sigma=None, alpha=None, contrib=None,

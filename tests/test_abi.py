@@ -103,6 +103,15 @@ def test_render_rejects_bad_camera_on_host():
     assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
 
 
+def test_tile_bound_rejects_bad_input_on_host():
+    L = tgs.lib()
+    assert L.tgs_scene_set_tile_bound(None, tgs.TGS_TILES_FOOTPRINT) == tgs.TGS_ERR_INVALID_ARG
+    dummy = C.c_void_p(1)      # never dereferenced: the rule is checked first
+    for bad in (-1, 2):
+        assert L.tgs_scene_set_tile_bound(dummy, bad) == tgs.TGS_ERR_INVALID_ARG
+        assert "tile bound" in L.tgs_last_error().decode()
+
+
 def test_state_create_rejects_bad_params_on_host():
     L = tgs.lib()
     h = C.c_void_p()

@@ -31,27 +31,29 @@ def _device():
 
 
 class Uploaded:
-    def __init__(self, scene):
+    def __init__(self, scene, bound=tgs.TGS_TILES_3SIGMA):
         self.scene = scene
+        self.bound = bound
 
     def __enter__(self):
         self.h = tgs.tgs_scene_upload(self.scene)
+        tgs.tgs_scene_set_tile_bound(self.h, self.bound)
         return self.h
 
     def __exit__(self, *a):
         tgs.tgs_scene_free(self.h)
 
 
-def _full_parity(scene, cams, sample_tiles=None, label=""):
+def _full_parity(scene, cams, sample_tiles=None, label="", bound=tgs.TGS_TILES_3SIGMA):
     n = scene.n
-    with Uploaded(scene) as h:
+    with Uploaded(scene, bound) as h:
         for k, cam in enumerate(cams):
             W, H = cam.width, cam.height
             TX, TY = cam.tiles
-            log(f"[full parity {label}] cam {k} {W}x{H} n={n}")
+            log(f"[full parity {label}] cam {k} {W}x{H} n={n} tile bound {bound}")
             res = gpu_full(h, cam, n)
             d = dumps(h, None, n)
-            g = O.gaussians(scene, cam)
+            g = O.gaussians(scene, cam, tile_bound=bound)
             ts, items = O.tile_lists(g, TX, TY)
             check_records(d, g)
             check_lists(d, ts, items)
@@ -87,6 +89,17 @@ def test_full_parity_ragged(n, seed, deg, W, H):
     _full_parity(sc, cams, label=f"ragged {W}x{H}")
 
 
+@pytest.mark.parametrize("n,seed,deg,W,H", [(3000, 1, 3, 200, 136), (2000, 4, 0, 300, 17)])
+def test_full_parity_footprint_tiles(n, seed, deg, W, H):
+    sc = synth.small_scene(n, seed, degree=deg)
+    rng = np.random.default_rng(seed)
+    low = rng.random(n) < 0.2          # opacities around the 1/255 cut
+    sc.opacities[low] = rng.uniform(0.002, 0.01, low.sum()).astype(np.float32)
+    cams = [synth.make_camera(synth.look_at(e, (0, 0, 0)), W, H)
+            for e in ((0.2, -3.0, 0.7), (2.5, 1.0, -0.4))]
+    _full_parity(sc, cams, label=f"footprint {W}x{H}", bound=tgs.TGS_TILES_FOOTPRINT)
+
+
 def test_full_parity_object_subset():
     w = synth.workload("object", n_gaussians=40_000)
     _full_parity(w.scene, [w.cameras[0], w.cameras[37]], label="object 40k")
@@ -114,13 +127,13 @@ def test_empty_and_invisible_scenes():
         tgs.tgs_state_free(s)
 
 
-def _temporal_parity(scene, cams, W, H, label, **pkw):
+def _temporal_parity(scene, cams, W, H, label, bound=tgs.TGS_TILES_3SIGMA, **pkw):
     import torch
     n = scene.n
     stats = dict(frames=0, tgs=0, margin_tiles=0, margin_px=0)
-    with Uploaded(scene) as h:
+    with Uploaded(scene, bound) as h:
         s = tgs.tgs_state_create(h, W, H, tgs.params(**pkw))
-        ora = O.TemporalOracle(scene, W, H, O.Params(**pkw))
+        ora = O.TemporalOracle(scene, W, H, O.Params(tile_bound=bound, **pkw))
         try:
             for k, cam in enumerate(cams):
                 blob = tgs.tgs_state_export(s)
@@ -202,6 +215,13 @@ def test_temporal_parity_room_subset(pkw):
     assert st["tgs"] >= 3
 
 
+def test_temporal_parity_room_subset_footprint_tiles():
+    sc = synth.scene_room(60_000, 2)
+    cams = synth.handheld_path(12, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 400, 232)
+    st = _temporal_parity(sc, cams, 400, 232, "room60k footprint", bound=tgs.TGS_TILES_FOOTPRINT)
+    assert st["tgs"] >= 3
+
+
 def test_temporal_parity_cube_occlusion():
     sc = synth.scene_uniform_cube(20_000, 7, degree=1, log_scale_mean=-3.3)
     cams = synth.orbit_path(10, 3.0, 15.0, 1.0, 144, 120)
@@ -273,6 +293,8 @@ def test_full_size_room_frame():
     sample = np.unique(np.concatenate([heavy, rng.choice(TX * TY, 40, replace=False),
                                        np.arange((TY - 1) * TX, TY * TX, 13)]))
     _full_parity(sc, cams[:1], sample_tiles=sample, label="room 1.5M")
+    _full_parity(sc, cams[1:2], sample_tiles=sample, label="room 1.5M footprint",
+                 bound=tgs.TGS_TILES_FOOTPRINT)
     _temporal_parity(sc, cams[:2], 1920, 1080, "room 1.5M")
     torch.cuda.synchronize()
 

@@ -52,6 +52,10 @@ def test_cov2d_isotropic_on_axis(s, Z):
     g = O.gaussians(_scene([[0, 0, Z]], [[s, s, s]]), cam)
     var = (f * s / Z) ** 2 + 0.3
     np.testing.assert_allclose(g["conic"][0], [1 / var, 0.0, 1 / var], rtol=2e-6, atol=1e-12)
+    r3 = 3 * math.sqrt(var)
+    for h in g["extent"][0]:   # 3DGS rule: ceil(3 sigma)
+        assert h == math.ceil(r3 - 1e-6) or abs(r3 - round(r3)) < 1e-4
+    g = O.gaussians(_scene([[0, 0, Z]], [[s, s, s]]), cam, tile_bound=O.TILES_FOOTPRINT)
     # footprint half extent: sqrt(2 ln(255 o) var), bounded above by the
     # tangent bound of log2 (at most 0.1 over) and the 0.1% + 0.01 px margin
     lo = math.sqrt(2 * math.log(255 * 0.9) * var)
@@ -131,9 +135,11 @@ def _footprint_ok(g, i):
     return hx, hy
 
 
-def test_tile_rect_closed_form():
+@pytest.mark.parametrize("bound", [0, 1])
+def test_tile_rect_closed_form(bound):
     """The rectangle holds exactly the tiles with a pixel centre inside the
-    footprint's bounding box [u-hx, u+hx] x [v-hy, v+hy]."""
+    box [u-hx, u+hx] x [v-hy, v+hy]: the 3-sigma square of the larger
+    eigenvalue of Sigma' (3DGS), or the footprint's bounding box."""
     W, H = 100, 70
     cam = _cam(np.eye(4), W, H)
     rng = np.random.default_rng(1)
@@ -143,17 +149,25 @@ def test_tile_rect_closed_form():
     q = rng.normal(size=(n, 4))
     q /= np.linalg.norm(q, axis=1, keepdims=True)
     opac = np.concatenate([rng.uniform(0.0, 0.012, 60), rng.uniform(0.004, 1.0, n - 60)])
-    g = O.gaussians(_scene(pts, scales, rots=q, opac=opac), cam)
+    g = O.gaussians(_scene(pts, scales, rots=q, opac=opac), cam, tile_bound=bound)
     TX, TY = 7, 5
     n_tiles = 0
     for i in range(n):
         if g["status"][i] == O.NEAR_CULLED:
             continue
-        if opac[i] < np.float32(1 / 255):
+        if bound == O.TILES_FOOTPRINT and opac[i] < np.float32(1 / 255):
             assert g["status"][i] == O.NO_TILES
             continue
         u, v = g["mean2d"][i]
-        hx, hy = _footprint_ok(g, i)
+        if bound == O.TILES_FOOTPRINT:
+            hx, hy = _footprint_ok(g, i)
+        else:
+            a, b, c = (float(x) for x in g["conic"][i])
+            det = a * c - b * b
+            lam = np.linalg.eigvalsh(np.array([[c, -b], [-b, a]]) / det).max()
+            hx = hy = float(g["extent"][i][0])
+            assert g["extent"][i][1] == hx
+            assert hx == math.ceil(3 * math.sqrt(lam)) or abs(3 * math.sqrt(lam) - round(3 * math.sqrt(lam))) < 1e-3
         tx = [k for k in range(TX) if 16 * k <= u + hx and 16 * k + 15 >= u - hx]
         ty = [k for k in range(TY) if 16 * k <= v + hy and 16 * k + 15 >= v - hy]
         if tx and ty:
@@ -167,15 +181,16 @@ def test_tile_rect_closed_form():
 
 @pytest.mark.parametrize("seed", [3, 4])
 def test_no_contribution_outside_rect(seed):
-    """At every pixel outside a Gaussian's tile rectangle its alpha, in fp64
-    from the conic, is below 1/255, so dropping it there changes nothing."""
+    """Footprint rule: at every pixel outside a Gaussian's tile rectangle its
+    alpha, in fp64 from the conic, is below 1/255, so dropping it there
+    changes nothing."""
     W, H = 90, 61
     sc = synth.small_scene(400, seed, degree=0, log_scale_mean=-2.8)
     rng = np.random.default_rng(seed)
     sc.opacities[:] = np.where(rng.random(sc.n) < 0.3, rng.uniform(0.0039, 0.02, sc.n),
                                sc.opacities).astype(np.float32)
     cam = _cam(synth.look_at((0.4, -2.6, 0.9), (0, 0, 0)), W, H)
-    g = O.gaussians(sc, cam)
+    g = O.gaussians(sc, cam, tile_bound=O.TILES_FOOTPRINT)
     ys, xs = np.mgrid[0:H, 0:W]
     tile_x, tile_y = xs // 16, ys // 16
     checked = 0
@@ -303,15 +318,20 @@ def test_blend_two_gaussians_on_one_ray():
 
 @pytest.mark.parametrize("seed,W,H", [(0, 64, 48), (1, 50, 37), (2, 33, 70)])
 def test_bruteforce_equals_tiled(seed, W, H):
+    """Tiled render = per-pixel blend of the Gaussians whose rectangle holds
+    the pixel's tile (both rules); with the footprint rule also = the blend
+    of every Gaussian at every pixel, so its rectangles drop no contribution."""
     sc = synth.small_scene(600, seed, degree=3, log_scale_mean=-3.2)
     cam = _cam(synth.look_at((0.3, -3.0, 0.8), (0, 0, 0)), W, H)
-    r = O.render_full(sc, cam)
-    bf = O.blend_bruteforce(W, H, r["g"])
+    for bound in (O.TILES_3SIGMA, O.TILES_FOOTPRINT):
+        r = O.render_full(sc, cam, tile_bound=bound)
+        bf = O.blend_bruteforce(W, H, r["g"])
+        for k in ("rgb", "D", "sigma", "alpha"):
+            assert np.array_equal(r[k], bf[k]), k
+        assert r["K"] > 0
     every = O.blend_bruteforce(W, H, r["g"], every_gaussian=True)
     for k in ("rgb", "D", "sigma", "alpha"):
-        assert np.array_equal(r[k], bf[k]), k
         assert np.array_equal(r[k], every[k]), k
-    assert r["K"] > 0
 
 
 def test_lists_sorted_and_complete():
@@ -506,10 +526,13 @@ def test_occluded_tiles_closed_form():
     R2 = 2 * var * math.log(255 * o)
     ys, xs = np.mgrid[0:H, 0:W]
     d2 = (xs - u) ** 2 + (ys - v) ** 2
+    hx, hy = g["extent"][0]
     TX, TY = W // 16, H // 16
     expect = np.zeros((TY, TX), np.uint8)
     for ty in range(TY):
         for tx in range(TX):
+            if not (16 * tx <= u + hx and 16 * tx + 15 >= u - hx and 16 * ty <= v + hy and 16 * ty + 15 >= v - hy):
+                continue
             expect[ty, tx] = (d2[16 * ty:16 * ty + 16, 16 * tx:16 * tx + 16] <= R2).any()
     assert expect.sum() >= 2
     assert np.array_equal(oc, expect)
