@@ -299,6 +299,42 @@ __global__ __launch_bounds__(256) void ranges_kernel(uint32_t K, const uint32_t 
     if (k == K - 1 || keys[k + 1] != t) ranges[t].y = k + 1;
 }
 
+// Blend order of the tiles to rasterise: longest lists first, bucketed by
+// floor(log2(length)).  Tile lists are bimodal (a few thousand long tiles
+// next to many short ones); launched in raster order, long tiles dispatched
+// last would set the blend's tail.  Tiles are independent, so the order
+// (which, within a bucket, depends on LDS atomics) changes only scheduling,
+// never a result.
+__global__ __launch_bounds__(1024) void order_tiles_kernel(int n, const int *tile_in,
+                                                           const uint2 *ranges, int *tile_out) {
+    __shared__ uint32_t s_cnt[33];
+    const int tid = threadIdx.x;
+    if (tid < 33) s_cnt[tid] = 0u;
+    __syncthreads();
+    for (int i = tid; i < n; i += 1024) {
+        const int t = tile_in ? tile_in[i] : i;
+        const uint2 r = ranges[t];
+        const uint32_t len = r.y - r.x;
+        atomicAdd(&s_cnt[len ? 32 - __clz(len) : 0], 1u);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t run = 0;
+        for (int b = 32; b >= 0; --b) {
+            const uint32_t c = s_cnt[b];
+            s_cnt[b] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += 1024) {
+        const int t = tile_in ? tile_in[i] : i;
+        const uint2 r = ranges[t];
+        const uint32_t len = r.y - r.x;
+        tile_out[atomicAdd(&s_cnt[len ? 32 - __clz(len) : 0], 1u)] = t;
+    }
+}
+
 inline uint32_t scan_parts(uint32_t n) { return (n + kScanTile - 1) / kScanTile; }
 
 }  // namespace
@@ -348,6 +384,11 @@ void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32
 
 void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st) {
     if (K > 0) ranges_kernel<<<(K + 255) / 256, 256, 0, st>>>(K, keys, ranges);
+}
+
+void launch_order_tiles(int n, const int *tile_in, const uint2 *ranges, int *tile_out,
+                        hipStream_t st) {
+    if (n > 0) order_tiles_kernel<<<1, 1024, 0, st>>>(n, tile_in, ranges, tile_out);
 }
 
 }  // namespace tgs

@@ -78,7 +78,7 @@ struct Workspace {
     DevBuf g0, g1, col, rect, status, count, partial;
     DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
-    DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt;
+    DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
     Counters *host_cnt = nullptr;
     int n = -1, W = 0, H = 0;
     size_t key_cap = 0;
@@ -118,6 +118,7 @@ struct Workspace {
             TGS_TRY(ranges.ensure(nt * sizeof(uint2)));
             TGS_TRY(sel.ensure(nt));
             TGS_TRY(sel_list.ensure(nt * sizeof(int)));
+            TGS_TRY(tile_order.ensure(nt * sizeof(int)));
             TGS_TRY(sel_cols.ensure(nt * sizeof(int)));
             TGS_TRY(rowpre.ensure((size_t)TY * (TX + 1) * sizeof(uint32_t)));
             W = W_;
@@ -421,6 +422,10 @@ tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, cons
         ProfScope ps(TGS_PROF_RANGES, st);
         launch_ranges(fr.K, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
+        // blend order: the selected tiles, or all of them, longest lists first
+        launch_order_tiles(rowpre ? (int)fr.n_sel : TX * TY, rowpre ? ws.sel_list.as<int>() : nullptr,
+                           ws.ranges.as<uint2>(), ws.tile_order.as<int>(), st);
+        TGS_LAUNCHED("tile order");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
     ws.last_K = fr.K;
@@ -662,6 +667,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
     if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
     BlendArgs a = blend_args(ws, W, H, vals);
+    a.tile_list = ws.tile_order.as<int>();
     a.rgb = out->rgb;
     a.depth = out->depth;
     a.sigma = out->sigma;
@@ -818,7 +824,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         TGS_TRY(step_keys(ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx, fr, st,
                           &vals));
         BlendArgs a = blend_args(ws, W, H, vals);
-        a.tile_list = ws.sel_list.as<int>();
+        a.tile_list = ws.tile_order.as<int>();
         a.rgb = out->rgb;
         a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
         {
@@ -847,6 +853,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, W, H, vals);
+        a.tile_list = ws.tile_order.as<int>();
         a.rgb = out->rgb;
         a.tab = s->tab.as<float>();
         a.depth = out->depth;

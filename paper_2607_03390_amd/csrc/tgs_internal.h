@@ -99,6 +99,10 @@ void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32
                       const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
                       int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
 void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st);
+// Tiles to rasterise (tile_in[0..n), or 0..n-1 when tile_in is NULL) in blend
+// order, longest lists first, into tile_out[0..n).
+void launch_order_tiles(int n, const int *tile_in, const uint2 *ranges, int *tile_out,
+                        hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
