@@ -236,7 +236,7 @@ enum { TGS_PROFILE_COUNT_PAIRS = 1, TGS_PROFILE_STAGES = 2 };
 enum {
     TGS_PROF_PREPROCESS = 0,  /* per-Gaussian stage (incl. counter reset)     */
     TGS_PROF_SCAN = 1,        /* key counts + exclusive scan                  */
-    TGS_PROF_READBACK = 2,    /* counter copy to the host (event-timed)       */
+    TGS_PROF_READBACK = 2,    /* unused: counters reach the host without a copy */
     TGS_PROF_DUPLICATE = 3,
     TGS_PROF_SORT = 4,        /* clear + histogram + all digit passes         */
     TGS_PROF_RANGES = 5,

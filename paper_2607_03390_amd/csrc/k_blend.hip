@@ -42,6 +42,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     __shared__ uint8_t s_list[4][256];
     __shared__ uint32_t s_cnt[4][4];
 
+    if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) return;   // block-uniform
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;

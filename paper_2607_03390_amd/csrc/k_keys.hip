@@ -111,11 +111,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(int n, const 
 }
 
 // One block: exclusive scan of the block sums in place; the total goes to
-// cnt->n_visible (MODE 0) or cnt->n_keys (MODE 1, saturated).
+// cnt->n_visible (MODE 0) or cnt->n_keys (MODE 1, saturated; cnt->n_sorted is
+// the same count when it fits the key capacity, else 0).
 template <int MODE>
 __global__ __launch_bounds__(1024) void scan_top_kernel(int nb, uint64_t *block_sums,
                                                         const uint32_t *pre_partial, int n_pre,
-                                                        Counters *cnt) {
+                                                        uint32_t cap, Counters *cnt,
+                                                        HostCounters *host, uint32_t tag) {
     __shared__ uint64_t s_wave[16];
     __shared__ uint64_t s_carry;
     __shared__ uint32_t s_pre[16][2];
@@ -174,8 +176,23 @@ __global__ __launch_bounds__(1024) void scan_top_kernel(int nb, uint64_t *block_
     if (threadIdx.x == 0) {
         const uint64_t total = s_carry;
         const uint32_t t32 = total > 0xffffffffull ? 0xffffffffu : (uint32_t)total;
-        if (MODE == 0) cnt->n_visible = t32;
-        else cnt->n_keys = t32;
+        if (MODE == 0) {
+            cnt->n_visible = t32;
+        } else {
+            const uint32_t sorted = t32 <= cap ? t32 : 0u;
+            cnt->n_keys = t32;
+            cnt->n_sorted = sorted;
+            // every other counter was written by an earlier kernel
+            volatile HostCounters *h = host;
+            h->n_keys = t32;
+            h->n_survivors = cnt->n_survivors;
+            h->n_newly = cnt->n_newly;
+            h->n_selected = cnt->n_selected;
+            h->n_visible = cnt->n_visible;
+            h->n_sorted = sorted;
+            __threadfence_system();
+            h->tag = tag;
+        }
     }
 }
 
@@ -227,7 +244,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(int n, const ui
 }
 
 // One output key per lane.  Wave w owns sorted positions [64w, 64w+64).
-__global__ __launch_bounds__(256) void duplicate_kernel(uint32_t V, uint32_t K,
+// Past the key capacity (cnt->n_sorted == 0 with keys) nothing is emitted:
+// the host grows the buffers and renders the frame again.
+__global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
                                                         const uint32_t *__restrict__ didx,
                                                         const uint32_t *__restrict__ offs,
                                                         const ushort4 *__restrict__ rect,
@@ -240,8 +259,9 @@ __global__ __launch_bounds__(256) void duplicate_kernel(uint32_t V, uint32_t K,
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < n_tiles; t += gridDim.x * blockDim.x)
         ranges[t] = make_uint2(0u, 0u);
+    const uint32_t V = cnt->n_visible, K = cnt->n_sorted;
     const uint32_t w0 = (blockIdx.x * 4u + (uint32_t)wave) * 64u;
-    if (w0 >= V) return;
+    if (K == 0u || w0 >= V) return;
     const uint32_t s = w0 + lane;
     const uint32_t m = V - w0 < 64u ? V - w0 : 64u;
     if (s < V) {
@@ -290,13 +310,14 @@ __global__ __launch_bounds__(256) void ranges_zero_kernel(int n_tiles, uint2 *ra
     if (t < n_tiles) ranges[t] = make_uint2(0u, 0u);
 }
 
-__global__ __launch_bounds__(256) void ranges_kernel(uint32_t K, const uint32_t *keys,
+__global__ __launch_bounds__(256) void ranges_kernel(const Counters *cnt, const uint32_t *keys,
                                                      uint2 *ranges) {
-    const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= K) return;
-    const uint32_t t = keys[k];
-    if (k == 0 || keys[k - 1] != t) ranges[t].x = k;
-    if (k == K - 1 || keys[k + 1] != t) ranges[t].y = k + 1;
+    const uint32_t K = cnt->n_sorted;
+    for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
+        const uint32_t t = keys[k];
+        if (k == 0 || keys[k - 1] != t) ranges[t].x = k;
+        if (k == K - 1 || keys[k + 1] != t) ranges[t].y = k + 1;
+    }
 }
 
 // Blend order of the tiles to rasterise: longest lists first, bucketed by
@@ -305,17 +326,48 @@ __global__ __launch_bounds__(256) void ranges_kernel(uint32_t K, const uint32_t 
 // last would set the blend's tail.  Tiles are independent, so the order
 // (which, within a bucket, depends on LDS atomics) changes only scheduling,
 // never a result.
-__global__ __launch_bounds__(1024) void order_tiles_kernel(int n, const int *tile_in,
+// Bucket of a list length: floor(log2(len)) + 1, 0 for an empty list.
+__device__ inline uint32_t length_bucket(const uint2 *ranges, int t) {
+    const uint2 r = ranges[t];
+    const uint32_t len = r.y - r.x;
+    return len ? 32u - (uint32_t)__clz(len) : 0u;
+}
+
+// Wave-aggregated LDS atomic: each distinct bucket of the wave takes one
+// atomicAdd; returns this lane's slot (old value + rank among its peers).
+__device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool active) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    uint64_t todo = __ballot(active);
+    uint32_t slot = 0;
+    while (todo) {
+        const int leader = __ffsll((long long)todo) - 1;
+        const uint32_t lb = __shfl(b, leader);
+        const uint64_t peers = __ballot(active && b == lb);
+        uint32_t base = 0;
+        if (lane == leader) base = atomicAdd(&s_cnt[lb], (uint32_t)__popcll(peers));
+        base = __shfl(base, leader);
+        if (active && b == lb) slot = base + (uint32_t)__popcll(peers & lt_mask);
+        todo &= ~peers;
+    }
+    return slot;
+}
+
+__global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uint32_t *n_dev,
+                                                           const int *tile_in,
                                                            const uint2 *ranges, int *tile_out) {
     __shared__ uint32_t s_cnt[33];
     const int tid = threadIdx.x;
+    const int n = n_dev ? (int)*n_dev : n_host;
     if (tid < 33) s_cnt[tid] = 0u;
     __syncthreads();
-    for (int i = tid; i < n; i += 1024) {
-        const int t = tile_in ? tile_in[i] : i;
-        const uint2 r = ranges[t];
-        const uint32_t len = r.y - r.x;
-        atomicAdd(&s_cnt[len ? 32 - __clz(len) : 0], 1u);
+    // loop bounds are uniform over the block so that every lane takes part
+    // in the wave-level aggregation
+    for (int c = 0; c < n; c += 1024) {
+        const int i = c + tid;
+        const bool active = i < n;
+        const uint32_t b = active ? length_bucket(ranges, tile_in ? tile_in[i] : i) : 0u;
+        (void)wave_bucket_add(s_cnt, b, active);
     }
     __syncthreads();
     if (tid == 0) {
@@ -327,11 +379,13 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n, const int *til
         }
     }
     __syncthreads();
-    for (int i = tid; i < n; i += 1024) {
-        const int t = tile_in ? tile_in[i] : i;
-        const uint2 r = ranges[t];
-        const uint32_t len = r.y - r.x;
-        tile_out[atomicAdd(&s_cnt[len ? 32 - __clz(len) : 0], 1u)] = t;
+    for (int c = 0; c < n; c += 1024) {
+        const int i = c + tid;
+        const bool active = i < n;
+        const int t = active ? (tile_in ? tile_in[i] : i) : 0;
+        const uint32_t b = active ? length_bucket(ranges, t) : 0u;
+        const uint32_t slot = wave_bucket_add(s_cnt, b, active);
+        if (active) tile_out[slot] = t;
     }
 }
 
@@ -356,39 +410,43 @@ void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32
     uint64_t *sums = static_cast<uint64_t *>(scratch);
     scan_reduce_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums);
     scan_top_kernel<0><<<1, 1024, 0, st>>>((int)nb, sums, pre_partial,
-                                           n > 0 ? preprocess_blocks(n) : 0, cnt);
+                                           n > 0 ? preprocess_blocks(n) : 0, 0u, cnt, nullptr, 0u);
     scan_down_kernel<0><<<nb, kScanThreads, 0, st>>>(n, count, nullptr, cnt, sums, g1, dkey, didx);
 }
 
 void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
-                              void *scratch, Counters *cnt, hipStream_t st) {
+                              void *scratch, Counters *cnt, uint32_t cap, HostCounters *host,
+                              uint32_t tag, hipStream_t st) {
     const uint32_t nb = scan_parts((uint32_t)(n > 0 ? n : 1));
     uint64_t *sums = static_cast<uint64_t *>(scratch);
     scan_reduce_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums);
-    scan_top_kernel<1><<<1, 1024, 0, st>>>((int)nb, sums, nullptr, 0, cnt);
+    scan_top_kernel<1><<<1, 1024, 0, st>>>((int)nb, sums, nullptr, 0, cap, cnt, host, tag);
     scan_down_kernel<1><<<nb, kScanThreads, 0, st>>>(n, count, didx, cnt, sums, nullptr, offs,
                                                      nullptr);
 }
 
-void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,
+void launch_duplicate(int n, const Counters *cnt, const uint32_t *didx, const uint32_t *offs,
                       const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
                       int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st) {
-    if (V == 0 || K == 0) {
+    if (n <= 0) {
         ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
         return;
     }
-    const uint32_t waves = (V + 63) / 64;
-    duplicate_kernel<<<(waves + 3) / 4, 256, 0, st>>>(V, K, didx, offs, rect, rowpre, sel_cols, TX,
+    const uint32_t waves = ((uint32_t)n + 63) / 64;
+    duplicate_kernel<<<(waves + 3) / 4, 256, 0, st>>>(cnt, didx, offs, rect, rowpre, sel_cols, TX,
                                                       n_tiles, tkey, tval, ranges);
 }
 
-void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st) {
-    if (K > 0) ranges_kernel<<<(K + 255) / 256, 256, 0, st>>>(K, keys, ranges);
+void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
+                   hipStream_t st) {
+    // grid-stride over at most 2048 blocks: the key count is on the device
+    const uint32_t blocks = (cap + 255) / 256 < 2048u ? (cap + 255) / 256 : 2048u;
+    if (cap > 0) ranges_kernel<<<blocks, 256, 0, st>>>(cnt, keys, ranges);
 }
 
-void launch_order_tiles(int n, const int *tile_in, const uint2 *ranges, int *tile_out,
-                        hipStream_t st) {
-    if (n > 0) order_tiles_kernel<<<1, 1024, 0, st>>>(n, tile_in, ranges, tile_out);
+void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
+                        int *tile_out, hipStream_t st) {
+    if (n > 0) order_tiles_kernel<<<1, 1024, 0, st>>>(n, n_dev, tile_in, ranges, tile_out);
 }
 
 }  // namespace tgs

@@ -8,6 +8,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
 #include <string>
 #include <vector>
 
@@ -79,7 +80,9 @@ struct Workspace {
     DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
-    Counters *host_cnt = nullptr;
+    HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
+    HostCounters *host_cnt_dev = nullptr; // its device-side address
+    uint32_t seq = 0;                     // tag of the last frame's counters
     int n = -1, W = 0, H = 0;
     size_t key_cap = 0;
     // last frame, for tgs_debug_dump
@@ -94,7 +97,12 @@ struct Workspace {
     tgs_status prepare(int n_, int W_, int H_) {
         const int TX = (W_ + 15) / 16, TY = (H_ + 15) / 16;
         const size_t nn = (size_t)(n_ > 0 ? n_ : 1);
-        if (!host_cnt) TGS_HIP(hipHostMalloc((void **)&host_cnt, sizeof(Counters), 0));
+        if (!host_cnt) {
+            TGS_HIP(hipHostMalloc((void **)&host_cnt, sizeof(HostCounters),
+                                  hipHostMallocCoherent | hipHostMallocMapped));
+            memset(host_cnt, 0, sizeof(HostCounters));
+            TGS_HIP(hipHostGetDevicePointer((void **)&host_cnt_dev, host_cnt, 0));
+        }
         if (n_ != n) {
             TGS_TRY(g0.ensure(nn * sizeof(float4)));
             TGS_TRY(g1.ensure(nn * sizeof(float4)));
@@ -128,11 +136,13 @@ struct Workspace {
         return TGS_OK;
     }
 
-    // Called after the frame's read-back (the stream is idle): grow the key
-    // buffers and the sort scratch for K keys.
-    tgs_status ensure_keys(uint32_t K, int passes) {
-        if (K > key_cap || !tkey.p) {
-            const size_t cap = (size_t)K + K / 2 + 1024;
+    // Key buffers and sort scratch for at least `want` keys (capped at the
+    // key limit).  Called before a frame is enqueued, or after an overflowed
+    // frame has drained: the stream holds no work that uses them.
+    tgs_status ensure_keys(size_t want, int passes) {
+        if (want > (size_t)kMaxKeys) want = kMaxKeys;
+        if (want > key_cap || !tkey.p) {
+            const size_t cap = want;
             TGS_TRY(tkey.ensure(cap * sizeof(uint32_t)));
             TGS_TRY(tval.ensure(cap * sizeof(uint32_t)));
             TGS_TRY(tkey_alt.ensure(cap * sizeof(uint32_t)));
@@ -343,10 +353,11 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
     return TGS_OK;
 }
 
-// Depth-order the Gaussians that have keys, scan their key counts in that
-// order, and read the counters back (the one host round trip of a frame).
-tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
-                          FrameResult &fr, const uint32_t **sorted_didx) {
+// Depth-order the Gaussians that have keys and scan their key counts in that
+// order.  The last scan kernel publishes the frame's counters to the host
+// (tag ws.seq); nothing here waits.
+tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
+                     const uint32_t **sorted_didx) {
     const uint32_t nn = (uint32_t)(n > 0 ? n : 0);
     int alt = 0;
     {
@@ -368,43 +379,69 @@ tgs_status step_scan_sync(Workspace &ws, int n, const uint32_t *rowpre, int TX, 
     const uint32_t *didx = alt ? ws.didx_alt.as<uint32_t>() : ws.didx.as<uint32_t>();
     {
         ProfScope ps(TGS_PROF_SCAN, st);
+        ws.seq += 1;
         launch_sorted_count_scan(n, didx, ws.count.as<uint32_t>(), ws.offs.as<uint32_t>(), ws.scan.p,
-                                 ws.cnt.as<Counters>(), st);
+                                 ws.cnt.as<Counters>(), (uint32_t)ws.key_cap, ws.host_cnt_dev,
+                                 ws.seq, st);
         TGS_LAUNCHED("key scan");
     }
-    {
-        ProfScope ps(TGS_PROF_READBACK, st);
-        TGS_HIP(hipMemcpyAsync(ws.host_cnt, ws.cnt.p, sizeof(Counters), hipMemcpyDeviceToHost, st));
-    }
-    // spin on the stream: a blocking wait adds tens of microseconds of wake-up
-    hipError_t q;
-    while ((q = hipStreamQuery(st)) == hipErrorNotReady) {
-    }
-    if (q != hipSuccess) return fail(TGS_ERR_DEVICE, std::string("frame read-back: ") + hipGetErrorString(q));
-    fr.K = ws.host_cnt->n_keys;
-    fr.V = ws.host_cnt->n_visible;
-    fr.n_surv = ws.host_cnt->n_survivors;
-    fr.n_newly = ws.host_cnt->n_newly;
-    fr.n_sel = ws.host_cnt->n_selected;
     *sorted_didx = didx;
-    if (fr.K > kMaxKeys)
+    return TGS_OK;
+}
+
+// Waits (spinning: a blocking wait adds tens of microseconds of wake-up) for
+// the counters of the frame enqueued last; the stream keeps working on the
+// rest of the frame meanwhile.  *overflow: the frame needed more keys than
+// the buffers hold (it rendered without keys; grow and render it again).
+tgs_status step_wait_counters(Workspace &ws, hipStream_t st, FrameResult &fr, bool *overflow) {
+    volatile HostCounters *h = ws.host_cnt;
+    for (uint32_t spins = 1; h->tag != ws.seq; ++spins) {
+        if ((spins & 4095u) == 0u) {
+            const hipError_t q = hipStreamQuery(st);
+            if (q == hipSuccess && h->tag != ws.seq)
+                return fail(TGS_ERR_DEVICE, "frame counters missing after the stream drained");
+            if (q != hipSuccess && q != hipErrorNotReady)
+                return fail(TGS_ERR_DEVICE, std::string("frame read-back: ") + hipGetErrorString(q));
+        }
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    fr.K = h->n_keys;
+    fr.V = h->n_visible;
+    fr.n_surv = h->n_survivors;
+    fr.n_newly = h->n_newly;
+    fr.n_sel = h->n_selected;
+    *overflow = fr.K > 0 && h->n_sorted == 0;
+    if (*overflow && fr.K > kMaxKeys)
         return fail(TGS_ERR_CAPACITY, "frame needs " + std::to_string(fr.K) +
                                           " Gaussian-tile keys; the limit is 2^30-1");
+    if (!*overflow) ws.last_K = fr.K;
     return TGS_OK;
+}
+
+// After an overflow: let the frame drain, then grow the key buffers.
+tgs_status grow_after_overflow(Workspace &ws, const FrameResult &fr, int passes, hipStream_t st) {
+    TGS_HIP(hipStreamSynchronize(st));
+    const size_t want = (size_t)fr.K + fr.K / 4 + 65536;
+    return ws.ensure_keys(want, passes);
+}
+
+int tile_sort_passes(int TX, int TY) {
+    int bits = 0;
+    while ((1 << bits) < TX * TY) ++bits;
+    return sort_passes_for_bits(bits);
 }
 
 // Emit the keys in depth order, sort them by tile (stable), find tile ranges;
 // returns the per-tile lists of Gaussian indices.
-tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, const int *sel_cols,
-                     const uint32_t *didx, const FrameResult &fr, hipStream_t st,
+tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpre,
+                     const int *sel_cols, const uint32_t *didx, hipStream_t st,
                      const uint32_t **sorted_vals) {
-    int bits = 0;
-    while ((1 << bits) < TX * TY) ++bits;
-    const int passes = sort_passes_for_bits(bits);
-    TGS_TRY(ws.ensure_keys(fr.K, passes));
+    const int passes = tile_sort_passes(TX, TY);
+    const uint32_t cap = (uint32_t)ws.key_cap;
+    Counters *cnt = ws.cnt.as<Counters>();
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
-        launch_duplicate(fr.V, fr.K, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
+        launch_duplicate(n, cnt, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
                          sel_cols, TX, TX * TY, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
                          ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("duplicate");
@@ -412,23 +449,23 @@ tgs_status step_keys(Workspace &ws, int TX, int TY, const uint32_t *rowpre, cons
     int alt = 0;
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        alt = launch_sort_u32(nullptr, fr.K, 0, passes, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
-                              ws.tkey_alt.as<uint32_t>(), ws.tval_alt.as<uint32_t>(),
-                              ws.sort.as<uint32_t>(), st);
+        alt = launch_sort_u32(&cnt->n_sorted, cap, 0, passes, ws.tkey.as<uint32_t>(),
+                              ws.tval.as<uint32_t>(), ws.tkey_alt.as<uint32_t>(),
+                              ws.tval_alt.as<uint32_t>(), ws.sort.as<uint32_t>(), st);
         TGS_LAUNCHED("tile sort");
     }
     const uint32_t *skeys = alt ? ws.tkey_alt.as<uint32_t>() : ws.tkey.as<uint32_t>();
     {
         ProfScope ps(TGS_PROF_RANGES, st);
-        launch_ranges(fr.K, skeys, ws.ranges.as<uint2>(), st);
+        launch_ranges(cap, cnt, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
         // blend order: the selected tiles, or all of them, longest lists first
-        launch_order_tiles(rowpre ? (int)fr.n_sel : TX * TY, rowpre ? ws.sel_list.as<int>() : nullptr,
-                           ws.ranges.as<uint2>(), ws.tile_order.as<int>(), st);
+        launch_order_tiles(TX * TY, rowpre ? &cnt->n_selected : nullptr,
+                           rowpre ? ws.sel_list.as<int>() : nullptr, ws.ranges.as<uint2>(),
+                           ws.tile_order.as<int>(), st);
         TGS_LAUNCHED("tile order");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
-    ws.last_K = fr.K;
     ws.last_keys = skeys;
     ws.last_vals = *sorted_vals;
     ws.has_frame = true;
@@ -660,25 +697,33 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     Workspace &ws = sc->ws;
     TGS_TRY(ws.prepare(sc->n, W, H));
     const CamK ck = make_camk(cam);
-    TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
+    const int passes = tile_sort_passes(TX, TY);
+    TGS_TRY(ws.ensure_keys(ws.key_cap ? ws.key_cap : 4 * (size_t)sc->n + 65536, passes));
     FrameResult fr;
-    const uint32_t *didx = nullptr, *vals = nullptr;
-    TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
-    TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
-    if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
-    BlendArgs a = blend_args(ws, W, H, vals);
-    a.tile_list = ws.tile_order.as<int>();
-    a.rgb = out->rgb;
-    a.depth = out->depth;
-    a.sigma = out->sigma;
-    a.alpha = out->alpha;
-    a.contrib = out->contrib;
-    a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
-    {
-        hipEvent_t ev0, ev1;
-        g_prof.kernel_events(TGS_PROF_BLEND_FULL, &ev0, &ev1);
-        launch_blend(a, TX * TY, st, ev0, ev1);
-        TGS_LAUNCHED("blend");
+    for (;;) {
+        TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
+        const uint32_t *didx = nullptr, *vals = nullptr;
+        TGS_TRY(step_scan(ws, sc->n, nullptr, TX, st, &didx));
+        TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, nullptr, didx, st, &vals));
+        if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
+        BlendArgs a = blend_args(ws, W, H, vals);
+        a.tile_list = ws.tile_order.as<int>();
+        a.rgb = out->rgb;
+        a.depth = out->depth;
+        a.sigma = out->sigma;
+        a.alpha = out->alpha;
+        a.contrib = out->contrib;
+        a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
+        {
+            hipEvent_t ev0, ev1;
+            g_prof.kernel_events(TGS_PROF_BLEND_FULL, &ev0, &ev1);
+            launch_blend(a, TX * TY, st, ev0, ev1);
+            TGS_LAUNCHED("blend");
+        }
+        bool overflow = false;
+        TGS_TRY(step_wait_counters(ws, st, fr, &overflow));
+        if (!overflow) break;
+        TGS_TRY(grow_after_overflow(ws, fr, passes, st));
     }
     if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)TX * TY, 1, st);
     TGS_LAUNCHED("tile mask");
@@ -766,121 +811,132 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
     else
         kind = TGS_FRAME_TGS;
 
+    const int passes = tile_sort_passes(TX, TY);
+    TGS_TRY(ws.ensure_keys(ws.key_cap ? ws.key_cap : 4 * (size_t)sc->n + 65536, passes));
     FrameResult fr;
-    const uint32_t *vals = nullptr;
-    if (kind == TGS_FRAME_TGS) {
-        WarpK w{};
-        relative_pose(s->ref_w2c, cam->world_to_cam, w.M, w.Minv);
-        for (int k = 0; k < 4; ++k) w.kref[k] = s->ref_intr[k];
-        w.kcur[0] = cam->fx;
-        w.kcur[1] = cam->fy;
-        w.kcur[2] = cam->cx;
-        w.kcur[3] = cam->cy;
-        w.z_near = p.z_near;
-        w.W = W;
-        w.H = H;
-        w.TX = TX;
-        w.TY = TY;
-        {
-            ProfScope ps(TGS_PROF_WARP, st);
-            launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
-                                 s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
-            launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
-                                s->smax.as<float>(), st);
-            TGS_LAUNCHED("warp");
-        }
-        {
-            ProfScope ps(TGS_PROF_FILL_QUERY, st);
-            launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
-                              s->um.as<uint8_t>(), st);
-            TGS_LAUNCHED("fill query");
-        }
-        CullK cull = no_cull(p.z_near, ws);
-        cull.afc = p.enable_afc;
-        cull.fbox = s->fbox.as<int>();
-        cull.toc = p.enable_toc;
-        cull.dmin = s->dmin.as<float>();
-        cull.smax = s->smax.as<float>();
-        cull.g_rendered = s->g_flag.as<uint8_t>();
-        cull.lambda1 = p.lambda1;
-        cull.lambda2 = p.lambda2;
-        TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
-        {
-            ProfScope ps(TGS_PROF_OCCLUDED, st);
-            launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g0.as<float4>(),
-                            ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
-            TGS_LAUNCHED("occluded tiles");
-        }
-        const int mode = (!p.enable_sr || p.force_all_dirty) ? 1 : 0;
-        {
-            ProfScope ps(TGS_PROF_SELECT, st);
-            launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(),
-                          ws.sel.as<uint8_t>(), ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(),
-                          ws.sel_cols.as<int>(), out->tile_mask, ws.cnt.as<Counters>(), st);
-            TGS_LAUNCHED("tile selection");
-        }
-        const uint32_t *didx = nullptr;
-        TGS_TRY(step_scan_sync(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, fr, &didx));
-        TGS_TRY(step_keys(ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx, fr, st,
-                          &vals));
-        BlendArgs a = blend_args(ws, W, H, vals);
-        a.tile_list = ws.tile_order.as<int>();
-        a.rgb = out->rgb;
-        a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
-        {
-            hipEvent_t ev0, ev1;
-            g_prof.kernel_events(TGS_PROF_BLEND_TGS, &ev0, &ev1);
-            launch_blend(a, (int)fr.n_sel, st, ev0, ev1);
-            TGS_LAUNCHED("blend");
-        }
-        {
-            ProfScope ps(TGS_PROF_STITCH, st);
-            launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
-                          out->rgb, st);
-            TGS_LAUNCHED("stitch");
-        }
-    } else {
-        CullK cull = no_cull(p.z_near, ws);
-        cull.afc = (kind == TGS_FRAME_PSEUDO_REF && p.enable_afc) ? 1 : 0;
-        cull.fbox = s->fbox.as<int>();
-        {
-            ProfScope ps(TGS_PROF_CAPTURE, st);
-            launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
-        }
-        TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
-        const uint32_t *didx = nullptr;
-        TGS_TRY(step_scan_sync(ws, sc->n, nullptr, TX, st, fr, &didx));
-        TGS_TRY(step_keys(ws, TX, TY, nullptr, nullptr, didx, fr, st, &vals));
-        if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
-        BlendArgs a = blend_args(ws, W, H, vals);
-        a.tile_list = ws.tile_order.as<int>();
-        a.rgb = out->rgb;
-        a.tab = s->tab.as<float>();
-        a.depth = out->depth;
-        a.sigma = out->sigma;
-        a.alpha = out->alpha;
-        a.tgb_depth = s->tgb_d.as<float>();
-        a.tgb_sigma = s->tgb_s.as<float>();
-        a.g_flag = s->g_flag.as<uint8_t>();
-        a.contrib = out->contrib;
-        a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
-        {
-            hipEvent_t ev0, ev1;
-            g_prof.kernel_events(TGS_PROF_BLEND_REF, &ev0, &ev1);
-            launch_blend(a, nt, st, ev0, ev1);
-            TGS_LAUNCHED("blend");
-        }
-        {
-            ProfScope ps(TGS_PROF_CAPTURE, st);
-            if (kind == TGS_FRAME_TRUE_REF) {
-                launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
-                                  s->fbox.as<int>(), st);
-                TGS_LAUNCHED("adaptive frustum");
+    for (;;) {
+        const uint32_t *vals = nullptr;
+        if (kind == TGS_FRAME_TGS) {
+            WarpK w{};
+            relative_pose(s->ref_w2c, cam->world_to_cam, w.M, w.Minv);
+            for (int k = 0; k < 4; ++k) w.kref[k] = s->ref_intr[k];
+            w.kcur[0] = cam->fx;
+            w.kcur[1] = cam->fy;
+            w.kcur[2] = cam->cx;
+            w.kcur[3] = cam->cy;
+            w.z_near = p.z_near;
+            w.W = W;
+            w.H = H;
+            w.TX = TX;
+            w.TY = TY;
+            {
+                ProfScope ps(TGS_PROF_WARP, st);
+                launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
+                                     s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
+                launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
+                                    s->smax.as<float>(), st);
+                TGS_LAUNCHED("warp");
             }
-            if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
-            launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
-            TGS_LAUNCHED("tile mask");
+            {
+                ProfScope ps(TGS_PROF_FILL_QUERY, st);
+                launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
+                                  s->um.as<uint8_t>(), st);
+                TGS_LAUNCHED("fill query");
+            }
+            CullK cull = no_cull(p.z_near, ws);
+            cull.afc = p.enable_afc;
+            cull.fbox = s->fbox.as<int>();
+            cull.toc = p.enable_toc;
+            cull.dmin = s->dmin.as<float>();
+            cull.smax = s->smax.as<float>();
+            cull.g_rendered = s->g_flag.as<uint8_t>();
+            cull.lambda1 = p.lambda1;
+            cull.lambda2 = p.lambda2;
+            TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
+            {
+                ProfScope ps(TGS_PROF_OCCLUDED, st);
+                launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g0.as<float4>(),
+                                ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
+                TGS_LAUNCHED("occluded tiles");
+            }
+            const int mode = (!p.enable_sr || p.force_all_dirty) ? 1 : 0;
+            {
+                ProfScope ps(TGS_PROF_SELECT, st);
+                launch_select(TX, TY, mode, s->oc.as<uint8_t>(), s->um.as<uint8_t>(),
+                              ws.sel.as<uint8_t>(), ws.sel_list.as<int>(), ws.rowpre.as<uint32_t>(),
+                              ws.sel_cols.as<int>(), out->tile_mask, ws.cnt.as<Counters>(), st);
+                TGS_LAUNCHED("tile selection");
+            }
+            const uint32_t *didx = nullptr;
+            TGS_TRY(step_scan(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, &didx));
+            TGS_TRY(step_keys(ws, sc->n, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx,
+                              st, &vals));
+            BlendArgs a = blend_args(ws, W, H, vals);
+            a.tile_list = ws.tile_order.as<int>();
+            a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
+            a.rgb = out->rgb;
+            a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
+            {
+                hipEvent_t ev0, ev1;
+                g_prof.kernel_events(TGS_PROF_BLEND_TGS, &ev0, &ev1);
+                launch_blend(a, nt, st, ev0, ev1);
+                TGS_LAUNCHED("blend");
+            }
+            {
+                ProfScope ps(TGS_PROF_STITCH, st);
+                launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
+                              out->rgb, st);
+                TGS_LAUNCHED("stitch");
+            }
+        } else {
+            CullK cull = no_cull(p.z_near, ws);
+            cull.afc = (kind == TGS_FRAME_PSEUDO_REF && p.enable_afc) ? 1 : 0;
+            cull.fbox = s->fbox.as<int>();
+            {
+                ProfScope ps(TGS_PROF_CAPTURE, st);
+                launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
+            }
+            TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
+            const uint32_t *didx = nullptr;
+            TGS_TRY(step_scan(ws, sc->n, nullptr, TX, st, &didx));
+            TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, nullptr, didx, st, &vals));
+            if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
+            BlendArgs a = blend_args(ws, W, H, vals);
+            a.tile_list = ws.tile_order.as<int>();
+            a.rgb = out->rgb;
+            a.tab = s->tab.as<float>();
+            a.depth = out->depth;
+            a.sigma = out->sigma;
+            a.alpha = out->alpha;
+            a.tgb_depth = s->tgb_d.as<float>();
+            a.tgb_sigma = s->tgb_s.as<float>();
+            a.g_flag = s->g_flag.as<uint8_t>();
+            a.contrib = out->contrib;
+            a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
+            {
+                hipEvent_t ev0, ev1;
+                g_prof.kernel_events(TGS_PROF_BLEND_REF, &ev0, &ev1);
+                launch_blend(a, nt, st, ev0, ev1);
+                TGS_LAUNCHED("blend");
+            }
+            {
+                ProfScope ps(TGS_PROF_CAPTURE, st);
+                if (kind == TGS_FRAME_TRUE_REF) {
+                    launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
+                                      s->fbox.as<int>(), st);
+                    TGS_LAUNCHED("adaptive frustum");
+                }
+                if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
+                launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
+                TGS_LAUNCHED("tile mask");
+            }
         }
+        bool overflow = false;
+        TGS_TRY(step_wait_counters(ws, st, fr, &overflow));
+        if (!overflow) break;
+        TGS_TRY(grow_after_overflow(ws, fr, passes, st));
+    }
+    if (kind != TGS_FRAME_TGS) {
         memcpy(s->ref_w2c, cam->world_to_cam, sizeof(s->ref_w2c));
         s->ref_intr[0] = cam->fx;
         s->ref_intr[1] = cam->fy;

@@ -64,7 +64,17 @@ struct Counters {
     uint32_t n_newly;
     uint32_t n_selected;
     uint32_t n_visible;       // Gaussians with at least one key
-    uint32_t pad[3];
+    uint32_t n_sorted;        // keys emitted and sorted: n_keys, or 0 past the key capacity
+    uint32_t pad[2];
+};
+
+// The frame's counters as the host reads them: written by the last counting
+// kernel straight into coherent pinned host memory, tag last (after a
+// system-scope fence), so the host waits for the tag instead of a copy.
+struct HostCounters {
+    uint32_t n_keys, n_survivors, n_newly, n_selected, n_visible, n_sorted;
+    uint32_t pad;
+    uint32_t tag;
 };
 
 // Ordered-int encoding of a float: signed-int order equals float order, so
@@ -91,18 +101,26 @@ void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int
 void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
                           uint32_t *didx, void *scratch, const uint32_t *pre_partial,
                           Counters *cnt, hipStream_t st);
+// Also sets cnt->n_sorted = n_keys when n_keys <= cap, else 0, then copies
+// the counters to `host` and sets host->tag = tag.
 void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
-                              void *scratch, Counters *cnt, hipStream_t st);
-// Also clears the tile ranges (filled by launch_ranges after the tile sort).
+                              void *scratch, Counters *cnt, uint32_t cap, HostCounters *host,
+                              uint32_t tag, hipStream_t st);
+// Emits the cnt->n_sorted keys of the cnt->n_visible depth-ordered Gaussians
+// (n bounds n_visible for the grid; nothing is emitted past the key capacity)
+// and clears the tile ranges (filled by launch_ranges after the tile sort).
 // rowpre / sel_cols are NULL in frames that render every tile.
-void launch_duplicate(uint32_t V, uint32_t K, const uint32_t *didx, const uint32_t *offs,
+void launch_duplicate(int n, const Counters *cnt, const uint32_t *didx, const uint32_t *offs,
                       const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
                       int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
-void launch_ranges(uint32_t K, const uint32_t *keys, uint2 *ranges, hipStream_t st);
-// Tiles to rasterise (tile_in[0..n), or 0..n-1 when tile_in is NULL) in blend
-// order, longest lists first, into tile_out[0..n).
-void launch_order_tiles(int n, const int *tile_in, const uint2 *ranges, int *tile_out,
-                        hipStream_t st);
+// Ranges of the cnt->n_sorted tile-sorted keys; cap bounds n_sorted for the grid.
+void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
+                   hipStream_t st);
+// Tiles to rasterise (tile_in[0..m), or 0..m-1 when tile_in is NULL; m =
+// *n_dev when n_dev is given, else n) in blend order, longest lists first,
+// into tile_out[0..m).
+void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
+                        int *tile_out, hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
@@ -118,6 +136,7 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
 struct BlendArgs {
     int W, H, TX, TY;
     const int *tile_list;     // NULL: blockIdx = tile
+    const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
     const uint2 *ranges;
     const uint32_t *vals;
     const float4 *g0, *g1, *col;

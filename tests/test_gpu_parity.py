@@ -105,6 +105,23 @@ def test_full_parity_object_subset():
     _full_parity(w.scene, [w.cameras[0], w.cameras[37]], label="object 40k")
 
 
+def test_key_capacity_growth():
+    """Frames whose Gaussian-tile keys exceed the key buffers (first sized
+    4N + 65536) render again after the buffers grow: a few thousand large
+    Gaussians seen from ever closer, so the capacity grows more than once."""
+    sc = synth.small_scene(3000, 11, degree=1, log_scale_mean=-1.6)
+    cams = [synth.make_camera(synth.look_at((0.0, -d, 0.4 * d), (0, 0, 0)), 512, 384)
+            for d in (3.2, 2.2, 1.5)]
+    g = O.gaussians(sc, cams[-1])
+    vis = g["status"] == O.VISIBLE
+    r = g["rect"][vis]
+    K = int(((r[:, 2] - r[:, 0] + 1) * (r[:, 3] - r[:, 1] + 1)).sum())
+    assert K > 2 * (4 * sc.n + 65536), K
+    _full_parity(sc, cams, label="capacity growth")
+    st = _temporal_parity(sc, cams, 512, 384, "capacity growth")
+    assert st["frames"] == 3
+
+
 def test_empty_and_invisible_scenes():
     import torch
     sc = synth.small_scene(0, 0, degree=0)
