@@ -208,6 +208,7 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
         }
         rec.rect[i] = rect;
         rec.count[i] = keys;
+        rec.dkey[i] = __float_as_uint(tz);
         rec.status[i] = (uint8_t)((survivor ? 1 : 0) | (newly ? 2 : 0));
     }
 

@@ -1,7 +1,7 @@
 // LSD radix sort of (uint32 key, uint32 value) pairs, 8-bit digits, for the
 // two sorts of a frame (Sec. III-A, per-tile depth order):
-//  1. the visible Gaussians by depth (float bits of a positive depth are
-//     ordered like the depths), input in Gaussian index order;
+//  1. the Gaussians that have keys, by depth (float bits of a positive depth
+//     are ordered like the depths), input in Gaussian index order;
 //  2. the Gaussian-tile keys by tile id, input in depth order.
 // Both sorts are stable, so each tile's list ends up ordered by
 // (depth bits, Gaussian index): deterministic and identical to a direct sort
@@ -9,18 +9,26 @@
 // passes run over the Gaussians, not over their tile copies).
 //
 // Structure for gfx950, per 8-bit pass: an upsweep kernel counts each
-// partition's digits (1024 keys per partition up to 2M keys, 3840 above), a column scan turns those counts into
-// per-(digit, partition) offsets and digit totals, and a downsweep kernel
-// ranks each partition in LDS and scatters it (the digit bases are a block
-// scan of the 256 totals).  No block ever waits on another and no
-// device-wide atomic is contended (same-address atomics serialise across the
-// eight XCDs), so the sort is deterministic and needs no forward-progress
-// assumption.  Ranking is stable (a wave's 64-lane match over the digit bits
-// plus per-wave digit counters in input order).  Keys are staged in LDS in
-// digit order before the scatter so that writes of one digit run are
-// contiguous.  The key count may live on the device (grids sized for an upper
-// bound; partitions past the count do no work and are not scanned), so no
-// host round trip is needed.
+// partition's digits (1024 keys per partition up to 2M keys, 3840 above), a
+// column scan turns those counts into per-(digit, partition) offsets and
+// digit totals, and a downsweep kernel ranks each partition in LDS and
+// scatters it (the digit bases are a block scan of the 256 totals).  No block
+// ever waits on another and no device-wide atomic is contended (same-address
+// atomics serialise across the eight XCDs), so the sort is deterministic and
+// needs no forward-progress assumption.  Ranking is stable (a wave's 64-lane
+// match over the digit bits plus per-wave digit counters in input order).
+// Keys are staged in LDS in digit order before the scatter so that writes of
+// one digit run are contiguous.  Key counts live on the device (grids sized
+// for an upper bound; partitions past the count do no work and are not
+// scanned), so no host round trip is needed.
+//
+// The depth sort folds two neighbouring steps into its first and last pass:
+//  - the first pass reads every Gaussian and keeps those with a key count
+//    above zero (the compaction), writing the number kept;
+//  - the last pass also carries each Gaussian's key count as a weight and
+//    writes, at each sorted position, the exclusive prefix of the weights:
+//    where the Gaussian's tile keys start.  It publishes the frame's
+//    counters to the host.
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -35,78 +43,100 @@ constexpr int kRadix = 256;
 constexpr int kIptLarge = 15;   // 3840-key partitions
 constexpr int kIptSmall = 4;    // 1024-key partitions
 
+enum { kPlain = 0, kFirst = 1, kLast = 2 };
+
 __device__ inline uint32_t key_count(const uint32_t *n_dev, uint32_t n_host) {
     return n_dev ? *n_dev : n_host;
 }
 
-__device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave) {
+__device__ inline uint32_t sat32(uint64_t v) { return v > 0xffffffffull ? 0xffffffffu : (uint32_t)v; }
+
+template <typename T>
+__device__ inline T block_exclusive_scan256(T v, T *s_wave, T *total = nullptr) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    uint32_t inc = v;
+    T inc = v;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t o = __shfl_up(inc, d);
+        const T o = __shfl_up(inc, d);
         if (lane >= d) inc += o;
     }
     if (lane == 63) s_wave[wave] = inc;
     __syncthreads();
-    uint32_t off = 0;
+    T off = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-        if (w < wave) off += s_wave[w];
+    for (int w = 0; w < 4; ++w) {
+        const T x = s_wave[w];
+        if (w < wave) off += x;
+        tot += x;
+    }
     __syncthreads();
+    if (total) *total = tot;
     return off + inc - v;
 }
 
-// Digit counts of one partition: counts[d * np + part].
-template <int IPT>
-__global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(const uint32_t *__restrict__ kin,
-                                                                    const uint32_t *n_dev,
-                                                                    uint32_t n_host, int shift,
-                                                                    uint32_t np, uint32_t *counts) {
+// Digit counts of one partition: counts[d * np + part]; in the last depth
+// pass also the digit's weight sum: weights[d * np + part].
+template <int IPT, int MODE>
+__global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
+    const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint32_t *n_dev,
+    uint32_t n_host, int shift, uint32_t np, const uint32_t *__restrict__ count, uint32_t *counts,
+    uint32_t *weights) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ uint32_t s_h[4][kRadix];
+    __shared__ uint32_t s_w[MODE == kLast ? 4 : 1][kRadix];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t K = key_count(n_dev, n_host);
+    const uint32_t K = MODE == kFirst ? n_host : key_count(n_dev, n_host);
     const uint32_t part = blockIdx.x;
     if (part * kTile >= K) return;   // block-uniform: beyond the keys
-    for (int k = tid; k < 4 * kRadix; k += kSortThreads) (&s_h[0][0])[k] = 0u;
+    for (int k = tid; k < 4 * kRadix; k += kSortThreads) {
+        (&s_h[0][0])[k] = 0u;
+        if (MODE == kLast) (&s_w[0][0])[k] = 0u;
+    }
     __syncthreads();
     const uint32_t wbase = part * kTile + (uint32_t)wave * (64u * IPT);
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        if (idx < K) atomicAdd(&s_h[wave][(kin[idx] >> shift) & 255u], 1u);
+        if (idx < K && (MODE != kFirst || count[idx] > 0u)) {
+            const uint32_t d = (kin[idx] >> shift) & 255u;
+            atomicAdd(&s_h[wave][d], 1u);
+            if (MODE == kLast) atomicAdd(&s_w[wave][d], count[vin[idx]]);
+        }
     }
     __syncthreads();
     counts[(size_t)tid * np + part] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
+    if (MODE == kLast)
+        weights[(size_t)tid * np + part] = s_w[0][tid] + s_w[1][tid] + s_w[2][tid] + s_w[3][tid];
 }
 
-// One block per digit: exclusive scan of the digit's counts over the
-// partitions that hold keys (in place) and the digit's total.  Each thread
-// scans 8 consecutive partitions, so one round covers 2048 partitions.
+// One block per (table, digit): exclusive scan of the digit's counts (table
+// 0) or weights (table 1) over the partitions that hold keys, in place, and
+// the digit's total; 64-bit running sums, stored saturated to 32 bits.  Each
+// thread scans 8 consecutive partitions, so one round covers 2048 partitions.
 __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev, uint32_t n_host,
                                                            uint32_t tile, uint32_t np,
                                                            uint32_t *counts, uint32_t *totals) {
-    __shared__ uint32_t s_scan[4];
-    __shared__ uint32_t s_run;
-    const int d = blockIdx.x;
+    __shared__ uint64_t s_scan[4];
+    __shared__ uint64_t s_run;
+    const int d = blockIdx.x & (kRadix - 1), table = blockIdx.x / kRadix;
     const uint32_t K = key_count(n_dev, n_host);
     const uint32_t npa = (K + tile - 1) / tile;   // <= np
-    uint32_t run = 0;
-    uint32_t *col = counts + (size_t)d * np;
+    uint64_t run = 0;
+    uint32_t *col = counts + (size_t)table * kRadix * np + (size_t)d * np;
     for (uint32_t c = 0; c < npa; c += 2048) {
         const uint32_t p0 = c + 8u * threadIdx.x;
-        uint32_t v[8], sum = 0;
+        uint32_t v[8];
+        uint64_t sum = 0;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             v[j] = p0 + j < npa ? col[p0 + j] : 0u;
             sum += v[j];
         }
-        const uint32_t ex = block_exclusive_scan256(sum, s_scan);
-        uint32_t o = run + ex;
+        const uint64_t ex = block_exclusive_scan256<uint64_t>(sum, s_scan);
+        uint64_t o = run + ex;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            if (p0 + j < npa) col[p0 + j] = o;
+            if (p0 + j < npa) col[p0 + j] = sat32(o);
             o += v[j];
         }
         if (threadIdx.x == 255) s_run = o;
@@ -114,46 +144,124 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
         run = s_run;
         __syncthreads();
     }
-    if (threadIdx.x == 0) totals[d] = run;
+    if (threadIdx.x == 0) totals[table * kRadix + d] = sat32(run);
 }
 
-template <int IPT>
+// Operands of the first and last depth-sort passes.
+struct DepthIo {
+    const uint32_t *count;      // key count per Gaussian
+    uint32_t *offs;             // last pass: start of each sorted Gaussian's keys
+    Counters *cnt;
+    HostCounters *host;         // last pass: the frame's counters, tag last
+    uint32_t tag, cap;
+    const uint32_t *pre_partial;   // preprocess per-block survivor / newly-visible counts
+    int n_pre;
+};
+
+// Last depth pass, block 0: the frame's totals to the device counters and,
+// tag last, to the host.
+__device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s_red) {
+    const int tid = threadIdx.x;
+    uint32_t a = 0, b = 0;
+    for (int k = tid; k < io.n_pre; k += kSortThreads) {
+        a += io.pre_partial[2 * k];
+        b += io.pre_partial[2 * k + 1];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        a += __shfl_xor(a, o);
+        b += __shfl_xor(b, o);
+    }
+    if ((tid & 63) == 0) {
+        s_red[2 * (tid >> 6)] = a;
+        s_red[2 * (tid >> 6) + 1] = b;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t surv = s_red[0] + s_red[2] + s_red[4] + s_red[6];
+        const uint32_t newly = s_red[1] + s_red[3] + s_red[5] + s_red[7];
+        const uint32_t k32 = sat32(n_keys);
+        const uint32_t sorted = k32 <= io.cap ? k32 : 0u;
+        io.cnt->n_keys = k32;
+        io.cnt->n_sorted = sorted;
+        io.cnt->n_survivors = surv;
+        io.cnt->n_newly = newly;
+        // n_visible and n_selected were written by earlier kernels
+        volatile HostCounters *h = io.host;
+        h->n_keys = k32;
+        h->n_survivors = surv;
+        h->n_newly = newly;
+        h->n_selected = io.cnt->n_selected;
+        h->n_visible = io.cnt->n_visible;
+        h->n_sorted = sorted;
+        __threadfence_system();
+        h->tag = io.tag;
+    }
+    __syncthreads();
+}
+
+template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
     uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
-    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ totals) {
+    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ totals, DepthIo io) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ uint32_t s_keys[kTile];
     __shared__ uint32_t s_vals[kTile];
+    __shared__ uint32_t s_wt[MODE == kLast ? kTile : 1];   // weights, then their exclusive scan
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
     __shared__ uint32_t s_dstart[kRadix];     // block-local start of each digit
     __shared__ uint32_t s_gbase[kRadix];      // global start of this block's digit run
+    __shared__ uint32_t s_wbase[MODE == kLast ? kRadix : 1];   // global weight prefix of the run
     __shared__ uint32_t s_scan[4];
+    __shared__ uint64_t s_scan64[4];
+    __shared__ uint32_t s_nvalid;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t K = key_count(n_dev, n_host);
+    const uint32_t K = MODE == kFirst ? n_host : key_count(n_dev, n_host);
     const uint32_t part = blockIdx.x;
     const uint32_t base = part * kTile;
+    // block 0 publishes the pass's totals (also when there is nothing to sort)
+    if (MODE == kFirst && part == 0) {
+        uint32_t n_kept;
+        (void)block_exclusive_scan256<uint32_t>(totals[tid], s_scan, &n_kept);
+        if (tid == 0) io.cnt->n_visible = n_kept;
+    }
+    if (MODE == kLast && part == 0) {
+        uint64_t n_keys;
+        (void)block_exclusive_scan256<uint64_t>(totals[kRadix + tid], s_scan64, &n_keys);
+        publish_counters(io, n_keys, s_wh);
+    }
     if (base >= K) return;   // block-uniform
     for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
     // global start of digit tid: digits below it, then partitions before this one
-    s_gbase[tid] = block_exclusive_scan256(totals[tid], s_scan) + offsets[(size_t)tid * np + part];
+    s_gbase[tid] = block_exclusive_scan256<uint32_t>(totals[tid], s_scan) +
+                   offsets[(size_t)tid * np + part];
+    if (MODE == kLast) {
+        const uint64_t wb = block_exclusive_scan256<uint64_t>(totals[kRadix + tid], s_scan64);
+        s_wbase[tid] = sat32(wb + offsets[(size_t)kRadix * np + (size_t)tid * np + part]);
+    }
     __syncthreads();
     const uint32_t wbase = base + (uint32_t)wave * (64u * IPT);
     const uint64_t lt_mask = (1ull << lane) - 1ull;
 
     uint32_t key[IPT], val[IPT], rank[IPT];
+    bool ok[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        const bool valid = idx < K;
-        key[j] = valid ? kin[idx] : 0xffffffffu;
-        val[j] = valid ? vin[idx] : 0u;
+        ok[j] = idx < K;
+        key[j] = ok[j] ? kin[idx] : 0xffffffffu;
+        if (MODE == kFirst) {
+            val[j] = idx;
+            ok[j] = ok[j] && io.count[idx] > 0u;
+        } else {
+            val[j] = ok[j] ? vin[idx] : 0u;
+        }
     }
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
-        const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        const bool valid = idx < K;
+        const bool valid = ok[j];
         const uint32_t d = (key[j] >> shift) & 255u;
         uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -181,27 +289,52 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     s_wh[kRadix + d] = c0;
     s_wh[2 * kRadix + d] = c0 + c1;
     s_wh[3 * kRadix + d] = c0 + c1 + c2;
-    s_dstart[d] = block_exclusive_scan256(total, s_scan);
+    uint32_t n_valid;
+    s_dstart[d] = block_exclusive_scan256<uint32_t>(total, s_scan, &n_valid);
+    if (tid == 0) s_nvalid = n_valid;
     __syncthreads();
 
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
-        const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        if (idx < K) {
+        if (ok[j]) {
             const uint32_t dj = (key[j] >> shift) & 255u;
             const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rank[j];
             s_keys[pos] = key[j];
             s_vals[pos] = val[j];
+            if (MODE == kLast) s_wt[pos] = io.count[val[j]];
         }
     }
     __syncthreads();
+    const uint32_t nv = s_nvalid;
 
-    const uint32_t n_valid = K - base < kTile ? K - base : kTile;
-    for (uint32_t i = tid; i < n_valid; i += kSortThreads) {
+    if (MODE == kLast) {
+        // exclusive scan of the weights in staged (digit, then input) order
+        uint32_t w[IPT], sum = 0;
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            const uint32_t p = (uint32_t)tid * IPT + j;
+            w[j] = p < nv ? s_wt[p] : 0u;
+            sum += w[j];
+        }
+        uint32_t o = block_exclusive_scan256<uint32_t>(sum, s_scan);
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            const uint32_t p = (uint32_t)tid * IPT + j;
+            if (p < nv) s_wt[p] = o;
+            o += w[j];
+        }
+        __syncthreads();
+    }
+
+    for (uint32_t i = tid; i < nv; i += kSortThreads) {
         const uint32_t kk = s_keys[i];
         const uint32_t dj = (kk >> shift) & 255u;
         const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
-        kout[out] = kk;
+        if (MODE == kLast) {
+            io.offs[out] = s_wbase[dj] + (s_wt[i] - s_wt[s_dstart[dj]]);
+        } else {
+            kout[out] = kk;
+        }
         vout[out] = s_vals[i];
     }
 }
@@ -209,22 +342,43 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
 inline int ipt_for(uint32_t n_max) { return n_max <= (2u << 20) ? kIptSmall : kIptLarge; }
 inline uint32_t n_partitions(uint32_t K, int ipt) {
     const uint32_t tile = (uint32_t)(kSortThreads * ipt);
-    return (K + tile - 1) / tile;
+    const uint32_t np = (K + tile - 1) / tile;
+    return np ? np : 1u;
+}
+
+template <int IPT, int MODE>
+void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *ki,
+              const uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, const DepthIo &io,
+              hipStream_t st) {
+    // at least one block: the last depth pass always publishes the counters
+    const uint32_t np = n_partitions(n_max, IPT);
+    uint32_t *totals = scratch;                    // [2][256]
+    uint32_t *table = scratch + 2 * kRadix;        // [2][256][np]
+    const uint32_t *nd = MODE == kFirst ? nullptr : n_dev;
+    sort_upsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(
+        ki, vi, nd, n_max, shift, np, io.count, table, table + (size_t)kRadix * np);
+    sort_colscan_kernel<<<MODE == kLast ? 2 * kRadix : kRadix, 256, 0, st>>>(
+        nd, n_max, kSortThreads * IPT, np, table, totals);
+    sort_downsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
+                                                                  np, table, totals, io);
 }
 
 template <int IPT>
-void sort_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes, uint32_t *ki,
-                 uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, hipStream_t st) {
-    const uint32_t np = n_partitions(n_max, IPT);
-    uint32_t *totals = scratch;
-    uint32_t *table = scratch + kRadix;
+void depth_passes(uint32_t n, const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
+                  uint32_t *v_b, uint32_t *scratch, const DepthIo &io, hipStream_t st) {
+    const uint32_t *n_vis = &io.cnt->n_visible;
+    one_pass<IPT, kFirst>(nullptr, n, 0, dkey, nullptr, k_a, v_a, scratch, io, st);
+    one_pass<IPT, kPlain>(n_vis, n, 8, k_a, v_a, k_b, v_b, scratch, io, st);
+    one_pass<IPT, kPlain>(n_vis, n, 16, k_b, v_b, k_a, v_a, scratch, io, st);
+    one_pass<IPT, kLast>(n_vis, n, 24, k_a, v_a, nullptr, v_b, scratch, io, st);
+}
+
+template <int IPT>
+void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes, uint32_t *ki,
+                  uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, hipStream_t st) {
+    const DepthIo none{};
     for (int p = 0; p < passes; ++p) {
-        const int shift = begin_bit + 8 * p;
-        sort_upsweep_kernel<IPT><<<np, kSortThreads, 0, st>>>(ki, n_dev, n_max, shift, np, table);
-        sort_colscan_kernel<<<kRadix, 256, 0, st>>>(n_dev, n_max, kSortThreads * IPT, np, table,
-                                                    totals);
-        sort_downsweep_kernel<IPT><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, n_dev, n_max, shift,
-                                                                np, table, totals);
+        one_pass<IPT, kPlain>(n_dev, n_max, begin_bit + 8 * p, ki, vi, ko, vo, scratch, none, st);
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }
@@ -234,10 +388,11 @@ void sort_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passe
 
 int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
 
-size_t sort_scratch_words(uint32_t max_keys, int passes) {
-    // digit totals + one (digit x partition) offset table, reused by every pass
-    (void)passes;
-    return (size_t)kRadix + (size_t)kRadix * (n_partitions(max_keys, ipt_for(max_keys)) + 1);
+size_t sort_scratch_words(uint32_t max_keys) {
+    // digit totals and weight totals, then a (digit x partition) count table
+    // and weight table, reused by every pass
+    const uint32_t np = n_partitions(max_keys, ipt_for(max_keys));
+    return (size_t)2 * kRadix + (size_t)2 * kRadix * np;
 }
 
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
@@ -245,12 +400,32 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
                     uint32_t *scratch, hipStream_t st) {
     if (n_max <= 1 || passes <= 0) return 0;
     if (ipt_for(n_max) == kIptSmall)
-        sort_passes<kIptSmall>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
-                               scratch, st);
+        plain_passes<kIptSmall>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
+                                scratch, st);
     else
-        sort_passes<kIptLarge>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
-                               scratch, st);
+        plain_passes<kIptLarge>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
+                                scratch, st);
     return passes & 1;
+}
+
+void launch_depth_sort(int n, const uint32_t *count, const uint32_t *dkey, uint32_t *k_a,
+                       uint32_t *v_a, uint32_t *k_b, uint32_t *v_b, uint32_t *offs,
+                       uint32_t *scratch, Counters *cnt, uint32_t cap, const uint32_t *pre_partial,
+                       int n_pre, HostCounters *host, uint32_t tag, hipStream_t st) {
+    DepthIo io;
+    io.count = count;
+    io.offs = offs;
+    io.cnt = cnt;
+    io.host = host;
+    io.tag = tag;
+    io.cap = cap;
+    io.pre_partial = pre_partial;
+    io.n_pre = n_pre;
+    const uint32_t nn = (uint32_t)(n > 0 ? n : 0);
+    if (ipt_for(nn) == kIptSmall)
+        depth_passes<kIptSmall>(nn, dkey, k_a, v_a, k_b, v_b, scratch, io, st);
+    else
+        depth_passes<kIptLarge>(nn, dkey, k_a, v_a, k_b, v_b, scratch, io, st);
 }
 
 }  // namespace tgs

@@ -12,7 +12,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/tgs.h"
+#include "tgs.h"
 #include "tgs_internal.h"
 
 using namespace tgs;
@@ -77,7 +77,7 @@ struct DevBuf {
 // Per-frame scratch of one render path (a scene's tgs_render_full, or a state).
 struct Workspace {
     DevBuf g0, g1, col, rect, status, count, partial;
-    DevBuf dkey, didx, dkey_alt, didx_alt, offs, scan;
+    DevBuf dkey, didx, dkey_alt, didx_alt, offs;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
     HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
@@ -116,9 +116,8 @@ struct Workspace {
             TGS_TRY(dkey_alt.ensure(nn * sizeof(uint32_t)));
             TGS_TRY(didx_alt.ensure(nn * sizeof(uint32_t)));
             TGS_TRY(offs.ensure(nn * sizeof(uint32_t)));
-            TGS_TRY(scan.ensure(scan_scratch_bytes(n_)));
-            // the depth sort runs over at most n keys, four passes
-            TGS_TRY(sort.ensure(sort_scratch_words((uint32_t)nn, 4) * sizeof(uint32_t)));
+            // the depth sort runs over at most n keys
+            TGS_TRY(sort.ensure(sort_scratch_words((uint32_t)nn) * sizeof(uint32_t)));
             n = n_;
         }
         if (W_ != W || H_ != H) {
@@ -150,8 +149,8 @@ struct Workspace {
             key_cap = cap;
         }
         const size_t nn = (size_t)(n > 0 ? n : 1);
-        const size_t words = sort_scratch_words((uint32_t)key_cap, passes);
-        const size_t words_depth = sort_scratch_words((uint32_t)nn, 4);
+        const size_t words = sort_scratch_words((uint32_t)key_cap);
+        const size_t words_depth = sort_scratch_words((uint32_t)nn);
         TGS_TRY(sort.ensure((words > words_depth ? words : words_depth) * sizeof(uint32_t)));
         return TGS_OK;
     }
@@ -159,7 +158,7 @@ struct Workspace {
     Records records() const {
         return Records{g0.as<float4>(),      g1.as<float4>(),       col.as<float4>(),
                        rect.as<ushort4>(),   status.as<uint8_t>(),  count.as<uint32_t>(),
-                       partial.as<uint32_t>()};
+                       dkey.as<uint32_t>(),  partial.as<uint32_t>()};
     }
 };
 
@@ -354,38 +353,27 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
 }
 
 // Depth-order the Gaussians that have keys and scan their key counts in that
-// order.  The last scan kernel publishes the frame's counters to the host
-// (tag ws.seq); nothing here waits.
+// order.  The last depth-sort pass publishes the frame's counters to the
+// host (tag ws.seq); nothing here waits.
 tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
                      const uint32_t **sorted_didx) {
-    const uint32_t nn = (uint32_t)(n > 0 ? n : 0);
-    int alt = 0;
-    {
+    if (rowpre) {
         ProfScope ps(TGS_PROF_SCAN, st);
-        if (rowpre) launch_count_masked(n, ws.rect.as<ushort4>(), rowpre, TX, ws.count.as<uint32_t>(), st);
-        launch_visible_scans(n, ws.count.as<uint32_t>(), ws.g1.as<float4>(), ws.dkey.as<uint32_t>(),
-                             ws.didx.as<uint32_t>(), ws.scan.p, ws.partial.as<uint32_t>(),
-                             ws.cnt.as<Counters>(), st);
-        TGS_LAUNCHED("visible scan");
+        launch_count_masked(n, ws.rect.as<ushort4>(), rowpre, TX, ws.count.as<uint32_t>(), st);
+        TGS_LAUNCHED("masked key counts");
     }
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        const uint32_t *n_dev = &ws.cnt.as<Counters>()->n_visible;
-        alt = launch_sort_u32(n_dev, nn, 0, 4, ws.dkey.as<uint32_t>(), ws.didx.as<uint32_t>(),
-                              ws.dkey_alt.as<uint32_t>(), ws.didx_alt.as<uint32_t>(),
-                              ws.sort.as<uint32_t>(), st);
+        ws.seq += 1;
+        launch_depth_sort(n, ws.count.as<uint32_t>(), ws.dkey.as<uint32_t>(),
+                          ws.dkey_alt.as<uint32_t>(), ws.didx_alt.as<uint32_t>(),
+                          ws.dkey.as<uint32_t>(), ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
+                          ws.sort.as<uint32_t>(), ws.cnt.as<Counters>(), (uint32_t)ws.key_cap,
+                          ws.partial.as<uint32_t>(), n > 0 ? preprocess_blocks(n) : 0,
+                          ws.host_cnt_dev, ws.seq, st);
         TGS_LAUNCHED("depth sort");
     }
-    const uint32_t *didx = alt ? ws.didx_alt.as<uint32_t>() : ws.didx.as<uint32_t>();
-    {
-        ProfScope ps(TGS_PROF_SCAN, st);
-        ws.seq += 1;
-        launch_sorted_count_scan(n, didx, ws.count.as<uint32_t>(), ws.offs.as<uint32_t>(), ws.scan.p,
-                                 ws.cnt.as<Counters>(), (uint32_t)ws.key_cap, ws.host_cnt_dev,
-                                 ws.seq, st);
-        TGS_LAUNCHED("key scan");
-    }
-    *sorted_didx = didx;
+    *sorted_didx = ws.didx.as<uint32_t>();
     return TGS_OK;
 }
 

@@ -43,6 +43,7 @@ struct Records {
     ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
     uint8_t *status;          // bit0 survivor, bit1 newly visible
     uint32_t *count;          // keys of the Gaussian (tiles of its rectangle)
+    uint32_t *dkey;           // float bits of the depth (depth-sort key)
     uint32_t *partial;        // per 256-Gaussian block: survivors, newly visible
 };
 
@@ -89,23 +90,15 @@ __device__ inline float ordered_to_float(int i) {
 
 // ---- launchers (k_preprocess.hip) ----
 // Writes the records and, per 256-Gaussian block, the survivor and
-// newly-visible counts (summed into cnt by the visible-compaction scan).
+// newly-visible counts (summed into cnt by the last depth-sort pass).
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
                        Counters *cnt, hipStream_t st);
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
 // ---- launchers (k_keys.hip) ----
-size_t scan_scratch_bytes(int n);
+// count[i] = number of selected tiles in Gaussian i's rectangle.
 void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
                          uint32_t *count, hipStream_t st);
-void launch_visible_scans(int n, const uint32_t *count, const float4 *g1, uint32_t *dkey,
-                          uint32_t *didx, void *scratch, const uint32_t *pre_partial,
-                          Counters *cnt, hipStream_t st);
-// Also sets cnt->n_sorted = n_keys when n_keys <= cap, else 0, then copies
-// the counters to `host` and sets host->tag = tag.
-void launch_sorted_count_scan(int n, const uint32_t *didx, const uint32_t *count, uint32_t *offs,
-                              void *scratch, Counters *cnt, uint32_t cap, HostCounters *host,
-                              uint32_t tag, hipStream_t st);
 // Emits the cnt->n_sorted keys of the cnt->n_visible depth-ordered Gaussians
 // (n bounds n_visible for the grid; nothing is emitted past the key capacity)
 // and clears the tile ranges (filled by launch_ranges after the tile sort).
@@ -124,13 +117,25 @@ void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const 
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
-size_t sort_scratch_words(uint32_t max_keys, int passes);
+// Scratch words of a sort of at most max_keys keys (either kind below).
+size_t sort_scratch_words(uint32_t max_keys);
 // Stable LSD sort of (key, value) pairs on key bits [begin_bit, begin_bit +
 // 8*passes).  The key count is *n_dev if n_dev is not NULL (n_max bounds it),
 // else n_max.  Returns 1 if the result is in the alt buffers.
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
                     uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt,
                     uint32_t *scratch, hipStream_t st);
+// Depth order of the Gaussians with count[i] > 0 among i < n, stable by index
+// (keys dkey[i], the depth's float bits): four passes (dkey -> a -> b -> a ->
+// v_b; k_b may alias dkey).  Writes cnt->n_visible (Gaussians kept), the
+// sorted indices to v_b[0..n_visible), offs[s] = exclusive prefix of their
+// counts, then cnt->n_keys, cnt->n_sorted (n_keys if <= cap, else 0),
+// cnt->n_survivors / n_newly (from the preprocess partials) and, tag last,
+// the same counters to `host`.
+void launch_depth_sort(int n, const uint32_t *count, const uint32_t *dkey, uint32_t *k_a,
+                       uint32_t *v_a, uint32_t *k_b, uint32_t *v_b, uint32_t *offs,
+                       uint32_t *scratch, Counters *cnt, uint32_t cap, const uint32_t *pre_partial,
+                       int n_pre, HostCounters *host, uint32_t tag, hipStream_t st);
 
 // ---- launchers (k_blend.hip) ----
 struct BlendArgs {
