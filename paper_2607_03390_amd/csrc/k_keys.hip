@@ -2,9 +2,9 @@
 //  - masked key counts: in a selective-rendering frame a Gaussian's count is
 //    the number of selected tiles of its rectangle, from per-row prefix sums
 //    of the tile mask (one subtraction per row);
-//  - key emission in depth order, one output key per lane so every store is
-//    coalesced (the owning Gaussian is found by a binary search over the
-//    wave's 64 offsets held in LDS);
+//  - key emission in depth order, a fixed slice of output keys per block with
+//    coalesced stores (owners from a search over the sorted offsets and an
+//    LDS max-scan);
 //  - per-tile [start, end) ranges of the tile-sorted keys and the blend
 //    order of the tiles.
 // Counts stay on the device, so nothing here needs a host round trip.
@@ -32,9 +32,41 @@ __global__ __launch_bounds__(256) void count_masked_kernel(int n, const ushort4 
     if (i < n) count[i] = masked_count(rect[i], rowpre, TX);
 }
 
-// One output key per lane.  Wave w owns sorted positions [64w, 64w+64).
-// Past the key capacity (cnt->n_sorted == 0 with keys) nothing is emitted:
-// the host grows the buffers and renders the frame again.
+// Tile of the r-th key of a Gaussian with tile rectangle rc: row-major over
+// the rectangle, or (rowpre != NULL) over its selected tiles, rows first,
+// O(1) per row from the per-row prefix sums of the tile mask.
+__device__ inline uint32_t key_tile(uint32_t r, ushort4 rc, const uint32_t *rowpre,
+                                    const int *sel_cols, int TX) {
+    int tx, ty;
+    if (!rowpre) {
+        const uint32_t w = (uint32_t)(rc.z - rc.x + 1);
+        ty = rc.y + (int)(r / w);
+        tx = rc.x + (int)(r % w);
+    } else {
+        ty = rc.y;
+        const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
+        for (;; ++ty, row += TX + 1) {
+            const uint32_t c = row[rc.z + 1] - row[rc.x];
+            if (r < c) break;
+            r -= c;
+        }
+        tx = sel_cols[(size_t)ty * TX + row[rc.x] + r];
+    }
+    return (uint32_t)(ty * TX + tx);
+}
+
+// Block b emits output keys [1024 b, 1024 b + 1024), four per thread at
+// consecutive positions across the block (coalesced stores), whatever the
+// Gaussians' key counts: a Gaussian spanning thousands of tiles is spread
+// over many blocks instead of holding one wave.  The owner of the block's
+// first key comes from a 64-way search over the sorted offsets (four rounds
+// of one wave load for a million Gaussians); the Gaussians starting inside
+// the block mark their first position in LDS and an inclusive max-scan gives
+// every position its owner.  Past the key capacity (cnt->n_sorted == 0 with
+// keys) nothing is emitted: the host grows the buffers and renders the frame
+// again.
+constexpr int kDupKeys = 1024;
+
 __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
                                                         const uint32_t *__restrict__ didx,
                                                         const uint32_t *__restrict__ offs,
@@ -42,55 +74,77 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
                                                         const uint32_t *rowpre, const int *sel_cols,
                                                         int TX, int n_tiles, uint32_t *tkey,
                                                         uint32_t *tval, uint2 *ranges) {
-    __shared__ uint32_t s_off[4][64];
-    __shared__ uint32_t s_g[4][64];
-    __shared__ ushort4 s_rect[4][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < n_tiles; t += gridDim.x * blockDim.x)
+    __shared__ int s_owner[kDupKeys];           // window index of each position's owner
+    __shared__ uint32_t s_off[kDupKeys + 1];    // offsets of window Gaussians j0 + k
+    __shared__ uint32_t s_g[kDupKeys + 1];      // their Gaussian indices
+    __shared__ int s_wmax[4];
+    __shared__ uint32_t s_j0;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int t = blockIdx.x * blockDim.x + tid; t < n_tiles; t += gridDim.x * blockDim.x)
         ranges[t] = make_uint2(0u, 0u);
     const uint32_t V = cnt->n_visible, K = cnt->n_sorted;
-    const uint32_t w0 = (blockIdx.x * 4u + (uint32_t)wave) * 64u;
-    if (K == 0u || w0 >= V) return;
-    const uint32_t s = w0 + lane;
-    const uint32_t m = V - w0 < 64u ? V - w0 : 64u;
-    if (s < V) {
-        const uint32_t g = didx[s];
-        s_off[wave][lane] = offs[s];
-        s_g[wave][lane] = g;
-        s_rect[wave][lane] = rect[g];
+    const uint32_t P0 = blockIdx.x * (uint32_t)kDupKeys;
+    if (K == 0u || P0 >= K) return;   // block-uniform
+    const uint32_t P1 = K - P0 < (uint32_t)kDupKeys ? K : P0 + kDupKeys;
+    if (wave == 0) {
+        // last j < V with offs[j] <= P0 (offs increases strictly from offs[0] = 0)
+        uint32_t lo = 0, n = V;
+        while (n > 1) {
+            const uint32_t step = (n + 63) / 64;
+            const uint32_t j = lo + (uint32_t)lane * step;
+            const uint64_t m = __ballot(j < lo + n && offs[j] <= P0);
+            const uint32_t nlo = lo + (63u - (uint32_t)__clzll(m)) * step;   // lane 0 is set
+            n = step < lo + n - nlo ? step : lo + n - nlo;
+            lo = nlo;
+        }
+        if (lane == 0) s_j0 = lo;
     }
-    // the LDS arrays are private to the wave: a wave-level barrier suffices
-    __builtin_amdgcn_wave_barrier();
-    const uint32_t start = s_off[wave][0];
-    const uint32_t end = w0 + 64u < V ? offs[w0 + 64u] : K;
-    for (uint32_t p = start + lane; p < end; p += 64u) {
-        // owner: the last j with s_off[j] <= p (offsets strictly increase)
-        uint32_t lo = 0, hi = m - 1;
-        while (lo < hi) {
-            const uint32_t mid = (lo + hi + 1) >> 1;
-            if (s_off[wave][mid] <= p) lo = mid;
-            else hi = mid - 1;
+    for (int k = tid; k < kDupKeys; k += 256) s_owner[k] = -1;
+    __syncthreads();
+    const uint32_t j0 = s_j0;
+    // at most 1024 Gaussians after j0 start inside the block's keys
+    for (int k = tid; k <= kDupKeys; k += 256) {
+        const uint32_t j = j0 + (uint32_t)k;
+        if (j < V) {
+            const uint32_t o = offs[j];
+            s_off[k] = o;
+            s_g[k] = didx[j];
+            if (k == 0) s_owner[0] = 0;
+            else if (o < P1) s_owner[o - P0] = k;
         }
-        uint32_t r = p - s_off[wave][lo];
-        const ushort4 rc = s_rect[wave][lo];
-        int tx, ty;
-        if (!rowpre) {
-            const uint32_t w = (uint32_t)(rc.z - rc.x + 1);
-            ty = rc.y + (int)(r / w);
-            tx = rc.x + (int)(r % w);
-        } else {
-            // r-th selected tile of the rectangle, rows first: O(1) per row
-            ty = rc.y;
-            const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
-            for (;; ++ty, row += TX + 1) {
-                const uint32_t c = row[rc.z + 1] - row[rc.x];
-                if (r < c) break;
-                r -= c;
-            }
-            tx = sel_cols[(size_t)ty * TX + row[rc.x] + r];
+    }
+    __syncthreads();
+    // inclusive max-scan of the marks: four consecutive entries per thread
+    int v[4], m = -1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        m = max(m, s_owner[4 * tid + i]);
+        v[i] = m;
+    }
+    int inc = m;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(inc, d);
+        if (lane >= d) inc = max(inc, o);
+    }
+    int ex = __shfl_up(inc, 1);
+    if (lane == 0) ex = -1;
+    if (lane == 63) s_wmax[wave] = inc;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) ex = max(ex, s_wmax[w]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_owner[4 * tid + i] = max(v[i], ex);
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t i = (uint32_t)(tid + 256 * k);
+        const uint32_t p = P0 + i;
+        if (p < P1) {
+            const int w = s_owner[i];
+            const uint32_t g = s_g[w];
+            tkey[p] = key_tile(p - s_off[w], rect[g], rowpre, sel_cols, TX);
+            tval[p] = g;
         }
-        tkey[p] = (uint32_t)(ty * TX + tx);
-        tval[p] = s_g[wave][lo];
     }
 }
 
@@ -186,16 +240,17 @@ void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int
     count_masked_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, rect, rowpre, TX, count);
 }
 
-void launch_duplicate(int n, const Counters *cnt, const uint32_t *didx, const uint32_t *offs,
-                      const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
-                      int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st) {
-    if (n <= 0) {
+void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
+                      const uint32_t *offs, const ushort4 *rect, const uint32_t *rowpre,
+                      const int *sel_cols, int TX, int n_tiles, uint32_t *tkey, uint32_t *tval,
+                      uint2 *ranges, hipStream_t st) {
+    if (n <= 0 || cap == 0) {
         ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
         return;
     }
-    const uint32_t waves = ((uint32_t)n + 63) / 64;
-    duplicate_kernel<<<(waves + 3) / 4, 256, 0, st>>>(cnt, didx, offs, rect, rowpre, sel_cols, TX,
-                                                      n_tiles, tkey, tval, ranges);
+    const uint32_t blocks = (cap + kDupKeys - 1) / kDupKeys;
+    duplicate_kernel<<<blocks, 256, 0, st>>>(cnt, didx, offs, rect, rowpre, sel_cols, TX, n_tiles,
+                                             tkey, tval, ranges);
 }
 
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,

@@ -9,10 +9,11 @@
 // passes run over the Gaussians, not over their tile copies).
 //
 // Structure for gfx950, per 8-bit pass: an upsweep kernel counts each
-// partition's digits (1024 keys per partition up to 2M keys, 3840 above), a
-// column scan turns those counts into per-(digit, partition) offsets and
-// digit totals, and a downsweep kernel ranks each partition in LDS and
-// scatters it (the digit bases are a block scan of the 256 totals).  No block
+// partition's digits (1024 keys per partition up to 2M keys, 3840 above) into
+// a partition-major table, a column scan turns those counts into offsets
+// within 16 chunks of partitions plus per-chunk digit sums, and a downsweep
+// kernel ranks each partition in LDS and scatters it (the digit bases are a
+// block scan of the 256 totals, plus the sums of earlier chunks).  No block
 // ever waits on another and no device-wide atomic is contended (same-address
 // atomics serialise across the eight XCDs), so the sort is deterministic and
 // needs no forward-progress assumption.  Ranking is stable (a wave's 64-lane
@@ -74,8 +75,9 @@ __device__ inline T block_exclusive_scan256(T v, T *s_wave, T *total = nullptr) 
     return off + inc - v;
 }
 
-// Digit counts of one partition: counts[d * np + part]; in the last depth
-// pass also the digit's weight sum: weights[d * np + part].
+// Digit counts of one partition: counts[part * 256 + d] (one coalesced 1 KB
+// row per block); in the last depth pass also the digit weight sums:
+// weights[part * 256 + d].
 template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint32_t *n_dev,
@@ -104,47 +106,60 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
         }
     }
     __syncthreads();
-    counts[(size_t)tid * np + part] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
+    counts[(size_t)part * kRadix + tid] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
     if (MODE == kLast)
-        weights[(size_t)tid * np + part] = s_w[0][tid] + s_w[1][tid] + s_w[2][tid] + s_w[3][tid];
+        weights[(size_t)part * kRadix + tid] = s_w[0][tid] + s_w[1][tid] + s_w[2][tid] + s_w[3][tid];
 }
 
-// One block per (table, digit): exclusive scan of the digit's counts (table
-// 0) or weights (table 1) over the partitions that hold keys, in place, and
-// the digit's total; 64-bit running sums, stored saturated to 32 bits.  Each
-// thread scans 8 consecutive partitions, so one round covers 2048 partitions.
+// The partitions holding keys are cut into kChunks chunks of L consecutive
+// partitions.  One block per (table, chunk, group of 16 digits): exclusive
+// scan, within the chunk, of each digit's counts (table 0) or weights
+// (table 1), in place, and the chunk's digit sums in chunk_sums[c * 256 + d]
+// (saturated to 32 bits).  A row of 16 digits is one 64-byte line, so every
+// load uses whole lines.  The downsweep adds the sums of earlier chunks.
+constexpr int kChunks = 16;
+
+__device__ inline uint32_t chunk_len(uint32_t npa) {
+    const uint32_t L = (npa + kChunks - 1) / kChunks;
+    return L ? L : 1u;
+}
+
 __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev, uint32_t n_host,
                                                            uint32_t tile, uint32_t np,
-                                                           uint32_t *counts, uint32_t *totals) {
-    __shared__ uint64_t s_scan[4];
-    __shared__ uint64_t s_run;
-    const int d = blockIdx.x & (kRadix - 1), table = blockIdx.x / kRadix;
+                                                           uint32_t *counts, uint32_t *chunk_sums) {
+    __shared__ uint64_t s_sum[16][16];
+    const int tid = threadIdx.x;
+    const int g = blockIdx.x & 15, c = (blockIdx.x >> 4) % kChunks, table = blockIdx.x / (16 * kChunks);
+    const int dl = tid & 15, lane = tid >> 4, d = 16 * g + dl;
     const uint32_t K = key_count(n_dev, n_host);
     const uint32_t npa = (K + tile - 1) / tile;   // <= np
-    uint64_t run = 0;
-    uint32_t *col = counts + (size_t)table * kRadix * np + (size_t)d * np;
-    for (uint32_t c = 0; c < npa; c += 2048) {
-        const uint32_t p0 = c + 8u * threadIdx.x;
-        uint32_t v[8];
-        uint64_t sum = 0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            v[j] = p0 + j < npa ? col[p0 + j] : 0u;
-            sum += v[j];
+    const uint32_t L = chunk_len(npa);
+    const uint32_t S = (L + 15) / 16;             // partitions per thread
+    uint32_t *tab = counts + (size_t)table * np * kRadix;
+    uint32_t p0 = (uint32_t)c * L + (uint32_t)lane * S;
+    uint32_t p1 = p0 + S;
+    const uint32_t cend = (uint32_t)(c + 1) * L < npa ? (uint32_t)(c + 1) * L : npa;
+    if (p1 > cend) p1 = cend;
+    uint64_t sum = 0;
+    for (uint32_t p = p0; p < p1; ++p) sum += tab[(size_t)p * kRadix + d];
+    s_sum[lane][dl] = sum;
+    __syncthreads();
+    if (tid < 16) {
+        uint64_t run = 0;
+        for (int l = 0; l < 16; ++l) {
+            const uint64_t v = s_sum[l][tid];
+            s_sum[l][tid] = run;
+            run += v;
         }
-        const uint64_t ex = block_exclusive_scan256<uint64_t>(sum, s_scan);
-        uint64_t o = run + ex;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            if (p0 + j < npa) col[p0 + j] = sat32(o);
-            o += v[j];
-        }
-        if (threadIdx.x == 255) s_run = o;
-        __syncthreads();
-        run = s_run;
-        __syncthreads();
+        chunk_sums[(size_t)table * kChunks * kRadix + (size_t)c * kRadix + 16 * g + tid] = sat32(run);
     }
-    if (threadIdx.x == 0) totals[table * kRadix + d] = sat32(run);
+    __syncthreads();
+    uint64_t o = s_sum[lane][dl];
+    for (uint32_t p = p0; p < p1; ++p) {
+        const uint32_t v = tab[(size_t)p * kRadix + d];
+        tab[(size_t)p * kRadix + d] = sat32(o);
+        o += v;
+    }
 }
 
 // Operands of the first and last depth-sort passes.
@@ -204,7 +219,7 @@ template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
     uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
-    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ totals, DepthIo io) {
+    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ chunk_sums, DepthIo io) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ uint32_t s_keys[kTile];
     __shared__ uint32_t s_vals[kTile];
@@ -221,25 +236,39 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t K = MODE == kFirst ? n_host : key_count(n_dev, n_host);
     const uint32_t part = blockIdx.x;
     const uint32_t base = part * kTile;
+    const uint32_t c_mine = part / chunk_len((K + kTile - 1) / kTile);
+    // digit tid: its total over all chunks and its sum over the chunks before this one
+    uint64_t tot = 0, pre = 0, wtot = 0, wpre = 0;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+        const uint32_t v = chunk_sums[c * kRadix + tid];
+        tot += v;
+        if ((uint32_t)c < c_mine) pre += v;
+        if (MODE == kLast) {
+            const uint32_t w = chunk_sums[kChunks * kRadix + c * kRadix + tid];
+            wtot += w;
+            if ((uint32_t)c < c_mine) wpre += w;
+        }
+    }
     // block 0 publishes the pass's totals (also when there is nothing to sort)
     if (MODE == kFirst && part == 0) {
         uint32_t n_kept;
-        (void)block_exclusive_scan256<uint32_t>(totals[tid], s_scan, &n_kept);
+        (void)block_exclusive_scan256<uint32_t>(sat32(tot), s_scan, &n_kept);
         if (tid == 0) io.cnt->n_visible = n_kept;
     }
     if (MODE == kLast && part == 0) {
         uint64_t n_keys;
-        (void)block_exclusive_scan256<uint64_t>(totals[kRadix + tid], s_scan64, &n_keys);
+        (void)block_exclusive_scan256<uint64_t>(wtot, s_scan64, &n_keys);
         publish_counters(io, n_keys, s_wh);
     }
     if (base >= K) return;   // block-uniform
     for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
     // global start of digit tid: digits below it, then partitions before this one
-    s_gbase[tid] = block_exclusive_scan256<uint32_t>(totals[tid], s_scan) +
-                   offsets[(size_t)tid * np + part];
+    s_gbase[tid] = block_exclusive_scan256<uint32_t>(sat32(tot), s_scan) + sat32(pre) +
+                   offsets[(size_t)part * kRadix + tid];
     if (MODE == kLast) {
-        const uint64_t wb = block_exclusive_scan256<uint64_t>(totals[kRadix + tid], s_scan64);
-        s_wbase[tid] = sat32(wb + offsets[(size_t)kRadix * np + (size_t)tid * np + part]);
+        const uint64_t wb = block_exclusive_scan256<uint64_t>(wtot, s_scan64);
+        s_wbase[tid] = sat32(wb + wpre + offsets[(size_t)np * kRadix + (size_t)part * kRadix + tid]);
     }
     __syncthreads();
     const uint32_t wbase = base + (uint32_t)wave * (64u * IPT);
@@ -352,15 +381,16 @@ void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *
               hipStream_t st) {
     // at least one block: the last depth pass always publishes the counters
     const uint32_t np = n_partitions(n_max, IPT);
-    uint32_t *totals = scratch;                    // [2][256]
-    uint32_t *table = scratch + 2 * kRadix;        // [2][256][np]
+    uint32_t *chunk_sums = scratch;                // [2][kChunks][256]
+    uint32_t *table = scratch + 2 * kChunks * kRadix;   // [2][np][256]
     const uint32_t *nd = MODE == kFirst ? nullptr : n_dev;
+    const int tables = MODE == kLast ? 2 : 1;
     sort_upsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(
-        ki, vi, nd, n_max, shift, np, io.count, table, table + (size_t)kRadix * np);
-    sort_colscan_kernel<<<MODE == kLast ? 2 * kRadix : kRadix, 256, 0, st>>>(
-        nd, n_max, kSortThreads * IPT, np, table, totals);
+        ki, vi, nd, n_max, shift, np, io.count, table, table + (size_t)np * kRadix);
+    sort_colscan_kernel<<<tables * 16 * kChunks, 256, 0, st>>>(nd, n_max, kSortThreads * IPT, np,
+                                                                table, chunk_sums);
     sort_downsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
-                                                                  np, table, totals, io);
+                                                                  np, table, chunk_sums, io);
 }
 
 template <int IPT>
@@ -389,10 +419,10 @@ void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pass
 int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
 
 size_t sort_scratch_words(uint32_t max_keys) {
-    // digit totals and weight totals, then a (digit x partition) count table
+    // chunk sums of counts and weights, then a (partition x digit) count table
     // and weight table, reused by every pass
     const uint32_t np = n_partitions(max_keys, ipt_for(max_keys));
-    return (size_t)2 * kRadix + (size_t)2 * kRadix * np;
+    return (size_t)2 * kChunks * kRadix + (size_t)2 * kRadix * np;
 }
 
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,

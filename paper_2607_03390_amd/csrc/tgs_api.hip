@@ -429,7 +429,7 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     Counters *cnt = ws.cnt.as<Counters>();
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
-        launch_duplicate(n, cnt, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
+        launch_duplicate(n, cap, cnt, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
                          sel_cols, TX, TX * TY, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
                          ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("duplicate");

@@ -100,12 +100,13 @@ inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
                          uint32_t *count, hipStream_t st);
 // Emits the cnt->n_sorted keys of the cnt->n_visible depth-ordered Gaussians
-// (n bounds n_visible for the grid; nothing is emitted past the key capacity)
-// and clears the tile ranges (filled by launch_ranges after the tile sort).
-// rowpre / sel_cols are NULL in frames that render every tile.
-void launch_duplicate(int n, const Counters *cnt, const uint32_t *didx, const uint32_t *offs,
-                      const ushort4 *rect, const uint32_t *rowpre, const int *sel_cols, int TX,
-                      int n_tiles, uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
+// (cap bounds n_sorted for the grid; nothing is emitted past the key
+// capacity) and clears the tile ranges (filled by launch_ranges after the
+// tile sort).  rowpre / sel_cols are NULL in frames that render every tile.
+void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
+                      const uint32_t *offs, const ushort4 *rect, const uint32_t *rowpre,
+                      const int *sel_cols, int TX, int n_tiles, uint32_t *tkey, uint32_t *tval,
+                      uint2 *ranges, hipStream_t st);
 // Ranges of the cnt->n_sorted tile-sorted keys; cap bounds n_sorted for the grid.
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
                    hipStream_t st);
