@@ -1,7 +1,4 @@
 // Gaussian-tile duplication (Sec. III-A) around the two sorts of a frame:
-//  - masked key counts: in a selective-rendering frame a Gaussian's count is
-//    the number of selected tiles of its rectangle, from per-row prefix sums
-//    of the tile mask (one subtraction per row);
 //  - key emission in depth order, a fixed slice of output keys per block with
 //    coalesced stores (owners from a search over the sorted offsets and an
 //    LDS max-scan);
@@ -14,23 +11,6 @@ namespace tgs {
 
 namespace {
 
-
-__device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int TX) {
-    if (r.x > r.z || r.y > r.w) return 0u;
-    uint32_t c = 0;
-    for (int y = r.y; y <= r.w; ++y) {
-        const uint32_t *row = rowpre + (size_t)y * (TX + 1);
-        c += row[r.z + 1] - row[r.x];
-    }
-    return c;
-}
-
-__global__ __launch_bounds__(256) void count_masked_kernel(int n, const ushort4 *rect,
-                                                           const uint32_t *rowpre, int TX,
-                                                           uint32_t *count) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) count[i] = masked_count(rect[i], rowpre, TX);
-}
 
 // Tile of the r-th key of a Gaussian with tile rectangle rc: row-major over
 // the rectangle, or (rowpre != NULL) over its selected tiles, rows first,
@@ -176,69 +156,71 @@ __device__ inline uint32_t length_bucket(const uint2 *ranges, int t) {
     return len ? 32u - (uint32_t)__clz(len) : 0u;
 }
 
-// Wave-aggregated LDS atomic: each distinct bucket of the wave takes one
-// atomicAdd; returns this lane's slot (old value + rank among its peers).
+// Wave-aggregated LDS atomic without a loop: lanes with equal buckets are
+// matched over the six bucket bits; the lowest lane of each group adds the
+// group's size (one LDS atomic instruction for all groups) and the others
+// take consecutive slots after its old value.
 __device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool active) {
     const int lane = threadIdx.x & 63;
-    const uint64_t lt_mask = (1ull << lane) - 1ull;
-    uint64_t todo = __ballot(active);
-    uint32_t slot = 0;
-    while (todo) {
-        const int leader = __ffsll((long long)todo) - 1;
-        const uint32_t lb = __shfl(b, leader);
-        const uint64_t peers = __ballot(active && b == lb);
-        uint32_t base = 0;
-        if (lane == leader) base = atomicAdd(&s_cnt[lb], (uint32_t)__popcll(peers));
-        base = __shfl(base, leader);
-        if (active && b == lb) slot = base + (uint32_t)__popcll(peers & lt_mask);
-        todo &= ~peers;
+    uint64_t peers = __ballot(active);
+#pragma unroll
+    for (int bit = 0; bit < 6; ++bit) {
+        const bool x = (b >> bit) & 1u;
+        const uint64_t m = __ballot(x);
+        peers &= x ? m : ~m;
     }
-    return slot;
+    const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
+    uint32_t base = 0;
+    if (active && lane == leader) base = atomicAdd(&s_cnt[b], (uint32_t)__popcll(peers));
+    base = __shfl(base, leader);
+    return base + (uint32_t)__popcll(peers & ((1ull << lane) - 1ull));
 }
 
 __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uint32_t *n_dev,
                                                            const int *tile_in,
                                                            const uint2 *ranges, int *tile_out) {
+    constexpr int kPer = 8;   // tiles per thread and round: all loads of a round in flight
     __shared__ uint32_t s_cnt[33];
     const int tid = threadIdx.x;
     const int n = n_dev ? (int)*n_dev : n_host;
     if (tid < 33) s_cnt[tid] = 0u;
     __syncthreads();
-    // loop bounds are uniform over the block so that every lane takes part
-    // in the wave-level aggregation
-    for (int c = 0; c < n; c += 1024) {
-        const int i = c + tid;
-        const bool active = i < n;
-        const uint32_t b = active ? length_bucket(ranges, tile_in ? tile_in[i] : i) : 0u;
-        (void)wave_bucket_add(s_cnt, b, active);
-    }
-    __syncthreads();
-    if (tid == 0) {
-        uint32_t run = 0;
-        for (int b = 32; b >= 0; --b) {
-            const uint32_t c = s_cnt[b];
-            s_cnt[b] = run;
-            run += c;
+    // every lane runs every round (bounds are block-uniform) so that the
+    // wave-level aggregation sees the whole wave
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int c0 = 0; c0 < n; c0 += kPer * 1024) {
+            int t[kPer];
+            uint32_t b[kPer];
+            bool act[kPer];
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const int i = c0 + k * 1024 + tid;
+                act[k] = i < n;
+                t[k] = act[k] ? (tile_in ? tile_in[i] : i) : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) b[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const uint32_t slot = wave_bucket_add(s_cnt, b[k], act[k]);
+                if (pass == 1 && act[k]) tile_out[slot] = t[k];
+            }
         }
-    }
-    __syncthreads();
-    for (int c = 0; c < n; c += 1024) {
-        const int i = c + tid;
-        const bool active = i < n;
-        const int t = active ? (tile_in ? tile_in[i] : i) : 0;
-        const uint32_t b = active ? length_bucket(ranges, t) : 0u;
-        const uint32_t slot = wave_bucket_add(s_cnt, b, active);
-        if (active) tile_out[slot] = t;
+        __syncthreads();
+        if (pass == 0 && tid == 0) {
+            // bucket starts, longest lists first
+            uint32_t run = 0;
+            for (int bk = 32; bk >= 0; --bk) {
+                const uint32_t c = s_cnt[bk];
+                s_cnt[bk] = run;
+                run += c;
+            }
+        }
+        __syncthreads();
     }
 }
 
 }  // namespace
-
-void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                         uint32_t *count, hipStream_t st) {
-    if (n <= 0) return;
-    count_masked_kernel<<<(n + 255) / 256, 256, 0, st>>>(n, rect, rowpre, TX, count);
-}
 
 void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
                       const uint32_t *offs, const ushort4 *rect, const uint32_t *rowpre,

@@ -25,7 +25,9 @@
 //
 // The depth sort folds two neighbouring steps into its first and last pass:
 //  - the first pass reads every Gaussian and keeps those with a key count
-//    above zero (the compaction), writing the number kept;
+//    above zero (the compaction), writing the number kept; in a
+//    selective-rendering frame its upsweep first recounts each Gaussian's
+//    keys over the selected tiles of its rectangle;
 //  - the last pass also carries each Gaussian's key count as a weight and
 //    writes, at each sorted position, the exclusive prefix of the weights:
 //    where the Gaussian's tile keys start.  It publishes the frame's
@@ -75,14 +77,27 @@ __device__ inline T block_exclusive_scan256(T v, T *s_wave, T *total = nullptr) 
     return off + inc - v;
 }
 
+// Operands of the first and last depth-sort passes.
+struct DepthIo {
+    uint32_t *count;            // key count per Gaussian
+    const ushort4 *rect;        // first pass of a selective frame: recount from
+    const uint32_t *rowpre;     // the rectangles and the tile mask's row prefix
+    int TX;                     // sums (rowpre NULL: count is final)
+    uint32_t *offs;             // last pass: start of each sorted Gaussian's keys
+    Counters *cnt;
+    HostCounters *host;         // last pass: the frame's counters, tag last
+    uint32_t tag, cap;
+    const uint32_t *pre_partial;   // preprocess per-block survivor / newly-visible counts
+    int n_pre;
+};
+
 // Digit counts of one partition: counts[part * 256 + d] (one coalesced 1 KB
 // row per block); in the last depth pass also the digit weight sums:
 // weights[part * 256 + d].
 template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint32_t *n_dev,
-    uint32_t n_host, int shift, uint32_t np, const uint32_t *__restrict__ count, uint32_t *counts,
-    uint32_t *weights) {
+    uint32_t n_host, int shift, uint32_t np, DepthIo io, uint32_t *counts, uint32_t *weights) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ uint32_t s_h[4][kRadix];
     __shared__ uint32_t s_w[MODE == kLast ? 4 : 1][kRadix];
@@ -99,10 +114,21 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        if (idx < K && (MODE != kFirst || count[idx] > 0u)) {
+        bool keep = idx < K;
+        if (MODE == kFirst && keep) {
+            uint32_t c;
+            if (io.rowpre) {
+                c = masked_count(io.rect[idx], io.rowpre, io.TX);
+                io.count[idx] = c;
+            } else {
+                c = io.count[idx];
+            }
+            keep = c > 0u;
+        }
+        if (keep) {
             const uint32_t d = (kin[idx] >> shift) & 255u;
             atomicAdd(&s_h[wave][d], 1u);
-            if (MODE == kLast) atomicAdd(&s_w[wave][d], count[vin[idx]]);
+            if (MODE == kLast) atomicAdd(&s_w[wave][d], io.count[vin[idx]]);
         }
     }
     __syncthreads();
@@ -140,8 +166,20 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
     uint32_t p1 = p0 + S;
     const uint32_t cend = (uint32_t)(c + 1) * L < npa ? (uint32_t)(c + 1) * L : npa;
     if (p1 > cend) p1 = cend;
+    // sub-chunks of up to kKeep partitions stay in registers between the sum
+    // and the write-back (one read of the table); longer ones are read twice
+    constexpr uint32_t kKeep = 16;
+    uint32_t keep[kKeep];
     uint64_t sum = 0;
-    for (uint32_t p = p0; p < p1; ++p) sum += tab[(size_t)p * kRadix + d];
+    if (S <= kKeep) {
+#pragma unroll
+        for (uint32_t k = 0; k < kKeep; ++k) {
+            keep[k] = p0 + k < p1 ? tab[(size_t)(p0 + k) * kRadix + d] : 0u;
+            sum += keep[k];
+        }
+    } else {
+        for (uint32_t p = p0; p < p1; ++p) sum += tab[(size_t)p * kRadix + d];
+    }
     s_sum[lane][dl] = sum;
     __syncthreads();
     if (tid < 16) {
@@ -155,23 +193,20 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
     }
     __syncthreads();
     uint64_t o = s_sum[lane][dl];
-    for (uint32_t p = p0; p < p1; ++p) {
-        const uint32_t v = tab[(size_t)p * kRadix + d];
-        tab[(size_t)p * kRadix + d] = sat32(o);
-        o += v;
+    if (S <= kKeep) {
+#pragma unroll
+        for (uint32_t k = 0; k < kKeep; ++k) {
+            if (p0 + k < p1) tab[(size_t)(p0 + k) * kRadix + d] = sat32(o);
+            o += keep[k];
+        }
+    } else {
+        for (uint32_t p = p0; p < p1; ++p) {
+            const uint32_t v = tab[(size_t)p * kRadix + d];
+            tab[(size_t)p * kRadix + d] = sat32(o);
+            o += v;
+        }
     }
 }
-
-// Operands of the first and last depth-sort passes.
-struct DepthIo {
-    const uint32_t *count;      // key count per Gaussian
-    uint32_t *offs;             // last pass: start of each sorted Gaussian's keys
-    Counters *cnt;
-    HostCounters *host;         // last pass: the frame's counters, tag last
-    uint32_t tag, cap;
-    const uint32_t *pre_partial;   // preprocess per-block survivor / newly-visible counts
-    int n_pre;
-};
 
 // Last depth pass, block 0: the frame's totals to the device counters and,
 // tag last, to the host.
@@ -262,19 +297,10 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         publish_counters(io, n_keys, s_wh);
     }
     if (base >= K) return;   // block-uniform
-    for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
-    // global start of digit tid: digits below it, then partitions before this one
-    s_gbase[tid] = block_exclusive_scan256<uint32_t>(sat32(tot), s_scan) + sat32(pre) +
-                   offsets[(size_t)part * kRadix + tid];
-    if (MODE == kLast) {
-        const uint64_t wb = block_exclusive_scan256<uint64_t>(wtot, s_scan64);
-        s_wbase[tid] = sat32(wb + wpre + offsets[(size_t)np * kRadix + (size_t)part * kRadix + tid]);
-    }
-    __syncthreads();
+    // issue every global load of the block before the first barrier
     const uint32_t wbase = base + (uint32_t)wave * (64u * IPT);
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-
-    uint32_t key[IPT], val[IPT], rank[IPT];
+    uint32_t key[IPT], val[IPT], rank[IPT], wt[MODE == kLast ? IPT : 1];
     bool ok[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
@@ -288,6 +314,20 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
             val[j] = ok[j] ? vin[idx] : 0u;
         }
     }
+    const uint32_t off_mine = offsets[(size_t)part * kRadix + tid];
+    const uint32_t woff_mine = MODE == kLast ? offsets[(size_t)np * kRadix + (size_t)part * kRadix + tid] : 0u;
+    if (MODE == kLast) {
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) wt[j] = ok[j] ? io.count[val[j]] : 0u;
+    }
+    for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
+    // global start of digit tid: digits below it, then partitions before this one
+    s_gbase[tid] = block_exclusive_scan256<uint32_t>(sat32(tot), s_scan) + sat32(pre) + off_mine;
+    if (MODE == kLast) {
+        const uint64_t wb = block_exclusive_scan256<uint64_t>(wtot, s_scan64);
+        s_wbase[tid] = sat32(wb + wpre + woff_mine);
+    }
+    __syncthreads();
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const bool valid = ok[j];
@@ -330,7 +370,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
             const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rank[j];
             s_keys[pos] = key[j];
             s_vals[pos] = val[j];
-            if (MODE == kLast) s_wt[pos] = io.count[val[j]];
+            if (MODE == kLast) s_wt[pos] = wt[j];
         }
     }
     __syncthreads();
@@ -386,7 +426,7 @@ void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *
     const uint32_t *nd = MODE == kFirst ? nullptr : n_dev;
     const int tables = MODE == kLast ? 2 : 1;
     sort_upsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(
-        ki, vi, nd, n_max, shift, np, io.count, table, table + (size_t)np * kRadix);
+        ki, vi, nd, n_max, shift, np, io, table, table + (size_t)np * kRadix);
     sort_colscan_kernel<<<tables * 16 * kChunks, 256, 0, st>>>(nd, n_max, kSortThreads * IPT, np,
                                                                 table, chunk_sums);
     sort_downsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
@@ -438,12 +478,16 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
     return passes & 1;
 }
 
-void launch_depth_sort(int n, const uint32_t *count, const uint32_t *dkey, uint32_t *k_a,
-                       uint32_t *v_a, uint32_t *k_b, uint32_t *v_b, uint32_t *offs,
-                       uint32_t *scratch, Counters *cnt, uint32_t cap, const uint32_t *pre_partial,
-                       int n_pre, HostCounters *host, uint32_t tag, hipStream_t st) {
+void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
+                       const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
+                       uint32_t *v_b, uint32_t *offs, uint32_t *scratch, Counters *cnt,
+                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
+                       uint32_t tag, hipStream_t st) {
     DepthIo io;
     io.count = count;
+    io.rect = rect;
+    io.rowpre = rowpre;
+    io.TX = TX;
     io.offs = offs;
     io.cnt = cnt;
     io.host = host;

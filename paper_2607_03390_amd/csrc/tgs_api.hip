@@ -357,15 +357,11 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
 // host (tag ws.seq); nothing here waits.
 tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
                      const uint32_t **sorted_didx) {
-    if (rowpre) {
-        ProfScope ps(TGS_PROF_SCAN, st);
-        launch_count_masked(n, ws.rect.as<ushort4>(), rowpre, TX, ws.count.as<uint32_t>(), st);
-        TGS_LAUNCHED("masked key counts");
-    }
     {
         ProfScope ps(TGS_PROF_SORT, st);
         ws.seq += 1;
-        launch_depth_sort(n, ws.count.as<uint32_t>(), ws.dkey.as<uint32_t>(),
+        launch_depth_sort(n, ws.count.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX,
+                          ws.dkey.as<uint32_t>(),
                           ws.dkey_alt.as<uint32_t>(), ws.didx_alt.as<uint32_t>(),
                           ws.dkey.as<uint32_t>(), ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
                           ws.sort.as<uint32_t>(), ws.cnt.as<Counters>(), (uint32_t)ws.key_cap,

@@ -88,6 +88,19 @@ __device__ inline float ordered_to_float(int i) {
     return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff);
 }
 
+// Key count of a Gaussian in a selective-rendering frame: the selected tiles
+// of its rectangle, from per-row prefix sums of the tile mask (rowpre, TY
+// rows of TX + 1 entries; one subtraction per row).
+__device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int TX) {
+    if (r.x > r.z || r.y > r.w) return 0u;
+    uint32_t c = 0;
+    for (int y = r.y; y <= r.w; ++y) {
+        const uint32_t *row = rowpre + (size_t)y * (TX + 1);
+        c += row[r.z + 1] - row[r.x];
+    }
+    return c;
+}
+
 // ---- launchers (k_preprocess.hip) ----
 // Writes the records and, per 256-Gaussian block, the survivor and
 // newly-visible counts (summed into cnt by the last depth-sort pass).
@@ -96,9 +109,6 @@ void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Re
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
 // ---- launchers (k_keys.hip) ----
-// count[i] = number of selected tiles in Gaussian i's rectangle.
-void launch_count_masked(int n, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                         uint32_t *count, hipStream_t st);
 // Emits the cnt->n_sorted keys of the cnt->n_visible depth-ordered Gaussians
 // (cap bounds n_sorted for the grid; nothing is emitted past the key
 // capacity) and clears the tile ranges (filled by launch_ranges after the
@@ -128,15 +138,17 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
                     uint32_t *scratch, hipStream_t st);
 // Depth order of the Gaussians with count[i] > 0 among i < n, stable by index
 // (keys dkey[i], the depth's float bits): four passes (dkey -> a -> b -> a ->
-// v_b; k_b may alias dkey).  Writes cnt->n_visible (Gaussians kept), the
+// v_b; k_b may alias dkey).  With rowpre (a selective-rendering frame) the
+// first pass first replaces count[i] by the masked count of rect[i].  Writes cnt->n_visible (Gaussians kept), the
 // sorted indices to v_b[0..n_visible), offs[s] = exclusive prefix of their
 // counts, then cnt->n_keys, cnt->n_sorted (n_keys if <= cap, else 0),
 // cnt->n_survivors / n_newly (from the preprocess partials) and, tag last,
 // the same counters to `host`.
-void launch_depth_sort(int n, const uint32_t *count, const uint32_t *dkey, uint32_t *k_a,
-                       uint32_t *v_a, uint32_t *k_b, uint32_t *v_b, uint32_t *offs,
-                       uint32_t *scratch, Counters *cnt, uint32_t cap, const uint32_t *pre_partial,
-                       int n_pre, HostCounters *host, uint32_t tag, hipStream_t st);
+void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
+                       const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
+                       uint32_t *v_b, uint32_t *offs, uint32_t *scratch, Counters *cnt,
+                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
+                       uint32_t tag, hipStream_t st);
 
 // ---- launchers (k_blend.hip) ----
 struct BlendArgs {
