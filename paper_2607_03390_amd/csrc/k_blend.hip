@@ -4,7 +4,8 @@
 // image (temporal appearance buffer) and the set of Gaussians with a
 // positive blending weight somewhere (temporal Gaussian buffer, Sec. III-C).
 //
-// One 256-thread block (four wave64s) per 16x16 tile, one pixel per thread.
+// One 256-thread block (four wave64s, one per 8x8 quadrant) per 16x16 tile,
+// one pixel per thread.
 // The tile's sorted Gaussians are staged through LDS in batches of 256
 // records (48 bytes each, one coalesced gather per thread); every wave then
 // reads each record as an LDS broadcast.  A pixel stops at the Gaussian that
@@ -36,9 +37,11 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     __shared__ float4 s_col[256];
     __shared__ int s_idx[256];
     __shared__ uint32_t s_flag[256];
-    // Wave w (pixel rows 4w..4w+3 of the tile) visits only the staged
-    // Gaussians whose alpha >= 1/255 ellipse, conservatively enlarged, meets
-    // its 16x4 strip, in staging (= depth) order.
+    // Wave w (the 8x8 quadrant w of the tile: column half w & 1, row half
+    // w >> 1) visits only the staged Gaussians whose alpha >= 1/255 ellipse,
+    // conservatively enlarged, meets its quadrant, in staging (= depth)
+    // order.  A square region touches fewer footprints than a 16x4 strip of
+    // the same area.
     __shared__ uint8_t s_list[4][256];
     __shared__ uint32_t s_cnt[4][4];
 
@@ -46,7 +49,8 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;
-    const int px = tx * kTile + (tid & 15), py = ty * kTile + (tid >> 4);
+    const int qx = wave & 1, qy = wave >> 1;
+    const int px = tx * kTile + 8 * qx + (lane & 7), py = ty * kTile + 8 * qy + (lane >> 3);
     const bool inside = px < a.W && py < a.H;
     const float fpx = (float)px, fpy = (float)py;
     const float tile_x0 = (float)(tx * kTile), tile_y0 = (float)(ty * kTile);
@@ -81,12 +85,12 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
                 const float det = g0.z * g1.x - g0.w * g0.w;
                 const float hx = sqrtf(kq * g1.x / det) * 1.002f + 0.05f;
                 const float hy = sqrtf(kq * g0.z / det) * 1.002f + 0.05f;
-                if (g0.x + hx >= tile_x0 && g0.x - hx <= tile_x0 + 15.0f) {
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const float ylo = tile_y0 + 4.0f * w;
-                        if (g0.y + hy >= ylo && g0.y - hy <= ylo + 3.0f) strips |= 1u << w;
-                    }
+                for (int w = 0; w < 4; ++w) {
+                    const float xlo = tile_x0 + 8.0f * (w & 1), ylo = tile_y0 + 8.0f * (w >> 1);
+                    if (g0.x + hx >= xlo && g0.x - hx <= xlo + 7.0f && g0.y + hy >= ylo &&
+                        g0.y - hy <= ylo + 7.0f)
+                        strips |= 1u << w;
                 }
             }
         }
