@@ -26,6 +26,10 @@ namespace tgs {
 
 namespace {
 
+// Wave votes on the execution mask itself (no 0/1 vector temporaries).
+__device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
+__device__ inline bool wave_all(bool p) { return __builtin_amdgcn_ballot_w64(!p) == 0ull; }
+
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     // Staged per Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
@@ -42,7 +46,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     // conservatively enlarged, meets its quadrant, in staging (= depth)
     // order.  A square region touches fewer footprints than a 16x4 strip of
     // the same area.
-    __shared__ uint8_t s_list[4][256];
+    __shared__ uint16_t s_list[4][256];   // byte offsets (16 * staging slot)
     __shared__ uint32_t s_cnt[4][4];
 
     if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) return;   // block-uniform
@@ -108,33 +112,49 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             if ((strips >> w) & 1u) {
                 uint32_t pos = (uint32_t)__popcll(bal[w] & lt_mask);
                 for (int sw2 = 0; sw2 < wave; ++sw2) pos += s_cnt[sw2][w];
-                s_list[w][pos] = (uint8_t)tid;
+                s_list[w][pos] = (uint16_t)(16 * tid);
             }
         }
-        const uint32_t n_mine = s_cnt[0][wave] + s_cnt[1][wave] + s_cnt[2][wave] + s_cnt[3][wave];
+        // the same for every lane of the wave: keep the loop on scalar registers
+        const uint32_t n_mine = __builtin_amdgcn_readfirstlane(
+            s_cnt[0][wave] + s_cnt[1][wave] + s_cnt[2][wave] + s_cnt[3][wave]);
         __syncthreads();
-        for (uint32_t e = 0; e < n_mine; ++e) {
-            if (__all(done)) break;
-            const int j = s_list[wave][e];
-            const float4 g0 = s_g0[j];
-            const float4 g1 = s_g1[j];
+        // a wave whose pixels have all stopped skips the batch
+        const uint32_t n_run = wave_all(done) ? 0u : n_mine;
+        for (uint32_t e = 0; e < n_run; ++e) {
+            const uint32_t jo = s_list[wave][e];
+            const int j = (int)(jo >> 4);
+            // staged records by byte offset: one LDS address for all three arrays
+            const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g0) + jo);
+            const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g1) + jo);
             const float dx = g0.x - fpx, dy = g0.y - fpy;
             // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
             const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
             const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
-            const bool hit = !done && !(p2 > 0.0f) && !(alpha < kAlphaMin);
-            if (!__any(hit)) continue;
+            // skipped: finished pixels, power > 0, alpha < 1/255; each vote
+            // below is a single compare, so it is the compare's lane mask
+            float alpha_eff = (done || p2 > 0.0f) ? 0.0f : alpha;
+            // keep the select materialised (an empty constraint, no code):
+            // otherwise the compiler turns it back into three combined masks
+            // and rebuilds a vector 0/1 for the vote
+            __asm__ volatile("" : "+v"(alpha_eff));
+            const bool hit = alpha_eff >= kAlphaMin;
+            if (!wave_any(hit)) continue;
             const float Tn = T * (1.0f - alpha);
-            const bool stop = hit && Tn < kTMin;
-            const bool inc = hit && !stop;
+            const bool inc = hit && Tn >= kTMin;
             const float w = inc ? alpha * T : 0.0f;
-            const float4 c = s_col[j];
+            const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_col) + jo);
             cr = __builtin_fmaf(w, c.x, cr);
             cg = __builtin_fmaf(w, c.y, cg);
             cb = __builtin_fmaf(w, c.z, cb);
             T = inc ? Tn : T;
-            if (COUNT && stop) stop_pos = b + (uint32_t)j;
-            done = done || stop;
+            bool all_done = false;
+            if (wave_any(Tn < kTMin)) {   // rare: a pixel may stop at this Gaussian
+                const bool stop = hit && Tn < kTMin;
+                if (COUNT && stop) stop_pos = b + (uint32_t)j;
+                done = done || stop;
+                all_done = wave_all(done);
+            }
             if (CAPTURE) {
                 const float dep = g1.z;
                 d0 = (inc && !pivot) ? dep : d0;
@@ -143,9 +163,10 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
                 sw += w;
                 s1 = __builtin_fmaf(w, dd, s1);
                 s2 = __builtin_fmaf(w * dd, dd, s2);
-                const uint64_t m = __ballot(inc);
-                if (m != 0ull && lane == 0) s_flag[j] = 1u;
-                if (CONTRIB && m != 0ull) {
+                // w > 0 exactly where the pixel composites (alpha, T > 0)
+                const bool any_inc = wave_any(w > 0.0f);
+                if (any_inc && lane == 0) s_flag[j] = 1u;
+                if (CONTRIB && any_inc) {
                     float mw = w;
 #pragma unroll
                     for (int o = 32; o >= 1; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
@@ -154,6 +175,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
                                   __float_as_uint(mw));
                 }
             }
+            if (all_done) break;
         }
         __syncthreads();
         if (CAPTURE && a.g_flag && k < range.y && s_flag[tid]) a.g_flag[s_idx[tid]] = 1u;
