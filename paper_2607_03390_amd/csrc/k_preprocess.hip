@@ -2,11 +2,11 @@
 // temporal dynamic culling of Sec. III-D and the newly-visible test of the
 // occluded-tile detection (Sec. III-E) folded in.
 //
-// One thread per Gaussian.  The scene is stored as 16-byte attribute groups
-// and wave-tiled SH blocks, so every wave load is one contiguous 1 KB request;
-// only the mean (16 bytes) is read for a culled Gaussian, and the SH
-// coefficients (192 of the 240 bytes per Gaussian at degree 3) only for
-// survivors that touch a tile.  The kernel is HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
+// One thread per Gaussian.  Only the mean (16 bytes, one coalesced 1 KB
+// request per wave) is read for a culled Gaussian; the geometry (32 bytes)
+// for the survivors and the SH coefficients (192 of the 240 bytes per
+// Gaussian at degree 3) for survivors that touch a tile, each Gaussian's
+// bytes contiguous so that sparse survivors fetch only their own lines.  The kernel is HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
 // and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.
@@ -49,10 +49,10 @@ __device__ inline void sh_colour(const SceneDev &s, int i, float dx, float dy, f
         }
     }
     float f[4 * SLOTS];
-    const float4 *p = s.sh + (size_t)(i >> 6) * SLOTS * 64 + (i & 63);
+    const float4 *p = s.sh + (size_t)i * SLOTS;
 #pragma unroll
     for (int j = 0; j < SLOTS; ++j) {
-        const float4 v = p[j * 64];
+        const float4 v = p[j];
         f[4 * j + 0] = v.x;
         f[4 * j + 1] = v.y;
         f[4 * j + 2] = v.z;
@@ -102,16 +102,23 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
             if (pxf >= 0.0f && pxf <= (float)(cam.W - 1) && pyf >= 0.0f &&
                 pyf <= (float)(cam.H - 1) && !cull.g_rendered[i]) {
                 const int p = (int)pyf * cam.W + (int)pxf;
-                const float dm = cull.dmin[p], sm = cull.smax[p];
-                if (tz > dm + cull.lambda2 * sm) alive = false;
-                else if (tz <= dm - cull.lambda1 * sm) newly = true;
+                const float dm = cull.dmin[p];
+                // with lambda2 = 0 the cull needs only the depth (dm + 0 * sm
+                // is dm: sm is finite), so sm is read for the survivors only
+                if (cull.lambda2 == 0.0f && tz > dm) {
+                    alive = false;
+                } else {
+                    const float sm = cull.smax[p];
+                    if (tz > dm + cull.lambda2 * sm) alive = false;
+                    else if (tz <= dm - cull.lambda1 * sm) newly = true;
+                }
             }
         }
         survivor = alive;
         if (alive) {
             // 3D covariance R S S^T R^T from the normalised quaternion
-            const float4 sq = s.scale_qw[i];
-            const float4 qv = s.qxyz[i];
+            const float4 sq = s.geo[2 * (size_t)i];
+            const float4 qv = s.geo[2 * (size_t)i + 1];
             const float q0 = sq.w, q1 = qv.x, q2 = qv.y, q3 = qv.z;
             const float qn = sqrtf(((q0 * q0 + q1 * q1) + q2 * q2) + q3 * q3);
             const float r = q0 / qn, x = q1 / qn, y = q2 / qn, z = q3 / qn;

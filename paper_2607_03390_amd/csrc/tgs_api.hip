@@ -578,7 +578,7 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
     sc->ncoef = ncoef;
     const int slots = (3 * ncoef + 3) / 4;
     const size_t n_pad = ((size_t)(n > 0 ? n : 1) + 63) / 64 * 64;
-    const size_t n_vec = n_pad * (3 + (size_t)slots);   // float4 count
+    const size_t n_vec = n_pad * (3 + (size_t)slots);   // float4 count: mean, 2 geometry, SH
     tgs_status s = sc->data.ensure(n_vec * sizeof(float4));
     if (s != TGS_OK) {
         delete sc;
@@ -604,19 +604,27 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
         stage[i] = make_float4(d->means[3 * (size_t)i], d->means[3 * (size_t)i + 1],
                                d->means[3 * (size_t)i + 2], d->opacities[i]);
     e = put(base);
+    // geometry: (sx, sy, sz, qw), (qx, qy, qz, 0) side by side per Gaussian
     if (e == hipSuccess) {
-        for (int i = 0; i < n; ++i)
-            stage[i] = make_float4(d->scales[3 * (size_t)i], d->scales[3 * (size_t)i + 1],
-                                   d->scales[3 * (size_t)i + 2], d->rotations[4 * (size_t)i]);
-        e = put(base + n_pad);
+        std::vector<float4> geo;
+        try {
+            geo.assign(2 * n_pad, make_float4(0.0f, 0.0f, 0.0f, 0.0f));
+        } catch (...) {
+            delete sc;
+            return fail(TGS_ERR_OUT_OF_MEMORY, "host staging allocation failed");
+        }
+        for (int i = 0; i < n; ++i) {
+            geo[2 * (size_t)i] = make_float4(d->scales[3 * (size_t)i], d->scales[3 * (size_t)i + 1],
+                                             d->scales[3 * (size_t)i + 2], d->rotations[4 * (size_t)i]);
+            geo[2 * (size_t)i + 1] =
+                make_float4(d->rotations[4 * (size_t)i + 1], d->rotations[4 * (size_t)i + 2],
+                            d->rotations[4 * (size_t)i + 3], 0.0f);
+        }
+        e = hipMemcpyAsync(base + n_pad, geo.data(), geo.size() * sizeof(float4),
+                           hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
     }
-    if (e == hipSuccess) {
-        for (int i = 0; i < n; ++i)
-            stage[i] = make_float4(d->rotations[4 * (size_t)i + 1], d->rotations[4 * (size_t)i + 2],
-                                   d->rotations[4 * (size_t)i + 3], 0.0f);
-        e = put(base + 2 * n_pad);
-    }
-    // SH: wave-tiled, one staging pass per 64-Gaussian block row of slots
+    // SH: each Gaussian's slots contiguous
     if (e == hipSuccess) {
         const size_t per = (size_t)ncoef * 3;
         std::vector<float4> sh;
@@ -634,7 +642,7 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
                     const size_t f = 4 * (size_t)j + c;
                     v[c] = f < per ? src[f] : 0.0f;
                 }
-                sh[((size_t)(i >> 6) * slots + j) * 64 + (i & 63)] = make_float4(v[0], v[1], v[2], v[3]);
+                sh[(size_t)i * slots + j] = make_float4(v[0], v[1], v[2], v[3]);
             }
         }
         e = hipMemcpyAsync(base + 3 * n_pad, sh.data(), sh.size() * sizeof(float4),
@@ -651,8 +659,7 @@ tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **o
     v.ncoef = ncoef;
     v.sh_slots = slots;
     v.mean_op = base;
-    v.scale_qw = base + n_pad;
-    v.qxyz = base + 2 * n_pad;
+    v.geo = base + n_pad;
     v.sh = base + 3 * n_pad;
     *out = sc;
     return TGS_OK;

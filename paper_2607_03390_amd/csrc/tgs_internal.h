@@ -23,16 +23,18 @@ struct CamK {
     float campos[3];          // camera centre in world space
 };
 
-// Device scene.  Attributes are grouped in 16-byte vectors so a wave loads
-// each group as one contiguous 1 KB request; the SH coefficients (the bulk of
-// the bytes) are stored wave-tiled: for Gaussian i, float4 slot j lives at
-// ((i / 64) * sh_slots + j) * 64 + i % 64.
+// Device scene.  Means and opacities are one float4 per Gaussian in their own
+// array (every Gaussian's is read each frame, one coalesced 1 KB request per
+// wave).  The rest is read only for Gaussians that survive the culls, often
+// a scattered minority of a wave, so each Gaussian's bytes are contiguous:
+// two geometry float4s (32 bytes) and sh_slots SH float4s (192 bytes, three
+// whole 64-byte lines, at degree 3), and a culled Gaussian's lines are
+// never fetched.
 struct SceneDev {
     int n, deg, ncoef, sh_slots;
     const float4 *mean_op;    // x, y, z, opacity
-    const float4 *scale_qw;   // sx, sy, sz, qw
-    const float4 *qxyz;       // qx, qy, qz, 0
-    const float4 *sh;         // wave-tiled coefficient-major (k*3 + channel) floats
+    const float4 *geo;        // [2i] = (sx, sy, sz, qw), [2i + 1] = (qx, qy, qz, 0)
+    const float4 *sh;         // [i * sh_slots + j]: coefficient-major (k*3 + channel) floats
 };
 
 // Per-Gaussian records written by the preprocess.
