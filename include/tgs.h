@@ -48,7 +48,7 @@ typedef enum {
     TGS_ERR_OUT_OF_MEMORY = 2,   /* a device or host allocation failed        */
     TGS_ERR_DEVICE = 3,          /* a HIP call or kernel launch failed        */
     TGS_ERR_STATE_MISMATCH = 4,  /* camera size differs from the state's      */
-    TGS_ERR_CAPACITY = 5         /* more than 2^30-1 keys in one frame        */
+    TGS_ERR_CAPACITY = 5         /* more than 0xffff0000 keys in one frame     */
 } tgs_status;
 
 /* Frame kinds reported in tgs_frame_out.frame_kind (Sec. III-B, III-E). */

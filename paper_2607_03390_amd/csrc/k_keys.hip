@@ -135,11 +135,11 @@ __global__ __launch_bounds__(256) void ranges_zero_kernel(int n_tiles, uint2 *ra
 
 __global__ __launch_bounds__(256) void ranges_kernel(const Counters *cnt, const uint32_t *keys,
                                                      uint2 *ranges) {
-    const uint32_t K = cnt->n_sorted;
-    for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
+    const uint64_t K = cnt->n_sorted;
+    for (uint64_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
         const uint32_t t = keys[k];
-        if (k == 0 || keys[k - 1] != t) ranges[t].x = k;
-        if (k == K - 1 || keys[k + 1] != t) ranges[t].y = k + 1;
+        if (k == 0 || keys[k - 1] != t) ranges[t].x = (uint32_t)k;
+        if (k == K - 1 || keys[k + 1] != t) ranges[t].y = (uint32_t)(k + 1);
     }
 }
 

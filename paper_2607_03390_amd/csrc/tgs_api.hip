@@ -397,7 +397,8 @@ tgs_status step_wait_counters(Workspace &ws, hipStream_t st, FrameResult &fr, bo
     *overflow = fr.K > 0 && h->n_sorted == 0;
     if (*overflow && fr.K > kMaxKeys)
         return fail(TGS_ERR_CAPACITY, "frame needs " + std::to_string(fr.K) +
-                                          " Gaussian-tile keys; the limit is 2^30-1");
+                                          " or more Gaussian-tile keys; the limit is " +
+                                          std::to_string(kMaxKeys));
     if (!*overflow) ws.last_K = fr.K;
     return TGS_OK;
 }

@@ -12,7 +12,9 @@ constexpr float kAlphaMin = 1.0f / 255.0f;
 constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 1e-4f;
 constexpr int kTile = 16;
-constexpr uint32_t kMaxKeys = (1u << 30) - 1;
+// Key positions are 32-bit; the limit leaves headroom so that block bases
+// (partition * tile, block * 1024) and loop strides never wrap.
+constexpr uint32_t kMaxKeys = 0xffff0000u;
 
 // Camera constants as the kernels consume them.
 struct CamK {
