@@ -8,8 +8,9 @@ one through the HIP kernels of libtgs.  The scene is resident in HBM before
 the timed region starts.
 
 Printed (one JSON line): temporal-mode FPS (value), full-render FPS over the
-same path (both with the 3DGS 3-sigma tile rule; the same two timings with
-the alpha-footprint tile rule alongside), PSNR of temporal vs full, the roofline of the dominant kernel (its
+same path (both with the 3DGS 3-sigma tile rule and the paper-literal empty
+pixels; the same timings with the alpha-footprint tile rule and with empty
+pixels on the far plane alongside), PSNR of temporal vs full, the roofline of the dominant kernel (its
 launch durations from HIP events attached to its dispatches inside the timed
 region), a per-stage breakdown from an untimed pass, and the CPU oracle timed
 on a bounded sample of the same workload.
@@ -52,7 +53,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-psnr", action="store_true")
     ap.add_argument("--no-footprint", action="store_true",
-                    help="skip the timing of the footprint tile rule")
+                    help="skip the variant timings (footprint tile rule, empty pixels at z_far)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also run the ablation and sensitivity study (culling and selective "
+                         "rendering toggles, lambda / eta sweeps, camera speed)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
     return ap.parse_args()
@@ -185,31 +189,86 @@ def main():
                     min_db=float(np.min(vals)) if vals else None,
                     frames_compared=len(vals), identical_frames=n_frames - len(vals))
 
-    # the same path with the alpha-footprint tile rule (same contributions
-    # up to the 3-sigma clipping, fewer Gaussian-tile keys)
-    fp = None
-    if not args.no_footprint:
-        tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_FOOTPRINT)
-        temporal_step()
-        full_step()
+    def variant(label, cams_v, tile_bound=tgs.TGS_TILES_3SIGMA, steps=None, full=False, **pkw):
+        """Temporal FPS, frame mix and PSNR vs the full render of one setting."""
+        steps = steps or args.steps
+        tgs.tgs_scene_set_tile_bound(scene_h, tile_bound)
+        sv = tgs.tgs_state_create(scene_h, W, H, tgs.params(**pkw))
+
+        def run(rec=None):
+            tgs.tgs_state_reset(sv)
+            for cam in cams_v:
+                info = tgs.tgs_render_temporal(sv, cam, **out_t)
+                if rec is not None:
+                    rec.append(info)
+
+        run()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for k in range(args.steps):
-            temporal_step()
+        for _ in range(steps):
+            run()
         torch.cuda.synchronize()
-        fp_t = time.perf_counter() - t0
-        t0 = time.perf_counter()
-        for k in range(args.steps):
-            full_step()
-        torch.cuda.synchronize()
-        fp_f = time.perf_counter() - t0
+        dt = time.perf_counter() - t0
+        rec = []
+        run(rec)
+        nv = len(cams_v)
+        sel = [100.0 * i["n_selected"] / (TX * TY) for i in rec if i["frame_kind"] == tgs.TGS_FRAME_TGS]
+        r = {"label": label, "params": pkw, "tile_rule": "footprint" if tile_bound else "3sigma",
+             "frames": nv, "temporal_fps": round(nv * steps / dt, 2),
+             "temporal_ms_per_frame": round(1e3 * dt / (steps * nv), 4),
+             "tgsf_pct": round(100.0 * sum(i["frame_kind"] == tgs.TGS_FRAME_TGS for i in rec) / nv, 2),
+             "sr_tile_pct": round(float(np.mean(sel)), 2) if sel else None}
+        if full:
+            for cam in cams_v:
+                tgs.tgs_render_full(scene_h, cam, **out_f)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                for cam in cams_v:
+                    tgs.tgs_render_full(scene_h, cam, **out_f)
+            torch.cuda.synchronize()
+            dtf = time.perf_counter() - t0
+            r["full_fps"] = round(nv * steps / dtf, 2)
+            r["full_ms_per_frame"] = round(1e3 * dtf / (steps * nv), 4)
+            r["speedup_temporal_vs_full"] = round(dtf / dt, 3)
+        if not args.no_psnr:
+            vals = []
+            tgs.tgs_state_reset(sv)
+            for cam in cams_v:
+                tgs.tgs_render_temporal(sv, cam, **out_t)
+                tgs.tgs_render_full(scene_h, cam, **out_f)
+                mse = torch.mean((out_t["rgb"].clamp(0, 1) - out_f["rgb"].clamp(0, 1)) ** 2).item()
+                if mse > 0:
+                    vals.append(-10.0 * math.log10(mse))
+            r["psnr_mean_db"] = round(float(np.mean(vals)), 2) if vals else None
+            r["psnr_min_db"] = round(float(np.min(vals)), 2) if vals else None
+        tgs.tgs_state_free(sv)
         tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_3SIGMA)
-        fp = {"tile_rule": "alpha >= 1/255 footprint box",
-              "temporal_fps": round(n_frames * args.steps / fp_t, 2),
-              "full_fps": round(n_frames * args.steps / fp_f, 2),
-              "temporal_ms_per_frame": round(1e3 * fp_t / (args.steps * n_frames), 4),
-              "full_ms_per_frame": round(1e3 * fp_f / (args.steps * n_frames), 4)}
-        log(f"[bench] footprint tile rule timed: {fp}")
+        log(f"[bench] variant {label}: {r}")
+        return r
+
+    variants = {}
+    if not args.no_footprint:
+        # the alpha-footprint tile rule (same contributions up to the 3-sigma
+        # clipping, fewer Gaussian-tile keys) and empty pixels on the far plane
+        variants["footprint_tile_rule"] = variant("footprint tile rule", cams,
+                                                  tile_bound=tgs.TGS_TILES_FOOTPRINT, full=True)
+        variants["empty_far"] = variant("empty pixels at z_far", cams, empty_far=1)
+    ablation = None
+    if args.ablation:
+        ablation = []
+        for label, kw in (("all on", {}), ("no AFC", dict(enable_afc=0)),
+                          ("no TOC", dict(enable_toc=0)), ("no SR", dict(enable_sr=0)),
+                          ("lambda_SR 2", dict(lambda_sr=2)), ("lambda_SR 10", dict(lambda_sr=10)),
+                          ("lambda_TDC 25", dict(lambda_tdc=25)), ("lambda_TDC 100", dict(lambda_tdc=100)),
+                          ("eta 0.2", dict(eta=0.2)), ("eta 0.6", dict(eta=0.6)),
+                          ("empty_far, footprint", dict(empty_far=1))):
+            tb = tgs.TGS_TILES_FOOTPRINT if "footprint" in label else tgs.TGS_TILES_3SIGMA
+            ablation.append(variant(label, cams, tile_bound=tb, steps=2, **kw))
+        for v in (2.0, 4.0):
+            cv = synth.workload(args.workload, n_frames=args.frames, speed=v).cameras
+            ablation.append(variant(f"camera speed x{v:g}", cv, steps=2))
+        log("[bench] ablation done")
 
     n_tgs = sum(1 for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS)
     sr_pct = [100.0 * i["n_selected"] / (TX * TY) for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS]
@@ -267,7 +326,7 @@ def main():
         "full": {"fps": round(fps_f, 2), "ms_per_frame": round(1e3 * t_full / (args.steps * n_frames), 4)},
         "speedup_temporal_vs_full": round(fps_t / fps_f, 3),
         "tile_rule": "3DGS 3-sigma square",
-        "footprint_tile_rule": fp,
+        **variants,
         "psnr_temporal_vs_full": psnr,
         "stage_ms_per_frame": {s: per_frame(s) for s in tgs.PROF_STAGES if detail[s]["ms"] > 0},
         "stage_full_ms_per_frame": {s: round(v["ms"] / n_frames, 4)
@@ -277,6 +336,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if ablation is not None:
+        res["ablation"] = ablation
     tgs.tgs_state_free(state_h)
     tgs.tgs_scene_free(scene_h)
     print(json.dumps(res), flush=True)

@@ -98,7 +98,13 @@ typedef struct {
     int32_t enable_afc;       /* 1: adaptive frustum culling                   */
     int32_t enable_toc;       /* 1: temporal occlusion culling                 */
     int32_t enable_sr;        /* 1: selective rendering (0 = render every tile)*/
-    int32_t force_all_dirty;  /* 0: select every tile in TGS frames (testing)  */
+    int32_t force_all_dirty;  /* 1: select every tile in TGS frames (testing)  */
+    int32_t empty_far;        /* 1: a reference pixel where no Gaussian is      */
+                              /*    composited gets depth z_far (1000) in the   */
+                              /*    geometry buffer and the depth output, so it */
+                              /*    warps and is stitched like a far surface;   */
+                              /*    0 (default): NOHIT, never warped, its tile  */
+                              /*    is re-rendered (Eq. 1 has no value there)   */
 } tgs_params;
 
 /* Outputs of one rendered frame.  rgb is required; the other pointers may be

@@ -32,6 +32,7 @@ GCC_CMD = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fno-fast-ma
            "-fPIC", "-shared", "-o", LIB_PATH, SRC_PATH, "-lm"]
 
 NOHIT = np.float32(1001.0)          # z_far + epsilon (Sec. III-C)
+Z_FAR = np.float32(1000.0)          # the far plane
 NEAR_CULLED, AFC_CULLED, TOC_CULLED, DEGENERATE, NO_TILES, VISIBLE = range(6)
 TILES_3SIGMA, TILES_FOOTPRINT = 0, 1   # tile rectangle rules (Sec. III-A intersection)
 TRUE_REF, PSEUDO_REF, TGS_FRAME = 0, 1, 2
@@ -103,6 +104,7 @@ class Params:
     enable_sr: bool = True
     force_all_dirty: bool = False
     tile_bound: int = 0          # TILES_3SIGMA or TILES_FOOTPRINT
+    empty_far: bool = False      # empty reference pixels at the far plane, not NOHIT
 
 
 # --------------------------------------------------------------------------
@@ -388,7 +390,11 @@ class TemporalOracle:
         if kind == PSEUDO_REF and self.p.enable_afc:
             cull = dict(afc=True, fbox=self.fbox)
         out = render_full(self.scene, cam, self.p.z_near, cull, self.p.tile_bound)
-        # temporal priors (Sec. III-C)
+        # temporal priors (Sec. III-C).  Eq. 1 has no value where nothing is
+        # composited: NOHIT (never warped), or with empty_far the far plane,
+        # so such pixels warp like a distant surface and are stitched
+        if self.p.empty_far:
+            out["D"] = np.where(out["D"] == float(NOHIT), float(Z_FAR), out["D"])
         self.D = out["D"].astype(np.float32)
         self.S = out["sigma"].astype(np.float32)
         self.tab = out["rgb"].astype(np.float32)

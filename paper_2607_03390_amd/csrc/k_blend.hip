@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
         a.tab[2 * HW + q] = cb;
     }
     if (CAPTURE) {
-        float D = kNoHit, S = 0.0f;
+        float D = a.empty_depth, S = 0.0f;
         if (sw > 0.0f) {
             const float m1 = s1 / sw;
             D = d0 + m1;

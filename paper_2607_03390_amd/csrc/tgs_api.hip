@@ -468,6 +468,7 @@ BlendArgs blend_args(const Workspace &ws, int W, int H, const uint32_t *vals) {
     a.g0 = ws.g0.as<float4>();
     a.g1 = ws.g1.as<float4>();
     a.col = ws.col.as<float4>();
+    a.empty_depth = kNoHit;
     return a;
 }
 
@@ -487,6 +488,8 @@ tgs_status check_params(const tgs_params *p) {
         return fail(TGS_ERR_INVALID_ARG, "lambda1, lambda2 must be finite");
     if (!(finite(p->z_near) && p->z_near > 0.0f))
         return fail(TGS_ERR_INVALID_ARG, "z_near must be finite and > 0");
+    if (p->empty_far != 0 && p->empty_far != 1)
+        return fail(TGS_ERR_INVALID_ARG, "empty_far must be 0 or 1");
     return TGS_OK;
 }
 
@@ -547,6 +550,7 @@ void tgs_params_default(tgs_params *p) {
     p->enable_toc = 1;
     p->enable_sr = 1;
     p->force_all_dirty = 0;
+    p->empty_far = 0;
 }
 
 tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **out) {
@@ -901,6 +905,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.sigma = out->sigma;
             a.alpha = out->alpha;
             a.tgb_depth = s->tgb_d.as<float>();
+        a.empty_depth = p.empty_far ? kZFar : kNoHit;
             a.tgb_sigma = s->tgb_s.as<float>();
             a.g_flag = s->g_flag.as<uint8_t>();
             a.contrib = out->contrib;

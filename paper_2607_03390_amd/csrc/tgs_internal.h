@@ -8,6 +8,7 @@
 namespace tgs {
 
 constexpr float kNoHit = 1001.0f;           // z_far (1000) + epsilon (1)
+constexpr float kZFar = 1000.0f;            // far plane
 constexpr float kAlphaMin = 1.0f / 255.0f;
 constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 1e-4f;
@@ -169,6 +170,7 @@ struct BlendArgs {
     uint8_t *g_flag;          // optional: Gaussian composited somewhere
     float *contrib;           // optional: max weight per Gaussian
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
+    float empty_depth;        // depth written where no Gaussian is composited
 };
 // start/stop (may be NULL) are attached to the dispatch itself
 // (hipExtLaunchKernelGGL): kernel timing without extra barrier packets.

@@ -308,32 +308,35 @@ WORKLOADS = {
 }
 
 
-def workload(name: str, n_frames: int | None = None, n_gaussians: int | None = None) -> Workload:
+def workload(name: str, n_frames: int | None = None, n_gaussians: int | None = None,
+             speed: float = 1.0) -> Workload:
     """Build one of the five seeded workloads.
 
     ``n_frames`` truncates the camera path; ``n_gaussians`` overrides the scene
-    size (used only by tests that want a smaller scene of the same structure).
+    size (used only by tests that want a smaller scene of the same structure);
+    ``speed`` scales the per-frame camera motion (the motion-speed study).
     """
+    v = float(speed)
     if name == "tiny":
         n = n_gaussians or 10_000
         scene = scene_uniform_cube(n, 0, degree=0)
-        cams = orbit_path(8, 3.0, 15.0, 1.0, 256, 256)
+        cams = orbit_path(8, 3.0, 15.0, 1.0 * v, 256, 256)
     elif name == "object":
         n = n_gaussians or 300_000
         scene = scene_clusters(n, 1)
-        cams = orbit_path(60, 6.0, 15.0, 0.5, 1280, 720)
+        cams = orbit_path(60, 6.0, 15.0, 0.5 * v, 1280, 720)
     elif name == "room":
         n = n_gaussians or 1_500_000
         scene = scene_room(n, 2)
-        cams = handheld_path(120, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 1920, 1080)
+        cams = handheld_path(120, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3 * v, 0.01 * v, 1920, 1080)
     elif name == "city":
         n = n_gaussians or 6_000_000
         scene = scene_city(n, 3)
-        cams = walk_path(240, (-60.0, 0.0, 1.7), 0.0, 0.2, 0.05, 1920, 1080)
+        cams = walk_path(240, (-60.0, 0.0, 1.7), 0.0, 0.2 * v, 0.05 * v, 1920, 1080)
     elif name == "stress":
         n = n_gaussians or 3_000_000
         scene = scene_room(n, 4, needle_fraction=0.2)
-        cams = orbit_path(60, 5.0, 10.0, 0.0, 3840, 2160, steps=(0.2, 8.0))
+        cams = orbit_path(60, 5.0, 10.0, 0.0, 3840, 2160, steps=(0.2 * v, 8.0 * v))
     else:
         raise KeyError(f"unknown workload {name!r}; choose from {sorted(WORKLOADS)}")
     if n_frames is not None:

@@ -56,7 +56,7 @@ class tgs_params(C.Structure):
     _fields_ = [("lambda_tdc", C.c_int32), ("lambda_sr", C.c_int32), ("eta", C.c_float),
                 ("lambda1", C.c_float), ("lambda2", C.c_float), ("z_near", C.c_float),
                 ("enable_afc", C.c_int32), ("enable_toc", C.c_int32), ("enable_sr", C.c_int32),
-                ("force_all_dirty", C.c_int32)]
+                ("force_all_dirty", C.c_int32), ("empty_far", C.c_int32)]
 
 
 class tgs_frame_out(C.Structure):

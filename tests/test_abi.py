@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layouts_match_header():
     # sizes follow from the C declarations with natural alignment
     assert C.sizeof(tgs.tgs_camera) == 16 * 4 + 4 * 4 + 2 * 4
-    assert C.sizeof(tgs.tgs_params) == 10 * 4
+    assert C.sizeof(tgs.tgs_params) == 11 * 4
     assert C.sizeof(tgs.tgs_frame_out) == 6 * 8 + 4 * 4 + 8
     assert C.sizeof(tgs.tgs_scene_desc) == 8 + 5 * 8
     assert C.sizeof(tgs.tgs_state_header) == 9 * 4 + 4 * 4 + 16 * 4 + 4 * 4
@@ -55,6 +55,7 @@ def test_params_default_are_the_papers():
     assert abs(p.eta - 0.40) < 1e-7 and p.lambda1 == 3.0 and p.lambda2 == 0.0
     assert abs(p.z_near - 0.2) < 1e-7
     assert p.enable_afc == p.enable_toc == p.enable_sr == 1 and p.force_all_dirty == 0
+    assert p.empty_far == 0
 
 
 def _bad_upload(**kw):

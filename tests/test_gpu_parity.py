@@ -223,8 +223,15 @@ def test_temporal_parity_tiny():
     assert st["tgs"] >= 1
 
 
+def test_temporal_parity_tiny_empty_far():
+    w = synth.workload("tiny")
+    st = _temporal_parity(w.scene, w.cameras, 256, 256, "tiny empty_far", empty_far=1)
+    assert st["tgs"] >= 4
+
+
 @pytest.mark.parametrize("pkw", [dict(), dict(lambda_sr=2), dict(enable_toc=0),
-                                 dict(enable_afc=0, eta=1.0), dict(enable_sr=0)])
+                                 dict(enable_afc=0, eta=1.0), dict(enable_sr=0),
+                                 dict(empty_far=1)])
 def test_temporal_parity_room_subset(pkw):
     sc = synth.scene_room(60_000, 2)
     cams = synth.handheld_path(12, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 400, 232)

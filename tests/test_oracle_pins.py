@@ -577,6 +577,28 @@ def test_static_camera_reuses_tab():
     np.testing.assert_allclose(o["rgb"][:, keep], ref["rgb"][:, keep], atol=1e-5)
 
 
+def test_static_camera_empty_far_renders_nothing():
+    """With empty pixels on the far plane every pixel of a static camera finds
+    itself, and a Gaussian that composited nowhere in the reference cannot
+    reach 1/255 anywhere: no tile is re-rendered and the frame is the TAB.
+    The paper-literal reading re-renders every tile with an empty pixel."""
+    w = synth.workload("tiny", n_frames=1)
+    cam = w.cameras[0]
+    T = O.TemporalOracle(w.scene, 256, 256, O.Params(empty_far=True))
+    ref = T.render(cam)
+    assert np.any(ref["D"] == float(O.Z_FAR)) and not np.any(ref["D"] == float(O.NOHIT))
+    o = T.render(cam)
+    assert o["kind"] == O.TGS_FRAME
+    assert np.all(o["matched"]) and not o["um"].any() and not o["oc"].any()
+    assert o["n_selected"] == 0
+    # the fp32 back-projection at the same pose lands within ~3e-5 px of the
+    # pixel centre, so the bilinear stitch is the TAB to about 1e-5
+    np.testing.assert_allclose(o["rgb"], ref["rgb"], atol=1e-5)
+    lit = O.TemporalOracle(w.scene, 256, 256)
+    lit.render(cam)
+    assert lit.render(cam)["n_selected"] > 0
+
+
 def _tgsf(lambda_tdc, lambda_sr, eta, n_frames):
     T = O.TemporalOracle.__new__(O.TemporalOracle)
     T.p = O.Params(lambda_tdc=lambda_tdc, lambda_sr=lambda_sr, eta=eta)
