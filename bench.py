@@ -29,8 +29,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "ms/frame & FPS (full vs temporal) at 1080p, 1.5M Gaussians; PSNR temporal-vs-full"
-# lane-operations per evaluated (pixel, Gaussian) pair of the blend (derivation in the design doc)
-BLEND_OPS_PER_PAIR = 25
+# Algorithmic VALU lane-operations per blended (pixel, Gaussian) pair, i.e. a
+# pair whose alpha reaches 1/255 (it is composited or stops the pixel):
+# offset 2, quadratic form 5, exp 1, alpha and its cap 2, threshold 1,
+# T(1 - alpha) 2, stop test 1, weight 1, colour 3 FMAs, T update 1 = 19;
+# reference frames add the Eq. 1/2 moments around the pivot (weight sum,
+# depth offset, two moment updates: 5) = 24.  Pairs below the threshold cost
+# nothing algorithmically (a blender may reject them by footprint bounds).
+BLEND_OPS_PER_HIT = {"blend_ref": 24, "blend_tgs": 19, "blend_full": 19}
 # non-packed fp32 VALU issue rate: 256 CUs x 64 lanes x 2.4 GHz
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "blend_traffic_room.json")
@@ -279,7 +285,8 @@ def main():
     launches = prof[dom]["launches"]
     avg_s = stage_ms[dom] / launches * 1e-3
     pairs_per_launch = counted[dom]["pairs"] / max(1, counted[dom]["launches"])
-    achieved = BLEND_OPS_PER_PAIR * pairs_per_launch / avg_s / 1e12
+    hits_per_launch = counted[dom]["hits"] / max(1, counted[dom]["launches"])
+    achieved = BLEND_OPS_PER_HIT[dom] * hits_per_launch / avg_s / 1e12
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
@@ -288,8 +295,8 @@ def main():
     roofline = {"bound": "alu", "kernel": f"blend ({dom})", "achieved": round(achieved, 3),
                 "peak": round(VALU_PEAK_TOPS, 2), "unit": "Tlane-op/s",
                 "frac": round(achieved / VALU_PEAK_TOPS, 4), "traffic": traffic,
-                "avg_launch_ms": round(avg_s * 1e3, 4), "pairs_per_launch": int(pairs_per_launch),
-                "ops_per_pair": BLEND_OPS_PER_PAIR}
+                "avg_launch_ms": round(avg_s * 1e3, 4), "hits_per_launch": int(hits_per_launch),
+                "ops_per_hit": BLEND_OPS_PER_HIT[dom], "list_pairs_per_launch": int(pairs_per_launch)}
 
     # CPU oracle on a bounded sample of the same workload
     cpu = None

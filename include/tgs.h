@@ -234,8 +234,9 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
  * separately recorded events on its stream (each such record adds a queue
  * barrier of several microseconds: use it in untimed passes).  With
  * TGS_PROFILE_COUNT_PAIRS the blend kernels also count the (pixel, Gaussian)
- * list entries their pixels evaluate up to termination (the blend's unit of
- * work).  tgs_profile_stop synchronises the device and returns, per stage,
+ * list entries their pixels evaluate up to termination (pairs) and, among
+ * them, those whose alpha reaches 1/255, i.e. that are composited or stop the
+ * pixel (hits: the pairs whose blending arithmetic cannot be skipped).  tgs_profile_stop synchronises the device and returns, per stage,
  * the summed event time and the number of timed launches.  Process-wide,
  * not thread-safe; renders must not overlap with start/stop. */
 enum { TGS_PROFILE_COUNT_PAIRS = 1, TGS_PROFILE_STAGES = 2 };
@@ -261,6 +262,7 @@ typedef struct {
     double ms[TGS_PROF_STAGES];
     int64_t launches[TGS_PROF_STAGES];
     int64_t pairs[TGS_PROF_STAGES];   /* blend stages only, if counted        */
+    int64_t hits[TGS_PROF_STAGES];    /* blend stages only, if counted        */
 } tgs_profile;
 tgs_status tgs_profile_start(int32_t flags);
 tgs_status tgs_profile_stop(tgs_profile *out);

@@ -213,12 +213,13 @@ def blend(W, H, ts, items, g, render_tiles=None):
     gu = np.zeros(n, np.uint8)
     rt = None if render_tiles is None else np.ascontiguousarray(render_tiles, np.int32)
     items_c = np.ascontiguousarray(items if items.size else np.zeros(1, np.int32), np.int32)
+    hits = C.c_int64(0)
     E = lib().or_blend(C.c_int32(W), C.c_int32(H), _p(ts), _p(items_c), _p(rt),
                        C.c_int32(0 if rt is None else rt.size), _p(g["mean2d"]), _p(g["conic"]),
                        _p(g["opacity"]), _p(g["depth"]), _p(g["rgb"]), _p(rgb), _p(D), _p(S),
-                       _p(A), _p(mpos), _p(maxw), _p(gc), _p(gu))
+                       _p(A), _p(mpos), _p(maxw), _p(gc), _p(gu), C.byref(hits))
     return dict(rgb=rgb, D=D, sigma=S, alpha=A, margin_pos=mpos, maxw=maxw,
-                g_certain=gc, g_uncertain=gu, pairs=int(E))
+                g_certain=gc, g_uncertain=gu, pairs=int(E), hits=int(hits.value))
 
 
 def blend_bruteforce(W, H, g, every_gaussian=False):

@@ -406,14 +406,14 @@ typedef struct {
     double *wbuf, *dbuf;     /* scratch of list length                         */
 } or_blend_ctx;
 
-typedef struct { double rgb[3], D, sigma, alpha; int32_t margin_pos; int64_t evaluated; } or_pixel;
+typedef struct { double rgb[3], D, sigma, alpha; int32_t margin_pos; int64_t evaluated, hits; } or_pixel;
 
 static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len, float px, float py,
                         or_pixel *out)
 {
     float T = 1.0f;
     double C[3] = {0.0, 0.0, 0.0};
-    int64_t ninc = 0;
+    int64_t ninc = 0, hits = 0;
     int32_t mpos = -1;
     int64_t j;
     for (j = 0; j < len; ++j) {
@@ -427,6 +427,7 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
             float alpha = fminf(OR_ALPHA_MAX, c->opac[i] * expf(power));
             if (fabs((double)alpha - (double)OR_ALPHA_MIN) <= OR_MARGIN_ALPHA) margin = 1;
             if (!(alpha < OR_ALPHA_MIN)) {
+                ++hits;   /* composited, or the pair that stops the pixel */
                 float Tn = T * (1.0f - alpha);
                 if (fabs((double)Tn - (double)OR_T_MIN) <= OR_MARGIN_T) margin = 1;
                 if (Tn < OR_T_MIN) {
@@ -451,6 +452,7 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
         if (stop) break;
     }
     out->evaluated = j < len ? j + 1 : len;
+    out->hits = hits;
     if (mpos >= 0 && c->g_uncertain)
         for (int64_t k = mpos; k < len; ++k) c->g_uncertain[list[k]] = 1;
     /* background is black: rgb = C + T * 0 */
@@ -473,13 +475,15 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
 
 /* Tiled blend over the listed tiles (all tiles if render_tiles == NULL).
  * Outputs are planar [3][H][W] / [H][W]; only pixels of rendered tiles are
- * written.  Returns the number of (pixel, Gaussian) pairs evaluated. */
+ * written.  Returns the number of (pixel, Gaussian) pairs evaluated (list
+ * entries up to and including the stopping one); *out_hits (if not NULL)
+ * receives the number of those pairs whose alpha reaches 1/255. */
 int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t *items,
                  const int32_t *render_tiles, int32_t n_render,
                  const float *mean2d, const float *conic, const float *opac, const float *depth,
                  const double *rgb, double *out_rgb, double *out_D, double *out_sigma,
                  double *out_alpha, int32_t *out_margin_pos, float *maxw, uint8_t *g_certain,
-                 uint8_t *g_uncertain)
+                 uint8_t *g_uncertain, int64_t *out_hits)
 {
     const int TX = (W + 15) / 16, TY = (H + 15) / 16;
     int64_t maxlen = 1;
@@ -488,7 +492,7 @@ int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t 
     or_blend_ctx c = {mean2d, conic, opac, depth, rgb, maxw, g_certain, g_uncertain,
                       (double *)malloc(sizeof(double) * (size_t)maxlen),
                       (double *)malloc(sizeof(double) * (size_t)maxlen)};
-    int64_t evaluated = 0;
+    int64_t evaluated = 0, hits = 0;
     const int nr = render_tiles ? n_render : TX * TY;
     for (int r = 0; r < nr; ++r) {
         int t = render_tiles ? render_tiles[r] : r;
@@ -506,10 +510,12 @@ int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t 
                 if (out_alpha) out_alpha[q] = p.alpha;
                 if (out_margin_pos) out_margin_pos[q] = p.margin_pos;
                 evaluated += p.evaluated;
+                hits += p.hits;
             }
     }
     free(c.wbuf);
     free(c.dbuf);
+    if (out_hits) *out_hits = hits;
     return evaluated;
 }
 

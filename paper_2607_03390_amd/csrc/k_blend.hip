@@ -67,6 +67,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     bool pivot = false;
     bool done = !inside;
     uint32_t stop_pos = range.y;   // list position of the stopping Gaussian (+1 below)
+    uint32_t n_hit = 0;            // pairs with alpha >= 1/255 before the pixel stopped
 
     for (uint32_t b = range.x; b < range.y; b += 256) {
         if (__syncthreads_count(done) == 256) break;
@@ -140,6 +141,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             __asm__ volatile("" : "+v"(alpha_eff));
             const bool hit = alpha_eff >= kAlphaMin;
             if (!wave_any(hit)) continue;
+            if (COUNT) n_hit += hit ? 1u : 0u;
             const float Tn = T * (1.0f - alpha);
             const bool inc = hit && Tn >= kTMin;
             const float w = inc ? alpha * T : 0.0f;
@@ -184,9 +186,14 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     if (COUNT) {
         // evaluated list entries: up to and including the stopping one
         unsigned long long e = inside ? (unsigned long long)(stop_pos < range.y ? stop_pos + 1 : range.y) - range.x : 0ull;
+        unsigned long long h = n_hit;
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) e += __shfl_xor(e, o);
+        for (int o = 32; o >= 1; o >>= 1) {
+            e += __shfl_xor(e, o);
+            h += __shfl_xor(h, o);
+        }
         if (lane == 0 && e) atomicAdd(a.pairs, e);
+        if (lane == 0 && h) atomicAdd(a.hits, h);
     }
     if (!inside) return;
     const size_t HW = (size_t)a.W * a.H;

@@ -273,7 +273,11 @@ struct Profiler {
         }
         return pool[used++];
     }
+    // d_pairs: [0, STAGES) evaluated pairs, [STAGES, 2 STAGES) pairs that reach alpha >= 1/255
     unsigned long long *pairs(int stage) { return on && count ? d_pairs + stage : nullptr; }
+    unsigned long long *hits(int stage) {
+        return on && count ? d_pairs + TGS_PROF_STAGES + stage : nullptr;
+    }
     // events attached to one kernel dispatch (no extra packets)
     void kernel_events(int stage, hipEvent_t *a, hipEvent_t *b) {
         *a = *b = nullptr;
@@ -506,9 +510,9 @@ const char *tgs_last_error(void) { return g_err.c_str(); }
 tgs_status tgs_profile_start(int32_t flags) {
     g_err.clear();
     if (!g_prof.d_pairs)
-        TGS_HIP(hipMalloc((void **)&g_prof.d_pairs, TGS_PROF_STAGES * sizeof(unsigned long long)));
+        TGS_HIP(hipMalloc((void **)&g_prof.d_pairs, 2 * TGS_PROF_STAGES * sizeof(unsigned long long)));
     TGS_HIP(hipDeviceSynchronize());
-    TGS_HIP(hipMemset(g_prof.d_pairs, 0, TGS_PROF_STAGES * sizeof(unsigned long long)));
+    TGS_HIP(hipMemset(g_prof.d_pairs, 0, 2 * TGS_PROF_STAGES * sizeof(unsigned long long)));
     g_prof.used = 0;
     g_prof.recs.clear();
     g_prof.count = (flags & TGS_PROFILE_COUNT_PAIRS) != 0;
@@ -529,9 +533,12 @@ tgs_status tgs_profile_stop(tgs_profile *out) {
         r.ms[rec.stage] += ms;
         r.launches[rec.stage] += 1;
     }
-    unsigned long long pairs[TGS_PROF_STAGES];
+    unsigned long long pairs[2 * TGS_PROF_STAGES];
     TGS_HIP(hipMemcpy(pairs, g_prof.d_pairs, sizeof(pairs), hipMemcpyDeviceToHost));
-    for (int k = 0; k < TGS_PROF_STAGES; ++k) r.pairs[k] = g_prof.count ? (int64_t)pairs[k] : 0;
+    for (int k = 0; k < TGS_PROF_STAGES; ++k) {
+        r.pairs[k] = g_prof.count ? (int64_t)pairs[k] : 0;
+        r.hits[k] = g_prof.count ? (int64_t)pairs[TGS_PROF_STAGES + k] : 0;
+    }
     g_prof.recs.clear();
     g_prof.used = 0;
     if (out) *out = r;
@@ -710,6 +717,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         a.alpha = out->alpha;
         a.contrib = out->contrib;
         a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
+        a.hits = g_prof.hits(TGS_PROF_BLEND_FULL);
         {
             hipEvent_t ev0, ev1;
             g_prof.kernel_events(TGS_PROF_BLEND_FULL, &ev0, &ev1);
@@ -872,6 +880,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
             a.rgb = out->rgb;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
+        a.hits = g_prof.hits(TGS_PROF_BLEND_TGS);
             {
                 hipEvent_t ev0, ev1;
                 g_prof.kernel_events(TGS_PROF_BLEND_TGS, &ev0, &ev1);
@@ -910,6 +919,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.g_flag = s->g_flag.as<uint8_t>();
             a.contrib = out->contrib;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
+        a.hits = g_prof.hits(TGS_PROF_BLEND_REF);
             {
                 hipEvent_t ev0, ev1;
                 g_prof.kernel_events(TGS_PROF_BLEND_REF, &ev0, &ev1);

@@ -170,6 +170,7 @@ struct BlendArgs {
     uint8_t *g_flag;          // optional: Gaussian composited somewhere
     float *contrib;           // optional: max weight per Gaussian
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
+    unsigned long long *hits;   // with pairs: count of pairs with alpha >= 1/255 (composited or stopping)
     float empty_depth;        // depth written where no Gaussian is composited
 };
 // start/stop (may be NULL) are attached to the dispatch itself

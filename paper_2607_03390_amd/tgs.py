@@ -67,7 +67,8 @@ class tgs_frame_out(C.Structure):
 
 
 class tgs_profile(C.Structure):
-    _fields_ = [("ms", C.c_double * 16), ("launches", C.c_int64 * 16), ("pairs", C.c_int64 * 16)]
+    _fields_ = [("ms", C.c_double * 16), ("launches", C.c_int64 * 16), ("pairs", C.c_int64 * 16),
+                ("hits", C.c_int64 * 16)]
 
 
 class tgs_state_header(C.Structure):
@@ -277,10 +278,10 @@ def tgs_profile_start(count_pairs=False, stages=False):
 
 
 def tgs_profile_stop():
-    """Per stage: summed event ms, launches, counted pairs."""
+    """Per stage: summed event ms, launches, counted pairs and hits."""
     p = tgs_profile()
     _check(lib().tgs_profile_stop(C.byref(p)))
-    return {name: dict(ms=p.ms[k], launches=p.launches[k], pairs=p.pairs[k])
+    return {name: dict(ms=p.ms[k], launches=p.launches[k], pairs=p.pairs[k], hits=p.hits[k])
             for k, name in enumerate(PROF_STAGES)}
 
 

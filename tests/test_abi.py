@@ -39,14 +39,23 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n)
 
 
-def test_struct_layouts_match_header():
-    # sizes follow from the C declarations with natural alignment
-    assert C.sizeof(tgs.tgs_camera) == 16 * 4 + 4 * 4 + 2 * 4
-    assert C.sizeof(tgs.tgs_params) == 11 * 4
-    assert C.sizeof(tgs.tgs_frame_out) == 6 * 8 + 4 * 4 + 8
-    assert C.sizeof(tgs.tgs_scene_desc) == 8 + 5 * 8
-    assert C.sizeof(tgs.tgs_state_header) == 9 * 4 + 4 * 4 + 16 * 4 + 4 * 4
-    assert C.sizeof(tgs.tgs_profile) == 16 * 8 * 3
+_STRUCTS = ("tgs_camera", "tgs_params", "tgs_frame_out", "tgs_scene_desc", "tgs_state_header",
+            "tgs_profile")
+
+
+def test_struct_layouts_match_header(tmp_path):
+    # the binding's ctypes structs against the C compiler's layout of the header
+    src = tmp_path / "sizes.c"
+    src.write_text('#include <stdio.h>\n#include "tgs.h"\nint main(void) {\n' +
+                   "".join(f'    printf("%zu\\n", sizeof({n}));\n' for n in _STRUCTS) +
+                   "    return 0;\n}\n")
+    exe = tmp_path / "sizes"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)],
+                   check=True)
+    sizes = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                            check=True).stdout.split()]
+    for name, size in zip(_STRUCTS, sizes):
+        assert C.sizeof(getattr(tgs, name)) == size, name
 
 
 def test_params_default_are_the_papers():

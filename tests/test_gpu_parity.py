@@ -324,8 +324,9 @@ def test_full_size_room_frame():
 
 
 def test_pair_count_matches_oracle():
-    """The blend's evaluated (pixel, Gaussian) pairs, the unit of the blend
-    roofline, equal the oracle's count up to margin pixels."""
+    """The blend's evaluated (pixel, Gaussian) pairs and its hits (pairs with
+    alpha >= 1/255, the unit of the blend roofline) equal the oracle's counts
+    up to margin pixels."""
     w = synth.workload("tiny", n_frames=2)
     with Uploaded(w.scene) as h:
         for cam in w.cameras:
@@ -334,6 +335,8 @@ def test_pair_count_matches_oracle():
             prof = tgs.tgs_profile_stop()
             r = O.render_full(w.scene, cam)
             got = prof["blend_full"]["pairs"]
-            log(f"    pairs gpu {got} oracle {r['pairs']}")
+            hits = prof["blend_full"]["hits"]
+            log(f"    pairs gpu {got} oracle {r['pairs']}; hits gpu {hits} oracle {r['hits']}")
             assert prof["blend_full"]["launches"] == 1
             assert abs(got - r["pairs"]) <= 1e-3 * r["pairs"]
+            assert abs(hits - r["hits"]) <= 1e-3 * r["hits"]

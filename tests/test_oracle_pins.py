@@ -289,6 +289,11 @@ def test_blend_single_gaussian_closed_form():
     np.testing.assert_allclose(r["D"][hit], Z, rtol=1e-7)
     assert np.all(r["sigma"][hit] == 0.0)
     assert np.all(r["D"][(a == 0) & ok] == float(O.NOHIT))
+    # blend work counts: each pixel of a tile in the rectangle evaluates the
+    # one list entry; the hits are the pixels whose alpha reaches 1/255
+    assert r["pairs"] == int(in_rect.sum())
+    assert abs(r["hits"] - int((a > 0).sum())) <= int((~ok).sum())
+    assert r["hits"] > 0
 
 
 def test_blend_two_gaussians_on_one_ray():
@@ -363,6 +368,7 @@ def test_blend_invariants():
     # temporal Gaussian buffer = Gaussians with a positive weight somewhere
     assert np.array_equal(r["maxw"] > 0, (r["g_certain"] > 0) | ((r["maxw"] > 0) & (r["g_uncertain"] > 0)))
     assert (r["margin_pos"] >= 0).mean() < 0.01
+    assert 0 < r["hits"] <= r["pairs"]
 
 
 # --------------------------------------------------------------------------
