@@ -4,8 +4,8 @@
 // image (temporal appearance buffer) and the set of Gaussians with a
 // positive blending weight somewhere (temporal Gaussian buffer, Sec. III-C).
 //
-// One 256-thread block (four wave64s, one per 8x8 quadrant) per 16x16 tile,
-// one pixel per thread.
+// One 256-thread block (four wave64s, one per 8x8 quadrant, each as four
+// 16-lane groups on 4x4 sub-blocks) per 16x16 tile, one pixel per thread.
 // The tile's sorted Gaussians are staged through LDS in batches of 256
 // records (48 bytes each, one coalesced gather per thread); every wave then
 // reads each record as an LDS broadcast.  A pixel stops at the Gaussian that
@@ -33,34 +33,42 @@ __device__ inline bool wave_all(bool p) { return __builtin_amdgcn_ballot_w64(!p)
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     // Staged per Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
-    // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares)
-    // so that log2 of the Gaussian falloff is a three-FMA quadratic form and
-    // the opacity is one v_exp_f32.
+    // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares,
+    // by the preprocess) so that log2 of the Gaussian falloff is a three-FMA
+    // quadratic form and the opacity is one v_exp_f32.
     __shared__ float4 s_g0[256];
     __shared__ float4 s_g1[256];
     __shared__ float4 s_col[256];
     __shared__ int s_idx[256];
-    __shared__ uint32_t s_flag[256];
-    // Wave w (the 8x8 quadrant w of the tile: column half w & 1, row half
-    // w >> 1) visits only the staged Gaussians whose alpha >= 1/255 ellipse,
-    // conservatively enlarged, meets its quadrant, in staging (= depth)
-    // order.  A square region touches fewer footprints than a 16x4 strip of
-    // the same area.
-    __shared__ uint16_t s_list[4][256];   // byte offsets (16 * staging slot)
-    __shared__ uint32_t s_cnt[4][4];
+    __shared__ uint8_t s_flag[256];
+    // The tile is cut into sixteen 4x4 sub-blocks; sub-block list L (wave
+    // L >> 2, group L & 3) holds the staging slots of the Gaussians whose
+    // alpha >= 1/255 ellipse, conservatively enlarged, meets the sub-block,
+    // in staging (= depth) order.  Each wave covers an 8x8 quadrant as four
+    // 16-lane groups, one per sub-block, and every iteration advances all
+    // four lists at once: a footprint a few pixels wide meets a 4x4 block
+    // about 60 % as often as the 8x8 quadrant.
+    __shared__ uint8_t s_list[16][256];
+    __shared__ uint32_t s_cnt[4][16];      // [staging wave][list] entries, then starts
+    __shared__ uint32_t s_len[16];         // list lengths
 
     if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) return;   // block-uniform
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;
-    const int qx = wave & 1, qy = wave >> 1;
-    const int px = tx * kTile + 8 * qx + (lane & 7), py = ty * kTile + 8 * qy + (lane >> 3);
+    // lane -> pixel: wave = 8x8 quadrant, lane >> 4 = 4x4 sub-block within it
+    const int grp = lane >> 4;
+    const int px = tx * kTile + 8 * (wave & 1) + 4 * (grp & 1) + (lane & 3);
+    const int py = ty * kTile + 8 * (wave >> 1) + 4 * (grp >> 1) + ((lane >> 2) & 3);
+    const int my_list = 4 * wave + grp;
     const bool inside = px < a.W && py < a.H;
     const float fpx = (float)px, fpy = (float)py;
     const float tile_x0 = (float)(tx * kTile), tile_y0 = (float)(ty * kTile);
     const uint2 range = a.ranges[tile];
-    constexpr float kLog2e = 1.4426950408889634f;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
+    // entries past a list's end are read too (and masked): zeroed lists make
+    // them name slot 0, which every non-empty batch stages
+    for (int k = tid; k < 16 * 256 / 4; k += 256) reinterpret_cast<uint32_t *>(&s_list[0][0])[k] = 0u;
 
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
@@ -72,90 +80,100 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     for (uint32_t b = range.x; b < range.y; b += 256) {
         if (__syncthreads_count(done) == 256) break;
         const uint32_t k = b + tid;
-        uint32_t strips = 0;
+        uint32_t lists = 0;   // bit L: the staged Gaussian meets sub-block L
         if (k < range.y) {
             const int idx = (int)a.vals[k];
-            const float4 g0 = a.g0[idx];
-            const float4 g1 = a.g1[idx];
+            const float4 *r = a.g + 4 * (size_t)idx;
+            const float4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
             s_idx[tid] = idx;
-            s_g0[tid] = make_float4(g0.x, g0.y, -0.5f * kLog2e * g0.z, -kLog2e * g0.w);
-            s_g1[tid] = make_float4(-0.5f * kLog2e * g1.x, g1.y, g1.z, 0.0f);
-            s_col[tid] = a.col[idx];
-            // alpha >= 1/255  <=>  d^T conic d <= 2 ln(255 o): an ellipse with
-            // half extents sqrt(k Sigma'_xx), sqrt(k Sigma'_yy); enlarged by
-            // 0.2% + 0.05 px so that every pixel left out has alpha well below
-            // the threshold.
-            if (g1.y >= 0.999f * kAlphaMin) {
-                const float kq = 2.0f * __logf(fmaxf(255.0f * g1.y, 1.0f)) + 1e-3f;
-                const float det = g0.z * g1.x - g0.w * g0.w;
-                const float hx = sqrtf(kq * g1.x / det) * 1.002f + 0.05f;
-                const float hy = sqrtf(kq * g0.z / det) * 1.002f + 0.05f;
+            s_g0[tid] = make_float4(r0.x, r0.y, r3.x, r3.y);
+            s_g1[tid] = make_float4(r3.z, r1.y, r1.z, 0.0f);
+            s_col[tid] = r2;
+            const float hx = r2.w, hy = r1.w;
+            if (hx >= 0.0f) {
+                // columns / rows of 4x4 sub-blocks the culling box meets
+                uint32_t cols = 0, rows = 0;
 #pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const float xlo = tile_x0 + 8.0f * (w & 1), ylo = tile_y0 + 8.0f * (w >> 1);
-                    if (g0.x + hx >= xlo && g0.x - hx <= xlo + 7.0f && g0.y + hy >= ylo &&
-                        g0.y - hy <= ylo + 7.0f)
-                        strips |= 1u << w;
+                for (int c = 0; c < 4; ++c) {
+                    const float x0 = tile_x0 + 4.0f * c, y0 = tile_y0 + 4.0f * c;
+                    if (r0.x + hx >= x0 && r0.x - hx <= x0 + 3.0f) cols |= 1u << c;
+                    if (r0.y + hy >= y0 && r0.y - hy <= y0 + 3.0f) rows |= 1u << c;
+                }
+                // list L covers column 2 (w & 1) + (g & 1), row 2 (w >> 1) + (g >> 1)
+#pragma unroll
+                for (int L = 0; L < 16; ++L) {
+                    const int w = L >> 2, g = L & 3;
+                    const int cx = 2 * (w & 1) + (g & 1), cy = 2 * (w >> 1) + (g >> 1);
+                    if (((cols >> cx) & (rows >> cy)) & 1u) lists |= 1u << L;
                 }
             }
         }
         if (CAPTURE) s_flag[tid] = 0u;
-        // order-preserving compaction of each strip's Gaussians
-        uint64_t bal[4];
+        // order-preserving compaction of each sub-block's Gaussians: counts
+        // per staging wave, then each wave's start in every list (s_cnt
+        // becomes the exclusive prefix over waves, s_len the totals), then
+        // the entries (the votes are taken again rather than kept live)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            bal[w] = __ballot((strips >> w) & 1u);
-            if (lane == 0) s_cnt[wave][w] = (uint32_t)__popcll(bal[w]);
+        for (int L = 0; L < 16; ++L) {
+            const uint64_t bal = __ballot((lists >> L) & 1u);
+            if (lane == 0) s_cnt[wave][L] = (uint32_t)__popcll(bal);
         }
         __syncthreads();
+        if (tid < 16) {
+            uint32_t run = 0;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            if ((strips >> w) & 1u) {
-                uint32_t pos = (uint32_t)__popcll(bal[w] & lt_mask);
-                for (int sw2 = 0; sw2 < wave; ++sw2) pos += s_cnt[sw2][w];
-                s_list[w][pos] = (uint16_t)(16 * tid);
+            for (int w2 = 0; w2 < 4; ++w2) {
+                const uint32_t c = s_cnt[w2][tid];
+                s_cnt[w2][tid] = run;
+                run += c;
             }
+            s_len[tid] = run;
         }
-        // the same for every lane of the wave: keep the loop on scalar registers
-        const uint32_t n_mine = __builtin_amdgcn_readfirstlane(
-            s_cnt[0][wave] + s_cnt[1][wave] + s_cnt[2][wave] + s_cnt[3][wave]);
+        __syncthreads();
+        // an empty constraint (no code): the bits are extracted again here
+        // instead of sixteen of them living across the barriers
+        __asm__ volatile("" : "+v"(lists));
+#pragma unroll
+        for (int L = 0; L < 16; ++L) {
+            const uint64_t bal = __ballot((lists >> L) & 1u);
+            if ((lists >> L) & 1u)
+                s_list[L][(uint32_t)__popcll(bal & lt_mask) + s_cnt[wave][L]] = (uint8_t)tid;
+        }
+        // this lane's list length, and the wave's trip count (its longest
+        // list; the same for every lane: kept on scalar registers)
+        const uint32_t n_mine = s_len[my_list];
+        const uint32_t n_long = __builtin_amdgcn_readfirstlane(
+            max(max(s_len[4 * wave], s_len[4 * wave + 1]), max(s_len[4 * wave + 2], s_len[4 * wave + 3])));
         __syncthreads();
         // a wave whose pixels have all stopped skips the batch
-        const uint32_t n_run = wave_all(done) ? 0u : n_mine;
+        const uint32_t n_run = wave_all(done) ? 0u : n_long;
         for (uint32_t e = 0; e < n_run; ++e) {
-            const uint32_t jo = s_list[wave][e];
-            const int j = (int)(jo >> 4);
-            // staged records by byte offset: one LDS address for all three arrays
+            const uint32_t j = s_list[my_list][e];
+            const uint32_t jo = j << 4;   // byte offset into the staged arrays
+            const bool live = e < n_mine;
             const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g0) + jo);
             const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g1) + jo);
             const float dx = g0.x - fpx, dy = g0.y - fpy;
             // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
             const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
             const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
-            // skipped: finished pixels, power > 0, alpha < 1/255; each vote
-            // below is a single compare, so it is the compare's lane mask
-            float alpha_eff = (done || p2 > 0.0f) ? 0.0f : alpha;
-            // keep the select materialised (an empty constraint, no code):
-            // otherwise the compiler turns it back into three combined masks
-            // and rebuilds a vector 0/1 for the vote
-            __asm__ volatile("" : "+v"(alpha_eff));
-            const bool hit = alpha_eff >= kAlphaMin;
-            if (!wave_any(hit)) continue;
-            if (COUNT) n_hit += hit ? 1u : 0u;
+            // composited or stopping: a live entry of a running pixel with
+            // power <= 0 and alpha >= 1/255
+            const bool hit = live && !done && !(p2 > 0.0f) && alpha >= kAlphaMin;
             const float Tn = T * (1.0f - alpha);
-            const bool inc = hit && Tn >= kTMin;
+            const bool keep = Tn >= kTMin;   // T stays above 1e-4 (Tn is never NaN)
+            const bool inc = hit && keep;
+            const bool stop = hit && !keep;
             const float w = inc ? alpha * T : 0.0f;
             const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_col) + jo);
             cr = __builtin_fmaf(w, c.x, cr);
             cg = __builtin_fmaf(w, c.y, cg);
             cb = __builtin_fmaf(w, c.z, cb);
             T = inc ? Tn : T;
-            bool all_done = false;
-            if (wave_any(Tn < kTMin)) {   // rare: a pixel may stop at this Gaussian
-                const bool stop = hit && Tn < kTMin;
-                if (COUNT && stop) stop_pos = b + (uint32_t)j;
-                done = done || stop;
-                all_done = wave_all(done);
+            done = done || stop;
+            if (COUNT) {
+                n_hit += hit ? 1u : 0u;
+                if (stop) stop_pos = b + j;
             }
             if (CAPTURE) {
                 const float dep = g1.z;
@@ -165,19 +183,20 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
                 sw += w;
                 s1 = __builtin_fmaf(w, dd, s1);
                 s2 = __builtin_fmaf(w * dd, dd, s2);
-                // w > 0 exactly where the pixel composites (alpha, T > 0)
-                const bool any_inc = wave_any(w > 0.0f);
-                if (any_inc && lane == 0) s_flag[j] = 1u;
-                if (CONTRIB && any_inc) {
+                // w > 0 exactly where the pixel composites (alpha, T > 0);
+                // the lanes of a group write the same flag
+                if (w > 0.0f) s_flag[j] = 1u;
+                if (CONTRIB) {
+                    // max weight over the group's 16 lanes (one Gaussian)
                     float mw = w;
 #pragma unroll
-                    for (int o = 32; o >= 1; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
-                    if (lane == 0)
+                    for (int o = 8; o >= 1; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
+                    if ((lane & 15) == 0 && mw > 0.0f)
                         atomicMax(reinterpret_cast<unsigned int *>(a.contrib + s_idx[j]),
                                   __float_as_uint(mw));
                 }
             }
-            if (all_done) break;
+            if (wave_all(done)) break;
         }
         __syncthreads();
         if (CAPTURE && a.g_flag && k < range.y && s_flag[tid]) a.g_flag[s_idx[tid]] = 1u;
@@ -228,14 +247,14 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
 constexpr int kAfcBlocks = kAfcPartials;
 
 __global__ __launch_bounds__(256) void afc_partial_kernel(int n, const uint8_t *g_flag,
-                                                          const float4 *g0, int W, int H,
+                                                          const float4 *g, int W, int H,
                                                           int *partial) {
     __shared__ int s_red[4][4];
     int v[4] = {float_to_ordered(__builtin_inff()), float_to_ordered(__builtin_inff()),
                 float_to_ordered(-__builtin_inff()), float_to_ordered(-__builtin_inff())};
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         if (!g_flag[i]) continue;
-        const float4 r = g0[i];
+        const float4 r = g[4 * (size_t)i];
         const int nx = float_to_ordered((2.0f * r.x + 1.0f) / (float)W - 1.0f);
         const int ny = float_to_ordered((2.0f * r.y + 1.0f) / (float)H - 1.0f);
         v[0] = min(v[0], nx);
@@ -308,11 +327,11 @@ void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t s
         launch_blend_v<false, false>(a, n_blocks, st, start, stop);
 }
 
-void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
+void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g, int W, int H, int *fbox,
                        hipStream_t st) {
     // fbox[0..3] is the result; fbox[4..] holds kAfcBlocks x 4 partials
     int *partial = fbox + 4;
-    afc_partial_kernel<<<kAfcBlocks, 256, 0, st>>>(n, g_flag, g0, W, H, partial);
+    afc_partial_kernel<<<kAfcBlocks, 256, 0, st>>>(n, g_flag, g, W, H, partial);
     afc_final_kernel<<<1, 64, 0, st>>>(partial, kAfcBlocks, fbox);
 }
 

@@ -207,9 +207,23 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
                     float cr, cg, cbl;
                     sh_colour<DEG>(s, i, mx - cam.campos[0], my - cam.campos[1],
                                    mz - cam.campos[2], cr, cg, cbl);
-                    rec.g0[i] = make_float4(u, v, cc * dinv, -cb * dinv);
-                    rec.g1[i] = make_float4(ca * dinv, mo.w, tz, 0.0f);
-                    rec.col[i] = make_float4(cr, cg, cbl, 0.0f);
+                    const float con_a = cc * dinv, con_b = -cb * dinv, con_c = ca * dinv;
+                    // blend culling box: alpha >= 1/255 <=> d^T Sigma'^-1 d <=
+                    // 2 ln(255 o), an ellipse with half extents sqrt(k Sigma'_xx),
+                    // sqrt(k Sigma'_yy); enlarged so that every pixel left out
+                    // has alpha well below the threshold
+                    float bx = -1.0f, by = -1.0f;
+                    if (mo.w >= 0.999f * kAlphaMin) {
+                        const float kq = 2.0f * __logf(fmaxf(255.0f * mo.w, 1.0f)) + 1e-3f;
+                        bx = sqrtf(kq * ca) * 1.002f + 0.05f;
+                        by = sqrtf(kq * cc) * 1.002f + 0.05f;
+                    }
+                    constexpr float kLog2e = 1.4426950408889634f;
+                    float4 *r = rec.g + 4 * (size_t)i;
+                    r[0] = make_float4(u, v, con_a, con_b);
+                    r[1] = make_float4(con_c, mo.w, tz, by);
+                    r[2] = make_float4(cr, cg, cbl, bx);
+                    r[3] = make_float4(-0.5f * kLog2e * con_a, -kLog2e * con_b, -0.5f * kLog2e * con_c, 0.0f);
                 }
             }
         }

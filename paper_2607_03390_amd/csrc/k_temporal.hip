@@ -109,8 +109,8 @@ __global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *_
 // centres per lane, with a ballot per tile.
 __global__ __launch_bounds__(256) void occluded_kernel(WarpK w, int n,
                                                        const uint8_t *__restrict__ status,
-                                                       const float4 *g0, const float4 *g1,
-                                                       const ushort4 *rect, uint8_t *oc) {
+                                                       const float4 *g, const ushort4 *rect,
+                                                       uint8_t *oc) {
     const int lane = threadIdx.x & 63;
     const int wave = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
     const int n_waves = (int)((gridDim.x * blockDim.x) >> 6);
@@ -124,8 +124,8 @@ __global__ __launch_bounds__(256) void occluded_kernel(WarpK w, int n,
             const int i = base + l;
             const ushort4 r = rect[i];
             if (r.x > r.z || r.y > r.w) continue;
-            const float4 a = g0[i];
-            const float4 b = g1[i];
+            const float4 a = g[4 * (size_t)i];
+            const float4 b = g[4 * (size_t)i + 1];
             if (!(b.y >= 0.999f * kAlphaMin)) continue;   // alpha < 1/255 everywhere
             // tiles meeting the box of the alpha >= 1/255 ellipse (enlarged
             // by 0.2% + 0.05 px): no pixel outside it can reach the threshold
@@ -296,12 +296,12 @@ void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *
     fill_query_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, dmin, dfill, uv, um);
 }
 
-void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g0,
-                     const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st) {
+void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
+                     const ushort4 *rect, uint8_t *oc, hipStream_t st) {
     if (n <= 0) return;
     int blocks = (n + 255) / 256;
     if (blocks > 1024) blocks = 1024;
-    occluded_kernel<<<blocks, 256, 0, st>>>(w, n, status, g0, g1, rect, oc);
+    occluded_kernel<<<blocks, 256, 0, st>>>(w, n, status, g, rect, oc);
 }
 
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,

@@ -76,7 +76,7 @@ struct DevBuf {
 
 // Per-frame scratch of one render path (a scene's tgs_render_full, or a state).
 struct Workspace {
-    DevBuf g0, g1, col, rect, status, count, partial;
+    DevBuf g, rect, status, count, partial;
     DevBuf dkey, didx, dkey_alt, didx_alt, offs;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort;
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
@@ -104,9 +104,7 @@ struct Workspace {
             TGS_HIP(hipHostGetDevicePointer((void **)&host_cnt_dev, host_cnt, 0));
         }
         if (n_ != n) {
-            TGS_TRY(g0.ensure(nn * sizeof(float4)));
-            TGS_TRY(g1.ensure(nn * sizeof(float4)));
-            TGS_TRY(col.ensure(nn * sizeof(float4)));
+            TGS_TRY(g.ensure(nn * 4 * sizeof(float4)));
             TGS_TRY(rect.ensure(nn * sizeof(ushort4)));
             TGS_TRY(status.ensure(nn));
             TGS_TRY(count.ensure((nn + 4) * sizeof(uint32_t)));
@@ -156,7 +154,7 @@ struct Workspace {
     }
 
     Records records() const {
-        return Records{g0.as<float4>(),      g1.as<float4>(),       col.as<float4>(),
+        return Records{g.as<float4>(),
                        rect.as<ushort4>(),   status.as<uint8_t>(),  count.as<uint32_t>(),
                        dkey.as<uint32_t>(),  partial.as<uint32_t>()};
     }
@@ -469,9 +467,7 @@ BlendArgs blend_args(const Workspace &ws, int W, int H, const uint32_t *vals) {
     a.TY = (H + 15) / 16;
     a.ranges = ws.ranges.as<uint2>();
     a.vals = vals;
-    a.g0 = ws.g0.as<float4>();
-    a.g1 = ws.g1.as<float4>();
-    a.col = ws.col.as<float4>();
+    a.g = ws.g.as<float4>();
     a.empty_depth = kNoHit;
     return a;
 }
@@ -859,8 +855,8 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
             {
                 ProfScope ps(TGS_PROF_OCCLUDED, st);
-                launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g0.as<float4>(),
-                                ws.g1.as<float4>(), ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
+                launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g.as<float4>(),
+                                ws.rect.as<ushort4>(), s->oc.as<uint8_t>(), st);
                 TGS_LAUNCHED("occluded tiles");
             }
             const int mode = (!p.enable_sr || p.force_all_dirty) ? 1 : 0;
@@ -929,7 +925,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             {
                 ProfScope ps(TGS_PROF_CAPTURE, st);
                 if (kind == TGS_FRAME_TRUE_REF) {
-                    launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g0.as<float4>(), W, H,
+                    launch_afc_bounds(sc->n, s->g_flag.as<uint8_t>(), ws.g.as<float4>(), W, H,
                                       s->fbox.as<int>(), st);
                     TGS_LAUNCHED("adaptive frustum");
                 }
@@ -1096,11 +1092,13 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
     TGS_HIP(hipDeviceSynchronize());
     if (what == TGS_DUMP_RECORDS) {
         float *dst = static_cast<float *>(host);
-        std::vector<float4> tmp((size_t)n);
-        const DevBuf *parts[3] = {&ws.g0, &ws.g1, &ws.col};
-        for (int k = 0; k < 3; ++k) {
-            if (n) TGS_HIP(hipMemcpy(tmp.data(), parts[k]->p, (size_t)n * 16, hipMemcpyDeviceToHost));
-            for (int i = 0; i < n; ++i) memcpy(dst + (size_t)i * 12 + 4 * k, &tmp[i], 16);
+        std::vector<float4> tmp((size_t)n * 4);
+        if (n) TGS_HIP(hipMemcpy(tmp.data(), ws.g.p, (size_t)n * 64, hipMemcpyDeviceToHost));
+        for (int i = 0; i < n; ++i) {
+            // (u, v, conic a, b), (conic c, opacity, depth, 0), (r, g, b, 0)
+            memcpy(dst + (size_t)i * 12, &tmp[4 * (size_t)i], 48);
+            dst[(size_t)i * 12 + 7] = 0.0f;
+            dst[(size_t)i * 12 + 11] = 0.0f;
         }
     } else if (size) {
         TGS_HIP(hipMemcpy(host, src, size, hipMemcpyDeviceToHost));

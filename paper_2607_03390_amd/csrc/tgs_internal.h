@@ -42,9 +42,14 @@ struct SceneDev {
 
 // Per-Gaussian records written by the preprocess.
 struct Records {
-    float4 *g0;               // u, v, conic a, conic b
-    float4 *g1;               // conic c, opacity, depth, 0
-    float4 *col;              // r, g, b, 0
+    // One 64-byte record per Gaussian (one aligned line per gather):
+    // g[4i] = (u, v, conic a, conic b), g[4i + 1] = (conic c, opacity,
+    // depth, hy), g[4i + 2] = (r, g, b, hx), g[4i + 3] = (qa, qb, qc, 0):
+    // the blend's constants, computed once per Gaussian instead of once per
+    // (Gaussian, tile): q* = conic pre-scaled by -log2(e) (1/2 on the
+    // squares), and hx, hy = half extents of the box of the alpha >= 1/255
+    // ellipse enlarged by 0.2% + 0.05 px (negative: alpha < 1/255 everywhere).
+    float4 *g;
     ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
     uint8_t *status;          // bit0 survivor, bit1 newly visible
     uint32_t *count;          // keys of the Gaussian (tiles of its rectangle)
@@ -162,7 +167,7 @@ struct BlendArgs {
     const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
     const uint2 *ranges;
     const uint32_t *vals;
-    const float4 *g0, *g1, *col;
+    const float4 *g;          // 64-byte records (Records::g)
     float *rgb;               // [3][H][W]
     float *tab;               // optional second copy of rgb
     float *depth, *sigma, *alpha;       // optional outputs
@@ -179,7 +184,7 @@ void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t s
                   hipEvent_t stop = nullptr);
 // fbox must hold 4 + 4 * kAfcPartials ints (result, then partials).
 constexpr int kAfcPartials = 256;
-void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g0, int W, int H, int *fbox,
+void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g, int W, int H, int *fbox,
                        hipStream_t st);
 
 // ---- launchers (k_temporal.hip) ----
@@ -196,8 +201,8 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
                          hipStream_t st);
 void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
                        hipStream_t st);
-void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g0,
-                     const float4 *g1, const ushort4 *rect, uint8_t *oc, hipStream_t st);
+void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
+                     const ushort4 *rect, uint8_t *oc, hipStream_t st);
 // sel_cols[ty * TX + k] = column of the k-th selected tile of row ty
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
                    int *sel_list, uint32_t *rowpre, int *sel_cols, uint8_t *mask_out,
