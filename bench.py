@@ -81,7 +81,7 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2607_03390_amd import synth, tgs
+    from paper_2607_03390_amd import metrics, synth, tgs
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
@@ -91,12 +91,36 @@ def main():
     W, H = cams[0].width, cams[0].height
     TX, TY = cams[0].tiles
     n = wl.scene.n
-    scene_h = tgs.tgs_scene_upload(wl.scene)
-    state_h = tgs.tgs_state_create(scene_h, W, H, tgs.params())
     out_t = tgs.alloc_frame(W, H)
     out_f = tgs.alloc_frame(W, H)
     torch.cuda.synchronize()
-    log(f"[bench] {n} Gaussians, {W}x{H}, {len(cams)} frames uploaded")
+
+    def used():
+        free, total = torch.cuda.mem_get_info()
+        return total - free
+
+    # device memory of each path (the library allocates with hipMalloc, so
+    # the device-wide figure is read): scene, then the full render's own
+    # buffers, then the temporal state's (priors and its frame buffers)
+    mem0 = used()
+    scene_h = tgs.tgs_scene_upload(wl.scene)
+    torch.cuda.synchronize()
+    mem_scene = used() - mem0
+    tgs.tgs_render_full(scene_h, cams[0], **out_f)
+    torch.cuda.synchronize()
+    mem_full_ws = used() - mem0 - mem_scene
+    state_h = tgs.tgs_state_create(scene_h, W, H, tgs.params())
+    for cam in cams:
+        tgs.tgs_render_temporal(state_h, cam, **out_t)
+    torch.cuda.synchronize()
+    mem_state = used() - mem0 - mem_scene - mem_full_ws
+    memory = {"scene_bytes": mem_scene, "full_render_bytes": mem_scene + mem_full_ws,
+              "temporal_bytes": mem_scene + mem_state,
+              "temporal_over_full": round((mem_scene + mem_state) / max(1, mem_scene + mem_full_ws), 4),
+              "note": "device memory held by the library (scene + its render buffers; scene + "
+                      "temporal state with priors and render buffers), from hipMemGetInfo; "
+                      "output images excluded"}
+    log(f"[bench] {n} Gaussians, {W}x{H}, {len(cams)} frames uploaded; memory {memory}")
 
     def temporal_step(record=None):
         tgs.tgs_state_reset(state_h)
@@ -180,20 +204,24 @@ def main():
         torch.cuda.synchronize()
         per_kind[info["frame_kind"]].append(e0.elapsed_time(e1))
 
-    # PSNR temporal vs full (images clamped to [0,1]); identical frames excluded
-    psnr = None
+    # PSNR and SSIM temporal vs full (images clamped to [0,1]); identical
+    # frames are excluded from the PSNR mean (infinite)
+    psnr = ssim = None
     if not args.no_psnr:
-        vals = []
+        vals, svals = [], []
         tgs.tgs_state_reset(state_h)
         for cam in cams:
             tgs.tgs_render_temporal(state_h, cam, **out_t)
             tgs.tgs_render_full(scene_h, cam, **out_f)
-            mse = torch.mean((out_t["rgb"].clamp(0, 1) - out_f["rgb"].clamp(0, 1)) ** 2).item()
-            if mse > 0:
-                vals.append(-10.0 * math.log10(mse))
+            p = metrics.psnr(out_t["rgb"], out_f["rgb"])
+            if math.isfinite(p):
+                vals.append(p)
+            svals.append(metrics.ssim(out_t["rgb"], out_f["rgb"]))
         psnr = dict(mean_db=float(np.mean(vals)) if vals else None,
                     min_db=float(np.min(vals)) if vals else None,
                     frames_compared=len(vals), identical_frames=n_frames - len(vals))
+        ssim = dict(mean=round(float(np.mean(svals)), 6), min=round(float(np.min(svals)), 6),
+                    frames=len(svals))
 
     def variant(label, cams_v, tile_bound=tgs.TGS_TILES_3SIGMA, steps=None, full=False, **pkw):
         """Temporal FPS, frame mix and PSNR vs the full render of one setting."""
@@ -238,16 +266,18 @@ def main():
             r["full_ms_per_frame"] = round(1e3 * dtf / (steps * nv), 4)
             r["speedup_temporal_vs_full"] = round(dtf / dt, 3)
         if not args.no_psnr:
-            vals = []
+            vals, svals = [], []
             tgs.tgs_state_reset(sv)
             for cam in cams_v:
                 tgs.tgs_render_temporal(sv, cam, **out_t)
                 tgs.tgs_render_full(scene_h, cam, **out_f)
-                mse = torch.mean((out_t["rgb"].clamp(0, 1) - out_f["rgb"].clamp(0, 1)) ** 2).item()
-                if mse > 0:
-                    vals.append(-10.0 * math.log10(mse))
+                p = metrics.psnr(out_t["rgb"], out_f["rgb"])
+                if math.isfinite(p):
+                    vals.append(p)
+                svals.append(metrics.ssim(out_t["rgb"], out_f["rgb"]))
             r["psnr_mean_db"] = round(float(np.mean(vals)), 2) if vals else None
             r["psnr_min_db"] = round(float(np.min(vals)), 2) if vals else None
+            r["ssim_mean"] = round(float(np.mean(svals)), 5)
         tgs.tgs_state_free(sv)
         tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_3SIGMA)
         log(f"[bench] variant {label}: {r}")
@@ -274,6 +304,14 @@ def main():
         for v in (2.0, 4.0):
             cv = synth.workload(args.workload, n_frames=args.frames, speed=v).cameras
             ablation.append(variant(f"camera speed x{v:g}", cv, steps=2))
+        if args.workload == "room":
+            # the paper's interval study: one curve through key poses, sampled
+            # at growing intervals of eye travel (faster camera)
+            for iv in (0.01, 0.02, 0.04):
+                cv = synth.keyframe_path(synth.ROOM_KEY_EYES, synth.ROOM_KEY_TARGETS, iv, W, H,
+                                         n_frames=len(cams))
+                ablation.append(variant(f"key-pose curve, interval {iv:g}", cv, steps=2,
+                                        full=True))
         log("[bench] ablation done")
 
     n_tgs = sum(1 for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS)
@@ -335,6 +373,8 @@ def main():
         "tile_rule": "3DGS 3-sigma square",
         **variants,
         "psnr_temporal_vs_full": psnr,
+        "ssim_temporal_vs_full": ssim,
+        "memory": memory,
         "stage_ms_per_frame": {s: per_frame(s) for s in tgs.PROF_STAGES if detail[s]["ms"] > 0},
         "stage_full_ms_per_frame": {s: round(v["ms"] / n_frames, 4)
                                     for s, v in detail_full.items() if v["ms"] > 0},

@@ -179,6 +179,55 @@ def walk_path(n_frames, eye0, heading_deg, step, yaw_deg_per_frame, width, heigh
     return cams
 
 
+def catmull_rom(keys, u):
+    """Uniform Catmull-Rom curve through keys[0..M-1] (M >= 2) at parameters
+    u in [0, M-1]: cubic Hermite segments between consecutive keys with
+    central-difference tangents (one-sided at the two ends), so the curve
+    passes through every key with a continuous first derivative."""
+    keys = np.asarray(keys, np.float64)
+    m = len(keys)
+    tan = np.empty_like(keys)
+    tan[1:-1] = 0.5 * (keys[2:] - keys[:-2])
+    tan[0] = keys[1] - keys[0]
+    tan[-1] = keys[-1] - keys[-2]
+    u = np.asarray(u, np.float64)
+    seg = np.clip(np.floor(u).astype(np.int64), 0, m - 2)
+    t = (u - seg)[:, None]
+    t2, t3 = t * t, t * t * t
+    return ((2 * t3 - 3 * t2 + 1) * keys[seg] + (t3 - 2 * t2 + t) * tan[seg] +
+            (-2 * t3 + 3 * t2) * keys[seg + 1] + (t3 - t2) * tan[seg + 1])
+
+
+def keyframe_path(key_eyes, key_targets, interval, width, height, n_frames=None,
+                  samples_per_segment=512):
+    """Cameras on curves fitted through consecutive key poses, sampled at a
+    fixed interval of eye travel (the paper's synthetic test trajectories,
+    Sec. IV-A; a larger interval is a faster camera, Table V).
+
+    Eye positions and look-at targets each follow a Catmull-Rom curve over the
+    key index; frame k sits where the eye curve's arc length (dense chord sum)
+    reaches k * interval.  n_frames truncates the path."""
+    m = len(key_eyes)
+    u_dense = np.linspace(0.0, m - 1.0, (m - 1) * samples_per_segment + 1)
+    p = catmull_rom(key_eyes, u_dense)
+    arc = np.concatenate([[0.0], np.cumsum(np.linalg.norm(np.diff(p, axis=0), axis=1))])
+    n = int(math.floor(arc[-1] / interval + 1e-9)) + 1
+    if n_frames is not None:
+        n = min(n, n_frames)
+    u = np.interp(interval * np.arange(n), arc, u_dense)
+    eyes = catmull_rom(key_eyes, u)
+    targets = catmull_rom(key_targets, u)
+    return [make_camera(look_at(e, t), width, height) for e, t in zip(eyes, targets)]
+
+
+# key poses of the room walk-through: the eye circles the central cluster at
+# about 5 units while the gaze drifts across it
+ROOM_KEY_EYES = ((-1.5, -5.0, 0.3), (-0.5, -5.2, 0.4), (0.5, -5.1, 0.35),
+                 (1.5, -4.8, 0.3), (2.4, -4.3, 0.45), (3.2, -3.6, 0.4))
+ROOM_KEY_TARGETS = ((0.0, 0.0, 0.0), (0.1, 0.0, 0.05), (0.2, 0.1, 0.0),
+                    (0.3, 0.1, 0.0), (0.3, 0.2, 0.05), (0.2, 0.3, 0.0))
+
+
 # --------------------------------------------------------------------------
 # scenes
 # --------------------------------------------------------------------------
@@ -309,13 +358,23 @@ WORKLOADS = {
 
 
 def workload(name: str, n_frames: int | None = None, n_gaussians: int | None = None,
-             speed: float = 1.0) -> Workload:
+             speed: float = 1.0, interval: float | None = None) -> Workload:
     """Build one of the five seeded workloads.
 
     ``n_frames`` truncates the camera path; ``n_gaussians`` overrides the scene
     size (used only by tests that want a smaller scene of the same structure);
-    ``speed`` scales the per-frame camera motion (the motion-speed study).
+    ``speed`` scales the per-frame camera motion (the motion-speed study);
+    ``interval`` (room only) replaces the path by the curve fitted through the
+    room's key poses, sampled every ``interval`` units of eye travel (120
+    frames unless ``n_frames`` says otherwise).
     """
+    if interval is not None:
+        if name != "room":
+            raise KeyError("key-pose paths are defined for the room workload only")
+        scene = scene_room(n_gaussians or 1_500_000, 2)
+        cams = keyframe_path(ROOM_KEY_EYES, ROOM_KEY_TARGETS, interval, 1920, 1080,
+                             n_frames=n_frames or 120)
+        return Workload(name, scene, cams)
     v = float(speed)
     if name == "tiny":
         n = n_gaussians or 10_000
