@@ -47,7 +47,8 @@ class _Cam(C.Structure):
 class _Cull(C.Structure):
     _fields_ = [("afc", C.c_int32), ("fbox", C.c_float * 4), ("toc", C.c_int32),
                 ("dmin", C.c_void_p), ("smax", C.c_void_p), ("g_rendered", C.c_void_p),
-                ("lambda1", C.c_float), ("lambda2", C.c_float)]
+                ("lambda1", C.c_float), ("lambda2", C.c_float), ("tgb_shift", C.c_int32),
+                ("tgb_w", C.c_int32)]
 
 
 _LIB = None
@@ -105,6 +106,7 @@ class Params:
     force_all_dirty: bool = False
     tile_bound: int = 0          # TILES_3SIGMA or TILES_FOOTPRINT
     empty_far: bool = False      # empty reference pixels at the far plane, not NOHIT
+    tgb_downscale: int = 1       # 1, or 2: the geometry buffer on the half-resolution grid
 
 
 # --------------------------------------------------------------------------
@@ -176,6 +178,9 @@ def gaussians(scene, cam, z_near=0.2, cull=None, tile_bound=0):
             cs.dmin, cs.smax, cs.g_rendered = _p(dmin), _p(smax), _p(gr)
         cs.lambda1 = float(cull.get("lambda1", 3.0))
         cs.lambda2 = float(cull.get("lambda2", 0.0))
+        # TGB grid: the image, or its half-resolution grid (2x2 blocks)
+        cs.tgb_shift = int(cull.get("tgb_shift", 0))
+        cs.tgb_w = int(cull["dmin"].shape[1]) if cs.toc else 0
     cam_s = _cam(cam)
     out["n_survivors"] = int(lib().or_gaussians(
         C.c_int32(n), C.c_int32(scene.sh_degree), _p(means), _p(scales), _p(rots), _p(opac),
@@ -265,13 +270,15 @@ def depth_fill(dmin):
     return out
 
 
-def backward_query(dfill, kcur, kref, Minv, z_near=0.2):
+def backward_query(dfill, kcur, kref, Minv, z_near=0.2, tile_px=16):
+    """Correspondences and unmatched tiles; ``tile_px``: pixels per tile side
+    on this grid (16 at full resolution, 8 on the half-resolution grid)."""
     H, W = dfill.shape
-    TX, TY = (W + 15) // 16, (H + 15) // 16
+    TX, TY = (W + tile_px - 1) // tile_px, (H + tile_px - 1) // tile_px
     uv = np.zeros((H, W, 2), np.float32)
     matched = np.zeros((H, W), np.uint8)
     um = np.zeros((TY, TX), np.uint8)
-    lib().or_backward_query(C.c_int32(W), C.c_int32(H),
+    lib().or_backward_query(C.c_int32(W), C.c_int32(H), C.c_int32(tile_px),
                             _p(np.ascontiguousarray(dfill, np.float32)), _p(kcur), _p(kref),
                             _p(np.ascontiguousarray(Minv, np.float32)), C.c_float(z_near),
                             _p(uv), _p(matched), _p(um))
@@ -287,6 +294,37 @@ def occluded_tiles(W, H, g):
                             _p(g["status"]), _p(g["rect"]), _p(g["mean2d"]), _p(g["conic"]),
                             _p(g["opacity"]), _p(oc), _p(ocm))
     return oc, ocm
+
+
+def half_intr(k):
+    """Intrinsics of the half-resolution grid whose pixel (i, j) is the 2x2
+    block of pixels {2i, 2i+1} x {2j, 2j+1}: its centre (2i + 1/2, 2j + 1/2)
+    maps to (i, j), so f' = f / 2 and c' = (c - 1/2) / 2 (fp32)."""
+    k = np.asarray(k, np.float32)
+    h = np.float32(0.5)
+    return np.array([k[0] * h, k[1] * h, (k[2] - h) * h, (k[3] - h) * h], np.float32)
+
+
+def tgb_pool(D, S, A, empty_depth):
+    """Eq. 1/2 over 2x2 blocks (the geometry buffer downscaled by 2)."""
+    H, W = D.shape
+    Dh = np.zeros(((H + 1) // 2, (W + 1) // 2), np.float32)
+    Sh = np.zeros_like(Dh)
+    lib().or_tgb_pool(C.c_int32(W), C.c_int32(H), _p(np.ascontiguousarray(D, np.float64)),
+                      _p(np.ascontiguousarray(S, np.float64)), _p(np.ascontiguousarray(A, np.float64)),
+                      C.c_float(empty_depth), _p(Dh), _p(Sh))
+    return Dh, Sh
+
+
+def stitch_depth(tab, dfill_h, kcur, kref, Minv, z_near, tile_sel, out_rgb):
+    """Eq. 4 for the non-selected tiles from a half-resolution repaired depth."""
+    _, H, W = tab.shape
+    lib().or_stitch_depth(C.c_int32(W), C.c_int32(H), _p(np.ascontiguousarray(tab, np.float32)),
+                          C.c_int32(dfill_h.shape[1]), _p(np.ascontiguousarray(dfill_h, np.float32)),
+                          _p(np.asarray(kcur, np.float32)), _p(np.asarray(kref, np.float32)),
+                          _p(np.ascontiguousarray(Minv, np.float32)), C.c_float(z_near),
+                          _p(np.ascontiguousarray(tile_sel, np.uint8)), _p(out_rgb))
+    return out_rgb
 
 
 def stitch(tab, uv, tile_sel, out_rgb):
@@ -396,8 +434,12 @@ class TemporalOracle:
         # so such pixels warp like a distant surface and are stitched
         if self.p.empty_far:
             out["D"] = np.where(out["D"] == float(NOHIT), float(Z_FAR), out["D"])
-        self.D = out["D"].astype(np.float32)
-        self.S = out["sigma"].astype(np.float32)
+        if self.p.tgb_downscale == 2:
+            empty = float(Z_FAR) if self.p.empty_far else float(NOHIT)
+            self.D, self.S = tgb_pool(out["D"], out["sigma"], out["alpha"], empty)
+        else:
+            self.D = out["D"].astype(np.float32)
+            self.S = out["sigma"].astype(np.float32)
         self.tab = out["rgb"].astype(np.float32)
         self.g_rendered = (out["maxw"] > 0).astype(np.uint8)
         if kind == TRUE_REF:
@@ -413,11 +455,17 @@ class TemporalOracle:
         W, H = self.W, self.H
         kcur = _intr(cam)
         M, Minv = relative_pose(self.ref_w2c, cam.w2c)
-        dmin, smax = forward_warp(self.D, self.S, self.ref_intr, kcur, M, p.z_near)
+        # Eq. 3, depth fill and correspondences on the TGB grid
+        half = p.tgb_downscale == 2
+        kref_g = half_intr(self.ref_intr) if half else self.ref_intr
+        kcur_g = half_intr(kcur) if half else kcur
+        dmin, smax = forward_warp(self.D, self.S, kref_g, kcur_g, M, p.z_near)
         dfill = depth_fill(dmin)
-        uv, matched, um = backward_query(dfill, kcur, self.ref_intr, Minv, p.z_near)
+        uv, matched, um = backward_query(dfill, kcur_g, kref_g, Minv, p.z_near,
+                                         tile_px=8 if half else 16)
         cull = dict(afc=p.enable_afc, fbox=self.fbox, toc=p.enable_toc, dmin=dmin, smax=smax,
-                    g_rendered=self.g_rendered, lambda1=p.lambda1, lambda2=p.lambda2)
+                    g_rendered=self.g_rendered, lambda1=p.lambda1, lambda2=p.lambda2,
+                    tgb_shift=1 if half else 0)
         g = gaussians(self.scene, cam, p.z_near, cull, p.tile_bound)
         oc, oc_margin = occluded_tiles(W, H, g)
         if p.enable_sr and not p.force_all_dirty:
@@ -427,7 +475,10 @@ class TemporalOracle:
         render_tiles = np.flatnonzero(sel.ravel()).astype(np.int32)
         ts, items = tile_lists(g, self.TX, self.TY, sel)
         b = blend(W, H, ts, items, g, render_tiles)
-        stitch(self.tab, uv, sel, b["rgb"])
+        if half:
+            stitch_depth(self.tab, dfill, kcur, self.ref_intr, Minv, p.z_near, sel, b["rgb"])
+        else:
+            stitch(self.tab, uv, sel, b["rgb"])
         b.update(g=g, tile_start=ts, items=items, K=int(items.size), tile_sel=sel,
                  oc=oc, oc_margin=oc_margin, um=um, dmin=dmin, smax=smax, dfill=dfill, uv=uv,
                  matched=matched, n_selected=int(render_tiles.size),

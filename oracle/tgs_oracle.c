@@ -170,10 +170,12 @@ typedef struct {
     int32_t afc;             /* apply adaptive frustum culling            */
     float fbox[4];           /* F_min.x, F_min.y, F_max.x, F_max.y (NDC)  */
     int32_t toc;             /* apply occlusion culling + newly-visible   */
-    const float *dmin;       /* warped min depth  [H][W]                  */
-    const float *smax;       /* warped max std    [H][W]                  */
+    const float *dmin;       /* warped min depth on the TGB grid          */
+    const float *smax;       /* warped max std on the TGB grid            */
     const uint8_t *g_rendered; /* temporal Gaussian buffer [N]            */
     float lambda1, lambda2;
+    int32_t tgb_shift;       /* TGB grid = image >> tgb_shift (0 or 1)    */
+    int32_t tgb_w;           /* width of the TGB grid                     */
 } or_cull;
 
 int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const float *scales,
@@ -229,7 +231,8 @@ int32_t or_gaussians(int32_t n, int32_t sh_degree, const float *means, const flo
             float pxf = floorf(u + 0.5f), pyf = floorf(v + 0.5f);
             if (pxf >= 0.0f && pxf <= (float)(W - 1) && pyf >= 0.0f && pyf <= (float)(H - 1) &&
                 !cull->g_rendered[i]) {
-                int p = (int)pyf * W + (int)pxf;
+                /* the TGB cell holding that pixel (a 2x2 block when downscaled) */
+                int p = ((int)pyf >> cull->tgb_shift) * cull->tgb_w + ((int)pxf >> cull->tgb_shift);
                 float dm = cull->dmin[p], sm = cull->smax[p];
                 if (tz > dm + cull->lambda2 * sm) { status[i] = OR_TOC_CULLED; continue; }
                 if (tz <= dm - cull->lambda1 * sm) newly_visible[i] = 1;
@@ -643,12 +646,14 @@ void or_depth_fill(int32_t W, int32_t H, const float *dmin, float *dfill)
 /* Backward correspondence query: unproject the repaired depth in the current
  * view, move it to the reference view, project; a pixel is matched when the
  * point is in front of the near plane and lands inside [0,W-1]x[0,H-1].
- * A tile is unmatched when any of its in-image pixels is unmatched. */
-void or_backward_query(int32_t W, int32_t H, const float *dfill, const float *kcur,
+ * A tile (tile_px x tile_px pixels of this grid: 16 at full resolution, 8 on
+ * the half-resolution TGB grid) is unmatched when any of its in-grid pixels
+ * is unmatched. */
+void or_backward_query(int32_t W, int32_t H, int32_t tile_px, const float *dfill, const float *kcur,
                        const float *kref, const float *Minv, float z_near, float *uv,
                        uint8_t *matched, uint8_t *tile_um)
 {
-    const int TX = (W + 15) / 16, TY = (H + 15) / 16;
+    const int TX = (W + tile_px - 1) / tile_px, TY = (H + tile_px - 1) / tile_px;
     memset(tile_um, 0, (size_t)TX * TY);
     for (int y = 0; y < H; ++y)
         for (int x = 0; x < W; ++x) {
@@ -672,7 +677,7 @@ void or_backward_query(int32_t W, int32_t H, const float *dfill, const float *kc
             matched[q] = (uint8_t)ok;
             uv[2 * q] = ok ? u : -1.0f;
             uv[2 * q + 1] = ok ? v : -1.0f;
-            if (!ok) tile_um[(y / 16) * TX + (x / 16)] = 1;
+            if (!ok) tile_um[(y / tile_px) * TX + (x / tile_px)] = 1;
         }
 }
 
@@ -721,6 +726,98 @@ void or_stitch(int32_t W, int32_t H, const float *tab, const float *uv, const ui
             size_t q = (size_t)y * W + x;
             float u = uv[2 * q], v = uv[2 * q + 1];
             if (!(u >= 0.0f && v >= 0.0f)) {   /* unmatched: cannot occur outside selected tiles */
+                for (int ch = 0; ch < 3; ++ch) out_rgb[(size_t)ch * W * H + q] = 0.0;
+                continue;
+            }
+            int x0 = (int)floorf(u), y0 = (int)floorf(v);
+            int x1 = x0 + 1 < W ? x0 + 1 : W - 1;
+            int y1 = y0 + 1 < H ? y0 + 1 : H - 1;
+            double ax = (double)(u - (float)x0), ay = (double)(v - (float)y0);
+            for (int ch = 0; ch < 3; ++ch) {
+                const float *I = tab + (size_t)ch * W * H;
+                double i00 = I[(size_t)y0 * W + x0], i10 = I[(size_t)y0 * W + x1];
+                double i01 = I[(size_t)y1 * W + x0], i11 = I[(size_t)y1 * W + x1];
+                out_rgb[(size_t)ch * W * H + q] =
+                    (1.0 - ay) * ((1.0 - ax) * i00 + ax * i10) + ay * ((1.0 - ax) * i01 + ax * i11);
+            }
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Temporal geometry buffer downscaled by 2 (Sec. IV-B, large scenes).       */
+/* ------------------------------------------------------------------------ */
+
+/* Eq. 1 and Eq. 2 over each 2x2 block of pixels taken as one pixel: the
+ * block's composited weights are the union of its pixels', so with
+ * A_p = sum of w over pixel p (= its alpha), D_p and sigma_p its Eq. 1/2,
+ *   D_h = sum_p A_p D_p / sum_p A_p,
+ *   sigma_h^2 = sum_p A_p (sigma_p^2 + (D_p - D_h)^2) / sum_p A_p
+ * (pooled mean and variance).  A block with no composited weight gets
+ * (empty_depth, 0).  Grid: ceil(W/2) x ceil(H/2); pixels outside the image
+ * count as empty. */
+void or_tgb_pool(int32_t W, int32_t H, const double *D, const double *S, const double *A,
+                 float empty_depth, float *Dh, float *Sh)
+{
+    const int Wh = (W + 1) / 2, Hh = (H + 1) / 2;
+    for (int j = 0; j < Hh; ++j)
+        for (int i = 0; i < Wh; ++i) {
+            double sa = 0.0, sad = 0.0;
+            for (int dy = 0; dy < 2; ++dy)
+                for (int dx = 0; dx < 2; ++dx) {
+                    int x = 2 * i + dx, y = 2 * j + dy;
+                    if (x >= W || y >= H) continue;
+                    size_t q = (size_t)y * W + x;
+                    if (A[q] > 0.0) { sa += A[q]; sad += A[q] * D[q]; }
+                }
+            size_t h = (size_t)j * Wh + i;
+            if (!(sa > 0.0)) { Dh[h] = empty_depth; Sh[h] = 0.0f; continue; }
+            double d = sad / sa, sv = 0.0;
+            for (int dy = 0; dy < 2; ++dy)
+                for (int dx = 0; dx < 2; ++dx) {
+                    int x = 2 * i + dx, y = 2 * j + dy;
+                    if (x >= W || y >= H) continue;
+                    size_t q = (size_t)y * W + x;
+                    if (A[q] > 0.0) sv += A[q] * (S[q] * S[q] + (D[q] - d) * (D[q] - d));
+                }
+            Dh[h] = (float)d;
+            Sh[h] = (float)sqrt(sv / sa);
+        }
+}
+
+/* Eq. 4 with a half-resolution TGB: each full-resolution pixel of a tile
+ * that is not re-rendered is unprojected with the repaired depth of its 2x2
+ * block (grid Wh x Hh), moved to the reference view and projected with the
+ * full-resolution intrinsics; the reference image is sampled bilinearly at
+ * that point, clamped to [0,W-1]x[0,H-1] (the block matched, the pixel may
+ * land up to about a pixel outside). */
+void or_stitch_depth(int32_t W, int32_t H, const float *tab, int32_t Wh, const float *dfill_h,
+                     const float *kcur, const float *kref, const float *Minv, float z_near,
+                     const uint8_t *tile_sel, double *out_rgb)
+{
+    const int TX = (W + 15) / 16;
+    for (int y = 0; y < H; ++y)
+        for (int x = 0; x < W; ++x) {
+            if (tile_sel[(y / 16) * TX + (x / 16)]) continue;
+            size_t q = (size_t)y * W + x;
+            float d = dfill_h[(size_t)(y >> 1) * Wh + (x >> 1)];
+            float u = -1.0f, v = -1.0f;
+            int ok = 0;
+            if (d != OR_NOHIT) {
+                float rx = ((float)x - kcur[2]) / kcur[0];
+                float ry = ((float)y - kcur[3]) / kcur[1];
+                float Px = d * rx, Py = d * ry, Pz = d;
+                float X = ((Minv[0] * Px + Minv[1] * Py) + Minv[2] * Pz) + Minv[3];
+                float Y = ((Minv[4] * Px + Minv[5] * Py) + Minv[6] * Pz) + Minv[7];
+                float Z = ((Minv[8] * Px + Minv[9] * Py) + Minv[10] * Pz) + Minv[11];
+                if (Z > z_near) {
+                    u = kref[0] * (X / Z) + kref[2];
+                    v = kref[1] * (Y / Z) + kref[3];
+                    u = fminf(fmaxf(u, 0.0f), (float)(W - 1));
+                    v = fminf(fmaxf(v, 0.0f), (float)(H - 1));
+                    ok = 1;
+                }
+            }
+            if (!ok) {   /* cannot occur outside selected tiles */
                 for (int ch = 0; ch < 3; ++ch) out_rgb[(size_t)ch * W * H + q] = 0.0;
                 continue;
             }

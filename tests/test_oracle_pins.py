@@ -665,3 +665,101 @@ def test_temporal_culls_respect_buffers():
         u = np.floor(o["g"]["mean2d"][idx] + 0.5).astype(int)
         assert np.all(o["g"]["depth"][idx] > o["dmin"][u[:, 1], u[:, 0]])
     assert g0["n_survivors"] == sc.n
+
+
+# --------------------------------------------------------------------------
+# geometry buffer downscaled by 2 (Sec. IV-B, large scenes)
+# --------------------------------------------------------------------------
+
+def test_tgb_pool_is_eq12_over_the_block():
+    """Pooled D, sigma of a 2x2 block = Eq. 1/2 over the union of its
+    pixels' weighted depths, computed here directly from the samples."""
+    rng = np.random.default_rng(5)
+    W, H = 5, 3   # ragged: the last column / row of blocks is partial
+    samples = {}
+    D = np.zeros((H, W))
+    S = np.zeros((H, W))
+    A = np.zeros((H, W))
+    for y in range(H):
+        for x in range(W):
+            k = rng.integers(0, 4)   # 0 samples: an empty pixel
+            w = rng.uniform(0.01, 0.3, k)
+            d = rng.uniform(2.0, 9.0, k)
+            samples[(x, y)] = (w, d)
+            if k:
+                A[y, x] = w.sum()
+                D[y, x] = np.average(d, weights=w)
+                S[y, x] = np.sqrt(np.average((d - D[y, x]) ** 2, weights=w))
+            else:
+                D[y, x] = float(O.NOHIT)
+    Dh, Sh = O.tgb_pool(D, S, A, float(O.NOHIT))
+    assert Dh.shape == (2, 3)
+    for j in range(2):
+        for i in range(3):
+            ws, ds = [], []
+            for y in (2 * j, 2 * j + 1):
+                for x in (2 * i, 2 * i + 1):
+                    if (x, y) in samples:
+                        ws += list(samples[(x, y)][0])
+                        ds += list(samples[(x, y)][1])
+            if not ws:
+                assert Dh[j, i] == O.NOHIT and Sh[j, i] == 0.0
+                continue
+            m = np.average(ds, weights=ws)
+            sd = np.sqrt(np.average((np.array(ds) - m) ** 2, weights=ws))
+            assert abs(Dh[j, i] - m) <= 2e-6 * m
+            assert abs(Sh[j, i] - sd) <= 2e-6 * max(1.0, m)
+
+
+def test_half_grid_intrinsics_map_block_centres():
+    """The half-resolution camera sends the centre of block (i, j), at
+    (2i + 1/2, 2j + 1/2) in full-resolution pixels, to (i, j)."""
+    cam = _cam(np.eye(4), 37, 21)
+    k, kh = _intr(cam), O.half_intr(_intr(cam))
+    for i, j in ((0, 0), (5, 3), (18, 10)):
+        X = (2 * i + 0.5 - k[2]) / k[0]
+        Y = (2 * j + 0.5 - k[3]) / k[1]
+        assert abs(kh[0] * X + kh[2] - i) < 1e-5 and abs(kh[1] * Y + kh[3] - j) < 1e-5
+
+
+def test_tgb_half_static_camera():
+    """At an unchanged pose the half-resolution TGB warps onto itself, every
+    block with a depth finds itself, and the stitched tiles are the TAB."""
+    w = synth.workload("tiny", n_frames=1)
+    cam = w.cameras[0]
+    T = O.TemporalOracle(w.scene, 256, 256, O.Params(tgb_downscale=2, empty_far=True))
+    ref = T.render(cam)
+    assert T.D.shape == (128, 128)
+    o = T.render(cam)
+    assert o["kind"] == O.TGS_FRAME
+    # every block lands on itself (the relative pose of a general rotation
+    # with itself is the identity up to fp32 rounding: depths within 1 ulp)
+    np.testing.assert_allclose(o["dmin"], T.D, rtol=3e-7)
+    assert np.all(o["matched"]) and not o["um"].any() and o["um"].shape == (16, 16)
+    np.testing.assert_allclose(o["rgb"], ref["rgb"], atol=1e-5)
+
+
+def test_tgb_half_all_dirty_no_cull_equals_full():
+    w = synth.workload("tiny", n_frames=6)
+    p = O.Params(enable_afc=False, enable_toc=False, force_all_dirty=True, tgb_downscale=2)
+    T = O.TemporalOracle(w.scene, 256, 256, p)
+    for cam in w.cameras:
+        o = T.render(cam)
+        assert np.array_equal(o["rgb"], O.render_full(w.scene, cam)["rgb"])
+
+
+def test_tgb_half_sequence_close_to_full():
+    """Ragged size (odd width and height): the downscaled path runs, selects
+    tiles and stays close to the full render."""
+    sc = synth.small_scene(3000, 9, degree=1, log_scale_mean=-3.2)
+    cams = synth.orbit_path(6, 3.0, 15.0, 0.5, 101, 75)
+    T = O.TemporalOracle(sc, 101, 75, O.Params(tgb_downscale=2))
+    kinds = []
+    for cam in cams:
+        o = T.render(cam)
+        kinds.append(o["kind"])
+        if o["kind"] == O.TGS_FRAME:
+            assert o["dmin"].shape == (38, 51) and o["um"].shape == (5, 7)
+            f = O.render_full(sc, cam)
+            assert np.abs(o["rgb"] - f["rgb"]).mean() < 0.02
+    assert O.TGS_FRAME in kinds
