@@ -63,6 +63,9 @@ def parse():
     ap.add_argument("--ablation", action="store_true",
                     help="also run the ablation and sensitivity study (culling and selective "
                          "rendering toggles, lambda / eta sweeps, camera speed)")
+    ap.add_argument("--tgb-downscale", type=int, default=None,
+                    help="geometry-buffer downscale (1 or 2); default: 2 for the large-scale "
+                         "city workload (the paper's large-scene setting), 1 otherwise")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
     return ap.parse_args()
@@ -74,6 +77,8 @@ def kernel_source_hash():
 
 def main():
     args = parse()
+    if args.tgb_downscale is None:
+        args.tgb_downscale = 2 if args.workload == "city" else 1
     if args.gpus != 1:
         print(json.dumps({"error": "this build targets one GPU: the TemporalGS hot path runs "
                                    "on a single MI355X; run with --gpus 1"}))
@@ -109,7 +114,7 @@ def main():
     tgs.tgs_render_full(scene_h, cams[0], **out_f)
     torch.cuda.synchronize()
     mem_full_ws = used() - mem0 - mem_scene
-    state_h = tgs.tgs_state_create(scene_h, W, H, tgs.params())
+    state_h = tgs.tgs_state_create(scene_h, W, H, tgs.params(tgb_downscale=args.tgb_downscale))
     for cam in cams:
         tgs.tgs_render_temporal(state_h, cam, **out_t)
     torch.cuda.synchronize()
@@ -227,6 +232,7 @@ def main():
         """Temporal FPS, frame mix and PSNR vs the full render of one setting."""
         steps = steps or args.steps
         tgs.tgs_scene_set_tile_bound(scene_h, tile_bound)
+        pkw = {"tgb_downscale": args.tgb_downscale, **pkw}
         sv = tgs.tgs_state_create(scene_h, W, H, tgs.params(**pkw))
 
         def run(rec=None):
@@ -290,6 +296,9 @@ def main():
         variants["footprint_tile_rule"] = variant("footprint tile rule", cams,
                                                   tile_bound=tgs.TGS_TILES_FOOTPRINT, full=True)
         variants["empty_far"] = variant("empty pixels at z_far", cams, empty_far=1)
+        other = 2 if args.tgb_downscale == 1 else 1
+        variants[f"tgb_downscale_{other}"] = variant(f"geometry buffer downscale x{other}", cams,
+                                                     tgb_downscale=other)
     ablation = None
     if args.ablation:
         ablation = []
@@ -361,7 +370,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": synth.WORKLOADS.get(args.workload, args.workload),
                    "frames_per_step": n_frames, "gaussians": n, "width": W, "height": H,
-                   "lambda_tdc": 50, "lambda_sr": 5, "eta": 0.4},
+                   "lambda_tdc": 50, "lambda_sr": 5, "eta": 0.4,
+                   "tgb_downscale": args.tgb_downscale},
         "temporal": {"fps": round(fps_t, 2), "ms_per_frame": round(1e3 * t_temporal / (args.steps * n_frames), 4),
                      "ms_per_kind": {name: round(float(np.mean(v)), 4) if v else None
                                      for name, v in zip(("true_ref", "pseudo_ref", "tgs"),

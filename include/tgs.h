@@ -105,6 +105,16 @@ typedef struct {
                               /*    warps and is stitched like a far surface;   */
                               /*    0 (default): NOHIT, never warped, its tile  */
                               /*    is re-rendered (Eq. 1 has no value there)   */
+    int32_t tgb_downscale;    /* 1 (default), or 2: the temporal geometry       */
+                              /*    buffer on the half-resolution grid, the     */
+                              /*    paper's large-scene setting (Sec. IV-B):    */
+                              /*    cell (i,j) is the 2x2 pixel block {2i,2i+1} */
+                              /*    x {2j,2j+1} with Eq. 1/2 pooled over it;    */
+                              /*    warp, fill and correspondences run on that  */
+                              /*    grid (intrinsics f/2, (c-1/2)/2), the       */
+                              /*    occlusion tests read the block of the       */
+                              /*    mean's pixel, and stitching unprojects each */
+                              /*    pixel with its block's repaired depth       */
 } tgs_params;
 
 /* Outputs of one rendered frame.  rgb is required; the other pointers may be
@@ -182,7 +192,9 @@ tgs_status tgs_render_temporal(tgs_state *state, const tgs_camera *cam, tgs_fram
                                void *stream);
 
 /* Host layout of an exported state: this header followed by
- *   float depth[H*W], float sigma[H*W]   (temporal geometry buffer, Eq. 1/2)
+ *   float depth[Hg*Wg], float sigma[Hg*Wg] (temporal geometry buffer, Eq. 1/2,
+ *                                        on its grid: Wg = ceil(W/s),
+ *                                        Hg = ceil(H/s), s = tgb_downscale)
  *   float tab[3*H*W]                     (temporal appearance buffer)
  *   uint8_t g_rendered[n]                (temporal Gaussian buffer)        */
 typedef struct {
@@ -196,6 +208,7 @@ typedef struct {
     float fbox[4];            /* adaptive frustum F_min.xy, F_max.xy (NDC)     */
     float ref_world_to_cam[16];
     float ref_intrinsics[4];  /* fx, fy, cx, cy of the reference frame         */
+    int32_t tgb_width, tgb_height;   /* grid of the geometry buffer (Wg, Hg)   */
 } tgs_state_header;
 
 /* Export: with host == NULL, *nbytes receives the blob size; otherwise the
@@ -216,10 +229,10 @@ enum {
     TGS_DUMP_RECORDS = 3,        /* float [n][12]: u, v, conic a, b | conic c, opacity, depth, 0 | r, g, b, 0 */
     TGS_DUMP_RECTS = 4,          /* uint16 [n][4] tile rectangle x0,y0,x1,y1 (x0 > x1: none) */
     TGS_DUMP_STATUS = 5,         /* uint8 [n] bit0 survivor, bit1 newly visible     */
-    TGS_DUMP_WARP_DEPTH = 6,     /* float [H*W] warped min depth (Eq. 3)            */
-    TGS_DUMP_WARP_SIGMA = 7,     /* float [H*W] warped max sigma                    */
-    TGS_DUMP_FILLED_DEPTH = 8,   /* float [H*W] repaired depth                       */
-    TGS_DUMP_CORRESPONDENCE = 9, /* float [H*W][2] reference (u,v), -1 if unmatched  */
+    TGS_DUMP_WARP_DEPTH = 6,     /* float [Hg*Wg] warped min depth (Eq. 3), TGB grid */
+    TGS_DUMP_WARP_SIGMA = 7,     /* float [Hg*Wg] warped max sigma                  */
+    TGS_DUMP_FILLED_DEPTH = 8,   /* float [Hg*Wg] repaired depth                     */
+    TGS_DUMP_CORRESPONDENCE = 9, /* float [Hg*Wg][2] reference (u,v) on the grid, -1 if unmatched */
     TGS_DUMP_UNMATCHED = 10,     /* uint8 [TX*TY] unmatched tiles                    */
     TGS_DUMP_OCCLUDED = 11,      /* uint8 [TX*TY] occluded tiles                     */
     TGS_DUMP_SELECTED = 12       /* uint8 [TX*TY] selected tiles                     */

@@ -214,6 +214,60 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
         if (lane == 0 && e) atomicAdd(a.pairs, e);
         if (lane == 0 && h) atomicAdd(a.hits, h);
     }
+    // Eq. 1 / Eq. 2 of the pixel
+    float D = a.empty_depth, S = 0.0f;
+    if (CAPTURE && sw > 0.0f) {
+        const float m1 = s1 / sw;
+        D = d0 + m1;
+        S = sqrtf(fmaxf(0.0f, s2 / sw - m1 * m1));
+    }
+    if (CAPTURE && a.tgbh_depth) {
+        // Eq. 1/2 over each 2x2 block of the tile taken as one pixel: its
+        // composited weights are the union of its pixels', so with
+        // A = 1 - T (the pixel's summed weight) the block has the pooled
+        // D_h = sum A D / sum A and sigma_h^2 = sum A (sigma^2 + (D - D_h)^2)
+        // / sum A.  The blocks lie inside the tile: pooled through LDS (the
+        // staging arrays are free once every wave has left the batch loop).
+        __syncthreads();
+        float *s_pa = reinterpret_cast<float *>(s_g0);   // 3 x 256 floats
+        float *s_pd = s_pa + 256, *s_ps = s_pa + 512;
+        const int lp = (py - ty * kTile) * kTile + (px - tx * kTile);
+        s_pa[lp] = inside ? 1.0f - T : 0.0f;
+        s_pd[lp] = D;
+        s_ps[lp] = S;
+        __syncthreads();
+        const int Wg = (a.W + 1) >> 1, Hg = (a.H + 1) >> 1;
+        const int gx = tx * (kTile / 2) + (tid & 7), gy = ty * (kTile / 2) + (tid >> 3);
+        if (tid < 64 && gx < Wg && gy < Hg) {
+            const int l0 = 2 * (tid >> 3) * kTile + 2 * (tid & 7);
+            const int ls[4] = {l0, l0 + 1, l0 + kTile, l0 + kTile + 1};
+            float sa = 0.0f, sad = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float ak = s_pa[ls[k]];
+                if (ak > 0.0f) {
+                    sa += ak;
+                    sad += ak * s_pd[ls[k]];
+                }
+            }
+            float dh = a.empty_depth, sh = 0.0f;
+            if (sa > 0.0f) {
+                dh = sad / sa;
+                float sv = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float ak = s_pa[ls[k]];
+                    if (ak > 0.0f) {
+                        const float sk = s_ps[ls[k]], ek = s_pd[ls[k]] - dh;
+                        sv += ak * (sk * sk + ek * ek);
+                    }
+                }
+                sh = sqrtf(sv / sa);
+            }
+            a.tgbh_depth[(size_t)gy * Wg + gx] = dh;
+            a.tgbh_sigma[(size_t)gy * Wg + gx] = sh;
+        }
+    }
     if (!inside) return;
     const size_t HW = (size_t)a.W * a.H;
     const size_t q = (size_t)py * a.W + px;
@@ -226,12 +280,6 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
         a.tab[2 * HW + q] = cb;
     }
     if (CAPTURE) {
-        float D = a.empty_depth, S = 0.0f;
-        if (sw > 0.0f) {
-            const float m1 = s1 / sw;
-            D = d0 + m1;
-            S = sqrtf(fmaxf(0.0f, s2 / sw - m1 * m1));
-        }
         if (a.depth) a.depth[q] = D;
         if (a.sigma) a.sigma[q] = S;
         if (a.alpha) a.alpha[q] = 1.0f - T;
@@ -317,8 +365,8 @@ void launch_blend_v(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t
 void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t start,
                   hipEvent_t stop) {
     if (n_blocks <= 0) return;
-    const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma || a.g_flag ||
-                         a.contrib;
+    const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma ||
+                         a.tgbh_depth || a.g_flag || a.contrib;
     if (a.contrib)
         launch_blend_v<true, true>(a, n_blocks, st, start, stop);
     else if (capture)

@@ -101,7 +101,9 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
             const float pxf = floorf(u + 0.5f), pyf = floorf(v + 0.5f);
             if (pxf >= 0.0f && pxf <= (float)(cam.W - 1) && pyf >= 0.0f &&
                 pyf <= (float)(cam.H - 1) && !cull.g_rendered[i]) {
-                const int p = (int)pyf * cam.W + (int)pxf;
+                // the geometry-buffer cell holding that pixel (its 2x2 block
+                // when the buffer is downscaled)
+                const int p = ((int)pyf >> cull.tgb_shift) * cull.tgb_w + ((int)pxf >> cull.tgb_shift);
                 const float dm = cull.dmin[p];
                 // with lambda2 = 0 the cull needs only the depth (dm + 0 * sm
                 // is dm: sm is finite), so sm is read for the survivors only

@@ -53,11 +53,14 @@ __global__ __launch_bounds__(256) void forward_warp_kernel(WarpK w, const float 
     atomicMax(reinterpret_cast<unsigned int *>(smax + p), __float_as_uint(S[q]) & 0x7fffffffu);
 }
 
+// One block of tp x tp threads per tile (tp = 16 on the image, 8 on the
+// half-resolution geometry-buffer grid, where a tile is 8 x 8 cells).
 __global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *__restrict__ dmin,
                                                          float *dfill, float2 *uv, uint8_t *um) {
     const int tile = blockIdx.x;
     const int tx = tile % w.TX, ty = tile / w.TX;
-    const int px = tx * kTile + (threadIdx.x & 15), py = ty * kTile + (threadIdx.x >> 4);
+    const int px = tx * w.tp + (int)(threadIdx.x % (unsigned)w.tp);
+    const int py = ty * w.tp + (int)(threadIdx.x / (unsigned)w.tp);
     int bad = 0;
     if (px < w.W && py < w.H) {
         const int q = py * w.W + px;
@@ -261,6 +264,57 @@ __global__ __launch_bounds__(256) void stitch_kernel(WarpK w, const uint8_t *sel
     }
 }
 
+// Eq. 4 from a half-resolution repaired depth: pixel (x, y) takes the depth
+// of its block (x >> 1, y >> 1), is unprojected and moved to the reference
+// view at full resolution, and samples the reference image bilinearly at
+// the projection clamped to the image (the block matched; the pixel itself
+// may land up to about a pixel outside).
+__global__ __launch_bounds__(256) void stitch_depth_kernel(WarpK w, int Wg, const uint8_t *sel,
+                                                           const float *__restrict__ tab,
+                                                           const float *__restrict__ dfill,
+                                                           float *rgb) {
+    const int tile = blockIdx.x;
+    if (sel[tile]) return;
+    const int tx = tile % w.TX, ty = tile / w.TX;
+    const int px = tx * kTile + (threadIdx.x & 15), py = ty * kTile + (threadIdx.x >> 4);
+    if (px >= w.W || py >= w.H) return;
+    const size_t HW = (size_t)w.W * w.H;
+    const size_t q = (size_t)py * w.W + px;
+    const float d = dfill[(size_t)(py >> 1) * Wg + (px >> 1)];
+    bool ok = false;
+    float u = 0.0f, v = 0.0f;
+    if (d != kNoHit) {
+        const float rx = ((float)px - w.kcur[2]) / w.kcur[0];
+        const float ry = ((float)py - w.kcur[3]) / w.kcur[1];
+        const float Px = d * rx, Py = d * ry, Pz = d;
+        const float *M = w.Minv;
+        const float X = ((M[0] * Px + M[1] * Py) + M[2] * Pz) + M[3];
+        const float Y = ((M[4] * Px + M[5] * Py) + M[6] * Pz) + M[7];
+        const float Z = ((M[8] * Px + M[9] * Py) + M[10] * Pz) + M[11];
+        if (Z > w.z_near) {
+            u = fminf(fmaxf(w.kref[0] * (X / Z) + w.kref[2], 0.0f), (float)(w.W - 1));
+            v = fminf(fmaxf(w.kref[1] * (Y / Z) + w.kref[3], 0.0f), (float)(w.H - 1));
+            ok = true;
+        }
+    }
+    if (!ok) {   // cannot occur outside selected tiles
+        rgb[q] = rgb[HW + q] = rgb[2 * HW + q] = 0.0f;
+        return;
+    }
+    const int x0 = (int)floorf(u), y0 = (int)floorf(v);
+    const int x1 = min(x0 + 1, w.W - 1), y1 = min(y0 + 1, w.H - 1);
+    const float ax = u - (float)x0, ay = v - (float)y0;
+    const size_t i00 = (size_t)y0 * w.W + x0, i10 = (size_t)y0 * w.W + x1;
+    const size_t i01 = (size_t)y1 * w.W + x0, i11 = (size_t)y1 * w.W + x1;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        const float *I = tab + ch * HW;
+        const float top = (1.0f - ax) * I[i00] + ax * I[i10];
+        const float bot = (1.0f - ax) * I[i01] + ax * I[i11];
+        rgb[ch * HW + q] = (1.0f - ay) * top + ay * bot;
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void fill_kernel(T *p, size_t n, T v) {
     for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n;
@@ -293,7 +347,12 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
 
 void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
                        hipStream_t st) {
-    fill_query_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, dmin, dfill, uv, um);
+    fill_query_kernel<<<w.TX * w.TY, w.tp * w.tp, 0, st>>>(w, dmin, dfill, uv, um);
+}
+
+void launch_stitch_depth(const WarpK &w, int Wg, const uint8_t *sel, const float *tab,
+                         const float *dfill, float *rgb, hipStream_t st) {
+    stitch_depth_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, Wg, sel, tab, dfill, rgb);
 }
 
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,

@@ -324,6 +324,7 @@ struct tgs_scene {
 struct tgs_state {
     tgs_scene *scene = nullptr;
     int W = 0, H = 0, TX = 0, TY = 0;
+    int Wg = 0, Hg = 0;               // grid of the geometry buffer (image / tgb_downscale)
     tgs_params p{};
     Workspace ws;
     DevBuf tgb_d, tgb_s, tab, g_flag, fbox, dmin, smax, dfill, uv, um, oc;
@@ -490,6 +491,8 @@ tgs_status check_params(const tgs_params *p) {
         return fail(TGS_ERR_INVALID_ARG, "z_near must be finite and > 0");
     if (p->empty_far != 0 && p->empty_far != 1)
         return fail(TGS_ERR_INVALID_ARG, "empty_far must be 0 or 1");
+    if (p->tgb_downscale != 1 && p->tgb_downscale != 2)
+        return fail(TGS_ERR_INVALID_ARG, "tgb_downscale must be 1 or 2");
     return TGS_OK;
 }
 
@@ -554,6 +557,7 @@ void tgs_params_default(tgs_params *p) {
     p->enable_sr = 1;
     p->force_all_dirty = 0;
     p->empty_far = 0;
+    p->tgb_downscale = 1;
 }
 
 tgs_status tgs_scene_upload(const tgs_scene_desc *d, void *stream, tgs_scene **out) {
@@ -755,18 +759,21 @@ tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
     s->TX = (width + 15) / 16;
     s->TY = (height + 15) / 16;
     s->p = p;
+    s->Wg = (width + p.tgb_downscale - 1) / p.tgb_downscale;
+    s->Hg = (height + p.tgb_downscale - 1) / p.tgb_downscale;
     const size_t px = (size_t)width * height, nt = (size_t)s->TX * s->TY;
+    const size_t pg = (size_t)s->Wg * s->Hg;
     const size_t nn = (size_t)(scene->n > 0 ? scene->n : 1);
     tgs_status st = TGS_OK;
-    if (st == TGS_OK) st = s->tgb_d.ensure(px * 4);
-    if (st == TGS_OK) st = s->tgb_s.ensure(px * 4);
+    if (st == TGS_OK) st = s->tgb_d.ensure(pg * 4);
+    if (st == TGS_OK) st = s->tgb_s.ensure(pg * 4);
     if (st == TGS_OK) st = s->tab.ensure(3 * px * 4);
     if (st == TGS_OK) st = s->g_flag.ensure(nn);
     if (st == TGS_OK) st = s->fbox.ensure((4 + 4 * kAfcPartials) * sizeof(int));
-    if (st == TGS_OK) st = s->dmin.ensure(px * 4);
-    if (st == TGS_OK) st = s->smax.ensure(px * 4);
-    if (st == TGS_OK) st = s->dfill.ensure(px * 4);
-    if (st == TGS_OK) st = s->uv.ensure(px * 8);
+    if (st == TGS_OK) st = s->dmin.ensure(pg * 4);
+    if (st == TGS_OK) st = s->smax.ensure(pg * 4);
+    if (st == TGS_OK) st = s->dfill.ensure(pg * 4);
+    if (st == TGS_OK) st = s->uv.ensure(pg * 8);
     if (st == TGS_OK) st = s->um.ensure(nt);
     if (st == TGS_OK) st = s->oc.ensure(nt);
     if (st == TGS_OK) st = s->ws.prepare(scene->n, width, height);
@@ -817,6 +824,8 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
     for (;;) {
         const uint32_t *vals = nullptr;
         if (kind == TGS_FRAME_TGS) {
+            // full-resolution view pair (occluded tiles, stitching) and the
+            // same on the geometry buffer's grid (warp, fill, correspondences)
             WarpK w{};
             relative_pose(s->ref_w2c, cam->world_to_cam, w.M, w.Minv);
             for (int k = 0; k < 4; ++k) w.kref[k] = s->ref_intr[k];
@@ -829,17 +838,32 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             w.H = H;
             w.TX = TX;
             w.TY = TY;
+            w.tp = kTile;
+            const bool half = p.tgb_downscale == 2;
+            WarpK wg = w;
+            if (half) {
+                // cell (i, j) = pixels {2i, 2i+1} x {2j, 2j+1}: f / 2, (c - 1/2) / 2
+                for (int k = 0; k < 2; ++k) {
+                    wg.kref[k] = w.kref[k] * 0.5f;
+                    wg.kcur[k] = w.kcur[k] * 0.5f;
+                    wg.kref[2 + k] = (w.kref[2 + k] - 0.5f) * 0.5f;
+                    wg.kcur[2 + k] = (w.kcur[2 + k] - 0.5f) * 0.5f;
+                }
+                wg.W = s->Wg;
+                wg.H = s->Hg;
+                wg.tp = kTile / 2;
+            }
             {
                 ProfScope ps(TGS_PROF_WARP, st);
-                launch_temporal_init(W * H, nt, s->dmin.as<float>(), s->smax.as<float>(),
+                launch_temporal_init(s->Wg * s->Hg, nt, s->dmin.as<float>(), s->smax.as<float>(),
                                      s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
-                launch_forward_warp(w, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
+                launch_forward_warp(wg, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
                                     s->smax.as<float>(), st);
                 TGS_LAUNCHED("warp");
             }
             {
                 ProfScope ps(TGS_PROF_FILL_QUERY, st);
-                launch_fill_query(w, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
+                launch_fill_query(wg, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
                                   s->um.as<uint8_t>(), st);
                 TGS_LAUNCHED("fill query");
             }
@@ -852,6 +876,8 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             cull.g_rendered = s->g_flag.as<uint8_t>();
             cull.lambda1 = p.lambda1;
             cull.lambda2 = p.lambda2;
+            cull.tgb_shift = half ? 1 : 0;
+            cull.tgb_w = s->Wg;
             TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
             {
                 ProfScope ps(TGS_PROF_OCCLUDED, st);
@@ -885,8 +911,12 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             }
             {
                 ProfScope ps(TGS_PROF_STITCH, st);
-                launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
-                              out->rgb, st);
+                if (half)
+                    launch_stitch_depth(w, s->Wg, ws.sel.as<uint8_t>(), s->tab.as<float>(),
+                                        s->dfill.as<float>(), out->rgb, st);
+                else
+                    launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
+                                  out->rgb, st);
                 TGS_LAUNCHED("stitch");
             }
         } else {
@@ -909,9 +939,14 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.depth = out->depth;
             a.sigma = out->sigma;
             a.alpha = out->alpha;
-            a.tgb_depth = s->tgb_d.as<float>();
-        a.empty_depth = p.empty_far ? kZFar : kNoHit;
-            a.tgb_sigma = s->tgb_s.as<float>();
+            a.empty_depth = p.empty_far ? kZFar : kNoHit;
+            if (p.tgb_downscale == 2) {
+                a.tgbh_depth = s->tgb_d.as<float>();   // pooled over 2x2 blocks
+                a.tgbh_sigma = s->tgb_s.as<float>();
+            } else {
+                a.tgb_depth = s->tgb_d.as<float>();
+                a.tgb_sigma = s->tgb_s.as<float>();
+            }
             a.g_flag = s->g_flag.as<uint8_t>();
             a.contrib = out->contrib;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
@@ -975,8 +1010,8 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
 tgs_status tgs_state_export(const tgs_state *s, void *host, size_t *nbytes) {
     g_err.clear();
     if (!s || !nbytes) return fail(TGS_ERR_INVALID_ARG, "state and nbytes must not be NULL");
-    const size_t px = (size_t)s->W * s->H, n = (size_t)s->scene->n;
-    const size_t need = sizeof(tgs_state_header) + (5 * px) * sizeof(float) + n;
+    const size_t px = (size_t)s->W * s->H, pg = (size_t)s->Wg * s->Hg, n = (size_t)s->scene->n;
+    const size_t need = sizeof(tgs_state_header) + (2 * pg + 3 * px) * sizeof(float) + n;
     if (!host) {
         *nbytes = need;
         return TGS_OK;
@@ -1001,13 +1036,15 @@ tgs_status tgs_state_export(const tgs_state *s, void *host, size_t *nbytes) {
     }
     memcpy(h.ref_world_to_cam, s->ref_w2c, sizeof(h.ref_world_to_cam));
     memcpy(h.ref_intrinsics, s->ref_intr, sizeof(h.ref_intrinsics));
+    h.tgb_width = s->Wg;
+    h.tgb_height = s->Hg;
     char *dst = static_cast<char *>(host);
     memcpy(dst, &h, sizeof(h));
     dst += sizeof(h);
-    TGS_HIP(hipMemcpy(dst, s->tgb_d.p, px * 4, hipMemcpyDeviceToHost));
-    dst += px * 4;
-    TGS_HIP(hipMemcpy(dst, s->tgb_s.p, px * 4, hipMemcpyDeviceToHost));
-    dst += px * 4;
+    TGS_HIP(hipMemcpy(dst, s->tgb_d.p, pg * 4, hipMemcpyDeviceToHost));
+    dst += pg * 4;
+    TGS_HIP(hipMemcpy(dst, s->tgb_s.p, pg * 4, hipMemcpyDeviceToHost));
+    dst += pg * 4;
     TGS_HIP(hipMemcpy(dst, s->tab.p, 3 * px * 4, hipMemcpyDeviceToHost));
     dst += 3 * px * 4;
     if (n) TGS_HIP(hipMemcpy(dst, s->g_flag.p, n, hipMemcpyDeviceToHost));
@@ -1018,20 +1055,21 @@ tgs_status tgs_state_export(const tgs_state *s, void *host, size_t *nbytes) {
 tgs_status tgs_state_import(tgs_state *s, const void *host, size_t nbytes) {
     g_err.clear();
     if (!s || !host) return fail(TGS_ERR_INVALID_ARG, "state and host must not be NULL");
-    const size_t px = (size_t)s->W * s->H, n = (size_t)s->scene->n;
-    const size_t need = sizeof(tgs_state_header) + (5 * px) * sizeof(float) + n;
+    const size_t px = (size_t)s->W * s->H, pg = (size_t)s->Wg * s->Hg, n = (size_t)s->scene->n;
+    const size_t need = sizeof(tgs_state_header) + (2 * pg + 3 * px) * sizeof(float) + n;
     if (nbytes != need) return fail(TGS_ERR_INVALID_ARG, "blob size does not match the state");
     tgs_state_header h;
     memcpy(&h, host, sizeof(h));
     if (h.magic != 0x54475331u) return fail(TGS_ERR_INVALID_ARG, "bad blob magic");
-    if (h.width != s->W || h.height != s->H || h.n != s->scene->n)
+    if (h.width != s->W || h.height != s->H || h.n != s->scene->n || h.tgb_width != s->Wg ||
+        h.tgb_height != s->Hg)
         return fail(TGS_ERR_STATE_MISMATCH, "blob sizes differ from the state's");
     TGS_HIP(hipDeviceSynchronize());
     const char *src = static_cast<const char *>(host) + sizeof(h);
-    TGS_HIP(hipMemcpy(s->tgb_d.p, src, px * 4, hipMemcpyHostToDevice));
-    src += px * 4;
-    TGS_HIP(hipMemcpy(s->tgb_s.p, src, px * 4, hipMemcpyHostToDevice));
-    src += px * 4;
+    TGS_HIP(hipMemcpy(s->tgb_d.p, src, pg * 4, hipMemcpyHostToDevice));
+    src += pg * 4;
+    TGS_HIP(hipMemcpy(s->tgb_s.p, src, pg * 4, hipMemcpyHostToDevice));
+    src += pg * 4;
     TGS_HIP(hipMemcpy(s->tab.p, src, 3 * px * 4, hipMemcpyHostToDevice));
     src += 3 * px * 4;
     if (n) TGS_HIP(hipMemcpy(s->g_flag.p, src, n, hipMemcpyHostToDevice));
@@ -1060,7 +1098,8 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
     const Workspace &ws = state ? state->ws : scene->ws;
     const int n = state ? state->scene->n : scene->n;
     const int W = state ? state->W : scene->last_W, H = state ? state->H : scene->last_H;
-    const size_t px = (size_t)W * H, nt = (size_t)((W + 15) / 16) * ((H + 15) / 16);
+    const size_t nt = (size_t)((W + 15) / 16) * ((H + 15) / 16);
+    const size_t pg = state ? (size_t)state->Wg * state->Hg : 0;   // geometry buffer grid
     const void *src = nullptr;
     size_t size = 0;
     if (!ws.has_frame) return fail(TGS_ERR_INVALID_ARG, "no frame has been rendered yet");
@@ -1075,10 +1114,10 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
         default:
             if (!state) return fail(TGS_ERR_INVALID_ARG, "this buffer exists only for a state");
             switch (what) {
-                case TGS_DUMP_WARP_DEPTH: src = state->dmin.p; size = px * 4; break;
-                case TGS_DUMP_WARP_SIGMA: src = state->smax.p; size = px * 4; break;
-                case TGS_DUMP_FILLED_DEPTH: src = state->dfill.p; size = px * 4; break;
-                case TGS_DUMP_CORRESPONDENCE: src = state->uv.p; size = px * 8; break;
+                case TGS_DUMP_WARP_DEPTH: src = state->dmin.p; size = pg * 4; break;
+                case TGS_DUMP_WARP_SIGMA: src = state->smax.p; size = pg * 4; break;
+                case TGS_DUMP_FILLED_DEPTH: src = state->dfill.p; size = pg * 4; break;
+                case TGS_DUMP_CORRESPONDENCE: src = state->uv.p; size = pg * 8; break;
                 case TGS_DUMP_UNMATCHED: src = state->um.p; size = nt; break;
                 case TGS_DUMP_OCCLUDED: src = state->oc.p; size = nt; break;
                 default: return fail(TGS_ERR_INVALID_ARG, "unknown dump id");

@@ -66,6 +66,8 @@ struct CullK {
     const uint8_t *g_rendered;
     float lambda1, lambda2;
     int footprint;            // tile rectangle: 0 = 3-sigma square, 1 = alpha footprint box
+    int tgb_shift;            // dmin/smax grid = image >> tgb_shift (0, or 1: 2x2 blocks)
+    int tgb_w;                // width of that grid
 };
 
 // Frame counters on the device (read back once per frame).
@@ -172,6 +174,8 @@ struct BlendArgs {
     float *tab;               // optional second copy of rgb
     float *depth, *sigma, *alpha;       // optional outputs
     float *tgb_depth, *tgb_sigma;       // optional second copies
+    float *tgbh_depth, *tgbh_sigma;     // optional: Eq. 1/2 pooled over 2x2 blocks
+                                        // (grid ceil(W/2) x ceil(H/2))
     uint8_t *g_flag;          // optional: Gaussian composited somewhere
     float *contrib;           // optional: max weight per Gaussian
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
@@ -193,7 +197,8 @@ struct WarpK {
     float Minv[12];           // current camera -> reference camera
     float kref[4], kcur[4];   // fx, fy, cx, cy
     float z_near;
-    int W, H, TX, TY;
+    int W, H, TX, TY;         // grid size (image, or the geometry buffer's) and tiles
+    int tp;                   // pixels per tile side on this grid (16, or 8 at half resolution)
 };
 void launch_temporal_init(int n_px, int n_tiles, float *dmin, float *smax, uint8_t *oc,
                           Counters *cnt, hipStream_t st);
@@ -209,6 +214,11 @@ void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *u
                    Counters *cnt, hipStream_t st);
 void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,
                    float *rgb, hipStream_t st);
+// Stitching from a half-resolution repaired depth (grid width Wg): each pixel
+// of a non-selected tile is unprojected with its 2x2 block's depth (w: the
+// full-resolution view pair).
+void launch_stitch_depth(const WarpK &w, int Wg, const uint8_t *sel, const float *tab,
+                         const float *dfill, float *rgb, hipStream_t st);
 void launch_fill_u8(uint8_t *p, size_t n, uint8_t v, hipStream_t st);
 void launch_fill_f32(float *p, size_t n, float v, hipStream_t st);
 void launch_fill_i32(int *p, size_t n, int v, hipStream_t st);

@@ -56,7 +56,8 @@ class tgs_params(C.Structure):
     _fields_ = [("lambda_tdc", C.c_int32), ("lambda_sr", C.c_int32), ("eta", C.c_float),
                 ("lambda1", C.c_float), ("lambda2", C.c_float), ("z_near", C.c_float),
                 ("enable_afc", C.c_int32), ("enable_toc", C.c_int32), ("enable_sr", C.c_int32),
-                ("force_all_dirty", C.c_int32), ("empty_far", C.c_int32)]
+                ("force_all_dirty", C.c_int32), ("empty_far", C.c_int32),
+                ("tgb_downscale", C.c_int32)]
 
 
 class tgs_frame_out(C.Structure):
@@ -76,7 +77,8 @@ class tgs_state_header(C.Structure):
                 ("n", C.c_int32), ("frame_index", C.c_int32), ("since_true_ref", C.c_int32),
                 ("since_ref", C.c_int32), ("force_pseudo", C.c_int32),
                 ("has_reference", C.c_int32), ("fbox", C.c_float * 4),
-                ("ref_world_to_cam", C.c_float * 16), ("ref_intrinsics", C.c_float * 4)]
+                ("ref_world_to_cam", C.c_float * 16), ("ref_intrinsics", C.c_float * 4),
+                ("tgb_width", C.c_int32), ("tgb_height", C.c_int32)]
 
 
 _LIB = None
@@ -237,8 +239,9 @@ def parse_state(blob: bytes):
     W, H, n = hdr.width, hdr.height, hdr.n
     off = C.sizeof(tgs_state_header)
     px = W * H
-    D = np.frombuffer(blob, np.float32, px, off).reshape(H, W); off += 4 * px
-    S = np.frombuffer(blob, np.float32, px, off).reshape(H, W); off += 4 * px
+    Wg, Hg = hdr.tgb_width, hdr.tgb_height
+    D = np.frombuffer(blob, np.float32, Wg * Hg, off).reshape(Hg, Wg); off += 4 * Wg * Hg
+    S = np.frombuffer(blob, np.float32, Wg * Hg, off).reshape(Hg, Wg); off += 4 * Wg * Hg
     tab = np.frombuffer(blob, np.float32, 3 * px, off).reshape(3, H, W); off += 12 * px
     g = np.frombuffer(blob, np.uint8, n, off)
     return dict(width=W, height=H, n=n, frame_index=hdr.frame_index,

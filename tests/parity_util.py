@@ -116,3 +116,24 @@ def import_into_oracle(ora, blob):
 def tile_pixels(mask_tiles, W, H):
     m = np.repeat(np.repeat(mask_tiles.astype(bool), 16, 0), 16, 1)
     return m[:H, :W]
+
+
+def check_pooled_tgb(st, ora, margin_px):
+    """Geometry buffer downscaled by 2: the GPU's Eq. 1/2 pooled over each
+    2x2 block (exported state) against the oracle's, blocks that hold a
+    margin pixel excluded; empty blocks carry the same empty depth."""
+    Dg, Sg = st["D"].astype(np.float64), st["S"].astype(np.float64)
+    Do, So = ora.D.astype(np.float64), ora.S.astype(np.float64)
+    assert Dg.shape == Do.shape, (Dg.shape, Do.shape)
+    H, W = margin_px.shape
+    m = np.zeros((2 * Do.shape[0], 2 * Do.shape[1]), bool)
+    m[:H, :W] = margin_px
+    ok = ~m.reshape(Do.shape[0], 2, Do.shape[1], 2).any(axis=(1, 3))
+    empty = ok & ((Do == float(O.NOHIT)) | (Do == float(O.Z_FAR)))
+    assert np.array_equal(Dg[empty], Do[empty]) and np.all(Sg[empty] == 0.0), "empty blocks differ"
+    hit = ok & ~empty
+    if hit.any():
+        rel = (np.abs(Dg[hit] - Do[hit]) / Do[hit]).max()
+        assert rel <= DEPTH_RTOL, f"pooled depth rel err {rel}"
+        serr = (np.abs(Sg[hit] - So[hit]) / np.maximum(1.0, Do[hit])).max()
+        assert serr <= SIGMA_TOL, f"pooled sigma err {serr}"

@@ -16,6 +16,7 @@ import pytest
 from oracle import oracle as O
 from paper_2607_03390_amd import synth, tgs
 from tests.parity_util import (RGB_TOL, STITCH_TOL, check_gaussian_buffer, check_image, check_lists,
+                               check_pooled_tgb,
                                check_moments, check_records, dumps, gpu_full, import_into_oracle,
                                log, tile_pixels)
 
@@ -170,10 +171,11 @@ def _temporal_parity(scene, cams, W, H, label, bound=tgs.TGS_TILES_3SIGMA, **pkw
                 if ref["kind"] == O.TGS_FRAME:
                     stats["tgs"] += 1
                     TX, TY = cam.tiles
-                    dm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_DEPTH).reshape(H, W)
-                    sm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_SIGMA).reshape(H, W)
-                    df = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_FILLED_DEPTH).reshape(H, W)
-                    uv = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_CORRESPONDENCE).reshape(H, W, 2)
+                    Hg, Wg = ref["dmin"].shape   # the geometry buffer's grid
+                    dm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_DEPTH).reshape(Hg, Wg)
+                    sm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_SIGMA).reshape(Hg, Wg)
+                    df = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_FILLED_DEPTH).reshape(Hg, Wg)
+                    uv = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_CORRESPONDENCE).reshape(Hg, Wg, 2)
                     um = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_UNMATCHED).reshape(TY, TX)
                     oc = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_OCCLUDED).reshape(TY, TX)
                     assert np.array_equal(dm.view(np.uint32), ref["dmin"].view(np.uint32)), "warped depth"
@@ -208,6 +210,8 @@ def _temporal_parity(scene, cams, W, H, label, bound=tgs.TGS_TILES_3SIGMA, **pkw
                     check_image(res["rgb"], ref["rgb"], ok, RGB_TOL, f"frame {k} reference")
                     check_moments(res, ref, ok)
                     check_gaussian_buffer(res["contrib"][:n] > 0, ref)
+                    if pkw.get("tgb_downscale", 1) == 2:
+                        check_pooled_tgb(tgs.parse_state(tgs.tgs_state_export(s)), ora, ~ok)
                     stats["margin_px"] += int((~ok).sum())
                 log(f"    kind {info['frame_kind']} sel {info['n_selected']} keys {info['n_keys']} "
                     f"surv {info['n_survivors']} newly {info['n_newly_visible']}")
@@ -231,12 +235,27 @@ def test_temporal_parity_tiny_empty_far():
 
 @pytest.mark.parametrize("pkw", [dict(), dict(lambda_sr=2), dict(enable_toc=0),
                                  dict(enable_afc=0, eta=1.0), dict(enable_sr=0),
-                                 dict(empty_far=1)])
+                                 dict(empty_far=1), dict(tgb_downscale=2),
+                                 dict(tgb_downscale=2, empty_far=1)])
 def test_temporal_parity_room_subset(pkw):
     sc = synth.scene_room(60_000, 2)
     cams = synth.handheld_path(12, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 400, 232)
     st = _temporal_parity(sc, cams, 400, 232, f"room60k {pkw}", **pkw)
     assert st["tgs"] >= 3
+
+
+def test_temporal_parity_tgb_half_ragged():
+    # odd width and height: partial 2x2 blocks on the last column and row
+    sc = synth.scene_room(60_000, 2)
+    cams = synth.handheld_path(10, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 401, 233)
+    st = _temporal_parity(sc, cams, 401, 233, "room60k ragged tgb/2", tgb_downscale=2)
+    assert st["tgs"] >= 3
+
+
+def test_temporal_parity_tiny_tgb_half():
+    w = synth.workload("tiny")
+    st = _temporal_parity(w.scene, w.cameras, 256, 256, "tiny tgb/2", tgb_downscale=2, empty_far=1)
+    assert st["tgs"] >= 4
 
 
 def test_temporal_parity_room_subset_footprint_tiles():
