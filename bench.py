@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--tgb-downscale", type=int, default=None,
                     help="geometry-buffer downscale (1 or 2); default: 2 for the large-scale "
                          "city workload (the paper's large-scene setting), 1 otherwise")
+    ap.add_argument("--sort-path", default="auto", choices=["auto", "depth_first", "per_tile"],
+                    help="how per-tile depth order is produced (tgs_set_sort_path)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
     return ap.parse_args()
@@ -90,6 +92,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    SORT_MODES = {"auto": tgs.SORT_AUTO, "depth_first": tgs.SORT_DEPTH_FIRST,
+                  "per_tile": tgs.SORT_PER_TILE}
+    tgs.tgs_set_sort_path(SORT_MODES[args.sort_path])
     log(f"[bench] generating workload {args.workload}")
     wl = synth.workload(args.workload, n_frames=args.frames)
     cams = wl.cameras
@@ -228,10 +233,13 @@ def main():
         ssim = dict(mean=round(float(np.mean(svals)), 6), min=round(float(np.min(svals)), 6),
                     frames=len(svals))
 
-    def variant(label, cams_v, tile_bound=tgs.TGS_TILES_3SIGMA, steps=None, full=False, **pkw):
+    def variant(label, cams_v, tile_bound=tgs.TGS_TILES_3SIGMA, steps=None, full=False,
+                sort_path=None, **pkw):
         """Temporal FPS, frame mix and PSNR vs the full render of one setting."""
         steps = steps or args.steps
         tgs.tgs_scene_set_tile_bound(scene_h, tile_bound)
+        if sort_path is not None:
+            tgs.tgs_set_sort_path(SORT_MODES[sort_path])
         pkw = {"tgb_downscale": args.tgb_downscale, **pkw}
         sv = tgs.tgs_state_create(scene_h, W, H, tgs.params(**pkw))
 
@@ -286,6 +294,9 @@ def main():
             r["ssim_mean"] = round(float(np.mean(svals)), 5)
         tgs.tgs_state_free(sv)
         tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_3SIGMA)
+        tgs.tgs_set_sort_path(SORT_MODES[args.sort_path])
+        if sort_path is not None:
+            r["sort_path"] = sort_path
         log(f"[bench] variant {label}: {r}")
         return r
 
@@ -296,6 +307,9 @@ def main():
         variants["footprint_tile_rule"] = variant("footprint tile rule", cams,
                                                   tile_bound=tgs.TGS_TILES_FOOTPRINT, full=True)
         variants["empty_far"] = variant("empty pixels at z_far", cams, empty_far=1)
+        for sp in ("depth_first", "per_tile"):
+            if sp != args.sort_path:
+                variants[f"sort_{sp}"] = variant(f"{sp} sort", cams, full=True, sort_path=sp)
         other = 2 if args.tgb_downscale == 1 else 1
         variants[f"tgb_downscale_{other}"] = variant(f"geometry buffer downscale x{other}", cams,
                                                      tgb_downscale=other)
@@ -381,6 +395,7 @@ def main():
         "full": {"fps": round(fps_f, 2), "ms_per_frame": round(1e3 * t_full / (args.steps * n_frames), 4)},
         "speedup_temporal_vs_full": round(fps_t / fps_f, 3),
         "tile_rule": "3DGS 3-sigma square",
+        "sort_path": args.sort_path,
         **variants,
         "psnr_temporal_vs_full": psnr,
         "ssim_temporal_vs_full": ssim,

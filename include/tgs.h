@@ -280,6 +280,23 @@ typedef struct {
 tgs_status tgs_profile_start(int32_t flags);
 tgs_status tgs_profile_stop(tgs_profile *out);
 
+/* How each tile's front-to-back order (Sec. III-A: sort by depth within a
+ * tile) is produced, process-wide.  Both ways give identical per-tile lists
+ * (depth bits, then Gaussian index):
+ *   TGS_SORT_DEPTH_FIRST: the Gaussians with keys are radix-sorted by depth
+ *     (four 8-bit passes over them), keys are emitted in that order and
+ *     stably radix-sorted by tile;
+ *   TGS_SORT_PER_TILE: key counts are scanned in index order, keys emitted
+ *     in index order and stably sorted by tile, then one block per tile
+ *     sorts its list by (depth bits, index) in LDS (lists above 4096 entries
+ *     take a slower in-block path);
+ *   TGS_SORT_AUTO (default): per frame, the per-tile sort for TemporalGS
+ *     frames (keys on the selected tiles only) when the longest tile list of
+ *     a recent frame has fewer than 4096 entries, else the depth-first sort.
+ * INVALID_ARG for another value.  Not thread-safe against running renders. */
+enum { TGS_SORT_AUTO = 0, TGS_SORT_DEPTH_FIRST = 1, TGS_SORT_PER_TILE = 2 };
+tgs_status tgs_set_sort_path(int32_t mode);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *tgs_last_error(void);
 

@@ -178,7 +178,8 @@ __device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool act
 
 __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uint32_t *n_dev,
                                                            const int *tile_in,
-                                                           const uint2 *ranges, int *tile_out) {
+                                                           const uint2 *ranges, int *tile_out,
+                                                           uint32_t *max_bucket) {
     constexpr int kPer = 8;   // tiles per thread and round: all loads of a round in flight
     __shared__ uint32_t s_cnt[33];
     const int tid = threadIdx.x;
@@ -209,11 +210,16 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
         __syncthreads();
         if (pass == 0 && tid == 0) {
             // bucket starts, longest lists first
-            uint32_t run = 0;
+            uint32_t run = 0, top = 0;
             for (int bk = 32; bk >= 0; --bk) {
                 const uint32_t c = s_cnt[bk];
+                if (c && !top) top = (uint32_t)bk;
                 s_cnt[bk] = run;
                 run += c;
+            }
+            if (max_bucket) {
+                *reinterpret_cast<volatile uint32_t *>(max_bucket) = top;
+                __threadfence_system();
             }
         }
         __syncthreads();
@@ -243,8 +249,9 @@ void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint
 }
 
 void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
-                        int *tile_out, hipStream_t st) {
-    if (n > 0) order_tiles_kernel<<<1, 1024, 0, st>>>(n, n_dev, tile_in, ranges, tile_out);
+                        int *tile_out, uint32_t *max_bucket, hipStream_t st) {
+    if (n > 0)
+        order_tiles_kernel<<<1, 1024, 0, st>>>(n, n_dev, tile_in, ranges, tile_out, max_bucket);
 }
 
 }  // namespace tgs

@@ -82,6 +82,9 @@ struct Workspace {
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
     HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
     HostCounters *host_cnt_dev = nullptr; // its device-side address
+    uint32_t *host_maxb = nullptr;        // pinned: longest tile list's log2 bucket (some recent frame)
+    uint32_t *host_maxb_dev = nullptr;
+    bool frame_seg = false;               // this frame orders tiles by the per-tile sort
     uint32_t seq = 0;                     // tag of the last frame's counters
     int n = -1, W = 0, H = 0;
     size_t key_cap = 0;
@@ -92,6 +95,7 @@ struct Workspace {
 
     ~Workspace() {
         if (host_cnt) (void)hipHostFree(host_cnt);
+        if (host_maxb) (void)hipHostFree(host_maxb);
     }
 
     tgs_status prepare(int n_, int W_, int H_) {
@@ -102,6 +106,12 @@ struct Workspace {
                                   hipHostMallocCoherent | hipHostMallocMapped));
             memset(host_cnt, 0, sizeof(HostCounters));
             TGS_HIP(hipHostGetDevicePointer((void **)&host_cnt_dev, host_cnt, 0));
+        }
+        if (!host_maxb) {
+            TGS_HIP(hipHostMalloc((void **)&host_maxb, sizeof(uint32_t),
+                                  hipHostMallocCoherent | hipHostMallocMapped));
+            *host_maxb = 0xffffffffu;   // unknown: the first frame takes the depth-sorted path
+            TGS_HIP(hipHostGetDevicePointer((void **)&host_maxb_dev, host_maxb, 0));
         }
         if (n_ != n) {
             TGS_TRY(g.ensure(nn * 4 * sizeof(float4)));
@@ -355,11 +365,38 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
     return TGS_OK;
 }
 
-// Depth-order the Gaussians that have keys and scan their key counts in that
-// order.  The last depth-sort pass publishes the frame's counters to the
-// host (tag ws.seq); nothing here waits.
+// Sort path: 0 = per frame (the per-tile sort in selective-rendering frames
+// when the longest tile list of a recent frame fits its LDS bound, else the
+// global depth sort), 1 = always the global depth sort, 2 = always the
+// per-tile sort.
+int g_sort_path = 0;
+
+// The Gaussians that have keys and the start of their keys, in the order the
+// keys are emitted: depth order (global depth sort; the last pass publishes
+// the frame's counters to the host, tag ws.seq) or index order (count scan,
+// each tile's list sorted by depth after the tile sort).  Nothing here waits.
 tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
                      const uint32_t **sorted_didx) {
+    // per frame: the per-tile sort pays off in selective-rendering frames
+    // (keys only on the selected tiles) whose lists fit its LDS bound; a
+    // frame rendering every tile sorts 3-4 times as many keys per tile as
+    // the depth sort sorts Gaussians, and takes the global depth sort
+    const uint32_t maxb = *reinterpret_cast<volatile uint32_t *>(ws.host_maxb);
+    ws.frame_seg = g_sort_path == 2 ||
+                   (g_sort_path == 0 && rowpre != nullptr && maxb <= (uint32_t)kSegBucketMax);
+    if (ws.frame_seg) {
+        ProfScope ps(TGS_PROF_SORT, st);
+        ws.seq += 1;
+        const int nb = count_scan_blocks(n > 0 ? n : 0);
+        uint32_t *part = ws.sort.as<uint32_t>();
+        launch_count_scan(n, ws.count.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX, part,
+                          part + 2 * (size_t)nb, ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
+                          ws.cnt.as<Counters>(), (uint32_t)ws.key_cap, ws.partial.as<uint32_t>(),
+                          n > 0 ? preprocess_blocks(n) : 0, ws.host_cnt_dev, ws.seq, st);
+        TGS_LAUNCHED("count scan");
+        *sorted_didx = ws.didx.as<uint32_t>();
+        return TGS_OK;
+    }
     {
         ProfScope ps(TGS_PROF_SORT, st);
         ws.seq += 1;
@@ -443,14 +480,26 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
         TGS_LAUNCHED("tile sort");
     }
     const uint32_t *skeys = alt ? ws.tkey_alt.as<uint32_t>() : ws.tkey.as<uint32_t>();
+    uint32_t *svals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
     {
         ProfScope ps(TGS_PROF_RANGES, st);
         launch_ranges(cap, cnt, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
+    }
+    if (ws.frame_seg) {
+        // each tile's list, emitted in index order, by (depth bits, index)
+        ProfScope ps(TGS_PROF_SORT, st);
+        launch_segment_sort(TX * TY, ws.ranges.as<uint2>(), svals,
+                            alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
+                            ws.dkey.as<uint32_t>(), st);
+        TGS_LAUNCHED("per-tile sort");
+    }
+    {
+        ProfScope ps(TGS_PROF_RANGES, st);
         // blend order: the selected tiles, or all of them, longest lists first
         launch_order_tiles(TX * TY, rowpre ? &cnt->n_selected : nullptr,
                            rowpre ? ws.sel_list.as<int>() : nullptr, ws.ranges.as<uint2>(),
-                           ws.tile_order.as<int>(), st);
+                           ws.tile_order.as<int>(), ws.host_maxb_dev, st);
         TGS_LAUNCHED("tile order");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
@@ -505,6 +554,13 @@ tgs_status check_params(const tgs_params *p) {
 extern "C" {
 
 const char *tgs_last_error(void) { return g_err.c_str(); }
+
+tgs_status tgs_set_sort_path(int32_t mode) {
+    g_err.clear();
+    if (mode < 0 || mode > 2) return fail(TGS_ERR_INVALID_ARG, "sort path must be 0, 1 or 2");
+    g_sort_path = mode;
+    return TGS_OK;
+}
 
 tgs_status tgs_profile_start(int32_t flags) {
     g_err.clear();

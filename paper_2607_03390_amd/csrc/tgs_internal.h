@@ -135,8 +135,10 @@ void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint
 // Tiles to rasterise (tile_in[0..m), or 0..m-1 when tile_in is NULL; m =
 // *n_dev when n_dev is given, else n) in blend order, longest lists first,
 // into tile_out[0..m).
+// max_bucket (optional, host-visible memory) receives floor(log2 of the
+// longest list length) + 1 (0: all lists empty).
 void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
-                        int *tile_out, hipStream_t st);
+                        int *tile_out, uint32_t *max_bucket, hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
@@ -161,6 +163,25 @@ void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32
                        uint32_t *v_b, uint32_t *offs, uint32_t *scratch, Counters *cnt,
                        uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
                        uint32_t tag, hipStream_t st);
+
+// ---- launchers (k_segsort.hip) ----
+// Per-tile depth order without the global depth sort: key counts scanned in
+// index order (part / bases: 2 words per 1024-Gaussian block each), the
+// Gaussians with keys compacted in index order into vidx / voffs (the
+// duplication's input), the frame's counters published as the depth sort
+// does; after the tile sort, each tile's list sorted by (depth bits, index)
+// in place (tmp: scratch of the same size as vals).
+int count_scan_blocks(int n);
+void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
+                       uint32_t *part, uint32_t *bases, uint32_t *vidx, uint32_t *voffs,
+                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
+                       HostCounters *host, uint32_t tag, hipStream_t st);
+void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
+                         const uint32_t *dkey, hipStream_t st);
+// Longest list the per-tile sort handles in LDS; longer ones take its slower
+// in-block path.  Lists of bucket <= kSegBucketMax (floor(log2 len) + 1)
+// fit.
+constexpr int kSegBucketMax = 12;
 
 // ---- launchers (k_blend.hip) ----
 struct BlendArgs {

@@ -28,7 +28,10 @@ EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_sce
             "tgs_scene_set_tile_bound",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
-            "tgs_profile_start", "tgs_profile_stop", "tgs_last_error"]
+            "tgs_profile_start", "tgs_profile_stop", "tgs_set_sort_path", "tgs_last_error"]
+
+# tgs_set_sort_path modes
+SORT_AUTO, SORT_DEPTH_FIRST, SORT_PER_TILE = 0, 1, 2
 
 PROF_STAGES = ["preprocess", "scan", "readback", "duplicate", "sort", "ranges", "blend_full",
                "blend_ref", "blend_tgs", "warp", "fill_query", "occluded", "select", "stitch",
@@ -271,6 +274,13 @@ def tgs_debug_dump(scene_h, state_h, what) -> np.ndarray:
 
 
 TGS_PROFILE_COUNT_PAIRS, TGS_PROFILE_STAGES = 1, 2
+
+
+def tgs_set_sort_path(mode):
+    """How per-tile depth order is produced (process-wide): SORT_AUTO,
+    SORT_DEPTH_FIRST (global depth sort, keys emitted in depth order) or
+    SORT_PER_TILE (keys in index order, each tile's list sorted)."""
+    _check(lib().tgs_set_sort_path(int(mode)))
 
 
 def tgs_profile_start(count_pairs=False, stages=False):

@@ -31,6 +31,17 @@ def _device():
     tgs.lib()
 
 
+# Every parity case runs with both ways of producing per-tile depth order
+# (global depth sort first; per-tile sort after the tile sort): the lists
+# must be the oracle's either way.
+@pytest.fixture(autouse=True, params=[tgs.SORT_DEPTH_FIRST, tgs.SORT_PER_TILE],
+                ids=["depth_first", "per_tile"])
+def sort_path(request):
+    tgs.tgs_set_sort_path(request.param)
+    yield request.param
+    tgs.tgs_set_sort_path(tgs.SORT_AUTO)
+
+
 class Uploaded:
     def __init__(self, scene, bound=tgs.TGS_TILES_3SIGMA):
         self.scene = scene
@@ -99,6 +110,19 @@ def test_full_parity_footprint_tiles(n, seed, deg, W, H):
     cams = [synth.make_camera(synth.look_at(e, (0, 0, 0)), W, H)
             for e in ((0.2, -3.0, 0.7), (2.5, 1.0, -0.4))]
     _full_parity(sc, cams, label=f"footprint {W}x{H}", bound=tgs.TGS_TILES_FOOTPRINT)
+
+
+def test_long_tile_lists(sort_path):
+    """Tile lists above the per-tile sort's LDS bound (4096 entries): its
+    in-block radix path, against the oracle's lists."""
+    sc = synth.scene_uniform_cube(24_000, 11, degree=0, log_scale_mean=-2.6)
+    cam = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (0, 0, 0)), 48, 40)
+    g = O.gaussians(sc, cam)
+    ts, _ = O.tile_lists(g, *cam.tiles)
+    longest = int(np.diff(ts).max())
+    log(f"    longest tile list {longest}")
+    assert longest > 4096
+    _full_parity(sc, [cam], label="long lists")
 
 
 def test_full_parity_object_subset():
