@@ -262,12 +262,13 @@ enum {
     TGS_PROF_RANGES = 5,
     TGS_PROF_BLEND_FULL = 6,  /* tgs_render_full                              */
     TGS_PROF_BLEND_REF = 7,   /* reference frames (with prior capture)        */
-    TGS_PROF_BLEND_TGS = 8,   /* selected tiles of TemporalGS frames          */
+    TGS_PROF_BLEND_TGS = 8,   /* TemporalGS frames: selected tiles blended,   */
+                              /*    the others stitched, in one launch        */
     TGS_PROF_WARP = 9,        /* buffer init + forward warp                   */
     TGS_PROF_FILL_QUERY = 10,
     TGS_PROF_OCCLUDED = 11,
     TGS_PROF_SELECT = 12,
-    TGS_PROF_STITCH = 13,
+    TGS_PROF_STITCH = 13,     /* unused: stitching runs in the TGS blend      */
     TGS_PROF_CAPTURE = 14,    /* adaptive frustum, flag/mask resets           */
     TGS_PROF_STAGES = 16
 };

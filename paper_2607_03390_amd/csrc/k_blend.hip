@@ -18,8 +18,12 @@
 // cancellation of the unshifted form at large depths.  Gaussians that a wave
 // composites are flagged through a wave ballot, so the temporal Gaussian
 // buffer costs one scalar test per record and wave.
+//
+// In a TemporalGS frame the blocks past the selected tiles stitch the other
+// tiles from the reference image (stitch.h) while the long tiles finish.
 #include <hip/hip_ext.h>
 
+#include "stitch.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -52,7 +56,16 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     __shared__ uint32_t s_cnt[4][16];      // [staging wave][list] entries, then starts
     __shared__ uint32_t s_len[16];         // list lengths
 
-    if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) return;   // block-uniform
+    if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) {   // block-uniform
+        if (a.stitch_list) {
+            const int t = a.stitch_list[blockIdx.x];
+            if (a.stitch_mode == 2)
+                stitch_tile_depth(a.sw, a.stitch_wg, t, a.stitch_tab, a.stitch_dfill, a.rgb);
+            else
+                stitch_tile_uv(a.sw, t, a.stitch_tab, a.stitch_uv, a.rgb);
+        }
+        return;
+    }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;

@@ -23,14 +23,38 @@ __device__ inline uint32_t key_tile(uint32_t r, ushort4 rc, const uint32_t *rowp
         ty = rc.y + (int)(r / w);
         tx = rc.x + (int)(r % w);
     } else {
+        // four rows per step (eight independent loads), then the row
+        // holding the r-th selected tile among them
         ty = rc.y;
-        const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
-        for (;; ++ty, row += TX + 1) {
-            const uint32_t c = row[rc.z + 1] - row[rc.x];
-            if (r < c) break;
-            r -= c;
+        const size_t s = (size_t)(TX + 1);
+        const uint32_t *row = rowpre + (size_t)ty * s;
+        for (;;) {
+            if (ty > (int)rc.w) {   // r past the Gaussian's count: cannot happen
+                tx = rc.x;
+                ty = rc.w;
+                break;
+            }
+            uint32_t c[4], b[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bool in = ty + k <= (int)rc.w;
+                b[k] = in ? row[k * s + rc.x] : 0u;
+                c[k] = in ? row[k * s + rc.z + 1] - b[k] : 0u;
+            }
+            int k = 0;
+            while (k < 3 && r >= c[k]) {
+                r -= c[k];
+                ++k;
+            }
+            if (r < c[k]) {
+                ty += k;
+                tx = sel_cols[(size_t)ty * TX + b[k] + r];
+                break;
+            }
+            r -= c[k];
+            ty += 4;
+            row += 4 * s;
         }
-        tx = sel_cols[(size_t)ty * TX + row[rc.x] + r];
     }
     return (uint32_t)(ty * TX + tx);
 }
@@ -208,19 +232,22 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
             }
         }
         __syncthreads();
-        if (pass == 0 && tid == 0) {
-            // bucket starts, longest lists first
-            uint32_t run = 0, top = 0;
-            for (int bk = 32; bk >= 0; --bk) {
-                const uint32_t c = s_cnt[bk];
-                if (c && !top) top = (uint32_t)bk;
-                s_cnt[bk] = run;
-                run += c;
+        if (pass == 0 && tid < 64) {
+            // bucket starts, longest lists first: lane l holds bucket 32 - l
+            const int bk = 32 - tid;
+            const uint32_t c = bk >= 0 ? s_cnt[bk] : 0u;
+            uint32_t inc = c;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const uint32_t o = __shfl_up(inc, d);
+                if (tid >= d) inc += o;
             }
-            if (max_bucket) {
-                *reinterpret_cast<volatile uint32_t *>(max_bucket) = top;
-                __threadfence_system();
-            }
+            if (bk >= 0) s_cnt[bk] = inc - c;
+            const uint64_t nz = __ballot(c != 0u);
+            // the host reads this value some frames later: no fence needed
+            if (max_bucket && tid == 0)
+                *reinterpret_cast<volatile uint32_t *>(max_bucket) =
+                    nz ? (uint32_t)(32 - (__ffsll((long long)nz) - 1)) : 0u;
         }
         __syncthreads();
     }

@@ -2,9 +2,10 @@
 // alternative to sorting every visible Gaussian by depth before emitting
 // its keys, for frames whose tile lists are short.
 //
-//  1. Key counts are scanned in Gaussian index order (three kernels: block
-//     partials, one-block scan that also publishes the frame's counters,
-//     emission of the compacted (index, key offset) pairs).
+//  1. Key counts are scanned in Gaussian index order (two kernels: block
+//     partials, then the emission of the compacted (index, key offset)
+//     pairs, each block summing the partials before it; block 0 publishes
+//     the frame's counters).
 //  2. Keys are emitted in index order and stably sorted by tile (the same
 //     duplication and tile-sort kernels as the depth-ordered path), so each
 //     tile's list comes out in index order.
@@ -71,17 +72,23 @@ __global__ __launch_bounds__(kScanThreads) void count_partials_kernel(int n, uin
     __shared__ uint32_t s_w[4];
     const int base = blockIdx.x * kScanBlock + threadIdx.x * kScanPer;
     uint32_t keys = 0, nz = 0;
+    if (rowpre) {
+        // the four rectangles are loaded before the first count
+        ushort4 r[kScanPer];
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
-        const int i = base + k;
-        if (i < n) {
-            uint32_t c;
-            if (rowpre) {
-                c = masked_count(rect[i], rowpre, TX);
-                count[i] = c;
-            } else {
-                c = count[i];
-            }
+        for (int k = 0; k < kScanPer; ++k)
+            r[k] = base + k < n ? rect[base + k] : make_ushort4(1, 0, 0, 0);
+#pragma unroll
+        for (int k = 0; k < kScanPer; ++k) {
+            const uint32_t c = masked_count(r[k], rowpre, TX);
+            if (base + k < n) count[base + k] = c;
+            keys += c;
+            nz += c ? 1u : 0u;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kScanPer; ++k) {
+            const uint32_t c = base + k < n ? count[base + k] : 0u;
             keys += c;
             nz += c ? 1u : 0u;
         }
@@ -95,129 +102,114 @@ __global__ __launch_bounds__(kScanThreads) void count_partials_kernel(int n, uin
     }
 }
 
-// One block: exclusive scan of the block partials into bases (keys, kept),
-// the frame's totals to the device counters and, tag last, to the host.
-__global__ __launch_bounds__(1024) void count_scan_kernel(int nb, const uint32_t *part, uint32_t *bases,
-                                                          const uint32_t *pre_partial, int n_pre,
-                                                          Counters *cnt, HostCounters *host,
-                                                          uint32_t tag, uint32_t cap) {
-    __shared__ unsigned long long s_k[16];
-    __shared__ uint32_t s_n[16];
-    __shared__ unsigned long long s_carry_k;
-    __shared__ uint32_t s_carry_n;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) {
-        s_carry_k = 0ull;
-        s_carry_n = 0u;
-    }
-    __syncthreads();
-    for (int b0 = 0; b0 < nb; b0 += 1024) {
-        const int b = b0 + tid;
-        unsigned long long k = b < nb ? part[2 * b] : 0ull;
-        uint32_t m = b < nb ? part[2 * b + 1] : 0u;
-        unsigned long long ik = k;
-        uint32_t im = m;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const unsigned long long ok = __shfl_up(ik, d);
-            const uint32_t om = __shfl_up(im, d);
-            if (lane >= d) {
-                ik += ok;
-                im += om;
-            }
-        }
-        if (lane == 63) {
-            s_k[wave] = ik;
-            s_n[wave] = im;
-        }
-        __syncthreads();
-        unsigned long long offk = s_carry_k, totk = 0;
-        uint32_t offn = s_carry_n, totn = 0;
-        for (int w = 0; w < 16; ++w) {
-            if (w < wave) {
-                offk += s_k[w];
-                offn += s_n[w];
-            }
-            totk += s_k[w];
-            totn += s_n[w];
-        }
-        if (b < nb) {
-            bases[2 * b] = sat32u(offk + ik - k);
-            bases[2 * b + 1] = offn + im - m;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            s_carry_k += totk;
-            s_carry_n += totn;
-        }
-        __syncthreads();
-    }
-    // survivors and newly visible Gaussians from the preprocess partials
-    uint32_t sv = 0, nw = 0;
-    for (int k = tid; k < n_pre; k += 1024) {
-        sv += pre_partial[2 * k];
-        nw += pre_partial[2 * k + 1];
-    }
+// Sum over a 256-thread block of 64-bit and 32-bit values; every thread gets
+// the totals.  s64 / s32 hold 4 entries each.
+__device__ inline void block_sum2(unsigned long long &x, uint32_t &y, unsigned long long *s64,
+                                  uint32_t *s32) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
-        sv += __shfl_xor(sv, o);
-        nw += __shfl_xor(nw, o);
+        x += __shfl_xor(x, o);
+        y += __shfl_xor(y, o);
     }
-    if (lane == 0) {
-        s_n[wave] = sv;
-        s_k[wave] = nw;
+    if ((threadIdx.x & 63) == 0) {
+        s64[threadIdx.x >> 6] = x;
+        s32[threadIdx.x >> 6] = y;
     }
     __syncthreads();
-    if (tid == 0) {
-        uint32_t surv = 0, newly = 0;
-        for (int w = 0; w < 16; ++w) {
-            surv += s_n[w];
-            newly += (uint32_t)s_k[w];
+    x = s64[0] + s64[1] + s64[2] + s64[3];
+    y = s32[0] + s32[1] + s32[2] + s32[3];
+    __syncthreads();
+}
+
+// Sum of the pairs v[0, m) over a 256-thread block: eight pairs per thread
+// and step, all loaded before they are summed; every thread gets the totals
+// (x 64-bit, y 32-bit).
+__device__ inline void block_sum_pairs(const uint2 *v, int m, unsigned long long &x, uint32_t &y,
+                                       unsigned long long *s64, uint32_t *s32) {
+    x = 0ull;
+    y = 0u;
+    for (int k0 = 0; k0 < m; k0 += 8 * kScanThreads) {
+        uint2 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int k = k0 + u * kScanThreads + (int)threadIdx.x;
+            t[u] = k < m ? v[k] : make_uint2(0u, 0u);
         }
-        const uint32_t k32 = sat32u(s_carry_k);
-        const uint32_t sorted = k32 <= cap ? k32 : 0u;
-        cnt->n_visible = s_carry_n;
-        cnt->n_keys = k32;
-        cnt->n_sorted = sorted;
-        cnt->n_survivors = surv;
-        cnt->n_newly = newly;
-        volatile HostCounters *h = host;
-        h->n_keys = k32;
-        h->n_survivors = surv;
-        h->n_newly = newly;
-        h->n_selected = cnt->n_selected;   // written by the tile selection
-        h->n_visible = s_carry_n;
-        h->n_sorted = sorted;
-        __threadfence_system();
-        h->tag = tag;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            x += t[u].x;
+            y += t[u].y;
+        }
     }
+    block_sum2(x, y, s64, s32);
 }
 
 // Per 1024-Gaussian block: the Gaussians with keys, in index order, at
-// compacted positions: vidx[p] = index, voffs[p] = start of its keys.
-__global__ __launch_bounds__(kScanThreads) void count_emit_kernel(int n, const uint32_t *count,
-                                                                  const uint32_t *bases,
-                                                                  uint32_t *vidx, uint32_t *voffs) {
+// compacted positions: vidx[p] = index, voffs[p] = start of its keys.  The
+// block's bases (keys and kept Gaussians of the blocks before it) are summed
+// from their partials by the block itself: a few KB read from cache, instead
+// of a one-block scan kernel between the two launches.  Block 0 (at least one
+// is launched), first to start, also sums every partial and writes the
+// frame's totals to the device counters and, tag last, to the host.
+__global__ __launch_bounds__(kScanThreads) void count_emit_kernel(
+    int n, int nb, const uint32_t *count, const uint32_t *part, uint32_t *vidx, uint32_t *voffs,
+    const uint32_t *pre_partial, int n_pre, Counters *cnt, HostCounters *host, uint32_t tag,
+    uint32_t cap) {
     __shared__ uint32_t s_w[4];
-    const int base = blockIdx.x * kScanBlock + threadIdx.x * kScanPer;
+    __shared__ unsigned long long s_k[4];
+    const int tid = threadIdx.x;
+    const int blk = blockIdx.x;
+    // this block's counts first: their loads overlap the partial sums
+    const int base = blk * kScanBlock + tid * kScanPer;
     uint32_t c[kScanPer], keys = 0, nz = 0;
 #pragma unroll
     for (int k = 0; k < kScanPer; ++k) {
-        c[k] = base + k < n ? count[base + k] : 0u;
+        c[k] = blk < nb && base + k < n ? count[base + k] : 0u;
         keys += c[k];
         nz += c[k] ? 1u : 0u;
     }
-    uint32_t tk, tn;
-    uint32_t ok = block_exscan<uint32_t>(keys, s_w, &tk) + bases[2 * blockIdx.x];
-    uint32_t on = block_exscan<uint32_t>(nz, s_w, &tn) + bases[2 * blockIdx.x + 1];
+    const uint2 *pp = reinterpret_cast<const uint2 *>(part);
+    unsigned long long bk;
+    uint32_t bn;
+    block_sum_pairs(pp, blk < nb ? blk : nb, bk, bn, s_k, s_w);   // blocks before this one
+    if (blk < nb) {
+        uint32_t tk, tn;
+        uint32_t ok = block_exscan<uint32_t>(keys, s_w, &tk) + sat32u(bk);
+        uint32_t on = block_exscan<uint32_t>(nz, s_w, &tn) + bn;
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
-        if (c[k]) {
-            vidx[on] = (uint32_t)(base + k);
-            voffs[on] = ok;
-            ++on;
-            ok += c[k];
+        for (int k = 0; k < kScanPer; ++k) {
+            if (c[k]) {
+                vidx[on] = (uint32_t)(base + k);
+                voffs[on] = ok;
+                ++on;
+                ok += c[k];
+            }
         }
+    }
+    if (blk != 0) return;   // block-uniform
+    unsigned long long tot_k, sv;
+    uint32_t tot_n, nw;
+    block_sum_pairs(pp, nb, tot_k, tot_n, s_k, s_w);
+    // survivors and newly visible Gaussians from the preprocess partials
+    block_sum_pairs(reinterpret_cast<const uint2 *>(pre_partial), n_pre, sv, nw, s_k, s_w);
+    if (tid == 0) {
+        const uint32_t n_surv = (uint32_t)sv, n_newly = nw;
+        const uint32_t k32 = sat32u(tot_k);
+        const uint32_t sorted = k32 <= cap ? k32 : 0u;
+        cnt->n_visible = tot_n;
+        cnt->n_keys = k32;
+        cnt->n_sorted = sorted;
+        cnt->n_survivors = n_surv;
+        cnt->n_newly = n_newly;
+        volatile HostCounters *h = host;
+        h->n_keys = k32;
+        h->n_survivors = n_surv;
+        h->n_newly = n_newly;
+        h->n_selected = cnt->n_selected;   // written by the tile selection
+        h->n_visible = tot_n;
+        h->n_sorted = sorted;
+        __threadfence_system();
+        h->tag = tag;
     }
 }
 
@@ -456,15 +448,16 @@ __global__ __launch_bounds__(kLongThreads) void segment_sort_long_kernel(const u
 int count_scan_blocks(int n) { return (n + kScanBlock - 1) / kScanBlock; }
 
 void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                       uint32_t *part, uint32_t *bases, uint32_t *vidx, uint32_t *voffs,
-                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
-                       HostCounters *host, uint32_t tag, hipStream_t st) {
+                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, Counters *cnt,
+                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
+                       uint32_t tag, hipStream_t st) {
     const int nb = count_scan_blocks(n > 0 ? n : 0);
     if (nb > 0)
         count_partials_kernel<<<nb, kScanThreads, 0, st>>>(n, count, rect, rowpre, TX, part);
-    // always: publishes the counters
-    count_scan_kernel<<<1, 1024, 0, st>>>(nb, part, bases, pre_partial, n_pre, cnt, host, tag, cap);
-    if (nb > 0) count_emit_kernel<<<nb, kScanThreads, 0, st>>>(n, count, bases, vidx, voffs);
+    // at least one block: the last one publishes the counters
+    count_emit_kernel<<<nb > 0 ? nb : 1, kScanThreads, 0, st>>>(n, nb, count, part, vidx, voffs,
+                                                                pre_partial, n_pre, cnt, host, tag,
+                                                                cap);
 }
 
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,

@@ -212,10 +212,21 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
 // tag last, to the host.
 __device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s_red) {
     const int tid = threadIdx.x;
+    // eight pairs per thread and step, loaded before they are summed
     uint32_t a = 0, b = 0;
-    for (int k = tid; k < io.n_pre; k += kSortThreads) {
-        a += io.pre_partial[2 * k];
-        b += io.pre_partial[2 * k + 1];
+    const uint2 *pp = reinterpret_cast<const uint2 *>(io.pre_partial);
+    for (int k0 = 0; k0 < io.n_pre; k0 += 8 * kSortThreads) {
+        uint2 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int k = k0 + u * kSortThreads + tid;
+            v[u] = k < io.n_pre ? pp[k] : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            a += v[u].x;
+            b += v[u].y;
+        }
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {

@@ -6,11 +6,12 @@
 //  - depth fill, backward correspondence query and unmatched tiles, one
 //    block per tile with a block-wide OR;
 //  - occluded tiles of the newly visible Gaussians, one wave per
-//    (Gaussian, tile) pair with a wave ballot over the tile's 256 pixels;
-//  - tile selection and compaction, one block per tile row, including the
-//    per-row prefix sums of the mask used by the key counts;
-//  - stitching of the warped reference image into the tiles that are not
-//    re-rendered (Eq. 4, bilinear).
+//    (Gaussian, tile) pair with a wave ballot over the tile's 256 pixels,
+//    the pairs of 1024 Gaussians dealt out over the waves of a block;
+//  - tile selection and compaction in one launch, one block per tile row,
+//    including the per-row prefix sums of the mask used by the key counts.
+// (The stitching of the tiles that are not re-rendered, Eq. 4, runs in the
+// blend launch: stitch.h.)
 // All of these are HBM- or latency-bound; none is a dense contraction.
 #include "tgs_internal.h"
 
@@ -107,60 +108,6 @@ __global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *_
     if (threadIdx.x == 0) um[tile] = (uint8_t)(any ? 1 : 0);
 }
 
-// Each wave scans 64 status bytes at a time; for every newly visible
-// Gaussian among them the whole wave tests its rectangle's tiles, four pixel
-// centres per lane, with a ballot per tile.
-__global__ __launch_bounds__(256) void occluded_kernel(WarpK w, int n,
-                                                       const uint8_t *__restrict__ status,
-                                                       const float4 *g, const ushort4 *rect,
-                                                       uint8_t *oc) {
-    const int lane = threadIdx.x & 63;
-    const int wave = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
-    const int n_waves = (int)((gridDim.x * blockDim.x) >> 6);
-    for (int base = wave * 64; base < n; base += n_waves * 64) {
-        const int me = base + lane;
-        const bool nv = me < n && (status[me] & 2u);
-        uint64_t todo = __ballot(nv);
-        while (todo) {
-            const int l = __ffsll((unsigned long long)todo) - 1;
-            todo &= todo - 1ull;
-            const int i = base + l;
-            const ushort4 r = rect[i];
-            if (r.x > r.z || r.y > r.w) continue;
-            const float4 a = g[4 * (size_t)i];
-            const float4 b = g[4 * (size_t)i + 1];
-            if (!(b.y >= 0.999f * kAlphaMin)) continue;   // alpha < 1/255 everywhere
-            // tiles meeting the box of the alpha >= 1/255 ellipse (enlarged
-            // by 0.2% + 0.05 px): no pixel outside it can reach the threshold
-            const float kq = 2.0f * __logf(fmaxf(255.0f * b.y, 1.0f)) + 1e-3f;
-            const float det = a.z * b.x - a.w * a.w;
-            const float hx = sqrtf(kq * b.x / det) * 1.002f + 0.05f;
-            const float hy = sqrtf(kq * a.z / det) * 1.002f + 0.05f;
-            const int ex0 = max((int)r.x, (int)ceilf((a.x - hx - 15.0f) * 0.0625f));
-            const int ex1 = min((int)r.z, (int)floorf((a.x + hx) * 0.0625f));
-            const int ey0 = max((int)r.y, (int)ceilf((a.y - hy - 15.0f) * 0.0625f));
-            const int ey1 = min((int)r.w, (int)floorf((a.y + hy) * 0.0625f));
-            for (int ty = ey0; ty <= ey1; ++ty)
-                for (int tx = ex0; tx <= ex1; ++tx) {
-                    float amax = 0.0f;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const int p = lane + 64 * k;
-                        const int x = tx * kTile + (p & 15), y = ty * kTile + (p >> 4);
-                        if (x < w.W && y < w.H) {
-                            const float dx = a.x - (float)x, dy = a.y - (float)y;
-                            const float power = -0.5f * (a.z * dx * dx + b.x * dy * dy) - a.w * dx * dy;
-                            if (!(power > 0.0f))
-                                amax = fmaxf(amax, fminf(kAlphaMax, b.y * __expf(power)));
-                        }
-                    }
-                    const uint64_t hit = __ballot(!(amax < kAlphaMin));
-                    if (hit != 0ull && lane == 0) oc[ty * w.TX + tx] = 1;
-                }
-        }
-    }
-}
-
 __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave, uint32_t *total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t inc = v;
@@ -183,135 +130,196 @@ __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave,
     return off + inc - v;
 }
 
+// value of x in lane j (j uniform across the wave)
+__device__ inline float lane_f(float x, int j) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), j));
+}
+
+// Tiles that Gaussian i can reach with alpha >= 1/255: its rectangle cut to
+// the tiles meeting the box of the alpha >= 1/255 ellipse (enlarged by 0.2%
+// + 0.05 px, from the record; negative half extents: alpha < 1/255
+// everywhere).  No pixel outside that box can reach the threshold.  Returns
+// the number of tiles (0: none) and the first column and row and the column
+// count in *box.
+__device__ inline uint32_t occ_box(int i, const float4 *g, const ushort4 *rect, int3 *box) {
+    const ushort4 r = rect[i];
+    const float4 a = g[4 * (size_t)i];
+    const float hx = g[4 * (size_t)i + 2].w, hy = g[4 * (size_t)i + 1].w;
+    if (r.x > r.z || r.y > r.w || !(hx >= 0.0f)) return 0u;
+    const int ex0 = max((int)r.x, (int)ceilf((a.x - hx - 15.0f) * 0.0625f));
+    const int ex1 = min((int)r.z, (int)floorf((a.x + hx) * 0.0625f));
+    const int ey0 = max((int)r.y, (int)ceilf((a.y - hy - 15.0f) * 0.0625f));
+    const int ey1 = min((int)r.w, (int)floorf((a.y + hy) * 0.0625f));
+    if (ex0 > ex1 || ey0 > ey1) return 0u;
+    *box = make_int3(ex0, ey0, ex1 - ex0 + 1);
+    return (uint32_t)((ex1 - ex0 + 1) * (ey1 - ey0 + 1));
+}
+
+constexpr int kOccThreads = 1024;            // one Gaussian per thread
+constexpr int kOccWaves = kOccThreads / 64;
+
+// Exclusive scan across a block of kOccThreads threads, one value each;
+// *total = the block's sum.
+__device__ inline uint32_t occ_block_scan(uint32_t v, uint32_t *s_wave, uint32_t *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_up(inc, d);
+        if (lane >= d) inc += o;
+    }
+    if (lane == 63) s_wave[wave] = inc;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int x = 0; x < kOccWaves; ++x) {
+        const uint32_t c = s_wave[x];
+        if (x < wave) off += c;
+        tot += c;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + inc - v;
+}
+
+// One block per 1024 Gaussians.  The newly visible ones that can reach a
+// tile are compacted in LDS with the start of their (Gaussian, tile) pairs
+// (two block scans).  Wave w takes the pairs p = w (mod 16), 64 at a time: lane
+// l finds the owner and tile of its pair (the searches run side by side),
+// then the wave tests the pairs one after another with their data broadcast
+// from the lanes: each lane tests four pixel centres and a ballot marks the
+// tile.  Dealing the pairs out one by one spreads a block's pairs, however
+// few Gaussians hold them, evenly over its sixteen waves.  Marks are plain
+// byte stores of 1, so concurrent writers agree.
+__global__ __launch_bounds__(kOccThreads) void occluded_kernel(WarpK w, int n,
+                                                               const uint8_t *__restrict__ status,
+                                                               const float4 *__restrict__ g,
+                                                               const ushort4 *__restrict__ rect,
+                                                               uint8_t *oc) {
+    __shared__ uint32_t s_idx[kOccThreads];   // compacted Gaussians
+    __shared__ uint32_t s_off[kOccThreads];   // start of their pairs
+    __shared__ uint32_t s_wave[kOccWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int i = blockIdx.x * kOccThreads + tid;
+    uint32_t c = 0u;
+    if (i < n && (status[i] & 2u)) {
+        int3 box;
+        c = occ_box(i, g, rect, &box);
+    }
+    uint32_t total, n_act;
+    const uint32_t oa = occ_block_scan(c ? 1u : 0u, s_wave, &n_act);
+    const uint32_t op = occ_block_scan(c, s_wave, &total);
+    if (c) {
+        s_idx[oa] = (uint32_t)i;
+        s_off[oa] = op;
+    }
+    __syncthreads();
+    const uint32_t mine = total > (uint32_t)wave ? (total - (uint32_t)wave + kOccWaves - 1) / kOccWaves : 0u;
+    for (uint32_t r0 = 0; r0 < mine; r0 += 64u) {
+        const uint32_t r = r0 + (uint32_t)lane;
+        int tx = 0, ty = 0;
+        float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f), b = a;
+        if (r < mine) {
+            const uint32_t p = (uint32_t)wave + kOccWaves * r;
+            // owner of pair p: the last entry whose start is <= p (starts
+            // increase strictly: every entry has a pair)
+            uint32_t lo = 0, hi = n_act;
+            while (hi - lo > 1u) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (s_off[mid] <= p) lo = mid;
+                else hi = mid;
+            }
+            const int gi = (int)s_idx[lo];
+            int3 box;
+            (void)occ_box(gi, g, rect, &box);
+            const int k = (int)(p - s_off[lo]);
+            tx = box.x + k % box.z;
+            ty = box.y + k / box.z;
+            a = g[4 * (size_t)gi];
+            b = g[4 * (size_t)gi + 1];
+        }
+        const int m = (int)min(64u, mine - r0);
+        for (int j = 0; j < m; ++j) {
+            const int jx = __builtin_amdgcn_readlane(tx, j), jy = __builtin_amdgcn_readlane(ty, j);
+            const float ax = lane_f(a.x, j), ay = lane_f(a.y, j), az = lane_f(a.z, j),
+                        aw = lane_f(a.w, j), bx = lane_f(b.x, j), by = lane_f(b.y, j);
+            float amax = 0.0f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int px = lane + 64 * q;
+                const int x = jx * kTile + (px & 15), y = jy * kTile + (px >> 4);
+                if (x < w.W && y < w.H) {
+                    const float dx = ax - (float)x, dy = ay - (float)y;
+                    const float power = -0.5f * (az * dx * dx + bx * dy * dy) - aw * dx * dy;
+                    if (!(power > 0.0f)) amax = fmaxf(amax, fminf(kAlphaMax, by * __expf(power)));
+                }
+            }
+            const uint64_t hit = __ballot(!(amax < kAlphaMin));
+            if (hit != 0ull && lane == 0) oc[jy * w.TX + jx] = 1;
+        }
+    }
+}
+
 // One block per tile row: selected = occluded | unmatched (or every tile),
-// and the row's exclusive prefix sums rowpre[ty][0..TX] (rowpre[ty][TX] is the
-// row's count).
-__global__ __launch_bounds__(256) void select_rows_kernel(int TX, int mode, const uint8_t *oc,
-                                                          const uint8_t *um, uint8_t *sel,
-                                                          uint32_t *rowpre, uint8_t *mask_out) {
+// the row's exclusive prefix sums rowpre[ty][0..TX] (rowpre[ty][TX] is the
+// row's count) and its entries of the ascending list of selected tiles (the
+// tiles not selected fill the list from the end, descending).  The
+// list offset of the row, the selected tiles of the rows above, is counted
+// by the block itself from the occluded and unmatched flags (a few KB read
+// from cache), so no second launch waits for the other rows.  The last row
+// also stores the total.
+__global__ __launch_bounds__(256) void select_kernel(int TX, int TY, int mode, const uint8_t *oc,
+                                                     const uint8_t *um, uint8_t *sel,
+                                                     uint32_t *rowpre, int *sel_list, int *sel_cols,
+                                                     uint8_t *mask_out, Counters *cnt) {
     __shared__ uint32_t s_wave[4];
     const int ty = blockIdx.x;
+    // selected tiles above the row: four flags per 32-bit word, then a byte tail
+    const uint32_t above = (uint32_t)ty * (uint32_t)TX;
+    uint32_t part = 0;
+    if (mode) {
+        part = threadIdx.x == 0 ? above : 0u;
+    } else {
+        const uint32_t nw = above / 4u;
+        const uint32_t *ow = reinterpret_cast<const uint32_t *>(oc);
+        const uint32_t *uw = reinterpret_cast<const uint32_t *>(um);
+        for (uint32_t k = threadIdx.x; k < nw; k += 256) {
+            const uint32_t f = (ow[k] | uw[k]) & 0x01010101u;   // flags are 0 or 1
+            part += (f * 0x01010101u) >> 24;
+        }
+        for (uint32_t t = 4u * nw + threadIdx.x; t < above; t += 256) part += (uint32_t)(oc[t] | um[t]);
+    }
+    uint32_t off;
+    (void)block_exclusive_scan256(part, s_wave, &off);
     uint32_t *row = rowpre + (size_t)ty * (TX + 1);
     uint32_t run = 0;
     for (int c = 0; c < TX; c += 256) {
         const int x = c + threadIdx.x;
         const int t = ty * TX + x;
-        uint32_t s = 0;
+        uint32_t f = 0;
         if (x < TX) {
-            s = mode ? 1u : (uint32_t)(oc[t] | um[t]);
-            sel[t] = (uint8_t)s;
-            if (mask_out) mask_out[t] = (uint8_t)s;
+            f = mode ? 1u : (uint32_t)(oc[t] | um[t]);
+            sel[t] = (uint8_t)f;
+            if (mask_out) mask_out[t] = (uint8_t)f;
         }
         uint32_t tot;
-        const uint32_t ex = block_exclusive_scan256(s, s_wave, &tot);
-        if (x < TX) row[x] = run + ex;
+        const uint32_t ex = block_exclusive_scan256(f, s_wave, &tot);
+        if (x < TX) {
+            row[x] = run + ex;
+            if (f) {
+                sel_list[off + run + ex] = t;
+                sel_cols[(size_t)ty * TX + run + ex] = x;
+            } else {
+                // the others from the end: tiles not selected above the row,
+                // then those of the row before this one
+                sel_list[TX * TY - 1 - ((above - off) + ((uint32_t)x - run - ex))] = t;
+            }
+        }
         run += tot;
     }
-    if (threadIdx.x == 0) row[TX] = run;
-}
-
-// One block per tile row: the ascending list of selected tiles; the last row
-// also stores the total.
-__global__ __launch_bounds__(256) void select_list_kernel(int TX, int TY, const uint8_t *sel,
-                                                          const uint32_t *rowpre, int *sel_list,
-                                                          int *sel_cols, Counters *cnt) {
-    __shared__ uint32_t s_sum[4];
-    const int ty = blockIdx.x;
-    uint32_t part = 0;
-    for (int r = threadIdx.x; r < ty; r += 256) part += rowpre[(size_t)r * (TX + 1) + TX];
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) part += __shfl_xor(part, o);
-    if ((threadIdx.x & 63) == 0) s_sum[threadIdx.x >> 6] = part;
-    __syncthreads();
-    const uint32_t off = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
-    const uint32_t *row = rowpre + (size_t)ty * (TX + 1);
-    for (int x = threadIdx.x; x < TX; x += 256) {
-        const int t = ty * TX + x;
-        if (sel[t]) {
-            sel_list[off + row[x]] = t;
-            sel_cols[(size_t)ty * TX + row[x]] = x;
-        }
-    }
-    if (ty == TY - 1 && threadIdx.x == 0) cnt->n_selected = off + row[TX];
-}
-
-__global__ __launch_bounds__(256) void stitch_kernel(WarpK w, const uint8_t *sel,
-                                                     const float *__restrict__ tab,
-                                                     const float2 *__restrict__ uv, float *rgb) {
-    const int tile = blockIdx.x;
-    if (sel[tile]) return;
-    const int tx = tile % w.TX, ty = tile / w.TX;
-    const int px = tx * kTile + (threadIdx.x & 15), py = ty * kTile + (threadIdx.x >> 4);
-    if (px >= w.W || py >= w.H) return;
-    const size_t HW = (size_t)w.W * w.H;
-    const size_t q = (size_t)py * w.W + px;
-    const float2 c = uv[q];
-    if (!(c.x >= 0.0f && c.y >= 0.0f)) {   // unmatched pixels only occur in selected tiles
-        rgb[q] = rgb[HW + q] = rgb[2 * HW + q] = 0.0f;
-        return;
-    }
-    const int x0 = (int)floorf(c.x), y0 = (int)floorf(c.y);
-    const int x1 = min(x0 + 1, w.W - 1), y1 = min(y0 + 1, w.H - 1);
-    const float ax = c.x - (float)x0, ay = c.y - (float)y0;
-    const size_t i00 = (size_t)y0 * w.W + x0, i10 = (size_t)y0 * w.W + x1;
-    const size_t i01 = (size_t)y1 * w.W + x0, i11 = (size_t)y1 * w.W + x1;
-#pragma unroll
-    for (int ch = 0; ch < 3; ++ch) {
-        const float *I = tab + ch * HW;
-        const float top = (1.0f - ax) * I[i00] + ax * I[i10];
-        const float bot = (1.0f - ax) * I[i01] + ax * I[i11];
-        rgb[ch * HW + q] = (1.0f - ay) * top + ay * bot;
-    }
-}
-
-// Eq. 4 from a half-resolution repaired depth: pixel (x, y) takes the depth
-// of its block (x >> 1, y >> 1), is unprojected and moved to the reference
-// view at full resolution, and samples the reference image bilinearly at
-// the projection clamped to the image (the block matched; the pixel itself
-// may land up to about a pixel outside).
-__global__ __launch_bounds__(256) void stitch_depth_kernel(WarpK w, int Wg, const uint8_t *sel,
-                                                           const float *__restrict__ tab,
-                                                           const float *__restrict__ dfill,
-                                                           float *rgb) {
-    const int tile = blockIdx.x;
-    if (sel[tile]) return;
-    const int tx = tile % w.TX, ty = tile / w.TX;
-    const int px = tx * kTile + (threadIdx.x & 15), py = ty * kTile + (threadIdx.x >> 4);
-    if (px >= w.W || py >= w.H) return;
-    const size_t HW = (size_t)w.W * w.H;
-    const size_t q = (size_t)py * w.W + px;
-    const float d = dfill[(size_t)(py >> 1) * Wg + (px >> 1)];
-    bool ok = false;
-    float u = 0.0f, v = 0.0f;
-    if (d != kNoHit) {
-        const float rx = ((float)px - w.kcur[2]) / w.kcur[0];
-        const float ry = ((float)py - w.kcur[3]) / w.kcur[1];
-        const float Px = d * rx, Py = d * ry, Pz = d;
-        const float *M = w.Minv;
-        const float X = ((M[0] * Px + M[1] * Py) + M[2] * Pz) + M[3];
-        const float Y = ((M[4] * Px + M[5] * Py) + M[6] * Pz) + M[7];
-        const float Z = ((M[8] * Px + M[9] * Py) + M[10] * Pz) + M[11];
-        if (Z > w.z_near) {
-            u = fminf(fmaxf(w.kref[0] * (X / Z) + w.kref[2], 0.0f), (float)(w.W - 1));
-            v = fminf(fmaxf(w.kref[1] * (Y / Z) + w.kref[3], 0.0f), (float)(w.H - 1));
-            ok = true;
-        }
-    }
-    if (!ok) {   // cannot occur outside selected tiles
-        rgb[q] = rgb[HW + q] = rgb[2 * HW + q] = 0.0f;
-        return;
-    }
-    const int x0 = (int)floorf(u), y0 = (int)floorf(v);
-    const int x1 = min(x0 + 1, w.W - 1), y1 = min(y0 + 1, w.H - 1);
-    const float ax = u - (float)x0, ay = v - (float)y0;
-    const size_t i00 = (size_t)y0 * w.W + x0, i10 = (size_t)y0 * w.W + x1;
-    const size_t i01 = (size_t)y1 * w.W + x0, i11 = (size_t)y1 * w.W + x1;
-#pragma unroll
-    for (int ch = 0; ch < 3; ++ch) {
-        const float *I = tab + ch * HW;
-        const float top = (1.0f - ax) * I[i00] + ax * I[i10];
-        const float bot = (1.0f - ax) * I[i01] + ax * I[i11];
-        rgb[ch * HW + q] = (1.0f - ay) * top + ay * bot;
+    if (threadIdx.x == 0) {
+        row[TX] = run;
+        if (ty == TY - 1) cnt->n_selected = off + run;
     }
 }
 
@@ -350,29 +358,18 @@ void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *
     fill_query_kernel<<<w.TX * w.TY, w.tp * w.tp, 0, st>>>(w, dmin, dfill, uv, um);
 }
 
-void launch_stitch_depth(const WarpK &w, int Wg, const uint8_t *sel, const float *tab,
-                         const float *dfill, float *rgb, hipStream_t st) {
-    stitch_depth_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, Wg, sel, tab, dfill, rgb);
-}
-
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
                      const ushort4 *rect, uint8_t *oc, hipStream_t st) {
     if (n <= 0) return;
-    int blocks = (n + 255) / 256;
-    if (blocks > 1024) blocks = 1024;
-    occluded_kernel<<<blocks, 256, 0, st>>>(w, n, status, g, rect, oc);
+    occluded_kernel<<<(n + kOccThreads - 1) / kOccThreads, kOccThreads, 0, st>>>(w, n, status, g,
+                                                                                rect, oc);
 }
 
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
                    int *sel_list, uint32_t *rowpre, int *sel_cols, uint8_t *mask_out,
                    Counters *cnt, hipStream_t st) {
-    select_rows_kernel<<<TY, 256, 0, st>>>(TX, mode, oc, um, sel, rowpre, mask_out);
-    select_list_kernel<<<TY, 256, 0, st>>>(TX, TY, sel, rowpre, sel_list, sel_cols, cnt);
-}
-
-void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,
-                   float *rgb, hipStream_t st) {
-    stitch_kernel<<<w.TX * w.TY, 256, 0, st>>>(w, sel, tab, uv, rgb);
+    select_kernel<<<TY, 256, 0, st>>>(TX, TY, mode, oc, um, sel, rowpre, sel_list, sel_cols,
+                                      mask_out, cnt);
 }
 
 void launch_fill_u8(uint8_t *p, size_t n, uint8_t v, hipStream_t st) { fill<uint8_t>(p, n, v, st); }

@@ -387,10 +387,9 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
     if (ws.frame_seg) {
         ProfScope ps(TGS_PROF_SORT, st);
         ws.seq += 1;
-        const int nb = count_scan_blocks(n > 0 ? n : 0);
         uint32_t *part = ws.sort.as<uint32_t>();
         launch_count_scan(n, ws.count.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX, part,
-                          part + 2 * (size_t)nb, ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
+                          ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
                           ws.cnt.as<Counters>(), (uint32_t)ws.key_cap, ws.partial.as<uint32_t>(),
                           n > 0 ? preprocess_blocks(n) : 0, ws.host_cnt_dev, ws.seq, st);
         TGS_LAUNCHED("count scan");
@@ -959,21 +958,19 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.rgb = out->rgb;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
         a.hits = g_prof.hits(TGS_PROF_BLEND_TGS);
+            // the blocks past the selected tiles stitch the others (Eq. 4)
+            a.stitch_list = ws.sel_list.as<int>();
+            a.stitch_mode = half ? 2 : 1;
+            a.stitch_wg = s->Wg;
+            a.stitch_tab = s->tab.as<float>();
+            a.stitch_uv = s->uv.as<float2>();
+            a.stitch_dfill = s->dfill.as<float>();
+            a.sw = w;
             {
                 hipEvent_t ev0, ev1;
                 g_prof.kernel_events(TGS_PROF_BLEND_TGS, &ev0, &ev1);
                 launch_blend(a, nt, st, ev0, ev1);
-                TGS_LAUNCHED("blend");
-            }
-            {
-                ProfScope ps(TGS_PROF_STITCH, st);
-                if (half)
-                    launch_stitch_depth(w, s->Wg, ws.sel.as<uint8_t>(), s->tab.as<float>(),
-                                        s->dfill.as<float>(), out->rgb, st);
-                else
-                    launch_stitch(w, ws.sel.as<uint8_t>(), s->tab.as<float>(), s->uv.as<float2>(),
-                                  out->rgb, st);
-                TGS_LAUNCHED("stitch");
+                TGS_LAUNCHED("blend and stitch");
             }
         } else {
             CullK cull = no_cull(p.z_near, ws);

@@ -106,7 +106,18 @@ __device__ inline float ordered_to_float(int i) {
 __device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int TX) {
     if (r.x > r.z || r.y > r.w) return 0u;
     uint32_t c = 0;
-    for (int y = r.y; y <= r.w; ++y) {
+    int y = r.y;
+    // four rows per step: all eight loads are in flight before the first use
+    for (; y + 3 <= (int)r.w; y += 4) {
+        const uint32_t *row = rowpre + (size_t)y * (TX + 1);
+        const size_t s = (size_t)(TX + 1);
+        const uint32_t a0 = row[r.z + 1], b0 = row[r.x];
+        const uint32_t a1 = row[s + r.z + 1], b1 = row[s + r.x];
+        const uint32_t a2 = row[2 * s + r.z + 1], b2 = row[2 * s + r.x];
+        const uint32_t a3 = row[3 * s + r.z + 1], b3 = row[3 * s + r.x];
+        c += (a0 - b0) + (a1 - b1) + (a2 - b2) + (a3 - b3);
+    }
+    for (; y <= (int)r.w; ++y) {
         const uint32_t *row = rowpre + (size_t)y * (TX + 1);
         c += row[r.z + 1] - row[r.x];
     }
@@ -166,16 +177,16 @@ void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32
 
 // ---- launchers (k_segsort.hip) ----
 // Per-tile depth order without the global depth sort: key counts scanned in
-// index order (part / bases: 2 words per 1024-Gaussian block each), the
+// index order (part: 2 words per 1024-Gaussian block), the
 // Gaussians with keys compacted in index order into vidx / voffs (the
 // duplication's input), the frame's counters published as the depth sort
 // does; after the tile sort, each tile's list sorted by (depth bits, index)
 // in place (tmp: scratch of the same size as vals).
 int count_scan_blocks(int n);
 void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                       uint32_t *part, uint32_t *bases, uint32_t *vidx, uint32_t *voffs,
-                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
-                       HostCounters *host, uint32_t tag, hipStream_t st);
+                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, Counters *cnt,
+                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
+                       uint32_t tag, hipStream_t st);
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
                          const uint32_t *dkey, hipStream_t st);
 // Longest list the per-tile sort handles in LDS; longer ones take its slower
@@ -184,6 +195,17 @@ void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint3
 constexpr int kSegBucketMax = 12;
 
 // ---- launchers (k_blend.hip) ----
+// View pair of a TemporalGS frame (reference -> current) for the temporal
+// kernels and stitching.
+struct WarpK {
+    float M[12];              // reference camera -> current camera
+    float Minv[12];           // current camera -> reference camera
+    float kref[4], kcur[4];   // fx, fy, cx, cy
+    float z_near;
+    int W, H, TX, TY;         // grid size (image, or the geometry buffer's) and tiles
+    int tp;                   // pixels per tile side on this grid (16, or 8 at half resolution)
+};
+
 struct BlendArgs {
     int W, H, TX, TY;
     const int *tile_list;     // NULL: blockIdx = tile
@@ -202,6 +224,18 @@ struct BlendArgs {
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
     unsigned long long *hits;   // with pairs: count of pairs with alpha >= 1/255 (composited or stopping)
     float empty_depth;        // depth written where no Gaussian is composited
+    // optional (TGS frames): blocks at or past *n_tiles_dev stitch tile
+    // stitch_list[block] from the reference image stitch_tab (Eq. 4)
+    // instead of blending, so that stitching overlaps the blend's tail:
+    // stitch_mode 1 samples at the per-pixel correspondences stitch_uv,
+    // 2 unprojects with the half-resolution repaired depth stitch_dfill
+    // (grid width stitch_wg); sw is the full-resolution view pair
+    const int *stitch_list;
+    int stitch_mode, stitch_wg;
+    const float *stitch_tab;
+    const float2 *stitch_uv;
+    const float *stitch_dfill;
+    WarpK sw;
 };
 // start/stop (may be NULL) are attached to the dispatch itself
 // (hipExtLaunchKernelGGL): kernel timing without extra barrier packets.
@@ -213,14 +247,6 @@ void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g, int W, int
                        hipStream_t st);
 
 // ---- launchers (k_temporal.hip) ----
-struct WarpK {
-    float M[12];              // reference camera -> current camera
-    float Minv[12];           // current camera -> reference camera
-    float kref[4], kcur[4];   // fx, fy, cx, cy
-    float z_near;
-    int W, H, TX, TY;         // grid size (image, or the geometry buffer's) and tiles
-    int tp;                   // pixels per tile side on this grid (16, or 8 at half resolution)
-};
 void launch_temporal_init(int n_px, int n_tiles, float *dmin, float *smax, uint8_t *oc,
                           Counters *cnt, hipStream_t st);
 void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *dmin, float *smax,
@@ -229,17 +255,12 @@ void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *
                        hipStream_t st);
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
                      const ushort4 *rect, uint8_t *oc, hipStream_t st);
+// sel_list: the selected tiles ascending in [0, n_selected), the others
+// descending from the end (a permutation of all tiles);
 // sel_cols[ty * TX + k] = column of the k-th selected tile of row ty
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
                    int *sel_list, uint32_t *rowpre, int *sel_cols, uint8_t *mask_out,
                    Counters *cnt, hipStream_t st);
-void launch_stitch(const WarpK &w, const uint8_t *sel, const float *tab, const float2 *uv,
-                   float *rgb, hipStream_t st);
-// Stitching from a half-resolution repaired depth (grid width Wg): each pixel
-// of a non-selected tile is unprojected with its 2x2 block's depth (w: the
-// full-resolution view pair).
-void launch_stitch_depth(const WarpK &w, int Wg, const uint8_t *sel, const float *tab,
-                         const float *dfill, float *rgb, hipStream_t st);
 void launch_fill_u8(uint8_t *p, size_t n, uint8_t v, hipStream_t st);
 void launch_fill_f32(float *p, size_t n, float v, hipStream_t st);
 void launch_fill_i32(int *p, size_t n, int v, hipStream_t st);
