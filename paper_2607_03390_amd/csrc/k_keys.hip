@@ -246,8 +246,8 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
             const uint64_t nz = __ballot(c != 0u);
             // the host reads this value some frames later: no fence needed
             if (max_bucket && tid == 0)
-                *reinterpret_cast<volatile uint32_t *>(max_bucket) =
-                    nz ? (uint32_t)(32 - (__ffsll((long long)nz) - 1)) : 0u;
+                __hip_atomic_store(max_bucket, nz ? (uint32_t)(32 - (__ffsll((long long)nz) - 1)) : 0u,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
         __syncthreads();
     }

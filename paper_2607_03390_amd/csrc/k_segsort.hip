@@ -201,15 +201,8 @@ __global__ __launch_bounds__(kScanThreads) void count_emit_kernel(
         cnt->n_sorted = sorted;
         cnt->n_survivors = n_surv;
         cnt->n_newly = n_newly;
-        volatile HostCounters *h = host;
-        h->n_keys = k32;
-        h->n_survivors = n_surv;
-        h->n_newly = n_newly;
-        h->n_selected = cnt->n_selected;   // written by the tile selection
-        h->n_visible = tot_n;
-        h->n_sorted = sorted;
-        __threadfence_system();
-        h->tag = tag;
+        // n_selected was written by the tile selection
+        publish_host(host, k32, n_surv, n_newly, cnt->n_selected, tot_n, sorted, tag);
     }
 }
 

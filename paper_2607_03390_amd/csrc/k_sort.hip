@@ -248,15 +248,8 @@ __device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s
         io.cnt->n_survivors = surv;
         io.cnt->n_newly = newly;
         // n_visible and n_selected were written by earlier kernels
-        volatile HostCounters *h = io.host;
-        h->n_keys = k32;
-        h->n_survivors = surv;
-        h->n_newly = newly;
-        h->n_selected = io.cnt->n_selected;
-        h->n_visible = io.cnt->n_visible;
-        h->n_sorted = sorted;
-        __threadfence_system();
-        h->tag = io.tag;
+        publish_host(io.host, k32, surv, newly, io.cnt->n_selected, io.cnt->n_visible, sorted,
+                     io.tag);
     }
     __syncthreads();
 }

@@ -82,13 +82,27 @@ struct Counters {
 };
 
 // The frame's counters as the host reads them: written by the last counting
-// kernel straight into coherent pinned host memory, tag last (after a
-// system-scope fence), so the host waits for the tag instead of a copy.
+// kernel straight into coherent pinned host memory (16-byte aligned), tag
+// last (after a system-scope fence), so the host waits for the tag instead of
+// a copy.
 struct HostCounters {
     uint32_t n_keys, n_survivors, n_newly, n_selected, n_visible, n_sorted;
     uint32_t pad;
     uint32_t tag;
 };
+
+// Writes the frame's counters to the host: the six values as two vector
+// stores, a system-scope fence (they are complete and visible), then the tag
+// as a relaxed store that nothing waits for.  (A volatile store would wait
+// for its own round trip to host memory, one after another.)
+__device__ inline void publish_host(HostCounters *h, uint32_t n_keys, uint32_t n_survivors,
+                                    uint32_t n_newly, uint32_t n_selected, uint32_t n_visible,
+                                    uint32_t n_sorted, uint32_t tag) {
+    reinterpret_cast<uint4 *>(h)[0] = make_uint4(n_keys, n_survivors, n_newly, n_selected);
+    reinterpret_cast<uint2 *>(h)[2] = make_uint2(n_visible, n_sorted);
+    __threadfence_system();
+    __hip_atomic_store(&h->tag, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
 
 // Ordered-int encoding of a float: signed-int order equals float order, so
 // integer atomic min/max give exact float min/max.
