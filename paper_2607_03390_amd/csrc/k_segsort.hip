@@ -377,16 +377,28 @@ __device__ void seg_sort_lds(uint32_t *vals, uint32_t L, const uint32_t *dkey, u
 // One block per tile: its list [ranges.x, ranges.y) of vals, in index order,
 // sorted by (depth bits, index) in place.  Short lists (up to 1024 entries):
 // up to 256 by counting, longer ones by the LDS radix sort.
+// Lists above 1024 entries: left to the long-list kernel (long_lists != 0),
+// else sorted here over global memory (tmp), for frames where they are rare
+// enough that a launch of their own costs more than it saves.
 __global__ __launch_bounds__(kShortThreads) void segment_sort_short_kernel(const uint2 *ranges,
                                                                          uint32_t *vals,
-                                                                         const uint32_t *dkey) {
+                                                                         uint32_t *tmp,
+                                                                         const uint32_t *dkey,
+                                                                         int long_lists) {
     __shared__ uint2 s_kv[kShortCap];
     __shared__ uint32_t s_wh[(kShortThreads / 64) * 256];
     __shared__ uint32_t s_dstart[256];
     __shared__ uint32_t s_scan[kShortThreads / 64];
     const uint2 r = ranges[blockIdx.x];
     const uint32_t L = r.y - r.x;
-    if (L <= 1 || L > (uint32_t)kShortCap) return;   // block-uniform
+    if (L <= 1) return;   // block-uniform
+    if (L > (uint32_t)kShortCap) {
+        if (long_lists) return;
+        uint32_t *s_hist = reinterpret_cast<uint32_t *>(s_kv);   // 256
+        uint32_t *s_run = s_hist + 256;                          // 256
+        segment_lsd<kShortThreads>(vals + r.x, tmp + r.x, L, dkey, s_hist, s_wh, s_run);
+        return;
+    }
     uint32_t *v = vals + r.x;
     if (L <= (uint32_t)kShortThreads) {
         // one entry per thread, ranked by counting: entry i goes to
@@ -454,10 +466,12 @@ void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32
 }
 
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
-                         const uint32_t *dkey, hipStream_t st) {
+                         const uint32_t *dkey, bool long_lists, hipStream_t st) {
     if (n_tiles <= 0) return;
-    segment_sort_long_kernel<<<n_tiles, kLongThreads, 0, st>>>(ranges, vals, tmp, dkey);
-    segment_sort_short_kernel<<<n_tiles, kShortThreads, 0, st>>>(ranges, vals, dkey);
+    if (long_lists)
+        segment_sort_long_kernel<<<n_tiles, kLongThreads, 0, st>>>(ranges, vals, tmp, dkey);
+    segment_sort_short_kernel<<<n_tiles, kShortThreads, 0, st>>>(ranges, vals, tmp, dkey,
+                                                                 long_lists ? 1 : 0);
 }
 
 }  // namespace tgs

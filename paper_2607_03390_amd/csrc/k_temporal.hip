@@ -19,14 +19,12 @@ namespace tgs {
 
 namespace {
 
-__global__ __launch_bounds__(256) void temporal_init_kernel(int n_px, int n_tiles, float *dmin,
-                                                            float *smax, uint8_t *oc) {
+__global__ __launch_bounds__(256) void temporal_init_kernel(int n_px, float *dmin, float *smax) {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k < n_px) {
         dmin[k] = kNoHit;
         smax[k] = 0.0f;
     }
-    if (k < n_tiles) oc[k] = 0;
 }
 
 __global__ __launch_bounds__(256) void forward_warp_kernel(WarpK w, const float *__restrict__ D,
@@ -56,15 +54,22 @@ __global__ __launch_bounds__(256) void forward_warp_kernel(WarpK w, const float 
 
 // One block of tp x tp threads per tile (tp = 16 on the image, 8 on the
 // half-resolution geometry-buffer grid, where a tile is 8 x 8 cells).
+// The block also clears its tile's occluded flag for this frame and resets
+// its cells of the other warp pair (dmin_next, smax_next) for the next one.
 __global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *__restrict__ dmin,
-                                                         float *dfill, float2 *uv, uint8_t *um) {
+                                                         float *dfill, float2 *uv, uint8_t *um,
+                                                         uint8_t *oc, float *dmin_next,
+                                                         float *smax_next) {
     const int tile = blockIdx.x;
     const int tx = tile % w.TX, ty = tile / w.TX;
     const int px = tx * w.tp + (int)(threadIdx.x % (unsigned)w.tp);
     const int py = ty * w.tp + (int)(threadIdx.x / (unsigned)w.tp);
     int bad = 0;
+    if (threadIdx.x == 0) oc[tile] = 0;
     if (px < w.W && py < w.H) {
         const int q = py * w.W + px;
+        dmin_next[q] = kNoHit;
+        smax_next[q] = 0.0f;
         float d = dmin[q];
         if (d == kNoHit && px >= 1 && py >= 1 && px <= w.W - 2 && py <= w.H - 2) {
             const float *r0 = dmin + (size_t)(py - 1) * w.W + px;
@@ -340,11 +345,8 @@ void fill(T *p, size_t n, T v, hipStream_t st) {
 
 }  // namespace
 
-void launch_temporal_init(int n_px, int n_tiles, float *dmin, float *smax, uint8_t *oc,
-                          Counters *cnt, hipStream_t st) {
-    const int n = n_px > n_tiles ? n_px : n_tiles;
-    temporal_init_kernel<<<(n + 255) / 256, 256, 0, st>>>(n_px, n_tiles, dmin, smax, oc);
-    (void)cnt;
+void launch_temporal_init(int n_px, float *dmin, float *smax, hipStream_t st) {
+    if (n_px > 0) temporal_init_kernel<<<(n_px + 255) / 256, 256, 0, st>>>(n_px, dmin, smax);
 }
 
 void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *dmin, float *smax,
@@ -354,8 +356,9 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
 }
 
 void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
-                       hipStream_t st) {
-    fill_query_kernel<<<w.TX * w.TY, w.tp * w.tp, 0, st>>>(w, dmin, dfill, uv, um);
+                       uint8_t *oc, float *dmin_next, float *smax_next, hipStream_t st) {
+    fill_query_kernel<<<w.TX * w.TY, w.tp * w.tp, 0, st>>>(w, dmin, dfill, uv, um, oc, dmin_next,
+                                                           smax_next);
 }
 
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,

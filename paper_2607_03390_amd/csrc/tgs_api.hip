@@ -337,7 +337,15 @@ struct tgs_state {
     int Wg = 0, Hg = 0;               // grid of the geometry buffer (image / tgb_downscale)
     tgs_params p{};
     Workspace ws;
-    DevBuf tgb_d, tgb_s, tab, g_flag, fbox, dmin, smax, dfill, uv, um, oc;
+    DevBuf tgb_d, tgb_s, tab, g_flag, fbox, dfill, uv, um, oc;
+    // forward-warp targets (Eq. 3), two pairs: a frame warps into pair
+    // warp_next while its fill / query kernel resets the other pair for the
+    // next frame, so no launch of its own clears them (warp_clean: pair
+    // warp_next holds its initial values; warp_last: the pair of the last
+    // frame, for the debug dumps)
+    DevBuf dmin[2], smax[2];
+    int warp_next = 0, warp_last = 0;
+    bool warp_clean = false;
     int frame_index = 0, since_true = 0, since_ref = 0, force_pseudo = 0, has_ref = 0;
     float fbox_host[4] = {0, 0, 0, 0};
     float ref_w2c[16] = {0};
@@ -488,9 +496,12 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     if (ws.frame_seg) {
         // each tile's list, emitted in index order, by (depth bits, index)
         ProfScope ps(TGS_PROF_SORT, st);
+        // lists of 1024 entries and more get a launch of their own when a
+        // recent frame had any (the longest list's bucket, from the host copy)
+        const uint32_t maxb = *reinterpret_cast<volatile uint32_t *>(ws.host_maxb);
         launch_segment_sort(TX * TY, ws.ranges.as<uint2>(), svals,
                             alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
-                            ws.dkey.as<uint32_t>(), st);
+                            ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, st);
         TGS_LAUNCHED("per-tile sort");
     }
     {
@@ -825,8 +836,10 @@ tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
     if (st == TGS_OK) st = s->tab.ensure(3 * px * 4);
     if (st == TGS_OK) st = s->g_flag.ensure(nn);
     if (st == TGS_OK) st = s->fbox.ensure((4 + 4 * kAfcPartials) * sizeof(int));
-    if (st == TGS_OK) st = s->dmin.ensure(pg * 4);
-    if (st == TGS_OK) st = s->smax.ensure(pg * 4);
+    for (int b = 0; b < 2; ++b) {
+        if (st == TGS_OK) st = s->dmin[b].ensure(pg * 4);
+        if (st == TGS_OK) st = s->smax[b].ensure(pg * 4);
+    }
     if (st == TGS_OK) st = s->dfill.ensure(pg * 4);
     if (st == TGS_OK) st = s->uv.ensure(pg * 8);
     if (st == TGS_OK) st = s->um.ensure(nt);
@@ -908,26 +921,33 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                 wg.H = s->Hg;
                 wg.tp = kTile / 2;
             }
+            const int wb = s->warp_next;
+            float *dmin = s->dmin[wb].as<float>(), *smax = s->smax[wb].as<float>();
             {
                 ProfScope ps(TGS_PROF_WARP, st);
-                launch_temporal_init(s->Wg * s->Hg, nt, s->dmin.as<float>(), s->smax.as<float>(),
-                                     s->oc.as<uint8_t>(), ws.cnt.as<Counters>(), st);
-                launch_forward_warp(wg, s->tgb_d.as<float>(), s->tgb_s.as<float>(), s->dmin.as<float>(),
-                                    s->smax.as<float>(), st);
+                if (!s->warp_clean) launch_temporal_init(s->Wg * s->Hg, dmin, smax, st);
+                s->warp_clean = false;
+                launch_forward_warp(wg, s->tgb_d.as<float>(), s->tgb_s.as<float>(), dmin, smax, st);
                 TGS_LAUNCHED("warp");
             }
             {
                 ProfScope ps(TGS_PROF_FILL_QUERY, st);
-                launch_fill_query(wg, s->dmin.as<float>(), s->dfill.as<float>(), s->uv.as<float2>(),
-                                  s->um.as<uint8_t>(), st);
+                // also clears the occluded-tile flags of this frame and resets
+                // the other warp pair for the next one
+                launch_fill_query(wg, dmin, s->dfill.as<float>(), s->uv.as<float2>(),
+                                  s->um.as<uint8_t>(), s->oc.as<uint8_t>(),
+                                  s->dmin[wb ^ 1].as<float>(), s->smax[wb ^ 1].as<float>(), st);
                 TGS_LAUNCHED("fill query");
+                s->warp_last = wb;
+                s->warp_next = wb ^ 1;
+                s->warp_clean = true;
             }
             CullK cull = no_cull(p.z_near, ws);
             cull.afc = p.enable_afc;
             cull.fbox = s->fbox.as<int>();
             cull.toc = p.enable_toc;
-            cull.dmin = s->dmin.as<float>();
-            cull.smax = s->smax.as<float>();
+            cull.dmin = dmin;
+            cull.smax = smax;
             cull.g_rendered = s->g_flag.as<uint8_t>();
             cull.lambda1 = p.lambda1;
             cull.lambda2 = p.lambda2;
@@ -1167,8 +1187,8 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
         default:
             if (!state) return fail(TGS_ERR_INVALID_ARG, "this buffer exists only for a state");
             switch (what) {
-                case TGS_DUMP_WARP_DEPTH: src = state->dmin.p; size = pg * 4; break;
-                case TGS_DUMP_WARP_SIGMA: src = state->smax.p; size = pg * 4; break;
+                case TGS_DUMP_WARP_DEPTH: src = state->dmin[state->warp_last].p; size = pg * 4; break;
+                case TGS_DUMP_WARP_SIGMA: src = state->smax[state->warp_last].p; size = pg * 4; break;
                 case TGS_DUMP_FILLED_DEPTH: src = state->dfill.p; size = pg * 4; break;
                 case TGS_DUMP_CORRESPONDENCE: src = state->uv.p; size = pg * 8; break;
                 case TGS_DUMP_UNMATCHED: src = state->um.p; size = nt; break;

@@ -201,8 +201,13 @@ void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32
                        uint32_t *part, uint32_t *vidx, uint32_t *voffs, Counters *cnt,
                        uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
                        uint32_t tag, hipStream_t st);
+// long_lists: lists above 1024 entries are expected (a launch of their own
+// for them); otherwise the few there are take a slower in-block path.
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
-                         const uint32_t *dkey, hipStream_t st);
+                         const uint32_t *dkey, bool long_lists, hipStream_t st);
+// Length bucket (floor(log2 len) + 1) from which a recent frame's lists make
+// the long-list launch worth its cost: lists of 1024 entries and more.
+constexpr int kSegLongBucket = 11;
 // Longest list the per-tile sort handles in LDS; longer ones take its slower
 // in-block path.  Lists of bucket <= kSegBucketMax (floor(log2 len) + 1)
 // fit.
@@ -261,12 +266,14 @@ void launch_afc_bounds(int n, const uint8_t *g_flag, const float4 *g, int W, int
                        hipStream_t st);
 
 // ---- launchers (k_temporal.hip) ----
-void launch_temporal_init(int n_px, int n_tiles, float *dmin, float *smax, uint8_t *oc,
-                          Counters *cnt, hipStream_t st);
+// dmin = empty depth, smax = 0 over n_px cells
+void launch_temporal_init(int n_px, float *dmin, float *smax, hipStream_t st);
 void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *dmin, float *smax,
                          hipStream_t st);
+// Also oc[tile] = 0 and dmin_next / smax_next reset to their initial values
+// (the other warp pair, for the next frame).
 void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
-                       hipStream_t st);
+                       uint8_t *oc, float *dmin_next, float *smax_next, hipStream_t st);
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
                      const ushort4 *rect, uint8_t *oc, hipStream_t st);
 // sel_list: the selected tiles ascending in [0, n_selected), the others

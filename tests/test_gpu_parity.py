@@ -125,6 +125,23 @@ def test_long_tile_lists(sort_path):
     _full_parity(sc, [cam], label="long lists")
 
 
+def test_long_lists_after_short_ones(sort_path):
+    """Long lists in a frame after one whose lists were all short: the
+    per-tile sort then has no launch for long lists and sorts them in its
+    short-list kernel over global memory."""
+    sc = synth.scene_uniform_cube(24_000, 11, degree=0, log_scale_mean=-2.6)
+    # the first camera looks away from the cube at a corner of it
+    away = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (6.0, -14.0, 0.5)), 48, 40)
+    near = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (0, 0, 0)), 48, 40)
+    lengths = []
+    for cam in (away, near):
+        ts, _ = O.tile_lists(O.gaussians(sc, cam), *cam.tiles)
+        lengths.append(int(np.diff(ts).max()))
+    log(f"    longest tile lists {lengths}")
+    assert lengths[0] < 1024 and lengths[1] > 4096
+    _full_parity(sc, [away, near], label="long after short")
+
+
 def test_full_parity_object_subset():
     w = synth.workload("object", n_gaussians=40_000)
     _full_parity(w.scene, [w.cameras[0], w.cameras[37]], label="object 40k")
