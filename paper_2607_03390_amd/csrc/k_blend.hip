@@ -35,7 +35,7 @@ __device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) 
 __device__ inline bool wave_all(bool p) { return __builtin_amdgcn_ballot_w64(!p) == 0ull; }
 
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
-__global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void blend_kernel(BlendArgs a) {
     // Staged per Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
     // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares,
     // by the preprocess) so that log2 of the Gaussian falloff is a three-FMA
@@ -86,12 +86,14 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
     bool pivot = false;
-    bool done = !inside;
+    // stopped lanes as a wave mask on scalar registers (lanes outside the
+    // image start stopped): tested and updated without vector instructions
+    uint64_t done = __builtin_amdgcn_ballot_w64(!inside);
     uint32_t stop_pos = range.y;   // list position of the stopping Gaussian (+1 below)
     uint32_t n_hit = 0;            // pairs with alpha >= 1/255 before the pixel stopped
 
     for (uint32_t b = range.x; b < range.y; b += 256) {
-        if (__syncthreads_count(done) == 256) break;
+        if (__syncthreads_and(done == ~0ull)) break;
         const uint32_t k = b + tid;
         uint32_t lists = 0;   // bit L: the staged Gaussian meets sub-block L
         if (k < range.y) {
@@ -159,7 +161,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             max(max(s_len[4 * wave], s_len[4 * wave + 1]), max(s_len[4 * wave + 2], s_len[4 * wave + 3])));
         __syncthreads();
         // a wave whose pixels have all stopped skips the batch
-        const uint32_t n_run = wave_all(done) ? 0u : n_long;
+        const uint32_t n_run = done == ~0ull ? 0u : n_long;
         for (uint32_t e = 0; e < n_run; ++e) {
             const uint32_t j = s_list[my_list][e];
             const uint32_t jo = j << 4;   // byte offset into the staged arrays
@@ -171,19 +173,24 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
             const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
             const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
             // composited or stopping: a live entry of a running pixel with
-            // power <= 0 and alpha >= 1/255
-            const bool hit = live && !done && !(p2 > 0.0f) && alpha >= kAlphaMin;
+            // power <= 0 and alpha >= 1/255.  The decisions are wave masks
+            // (compares straight into scalar registers, combined there)
+            const uint64_t hitm = __builtin_amdgcn_ballot_w64(live) &
+                                  __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
+                                  __builtin_amdgcn_ballot_w64(alpha >= kAlphaMin) & ~done;
             const float Tn = T * (1.0f - alpha);
-            const bool keep = Tn >= kTMin;   // T stays above 1e-4 (Tn is never NaN)
-            const bool inc = hit && keep;
-            const bool stop = hit && !keep;
+            // T stays above 1e-4 (Tn is never NaN)
+            const uint64_t keepm = __builtin_amdgcn_ballot_w64(Tn >= kTMin);
+            const bool hit = __builtin_amdgcn_inverse_ballot_w64(hitm);
+            const bool inc = __builtin_amdgcn_inverse_ballot_w64(hitm & keepm);
+            const bool stop = __builtin_amdgcn_inverse_ballot_w64(hitm & ~keepm);
             const float w = inc ? alpha * T : 0.0f;
             const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_col) + jo);
             cr = __builtin_fmaf(w, c.x, cr);
             cg = __builtin_fmaf(w, c.y, cg);
             cb = __builtin_fmaf(w, c.z, cb);
             T = inc ? Tn : T;
-            done = done || stop;
+            done |= hitm & ~keepm;
             if (COUNT) {
                 n_hit += hit ? 1u : 0u;
                 if (stop) stop_pos = b + j;
@@ -209,7 +216,7 @@ __global__ __launch_bounds__(256) void blend_kernel(BlendArgs a) {
                                   __float_as_uint(mw));
                 }
             }
-            if (wave_all(done)) break;
+            if (done == ~0ull) break;
         }
         __syncthreads();
         if (CAPTURE && a.g_flag && k < range.y && s_flag[tid]) a.g_flag[s_idx[tid]] = 1u;
