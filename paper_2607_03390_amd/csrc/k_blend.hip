@@ -6,9 +6,10 @@
 //
 // One 256-thread block (four wave64s, one per 8x8 quadrant, each as four
 // 16-lane groups on 4x4 sub-blocks) per 16x16 tile, one pixel per thread.
-// The tile's sorted Gaussians are staged through LDS in batches of 256
-// records (48 bytes each, one coalesced gather per thread); every wave then
-// reads each record as an LDS broadcast.  A pixel stops at the Gaussian that
+// The tile's sorted Gaussians are staged through LDS in batches of 255
+// records (48 bytes each, one coalesced gather per thread; the 256th slot is
+// a sentinel that pads the lists); every wave then reads each record as an
+// LDS broadcast.  A pixel stops at the Gaussian that
 // would take its transmittance below 1e-4; the block leaves as soon as all
 // 256 pixels have stopped.  The work is VALU-bound (one exp and ~25 lane-ops
 // per pixel-Gaussian pair).
@@ -29,6 +30,8 @@
 namespace tgs {
 
 namespace {
+
+constexpr int kBatch = 255;   // Gaussians staged per batch (slot 255: the sentinel)
 
 // Wave votes on the execution mask itself (no 0/1 vector temporaries).
 __device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
@@ -52,7 +55,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     // 16-lane groups, one per sub-block, and every iteration advances all
     // four lists at once: a footprint a few pixels wide meets a 4x4 block
     // about 60 % as often as the 8x8 quadrant.
-    __shared__ uint8_t s_list[16][256];
+    __shared__ __align__(16) uint8_t s_list[16][256];
     __shared__ uint32_t s_cnt[4][16];      // [staging wave][list] entries, then starts
     __shared__ uint32_t s_len[16];         // list lengths
 
@@ -75,13 +78,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     const int py = ty * kTile + 8 * (wave >> 1) + 4 * (grp >> 1) + ((lane >> 2) & 3);
     const int my_list = 4 * wave + grp;
     const bool inside = px < a.W && py < a.H;
-    const float fpx = (float)px, fpy = (float)py;
+    float fpx = (float)px, fpy = (float)py;
+    // kept in registers through the loops (cheaper than converting them
+    // again in every iteration, which the register allocator would prefer)
+    __asm__ volatile("" : "+v"(fpx), "+v"(fpy));
     const float tile_x0 = (float)(tx * kTile), tile_y0 = (float)(ty * kTile);
     const uint2 range = a.ranges[tile];
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-    // entries past a list's end are read too (and masked): zeroed lists make
-    // them name slot 0, which every non-empty batch stages
-    for (int k = tid; k < 16 * 256 / 4; k += 256) reinterpret_cast<uint32_t *>(&s_list[0][0])[k] = 0u;
 
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;
@@ -92,11 +95,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     uint32_t stop_pos = range.y;   // list position of the stopping Gaussian (+1 below)
     uint32_t n_hit = 0;            // pairs with alpha >= 1/255 before the pixel stopped
 
-    for (uint32_t b = range.x; b < range.y; b += 256) {
+    // Batches of 255 Gaussians in slots 0..254; slot 255 holds a sentinel
+    // (opacity 0, conic 0: alpha 0 at every pixel) that pads every list, so
+    // entries past a list's end need no test of their own.
+    for (uint32_t b = range.x; b < range.y; b += kBatch) {
         if (__syncthreads_and(done == ~0ull)) break;
+        reinterpret_cast<uint4 *>(&s_list[0][0])[tid] =
+            make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
         const uint32_t k = b + tid;
         uint32_t lists = 0;   // bit L: the staged Gaussian meets sub-block L
-        if (k < range.y) {
+        if (tid == kBatch) {
+            s_g0[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s_g1[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s_col[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s_idx[tid] = 0;
+        } else if (k < range.y) {
             const int idx = (int)a.vals[k];
             const float4 *r = a.g + 4 * (size_t)idx;
             const float4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
@@ -154,9 +167,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
             if ((lists >> L) & 1u)
                 s_list[L][(uint32_t)__popcll(bal & lt_mask) + s_cnt[wave][L]] = (uint8_t)tid;
         }
-        // this lane's list length, and the wave's trip count (its longest
-        // list; the same for every lane: kept on scalar registers)
-        const uint32_t n_mine = s_len[my_list];
+        // the wave's trip count: its longest list (the same for every lane:
+        // kept on scalar registers; shorter lists are padded)
         const uint32_t n_long = __builtin_amdgcn_readfirstlane(
             max(max(s_len[4 * wave], s_len[4 * wave + 1]), max(s_len[4 * wave + 2], s_len[4 * wave + 3])));
         __syncthreads();
@@ -165,18 +177,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         for (uint32_t e = 0; e < n_run; ++e) {
             const uint32_t j = s_list[my_list][e];
             const uint32_t jo = j << 4;   // byte offset into the staged arrays
-            const bool live = e < n_mine;
             const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g0) + jo);
             const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g1) + jo);
             const float dx = g0.x - fpx, dy = g0.y - fpy;
             // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
             const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
             const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
-            // composited or stopping: a live entry of a running pixel with
-            // power <= 0 and alpha >= 1/255.  The decisions are wave masks
+            // composited or stopping: an entry of a running pixel with power
+            // <= 0 and alpha >= 1/255.  The decisions are wave masks
             // (compares straight into scalar registers, combined there)
-            const uint64_t hitm = __builtin_amdgcn_ballot_w64(live) &
-                                  __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
+            const uint64_t hitm = __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
                                   __builtin_amdgcn_ballot_w64(alpha >= kAlphaMin) & ~done;
             const float Tn = T * (1.0f - alpha);
             // T stays above 1e-4 (Tn is never NaN)
@@ -203,9 +213,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                 sw += w;
                 s1 = __builtin_fmaf(w, dd, s1);
                 s2 = __builtin_fmaf(w * dd, dd, s2);
-                // w > 0 exactly where the pixel composites (alpha, T > 0);
-                // the lanes of a group write the same flag
-                if (w > 0.0f) s_flag[j] = 1u;
+                // the pixel composites the Gaussian (w = alpha T > 0); the
+                // lanes of a group write the same flag
+                if (inc) s_flag[j] = 1u;
                 if (CONTRIB) {
                     // max weight over the group's 16 lanes (one Gaussian)
                     float mw = w;
@@ -219,7 +229,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
             if (done == ~0ull) break;
         }
         __syncthreads();
-        if (CAPTURE && a.g_flag && k < range.y && s_flag[tid]) a.g_flag[s_idx[tid]] = 1u;
+        if (CAPTURE && a.g_flag && tid < kBatch && k < range.y && s_flag[tid])
+            a.g_flag[s_idx[tid]] = 1u;
     }
 
     if (COUNT) {
