@@ -40,7 +40,10 @@ BLEND_OPS_PER_HIT = {"blend_ref": 24, "blend_tgs": 19, "blend_full": 19}
 # non-packed fp32 VALU issue rate: 256 CUs x 64 lanes x 2.4 GHz
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "blend_traffic_room.json")
-BLEND_SRC = os.path.join(ROOT, "paper_2607_03390_amd", "csrc", "k_blend.hip")
+# sources the blend kernel is compiled from (its traffic counters are valid
+# for these exact files)
+BLEND_SRCS = [os.path.join(ROOT, "paper_2607_03390_amd", "csrc", f)
+              for f in ("k_blend.hip", "stitch.h", "tgs_internal.h")]
 
 
 def log(msg):
@@ -74,7 +77,10 @@ def parse():
 
 
 def kernel_source_hash():
-    return hashlib.sha256(open(BLEND_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in BLEND_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def main():
