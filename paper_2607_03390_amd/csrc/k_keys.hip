@@ -63,17 +63,17 @@ __device__ inline uint32_t key_tile(uint32_t r, ushort4 rc, const uint32_t *rowp
 // consecutive positions across the block (coalesced stores), whatever the
 // Gaussians' key counts: a Gaussian spanning thousands of tiles is spread
 // over many blocks instead of holding one wave.  The owner of the block's
-// first key comes from a 64-way search over the sorted offsets (four rounds
-// of one wave load for a million Gaussians); the Gaussians starting inside
-// the block mark their first position in LDS and an inclusive max-scan gives
-// every position its owner.  Past the key capacity (cnt->n_sorted == 0 with
-// keys) nothing is emitted: the host grows the buffers and renders the frame
-// again.
-constexpr int kDupKeys = 1024;
+// first key comes from the key-block table written with the offsets; the
+// Gaussians starting inside the block mark their first position in LDS and
+// an inclusive max-scan gives every position its owner.  Past the key
+// capacity (cnt->n_sorted == 0 with keys) nothing is emitted: the host grows
+// the buffers and renders the frame again.
+constexpr int kDupKeys = kKeyBlock;
 
 __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
                                                         const uint32_t *__restrict__ didx,
                                                         const uint32_t *__restrict__ offs,
+                                                        const uint32_t *__restrict__ kfirst,
                                                         const ushort4 *__restrict__ rect,
                                                         const uint32_t *rowpre, const int *sel_cols,
                                                         int TX, int n_tiles, uint32_t *tkey,
@@ -82,7 +82,6 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
     __shared__ uint32_t s_off[kDupKeys + 1];    // offsets of window Gaussians j0 + k
     __shared__ uint32_t s_g[kDupKeys + 1];      // their Gaussian indices
     __shared__ int s_wmax[4];
-    __shared__ uint32_t s_j0;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int t = blockIdx.x * blockDim.x + tid; t < n_tiles; t += gridDim.x * blockDim.x)
         ranges[t] = make_uint2(0u, 0u);
@@ -90,22 +89,9 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
     const uint32_t P0 = blockIdx.x * (uint32_t)kDupKeys;
     if (K == 0u || P0 >= K) return;   // block-uniform
     const uint32_t P1 = K - P0 < (uint32_t)kDupKeys ? K : P0 + kDupKeys;
-    if (wave == 0) {
-        // last j < V with offs[j] <= P0 (offs increases strictly from offs[0] = 0)
-        uint32_t lo = 0, n = V;
-        while (n > 1) {
-            const uint32_t step = (n + 63) / 64;
-            const uint32_t j = lo + (uint32_t)lane * step;
-            const uint64_t m = __ballot(j < lo + n && offs[j] <= P0);
-            const uint32_t nlo = lo + (63u - (uint32_t)__clzll(m)) * step;   // lane 0 is set
-            n = step < lo + n - nlo ? step : lo + n - nlo;
-            lo = nlo;
-        }
-        if (lane == 0) s_j0 = lo;
-    }
     for (int k = tid; k < kDupKeys; k += 256) s_owner[k] = -1;
+    const uint32_t j0 = kfirst[blockIdx.x];   // owner of key P0 (offs[j0] <= P0)
     __syncthreads();
-    const uint32_t j0 = s_j0;
     // at most 1024 Gaussians after j0 start inside the block's keys
     for (int k = tid; k <= kDupKeys; k += 256) {
         const uint32_t j = j0 + (uint32_t)k;
@@ -210,39 +196,48 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
     const int n = n_dev ? (int)*n_dev : n_host;
     if (tid < 33) s_cnt[tid] = 0u;
     __syncthreads();
+    // up to 8192 tiles (one round) the tiles and buckets stay in registers
+    // between the counting and the placing pass; more take a second load
+    const bool one_round = n <= kPer * 1024;
+    int t[kPer];
+    uint32_t bk[kPer];
+    bool act[kPer];
     // every lane runs every round (bounds are block-uniform) so that the
     // wave-level aggregation sees the whole wave
     for (int pass = 0; pass < 2; ++pass) {
         for (int c0 = 0; c0 < n; c0 += kPer * 1024) {
-            int t[kPer];
-            uint32_t b[kPer];
-            bool act[kPer];
+            if (pass == 0 || !one_round) {
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const int i = c0 + k * 1024 + tid;
-                act[k] = i < n;
-                t[k] = act[k] ? (tile_in ? tile_in[i] : i) : 0;
+                for (int k = 0; k < kPer; ++k) {
+                    const int i = c0 + k * 1024 + tid;
+                    act[k] = i < n;
+                    t[k] = act[k] ? (tile_in ? tile_in[i] : i) : 0;
+                }
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) bk[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
             }
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) b[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
-#pragma unroll
             for (int k = 0; k < kPer; ++k) {
-                const uint32_t slot = wave_bucket_add(s_cnt, b[k], act[k]);
-                if (pass == 1 && act[k]) tile_out[slot] = t[k];
+                if (pass == 0) {
+                    if (act[k]) atomicAdd(&s_cnt[bk[k]], 1u);
+                } else {
+                    const uint32_t slot = wave_bucket_add(s_cnt, bk[k], act[k]);
+                    if (act[k]) tile_out[slot] = t[k];
+                }
             }
         }
         __syncthreads();
         if (pass == 0 && tid < 64) {
             // bucket starts, longest lists first: lane l holds bucket 32 - l
-            const int bk = 32 - tid;
-            const uint32_t c = bk >= 0 ? s_cnt[bk] : 0u;
+            const int b = 32 - tid;
+            const uint32_t c = b >= 0 ? s_cnt[b] : 0u;
             uint32_t inc = c;
 #pragma unroll
             for (int d = 1; d < 64; d <<= 1) {
                 const uint32_t o = __shfl_up(inc, d);
                 if (tid >= d) inc += o;
             }
-            if (bk >= 0) s_cnt[bk] = inc - c;
+            if (b >= 0) s_cnt[b] = inc - c;
             const uint64_t nz = __ballot(c != 0u);
             // the host reads this value some frames later: no fence needed
             if (max_bucket && tid == 0)
@@ -256,16 +251,16 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
 }  // namespace
 
 void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
-                      const uint32_t *offs, const ushort4 *rect, const uint32_t *rowpre,
-                      const int *sel_cols, int TX, int n_tiles, uint32_t *tkey, uint32_t *tval,
-                      uint2 *ranges, hipStream_t st) {
+                      const uint32_t *offs, const uint32_t *kfirst, const ushort4 *rect,
+                      const uint32_t *rowpre, const int *sel_cols, int TX, int n_tiles,
+                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st) {
     if (n <= 0 || cap == 0) {
         ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
         return;
     }
     const uint32_t blocks = (cap + kDupKeys - 1) / kDupKeys;
-    duplicate_kernel<<<blocks, 256, 0, st>>>(cnt, didx, offs, rect, rowpre, sel_cols, TX, n_tiles,
-                                             tkey, tval, ranges);
+    duplicate_kernel<<<blocks, 256, 0, st>>>(cnt, didx, offs, kfirst, rect, rowpre, sel_cols, TX,
+                                             n_tiles, tkey, tval, ranges);
 }
 
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,

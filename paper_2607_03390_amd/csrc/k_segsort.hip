@@ -153,8 +153,8 @@ __device__ inline void block_sum_pairs(const uint2 *v, int m, unsigned long long
 // frame's totals to the device counters and, tag last, to the host.
 __global__ __launch_bounds__(kScanThreads) void count_emit_kernel(
     int n, int nb, const uint32_t *count, const uint32_t *part, uint32_t *vidx, uint32_t *voffs,
-    const uint32_t *pre_partial, int n_pre, Counters *cnt, HostCounters *host, uint32_t tag,
-    uint32_t cap) {
+    uint32_t *kfirst, const uint32_t *pre_partial, int n_pre, Counters *cnt, HostCounters *host,
+    uint32_t tag, uint32_t cap) {
     __shared__ uint32_t s_w[4];
     __shared__ unsigned long long s_k[4];
     const int tid = threadIdx.x;
@@ -181,6 +181,7 @@ __global__ __launch_bounds__(kScanThreads) void count_emit_kernel(
             if (c[k]) {
                 vidx[on] = (uint32_t)(base + k);
                 voffs[on] = ok;
+                mark_key_blocks(kfirst, (uint32_t)key_blocks(cap), on, ok, c[k]);
                 ++on;
                 ok += c[k];
             }
@@ -453,16 +454,16 @@ __global__ __launch_bounds__(kLongThreads) void segment_sort_long_kernel(const u
 int count_scan_blocks(int n) { return (n + kScanBlock - 1) / kScanBlock; }
 
 void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, Counters *cnt,
-                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
-                       uint32_t tag, hipStream_t st) {
+                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, uint32_t *kfirst,
+                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
+                       HostCounters *host, uint32_t tag, hipStream_t st) {
     const int nb = count_scan_blocks(n > 0 ? n : 0);
     if (nb > 0)
         count_partials_kernel<<<nb, kScanThreads, 0, st>>>(n, count, rect, rowpre, TX, part);
     // at least one block: the last one publishes the counters
     count_emit_kernel<<<nb > 0 ? nb : 1, kScanThreads, 0, st>>>(n, nb, count, part, vidx, voffs,
-                                                                pre_partial, n_pre, cnt, host, tag,
-                                                                cap);
+                                                                kfirst, pre_partial, n_pre, cnt,
+                                                                host, tag, cap);
 }
 
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,

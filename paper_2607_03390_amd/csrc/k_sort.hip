@@ -30,8 +30,8 @@
 //    keys over the selected tiles of its rectangle;
 //  - the last pass also carries each Gaussian's key count as a weight and
 //    writes, at each sorted position, the exclusive prefix of the weights:
-//    where the Gaussian's tile keys start.  It publishes the frame's
-//    counters to the host.
+//    where the Gaussian's tile keys start, and the owner of every 1024-key
+//    block of the emission.  It publishes the frame's counters to the host.
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -84,6 +84,7 @@ struct DepthIo {
     const uint32_t *rowpre;     // the rectangles and the tile mask's row prefix
     int TX;                     // sums (rowpre NULL: count is final)
     uint32_t *offs;             // last pass: start of each sorted Gaussian's keys
+    uint32_t *kfirst;           // last pass: owner of each key block (key_blocks(cap))
     Counters *cnt;
     HostCounters *host;         // last pass: the frame's counters, tag last
     uint32_t tag, cap;
@@ -270,6 +271,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     __shared__ uint32_t s_scan[4];
     __shared__ uint64_t s_scan64[4];
     __shared__ uint32_t s_nvalid;
+    __shared__ uint32_t s_wtot;   // last pass: the block's weight total
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t K = MODE == kFirst ? n_host : key_count(n_dev, n_host);
@@ -389,13 +391,15 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
             w[j] = p < nv ? s_wt[p] : 0u;
             sum += w[j];
         }
-        uint32_t o = block_exclusive_scan256<uint32_t>(sum, s_scan);
+        uint32_t wtot;
+        uint32_t o = block_exclusive_scan256<uint32_t>(sum, s_scan, &wtot);
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
             const uint32_t p = (uint32_t)tid * IPT + j;
             if (p < nv) s_wt[p] = o;
             o += w[j];
         }
+        if (tid == 0) s_wtot = wtot;
         __syncthreads();
     }
 
@@ -404,7 +408,11 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         const uint32_t dj = (kk >> shift) & 255u;
         const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
         if (MODE == kLast) {
-            io.offs[out] = s_wbase[dj] + (s_wt[i] - s_wt[s_dstart[dj]]);
+            const uint32_t o = s_wbase[dj] + (s_wt[i] - s_wt[s_dstart[dj]]);
+            io.offs[out] = o;
+            // the Gaussian's key count is its weight: the next prefix minus this one
+            const uint32_t c = (i + 1 < nv ? s_wt[i + 1] : s_wtot) - s_wt[i];
+            mark_key_blocks(io.kfirst, (uint32_t)key_blocks(io.cap), out, o, c);
         } else {
             kout[out] = kk;
         }
@@ -484,15 +492,16 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
 
 void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
                        const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
-                       uint32_t *v_b, uint32_t *offs, uint32_t *scratch, Counters *cnt,
-                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
-                       uint32_t tag, hipStream_t st) {
+                       uint32_t *v_b, uint32_t *offs, uint32_t *kfirst, uint32_t *scratch,
+                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
+                       HostCounters *host, uint32_t tag, hipStream_t st) {
     DepthIo io;
     io.count = count;
     io.rect = rect;
     io.rowpre = rowpre;
     io.TX = TX;
     io.offs = offs;
+    io.kfirst = kfirst;
     io.cnt = cnt;
     io.host = host;
     io.tag = tag;

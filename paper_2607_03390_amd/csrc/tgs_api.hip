@@ -78,7 +78,7 @@ struct DevBuf {
 struct Workspace {
     DevBuf g, rect, status, count, partial;
     DevBuf dkey, didx, dkey_alt, didx_alt, offs;
-    DevBuf tkey, tval, tkey_alt, tval_alt, sort;
+    DevBuf tkey, tval, tkey_alt, tval_alt, sort, kfirst;
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
     HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
     HostCounters *host_cnt_dev = nullptr; // its device-side address
@@ -154,6 +154,7 @@ struct Workspace {
             TGS_TRY(tval.ensure(cap * sizeof(uint32_t)));
             TGS_TRY(tkey_alt.ensure(cap * sizeof(uint32_t)));
             TGS_TRY(tval_alt.ensure(cap * sizeof(uint32_t)));
+            TGS_TRY(kfirst.ensure(key_blocks(cap) * sizeof(uint32_t)));
             key_cap = cap;
         }
         const size_t nn = (size_t)(n > 0 ? n : 1);
@@ -397,7 +398,7 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
         ws.seq += 1;
         uint32_t *part = ws.sort.as<uint32_t>();
         launch_count_scan(n, ws.count.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre, TX, part,
-                          ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
+                          ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(), ws.kfirst.as<uint32_t>(),
                           ws.cnt.as<Counters>(), (uint32_t)ws.key_cap, ws.partial.as<uint32_t>(),
                           n > 0 ? preprocess_blocks(n) : 0, ws.host_cnt_dev, ws.seq, st);
         TGS_LAUNCHED("count scan");
@@ -411,7 +412,8 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
                           ws.dkey.as<uint32_t>(),
                           ws.dkey_alt.as<uint32_t>(), ws.didx_alt.as<uint32_t>(),
                           ws.dkey.as<uint32_t>(), ws.didx.as<uint32_t>(), ws.offs.as<uint32_t>(),
-                          ws.sort.as<uint32_t>(), ws.cnt.as<Counters>(), (uint32_t)ws.key_cap,
+                          ws.kfirst.as<uint32_t>(), ws.sort.as<uint32_t>(), ws.cnt.as<Counters>(),
+                          (uint32_t)ws.key_cap,
                           ws.partial.as<uint32_t>(), n > 0 ? preprocess_blocks(n) : 0,
                           ws.host_cnt_dev, ws.seq, st);
         TGS_LAUNCHED("depth sort");
@@ -473,9 +475,9 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     Counters *cnt = ws.cnt.as<Counters>();
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
-        launch_duplicate(n, cap, cnt, didx, ws.offs.as<uint32_t>(), ws.rect.as<ushort4>(), rowpre,
-                         sel_cols, TX, TX * TY, ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(),
-                         ws.ranges.as<uint2>(), st);
+        launch_duplicate(n, cap, cnt, didx, ws.offs.as<uint32_t>(), ws.kfirst.as<uint32_t>(),
+                         ws.rect.as<ushort4>(), rowpre, sel_cols, TX, TX * TY,
+                         ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(), ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("duplicate");
     }
     int alt = 0;

@@ -145,15 +145,29 @@ void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Re
                        Counters *cnt, hipStream_t st);
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
+// Keys are emitted in blocks of kKeyBlock consecutive positions; kfirst[B]
+// (written by whichever kernel produces the key offsets) is the sorted
+// position of the Gaussian that owns key B * kKeyBlock, for every block below
+// the key capacity.
+constexpr int kKeyBlock = 1024;
+__host__ __device__ inline size_t key_blocks(size_t cap) { return (cap + kKeyBlock - 1) / kKeyBlock; }
+// Records, for a sorted Gaussian at position s with keys [o, o + c), s as
+// the owner of every key block that starts inside that range (below nb).
+__device__ inline void mark_key_blocks(uint32_t *kfirst, uint32_t nb, uint32_t s, uint64_t o,
+                                       uint32_t c) {
+    for (uint64_t b = (o + kKeyBlock - 1) / kKeyBlock; b < nb && b * kKeyBlock < o + c; ++b)
+        kfirst[b] = s;
+}
+
 // ---- launchers (k_keys.hip) ----
 // Emits the cnt->n_sorted keys of the cnt->n_visible depth-ordered Gaussians
 // (cap bounds n_sorted for the grid; nothing is emitted past the key
 // capacity) and clears the tile ranges (filled by launch_ranges after the
 // tile sort).  rowpre / sel_cols are NULL in frames that render every tile.
 void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
-                      const uint32_t *offs, const ushort4 *rect, const uint32_t *rowpre,
-                      const int *sel_cols, int TX, int n_tiles, uint32_t *tkey, uint32_t *tval,
-                      uint2 *ranges, hipStream_t st);
+                      const uint32_t *offs, const uint32_t *kfirst, const ushort4 *rect,
+                      const uint32_t *rowpre, const int *sel_cols, int TX, int n_tiles,
+                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
 // Ranges of the cnt->n_sorted tile-sorted keys; cap bounds n_sorted for the grid.
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
                    hipStream_t st);
@@ -180,14 +194,15 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int pa
 // v_b; k_b may alias dkey).  With rowpre (a selective-rendering frame) the
 // first pass first replaces count[i] by the masked count of rect[i].  Writes cnt->n_visible (Gaussians kept), the
 // sorted indices to v_b[0..n_visible), offs[s] = exclusive prefix of their
-// counts, then cnt->n_keys, cnt->n_sorted (n_keys if <= cap, else 0),
+// counts and the key-block owners kfirst[0 .. key_blocks(cap)), then
+// cnt->n_keys, cnt->n_sorted (n_keys if <= cap, else 0),
 // cnt->n_survivors / n_newly (from the preprocess partials) and, tag last,
 // the same counters to `host`.
 void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
                        const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
-                       uint32_t *v_b, uint32_t *offs, uint32_t *scratch, Counters *cnt,
-                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
-                       uint32_t tag, hipStream_t st);
+                       uint32_t *v_b, uint32_t *offs, uint32_t *kfirst, uint32_t *scratch,
+                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
+                       HostCounters *host, uint32_t tag, hipStream_t st);
 
 // ---- launchers (k_segsort.hip) ----
 // Per-tile depth order without the global depth sort: key counts scanned in
@@ -198,9 +213,9 @@ void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32
 // in place (tmp: scratch of the same size as vals).
 int count_scan_blocks(int n);
 void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32_t *rowpre, int TX,
-                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, Counters *cnt,
-                       uint32_t cap, const uint32_t *pre_partial, int n_pre, HostCounters *host,
-                       uint32_t tag, hipStream_t st);
+                       uint32_t *part, uint32_t *vidx, uint32_t *voffs, uint32_t *kfirst,
+                       Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
+                       HostCounters *host, uint32_t tag, hipStream_t st);
 // long_lists: lists above 1024 entries are expected (a launch of their own
 // for them); otherwise the few there are take a slower in-block path.
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
