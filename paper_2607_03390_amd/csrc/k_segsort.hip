@@ -12,7 +12,7 @@
 //  3. One block per tile sorts its list by (depth bits, Gaussian index): a
 //     stable LSD radix sort on the depth bits (four 8-bit passes, the list
 //     in index order stays in index order among equal depths) with the
-//     (depth key, index) pairs in LDS and 1-16 entries per thread, for lists
+//     (depth key, index) pairs in LDS and 1-8 entries per thread, for lists
 //     of up to 4096 entries; the same sort over global memory for longer
 //     ones (correct for any length, meant for the rare list that outgrows
 //     the bound).
@@ -26,11 +26,11 @@ namespace {
 constexpr int kScanThreads = 256;
 constexpr int kScanPer = 4;                               // Gaussians per thread
 constexpr int kScanBlock = kScanThreads * kScanPer;       // 1024 Gaussians per block
-// per-tile sort: lists of up to 1024 entries on 256-thread blocks (1-4
-// entries per thread), longer ones on 512-thread blocks (4-8 per thread, or
+// per-tile sort: lists of up to 2048 entries on 256-thread blocks (1-8
+// entries per thread), longer ones on 512-thread blocks (8 per thread, or
 // the global-memory path above 4096)
 constexpr int kShortThreads = 256;
-constexpr int kShortCap = 1024;
+constexpr int kShortCap = 2048;
 constexpr int kLongThreads = 512;
 constexpr int kSegCap = 4096;
 
@@ -376,9 +376,9 @@ __device__ void seg_sort_lds(uint32_t *vals, uint32_t L, const uint32_t *dkey, u
 }
 
 // One block per tile: its list [ranges.x, ranges.y) of vals, in index order,
-// sorted by (depth bits, index) in place.  Short lists (up to 1024 entries):
+// sorted by (depth bits, index) in place.  Short lists (up to 2048 entries):
 // up to 256 by counting, longer ones by the LDS radix sort.
-// Lists above 1024 entries: left to the long-list kernel (long_lists != 0),
+// Lists above 2048 entries: left to the long-list kernel (long_lists != 0),
 // else sorted here over global memory (tmp), for frames where they are rare
 // enough that a launch of their own costs more than it saves.
 __global__ __launch_bounds__(kShortThreads) void segment_sort_short_kernel(const uint2 *ranges,
@@ -423,10 +423,11 @@ __global__ __launch_bounds__(kShortThreads) void segment_sort_short_kernel(const
             v[rank] = val;
         }
     } else if (L <= 512) seg_sort_lds<2, kShortThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
-    else seg_sort_lds<4, kShortThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
+    else if (L <= 1024) seg_sort_lds<4, kShortThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
+    else seg_sort_lds<8, kShortThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
 }
 
-// The same for lists above 1024 entries: in LDS up to 4096, over global
+// The same for lists above 2048 entries: in LDS up to 4096, over global
 // memory (tmp: scratch of the same layout as vals) beyond.
 __global__ __launch_bounds__(kLongThreads) void segment_sort_long_kernel(const uint2 *ranges,
                                                                        uint32_t *vals, uint32_t *tmp,
@@ -445,8 +446,7 @@ __global__ __launch_bounds__(kLongThreads) void segment_sort_long_kernel(const u
         return;
     }
     uint32_t *v = vals + r.x;
-    if (L <= 2048) seg_sort_lds<4, kLongThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
-    else seg_sort_lds<8, kLongThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
+    seg_sort_lds<8, kLongThreads>(v, L, dkey, s_kv, s_wh, s_dstart, s_scan);
 }
 
 }  // namespace

@@ -82,7 +82,9 @@ struct Workspace {
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
     HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
     HostCounters *host_cnt_dev = nullptr; // its device-side address
-    uint32_t *host_maxb = nullptr;        // pinned: longest tile list's log2 bucket (some recent frame)
+    // pinned: longest tile list's log2 bucket of some recent frame, [0] of
+    // frames that render every tile, [1] of selective-rendering frames
+    uint32_t *host_maxb = nullptr;
     uint32_t *host_maxb_dev = nullptr;
     bool frame_seg = false;               // this frame orders tiles by the per-tile sort
     uint32_t seq = 0;                     // tag of the last frame's counters
@@ -108,9 +110,10 @@ struct Workspace {
             TGS_HIP(hipHostGetDevicePointer((void **)&host_cnt_dev, host_cnt, 0));
         }
         if (!host_maxb) {
-            TGS_HIP(hipHostMalloc((void **)&host_maxb, sizeof(uint32_t),
+            TGS_HIP(hipHostMalloc((void **)&host_maxb, 2 * sizeof(uint32_t),
                                   hipHostMallocCoherent | hipHostMallocMapped));
-            *host_maxb = 0xffffffffu;   // unknown: the first frame takes the depth-sorted path
+            // unknown: the first frame takes the depth-sorted path
+            host_maxb[0] = host_maxb[1] = 0xffffffffu;
             TGS_HIP(hipHostGetDevicePointer((void **)&host_maxb_dev, host_maxb, 0));
         }
         if (n_ != n) {
@@ -390,7 +393,7 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
     // (keys only on the selected tiles) whose lists fit its LDS bound; a
     // frame rendering every tile sorts 3-4 times as many keys per tile as
     // the depth sort sorts Gaussians, and takes the global depth sort
-    const uint32_t maxb = *reinterpret_cast<volatile uint32_t *>(ws.host_maxb);
+    const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[1];
     ws.frame_seg = g_sort_path == 2 ||
                    (g_sort_path == 0 && rowpre != nullptr && maxb <= (uint32_t)kSegBucketMax);
     if (ws.frame_seg) {
@@ -498,9 +501,10 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     if (ws.frame_seg) {
         // each tile's list, emitted in index order, by (depth bits, index)
         ProfScope ps(TGS_PROF_SORT, st);
-        // lists of 1024 entries and more get a launch of their own when a
-        // recent frame had any (the longest list's bucket, from the host copy)
-        const uint32_t maxb = *reinterpret_cast<volatile uint32_t *>(ws.host_maxb);
+        // lists above 2048 entries get a launch of their own when a recent
+        // frame of the same kind had any (the longest list's bucket, from the
+        // host copy)
+        const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0];
         launch_segment_sort(TX * TY, ws.ranges.as<uint2>(), svals,
                             alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
                             ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, st);
@@ -511,7 +515,7 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
         // blend order: the selected tiles, or all of them, longest lists first
         launch_order_tiles(TX * TY, rowpre ? &cnt->n_selected : nullptr,
                            rowpre ? ws.sel_list.as<int>() : nullptr, ws.ranges.as<uint2>(),
-                           ws.tile_order.as<int>(), ws.host_maxb_dev, st);
+                           ws.tile_order.as<int>(), ws.host_maxb_dev + (rowpre ? 1 : 0), st);
         TGS_LAUNCHED("tile order");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();

@@ -216,13 +216,13 @@ void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32
                        uint32_t *part, uint32_t *vidx, uint32_t *voffs, uint32_t *kfirst,
                        Counters *cnt, uint32_t cap, const uint32_t *pre_partial, int n_pre,
                        HostCounters *host, uint32_t tag, hipStream_t st);
-// long_lists: lists above 1024 entries are expected (a launch of their own
+// long_lists: lists above 2048 entries are expected (a launch of their own
 // for them); otherwise the few there are take a slower in-block path.
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
                          const uint32_t *dkey, bool long_lists, hipStream_t st);
 // Length bucket (floor(log2 len) + 1) from which a recent frame's lists make
-// the long-list launch worth its cost: lists of 1024 entries and more.
-constexpr int kSegLongBucket = 11;
+// the long-list launch worth its cost: lists of 2048 entries and more.
+constexpr int kSegLongBucket = 12;
 // Longest list the per-tile sort handles in LDS; longer ones take its slower
 // in-block path.  Lists of bucket <= kSegBucketMax (floor(log2 len) + 1)
 // fit.
