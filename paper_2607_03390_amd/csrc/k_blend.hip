@@ -127,12 +127,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                     if (r0.x + hx >= x0 && r0.x - hx <= x0 + 3.0f) cols |= 1u << c;
                     if (r0.y + hy >= y0 && r0.y - hy <= y0 + 3.0f) rows |= 1u << c;
                 }
+                // and whose centre lies within sqrt(k) + m of the mean in the
+                // metric of the conic (q(d) = a dx^2 + 2 b dx dy + c dy^2;
+                // k = 2 ln(255 o), from the record; m = the largest q-length
+                // from a sub-block's centre to its corner pixel centres, at
+                // offset (1.5, +-1.5)): by the triangle inequality of that
+                // norm no pixel centre of a sub-block farther out has
+                // q <= k, i.e. alpha >= 1/255.  Enlarged by 0.2 % + 0.01.
+                const float ca = r0.z, cb = r0.w, cc = r1.x;
+                const float m = sqrtf(2.25f * (ca + cc + 2.0f * fabsf(cb)));
+                const float rr = (sqrtf(r3.w) + m) * 1.002f + 0.01f;
+                const float R = rr * rr;
                 // list L covers column 2 (w & 1) + (g & 1), row 2 (w >> 1) + (g >> 1)
 #pragma unroll
                 for (int L = 0; L < 16; ++L) {
                     const int w = L >> 2, g = L & 3;
                     const int cx = 2 * (w & 1) + (g & 1), cy = 2 * (w >> 1) + (g >> 1);
-                    if (((cols >> cx) & (rows >> cy)) & 1u) lists |= 1u << L;
+                    const float dx = tile_x0 + (4.0f * cx + 1.5f) - r0.x;
+                    const float dy = tile_y0 + (4.0f * cy + 1.5f) - r0.y;
+                    const float q = ca * dx * dx + 2.0f * cb * dx * dy + cc * dy * dy;
+                    if ((((cols >> cx) & (rows >> cy)) & 1u) && !(q > R)) lists |= 1u << L;
                 }
             }
         }

@@ -214,9 +214,9 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
                     // 2 ln(255 o), an ellipse with half extents sqrt(k Sigma'_xx),
                     // sqrt(k Sigma'_yy); enlarged so that every pixel left out
                     // has alpha well below the threshold
-                    float bx = -1.0f, by = -1.0f;
+                    float bx = -1.0f, by = -1.0f, kq = 0.0f;
                     if (mo.w >= 0.999f * kAlphaMin) {
-                        const float kq = 2.0f * __logf(fmaxf(255.0f * mo.w, 1.0f)) + 1e-3f;
+                        kq = 2.0f * __logf(fmaxf(255.0f * mo.w, 1.0f)) + 1e-3f;
                         bx = sqrtf(kq * ca) * 1.002f + 0.05f;
                         by = sqrtf(kq * cc) * 1.002f + 0.05f;
                     }
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
                     r[0] = make_float4(u, v, con_a, con_b);
                     r[1] = make_float4(con_c, mo.w, tz, by);
                     r[2] = make_float4(cr, cg, cbl, bx);
-                    r[3] = make_float4(-0.5f * kLog2e * con_a, -kLog2e * con_b, -0.5f * kLog2e * con_c, 0.0f);
+                    r[3] = make_float4(-0.5f * kLog2e * con_a, -kLog2e * con_b, -0.5f * kLog2e * con_c, kq);
                 }
             }
         }

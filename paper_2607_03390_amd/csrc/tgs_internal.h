@@ -44,11 +44,12 @@ struct SceneDev {
 struct Records {
     // One 64-byte record per Gaussian (one aligned line per gather):
     // g[4i] = (u, v, conic a, conic b), g[4i + 1] = (conic c, opacity,
-    // depth, hy), g[4i + 2] = (r, g, b, hx), g[4i + 3] = (qa, qb, qc, 0):
+    // depth, hy), g[4i + 2] = (r, g, b, hx), g[4i + 3] = (qa, qb, qc, k):
     // the blend's constants, computed once per Gaussian instead of once per
     // (Gaussian, tile): q* = conic pre-scaled by -log2(e) (1/2 on the
     // squares), and hx, hy = half extents of the box of the alpha >= 1/255
-    // ellipse enlarged by 0.2% + 0.05 px (negative: alpha < 1/255 everywhere).
+    // ellipse enlarged by 0.2% + 0.05 px (negative: alpha < 1/255 everywhere);
+    // g[4i + 3].w = k >= 2 ln(255 o), the ellipse's bound on the conic form.
     float4 *g;
     ushort4 *rect;            // tile rectangle x0, y0, x1, y1 (x0 > x1: empty)
     uint8_t *status;          // bit0 survivor, bit1 newly visible
