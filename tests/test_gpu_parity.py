@@ -142,6 +142,18 @@ def test_long_lists_after_short_ones(sort_path):
     _full_parity(sc, [away, near], label="long after short")
 
 
+@pytest.mark.parametrize("W,H", [(3840, 2160), (7680, 4320)])
+def test_full_parity_large_grids(W, H):
+    """Tile grids of 240 x 135 and 480 x 270 (two and three 8-bit tile-sort
+    passes over 15- and 17-bit tile ids): lists
+    bit-exact, colour on sampled tiles."""
+    sc = synth.small_scene(20_000, 13, degree=1, log_scale_mean=-3.6)
+    cam = synth.make_camera(synth.look_at((0.0, -3.0, 1.0), (0, 0, 0)), W, H)
+    TX, TY = cam.tiles
+    sample = np.random.default_rng(1).choice(TX * TY, 60, replace=False)
+    _full_parity(sc, [cam], sample_tiles=sample, label=f"grid {TX}x{TY}")
+
+
 def test_full_parity_object_subset():
     w = synth.workload("object", n_gaussians=40_000)
     _full_parity(w.scene, [w.cameras[0], w.cameras[37]], label="object 40k")
