@@ -188,8 +188,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         __syncthreads();
         // a wave whose pixels have all stopped skips the batch
         const uint32_t n_run = done == ~0ull ? 0u : n_long;
+        // list slots are read four at a time (one aligned 32-bit LDS load
+        // every fourth entry): three iterations in four wait for one LDS
+        // round trip (the staged record) instead of two
+        uint32_t quad = 0;
         for (uint32_t e = 0; e < n_run; ++e) {
-            const uint32_t j = s_list[my_list][e];
+            if ((e & 3u) == 0u) quad = *reinterpret_cast<const uint32_t *>(&s_list[my_list][e]);
+            const uint32_t j = (quad >> (8u * (e & 3u))) & 255u;
             const uint32_t jo = j << 4;   // byte offset into the staged arrays
             const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g0) + jo);
             const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g1) + jo);
