@@ -56,7 +56,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     // four lists at once: a footprint a few pixels wide meets a 4x4 block
     // about 60 % as often as the 8x8 quadrant.
     __shared__ __align__(16) uint8_t s_list[16][256];
-    __shared__ uint32_t s_cnt[4][16];      // [staging wave][list] entries, then starts
+    __shared__ __align__(16) uint32_t s_cnt[4][16];   // [staging wave][list] entries, then starts
     __shared__ uint32_t s_len[16];         // list lengths
 
     if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) {   // block-uniform
@@ -119,35 +119,52 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
             s_col[tid] = r2;
             const float hx = r2.w, hy = r1.w;
             if (hx >= 0.0f) {
-                // columns / rows of 4x4 sub-blocks the culling box meets
-                uint32_t cols = 0, rows = 0;
+                // sub-blocks the culling box meets: list L covers column
+                // cx = 2 (w & 1) + (g & 1), row cy = 2 (w >> 1) + (g >> 1)
+                // (w = L >> 2, g = L & 3); kColL[c] / kRowL[c] are the lists
+                // of column / row c
+                constexpr uint32_t kColL[4] = {0x0505u, 0x0a0au, 0x5050u, 0xa0a0u};
+                constexpr uint32_t kRowL[4] = {0x0033u, 0x00ccu, 0x3300u, 0xcc00u};
+                uint32_t box = 0u, rows = 0u;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const float x0 = tile_x0 + 4.0f * c, y0 = tile_y0 + 4.0f * c;
-                    if (r0.x + hx >= x0 && r0.x - hx <= x0 + 3.0f) cols |= 1u << c;
-                    if (r0.y + hy >= y0 && r0.y - hy <= y0 + 3.0f) rows |= 1u << c;
+                    box |= (r0.x + hx >= x0 && r0.x - hx <= x0 + 3.0f) ? kColL[c] : 0u;
+                    rows |= (r0.y + hy >= y0 && r0.y - hy <= y0 + 3.0f) ? kRowL[c] : 0u;
                 }
+                box &= rows;
                 // and whose centre lies within sqrt(k) + m of the mean in the
                 // metric of the conic (q(d) = a dx^2 + 2 b dx dy + c dy^2;
                 // k = 2 ln(255 o), from the record; m = the largest q-length
                 // from a sub-block's centre to its corner pixel centres, at
                 // offset (1.5, +-1.5)): by the triangle inequality of that
                 // norm no pixel centre of a sub-block farther out has
-                // q <= k, i.e. alpha >= 1/255.  Enlarged by 0.2 % + 0.01.
+                // q <= k, i.e. alpha >= 1/255.  Enlarged by 0.2 % + 0.01,
+                // which also covers the hardware square root (1 ulp) and the
+                // rounding of q.  The terms of q are taken per column and per
+                // row, then one FMA and one add per sub-block, without branches.
                 const float ca = r0.z, cb = r0.w, cc = r1.x;
-                const float m = sqrtf(2.25f * (ca + cc + 2.0f * fabsf(cb)));
-                const float rr = (sqrtf(r3.w) + m) * 1.002f + 0.01f;
+                const float m = __builtin_amdgcn_sqrtf(2.25f * (ca + cc + 2.0f * fabsf(cb)));
+                const float rr = (__builtin_amdgcn_sqrtf(r3.w) + m) * 1.002f + 0.01f;
                 const float R = rr * rr;
-                // list L covers column 2 (w & 1) + (g & 1), row 2 (w >> 1) + (g >> 1)
+                float ax[4], bx[4], dyr[4], cy2[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float dx = tile_x0 + (4.0f * c + 1.5f) - r0.x;
+                    const float dy = tile_y0 + (4.0f * c + 1.5f) - r0.y;
+                    ax[c] = ca * dx * dx;
+                    bx[c] = 2.0f * cb * dx;
+                    dyr[c] = dy;
+                    cy2[c] = cc * dy * dy;
+                }
 #pragma unroll
                 for (int L = 0; L < 16; ++L) {
                     const int w = L >> 2, g = L & 3;
                     const int cx = 2 * (w & 1) + (g & 1), cy = 2 * (w >> 1) + (g >> 1);
-                    const float dx = tile_x0 + (4.0f * cx + 1.5f) - r0.x;
-                    const float dy = tile_y0 + (4.0f * cy + 1.5f) - r0.y;
-                    const float q = ca * dx * dx + 2.0f * cb * dx * dy + cc * dy * dy;
-                    if ((((cols >> cx) & (rows >> cy)) & 1u) && !(q > R)) lists |= 1u << L;
+                    const float q = __builtin_fmaf(bx[cx], dyr[cy], ax[cx] + cy2[cy]);
+                    lists |= !(q > R) ? (1u << L) : 0u;
                 }
+                lists &= box;
             }
         }
         if (CAPTURE) s_flag[tid] = 0u;
@@ -175,11 +192,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         // an empty constraint (no code): the bits are extracted again here
         // instead of sixteen of them living across the barriers
         __asm__ volatile("" : "+v"(lists));
+        // the wave's 16 list starts in four 16-byte LDS loads
+        uint4 st4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) st4[q] = reinterpret_cast<const uint4 *>(&s_cnt[wave][0])[q];
 #pragma unroll
         for (int L = 0; L < 16; ++L) {
             const uint64_t bal = __ballot((lists >> L) & 1u);
-            if ((lists >> L) & 1u)
-                s_list[L][(uint32_t)__popcll(bal & lt_mask) + s_cnt[wave][L]] = (uint8_t)tid;
+            const uint4 v4 = st4[L >> 2];
+            const uint32_t st = (L & 3) == 0 ? v4.x : (L & 3) == 1 ? v4.y : (L & 3) == 2 ? v4.z : v4.w;
+            if ((lists >> L) & 1u) s_list[L][(uint32_t)__popcll(bal & lt_mask) + st] = (uint8_t)tid;
         }
         // the wave's trip count: its longest list (the same for every lane:
         // kept on scalar registers; shorter lists are padded)

@@ -219,7 +219,9 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uin
 #pragma unroll
             for (int k = 0; k < kPer; ++k) {
                 if (pass == 0) {
-                    if (act[k]) atomicAdd(&s_cnt[bk[k]], 1u);
+                    // one LDS atomic per bucket present in the wave (lists
+                    // fall into a dozen buckets: per-lane atomics contend)
+                    (void)wave_bucket_add(s_cnt, bk[k], act[k]);
                 } else {
                     const uint32_t slot = wave_bucket_add(s_cnt, bk[k], act[k]);
                     if (act[k]) tile_out[slot] = t[k];
