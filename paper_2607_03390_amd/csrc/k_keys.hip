@@ -5,6 +5,7 @@
 //  - per-tile [start, end) ranges of the tile-sorted keys and the blend
 //    order of the tiles.
 // Counts stay on the device, so nothing here needs a host round trip.
+#include "order.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -153,101 +154,9 @@ __global__ __launch_bounds__(256) void ranges_kernel(const Counters *cnt, const 
     }
 }
 
-// Blend order of the tiles to rasterise: longest lists first, bucketed by
-// floor(log2(length)).  Tile lists are bimodal (a few thousand long tiles
-// next to many short ones); launched in raster order, long tiles dispatched
-// last would set the blend's tail.  Tiles are independent, so the order
-// (which, within a bucket, depends on LDS atomics) changes only scheduling,
-// never a result.
-// Bucket of a list length: floor(log2(len)) + 1, 0 for an empty list.
-__device__ inline uint32_t length_bucket(const uint2 *ranges, int t) {
-    const uint2 r = ranges[t];
-    const uint32_t len = r.y - r.x;
-    return len ? 32u - (uint32_t)__clz(len) : 0u;
-}
-
-// Wave-aggregated LDS atomic without a loop: lanes with equal buckets are
-// matched over the six bucket bits; the lowest lane of each group adds the
-// group's size (one LDS atomic instruction for all groups) and the others
-// take consecutive slots after its old value.
-__device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool active) {
-    const int lane = threadIdx.x & 63;
-    uint64_t peers = __ballot(active);
-#pragma unroll
-    for (int bit = 0; bit < 6; ++bit) {
-        const bool x = (b >> bit) & 1u;
-        const uint64_t m = __ballot(x);
-        peers &= x ? m : ~m;
-    }
-    const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
-    uint32_t base = 0;
-    if (active && lane == leader) base = atomicAdd(&s_cnt[b], (uint32_t)__popcll(peers));
-    base = __shfl(base, leader);
-    return base + (uint32_t)__popcll(peers & ((1ull << lane) - 1ull));
-}
-
-__global__ __launch_bounds__(1024) void order_tiles_kernel(int n_host, const uint32_t *n_dev,
-                                                           const int *tile_in,
-                                                           const uint2 *ranges, int *tile_out,
-                                                           uint32_t *max_bucket) {
-    constexpr int kPer = 8;   // tiles per thread and round: all loads of a round in flight
+__global__ __launch_bounds__(1024) void order_tiles_kernel(OrderK o) {
     __shared__ uint32_t s_cnt[33];
-    const int tid = threadIdx.x;
-    const int n = n_dev ? (int)*n_dev : n_host;
-    if (tid < 33) s_cnt[tid] = 0u;
-    __syncthreads();
-    // up to 8192 tiles (one round) the tiles and buckets stay in registers
-    // between the counting and the placing pass; more take a second load
-    const bool one_round = n <= kPer * 1024;
-    int t[kPer];
-    uint32_t bk[kPer];
-    bool act[kPer];
-    // every lane runs every round (bounds are block-uniform) so that the
-    // wave-level aggregation sees the whole wave
-    for (int pass = 0; pass < 2; ++pass) {
-        for (int c0 = 0; c0 < n; c0 += kPer * 1024) {
-            if (pass == 0 || !one_round) {
-#pragma unroll
-                for (int k = 0; k < kPer; ++k) {
-                    const int i = c0 + k * 1024 + tid;
-                    act[k] = i < n;
-                    t[k] = act[k] ? (tile_in ? tile_in[i] : i) : 0;
-                }
-#pragma unroll
-                for (int k = 0; k < kPer; ++k) bk[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
-            }
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                if (pass == 0) {
-                    // one LDS atomic per bucket present in the wave (lists
-                    // fall into a dozen buckets: per-lane atomics contend)
-                    (void)wave_bucket_add(s_cnt, bk[k], act[k]);
-                } else {
-                    const uint32_t slot = wave_bucket_add(s_cnt, bk[k], act[k]);
-                    if (act[k]) tile_out[slot] = t[k];
-                }
-            }
-        }
-        __syncthreads();
-        if (pass == 0 && tid < 64) {
-            // bucket starts, longest lists first: lane l holds bucket 32 - l
-            const int b = 32 - tid;
-            const uint32_t c = b >= 0 ? s_cnt[b] : 0u;
-            uint32_t inc = c;
-#pragma unroll
-            for (int d = 1; d < 64; d <<= 1) {
-                const uint32_t o = __shfl_up(inc, d);
-                if (tid >= d) inc += o;
-            }
-            if (b >= 0) s_cnt[b] = inc - c;
-            const uint64_t nz = __ballot(c != 0u);
-            // the host reads this value some frames later: no fence needed
-            if (max_bucket && tid == 0)
-                __hip_atomic_store(max_bucket, nz ? (uint32_t)(32 - (__ffsll((long long)nz) - 1)) : 0u,
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        }
-        __syncthreads();
-    }
+    order_tiles_block<1024>(o, s_cnt);
 }
 
 }  // namespace
@@ -272,10 +181,8 @@ void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint
     if (cap > 0) ranges_kernel<<<blocks, 256, 0, st>>>(cnt, keys, ranges);
 }
 
-void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
-                        int *tile_out, uint32_t *max_bucket, hipStream_t st) {
-    if (n > 0)
-        order_tiles_kernel<<<1, 1024, 0, st>>>(n, n_dev, tile_in, ranges, tile_out, max_bucket);
+void launch_order_tiles(const OrderK &o, hipStream_t st) {
+    if (o.n_host > 0) order_tiles_kernel<<<1, 1024, 0, st>>>(o);
 }
 
 }  // namespace tgs

@@ -10,6 +10,7 @@
 // and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.
+#include "fill_query.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -70,9 +71,18 @@ __device__ inline void sh_colour(const SceneDev &s, int i, float dx, float dy, f
     b = fmaxf(acc2 + 0.5f, 0.0f);
 }
 
+// Blocks at or past n_pre (a TemporalGS frame with the full-resolution
+// geometry buffer) run the depth fill / correspondence query of tile
+// blockIdx.x - n_pre instead: independent of the preprocess, so it fills in
+// beside it rather than taking a launch of its own.
 template <int DEG>
 __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, CullK cull,
-                                                         Records rec, Counters *cnt) {
+                                                         Records rec, Counters *cnt, FillK fill,
+                                                         int n_pre) {
+    if ((int)blockIdx.x >= n_pre) {   // block-uniform
+        fill_query_tile(fill, (int)blockIdx.x - n_pre);
+        return;
+    }
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     bool survivor = false, newly = false;
     ushort4 rect = make_ushort4(1, 1, 0, 0);
@@ -254,14 +264,20 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
 }  // namespace
 
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
-                       Counters *cnt, hipStream_t st) {
-    if (s.n <= 0) return;
-    const dim3 grid(preprocess_blocks(s.n)), block(256);
+                       Counters *cnt, const FillK *fill, hipStream_t st) {
+    const int n_pre = s.n > 0 ? preprocess_blocks(s.n) : 0;
+    // the fill blocks need 256 threads per tile: full-resolution grid only
+    const bool with_fill = fill && fill->w.tp * fill->w.tp == 256;
+    if (fill && !with_fill) launch_fill_query(*fill, st);
+    const int n_fill = with_fill ? fill->w.TX * fill->w.TY : 0;
+    if (n_pre + n_fill <= 0) return;
+    const FillK f = with_fill ? *fill : FillK{};
+    const dim3 grid(n_pre + n_fill), block(256);
     switch (s.deg) {
-        case 0: preprocess_kernel<0><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
-        case 1: preprocess_kernel<1><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
-        case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
-        default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt); break;
+        case 0: preprocess_kernel<0><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
+        case 1: preprocess_kernel<1><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
+        case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
+        default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
     }
 }
 

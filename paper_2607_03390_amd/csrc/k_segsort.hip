@@ -17,6 +17,7 @@
 //     ones (correct for any length, meant for the rare list that outgrows
 //     the bound).
 // The per-tile lists are identical to those of the depth-ordered path.
+#include "order.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -381,16 +382,30 @@ __device__ void seg_sort_lds(uint32_t *vals, uint32_t L, const uint32_t *dkey, u
 // Lists above 2048 entries: left to the long-list kernel (long_lists != 0),
 // else sorted here over global memory (tmp), for frames where they are rare
 // enough that a launch of their own costs more than it saves.
+// With with_order, block 0 computes the blend order of the tiles (it needs
+// only the list lengths, which the sort leaves unchanged) while the other
+// blocks sort tile blockIdx.x - 1: the order costs no launch of its own.
 __global__ __launch_bounds__(kShortThreads) void segment_sort_short_kernel(const uint2 *ranges,
                                                                          uint32_t *vals,
                                                                          uint32_t *tmp,
                                                                          const uint32_t *dkey,
-                                                                         int long_lists) {
+                                                                         int long_lists,
+                                                                         OrderK order,
+                                                                         int with_order) {
     __shared__ uint2 s_kv[kShortCap];
     __shared__ uint32_t s_wh[(kShortThreads / 64) * 256];
     __shared__ uint32_t s_dstart[256];
     __shared__ uint32_t s_scan[kShortThreads / 64];
-    const uint2 r = ranges[blockIdx.x];
+    __shared__ uint32_t s_ocnt[33];
+    int tile = (int)blockIdx.x;
+    if (with_order) {
+        if (tile == 0) {   // block-uniform
+            order_tiles_block<kShortThreads>(order, s_ocnt);
+            return;
+        }
+        tile -= 1;
+    }
+    const uint2 r = ranges[tile];
     const uint32_t L = r.y - r.x;
     if (L <= 1) return;   // block-uniform
     if (L > (uint32_t)kShortCap) {
@@ -467,12 +482,15 @@ void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32
 }
 
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
-                         const uint32_t *dkey, bool long_lists, hipStream_t st) {
+                         const uint32_t *dkey, bool long_lists, const OrderK *order,
+                         hipStream_t st) {
     if (n_tiles <= 0) return;
     if (long_lists)
         segment_sort_long_kernel<<<n_tiles, kLongThreads, 0, st>>>(ranges, vals, tmp, dkey);
-    segment_sort_short_kernel<<<n_tiles, kShortThreads, 0, st>>>(ranges, vals, tmp, dkey,
-                                                                 long_lists ? 1 : 0);
+    const bool with_order = order && order->n_host > 0;
+    segment_sort_short_kernel<<<n_tiles + (with_order ? 1 : 0), kShortThreads, 0, st>>>(
+        ranges, vals, tmp, dkey, long_lists ? 1 : 0, with_order ? *order : OrderK{},
+        with_order ? 1 : 0);
 }
 
 }  // namespace tgs

@@ -13,6 +13,7 @@
 // (The stitching of the tiles that are not re-rendered, Eq. 4, runs in the
 // blend launch: stitch.h.)
 // All of these are HBM- or latency-bound; none is a dense contraction.
+#include "fill_query.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -52,66 +53,7 @@ __global__ __launch_bounds__(256) void forward_warp_kernel(WarpK w, const float 
     atomicMax(reinterpret_cast<unsigned int *>(smax + p), __float_as_uint(S[q]) & 0x7fffffffu);
 }
 
-// One block of tp x tp threads per tile (tp = 16 on the image, 8 on the
-// half-resolution geometry-buffer grid, where a tile is 8 x 8 cells).
-// The block also clears its tile's occluded flag for this frame and resets
-// its cells of the other warp pair (dmin_next, smax_next) for the next one.
-__global__ __launch_bounds__(256) void fill_query_kernel(WarpK w, const float *__restrict__ dmin,
-                                                         float *dfill, float2 *uv, uint8_t *um,
-                                                         uint8_t *oc, float *dmin_next,
-                                                         float *smax_next) {
-    const int tile = blockIdx.x;
-    const int tx = tile % w.TX, ty = tile / w.TX;
-    const int px = tx * w.tp + (int)(threadIdx.x % (unsigned)w.tp);
-    const int py = ty * w.tp + (int)(threadIdx.x / (unsigned)w.tp);
-    int bad = 0;
-    if (threadIdx.x == 0) oc[tile] = 0;
-    if (px < w.W && py < w.H) {
-        const int q = py * w.W + px;
-        dmin_next[q] = kNoHit;
-        smax_next[q] = 0.0f;
-        float d = dmin[q];
-        if (d == kNoHit && px >= 1 && py >= 1 && px <= w.W - 2 && py <= w.H - 2) {
-            const float *r0 = dmin + (size_t)(py - 1) * w.W + px;
-            const float *r1 = r0 + w.W, *r2 = r1 + w.W;
-            const float n0 = r0[-1], n1 = r0[0], n2 = r0[1], n3 = r1[-1], n4 = r1[1], n5 = r2[-1],
-                        n6 = r2[0], n7 = r2[1];
-            if (n0 != kNoHit && n1 != kNoHit && n2 != kNoHit && n3 != kNoHit && n4 != kNoHit &&
-                n5 != kNoHit && n6 != kNoHit && n7 != kNoHit) {
-                float s = n0;
-                s = s + n1;
-                s = s + n2;
-                s = s + n3;
-                s = s + n4;
-                s = s + n5;
-                s = s + n6;
-                s = s + n7;
-                d = s / 8.0f;
-            }
-        }
-        dfill[q] = d;
-        bool ok = false;
-        float u = -1.0f, v = -1.0f;
-        if (d != kNoHit) {
-            const float rx = ((float)px - w.kcur[2]) / w.kcur[0];
-            const float ry = ((float)py - w.kcur[3]) / w.kcur[1];
-            const float Px = d * rx, Py = d * ry, Pz = d;
-            const float *M = w.Minv;
-            const float X = ((M[0] * Px + M[1] * Py) + M[2] * Pz) + M[3];
-            const float Y = ((M[4] * Px + M[5] * Py) + M[6] * Pz) + M[7];
-            const float Z = ((M[8] * Px + M[9] * Py) + M[10] * Pz) + M[11];
-            if (Z > w.z_near) {
-                u = w.kref[0] * (X / Z) + w.kref[2];
-                v = w.kref[1] * (Y / Z) + w.kref[3];
-                ok = u >= 0.0f && u <= (float)(w.W - 1) && v >= 0.0f && v <= (float)(w.H - 1);
-            }
-        }
-        uv[q] = ok ? make_float2(u, v) : make_float2(-1.0f, -1.0f);
-        bad = ok ? 0 : 1;
-    }
-    const int any = __syncthreads_or(bad);
-    if (threadIdx.x == 0) um[tile] = (uint8_t)(any ? 1 : 0);
-}
+__global__ __launch_bounds__(256) void fill_query_kernel(FillK f) { fill_query_tile(f, blockIdx.x); }
 
 __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave, uint32_t *total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -355,10 +297,8 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
     forward_warp_kernel<<<(n + 255) / 256, 256, 0, st>>>(w, D, S, dmin, smax);
 }
 
-void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
-                       uint8_t *oc, float *dmin_next, float *smax_next, hipStream_t st) {
-    fill_query_kernel<<<w.TX * w.TY, w.tp * w.tp, 0, st>>>(w, dmin, dfill, uv, um, oc, dmin_next,
-                                                           smax_next);
+void launch_fill_query(const FillK &f, hipStream_t st) {
+    fill_query_kernel<<<f.w.TX * f.w.TY, f.w.tp * f.w.tp, 0, st>>>(f);
 }
 
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,

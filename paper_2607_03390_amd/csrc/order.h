@@ -1,0 +1,110 @@
+// Blend order of the tiles to rasterise, run by the standalone order kernel
+// or, in frames with a per-tile sort, by the first block of that launch.
+#pragma once
+
+#include "tgs_internal.h"
+
+namespace tgs {
+
+// Blend order of the tiles to rasterise: longest lists first, bucketed by
+// floor(log2(length)).  Tile lists are bimodal (a few thousand long tiles
+// next to many short ones); launched in raster order, long tiles dispatched
+// last would set the blend's tail.  Tiles are independent, so the order
+// (which, within a bucket, depends on LDS atomics) changes only scheduling,
+// never a result.
+// Bucket of a list length: floor(log2(len)) + 1, 0 for an empty list.
+__device__ inline uint32_t length_bucket(const uint2 *ranges, int t) {
+    const uint2 r = ranges[t];
+    const uint32_t len = r.y - r.x;
+    return len ? 32u - (uint32_t)__clz(len) : 0u;
+}
+
+// Wave-aggregated LDS atomic without a loop: lanes with equal buckets are
+// matched over the six bucket bits; the lowest lane of each group adds the
+// group's size (one LDS atomic instruction for all groups) and the others
+// take consecutive slots after its old value.
+__device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool active) {
+    const int lane = threadIdx.x & 63;
+    uint64_t peers = __ballot(active);
+#pragma unroll
+    for (int bit = 0; bit < 6; ++bit) {
+        const bool x = (b >> bit) & 1u;
+        const uint64_t m = __ballot(x);
+        peers &= x ? m : ~m;
+    }
+    const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
+    uint32_t base = 0;
+    if (active && lane == leader) base = atomicAdd(&s_cnt[b], (uint32_t)__popcll(peers));
+    base = __shfl(base, leader);
+    return base + (uint32_t)__popcll(peers & ((1ull << lane) - 1ull));
+}
+
+// One block of NT threads orders the tiles (s_cnt: 33 words of LDS).
+template <int NT>
+__device__ void order_tiles_block(const OrderK &o, uint32_t *s_cnt) {
+    constexpr int kPer = 8;   // tiles per thread and round: all loads of a round in flight
+    const int tid = threadIdx.x;
+    const int n = o.n_dev ? (int)*o.n_dev : o.n_host;
+    const int *tile_in = o.tile_in;
+    const uint2 *ranges = o.ranges;
+    int *tile_out = o.tile_out;
+    uint32_t *max_bucket = o.max_bucket;
+    if (tid < 33) s_cnt[tid] = 0u;
+    __syncthreads();
+    // up to kPer * NT tiles (one round) the tiles and buckets stay in
+    // registers between the counting and the placing pass; more take a
+    // second load
+    const bool one_round = n <= kPer * NT;
+    int t[kPer];
+    uint32_t bk[kPer];
+    bool act[kPer];
+    // every lane runs every round (bounds are block-uniform) so that the
+    // wave-level aggregation sees the whole wave
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int c0 = 0; c0 < n; c0 += kPer * NT) {
+            if (pass == 0 || !one_round) {
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) {
+                    const int i = c0 + k * NT + tid;
+                    act[k] = i < n;
+                    t[k] = act[k] ? (tile_in ? tile_in[i] : i) : 0;
+                }
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) bk[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
+            }
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                if (pass == 0) {
+                    // one LDS atomic per bucket present in the wave (lists
+                    // fall into a dozen buckets: per-lane atomics contend)
+                    (void)wave_bucket_add(s_cnt, bk[k], act[k]);
+                } else {
+                    const uint32_t slot = wave_bucket_add(s_cnt, bk[k], act[k]);
+                    if (act[k]) tile_out[slot] = t[k];
+                }
+            }
+        }
+        __syncthreads();
+        if (pass == 0 && tid < 64) {
+            // bucket starts, longest lists first: lane l holds bucket 32 - l
+            const int b = 32 - tid;
+            const uint32_t c = b >= 0 ? s_cnt[b] : 0u;
+            uint32_t inc = c;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const uint32_t o = __shfl_up(inc, d);
+                if (tid >= d) inc += o;
+            }
+            if (b >= 0) s_cnt[b] = inc - c;
+            const uint64_t nz = __ballot(c != 0u);
+            // the host reads this value some frames later: no fence needed
+            if (max_bucket && tid == 0)
+                __hip_atomic_store(max_bucket, nz ? (uint32_t)(32 - (__ffsll((long long)nz) - 1)) : 0u,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        __syncthreads();
+    }
+}
+
+
+}  // namespace tgs

@@ -368,11 +368,11 @@ struct FrameResult {
 
 // Zero the counters and run the per-Gaussian stage.
 tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
-                           hipStream_t st) {
+                           hipStream_t st, const FillK *fill = nullptr) {
     ProfScope ps(TGS_PROF_PREPROCESS, st);
     CullK c = cull;
     c.footprint = sc->tile_bound == TGS_TILES_FOOTPRINT ? 1 : 0;
-    launch_preprocess(sc->view, cam, c, ws.records(), ws.cnt.as<Counters>(), st);
+    launch_preprocess(sc->view, cam, c, ws.records(), ws.cnt.as<Counters>(), fill, st);
     TGS_LAUNCHED("preprocess");
     return TGS_OK;
 }
@@ -498,24 +498,29 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
         launch_ranges(cap, cnt, skeys, ws.ranges.as<uint2>(), st);
         TGS_LAUNCHED("ranges");
     }
+    // blend order: the selected tiles, or all of them, longest lists first
+    OrderK order{};
+    order.n_host = TX * TY;
+    order.n_dev = rowpre ? &cnt->n_selected : nullptr;
+    order.tile_in = rowpre ? ws.sel_list.as<int>() : nullptr;
+    order.ranges = ws.ranges.as<uint2>();
+    order.tile_out = ws.tile_order.as<int>();
+    order.max_bucket = ws.host_maxb_dev + (rowpre ? 1 : 0);
     if (ws.frame_seg) {
         // each tile's list, emitted in index order, by (depth bits, index)
         ProfScope ps(TGS_PROF_SORT, st);
         // lists above 2048 entries get a launch of their own when a recent
         // frame of the same kind had any (the longest list's bucket, from the
         // host copy)
+        // the blend order (below) is computed by one more block of this launch
         const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0];
         launch_segment_sort(TX * TY, ws.ranges.as<uint2>(), svals,
                             alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
-                            ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, st);
-        TGS_LAUNCHED("per-tile sort");
-    }
-    {
+                            ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, &order, st);
+        TGS_LAUNCHED("per-tile sort and tile order");
+    } else {
         ProfScope ps(TGS_PROF_RANGES, st);
-        // blend order: the selected tiles, or all of them, longest lists first
-        launch_order_tiles(TX * TY, rowpre ? &cnt->n_selected : nullptr,
-                           rowpre ? ws.sel_list.as<int>() : nullptr, ws.ranges.as<uint2>(),
-                           ws.tile_order.as<int>(), ws.host_maxb_dev + (rowpre ? 1 : 0), st);
+        launch_order_tiles(order, st);
         TGS_LAUNCHED("tile order");
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
@@ -936,18 +941,22 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                 launch_forward_warp(wg, s->tgb_d.as<float>(), s->tgb_s.as<float>(), dmin, smax, st);
                 TGS_LAUNCHED("warp");
             }
-            {
-                ProfScope ps(TGS_PROF_FILL_QUERY, st);
-                // also clears the occluded-tile flags of this frame and resets
-                // the other warp pair for the next one
-                launch_fill_query(wg, dmin, s->dfill.as<float>(), s->uv.as<float2>(),
-                                  s->um.as<uint8_t>(), s->oc.as<uint8_t>(),
-                                  s->dmin[wb ^ 1].as<float>(), s->smax[wb ^ 1].as<float>(), st);
-                TGS_LAUNCHED("fill query");
-                s->warp_last = wb;
-                s->warp_next = wb ^ 1;
-                s->warp_clean = true;
-            }
+            // depth fill and backward query; it also clears the occluded-tile
+            // flags of this frame and resets the other warp pair for the next
+            // one.  Run by the preprocess launch (blocks past the Gaussians'),
+            // or by a launch of its own on the half-resolution grid.
+            FillK fq{};
+            fq.w = wg;
+            fq.dmin = dmin;
+            fq.dfill = s->dfill.as<float>();
+            fq.uv = s->uv.as<float2>();
+            fq.um = s->um.as<uint8_t>();
+            fq.oc = s->oc.as<uint8_t>();
+            fq.dmin_next = s->dmin[wb ^ 1].as<float>();
+            fq.smax_next = s->smax[wb ^ 1].as<float>();
+            s->warp_last = wb;
+            s->warp_next = wb ^ 1;
+            s->warp_clean = true;
             CullK cull = no_cull(p.z_near, ws);
             cull.afc = p.enable_afc;
             cull.fbox = s->fbox.as<int>();
@@ -959,7 +968,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             cull.lambda2 = p.lambda2;
             cull.tgb_shift = half ? 1 : 0;
             cull.tgb_w = s->Wg;
-            TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
+            TGS_TRY(step_preprocess(sc, ws, ck, cull, st, &fq));
             {
                 ProfScope ps(TGS_PROF_OCCLUDED, st);
                 launch_occluded(w, sc->n, ws.status.as<uint8_t>(), ws.g.as<float4>(),

@@ -142,8 +142,12 @@ __device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int T
 // ---- launchers (k_preprocess.hip) ----
 // Writes the records and, per 256-Gaussian block, the survivor and
 // newly-visible counts (summed into cnt by the last depth-sort pass).
+// fill (optional): the depth fill / correspondence query of a TemporalGS
+// frame (full-resolution geometry buffer) run by blocks of the same launch
+// past the Gaussians' (independent work: both read only the forward warp).
+struct FillK;
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
-                       Counters *cnt, hipStream_t st);
+                       Counters *cnt, const FillK *fill, hipStream_t st);
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
 // Keys are emitted in blocks of kKeyBlock consecutive positions; kfirst[B]
@@ -177,8 +181,15 @@ void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint
 // into tile_out[0..m).
 // max_bucket (optional, host-visible memory) receives floor(log2 of the
 // longest list length) + 1 (0: all lists empty).
-void launch_order_tiles(int n, const uint32_t *n_dev, const int *tile_in, const uint2 *ranges,
-                        int *tile_out, uint32_t *max_bucket, hipStream_t st);
+struct OrderK {
+    int n_host;
+    const uint32_t *n_dev;
+    const int *tile_in;
+    const uint2 *ranges;
+    int *tile_out;
+    uint32_t *max_bucket;
+};
+void launch_order_tiles(const OrderK &o, hipStream_t st);
 
 // ---- launchers (k_sort.hip) ----
 int sort_passes_for_bits(int bits);
@@ -219,8 +230,11 @@ void launch_count_scan(int n, uint32_t *count, const ushort4 *rect, const uint32
                        HostCounters *host, uint32_t tag, hipStream_t st);
 // long_lists: lists above 2048 entries are expected (a launch of their own
 // for them); otherwise the few there are take a slower in-block path.
+// order (optional): the blend order of the tiles is computed by one more
+// block of the short-list launch, beside the sorting blocks.
 void launch_segment_sort(int n_tiles, const uint2 *ranges, uint32_t *vals, uint32_t *tmp,
-                         const uint32_t *dkey, bool long_lists, hipStream_t st);
+                         const uint32_t *dkey, bool long_lists, const OrderK *order,
+                         hipStream_t st);
 // Length bucket (floor(log2 len) + 1) from which a recent frame's lists make
 // the long-list launch worth its cost: lists of 2048 entries and more.
 constexpr int kSegLongBucket = 12;
@@ -239,6 +253,18 @@ struct WarpK {
     float z_near;
     int W, H, TX, TY;         // grid size (image, or the geometry buffer's) and tiles
     int tp;                   // pixels per tile side on this grid (16, or 8 at half resolution)
+};
+
+// Operands of the depth fill / backward query: one block of tp x tp threads
+// per tile; also clears oc[tile] and resets this tile's cells of the other
+// warp pair (dmin_next = empty depth, smax_next = 0) for the next frame.
+struct FillK {
+    WarpK w;
+    const float *dmin;
+    float *dfill;
+    float2 *uv;
+    uint8_t *um, *oc;
+    float *dmin_next, *smax_next;
 };
 
 struct BlendArgs {
@@ -288,8 +314,7 @@ void launch_forward_warp(const WarpK &w, const float *D, const float *S, float *
                          hipStream_t st);
 // Also oc[tile] = 0 and dmin_next / smax_next reset to their initial values
 // (the other warp pair, for the next frame).
-void launch_fill_query(const WarpK &w, const float *dmin, float *dfill, float2 *uv, uint8_t *um,
-                       uint8_t *oc, float *dmin_next, float *smax_next, hipStream_t st);
+void launch_fill_query(const FillK &f, hipStream_t st);
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
                      const ushort4 *rect, uint8_t *oc, hipStream_t st);
 // sel_list: the selected tiles ascending in [0, n_selected), the others
