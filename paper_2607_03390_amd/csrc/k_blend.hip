@@ -72,6 +72,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;
+    if (tid == 0) {
+        if (a.mark_sel) a.mark_sel[tile] = 1u;
+        if (a.mark_mask) a.mark_mask[tile] = 1u;
+    }
     // lane -> pixel: wave = 8x8 quadrant, lane >> 4 = 4x4 sub-block within it
     const int grp = lane >> 4;
     const int px = tx * kTile + 8 * (wave & 1) + 4 * (grp & 1) + (lane & 3);

@@ -243,6 +243,7 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
         rec.count[i] = keys;
         rec.dkey[i] = __float_as_uint(tz);
         rec.status[i] = (uint8_t)((survivor ? 1 : 0) | (newly ? 2 : 0));
+        if (cull.clear_flag) cull.clear_flag[i] = 0u;
     }
 
     // per-block counts (no contended device-wide atomics)

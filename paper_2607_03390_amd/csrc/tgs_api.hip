@@ -793,6 +793,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         a.sigma = out->sigma;
         a.alpha = out->alpha;
         a.contrib = out->contrib;
+        a.mark_mask = out->tile_mask;   // every tile is rendered
         a.pairs = g_prof.pairs(TGS_PROF_BLEND_FULL);
         a.hits = g_prof.hits(TGS_PROF_BLEND_FULL);
         {
@@ -806,8 +807,6 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         if (!overflow) break;
         TGS_TRY(grow_after_overflow(ws, fr, passes, st));
     }
-    if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)TX * TY, 1, st);
-    TGS_LAUNCHED("tile mask");
     sc->last_W = W;
     sc->last_H = H;
     out->frame_kind = TGS_FRAME_FULL;
@@ -1011,10 +1010,8 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             CullK cull = no_cull(p.z_near, ws);
             cull.afc = (kind == TGS_FRAME_PSEUDO_REF && p.enable_afc) ? 1 : 0;
             cull.fbox = s->fbox.as<int>();
-            {
-                ProfScope ps(TGS_PROF_CAPTURE, st);
-                launch_fill_u8(s->g_flag.as<uint8_t>(), (size_t)(sc->n > 0 ? sc->n : 1), 0, st);
-            }
+            // the preprocess clears the temporal Gaussian buffer the blend fills
+            cull.clear_flag = s->g_flag.as<uint8_t>();
             TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
             const uint32_t *didx = nullptr;
             TGS_TRY(step_scan(ws, sc->n, nullptr, TX, st, &didx));
@@ -1037,6 +1034,9 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             }
             a.g_flag = s->g_flag.as<uint8_t>();
             a.contrib = out->contrib;
+            // every tile is rendered: the blend marks them
+            a.mark_sel = ws.sel.as<uint8_t>();
+            a.mark_mask = out->tile_mask;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
         a.hits = g_prof.hits(TGS_PROF_BLEND_REF);
             {
@@ -1052,9 +1052,6 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                                       s->fbox.as<int>(), st);
                     TGS_LAUNCHED("adaptive frustum");
                 }
-                if (out->tile_mask) launch_fill_u8(out->tile_mask, (size_t)nt, 1, st);
-                launch_fill_u8(ws.sel.as<uint8_t>(), (size_t)nt, 1, st);
-                TGS_LAUNCHED("tile mask");
             }
         }
         bool overflow = false;

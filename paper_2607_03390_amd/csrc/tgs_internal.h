@@ -69,6 +69,8 @@ struct CullK {
     int footprint;            // tile rectangle: 0 = 3-sigma square, 1 = alpha footprint box
     int tgb_shift;            // dmin/smax grid = image >> tgb_shift (0, or 1: 2x2 blocks)
     int tgb_w;                // width of that grid
+    uint8_t *clear_flag;      // optional (reference frames): set to 0 for every Gaussian
+                              // (the temporal Gaussian buffer the blend then fills)
 };
 
 // Frame counters on the device (read back once per frame).
@@ -285,6 +287,7 @@ struct BlendArgs {
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
     unsigned long long *hits;   // with pairs: count of pairs with alpha >= 1/255 (composited or stopping)
     float empty_depth;        // depth written where no Gaussian is composited
+    uint8_t *mark_sel, *mark_mask;   // optional: set to 1 for every blended tile
     // optional (TGS frames): blocks at or past *n_tiles_dev stitch tile
     // stitch_list[block] from the reference image stitch_tab (Eq. 4)
     // instead of blending, so that stitching overlaps the blend's tail:
