@@ -292,8 +292,10 @@ tgs_status tgs_profile_stop(tgs_profile *out);
  *     sorts its list by (depth bits, index) in LDS (lists above 4096 entries
  *     take a slower in-block path);
  *   TGS_SORT_AUTO (default): per frame, the per-tile sort for TemporalGS
- *     frames (keys on the selected tiles only) when the longest tile list of
- *     a recent frame has fewer than 4096 entries, else the depth-first sort.
+ *     frames (keys on the selected tiles only), and for every frame of a
+ *     scene with fewer than 131072 Gaussians, when the longest tile list of
+ *     a recent frame of the same kind has fewer than 4096 entries; else the
+ *     depth-first sort.
  * INVALID_ARG for another value.  Not thread-safe against running renders. */
 enum { TGS_SORT_AUTO = 0, TGS_SORT_DEPTH_FIRST = 1, TGS_SORT_PER_TILE = 2 };
 tgs_status tgs_set_sort_path(int32_t mode);

@@ -382,6 +382,7 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
 // global depth sort), 1 = always the global depth sort, 2 = always the
 // per-tile sort.
 int g_sort_path = 0;
+constexpr int kSegSmallScene = 131072;
 
 // The Gaussians that have keys and the start of their keys, in the order the
 // keys are emitted: depth order (global depth sort; the last pass publishes
@@ -393,9 +394,12 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
     // (keys only on the selected tiles) whose lists fit its LDS bound; a
     // frame rendering every tile sorts 3-4 times as many keys per tile as
     // the depth sort sorts Gaussians, and takes the global depth sort
-    const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[1];
+    // (and in every frame of a small scene: below kSegSmallScene Gaussians the
+    // four depth passes are launch latency, not work)
+    const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0];
     ws.frame_seg = g_sort_path == 2 ||
-                   (g_sort_path == 0 && rowpre != nullptr && maxb <= (uint32_t)kSegBucketMax);
+                   (g_sort_path == 0 && (rowpre != nullptr || n < kSegSmallScene) &&
+                    maxb <= (uint32_t)kSegBucketMax);
     if (ws.frame_seg) {
         ProfScope ps(TGS_PROF_SORT, st);
         ws.seq += 1;
