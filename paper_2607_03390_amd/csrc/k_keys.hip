@@ -144,13 +144,38 @@ __global__ __launch_bounds__(256) void ranges_zero_kernel(int n_tiles, uint2 *ra
     if (t < n_tiles) ranges[t] = make_uint2(0u, 0u);
 }
 
+// Four consecutive sorted keys per thread (one 16-byte load) and the key on
+// either side: the thread writes the start / end of every tile run that
+// begins / ends among its four.
 __global__ __launch_bounds__(256) void ranges_kernel(const Counters *cnt, const uint32_t *keys,
                                                      uint2 *ranges) {
     const uint64_t K = cnt->n_sorted;
-    for (uint64_t k = blockIdx.x * blockDim.x + threadIdx.x; k < K; k += gridDim.x * blockDim.x) {
-        const uint32_t t = keys[k];
-        if (k == 0 || keys[k - 1] != t) ranges[t].x = (uint32_t)k;
-        if (k == K - 1 || keys[k + 1] != t) ranges[t].y = (uint32_t)(k + 1);
+    const uint64_t G = (K + 3) / 4;
+    for (uint64_t g = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; g < G;
+         g += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t k0 = 4 * g;
+        uint32_t t[4];
+        if (k0 + 4 <= K) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(keys + k0);
+            t[0] = v.x;
+            t[1] = v.y;
+            t[2] = v.z;
+            t[3] = v.w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) t[j] = k0 + j < K ? keys[k0 + j] : 0xffffffffu;
+        }
+        const uint32_t prev = k0 > 0 ? keys[k0 - 1] : 0xffffffffu;
+        const uint32_t next = k0 + 4 < K ? keys[k0 + 4] : 0xffffffffu;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint64_t k = k0 + j;
+            if (k >= K) break;
+            const uint32_t tp = j == 0 ? prev : t[j - 1];
+            const uint32_t tn = j == 3 ? next : t[j + 1];
+            if (k == 0 || tp != t[j]) ranges[t[j]].x = (uint32_t)k;
+            if (k == K - 1 || tn != t[j]) ranges[t[j]].y = (uint32_t)(k + 1);
+        }
     }
 }
 
@@ -176,8 +201,10 @@ void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *
 
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
                    hipStream_t st) {
-    // grid-stride over at most 2048 blocks: the key count is on the device
-    const uint32_t blocks = (cap + 255) / 256 < 2048u ? (cap + 255) / 256 : 2048u;
+    // sized for the key capacity (the key count is on the device), at most
+    // 65535 blocks, grid-stride beyond
+    const uint64_t groups = ((uint64_t)cap + 3) / 4;
+    const uint32_t blocks = (uint32_t)((groups + 255) / 256 < 65535u ? (groups + 255) / 256 : 65535u);
     if (cap > 0) ranges_kernel<<<blocks, 256, 0, st>>>(cnt, keys, ranges);
 }
 
