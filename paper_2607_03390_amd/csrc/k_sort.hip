@@ -473,15 +473,17 @@ int sort_passes_for_bits(int bits) { return (bits + 7) / 8; }
 size_t sort_scratch_words(uint32_t max_keys) {
     // chunk sums of counts and weights, then a (partition x digit) count table
     // and weight table, reused by every pass
-    const uint32_t np = n_partitions(max_keys, ipt_for(max_keys));
+    // (sized for the small partitions: a sort may take them for any count)
+    const uint32_t np = n_partitions(max_keys, kIptSmall);
     return (size_t)2 * kChunks * kRadix + (size_t)2 * kRadix * np;
 }
 
-int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes,
-                    uint32_t *keys, uint32_t *vals, uint32_t *keys_alt, uint32_t *vals_alt,
-                    uint32_t *scratch, hipStream_t st) {
+int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int begin_bit,
+                    int passes, uint32_t *keys, uint32_t *vals, uint32_t *keys_alt,
+                    uint32_t *vals_alt, uint32_t *scratch, hipStream_t st) {
     if (n_max <= 1 || passes <= 0) return 0;
-    if (ipt_for(n_max) == kIptSmall)
+    // partition size from the expected count (the grid covers n_max either way)
+    if (ipt_for(n_hint < n_max ? n_hint : n_max) == kIptSmall)
         plain_passes<kIptSmall>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
     else

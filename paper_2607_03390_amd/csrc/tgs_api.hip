@@ -92,6 +92,8 @@ struct Workspace {
     size_t key_cap = 0;
     // last frame, for tgs_debug_dump
     uint32_t last_K = 0;
+    uint32_t recent_K[2] = {0xffffffffu, 0xffffffffu};   // keys of the last frame per kind
+                                                        // ([1]: selective rendering)
     const uint32_t *last_keys = nullptr, *last_vals = nullptr;
     bool has_frame = false;
 
@@ -490,7 +492,8 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     int alt = 0;
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        alt = launch_sort_u32(&cnt->n_sorted, cap, 0, passes, ws.tkey.as<uint32_t>(),
+        alt = launch_sort_u32(&cnt->n_sorted, cap, ws.recent_K[rowpre ? 1 : 0], 0, passes,
+                              ws.tkey.as<uint32_t>(),
                               ws.tval.as<uint32_t>(), ws.tkey_alt.as<uint32_t>(),
                               ws.tval_alt.as<uint32_t>(), ws.sort.as<uint32_t>(), st);
         TGS_LAUNCHED("tile sort");
@@ -808,6 +811,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         }
         bool overflow = false;
         TGS_TRY(step_wait_counters(ws, st, fr, &overflow));
+        ws.recent_K[0] = fr.K;
         if (!overflow) break;
         TGS_TRY(grow_after_overflow(ws, fr, passes, st));
     }
@@ -1060,6 +1064,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
         }
         bool overflow = false;
         TGS_TRY(step_wait_counters(ws, st, fr, &overflow));
+        ws.recent_K[kind == TGS_FRAME_TGS ? 1 : 0] = fr.K;
         if (!overflow) break;
         TGS_TRY(grow_after_overflow(ws, fr, passes, st));
     }
