@@ -6,7 +6,10 @@
 // request per wave) is read for a culled Gaussian; the geometry (32 bytes)
 // for the survivors and the SH coefficients (192 of the 240 bytes per
 // Gaussian at degree 3) for survivors that touch a tile, each Gaussian's
-// bytes contiguous so that sparse survivors fetch only their own lines.  The kernel is HBM-bound.  Quantities that decide a discrete outcome (near cull, frustum
+// bytes contiguous so that sparse survivors fetch only their own lines.  The
+// kernel is HBM-bound.  In TemporalGS frames the launch also carries the
+// depth fill / correspondence query (fill_query.h) on its blocks past the
+// Gaussians', and in reference frames it clears the temporal Gaussian buffer.  Quantities that decide a discrete outcome (near cull, frustum
 // and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.

@@ -16,7 +16,9 @@
 //     of up to 4096 entries; the same sort over global memory for longer
 //     ones (correct for any length, meant for the rare list that outgrows
 //     the bound).
-// The per-tile lists are identical to those of the depth-ordered path.
+// The per-tile lists are identical to those of the depth-ordered path.  One
+// more block of the short-list launch computes the blend order of the tiles
+// (order.h).
 #include "order.h"
 #include "tgs_internal.h"
 

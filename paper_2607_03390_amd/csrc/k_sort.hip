@@ -9,7 +9,8 @@
 // passes run over the Gaussians, not over their tile copies).
 //
 // Structure for gfx950, per 8-bit pass: an upsweep kernel counts each
-// partition's digits (1024 keys per partition up to 2M keys, 3840 above) into
+// partition's digits (1024 keys per partition for an expected count up to 2M
+// keys, 3840 above) into
 // a partition-major table, a column scan turns those counts into offsets
 // within 16 chunks of partitions plus per-chunk digit sums, and a downsweep
 // kernel ranks each partition in LDS and scatters it (the digit bases are a

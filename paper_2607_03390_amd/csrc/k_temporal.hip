@@ -4,7 +4,8 @@
 //    deviation by integer atomics on the float bits (both are non-negative,
 //    so unsigned order is float order and the result is order-independent);
 //  - depth fill, backward correspondence query and unmatched tiles, one
-//    block per tile with a block-wide OR;
+//    block per tile with a block-wide OR (fill_query.h; with the
+//    full-resolution geometry buffer the preprocess launch runs it);
 //  - occluded tiles of the newly visible Gaussians, one wave per
 //    (Gaussian, tile) pair with a wave ballot over the tile's 256 pixels,
 //    the pairs of 1024 Gaussians dealt out over the waves of a block;
