@@ -9,7 +9,8 @@
 // bytes contiguous so that sparse survivors fetch only their own lines.  The
 // kernel is HBM-bound.  In TemporalGS frames the launch also carries the
 // depth fill / correspondence query (fill_query.h) on its blocks past the
-// Gaussians', and in reference frames it clears the temporal Gaussian buffer.  Quantities that decide a discrete outcome (near cull, frustum
+// Gaussians', and in reference frames it clears the temporal Gaussian buffer.
+// Quantities that decide a discrete outcome (near cull, frustum
 // and occlusion tests, tile rectangle, sort depth) are computed in fp32 in a
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.
