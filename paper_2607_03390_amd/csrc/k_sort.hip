@@ -180,7 +180,16 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
             sum += keep[k];
         }
     } else {
-        for (uint32_t p = p0; p < p1; ++p) sum += tab[(size_t)p * kRadix + d];
+        // long runs (huge sorts): eight loads in flight per step
+        uint32_t p = p0;
+        for (; p + 8 <= p1; p += 8) {
+            uint32_t v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = tab[(size_t)(p + k) * kRadix + d];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) sum += v[k];
+        }
+        for (; p < p1; ++p) sum += tab[(size_t)p * kRadix + d];
     }
     s_sum[lane][dl] = sum;
     __syncthreads();
@@ -202,7 +211,18 @@ __global__ __launch_bounds__(256) void sort_colscan_kernel(const uint32_t *n_dev
             o += keep[k];
         }
     } else {
-        for (uint32_t p = p0; p < p1; ++p) {
+        uint32_t p = p0;
+        for (; p + 8 <= p1; p += 8) {
+            uint32_t v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = tab[(size_t)(p + k) * kRadix + d];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                tab[(size_t)(p + k) * kRadix + d] = sat32(o);
+                o += v[k];
+            }
+        }
+        for (; p < p1; ++p) {
             const uint32_t v = tab[(size_t)p * kRadix + d];
             tab[(size_t)p * kRadix + d] = sat32(o);
             o += v;

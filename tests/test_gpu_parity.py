@@ -142,12 +142,14 @@ def test_long_lists_after_short_ones(sort_path):
     _full_parity(sc, [away, near], label="long after short")
 
 
-@pytest.mark.parametrize("W,H", [(3840, 2160), (7680, 4320)])
-def test_full_parity_large_grids(W, H):
+@pytest.mark.parametrize("W,H,log_scale", [(3840, 2160, -3.6), (7680, 4320, -3.6),
+                                           (3840, 2160, -2.2)])
+def test_full_parity_large_grids(W, H, log_scale):
     """Tile grids of 240 x 135 and 480 x 270 (two and three 8-bit tile-sort
-    passes over 15- and 17-bit tile ids): lists
-    bit-exact, colour on sampled tiles."""
-    sc = synth.small_scene(20_000, 13, degree=1, log_scale_mean=-3.6)
+    passes over 15- and 17-bit tile ids), and 35M keys on the first (the
+    radix column scan's long-table path, key buffers grown after an
+    overflow): lists bit-exact, colour on sampled tiles."""
+    sc = synth.small_scene(20_000, 13, degree=1, log_scale_mean=log_scale)
     cam = synth.make_camera(synth.look_at((0.0, -3.0, 1.0), (0, 0, 0)), W, H)
     TX, TY = cam.tiles
     sample = np.random.default_rng(1).choice(TX * TY, 60, replace=False)
