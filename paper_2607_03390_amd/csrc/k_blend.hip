@@ -102,6 +102,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     // Batches of 255 Gaussians in slots 0..254; slot 255 holds a sentinel
     // (opacity 0, conic 0: alpha 0 at every pixel) that pads every list, so
     // entries past a list's end need no test of their own.
+    // this thread's entry index of the next batch, loaded while the current
+    // batch is blended: a batch then waits for one dependent global load
+    // (its records) instead of two, which sets the pace of the tiles with
+    // thousands of batches
+    int nidx = (tid < kBatch && range.x + tid < range.y) ? (int)a.vals[range.x + tid] : 0;
     for (uint32_t b = range.x; b < range.y; b += kBatch) {
         if (__syncthreads_and(done == ~0ull)) break;
         reinterpret_cast<uint4 *>(&s_list[0][0])[tid] =
@@ -114,7 +119,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
             s_col[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             s_idx[tid] = 0;
         } else if (k < range.y) {
-            const int idx = (int)a.vals[k];
+            const int idx = nidx;
             const float4 *r = a.g + 4 * (size_t)idx;
             const float4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
             s_idx[tid] = idx;
@@ -212,6 +217,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         const uint32_t n_long = __builtin_amdgcn_readfirstlane(
             max(max(s_len[4 * wave], s_len[4 * wave + 1]), max(s_len[4 * wave + 2], s_len[4 * wave + 3])));
         __syncthreads();
+        {
+            const uint32_t kn = b + kBatch + tid;
+            nidx = (tid < kBatch && kn < range.y) ? (int)a.vals[kn] : 0;
+        }
         // a wave whose pixels have all stopped skips the batch
         const uint32_t n_run = done == ~0ull ? 0u : n_long;
         // list slots are read four at a time (one aligned 32-bit LDS load
