@@ -71,6 +71,9 @@ def parse():
                          "city workload (the paper's large-scene setting), 1 otherwise")
     ap.add_argument("--sort-path", default="auto", choices=["auto", "depth_first", "per_tile"],
                     help="how per-tile depth order is produced (tgs_set_sort_path)")
+    ap.add_argument("--blend-split", type=int, default=12,
+                    help="tiles with at least 2**N list entries are blended as four quadrant "
+                         "blocks (tgs_set_blend_split; -1: never)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
     return ap.parse_args()
@@ -101,6 +104,7 @@ def main():
     SORT_MODES = {"auto": tgs.SORT_AUTO, "depth_first": tgs.SORT_DEPTH_FIRST,
                   "per_tile": tgs.SORT_PER_TILE}
     tgs.tgs_set_sort_path(SORT_MODES[args.sort_path])
+    tgs.tgs_set_blend_split(args.blend_split)
     log(f"[bench] generating workload {args.workload}")
     wl = synth.workload(args.workload, n_frames=args.frames)
     cams = wl.cameras
@@ -402,6 +406,7 @@ def main():
         "speedup_temporal_vs_full": round(fps_t / fps_f, 3),
         "tile_rule": "3DGS 3-sigma square",
         "sort_path": args.sort_path,
+        "blend_split_log2": args.blend_split,
         **variants,
         "psnr_temporal_vs_full": psnr,
         "ssim_temporal_vs_full": ssim,

@@ -300,6 +300,21 @@ tgs_status tgs_profile_stop(tgs_profile *out);
 enum { TGS_SORT_AUTO = 0, TGS_SORT_DEPTH_FIRST = 1, TGS_SORT_PER_TILE = 2 };
 tgs_status tgs_set_sort_path(int32_t mode);
 
+/* Which tiles the blend (Sec. III-A) splits, process-wide: a tile whose
+ * sorted list has at least 2^log2_min entries is blended by four blocks, one
+ * per 8x8 quadrant, each taking four list entries per pixel at a time
+ * (composited in list order: the result is the unsplit blend's up to the
+ * order of the colour and moment sums).  If more than max_tiles tiles
+ * qualify, the threshold is doubled until at most max_tiles do (whole
+ * length classes, so a frame's result never depends on scheduling).  The few
+ * longest lists set the blend's tail; a quadrant block re-reads the whole
+ * list, so shorter ones are cheaper unsplit.  log2_min in [0, 31], or -1
+ * for no split; max_tiles in [0, TGS_BLEND_SPLIT_MAX].  Defaults:
+ * TGS_BLEND_SPLIT_DEFAULT, TGS_BLEND_SPLIT_MAX.  INVALID_ARG for other
+ * values.  Not thread-safe against running renders. */
+enum { TGS_BLEND_SPLIT_DEFAULT = 12, TGS_BLEND_SPLIT_MAX = 1024 };
+tgs_status tgs_set_blend_split(int32_t log2_min, int32_t max_tiles);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *tgs_last_error(void);
 

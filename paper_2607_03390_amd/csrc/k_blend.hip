@@ -37,50 +37,82 @@ constexpr int kBatch = 255;   // Gaussians staged per batch (slot 255: the senti
 __device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
 __device__ inline bool wave_all(bool p) { return __builtin_amdgcn_ballot_w64(!p) == 0ull; }
 
-template <bool CAPTURE, bool CONTRIB, bool COUNT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void blend_kernel(BlendArgs a) {
-    // Staged per Gaussian: (u, v, qa, qb) and (qc, opacity, depth, -) where
-    // q* = conic coefficients pre-scaled by -log2(e) (and 1/2 on the squares,
-    // by the preprocess) so that log2 of the Gaussian falloff is a three-FMA
-    // quadratic form and the opacity is one v_exp_f32.
-    __shared__ float4 s_g0[256];
-    __shared__ float4 s_g1[256];
-    __shared__ float4 s_col[256];
-    __shared__ int s_idx[256];
-    __shared__ uint8_t s_flag[256];
-    // The tile is cut into sixteen 4x4 sub-blocks; sub-block list L (wave
-    // L >> 2, group L & 3) holds the staging slots of the Gaussians whose
-    // alpha >= 1/255 ellipse, conservatively enlarged, meets the sub-block,
-    // in staging (= depth) order.  Each wave covers an 8x8 quadrant as four
-    // 16-lane groups, one per sub-block, and every iteration advances all
-    // four lists at once: a footprint a few pixels wide meets a 4x4 block
-    // about 60 % as often as the 8x8 quadrant.
-    __shared__ __align__(16) uint8_t s_list[16][256];
-    __shared__ __align__(16) uint32_t s_cnt[4][16];   // [staging wave][list] entries, then starts
-    __shared__ uint32_t s_len[16];         // list lengths
+// Broadcast of lane K of each group of four lanes (DPP quad_perm).
+template <int K>
+__device__ inline float quad_bcast(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v),
+                                                              K | (K << 2) | (K << 4) | (K << 6),
+                                                              0xf, 0xf, false));
+}
+template <int K>
+__device__ inline uint32_t quad_bcast_u(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, K | (K << 2) | (K << 4) | (K << 6), 0xf,
+                                              0xf, false);
+}
+// Sum over each group of four lanes (quad_perm [1,0,3,2], then [2,3,0,1]).
+__device__ inline float quad_sum(float v) {
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xb1,
+                                                            0xf, 0xf, false));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4e,
+                                                            0xf, 0xf, false));
+    return v;
+}
 
-    if (a.n_tiles_dev && blockIdx.x >= *a.n_tiles_dev) {   // block-uniform
-        if (a.stitch_list) {
-            const int t = a.stitch_list[blockIdx.x];
-            if (a.stitch_mode == 2)
-                stitch_tile_depth(a.sw, a.stitch_wg, t, a.stitch_tab, a.stitch_dfill, a.rgb);
-            else
-                stitch_tile_uv(a.sw, t, a.stitch_tab, a.stitch_uv, a.rgb);
-        }
-        return;
-    }
+// LDS of one blend block.  Staged per Gaussian: (u, v, qa, qb) and (qc,
+// opacity, depth, -) where q* = conic coefficients pre-scaled by -log2(e)
+// (and 1/2 on the squares, by the preprocess) so that log2 of the Gaussian
+// falloff is a three-FMA quadratic form and the opacity is one v_exp_f32.
+// The tile is cut into sixteen 4x4 sub-blocks; sub-block list L (quadrant
+// L >> 2, sub-block L & 3 within it: column 2 (L >> 2 & 1) + (L & 1), row
+// 2 (L >> 3) + (L >> 1 & 1)) holds the staging slots of the Gaussians whose
+// alpha >= 1/255 ellipse, conservatively enlarged, meets the sub-block, in
+// staging (= depth) order: a footprint a few pixels wide meets a 4x4 block
+// about 60 % as often as the 8x8 quadrant.
+struct BlendLds {
+    float4 g0[256];
+    float4 g1[256];
+    float4 col[256];
+    int idx[256];
+    uint8_t flag[256];
+    __align__(16) uint8_t list[16][256];
+    __align__(16) uint32_t cnt[4][16];   // [staging wave][list] entries, then starts
+    uint32_t len[16];                    // list lengths
+};
+
+// One 16x16 tile, or (QUAD) one 8x8 quadrant q of it.
+//  - tile: each wave covers an 8x8 quadrant as four 16-lane groups, one per
+//    sub-block, and every iteration advances the four lists at once (the
+//    wave's trip count is its longest list);
+//  - quadrant (the longest lists of the frame, whose tiles would set the
+//    launch's tail): each wave covers one sub-block, four lanes per pixel
+//    taking four consecutive entries of its list per iteration, composited
+//    in list order through the quad's transmittance products.  The four
+//    blocks of a tile each stage the whole list.
+template <bool CAPTURE, bool CONTRIB, bool COUNT, bool QUAD>
+__device__ __attribute__((always_inline)) inline void blend_block(const BlendArgs &a, BlendLds &s,
+                                                                  int tile, int q) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int tile = a.tile_list ? a.tile_list[blockIdx.x] : (int)blockIdx.x;
     const int tx = tile % a.TX, ty = tile / a.TX;
-    if (tid == 0) {
+    if (tid == 0 && (!QUAD || q == 0)) {
         if (a.mark_sel) a.mark_sel[tile] = 1u;
         if (a.mark_mask) a.mark_mask[tile] = 1u;
     }
-    // lane -> pixel: wave = 8x8 quadrant, lane >> 4 = 4x4 sub-block within it
-    const int grp = lane >> 4;
-    const int px = tx * kTile + 8 * (wave & 1) + 4 * (grp & 1) + (lane & 3);
-    const int py = ty * kTile + 8 * (wave >> 1) + 4 * (grp >> 1) + ((lane >> 2) & 3);
-    const int my_list = 4 * wave + grp;
+    // lane -> pixel.  Tile: wave = 8x8 quadrant, lane >> 4 = 4x4 sub-block
+    // within it.  Quadrant: wave = sub-block, lane >> 2 = pixel of it,
+    // lane & 3 = entry of the group of four.
+    const int k = lane & 3;
+    int px, py, my_list;
+    if (QUAD) {
+        const int pix = lane >> 2;
+        px = tx * kTile + 8 * (q & 1) + 4 * (wave & 1) + (pix & 3);
+        py = ty * kTile + 8 * (q >> 1) + 4 * (wave >> 1) + (pix >> 2);
+        my_list = 4 * q + wave;
+    } else {
+        const int grp = lane >> 4;
+        px = tx * kTile + 8 * (wave & 1) + 4 * (grp & 1) + (lane & 3);
+        py = ty * kTile + 8 * (wave >> 1) + 4 * (grp >> 1) + ((lane >> 2) & 3);
+        my_list = 4 * wave + grp;
+    }
     const bool inside = px < a.W && py < a.H;
     float fpx = (float)px, fpy = (float)py;
     // kept in registers through the loops (cheaper than converting them
@@ -109,23 +141,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     int nidx = (tid < kBatch && range.x + tid < range.y) ? (int)a.vals[range.x + tid] : 0;
     for (uint32_t b = range.x; b < range.y; b += kBatch) {
         if (__syncthreads_and(done == ~0ull)) break;
-        reinterpret_cast<uint4 *>(&s_list[0][0])[tid] =
+        reinterpret_cast<uint4 *>(&s.list[0][0])[tid] =
             make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
-        const uint32_t k = b + tid;
+        const uint32_t kb = b + tid;
         uint32_t lists = 0;   // bit L: the staged Gaussian meets sub-block L
         if (tid == kBatch) {
-            s_g0[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            s_g1[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            s_col[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            s_idx[tid] = 0;
-        } else if (k < range.y) {
+            s.g0[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s.g1[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s.col[tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            s.idx[tid] = 0;
+        } else if (kb < range.y) {
             const int idx = nidx;
             const float4 *r = a.g + 4 * (size_t)idx;
             const float4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
-            s_idx[tid] = idx;
-            s_g0[tid] = make_float4(r0.x, r0.y, r3.x, r3.y);
-            s_g1[tid] = make_float4(r3.z, r1.y, r1.z, 0.0f);
-            s_col[tid] = r2;
+            s.idx[tid] = idx;
+            s.g0[tid] = make_float4(r0.x, r0.y, r3.x, r3.y);
+            s.g1[tid] = make_float4(r3.z, r1.y, r1.z, 0.0f);
+            s.col[tid] = r2;
             const float hx = r2.w, hy = r1.w;
             if (hx >= 0.0f) {
                 // sub-blocks the culling box meets: list L covers column
@@ -152,8 +184,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                 // which also covers the hardware square root (1 ulp) and the
                 // rounding of q.  The terms of q are taken per column and per
                 // row, then one FMA and one add per sub-block, without branches.
-                const float ca = r0.z, cb = r0.w, cc = r1.x;
-                const float m = __builtin_amdgcn_sqrtf(2.25f * (ca + cc + 2.0f * fabsf(cb)));
+                const float ca = r0.z, cbq = r0.w, cc = r1.x;
+                const float m = __builtin_amdgcn_sqrtf(2.25f * (ca + cc + 2.0f * fabsf(cbq)));
                 const float rr = (__builtin_amdgcn_sqrtf(r3.w) + m) * 1.002f + 0.01f;
                 const float R = rr * rr;
                 float ax[4], bx[4], dyr[4], cy2[4];
@@ -162,7 +194,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                     const float dx = tile_x0 + (4.0f * c + 1.5f) - r0.x;
                     const float dy = tile_y0 + (4.0f * c + 1.5f) - r0.y;
                     ax[c] = ca * dx * dx;
-                    bx[c] = 2.0f * cb * dx;
+                    bx[c] = 2.0f * cbq * dx;
                     dyr[c] = dy;
                     cy2[c] = cc * dy * dy;
                 }
@@ -170,32 +202,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                 for (int L = 0; L < 16; ++L) {
                     const int w = L >> 2, g = L & 3;
                     const int cx = 2 * (w & 1) + (g & 1), cy = 2 * (w >> 1) + (g >> 1);
-                    const float q = __builtin_fmaf(bx[cx], dyr[cy], ax[cx] + cy2[cy]);
-                    lists |= !(q > R) ? (1u << L) : 0u;
+                    const float qf = __builtin_fmaf(bx[cx], dyr[cy], ax[cx] + cy2[cy]);
+                    lists |= !(qf > R) ? (1u << L) : 0u;
                 }
                 lists &= box;
+                // a quadrant block lists its own four sub-blocks only
+                if (QUAD) lists &= 0xfu << (4 * q);
             }
         }
-        if (CAPTURE) s_flag[tid] = 0u;
+        if (CAPTURE) s.flag[tid] = 0u;
         // order-preserving compaction of each sub-block's Gaussians: counts
-        // per staging wave, then each wave's start in every list (s_cnt
-        // becomes the exclusive prefix over waves, s_len the totals), then
+        // per staging wave, then each wave's start in every list (s.cnt
+        // becomes the exclusive prefix over waves, s.len the totals), then
         // the entries (the votes are taken again rather than kept live)
 #pragma unroll
         for (int L = 0; L < 16; ++L) {
+            if (QUAD && (L >> 2) != q) continue;
             const uint64_t bal = __ballot((lists >> L) & 1u);
-            if (lane == 0) s_cnt[wave][L] = (uint32_t)__popcll(bal);
+            if (lane == 0) s.cnt[wave][L] = (uint32_t)__popcll(bal);
         }
         __syncthreads();
-        if (tid < 16) {
+        if (QUAD ? (tid >= 4 * q && tid < 4 * q + 4) : tid < 16) {
             uint32_t run = 0;
 #pragma unroll
             for (int w2 = 0; w2 < 4; ++w2) {
-                const uint32_t c = s_cnt[w2][tid];
-                s_cnt[w2][tid] = run;
+                const uint32_t c = s.cnt[w2][tid];
+                s.cnt[w2][tid] = run;
                 run += c;
             }
-            s_len[tid] = run;
+            s.len[tid] = run;
         }
         __syncthreads();
         // an empty constraint (no code): the bits are extracted again here
@@ -204,18 +239,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         // the wave's 16 list starts in four 16-byte LDS loads
         uint4 st4[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) st4[q] = reinterpret_cast<const uint4 *>(&s_cnt[wave][0])[q];
+        for (int qq = 0; qq < 4; ++qq) st4[qq] = reinterpret_cast<const uint4 *>(&s.cnt[wave][0])[qq];
 #pragma unroll
         for (int L = 0; L < 16; ++L) {
+            if (QUAD && (L >> 2) != q) continue;
             const uint64_t bal = __ballot((lists >> L) & 1u);
             const uint4 v4 = st4[L >> 2];
             const uint32_t st = (L & 3) == 0 ? v4.x : (L & 3) == 1 ? v4.y : (L & 3) == 2 ? v4.z : v4.w;
-            if ((lists >> L) & 1u) s_list[L][(uint32_t)__popcll(bal & lt_mask) + st] = (uint8_t)tid;
+            if ((lists >> L) & 1u) s.list[L][(uint32_t)__popcll(bal & lt_mask) + st] = (uint8_t)tid;
         }
-        // the wave's trip count: its longest list (the same for every lane:
-        // kept on scalar registers; shorter lists are padded)
-        const uint32_t n_long = __builtin_amdgcn_readfirstlane(
-            max(max(s_len[4 * wave], s_len[4 * wave + 1]), max(s_len[4 * wave + 2], s_len[4 * wave + 3])));
+        // the wave's trip count, the same for every lane (kept on scalar
+        // registers): its longest list (tile; shorter lists are padded), or
+        // its list's length rounded up to whole groups of four (quadrant)
+        const uint32_t n_long = QUAD
+            ? (__builtin_amdgcn_readfirstlane(s.len[my_list]) + 3u) & ~3u
+            : __builtin_amdgcn_readfirstlane(max(max(s.len[4 * wave], s.len[4 * wave + 1]),
+                                                 max(s.len[4 * wave + 2], s.len[4 * wave + 3])));
         __syncthreads();
         {
             const uint32_t kn = b + kBatch + tid;
@@ -223,73 +262,161 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         }
         // a wave whose pixels have all stopped skips the batch
         const uint32_t n_run = done == ~0ull ? 0u : n_long;
-        // list slots are read four at a time (one aligned 32-bit LDS load
-        // every fourth entry): three iterations in four wait for one LDS
-        // round trip (the staged record) instead of two
-        uint32_t quad = 0;
-        for (uint32_t e = 0; e < n_run; ++e) {
-            if ((e & 3u) == 0u) quad = *reinterpret_cast<const uint32_t *>(&s_list[my_list][e]);
-            const uint32_t j = (quad >> (8u * (e & 3u))) & 255u;
-            const uint32_t jo = j << 4;   // byte offset into the staged arrays
-            const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g0) + jo);
-            const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_g1) + jo);
-            const float dx = g0.x - fpx, dy = g0.y - fpy;
-            // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
-            const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
-            const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
-            // composited or stopping: an entry of a running pixel with power
-            // <= 0 and alpha >= 1/255.  The decisions are wave masks
-            // (compares straight into scalar registers, combined there)
-            const uint64_t hitm = __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
-                                  __builtin_amdgcn_ballot_w64(alpha >= kAlphaMin) & ~done;
-            const float Tn = T * (1.0f - alpha);
-            // T stays above 1e-4 (Tn is never NaN)
-            const uint64_t keepm = __builtin_amdgcn_ballot_w64(Tn >= kTMin);
-            const bool hit = __builtin_amdgcn_inverse_ballot_w64(hitm);
-            const bool inc = __builtin_amdgcn_inverse_ballot_w64(hitm & keepm);
-            const bool stop = __builtin_amdgcn_inverse_ballot_w64(hitm & ~keepm);
-            const float w = inc ? alpha * T : 0.0f;
-            const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s_col) + jo);
-            cr = __builtin_fmaf(w, c.x, cr);
-            cg = __builtin_fmaf(w, c.y, cg);
-            cb = __builtin_fmaf(w, c.z, cb);
-            T = inc ? Tn : T;
-            done |= hitm & ~keepm;
-            if (COUNT) {
-                n_hit += hit ? 1u : 0u;
-                if (stop) stop_pos = b + j;
-            }
-            if (CAPTURE) {
-                const float dep = g1.z;
-                d0 = (inc && !pivot) ? dep : d0;
-                pivot = pivot || inc;
-                const float dd = dep - d0;
-                sw += w;
-                s1 = __builtin_fmaf(w, dd, s1);
-                s2 = __builtin_fmaf(w * dd, dd, s2);
-                // the pixel composites the Gaussian (w = alpha T > 0); the
-                // lanes of a group write the same flag
-                if (inc) s_flag[j] = 1u;
-                if (CONTRIB) {
-                    // max weight over the group's 16 lanes (one Gaussian)
-                    float mw = w;
-#pragma unroll
-                    for (int o = 8; o >= 1; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
-                    if ((lane & 15) == 0 && mw > 0.0f)
-                        atomicMax(reinterpret_cast<unsigned int *>(a.contrib + s_idx[j]),
-                                  __float_as_uint(mw));
+        if (QUAD) {
+            for (uint32_t e = 0; e < n_run; e += 4) {
+                // the group's four slots in one aligned 32-bit LDS load
+                const uint32_t j = (*reinterpret_cast<const uint32_t *>(&s.list[my_list][e]) >> (8 * k)) & 255u;
+                const uint32_t jo = j << 4;   // byte offset into the staged arrays
+                const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g0) + jo);
+                const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g1) + jo);
+                const float dx = g0.x - fpx, dy = g0.y - fpy;
+                const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
+                const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
+                // a running pixel's entry with power <= 0 and alpha >= 1/255
+                const uint64_t hitm = __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
+                                      __builtin_amdgcn_ballot_w64(alpha >= kAlphaMin) & ~done;
+                const bool hit = __builtin_amdgcn_inverse_ballot_w64(hitm);
+                // transmittance through the four entries in list order, one
+                // product at a time (the fp32 products of a sequential walk;
+                // an entry that is no hit multiplies by exactly 1)
+                const float f = hit ? 1.0f - alpha : 1.0f;
+                const float t1 = T * quad_bcast<0>(f);
+                const float t2 = t1 * quad_bcast<1>(f);
+                const float t3 = t2 * quad_bcast<2>(f);
+                const float t4 = t3 * quad_bcast<3>(f);
+                // the pixel stops at the first entry whose product falls
+                // below 1e-4 (a hit; that entry is not composited)
+                const int ks = !(t1 >= kTMin) ? 0 : !(t2 >= kTMin) ? 1 : !(t3 >= kTMin) ? 2
+                             : !(t4 >= kTMin) ? 3 : 4;
+                const float Tin = k == 0 ? T : k == 1 ? t1 : k == 2 ? t2 : t3;
+                const bool inc = hit && k < ks;
+                const float w = inc ? alpha * Tin : 0.0f;
+                const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.col) + jo);
+                cr = __builtin_fmaf(w, c.x, cr);
+                cg = __builtin_fmaf(w, c.y, cg);
+                cb = __builtin_fmaf(w, c.z, cb);
+                const bool stopping = ks < 4;
+                T = ks == 0 ? T : ks == 1 ? t1 : ks == 2 ? t2 : ks == 3 ? t3 : t4;
+                if (COUNT) {
+                    n_hit += (hit && k <= ks) ? 1u : 0u;
+                    if (stopping) {
+                        const uint32_t jk = ks == 0 ? quad_bcast_u<0>(j) : ks == 1 ? quad_bcast_u<1>(j)
+                                          : ks == 2 ? quad_bcast_u<2>(j) : quad_bcast_u<3>(j);
+                        stop_pos = b + jk;
+                    }
                 }
+                if (CAPTURE) {
+                    const float dep = g1.z;
+                    // the pivot: depth of the pixel's first composited entry
+                    if (__builtin_amdgcn_ballot_w64(inc && !pivot)) {
+                        const int km0 = inc ? k : 4;
+                        int km = min(km0, (int)__builtin_amdgcn_mov_dpp(km0, 0xb1, 0xf, 0xf, false));
+                        km = min(km, (int)__builtin_amdgcn_mov_dpp(km, 0x4e, 0xf, 0xf, false));
+                        const float dk = km == 0 ? quad_bcast<0>(dep) : km == 1 ? quad_bcast<1>(dep)
+                                       : km == 2 ? quad_bcast<2>(dep) : quad_bcast<3>(dep);
+                        d0 = (!pivot && km < 4) ? dk : d0;
+                        pivot = pivot || km < 4;
+                    }
+                    const float dd = dep - d0;
+                    sw += w;
+                    s1 = __builtin_fmaf(w, dd, s1);
+                    s2 = __builtin_fmaf(w * dd, dd, s2);
+                    if (inc) s.flag[j] = 1u;
+                    if (CONTRIB) {
+                        // max weight of this lane's entry over the wave's 16 pixels
+                        float mw = w;
+#pragma unroll
+                        for (int o = 4; o <= 32; o <<= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
+                        if (lane < 4 && mw > 0.0f)
+                            atomicMax(reinterpret_cast<unsigned int *>(a.contrib + s.idx[j]),
+                                      __float_as_uint(mw));
+                    }
+                }
+                done |= __builtin_amdgcn_ballot_w64(stopping);
+                if (done == ~0ull) break;
             }
-            if (done == ~0ull) break;
+        } else {
+            // list slots are read four at a time (one aligned 32-bit LDS load
+            // every fourth entry): three iterations in four wait for one LDS
+            // round trip (the staged record) instead of two
+            uint32_t quad = 0;
+            for (uint32_t e = 0; e < n_run; ++e) {
+                if ((e & 3u) == 0u) quad = *reinterpret_cast<const uint32_t *>(&s.list[my_list][e]);
+                const uint32_t j = (quad >> (8u * (e & 3u))) & 255u;
+                const uint32_t jo = j << 4;   // byte offset into the staged arrays
+                const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g0) + jo);
+                const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g1) + jo);
+                const float dx = g0.x - fpx, dy = g0.y - fpy;
+                // log2 of exp(power) with power = -(A dx^2 + 2B dx dy + C dy^2)/2
+                const float p2 = __builtin_fmaf(dx, __builtin_fmaf(g0.z, dx, g0.w * dy), g1.x * dy * dy);
+                const float alpha = fminf(kAlphaMax, g1.y * __builtin_amdgcn_exp2f(p2));
+                // composited or stopping: an entry of a running pixel with power
+                // <= 0 and alpha >= 1/255.  The decisions are wave masks
+                // (compares straight into scalar registers, combined there)
+                const uint64_t hitm = __builtin_amdgcn_ballot_w64(!(p2 > 0.0f)) &
+                                      __builtin_amdgcn_ballot_w64(alpha >= kAlphaMin) & ~done;
+                const float Tn = T * (1.0f - alpha);
+                // T stays above 1e-4 (Tn is never NaN)
+                const uint64_t keepm = __builtin_amdgcn_ballot_w64(Tn >= kTMin);
+                const bool hit = __builtin_amdgcn_inverse_ballot_w64(hitm);
+                const bool inc = __builtin_amdgcn_inverse_ballot_w64(hitm & keepm);
+                const bool stop = __builtin_amdgcn_inverse_ballot_w64(hitm & ~keepm);
+                const float w = inc ? alpha * T : 0.0f;
+                const float4 c = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.col) + jo);
+                cr = __builtin_fmaf(w, c.x, cr);
+                cg = __builtin_fmaf(w, c.y, cg);
+                cb = __builtin_fmaf(w, c.z, cb);
+                T = inc ? Tn : T;
+                done |= hitm & ~keepm;
+                if (COUNT) {
+                    n_hit += hit ? 1u : 0u;
+                    if (stop) stop_pos = b + j;
+                }
+                if (CAPTURE) {
+                    const float dep = g1.z;
+                    d0 = (inc && !pivot) ? dep : d0;
+                    pivot = pivot || inc;
+                    const float dd = dep - d0;
+                    sw += w;
+                    s1 = __builtin_fmaf(w, dd, s1);
+                    s2 = __builtin_fmaf(w * dd, dd, s2);
+                    // the pixel composites the Gaussian (w = alpha T > 0); the
+                    // lanes of a group write the same flag
+                    if (inc) s.flag[j] = 1u;
+                    if (CONTRIB) {
+                        // max weight over the group's 16 lanes (one Gaussian)
+                        float mw = w;
+#pragma unroll
+                        for (int o = 8; o >= 1; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
+                        if ((lane & 15) == 0 && mw > 0.0f)
+                            atomicMax(reinterpret_cast<unsigned int *>(a.contrib + s.idx[j]),
+                                      __float_as_uint(mw));
+                    }
+                }
+                if (done == ~0ull) break;
+            }
         }
         __syncthreads();
-        if (CAPTURE && a.g_flag && tid < kBatch && k < range.y && s_flag[tid])
-            a.g_flag[s_idx[tid]] = 1u;
+        if (CAPTURE && a.g_flag && tid < kBatch && kb < range.y && s.flag[tid])
+            a.g_flag[s.idx[tid]] = 1u;
     }
 
+    if (QUAD) {
+        // a pixel's sums over its four lanes
+        cr = quad_sum(cr);
+        cg = quad_sum(cg);
+        cb = quad_sum(cb);
+        if (CAPTURE) {
+            sw = quad_sum(sw);
+            s1 = quad_sum(s1);
+            s2 = quad_sum(s2);
+        }
+    }
     if (COUNT) {
-        // evaluated list entries: up to and including the stopping one
-        unsigned long long e = inside ? (unsigned long long)(stop_pos < range.y ? stop_pos + 1 : range.y) - range.x : 0ull;
+        // evaluated list entries: up to and including the stopping one (one
+        // lane per pixel), and the hits (every lane its own entries)
+        unsigned long long e = (inside && (!QUAD || k == 0))
+            ? (unsigned long long)(stop_pos < range.y ? stop_pos + 1 : range.y) - range.x : 0ull;
         unsigned long long h = n_hit;
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) {
@@ -311,28 +438,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
         // composited weights are the union of its pixels', so with
         // A = 1 - T (the pixel's summed weight) the block has the pooled
         // D_h = sum A D / sum A and sigma_h^2 = sum A (sigma^2 + (D - D_h)^2)
-        // / sum A.  The blocks lie inside the tile: pooled through LDS (the
-        // staging arrays are free once every wave has left the batch loop).
+        // / sum A.  The blocks lie inside the block's region (the tile or
+        // the quadrant, PW pixels wide): pooled through LDS (the staging
+        // arrays are free once every wave has left the batch loop).
+        constexpr int PW = QUAD ? 8 : kTile, NB = PW / 2;
+        const int ox = QUAD ? 8 * (q & 1) : 0, oy = QUAD ? 8 * (q >> 1) : 0;
         __syncthreads();
-        float *s_pa = reinterpret_cast<float *>(s_g0);   // 3 x 256 floats
+        float *s_pa = reinterpret_cast<float *>(s.g0);   // 3 x 256 floats
         float *s_pd = s_pa + 256, *s_ps = s_pa + 512;
-        const int lp = (py - ty * kTile) * kTile + (px - tx * kTile);
+        const int lp = (py - ty * kTile - oy) * PW + (px - tx * kTile - ox);
         s_pa[lp] = inside ? 1.0f - T : 0.0f;
         s_pd[lp] = D;
         s_ps[lp] = S;
         __syncthreads();
         const int Wg = (a.W + 1) >> 1, Hg = (a.H + 1) >> 1;
-        const int gx = tx * (kTile / 2) + (tid & 7), gy = ty * (kTile / 2) + (tid >> 3);
-        if (tid < 64 && gx < Wg && gy < Hg) {
-            const int l0 = 2 * (tid >> 3) * kTile + 2 * (tid & 7);
-            const int ls[4] = {l0, l0 + 1, l0 + kTile, l0 + kTile + 1};
+        const int gx = tx * (kTile / 2) + ox / 2 + tid % NB, gy = ty * (kTile / 2) + oy / 2 + tid / NB;
+        if (tid < NB * NB && gx < Wg && gy < Hg) {
+            const int l0 = 2 * (tid / NB) * PW + 2 * (tid % NB);
+            const int ls[4] = {l0, l0 + 1, l0 + PW, l0 + PW + 1};
             float sa = 0.0f, sad = 0.0f;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float ak = s_pa[ls[k]];
+            for (int i = 0; i < 4; ++i) {
+                const float ak = s_pa[ls[i]];
                 if (ak > 0.0f) {
                     sa += ak;
-                    sad += ak * s_pd[ls[k]];
+                    sad += ak * s_pd[ls[i]];
                 }
             }
             float dh = a.empty_depth, sh = 0.0f;
@@ -340,10 +470,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
                 dh = sad / sa;
                 float sv = 0.0f;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const float ak = s_pa[ls[k]];
+                for (int i = 0; i < 4; ++i) {
+                    const float ak = s_pa[ls[i]];
                     if (ak > 0.0f) {
-                        const float sk = s_ps[ls[k]], ek = s_pd[ls[k]] - dh;
+                        const float sk = s_ps[ls[i]], ek = s_pd[ls[i]] - dh;
                         sv += ak * (sk * sk + ek * ek);
                     }
                 }
@@ -353,24 +483,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
             a.tgbh_sigma[(size_t)gy * Wg + gx] = sh;
         }
     }
-    if (!inside) return;
+    if (!inside || (QUAD && k != 0)) return;
     const size_t HW = (size_t)a.W * a.H;
-    const size_t q = (size_t)py * a.W + px;
-    a.rgb[q] = cr;
-    a.rgb[HW + q] = cg;
-    a.rgb[2 * HW + q] = cb;
+    const size_t o = (size_t)py * a.W + px;
+    a.rgb[o] = cr;
+    a.rgb[HW + o] = cg;
+    a.rgb[2 * HW + o] = cb;
     if (a.tab) {
-        a.tab[q] = cr;
-        a.tab[HW + q] = cg;
-        a.tab[2 * HW + q] = cb;
+        a.tab[o] = cr;
+        a.tab[HW + o] = cg;
+        a.tab[2 * HW + o] = cb;
     }
     if (CAPTURE) {
-        if (a.depth) a.depth[q] = D;
-        if (a.sigma) a.sigma[q] = S;
-        if (a.alpha) a.alpha[q] = 1.0f - T;
-        if (a.tgb_depth) a.tgb_depth[q] = D;
-        if (a.tgb_sigma) a.tgb_sigma[q] = S;
+        if (a.depth) a.depth[o] = D;
+        if (a.sigma) a.sigma[o] = S;
+        if (a.alpha) a.alpha[o] = 1.0f - T;
+        if (a.tgb_depth) a.tgb_depth[o] = D;
+        if (a.tgb_sigma) a.tgb_sigma[o] = S;
     }
+}
+
+template <bool CAPTURE, bool CONTRIB, bool COUNT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void blend_kernel(BlendArgs a) {
+    __shared__ BlendLds s;
+    // block roles (block-uniform): with a split count, the first 4 n_split
+    // blocks take the quadrants of the first n_split tiles of the blend
+    // order, the rest shift down by 3 n_split; then the tiles, then (TGS
+    // frames) the stitched tiles
+    int blk = (int)blockIdx.x;
+    if (a.n_split_dev) {
+        const int ns = (int)*a.n_split_dev;
+        if (blk < 4 * ns) {
+            blend_block<CAPTURE, CONTRIB, COUNT, true>(a, s, a.tile_list[blk >> 2], blk & 3);
+            return;
+        }
+        blk -= 3 * ns;
+        if (blk >= a.n_grid) return;
+    }
+    if (a.n_tiles_dev && blk >= (int)*a.n_tiles_dev) {
+        if (a.stitch_list) {
+            const int t = a.stitch_list[blk];
+            if (a.stitch_mode == 2)
+                stitch_tile_depth(a.sw, a.stitch_wg, t, a.stitch_tab, a.stitch_dfill, a.rgb);
+            else
+                stitch_tile_uv(a.sw, t, a.stitch_tab, a.stitch_uv, a.rgb);
+        }
+        return;
+    }
+    blend_block<CAPTURE, CONTRIB, COUNT, false>(a, s, a.tile_list ? a.tile_list[blk] : blk, 0);
 }
 
 // Adaptive frustum (Sec. III-D): min / max NDC of the projected means of the
@@ -447,9 +607,13 @@ void launch_blend_v(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t
                               e0, e1, 0, a);
 }
 
-void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t start,
+void launch_blend(const BlendArgs &a0, int n_blocks, hipStream_t st, hipEvent_t start,
                   hipEvent_t stop) {
     if (n_blocks <= 0) return;
+    BlendArgs a = a0;
+    a.n_grid = n_blocks;
+    if (a.n_split_dev && a.tile_list) n_blocks += 3 * kMaxSplit;
+    else a.n_split_dev = nullptr;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma ||
                          a.tgbh_depth || a.g_flag || a.contrib;
     if (a.contrib)

@@ -96,6 +96,14 @@ __device__ void order_tiles_block(const OrderK &o, uint32_t *s_cnt) {
                 if (tid >= d) inc += o;
             }
             if (b >= 0) s_cnt[b] = inc - c;
+            // the tiles the blend splits, a prefix of the order: those of
+            // the buckets from the lowest one >= split_bucket that leaves at
+            // most max_split tiles in it and above (whole buckets, so the set
+            // does not depend on the order within a bucket)
+            const int sb = o.split_bucket;
+            const uint64_t fit = __ballot(sb >= 1 && b >= sb && inc <= (uint32_t)o.max_split);
+            const uint32_t ns = __shfl(inc, fit ? 63 - __clzll((long long)fit) : 0);
+            if (o.n_split && tid == 0) *o.n_split = fit ? ns : 0u;
             const uint64_t nz = __ballot(c != 0u);
             // the host reads this value some frames later: no fence needed
             if (max_bucket && tid == 0)

@@ -384,6 +384,10 @@ tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const 
 // global depth sort), 1 = always the global depth sort, 2 = always the
 // per-tile sort.
 int g_sort_path = 0;
+// list length bucket from which the blend splits tiles into quadrants (0:
+// never), and the most tiles split
+int g_split_bucket = kSplitBucket;
+int g_split_max = kMaxSplit;
 constexpr int kSegSmallScene = 131072;
 
 // The Gaussians that have keys and the start of their keys, in the order the
@@ -513,6 +517,9 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     order.ranges = ws.ranges.as<uint2>();
     order.tile_out = ws.tile_order.as<int>();
     order.max_bucket = ws.host_maxb_dev + (rowpre ? 1 : 0);
+    order.n_split = &cnt->n_split;
+    order.split_bucket = g_split_bucket;
+    order.max_split = g_split_max;
     if (ws.frame_seg) {
         // each tile's list, emitted in index order, by (depth bits, index)
         ProfScope ps(TGS_PROF_SORT, st);
@@ -587,6 +594,16 @@ tgs_status tgs_set_sort_path(int32_t mode) {
     g_err.clear();
     if (mode < 0 || mode > 2) return fail(TGS_ERR_INVALID_ARG, "sort path must be 0, 1 or 2");
     g_sort_path = mode;
+    return TGS_OK;
+}
+
+tgs_status tgs_set_blend_split(int32_t log2_min, int32_t max_tiles) {
+    g_err.clear();
+    if (log2_min < -1 || log2_min > 31) return fail(TGS_ERR_INVALID_ARG, "log2_min must be in [-1, 31]");
+    if (max_tiles < 0 || max_tiles > kMaxSplit)
+        return fail(TGS_ERR_INVALID_ARG, "max_tiles must be in [0, " + std::to_string(kMaxSplit) + "]");
+    g_split_bucket = log2_min + 1;
+    g_split_max = max_tiles;
     return TGS_OK;
 }
 
@@ -795,6 +812,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, W, H, vals);
         a.tile_list = ws.tile_order.as<int>();
+        a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
         a.rgb = out->rgb;
         a.depth = out->depth;
         a.sigma = out->sigma;
@@ -996,6 +1014,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                               st, &vals));
             BlendArgs a = blend_args(ws, W, H, vals);
             a.tile_list = ws.tile_order.as<int>();
+            a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
             a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
             a.rgb = out->rgb;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
@@ -1027,6 +1046,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
             BlendArgs a = blend_args(ws, W, H, vals);
             a.tile_list = ws.tile_order.as<int>();
+            a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
             a.rgb = out->rgb;
             a.tab = s->tab.as<float>();
             a.depth = out->depth;

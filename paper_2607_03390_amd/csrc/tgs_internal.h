@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include "tgs.h"
 
 namespace tgs {
 
@@ -81,7 +82,8 @@ struct Counters {
     uint32_t n_selected;
     uint32_t n_visible;       // Gaussians with at least one key
     uint32_t n_sorted;        // keys emitted and sorted: n_keys, or 0 past the key capacity
-    uint32_t pad[2];
+    uint32_t n_split;         // tiles the blend splits into quadrants (the blend order's first)
+    uint32_t pad;
 };
 
 // The frame's counters as the host reads them: written by the last counting
@@ -190,6 +192,13 @@ struct OrderK {
     const uint2 *ranges;
     int *tile_out;
     uint32_t *max_bucket;
+    // optional: the number of tiles the blend splits, the first of the
+    // order: those whose list length bucket is at least split_bucket, or, if
+    // more than max_split (<= kMaxSplit) are, at least the lowest higher
+    // bucket that leaves at most max_split (0: no split)
+    uint32_t *n_split;
+    int split_bucket;
+    int max_split;
 };
 void launch_order_tiles(const OrderK &o, hipStream_t st);
 
@@ -275,6 +284,11 @@ struct BlendArgs {
     int W, H, TX, TY;
     const int *tile_list;     // NULL: blockIdx = tile
     const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
+    // optional (with tile_list): the first *n_split_dev (<= kMaxSplit) tiles
+    // of tile_list are blended as four quadrant blocks each; the launch adds
+    // 3 kMaxSplit blocks (n_grid: the launch's tile blocks, set by launch_blend)
+    const uint32_t *n_split_dev;
+    int n_grid;
     const uint2 *ranges;
     const uint32_t *vals;
     const float4 *g;          // 64-byte records (Records::g)
@@ -303,6 +317,12 @@ struct BlendArgs {
     const float *stitch_dfill;
     WarpK sw;
 };
+// Longest lists split into quadrant blocks by the blend: at most kMaxSplit
+// tiles (the launch adds 3 kMaxSplit blocks; those without a quadrant exit
+// at once), by default those of kSplitBucket (lists of 2^(kSplitBucket-1)
+// entries) and up.
+constexpr int kMaxSplit = TGS_BLEND_SPLIT_MAX;
+constexpr int kSplitBucket = TGS_BLEND_SPLIT_DEFAULT + 1;
 // start/stop (may be NULL) are attached to the dispatch itself
 // (hipExtLaunchKernelGGL): kernel timing without extra barrier packets.
 void launch_blend(const BlendArgs &a, int n_blocks, hipStream_t st, hipEvent_t start = nullptr,

@@ -28,10 +28,14 @@ EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_sce
             "tgs_scene_set_tile_bound",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
-            "tgs_profile_start", "tgs_profile_stop", "tgs_set_sort_path", "tgs_last_error"]
+            "tgs_profile_start", "tgs_profile_stop", "tgs_set_sort_path", "tgs_set_blend_split",
+            "tgs_last_error"]
 
 # tgs_set_sort_path modes
 SORT_AUTO, SORT_DEPTH_FIRST, SORT_PER_TILE = 0, 1, 2
+# tgs_set_blend_split: default log2 of the list length from which tiles are
+# split into quadrant blocks, and the most tiles split per frame
+BLEND_SPLIT_DEFAULT, BLEND_SPLIT_MAX = 12, 1024
 
 PROF_STAGES = ["preprocess", "scan", "readback", "duplicate", "sort", "ranges", "blend_full",
                "blend_ref", "blend_tgs", "warp", "fill_query", "occluded", "select", "stitch",
@@ -111,6 +115,8 @@ def lib():
         L.tgs_debug_dump.argtypes = [vp, vp, i32, vp, C.POINTER(sz)]
         L.tgs_profile_start.argtypes = [i32]
         L.tgs_profile_stop.argtypes = [C.POINTER(tgs_profile)]
+        L.tgs_set_sort_path.argtypes = [i32]
+        L.tgs_set_blend_split.argtypes = [i32, i32]
         for name in EXPORTED:
             if name not in ("tgs_last_error", "tgs_params_default", "tgs_scene_free",
                             "tgs_state_free", "tgs_scene_count"):
@@ -281,6 +287,13 @@ def tgs_set_sort_path(mode):
     SORT_DEPTH_FIRST (global depth sort, keys emitted in depth order) or
     SORT_PER_TILE (keys in index order, each tile's list sorted)."""
     _check(lib().tgs_set_sort_path(int(mode)))
+
+
+def tgs_set_blend_split(log2_min=BLEND_SPLIT_DEFAULT, max_tiles=BLEND_SPLIT_MAX):
+    """Tiles with at least 2**log2_min list entries are blended as four
+    quadrant blocks (process-wide; -1: never); if more than max_tiles tiles
+    qualify, the threshold doubles until at most max_tiles do."""
+    _check(lib().tgs_set_blend_split(int(log2_min), int(max_tiles)))
 
 
 def tgs_profile_start(count_pairs=False, stages=False):

@@ -122,6 +122,22 @@ def test_tile_bound_rejects_bad_input_on_host():
         assert "tile bound" in L.tgs_last_error().decode()
 
 
+def test_process_wide_settings_reject_bad_values():
+    L = tgs.lib()
+    for bad in (-1, 3):
+        assert L.tgs_set_sort_path(bad) == tgs.TGS_ERR_INVALID_ARG
+    for bad in (-2, 32):
+        assert L.tgs_set_blend_split(bad, 16) == tgs.TGS_ERR_INVALID_ARG
+        assert "log2_min" in L.tgs_last_error().decode()
+    for bad in (-1, tgs.BLEND_SPLIT_MAX + 1):
+        assert L.tgs_set_blend_split(0, bad) == tgs.TGS_ERR_INVALID_ARG
+        assert "max_tiles" in L.tgs_last_error().decode()
+    # valid values only set variables (no GPU work)
+    assert L.tgs_set_blend_split(-1, 0) == 0
+    assert L.tgs_set_blend_split(tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX) == 0
+    assert L.tgs_set_sort_path(tgs.SORT_AUTO) == 0
+
+
 def test_state_create_rejects_bad_params_on_host():
     L = tgs.lib()
     h = C.c_void_p()

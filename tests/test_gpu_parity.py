@@ -142,6 +142,83 @@ def test_long_lists_after_short_ones(sort_path):
     _full_parity(sc, [away, near], label="long after short")
 
 
+@pytest.fixture(params=[(0, tgs.BLEND_SPLIT_MAX), (0, 40)], ids=["split_all", "split_capped"])
+def split_all(request):
+    """Quadrant blocks for every tile with a non-empty list, or (capped) for
+    the tiles of the longest length classes that hold at most 40 tiles, the
+    other tiles whole."""
+    tgs.tgs_set_blend_split(*request.param)
+    yield request.param
+    tgs.tgs_set_blend_split(tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX)
+
+
+@pytest.mark.parametrize("n,seed,deg,W,H", [(3000, 1, 3, 200, 136), (500, 2, 2, 37, 53),
+                                            (4000, 5, 3, 64, 64)])
+def test_split_blend_full_parity(split_all, n, seed, deg, W, H):
+    """Quadrant blocks (the first 64 tiles of the blend order) next to whole
+    tiles, ragged images: colour, moments and the Gaussian buffer against the
+    oracle."""
+    sc = synth.small_scene(n, seed, degree=deg)
+    cams = [synth.make_camera(synth.look_at(e, (0, 0, 0)), W, H)
+            for e in ((0.2, -3.0, 0.7), (2.5, 1.0, -0.4))]
+    _full_parity(sc, cams, label=f"split {W}x{H}")
+
+
+def test_split_blend_long_lists(split_all):
+    """Quadrant blocks on lists of several thousand entries (many batches,
+    pixels stopping inside a group of four entries)."""
+    sc = synth.scene_uniform_cube(24_000, 11, degree=0, log_scale_mean=-2.6)
+    cam = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (0, 0, 0)), 48, 40)
+    _full_parity(sc, [cam], label="split long lists")
+
+
+@pytest.mark.parametrize("pkw", [dict(), dict(tgb_downscale=2)])
+def test_split_blend_temporal_parity(split_all, pkw):
+    """Reference frames (capture of Eq. 1/2, pooled 2x2 geometry buffer on a
+    ragged grid) and TemporalGS frames (split selected tiles, stitched tiles
+    shifted past the quadrant blocks) with quadrant blocks."""
+    sc = synth.scene_room(60_000, 2)
+    cams = synth.handheld_path(10, (0.0, -5.0, 0.3), (0.0, 0.0, 0.0), 0.3, 0.01, 401, 233)
+    st = _temporal_parity(sc, cams, 401, 233, f"split room60k {pkw}", **pkw)
+    assert st["tgs"] >= 3
+
+
+def test_split_blend_determinism(split_all):
+    """Which tiles are split depends on whole length classes, never on the
+    order of tiles within one: a replay gives the same bits."""
+    import torch
+    w = synth.workload("tiny", n_frames=4)
+    with Uploaded(w.scene) as h:
+        runs = []
+        for rep in range(2):
+            frames = []
+            for cam in w.cameras:
+                o = tgs.alloc_frame(256, 256, w.scene.n, depth=True)
+                tgs.tgs_render_full(h, cam, **o)
+                torch.cuda.synchronize()
+                frames.append(torch.cat([o["rgb"].flatten(), o["depth"].flatten(),
+                                         o["sigma"].flatten()]).cpu().numpy())
+            runs.append(frames)
+        for a, b in zip(*runs):
+            assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_split_blend_pair_count(split_all):
+    """Evaluated pairs and hits of quadrant blocks: one count per pixel for
+    the entries up to its stopping one, one per entry for the hits."""
+    w = synth.workload("tiny", n_frames=2)
+    with Uploaded(w.scene) as h:
+        for cam in w.cameras:
+            tgs.tgs_profile_start(count_pairs=True)
+            gpu_full(h, cam, w.scene.n, depth=False, contrib=False)
+            prof = tgs.tgs_profile_stop()
+            r = O.render_full(w.scene, cam)
+            got, hits = prof["blend_full"]["pairs"], prof["blend_full"]["hits"]
+            log(f"    split: pairs gpu {got} oracle {r['pairs']}; hits gpu {hits} oracle {r['hits']}")
+            assert abs(got - r["pairs"]) <= 1e-3 * r["pairs"]
+            assert abs(hits - r["hits"]) <= 1e-3 * r["hits"]
+
+
 @pytest.mark.parametrize("W,H,log_scale", [(3840, 2160, -3.6), (7680, 4320, -3.6),
                                            (3840, 2160, -2.2)])
 def test_full_parity_large_grids(W, H, log_scale):
