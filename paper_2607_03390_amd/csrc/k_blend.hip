@@ -20,8 +20,13 @@
 // composites are flagged through a wave ballot, so the temporal Gaussian
 // buffer costs one scalar test per record and wave.
 //
-// In a TemporalGS frame the blocks past the selected tiles stitch the other
-// tiles from the reference image (stitch.h) while the long tiles finish.
+// The tiles with the longest lists (the first of the blend order, counted
+// by the order kernel) are blended by four blocks each, one per 8x8
+// quadrant, four lanes per pixel on four consecutive list entries: on large
+// scenes a few tiles with tens of batches would otherwise set the launch's
+// tail.  In a TemporalGS frame the blocks past the selected tiles stitch the
+// other tiles from the reference image (stitch.h) while the long tiles
+// finish.
 #include <hip/hip_ext.h>
 
 #include "stitch.h"
