@@ -70,6 +70,7 @@ __device__ inline uint32_t key_tile(uint32_t r, ushort4 rc, const uint32_t *rowp
 // capacity (cnt->n_sorted == 0 with keys) nothing is emitted: the host grows
 // the buffers and renders the frame again.
 constexpr int kDupKeys = kKeyBlock;
+static_assert(kDupKeys % 256 == 0, "whole keys per thread");
 
 __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
                                                         const uint32_t *__restrict__ didx,
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
     for (int k = tid; k < kDupKeys; k += 256) s_owner[k] = -1;
     const uint32_t j0 = kfirst[blockIdx.x];   // owner of key P0 (offs[j0] <= P0)
     __syncthreads();
-    // at most 1024 Gaussians after j0 start inside the block's keys
+    // at most kDupKeys Gaussians after j0 start inside the block's keys
     for (int k = tid; k <= kDupKeys; k += 256) {
         const uint32_t j = j0 + (uint32_t)k;
         if (j < V) {
@@ -105,11 +106,12 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
         }
     }
     __syncthreads();
-    // inclusive max-scan of the marks: four consecutive entries per thread
-    int v[4], m = -1;
+    // inclusive max-scan of the marks: kPer consecutive entries per thread
+    constexpr int kPer = kDupKeys / 256;
+    int v[kPer], m = -1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        m = max(m, s_owner[4 * tid + i]);
+    for (int i = 0; i < kPer; ++i) {
+        m = max(m, s_owner[kPer * tid + i]);
         v[i] = m;
     }
     int inc = m;
@@ -124,10 +126,10 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
     __syncthreads();
     for (int w = 0; w < wave; ++w) ex = max(ex, s_wmax[w]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s_owner[4 * tid + i] = max(v[i], ex);
+    for (int i = 0; i < kPer; ++i) s_owner[kPer * tid + i] = max(v[i], ex);
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < kPer; ++k) {
         const uint32_t i = (uint32_t)(tid + 256 * k);
         const uint32_t p = P0 + i;
         if (p < P1) {
