@@ -511,18 +511,23 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void blend_kernel(BlendArgs a) {
     __shared__ BlendLds s;
-    // block roles (block-uniform): with a split count, the first 4 n_split
-    // blocks take the quadrants of the first n_split tiles of the blend
-    // order, the rest shift down by 3 n_split; then the tiles, then (TGS
-    // frames) the stitched tiles
+    // block roles (block-uniform): with a split count ns, the first
+    // nq = 4 ceil8(ns) blocks take the quadrants of the first ns tiles of the
+    // blend order, the rest shift down by nq - ns; then the tiles, then (TGS
+    // frames) the stitched tiles.  Blocks are dealt to the eight XCDs in
+    // turn (block b on XCD b mod 8), so block b takes quadrant (b >> 3) & 3
+    // of split tile 8 (b >> 5) + (b & 7): the four blocks of a tile, which
+    // stage the same records, share one XCD's L2.
     int blk = (int)blockIdx.x;
     if (a.n_split_dev) {
         const int ns = (int)*a.n_split_dev;
-        if (blk < 4 * ns) {
-            blend_block<CAPTURE, CONTRIB, COUNT, true>(a, s, a.tile_list[blk >> 2], blk & 3);
+        const int nq = 4 * ((ns + 7) & ~7);
+        if (blk < nq) {
+            const int t = 8 * (blk >> 5) + (blk & 7);
+            if (t < ns) blend_block<CAPTURE, CONTRIB, COUNT, true>(a, s, a.tile_list[t], (blk >> 3) & 3);
             return;
         }
-        blk -= 3 * ns;
+        blk -= nq - ns;
         if (blk >= a.n_grid) return;
     }
     if (a.n_tiles_dev && blk >= (int)*a.n_tiles_dev) {
@@ -617,7 +622,8 @@ void launch_blend(const BlendArgs &a0, int n_blocks, hipStream_t st, hipEvent_t 
     if (n_blocks <= 0) return;
     BlendArgs a = a0;
     a.n_grid = n_blocks;
-    if (a.n_split_dev && a.tile_list) n_blocks += 3 * kMaxSplit;
+    // the quadrant blocks: 4 ceil8(n_split) <= 3 kMaxSplit + 28 more than the tiles
+    if (a.n_split_dev && a.tile_list) n_blocks += 3 * kMaxSplit + 28;
     else a.n_split_dev = nullptr;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma ||
                          a.tgbh_depth || a.g_flag || a.contrib;

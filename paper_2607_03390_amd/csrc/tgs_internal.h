@@ -286,7 +286,8 @@ struct BlendArgs {
     const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
     // optional (with tile_list): the first *n_split_dev (<= kMaxSplit) tiles
     // of tile_list are blended as four quadrant blocks each; the launch adds
-    // 3 kMaxSplit blocks (n_grid: the launch's tile blocks, set by launch_blend)
+    // 3 kMaxSplit + 28 blocks (n_grid: the launch's tile blocks, set by
+    // launch_blend)
     const uint32_t *n_split_dev;
     int n_grid;
     const uint2 *ranges;
