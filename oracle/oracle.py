@@ -421,8 +421,11 @@ class TemporalOracle:
             self.since_true += 1
             self.since_ref += 1
             if self.p.enable_sr:
-                # adaptive reference insertion: "exceeds" eta of all tiles
-                self.force_pseudo = n_selected > self.p.eta * self.TX * self.TY
+                # adaptive reference insertion: "exceeds" eta of all tiles.
+                # eta is a float32 parameter of the interface, so the product
+                # is taken with that float32 value, widened exactly
+                eta = float(np.float32(self.p.eta))
+                self.force_pseudo = n_selected > eta * (self.TX * self.TY)
 
     def _reference(self, cam, kind):
         cull = None

@@ -459,6 +459,126 @@ def test_lateral_translation_unmatched_strip():
     assert np.array_equal(um.any(0), np.array([expect_cols[16 * k:16 * k + 16].any() for k in range(W // 16)]))
 
 
+def _bilinear_field(W, H):
+    """A TAB whose channels are bilinear in the pixel coordinates,
+    I = a + b x + c y + e x y: bilinear interpolation reproduces such a
+    field exactly at any sub-pixel point, nearest-pixel sampling does not,
+    and the distinct x and y slopes catch transposed weights."""
+    ys, xs = np.mgrid[0:H, 0:W].astype(np.float64)
+    coef = [(0.10, 0.0040, 0.0025, 1.0e-5), (0.30, -0.0020, 0.0050, -2.0e-5),
+            (0.55, 0.0015, -0.0030, 3.0e-5)]
+    tab = np.stack([a + b * xs + c * ys + e * xs * ys for a, b, c, e in coef]).astype(np.float32)
+    return tab, coef
+
+
+def _field_at(coef, u, v):
+    return np.stack([a + b * u + c * v + e * u * v for a, b, c, e in coef])
+
+
+def test_stitch_is_bilinear_at_subpixel_shift():
+    """Eq. 4 samples the reference image bilinearly (Sec. III-C): after a
+    sub-pixel lateral and vertical translation over a fronto-parallel plane,
+    each matched pixel's correspondence is the closed-form shifted position
+    and the stitched value is the bilinear field at it."""
+    W, H = 96, 64
+    cam = _cam(np.eye(4), W, H)
+    Z = 5.0
+    dx, dy = 0.37 * Z / cam.fx, -0.29 * Z / cam.fy      # shifts of 0.37 and -0.29 px
+    cur = np.eye(4, dtype=np.float32)
+    cur[0, 3], cur[1, 3] = -dx, -dy
+    M, Mi = O.relative_pose(np.eye(4, dtype=np.float32), cur)
+    D = np.full((H, W), Z, np.float32)
+    dmin, _ = O.forward_warp(D, np.zeros_like(D), _intr(cam), _intr(cam), M)
+    dfill = O.depth_fill(dmin)
+    uv, matched, _ = O.backward_query(dfill, _intr(cam), _intr(cam), Mi)
+    m = matched.astype(bool)
+    assert m.mean() > 0.9
+    ys, xs = np.mgrid[0:H, 0:W]
+    # a point seen at pixel x of the moved camera sits at x + f dx / Z in the
+    # reference view (and likewise in y)
+    np.testing.assert_allclose(uv[..., 0][m], (xs + cam.fx * dx / Z)[m], atol=1e-3)
+    np.testing.assert_allclose(uv[..., 1][m], (ys + cam.fy * dy / Z)[m], atol=1e-3)
+    tab, coef = _bilinear_field(W, H)
+    out = np.zeros((3, H, W))
+    O.stitch(tab, uv, np.zeros(((H + 15) // 16, (W + 15) // 16), np.uint8), out)
+    want = _field_at(coef, uv[..., 0].astype(np.float64), uv[..., 1].astype(np.float64))
+    np.testing.assert_allclose(out[:, m], want[:, m], atol=1e-6)
+    # the sample points are genuinely between pixel centres
+    frac = uv[..., 0][m] - np.floor(uv[..., 0][m])
+    assert np.all((frac > 0.3) & (frac < 0.45))
+
+
+def test_stitch_depth_is_bilinear_and_clamped():
+    """Eq. 4 from the half-resolution geometry buffer: every pixel is
+    unprojected with its block's depth and the reference image is sampled
+    bilinearly at the projection, clamped to the image (the border columns
+    and rows whose projection leaves it take the edge value)."""
+    W, H = 70, 46
+    cam = _cam(np.eye(4), W, H)
+    Z = 4.0
+    sx, sy = 0.61, 0.23                                   # pixels, in the reference view
+    cur = np.eye(4, dtype=np.float32)
+    cur[0, 3], cur[1, 3] = -sx * Z / cam.fx, -sy * Z / cam.fy
+    _, Mi = O.relative_pose(np.eye(4, dtype=np.float32), cur)
+    dfill_h = np.full(((H + 1) // 2, (W + 1) // 2), Z, np.float32)
+    tab, coef = _bilinear_field(W, H)
+    out = np.zeros((3, H, W))
+    O.stitch_depth(tab, dfill_h, _intr(cam), _intr(cam), Mi, 0.2,
+                   np.zeros(((H + 15) // 16, (W + 15) // 16), np.uint8), out)
+    ys, xs = np.mgrid[0:H, 0:W].astype(np.float64)
+    u = np.clip(xs + sx, 0, W - 1)
+    v = np.clip(ys + sy, 0, H - 1)
+    want = _field_at(coef, u, v)
+    np.testing.assert_allclose(out, want, atol=1e-6)
+    # the last column and row are clamped (their projection leaves the image)
+    assert np.all(xs[:, -1] + sx > W - 1) and np.all(ys[-1] + sy > H - 1)
+    np.testing.assert_allclose(out[:, :, -1], _field_at(coef, np.full(H, W - 1.0), v[:, -1]), atol=1e-6)
+
+
+def test_warp_collisions_keep_min_depth_and_max_sigma():
+    """Eq. 3 with many-to-one destinations: two fronto-parallel planes seen
+    by a camera moved sideways shift by f dx / Z pixels each, so the nearer
+    plane's pixels land on the farther plane's.  Each destination keeps the
+    smallest warped depth and, independently, the largest sigma among its
+    sources (Sec. III-C: maximum depth standard deviation), even where the
+    nearest source has the smaller sigma."""
+    W, H = 80, 40
+    cam = _cam(np.eye(4), W, H)
+    Z1, Z2 = 2.0, 4.0
+    dx = 0.25
+    cur = np.eye(4, dtype=np.float32)
+    cur[0, 3] = -dx
+    M, _ = O.relative_pose(np.eye(4, dtype=np.float32), cur)
+    rng = np.random.default_rng(8)
+    near = rng.random((H, W)) < 0.5
+    D = np.where(near, Z1, Z2).astype(np.float32)
+    # the near plane carries the small deviations
+    S = np.where(near, rng.uniform(0.0, 0.1, (H, W)), rng.uniform(0.2, 0.6, (H, W))).astype(np.float32)
+    dmin, smax = O.forward_warp(D, S, _intr(cam), _intr(cam), M)
+    # closed-form destinations: x' = x - f dx / Z, rows unchanged
+    ys, xs = np.mgrid[0:H, 0:W]
+    u = xs - cam.fx * dx / D.astype(np.float64)
+    xd = np.floor(u + 0.5).astype(int)
+    safe = np.abs(u - np.floor(u) - 0.5) > 1e-3
+    assert safe.all()
+    inside = (xd >= 0) & (xd < W)
+    want_d = np.full((H, W), np.inf)
+    want_s = np.zeros((H, W))
+    n_src = np.zeros((H, W), int)
+    for y, x, xx in zip(ys[inside], xs[inside], xd[inside]):
+        want_d[y, xx] = min(want_d[y, xx], float(D[y, x]))
+        want_s[y, xx] = max(want_s[y, xx], float(S[y, x]))
+        n_src[y, xx] += 1
+    hit = n_src > 0
+    assert np.array_equal(dmin != O.NOHIT, hit)
+    np.testing.assert_allclose(dmin[hit], want_d[hit], rtol=1e-6)
+    assert np.array_equal(smax[hit], want_s[hit].astype(np.float32))
+    # the case the rule decides: a near source (small sigma) wins the depth
+    # while a farther one brings the larger sigma
+    both = hit & (np.abs(dmin - Z1) < 1e-4) & (smax >= 0.2)
+    assert both.sum() > 50 and (n_src[both] >= 2).all()
+
+
 def test_depth_fill_examples():
     N = O.NOHIT
     a = np.full((5, 5), 3.0, np.float32)
@@ -640,6 +760,21 @@ def test_schedule_pattern_and_eta():
     T.advance(T.next_kind(), 40)            # TGS frame at exactly eta: no insertion
     assert T.next_kind() == O.TGS_FRAME
     T.advance(O.TGS_FRAME, 41)              # exceeds eta
+    assert T.next_kind() == O.PSEUDO_REF
+
+
+def test_eta_taken_at_float32():
+    """eta reaches the library as a float32: 0.7 is stored as 0.69999999,
+    so on 120 x 68 tiles 5712 selected tiles exceed eta of all tiles
+    (0.7 x 8160 = 5712 in exact arithmetic would not)."""
+    T = O.TemporalOracle.__new__(O.TemporalOracle)
+    T.p = O.Params(eta=0.7)
+    T.TX, T.TY = 120, 68
+    T.reset()
+    T.advance(T.next_kind(), 8160)
+    T.advance(O.TGS_FRAME, 5711)
+    assert T.next_kind() == O.TGS_FRAME
+    T.advance(O.TGS_FRAME, 5712)
     assert T.next_kind() == O.PSEUDO_REF
 
 
