@@ -7,13 +7,21 @@ schedule renders true references, pseudo references and TemporalGS frames
 one through the HIP kernels of libtgs.  The scene is resident in HBM before
 the timed region starts.
 
-Printed (one JSON line): temporal-mode FPS (value), full-render FPS over the
-same path (both with the 3DGS 3-sigma tile rule and the paper-literal empty
-pixels; the same timings with the alpha-footprint tile rule and with empty
-pixels on the far plane alongside), PSNR of temporal vs full, the roofline of the dominant kernel (its
-launch durations from HIP events attached to its dispatches inside the timed
-region), a per-stage breakdown from an untimed pass, and the CPU oracle timed
-on a bounded sample of the same workload.
+Printed (one JSON line): temporal-mode FPS (value: the median of three
+timed runs of --steps steps), full-render FPS over the same path (both with
+the 3DGS 3-sigma tile rule and the paper-literal empty pixels; the same
+timings with the alpha-footprint tile rule and with empty pixels on the far
+plane alongside), PSNR and SSIM of temporal vs full, the roofline of the
+dominant kernel (the one with the largest summed time in the timed region,
+among the preprocess and blend dispatches, which carry HIP events of their
+own), the blend's roofline on both work units, the whole-frame roofline per
+frame kind, a per-stage breakdown from an untimed pass, and the CPU oracle
+timed on a bounded sample of the same workload.
+
+Helper modes that only read files (for the summaries under profiles/):
+--aggregate-counters (per-kernel means of a rocprofv3 counter CSV),
+--traffic-summary (calibrated HBM bytes and GB/s per kernel) and
+--trace-summary (a kernel-trace stats table).
 """
 from __future__ import annotations
 
@@ -37,13 +45,62 @@ METRIC = "ms/frame & FPS (full vs temporal) at 1080p, 1.5M Gaussians; PSNR tempo
 # depth offset, two moment updates: 5) = 24.  Pairs below the threshold cost
 # nothing algorithmically (a blender may reject them by footprint bounds).
 BLEND_OPS_PER_HIT = {"blend_ref": 24, "blend_tgs": 19, "blend_full": 19}
+# the same pairs priced per evaluated list pair (25 lane-ops each), the unit
+# the work was first scoped in: the kernel rejects most list pairs by
+# footprint bounds before any per-pixel arithmetic, so on this unit the
+# fraction exceeds 1
+OPS_PER_EVALUATED_PAIR = 25
 # non-packed fp32 VALU issue rate: 256 CUs x 64 lanes x 2.4 GHz
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "blend_traffic_room.json")
-# sources the blend kernel is compiled from (its traffic counters are valid
-# for these exact files)
-BLEND_SRCS = [os.path.join(ROOT, "paper_2607_03390_amd", "csrc", f)
-              for f in ("k_blend.hip", "stitch.h", "tgs_internal.h")]
+HBM_PEAK_GBS = 8000.0
+# HBM counters per kernel (FETCH_SIZE / WRITE_SIZE, copy-calibrated),
+# valid for the kernel sources they were taken with
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kernel_traffic_room.json")
+CSRC = os.path.join(ROOT, "paper_2607_03390_amd", "csrc")
+# kernel-trace names of the timed stages
+STAGE_KERNELS = {"preprocess": "preprocess_kernel", "blend_ref": "blend_kernel<true, false, false>",
+                 "blend_tgs": "blend_kernel<false, false, false>",
+                 "blend_full": "blend_kernel<false, false, false>"}
+
+
+def preprocess_bytes(n, deg, n_surv, n_rect, kind, px):
+    """Algorithmic HBM bytes of one preprocess launch as the kernel is built:
+    per Gaussian its mean and opacity read (16 B) and its tile rectangle,
+    key count, depth key and status written (17 B); per survivor of the
+    culls its scale and rotation (32 B); per survivor with a tile rectangle
+    its SH coefficients (12 (deg+1)^2 B) and its 64-byte record.  Reference
+    frames also clear the temporal Gaussian buffer (1 B per Gaussian);
+    TemporalGS frames run the depth fill and correspondence query in the
+    same launch (per pixel: warped depth read 4 B, repaired depth 4 B and
+    correspondence 8 B written, the other warp pair reset 8 B).  The
+    occlusion tests' reads of the warped buffers are left out."""
+    b = 33 * n + 32 * n_surv + (12 * (deg + 1) ** 2 + 64) * n_rect
+    if kind in (0, 1):
+        b += n
+    if kind == 2:
+        b += 24 * px
+    return b
+
+
+def frame_roofline_bytes(n, deg, kind, n_surv, K, px, px_rendered, hits):
+    """Algorithmic bytes and VALU lane-ops of one frame by the stage model of
+    the scoped work (what the method must move, not what a design avoids):
+    cull 12 N + N/8; preprocess (sh + 52) N_s with sh = 236 at degree 3
+    (56 at 0); duplication 12 N_s + 12 K; a six-pass 64-bit key sort
+    8 K + 24 p K; ranges 8 K; blend 40 K + 12 P_r, plus 12 P + 4 N of priors
+    on references; TemporalGS warps 8 P (read) + 8 P (atomics) + 8 P (fill)
+    + 12 P (query) + 24 (P - P_r) (stitch).  Blend lane-ops: 19 per blended
+    pair (24 with the Eq. 1/2 capture of references)."""
+    sh = 236 if deg == 3 else 56 if deg == 0 else 12 * (deg + 1) ** 2 + 44
+    p = 6 if deg > 0 else 5
+    B = {"cull": 12 * n + n / 8, "preprocess": (sh + 52) * n_surv, "duplicate": 12 * n_surv + 12 * K,
+         "sort": 8 * K + 24 * p * K, "ranges": 8 * K, "blend": 40 * K + 12 * px_rendered}
+    if kind in (0, 1):
+        B["blend"] += 12 * px + 4 * n
+    if kind == 2:
+        B["warp"] = 8 * px + 8 * px + 8 * px + 12 * px + 24 * (px - px_rendered)
+    ops = (24 if kind in (0, 1) else 19) * hits
+    return B, ops
 
 
 def log(msg):
@@ -57,8 +114,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="room")
     ap.add_argument("--frames", type=int, default=None, help="truncate the camera path")
-    ap.add_argument("--cpu-frames", type=int, default=3,
-                    help="frames of the path the CPU oracle renders for its baseline")
+    ap.add_argument("--runs", type=int, default=3,
+                    help="timed runs of --steps steps each; value is the median run")
+    ap.add_argument("--cpu-frames", type=int, default=None,
+                    help="temporal frames of the path the CPU oracle renders for its baseline "
+                         "(default 2 lambda_SR + 1 = 11), plus --cpu-full-frames full renders")
+    ap.add_argument("--cpu-full-frames", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-psnr", action="store_true")
     ap.add_argument("--no-footprint", action="store_true",
@@ -70,24 +131,156 @@ def parse():
                     help="geometry-buffer downscale (1 or 2); default: 2 for the large-scale "
                          "city workload (the paper's large-scene setting), 1 otherwise")
     ap.add_argument("--sort-path", default="auto", choices=["auto", "depth_first", "per_tile"],
-                    help="how per-tile depth order is produced (tgs_set_sort_path)")
+                    help="how per-tile depth order is produced (tgs_scene_set_sort_path)")
     ap.add_argument("--blend-split", type=int, default=12,
                     help="tiles with at least 2**N list entries are blended as four quadrant "
-                         "blocks (tgs_set_blend_split; -1: never)")
+                         "blocks (tgs_scene_set_blend_split; -1: never)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one device copy of this size (for HBM counter calibration)")
+    ap.add_argument("--aggregate-counters", nargs=2, metavar=("CSV", "JSON"),
+                    help="per-kernel mean / min / max / count of each counter of a rocprofv3 "
+                         "counter_collection.csv, written as JSON (no GPU)")
+    ap.add_argument("--traffic-summary", nargs=3, metavar=("FETCH_JSON", "WRITE_JSON", "STATS_CSV"),
+                    help="HBM bytes per launch and GB/s per kernel from aggregated FETCH_SIZE / "
+                         "WRITE_SIZE runs, calibrated by the copy of --copy-calibration-mb, with "
+                         "durations from a kernel_stats.csv; writes --out-json / --out-md (no GPU)")
+    ap.add_argument("--trace-summary", metavar="STATS_CSV",
+                    help="markdown table of a rocprofv3 kernel_stats.csv to --out-md (no GPU)")
+    ap.add_argument("--out-json")
+    ap.add_argument("--out-md")
+    ap.add_argument("--command", default="", help="the profiled command, quoted in the summary")
     return ap.parse_args()
 
 
 def kernel_source_hash():
+    """Hash of every kernel source: counters are valid for these files."""
     h = hashlib.sha256()
-    for f in BLEND_SRCS:
-        h.update(open(f, "rb").read())
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(CSRC, f), "rb").read())
+    h.update(open(os.path.join(ROOT, "include", "tgs.h"), "rb").read())
     return h.hexdigest()[:16]
+
+
+# --------------------------------------------------------------------------
+# profile summaries (file readers only)
+# --------------------------------------------------------------------------
+
+def aggregate_counters(src, dst):
+    import collections
+    import csv
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    with open(src) as f:
+        for r in csv.DictReader(f):
+            agg[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    out = {k: {c: {"mean": sum(v) / len(v), "min": min(v), "max": max(v), "n": len(v)}
+               for c, v in d.items()} for k, d in agg.items()}
+    json.dump(out, open(dst, "w"), indent=1)
+    print(f"aggregated {len(out)} kernels -> {dst}")
+
+
+def _kernel_stats(path):
+    import csv
+    rows = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows[r["Name"]] = dict(calls=int(r["Calls"]), total_ns=float(r["TotalDurationNs"]),
+                                   avg_ns=float(r["AverageNs"]), min_ns=float(r["MinNs"]),
+                                   max_ns=float(r["MaxNs"]))
+    return rows
+
+
+def _short(name):
+    """Kernel name without the return type, namespaces and parameter list."""
+    n = name.replace("tgs::(anonymous namespace)::", "").replace("tgs::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    return n.split("(")[0]
+
+
+def trace_summary(stats_csv, out_md, command):
+    rows = sorted(_kernel_stats(stats_csv).items(), key=lambda kv: -kv[1]["total_ns"])
+    total = sum(r["total_ns"] for _, r in rows)
+    lines = ["| total ms | % | calls | avg us | min us | max us | kernel |",
+             "|---:|---:|---:|---:|---:|---:|---|"]
+    for name, r in rows:
+        lines.append(f"| {r['total_ns'] / 1e6:.2f} | {100 * r['total_ns'] / total:.1f} | {r['calls']} | "
+                     f"{r['avg_ns'] / 1e3:.1f} | {r['min_ns'] / 1e3:.1f} | {r['max_ns'] / 1e3:.1f} | "
+                     f"`{_short(name)}` |")
+    md = "\n".join(["Command (one MI355X, from the repository root):", "", "```", command, "```", "",
+                    f"{len(rows)} kernels, {total / 1e6:.1f} ms in total, sorted by total time.",
+                    ""] + lines) + "\n"
+    if out_md:
+        open(out_md, "w").write(md)
+    print(md)
+
+
+def traffic_summary(fetch_json, write_json, stats_csv, calib_mib, out_json, out_md, command):
+    """Bytes per launch = counter mean (KiB per dispatch) x the factor that
+    maps the copy kernel's reading to the bytes it moved (calib_mib MiB read
+    and written); GB/s = bytes per launch / the trace's average duration."""
+    fe, wr = json.load(open(fetch_json)), json.load(open(write_json))
+    stats = _kernel_stats(stats_csv)
+
+    def one(agg, ctr, pat):
+        ks = [k for k in agg if pat in k]
+        assert ks, pat
+        return agg[ks[0]][ctr]
+
+    moved_kib = calib_mib * 1024.0
+    f_scale = moved_kib / one(fe, "FETCH_SIZE", "copyBuffer")["max"]
+    w_scale = moved_kib / one(wr, "WRITE_SIZE", "copyBuffer")["max"]
+    per = {}
+    for name, d in fe.items():
+        if "rocclr" in name or name not in wr or "FETCH_SIZE" not in d:
+            continue
+        fb = d["FETCH_SIZE"]["mean"] * 1024.0 * f_scale
+        wb = wr[name]["WRITE_SIZE"]["mean"] * 1024.0 * w_scale
+        st = stats.get(name)
+        e = {"fetch_bytes": round(fb), "write_bytes": round(wb), "bytes_per_launch": round(fb + wb),
+             "dispatches": d["FETCH_SIZE"]["n"]}
+        if st:
+            e["avg_us"] = round(st["avg_ns"] / 1e3, 2)
+            e["calls"] = st["calls"]
+            e["gbs"] = round((fb + wb) / st["avg_ns"], 1)
+            e["hbm_frac"] = round((fb + wb) / st["avg_ns"] / HBM_PEAK_GBS, 4)
+            e["total_ms"] = round(st["total_ns"] / 1e6, 2)
+        per[_short(name) if _short(name) not in per else name] = e
+    js = {"kernel_source_sha": kernel_source_hash(), "fetch_scale": round(f_scale, 3),
+          "write_scale": round(w_scale, 3), "calibration_mib": calib_mib, "command": command,
+          "kernels": per}
+    if out_json:
+        json.dump(js, open(out_json, "w"), indent=1)
+    rows = sorted(per.items(), key=lambda kv: -kv[1].get("total_ms", 0.0))
+    lines = ["| kernel | launches | avg us | fetch MB | write MB | GB/s | of 8 TB/s |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+    for name, e in rows:
+        lines.append(f"| `{name}` | {e.get('calls', e['dispatches'])} | {e.get('avg_us', float('nan')):.1f} | "
+                     f"{e['fetch_bytes'] / 1e6:.2f} | {e['write_bytes'] / 1e6:.2f} | "
+                     f"{e.get('gbs', float('nan')):.0f} | {e.get('hbm_frac', float('nan')):.3f} |")
+    md = "\n".join(["Commands (one MI355X, from the repository root; one counter per pass):", "", "```",
+                    command, "```", "",
+                    f"Calibration: a {calib_mib} MiB device copy reads FETCH_SIZE x {f_scale:.3f} and "
+                    f"WRITE_SIZE x {w_scale:.3f} of the bytes it moves; every kernel's counters are "
+                    "scaled by those factors.  GB/s = calibrated bytes per launch / the kernel "
+                    "trace's average duration of the same kernel.", ""] + lines) + "\n"
+    if out_md:
+        open(out_md, "w").write(md)
+    print(md)
 
 
 def main():
     args = parse()
+    if args.aggregate_counters:
+        aggregate_counters(*args.aggregate_counters)
+        return
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary, args.copy_calibration_mb or 256, args.out_json,
+                        args.out_md, args.command)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args.out_md, args.command)
+        return
     if args.tgb_downscale is None:
         args.tgb_downscale = 2 if args.workload == "city" else 1
     if args.gpus != 1:
@@ -103,8 +296,6 @@ def main():
     torch.cuda.set_device(0)
     SORT_MODES = {"auto": tgs.SORT_AUTO, "depth_first": tgs.SORT_DEPTH_FIRST,
                   "per_tile": tgs.SORT_PER_TILE}
-    tgs.tgs_set_sort_path(SORT_MODES[args.sort_path])
-    tgs.tgs_set_blend_split(args.blend_split)
     log(f"[bench] generating workload {args.workload}")
     wl = synth.workload(args.workload, n_frames=args.frames)
     cams = wl.cameras
@@ -124,6 +315,8 @@ def main():
     # buffers, then the temporal state's (priors and its frame buffers)
     mem0 = used()
     scene_h = tgs.tgs_scene_upload(wl.scene)
+    tgs.tgs_scene_set_sort_path(scene_h, SORT_MODES[args.sort_path])
+    tgs.tgs_scene_set_blend_split(scene_h, args.blend_split)
     torch.cuda.synchronize()
     mem_scene = used() - mem0
     tgs.tgs_render_full(scene_h, cams[0], **out_f)
@@ -169,13 +362,37 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] warmup {w + 1}/{args.warmup} done")
 
-    # untimed: evaluated pixel-Gaussian pairs per blend stage (deterministic)
-    tgs.tgs_profile_start(count_pairs=True)
+    # untimed, per frame (the path is deterministic): kind, counts, blended
+    # pairs and the survivors with a tile rectangle (the preprocess's record
+    # writes), for the rooflines
+    px = W * H
+
+    def count_frame(render, handle, cam, out):
+        tgs.tgs_profile_start(count_pairs=True)
+        info = render(handle, cam, **out)
+        prof_c = tgs.tgs_profile_stop()
+        full = render is tgs.tgs_render_full
+        rects = tgs.tgs_debug_dump(handle if full else None, None if full else handle,
+                                   tgs.TGS_DUMP_RECTS).reshape(-1, 4) if n else np.zeros((0, 4))
+        info["n_rect"] = int((rects[:, 0] <= rects[:, 2]).sum())
+        stage = {0: "blend_ref", 1: "blend_ref", 2: "blend_tgs", 3: "blend_full"}[info["frame_kind"]]
+        info["pairs"] = prof_c[stage]["pairs"]
+        info["hits"] = prof_c[stage]["hits"]
+        if "tile_mask" in out:
+            m = out["tile_mask"].cpu().numpy().astype(bool)
+            full_tiles = np.repeat(np.repeat(m, 16, 0), 16, 1)[:H, :W]
+            info["px_rendered"] = int(full_tiles.sum())
+        return info
+
+    out_tm = tgs.alloc_frame(W, H, tile_mask=True)
+    out_fm = tgs.alloc_frame(W, H, tile_mask=True)
     kinds = []
-    temporal_step(kinds)
-    full_step()
-    counted = tgs.tgs_profile_stop()
-    log("[bench] pair counts done")
+    tgs.tgs_state_reset(state_h)
+    for cam in cams:
+        kinds.append(count_frame(tgs.tgs_render_temporal, state_h, cam, out_tm))
+    full_counts = [count_frame(tgs.tgs_render_full, scene_h, cam, out_fm) for cam in cams]
+    del out_tm, out_fm
+    log("[bench] per-frame counts done")
 
     # untimed: per-stage breakdown (stage events add queue barriers)
     tgs.tgs_profile_start(stages=True)
@@ -186,27 +403,26 @@ def main():
     detail_full = tgs.tgs_profile_stop()
     log("[bench] stage breakdown done")
 
-    # timed: temporal mode; the blend dispatches carry their own timing events
-    torch.cuda.synchronize()
-    tgs.tgs_profile_start(count_pairs=False)
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        temporal_step()
-    torch.cuda.synchronize()
-    t_temporal = time.perf_counter() - t0
-    prof = tgs.tgs_profile_stop()
-    log(f"[bench] temporal timed: {t_temporal:.3f}s for {args.steps} steps")
+    # timed: temporal mode, then the full render of the same path, each
+    # --runs times; the preprocess and blend dispatches carry their own
+    # timing events.  The median run is reported.
+    def timed(step):
+        runs = []
+        for r in range(args.runs):
+            torch.cuda.synchronize()
+            tgs.tgs_profile_start(count_pairs=False)
+            t0 = time.perf_counter()
+            for k in range(args.steps):
+                step()
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            runs.append((dt, tgs.tgs_profile_stop()))
+            log(f"[bench] {step.__name__} run {r + 1}/{args.runs}: {dt:.3f}s for {args.steps} steps")
+        runs.sort(key=lambda x: x[0])
+        return runs[len(runs) // 2], [round(x[0], 4) for x in runs]
 
-    # timed: full render of the same path
-    torch.cuda.synchronize()
-    tgs.tgs_profile_start(count_pairs=False)
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        full_step()
-    torch.cuda.synchronize()
-    t_full = time.perf_counter() - t0
-    prof_full = tgs.tgs_profile_stop()
-    log(f"[bench] full timed: {t_full:.3f}s for {args.steps} steps")
+    (t_temporal, prof), t_runs = timed(temporal_step)
+    (t_full, prof_full), f_runs = timed(full_step)
 
     n_frames = len(cams)
     fps_t = n_frames * args.steps / t_temporal
@@ -249,7 +465,7 @@ def main():
         steps = steps or args.steps
         tgs.tgs_scene_set_tile_bound(scene_h, tile_bound)
         if sort_path is not None:
-            tgs.tgs_set_sort_path(SORT_MODES[sort_path])
+            tgs.tgs_scene_set_sort_path(scene_h, SORT_MODES[sort_path])
         pkw = {"tgb_downscale": args.tgb_downscale, **pkw}
         sv = tgs.tgs_state_create(scene_h, W, H, tgs.params(**pkw))
 
@@ -304,7 +520,7 @@ def main():
             r["ssim_mean"] = round(float(np.mean(svals)), 5)
         tgs.tgs_state_free(sv)
         tgs.tgs_scene_set_tile_bound(scene_h, tgs.TGS_TILES_3SIGMA)
-        tgs.tgs_set_sort_path(SORT_MODES[args.sort_path])
+        tgs.tgs_scene_set_sort_path(scene_h, SORT_MODES[args.sort_path])
         if sort_path is not None:
             r["sort_path"] = sort_path
         log(f"[bench] variant {label}: {r}")
@@ -350,40 +566,120 @@ def main():
     n_tgs = sum(1 for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS)
     sr_pct = [100.0 * i["n_selected"] / (TX * TY) for i in kinds if i["frame_kind"] == tgs.TGS_FRAME_TGS]
 
-    # roofline of the dominant kernel (largest summed time in the timed region)
-    stage_ms = {k: v["ms"] for k, v in prof.items()}
-    dom = max(("blend_ref", "blend_tgs"), key=lambda s: stage_ms[s])
-    launches = prof[dom]["launches"]
-    avg_s = stage_ms[dom] / launches * 1e-3
-    pairs_per_launch = counted[dom]["pairs"] / max(1, counted[dom]["launches"])
-    hits_per_launch = counted[dom]["hits"] / max(1, counted[dom]["launches"])
-    achieved = BLEND_OPS_PER_HIT[dom] * hits_per_launch / avg_s / 1e12
-    traffic = None
+    # roofline of the dominant kernel: the largest summed time in the timed
+    # temporal region among the dispatches that carry their own events (the
+    # kernel traces show no other kernel with more)
+    deg = wl.scene.sh_degree
+    stage_ms = {k: prof[k]["ms"] for k in ("preprocess", "blend_ref", "blend_tgs")}
+    dom = max(stage_ms, key=lambda k: stage_ms[k])
+    traffic_all = None
     if os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
-        if tr.get("kernel_source_sha") == kernel_source_hash() and dom in tr.get("bytes_per_launch", {}):
-            traffic = tr["bytes_per_launch"][dom]
-    roofline = {"bound": "alu", "kernel": f"blend ({dom})", "achieved": round(achieved, 3),
-                "peak": round(VALU_PEAK_TOPS, 2), "unit": "Tlane-op/s",
-                "frac": round(achieved / VALU_PEAK_TOPS, 4), "traffic": traffic,
-                "avg_launch_ms": round(avg_s * 1e3, 4), "hits_per_launch": int(hits_per_launch),
-                "ops_per_hit": BLEND_OPS_PER_HIT[dom], "list_pairs_per_launch": int(pairs_per_launch)}
+        if tr.get("kernel_source_sha") == kernel_source_hash():
+            traffic_all = tr["kernels"]
 
-    # CPU oracle on a bounded sample of the same workload
+    def traffic_of(stage):
+        if traffic_all is None:
+            return None
+        pat = STAGE_KERNELS[stage] + ("<%d>" % deg if stage == "preprocess" else "")
+        hit = [v for k, v in traffic_all.items() if k.startswith(pat)]
+        return hit[0]["bytes_per_launch"] if hit else None
+
+    def blend_roofline(stage):
+        launches = prof[stage]["launches"]
+        avg_s = prof[stage]["ms"] / max(1, launches) * 1e-3
+        fr = [f for f in kinds if {0: "blend_ref", 1: "blend_ref", 2: "blend_tgs"}[f["frame_kind"]] == stage]
+        hits_pl = float(np.mean([f["hits"] for f in fr]))
+        pairs_pl = float(np.mean([f["pairs"] for f in fr]))
+        ach = BLEND_OPS_PER_HIT[stage] * hits_pl / avg_s / 1e12
+        return {"bound": "alu", "kernel": f"blend ({stage})", "achieved": round(ach, 3),
+                "peak": round(VALU_PEAK_TOPS, 2), "unit": "Tlane-op/s",
+                "frac": round(ach / VALU_PEAK_TOPS, 4), "traffic": traffic_of(stage),
+                "avg_launch_ms": round(avg_s * 1e3, 4), "launches": launches,
+                "work_unit": f"{BLEND_OPS_PER_HIT[stage]} lane-ops per blended pair (alpha >= 1/255, "
+                             "composited or stopping the pixel)",
+                "hits_per_launch": int(hits_pl), "list_pairs_per_launch": int(pairs_pl),
+                "frac_per_evaluated_pair": round(OPS_PER_EVALUATED_PAIR * pairs_pl / avg_s / 1e12
+                                                 / VALU_PEAK_TOPS, 4),
+                "frac_per_evaluated_pair_note": f"the same launches priced at {OPS_PER_EVALUATED_PAIR} "
+                "lane-ops per evaluated list pair (the unit the work was first scoped in); the "
+                "kernel rejects most list pairs by footprint bounds, so this exceeds 1"}
+
+    pre_bytes = [preprocess_bytes(n, deg, f["n_survivors"], f["n_rect"], f["frame_kind"], px) for f in kinds]
+    pre_launches = prof["preprocess"]["launches"]
+    pre_avg_s = prof["preprocess"]["ms"] / max(1, pre_launches) * 1e-3
+    pre_ach = float(np.mean(pre_bytes)) / pre_avg_s / 1e9
+    pre_roof = {"bound": "hbm", "kernel": f"preprocess_kernel<{deg}>", "achieved": round(pre_ach, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(pre_ach / HBM_PEAK_GBS, 4),
+                "traffic": traffic_of("preprocess"), "avg_launch_ms": round(pre_avg_s * 1e3, 4),
+                "launches": pre_launches, "algorithmic_bytes_per_launch": int(np.mean(pre_bytes)),
+                "work_unit": "bytes per launch as built: 33 B per Gaussian, 32 B per survivor, "
+                             "12 (deg+1)^2 + 64 B per survivor with tiles, + 1 B per Gaussian on "
+                             "references, + 24 B per pixel of the fill / query blocks on TemporalGS "
+                             "frames"}
+    rooflines = {"preprocess": pre_roof, "blend_ref": blend_roofline("blend_ref"),
+                 "blend_tgs": blend_roofline("blend_tgs")}
+    roofline = dict(rooflines[dom])
+    roofline["timed_ms_per_step"] = {k: round(v / args.steps, 3) for k, v in stage_ms.items()}
+
+    # whole-frame roofline per frame kind: T_roof = sum over stages of
+    # max(bytes / 8 TB/s, lane-ops / 39.3 T), against the measured frame time
+    def t_roof(f, kind):
+        B, ops = frame_roofline_bytes(n, deg, kind, f["n_survivors"], f["n_keys"], px,
+                                      f.get("px_rendered", px), f["hits"])
+        t = sum(b / (HBM_PEAK_GBS * 1e9) for k, b in B.items() if k != "blend")
+        t += max(B["blend"] / (HBM_PEAK_GBS * 1e9), ops / (VALU_PEAK_TOPS * 1e12))
+        return t, B, ops
+
+    frame_roof = {}
+    for kind, name, frames_k, meas in ((0, "true_ref", kinds, per_kind[0]),
+                                       (1, "pseudo_ref", kinds, per_kind[1]),
+                                       (2, "tgs", kinds, per_kind[2]), (3, "full", full_counts, None)):
+        fs = [f for f in frames_k if f["frame_kind"] == kind]
+        if not fs:
+            continue
+        tr_ = [t_roof(f, kind) for f in fs]
+        t_ms = 1e3 * float(np.mean([t[0] for t in tr_]))
+        m_ms = float(np.mean(meas)) if meas else 1e3 * t_full / (args.steps * n_frames)
+        frame_roof[name] = {"t_roof_ms": round(t_ms, 4), "t_measured_ms": round(m_ms, 4),
+                            "frac": round(t_ms / m_ms, 4), "frames": len(fs),
+                            "bytes": {k: int(np.mean([t[1][k] for t in tr_])) for k in tr_[0][1]},
+                            "blend_lane_ops": int(np.mean([t[2] for t in tr_]))}
+
+    # CPU oracle on a bounded sample of the same workload: the first
+    # 2 lambda_SR + 1 frames of the temporal sequence and the first full
+    # renders, single-threaded
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import oracle as O
-        nf = min(args.cpu_frames, n_frames)
-        ora = O.TemporalOracle(wl.scene, W, H)
+        nf = min(args.cpu_frames or 2 * 5 + 1, n_frames)
+        nfull = min(args.cpu_full_frames, n_frames)
+        ora = O.TemporalOracle(wl.scene, W, H, O.Params(tgb_downscale=args.tgb_downscale))
         t0 = time.perf_counter()
-        for cam in cams[:nf]:
-            ora.render(cam)
-        dt = time.perf_counter() - t0
-        cpu = {"value": round(nf / dt, 5), "unit": "frames/s", "cores": 1, "kind": "oracle",
+        kinds_cpu = [ora.render(cam)["kind"] for cam in cams[:nf]]
+        dt_t = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        for cam in cams[:nfull]:
+            O.render_full(wl.scene, cam)
+        dt_f = time.perf_counter() - t0
+        model = "unknown"
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
+        cpu = {"value": round((nf + nfull) / (dt_t + dt_f), 5), "unit": "frames/s", "cores": 1,
+               "kind": "oracle",
+               "temporal_fps": round(nf / dt_t, 5), "full_fps": round(nfull / dt_f, 5),
+               "host_cores": os.cpu_count(), "cpu_model": model,
                "sample": f"frames 0-{nf - 1} of the {n_frames}-frame temporal sequence "
-                         f"(1 true reference + {nf - 1} TemporalGS frames), single-threaded C "
-                         f"oracle, {dt:.1f} s on {os.cpu_count()} host cores"}
-        log(f"[bench] cpu oracle: {nf} frames in {dt:.1f}s")
+                         f"({kinds_cpu.count(0)} true reference, {kinds_cpu.count(1)} pseudo "
+                         f"references, {kinds_cpu.count(2)} TemporalGS frames; {dt_t:.1f} s) and "
+                         f"full renders of frames 0-{nfull - 1} ({dt_f:.1f} s), single-threaded C "
+                         f"oracle on 1 of {os.cpu_count()} host cores ({model})"}
+        log(f"[bench] cpu oracle: {nf} temporal frames in {dt_t:.1f}s, {nfull} full in {dt_f:.1f}s")
 
     per_frame = lambda s: round(detail[s]["ms"] / n_frames, 4)
     res = {
@@ -417,6 +713,14 @@ def main():
         "stage_breakdown_note": "untimed pass with every stage bracketed by separately "
                                 "recorded HIP events (each adds a queue barrier)",
         "roofline": roofline,
+        "rooflines": rooflines,
+        "frame_roofline": frame_roof,
+        "frame_roofline_note": "T_roof = sum over stages of max(algorithmic bytes / 8 TB/s, "
+                               "lane-ops / 39.3 T) by the scoped stage model (a six-pass 64-bit "
+                               "key sort, 24 B per key per pass), per frame kind, against the "
+                               "measured frame time (untimed per-kind pass; full renders: the "
+                               "timed median run)",
+        "runs": {"temporal_s": t_runs, "full_s": f_runs, "reported": "median"},
         "cpu_baseline": cpu,
     }
     if ablation is not None:

@@ -83,11 +83,21 @@ typedef struct {
     float world_to_cam[16];   /* row-major rigid transform                    */
     float fx, fy, cx, cy;     /* pinhole intrinsics (pixels), fx, fy > 0      */
     int32_t width, height;    /* image size, 1..16384                         */
+    float bg[3];              /* background colour (finite): front-to-back    */
+                              /*    blending ends with RGB = C + T bg, T the  */
+                              /*    transmittance left after the pixel's last */
+                              /*    composited Gaussian (Sec. III-A)          */
 } tgs_camera;
 
 /* Method parameters: lambda_TDC, lambda_SR (Sec. III-B, IV-B), eta
  * (Sec. III-E), lambda1/lambda2 of the surface range (Sec. III-C), the near
- * plane of the 3DGS preprocess, and the ablation switches of Table IV. */
+ * plane of the 3DGS preprocess, and the ablation switches of Table IV.
+ * Fixed, not parameters: the far plane z_far = 1000 and its margin eps = 1
+ * (the empty depth z_far + eps of Sec. III-C is the value 1001, tested by
+ * equality), and the 3DGS blending constants (alpha cap 0.99, alpha_min =
+ * 1/255, termination below T = 1e-4): they define the full render that the
+ * method approximates, and the occluded-tile test of Sec. III-E reuses the
+ * same 1/255. */
 typedef struct {
     int32_t lambda_tdc;       /* 50: interval between true references          */
     int32_t lambda_sr;        /* 5: interval between references of any kind    */
@@ -239,6 +249,14 @@ enum {
 };
 tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_t what,
                           void *host, size_t *nbytes);
+/* Elements [first, first + count) of TGS_DUMP_SORTED_VALUES or
+ * TGS_DUMP_SORTED_KEYS (uint32 each) into host (count * 4 bytes,
+ * synchronous): the lists of a few tiles of a frame whose sorted keys are
+ * too many to copy whole (their positions come from TGS_DUMP_TILE_RANGES).
+ * INVALID_ARG for another buffer, a NULL host with count > 0, or a range
+ * past the frame's keys. */
+tgs_status tgs_debug_dump_range(const tgs_scene *scene, const tgs_state *state, int32_t what,
+                                size_t first, size_t count, void *host);
 
 /* Kernel timing for benchmarking.  Between tgs_profile_start and
  * tgs_profile_stop the blend dispatches carry HIP start/stop events attached
@@ -282,8 +300,9 @@ tgs_status tgs_profile_start(int32_t flags);
 tgs_status tgs_profile_stop(tgs_profile *out);
 
 /* How each tile's front-to-back order (Sec. III-A: sort by depth within a
- * tile) is produced, process-wide.  Both ways give identical per-tile lists
- * (depth bits, then Gaussian index):
+ * tile) is produced, for every later render through `scene` (tgs_render_full
+ * and the temporal states bound to it).  Both ways give identical per-tile
+ * lists (depth bits, then Gaussian index):
  *   TGS_SORT_DEPTH_FIRST: the Gaussians with keys are radix-sorted by depth
  *     (four 8-bit passes over them), keys are emitted in that order and
  *     stably radix-sorted by tile;
@@ -296,24 +315,25 @@ tgs_status tgs_profile_stop(tgs_profile *out);
  *     scene with fewer than 131072 Gaussians, when the longest tile list of
  *     a recent frame of the same kind has fewer than 4096 entries; else the
  *     depth-first sort.
- * INVALID_ARG for another value.  Not thread-safe against running renders. */
+ * INVALID_ARG for a NULL scene or another value.  Like every call on a
+ * scene, it must not overlap with renders through it. */
 enum { TGS_SORT_AUTO = 0, TGS_SORT_DEPTH_FIRST = 1, TGS_SORT_PER_TILE = 2 };
-tgs_status tgs_set_sort_path(int32_t mode);
+tgs_status tgs_scene_set_sort_path(tgs_scene *scene, int32_t mode);
 
-/* Which tiles the blend (Sec. III-A) splits, process-wide: a tile whose
- * sorted list has at least 2^log2_min entries is blended by four blocks, one
- * per 8x8 quadrant, each taking four list entries per pixel at a time
- * (composited in list order: the result is the unsplit blend's up to the
- * order of the colour and moment sums).  If more than max_tiles tiles
- * qualify, the threshold is doubled until at most max_tiles do (whole
- * length classes, so a frame's result never depends on scheduling).  The few
- * longest lists set the blend's tail; a quadrant block re-reads the whole
- * list, so shorter ones are cheaper unsplit.  log2_min in [0, 31], or -1
- * for no split; max_tiles in [0, TGS_BLEND_SPLIT_MAX].  Defaults:
- * TGS_BLEND_SPLIT_DEFAULT, TGS_BLEND_SPLIT_MAX.  INVALID_ARG for other
- * values.  Not thread-safe against running renders. */
+/* Which tiles the blend (Sec. III-A) splits, for every later render through
+ * `scene`: a tile whose sorted list has at least 2^log2_min entries is
+ * blended by four blocks, one per 8x8 quadrant, each taking four list
+ * entries per pixel at a time (composited in list order: the result is the
+ * unsplit blend's up to the order of the colour and moment sums).  If more
+ * than max_tiles tiles qualify, the threshold is doubled until at most
+ * max_tiles do (whole length classes, so a frame's result never depends on
+ * scheduling).  The few longest lists set the blend's tail; a quadrant
+ * block re-reads the whole list, so shorter ones are cheaper unsplit.
+ * log2_min in [0, 31], or -1 for no split; max_tiles in [0,
+ * TGS_BLEND_SPLIT_MAX].  Defaults: TGS_BLEND_SPLIT_DEFAULT,
+ * TGS_BLEND_SPLIT_MAX.  INVALID_ARG for a NULL scene or other values. */
 enum { TGS_BLEND_SPLIT_DEFAULT = 12, TGS_BLEND_SPLIT_MAX = 1024 };
-tgs_status tgs_set_blend_split(int32_t log2_min, int32_t max_tiles);
+tgs_status tgs_scene_set_blend_split(tgs_scene *scene, int32_t log2_min, int32_t max_tiles);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *tgs_last_error(void);

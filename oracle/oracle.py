@@ -91,6 +91,11 @@ def _intr(cam):
     return np.array([cam.fx, cam.fy, cam.cx, cam.cy], np.float32)
 
 
+def camera_bg(cam):
+    """The camera's background colour (black if it has none)."""
+    return _bg(getattr(cam, "bg", None))
+
+
 @dataclass
 class Params:
     """Method parameters (Sec. III-C..E, Sec. IV-B)."""
@@ -192,6 +197,17 @@ def gaussians(scene, cam, z_near=0.2, cull=None, tile_bound=0):
     return out
 
 
+def tile_counts(g, TX, TY, tile_sel=None):
+    """Per-tile list lengths as exclusive offsets tile_start[TX*TY+1] (of the
+    selected tiles only if ``tile_sel``), without building the lists."""
+    n = g["status"].shape[0]
+    ts = np.zeros(TX * TY + 1, np.int64)
+    sel = None if tile_sel is None else np.ascontiguousarray(tile_sel, np.uint8).ravel()
+    lib().or_tile_counts(C.c_int32(n), _p(g["status"]), _p(g["rect"]), C.c_int32(TX),
+                         C.c_int32(TY), _p(sel), _p(ts))
+    return ts
+
+
 def tile_lists(g, TX, TY, tile_sel=None):
     """Per-tile front-to-back lists: (tile_start[TX*TY+1], items[K])."""
     n = g["status"].shape[0]
@@ -205,9 +221,15 @@ def tile_lists(g, TX, TY, tile_sel=None):
     return ts, items[:K]
 
 
-def blend(W, H, ts, items, g, render_tiles=None):
-    """Alpha blending of the listed tiles (all if None)."""
+def _bg(bg):
+    return np.zeros(3, np.float32) if bg is None else np.ascontiguousarray(bg, np.float32).reshape(3)
+
+
+def blend(W, H, ts, items, g, render_tiles=None, bg=None):
+    """Alpha blending of the listed tiles (all if None) over the background
+    colour ``bg`` (black if None)."""
     n = g["status"].shape[0]
+    bgv = _bg(bg)
     rgb = np.zeros((3, H, W), np.float64)
     D = np.full((H, W), float(NOHIT), np.float64)
     S = np.zeros((H, W), np.float64)
@@ -219,15 +241,23 @@ def blend(W, H, ts, items, g, render_tiles=None):
     rt = None if render_tiles is None else np.ascontiguousarray(render_tiles, np.int32)
     items_c = np.ascontiguousarray(items if items.size else np.zeros(1, np.int32), np.int32)
     hits = C.c_int64(0)
+    ninc = np.zeros((H, W), np.int32)
+    spread = np.zeros((H, W), np.float32)
+    wrel = np.zeros((H, W), np.float32)
     E = lib().or_blend(C.c_int32(W), C.c_int32(H), _p(ts), _p(items_c), _p(rt),
                        C.c_int32(0 if rt is None else rt.size), _p(g["mean2d"]), _p(g["conic"]),
-                       _p(g["opacity"]), _p(g["depth"]), _p(g["rgb"]), _p(rgb), _p(D), _p(S),
-                       _p(A), _p(mpos), _p(maxw), _p(gc), _p(gu), C.byref(hits))
+                       _p(g["opacity"]), _p(g["depth"]), _p(g["rgb"]), _p(bgv), _p(rgb), _p(D), _p(S),
+                       _p(A), _p(mpos), _p(maxw), _p(gc), _p(gu), C.byref(hits), _p(ninc),
+                       _p(spread), _p(wrel))
+    # ninc: Gaussians composited per pixel; spread: their largest depth
+    # distance to the first (the size of the Eq. 1/2 sums); wrel: bound on
+    # the relative fp32 error of any of their weights
     return dict(rgb=rgb, D=D, sigma=S, alpha=A, margin_pos=mpos, maxw=maxw,
-                g_certain=gc, g_uncertain=gu, pairs=int(E), hits=int(hits.value))
+                g_certain=gc, g_uncertain=gu, pairs=int(E), hits=int(hits.value),
+                ninc=ninc, spread=spread, wrel=wrel)
 
 
-def blend_bruteforce(W, H, g, every_gaussian=False):
+def blend_bruteforce(W, H, g, every_gaussian=False, bg=None):
     """Per-pixel blend without tiles.  ``every_gaussian``: every Gaussian with
     a 2D footprint at every pixel (tests the tile rectangles); otherwise the
     Gaussians whose rectangle contains the pixel's tile."""
@@ -238,7 +268,7 @@ def blend_bruteforce(W, H, g, every_gaussian=False):
     n = g["status"].shape[0]
     lib().or_blend_bruteforce(C.c_int32(W), C.c_int32(H), C.c_int32(n), _p(g["status"]),
                               _p(g["rect"]), _p(g["mean2d"]), _p(g["conic"]), _p(g["opacity"]),
-                              _p(g["depth"]), _p(g["rgb"]), C.c_int32(int(every_gaussian)),
+                              _p(g["depth"]), _p(g["rgb"]), _p(_bg(bg)), C.c_int32(int(every_gaussian)),
                               _p(rgb), _p(D), _p(S), _p(A))
     return dict(rgb=rgb, D=D, sigma=S, alpha=A)
 
@@ -339,12 +369,27 @@ def stitch(tab, uv, tile_sel, out_rgb):
 # a full 3DGS frame
 # --------------------------------------------------------------------------
 
-def render_full(scene, cam, z_near=0.2, cull=None, tile_bound=0):
+def sample_mask(sample_tiles, TX, TY):
+    """uint8 [TY][TX] mask of the tile indices in ``sample_tiles`` (all tiles
+    if None)."""
+    m = np.zeros(TX * TY, np.uint8)
+    if sample_tiles is None:
+        m[:] = 1
+    else:
+        m[np.asarray(sample_tiles, np.int64)] = 1
+    return m.reshape(TY, TX)
+
+
+def render_full(scene, cam, z_near=0.2, cull=None, tile_bound=0, sample_tiles=None):
+    """One full 3DGS frame; with ``sample_tiles`` (tile indices) only those
+    tiles' lists are built and blended (for images too large to list)."""
     W, H = cam.width, cam.height
     TX, TY = (W + 15) // 16, (H + 15) // 16
     g = gaussians(scene, cam, z_near, cull, tile_bound)
-    ts, items = tile_lists(g, TX, TY)
-    b = blend(W, H, ts, items, g)
+    sel = None if sample_tiles is None else sample_mask(sample_tiles, TX, TY)
+    ts, items = tile_lists(g, TX, TY, sel)
+    rt = None if sel is None else np.flatnonzero(sel.ravel()).astype(np.int32)
+    b = blend(W, H, ts, items, g, rt, bg=camera_bg(cam))
     b.update(g=g, tile_start=ts, items=items, K=int(items.size),
              n_survivors=g["n_survivors"])
     return b
@@ -382,8 +427,9 @@ class TemporalOracle:
             return PSEUDO_REF
         return TGS_FRAME
 
-    def import_state(self, D, S, tab, g_rendered, fbox, ref_w2c, ref_intr, frame_index,
-                     since_true, since_ref, force_pseudo):
+    def import_priors(self, D, S, tab, g_rendered, fbox, ref_w2c, ref_intr):
+        """Replaces the temporal priors (state injection); the schedule
+        counters stay the oracle's own."""
         self.D = np.array(D, np.float32)
         self.S = np.array(S, np.float32)
         self.tab = np.array(tab, np.float32)
@@ -391,17 +437,18 @@ class TemporalOracle:
         self.fbox = np.array(fbox, np.float32)
         self.ref_w2c = np.array(ref_w2c, np.float32).reshape(4, 4)
         self.ref_intr = np.array(ref_intr, np.float32)
-        self.frame_index = int(frame_index)
-        self.since_true = int(since_true)
-        self.since_ref = int(since_ref)
-        self.force_pseudo = bool(force_pseudo)
 
-    def render(self, cam, kind=None):
+    def render(self, cam, kind=None, sample_tiles=None):
+        """The next frame of the stream.  ``sample_tiles`` (tile indices):
+        lists are built and blended for those tiles only (the selected ones
+        among them in a TemporalGS frame), for images too large to list in
+        full; the priors a reference frame captures are then valid on those
+        tiles only."""
         kind = self.next_kind() if kind is None else kind
         if kind == TGS_FRAME:
-            out = self._tgs_frame(cam)
+            out = self._tgs_frame(cam, sample_tiles)
         else:
-            out = self._reference(cam, kind)
+            out = self._reference(cam, kind, sample_tiles)
         out["kind"] = kind
         self.advance(kind, out["n_selected"])
         return out
@@ -427,11 +474,11 @@ class TemporalOracle:
                 eta = float(np.float32(self.p.eta))
                 self.force_pseudo = n_selected > eta * (self.TX * self.TY)
 
-    def _reference(self, cam, kind):
+    def _reference(self, cam, kind, sample_tiles=None):
         cull = None
         if kind == PSEUDO_REF and self.p.enable_afc:
             cull = dict(afc=True, fbox=self.fbox)
-        out = render_full(self.scene, cam, self.p.z_near, cull, self.p.tile_bound)
+        out = render_full(self.scene, cam, self.p.z_near, cull, self.p.tile_bound, sample_tiles)
         # temporal priors (Sec. III-C).  Eq. 1 has no value where nothing is
         # composited: NOHIT (never warped), or with empty_far the far plane,
         # so such pixels warp like a distant surface and are stitched
@@ -453,7 +500,7 @@ class TemporalOracle:
         out["n_selected"] = self.TX * self.TY
         return out
 
-    def _tgs_frame(self, cam):
+    def _tgs_frame(self, cam, sample_tiles=None):
         p = self.p
         W, H = self.W, self.H
         kcur = _intr(cam)
@@ -475,15 +522,17 @@ class TemporalOracle:
             sel = (oc | um).astype(np.uint8)
         else:
             sel = np.ones((self.TY, self.TX), np.uint8)
-        render_tiles = np.flatnonzero(sel.ravel()).astype(np.int32)
-        ts, items = tile_lists(g, self.TX, self.TY, sel)
-        b = blend(W, H, ts, items, g, render_tiles)
+        n_sel = int(sel.sum())
+        listed = sel if sample_tiles is None else sel & sample_mask(sample_tiles, self.TX, self.TY)
+        render_tiles = np.flatnonzero(listed.ravel()).astype(np.int32)
+        ts, items = tile_lists(g, self.TX, self.TY, listed)
+        b = blend(W, H, ts, items, g, render_tiles, bg=camera_bg(cam))
         if half:
             stitch_depth(self.tab, dfill, kcur, self.ref_intr, Minv, p.z_near, sel, b["rgb"])
         else:
             stitch(self.tab, uv, sel, b["rgb"])
         b.update(g=g, tile_start=ts, items=items, K=int(items.size), tile_sel=sel,
                  oc=oc, oc_margin=oc_margin, um=um, dmin=dmin, smax=smax, dfill=dfill, uv=uv,
-                 matched=matched, n_selected=int(render_tiles.size),
+                 matched=matched, n_selected=n_sel,
                  n_survivors=g["n_survivors"], M=M, Minv=Minv)
         return b

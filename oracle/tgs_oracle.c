@@ -33,6 +33,15 @@
 #define OR_MARGIN_ALPHA (1e-5 / 255.0)
 #define OR_MARGIN_T (1e-4 * 1e-4)
 #define OR_MARGIN_POWER 1e-6
+/* Relative difference between two evaluations of one alpha from the same
+ * fp32 exponent (exp2 implementations and the opacity product), in units of
+ * roundoff u = 2^-24: bounds the difference of each composited weight, and
+ * through it of Eq. 1/2, reported per pixel. */
+#define OR_U32 5.9604644775390625e-8
+#define OR_ALPHA_ULPS 4.0
+/* log2(e) as a float: the blend takes alpha = o 2^p2 with the exponent in
+ * base 2 */
+#define OR_LOG2E 1.4426950408889634f
 
 enum { OR_TILES_3SIGMA = 0, OR_TILES_FOOTPRINT = 1 };
 enum { OR_NEAR_CULLED = 0, OR_AFC_CULLED = 1, OR_TOC_CULLED = 2, OR_DEGENERATE = 3,
@@ -403,19 +412,31 @@ void or_tile_lists(int32_t n, const int32_t *status, const int32_t *rect, const 
 typedef struct {
     const float *mean2d, *conic, *opac, *depth;
     const double *rgb;
+    const float *bg;         /* background colour [3] */
     float *maxw;             /* [N] or NULL */
     uint8_t *g_certain;      /* [N] or NULL: included before any margin event */
     uint8_t *g_uncertain;    /* [N] or NULL: at/after a margin event          */
     double *wbuf, *dbuf;     /* scratch of list length                         */
 } or_blend_ctx;
 
-typedef struct { double rgb[3], D, sigma, alpha; int32_t margin_pos; int64_t evaluated, hits; } or_pixel;
+typedef struct {
+    double rgb[3], D, sigma, alpha;
+    int32_t margin_pos;
+    int64_t evaluated, hits;
+    int32_t ninc;            /* Gaussians composited                          */
+    float spread;            /* largest |d - d0| among them (d0: the first)   */
+    float wrel;              /* bound on the relative error of any of their   */
+                             /* weights alpha T in fp32: the alpha's own      */
+                             /* evaluation and the transmittance product      */
+                             /* before it                                     */
+} or_pixel;
 
 static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len, float px, float py,
                         or_pixel *out)
 {
     float T = 1.0f;
     double C[3] = {0.0, 0.0, 0.0};
+    double chain = 0.0, wrel = 0.0;   /* relative error of T, and the largest of a weight */
     int64_t ninc = 0, hits = 0;
     int32_t mpos = -1;
     int64_t j;
@@ -423,11 +444,19 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
         int i = list[j];
         float dx = c->mean2d[2 * i] - px, dy = c->mean2d[2 * i + 1] - py;
         float A = c->conic[3 * i], B = c->conic[3 * i + 1], Cc = c->conic[3 * i + 2];
-        float power = -0.5f * (A * dx * dx + Cc * dy * dy) - B * dx * dy;
+        /* the exponent -(A dx^2 + C dy^2)/2 - B dx dy in base 2, evaluated as
+         * the blend kernel evaluates it: a conic pre-scaled by -log2(e) (1/2
+         * on the squares) and fused multiply-adds.  For an elongated
+         * footprint the terms are thousands of times the result, so any
+         * other order of evaluation would differ by far more than a unit of
+         * roundoff; taken in the kernel's order the alpha decisions and
+         * weights differ only by the exp2 implementations. */
+        const float qa = (-0.5f * OR_LOG2E) * A, qb = -OR_LOG2E * B, qc = (-0.5f * OR_LOG2E) * Cc;
+        float power = fmaf(dx, fmaf(qa, dx, qb * dy), qc * dy * dy);
         int margin = fabs((double)power) <= OR_MARGIN_POWER;
         int include = 0, stop = 0;
         if (!(power > 0.0f)) {
-            float alpha = fminf(OR_ALPHA_MAX, c->opac[i] * expf(power));
+            float alpha = fminf(OR_ALPHA_MAX, c->opac[i] * exp2f(power));
             if (fabs((double)alpha - (double)OR_ALPHA_MIN) <= OR_MARGIN_ALPHA) margin = 1;
             if (!(alpha < OR_ALPHA_MIN)) {
                 ++hits;   /* composited, or the pair that stops the pixel */
@@ -437,6 +466,13 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
                     stop = 1;
                 } else {
                     float w = alpha * T;
+                    /* alpha's relative error: its exponent's (zero where the
+                     * 0.99 cap decides); 1 - alpha carries alpha / (1 - alpha)
+                     * of it into every later transmittance */
+                    const double ra = alpha == OR_ALPHA_MAX ? 0.0 : OR_ALPHA_ULPS * OR_U32;
+                    const double rw = ra + chain + 2.0 * OR_U32;
+                    if (rw > wrel) wrel = rw;
+                    chain += (double)alpha / (1.0 - (double)alpha) * ra + 2.0 * OR_U32;
                     for (int ch = 0; ch < 3; ++ch) C[ch] += (double)w * c->rgb[3 * i + ch];
                     c->wbuf[ninc] = (double)w;
                     c->dbuf[ninc] = (double)c->depth[i];
@@ -458,9 +494,17 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
     out->hits = hits;
     if (mpos >= 0 && c->g_uncertain)
         for (int64_t k = mpos; k < len; ++k) c->g_uncertain[list[k]] = 1;
-    /* background is black: rgb = C + T * 0 */
-    for (int ch = 0; ch < 3; ++ch) out->rgb[ch] = C[ch];
+    /* the background seen through the transmittance left: rgb = C + T bg */
+    for (int ch = 0; ch < 3; ++ch) out->rgb[ch] = C[ch] + (double)T * (double)c->bg[ch];
     out->alpha = 1.0 - (double)T;
+    /* the arithmetic size of Eq. 1/2 at this pixel: terms and depth spread */
+    out->ninc = (int32_t)ninc;
+    out->wrel = (float)wrel;
+    out->spread = 0.0f;
+    for (int64_t k = 1; k < ninc; ++k) {
+        double e = fabs(c->dbuf[k] - c->dbuf[0]);
+        if (e > out->spread) out->spread = (float)e;
+    }
     /* Eq. 1 and Eq. 2 (two-pass) over the included weights */
     double sw = 0.0, swd = 0.0;
     for (int64_t k = 0; k < ninc; ++k) { sw += c->wbuf[k]; swd += c->wbuf[k] * c->dbuf[k]; }
@@ -484,15 +528,16 @@ static void blend_pixel(const or_blend_ctx *c, const int32_t *list, int64_t len,
 int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t *items,
                  const int32_t *render_tiles, int32_t n_render,
                  const float *mean2d, const float *conic, const float *opac, const float *depth,
-                 const double *rgb, double *out_rgb, double *out_D, double *out_sigma,
+                 const double *rgb, const float *bg, double *out_rgb, double *out_D, double *out_sigma,
                  double *out_alpha, int32_t *out_margin_pos, float *maxw, uint8_t *g_certain,
-                 uint8_t *g_uncertain, int64_t *out_hits)
+                 uint8_t *g_uncertain, int64_t *out_hits, int32_t *out_ninc, float *out_spread,
+                 float *out_wrel)
 {
     const int TX = (W + 15) / 16, TY = (H + 15) / 16;
     int64_t maxlen = 1;
     for (int t = 0; t < TX * TY; ++t)
         if (tile_start[t + 1] - tile_start[t] > maxlen) maxlen = tile_start[t + 1] - tile_start[t];
-    or_blend_ctx c = {mean2d, conic, opac, depth, rgb, maxw, g_certain, g_uncertain,
+    or_blend_ctx c = {mean2d, conic, opac, depth, rgb, bg, maxw, g_certain, g_uncertain,
                       (double *)malloc(sizeof(double) * (size_t)maxlen),
                       (double *)malloc(sizeof(double) * (size_t)maxlen)};
     int64_t evaluated = 0, hits = 0;
@@ -512,6 +557,9 @@ int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t 
                 if (out_sigma) out_sigma[q] = p.sigma;
                 if (out_alpha) out_alpha[q] = p.alpha;
                 if (out_margin_pos) out_margin_pos[q] = p.margin_pos;
+                if (out_ninc) out_ninc[q] = p.ninc;
+                if (out_spread) out_spread[q] = p.spread;
+                if (out_wrel) out_wrel[q] = p.wrel;
                 evaluated += p.evaluated;
                 hits += p.hits;
             }
@@ -527,8 +575,9 @@ int64_t or_blend(int32_t W, int32_t H, const int64_t *tile_start, const int32_t 
  * per-tile lists, no keys.  Must reproduce or_blend bit for bit. */
 void or_blend_bruteforce(int32_t W, int32_t H, int32_t n, const int32_t *status, const int32_t *rect,
                          const float *mean2d, const float *conic, const float *opac,
-                         const float *depth, const double *rgb, int32_t every_gaussian,
-                         double *out_rgb, double *out_D, double *out_sigma, double *out_alpha)
+                         const float *depth, const double *rgb, const float *bg,
+                         int32_t every_gaussian, double *out_rgb, double *out_D, double *out_sigma,
+                         double *out_alpha)
 {
     /* every_gaussian != 0: each pixel blends every Gaussian that has a 2D
      * footprint (tile rectangle or not), so the tile rectangles themselves
@@ -542,7 +591,7 @@ void or_blend_bruteforce(int32_t W, int32_t H, int32_t n, const int32_t *status,
         }
     qsort(order, (size_t)m, sizeof(or_item), item_cmp);
     int32_t *list = (int32_t *)malloc(sizeof(int32_t) * (size_t)(m > 0 ? m : 1));
-    or_blend_ctx c = {mean2d, conic, opac, depth, rgb, NULL, NULL, NULL,
+    or_blend_ctx c = {mean2d, conic, opac, depth, rgb, bg, NULL, NULL, NULL,
                       (double *)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1)),
                       (double *)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1))};
     for (int y = 0; y < H; ++y)

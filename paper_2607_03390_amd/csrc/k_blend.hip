@@ -491,6 +491,10 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
     if (!inside || (QUAD && k != 0)) return;
     const size_t HW = (size_t)a.W * a.H;
     const size_t o = (size_t)py * a.W + px;
+    // the background seen through the remaining transmittance
+    cr = __builtin_fmaf(T, a.bg[0], cr);
+    cg = __builtin_fmaf(T, a.bg[1], cg);
+    cb = __builtin_fmaf(T, a.bg[2], cb);
     a.rgb[o] = cr;
     a.rgb[HW + o] = cg;
     a.rgb[2 * HW + o] = cb;

@@ -15,6 +15,8 @@
 // fixed order with contraction disabled for the whole library, so they are
 // reproducible by any implementation that follows the same order.
 #include "fill_query.h"
+#include <hip/hip_ext.h>
+
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -269,7 +271,8 @@ __global__ __launch_bounds__(256) void preprocess_kernel(SceneDev s, CamK cam, C
 }  // namespace
 
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
-                       Counters *cnt, const FillK *fill, hipStream_t st) {
+                       Counters *cnt, const FillK *fill, hipStream_t st, hipEvent_t start,
+                       hipEvent_t stop) {
     const int n_pre = s.n > 0 ? preprocess_blocks(s.n) : 0;
     // the fill blocks need 256 threads per tile: full-resolution grid only
     const bool with_fill = fill && fill->w.tp * fill->w.tp == 256;
@@ -278,11 +281,24 @@ void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Re
     if (n_pre + n_fill <= 0) return;
     const FillK f = with_fill ? *fill : FillK{};
     const dim3 grid(n_pre + n_fill), block(256);
+    // start / stop (may be NULL) are attached to the dispatch itself
     switch (s.deg) {
-        case 0: preprocess_kernel<0><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
-        case 1: preprocess_kernel<1><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
-        case 2: preprocess_kernel<2><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
-        default: preprocess_kernel<3><<<grid, block, 0, st>>>(s, cam, cull, rec, cnt, f, n_pre); break;
+        case 0:
+            hipExtLaunchKernelGGL(preprocess_kernel<0>, grid, block, 0, st, start, stop, 0, s, cam, cull,
+                                  rec, cnt, f, n_pre);
+            break;
+        case 1:
+            hipExtLaunchKernelGGL(preprocess_kernel<1>, grid, block, 0, st, start, stop, 0, s, cam, cull,
+                                  rec, cnt, f, n_pre);
+            break;
+        case 2:
+            hipExtLaunchKernelGGL(preprocess_kernel<2>, grid, block, 0, st, start, stop, 0, s, cam, cull,
+                                  rec, cnt, f, n_pre);
+            break;
+        default:
+            hipExtLaunchKernelGGL(preprocess_kernel<3>, grid, block, 0, st, start, stop, 0, s, cam, cull,
+                                  rec, cnt, f, n_pre);
+            break;
     }
 }
 

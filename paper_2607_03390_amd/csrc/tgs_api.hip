@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -47,14 +48,21 @@ tgs_status fail(tgs_status s, const std::string &msg) {
         if (s_ != TGS_OK) return s_;    \
     } while (0)
 
-// A growable device allocation.
+// A growable device allocation, or (borrowed) a view of memory it does not own.
 struct DevBuf {
     void *p = nullptr;
     size_t bytes = 0;
+    bool borrowed = false;
     ~DevBuf() {
-        if (p) (void)hipFree(p);
+        if (p && !borrowed) (void)hipFree(p);
+    }
+    void borrow(void *q, size_t b) {
+        p = q;
+        bytes = b;
+        borrowed = true;
     }
     tgs_status ensure(size_t want) {
+        if (borrowed) return fail(TGS_ERR_CAPACITY, "a borrowed buffer cannot grow");
         if (want <= bytes && p) return TGS_OK;
         if (p) {
             (void)hipFree(p);
@@ -185,6 +193,8 @@ tgs_status check_camera(const tgs_camera *c) {
     if (!(finite(c->fx) && finite(c->fy) && c->fx > 0.0f && c->fy > 0.0f && finite(c->cx) &&
           finite(c->cy)))
         return fail(TGS_ERR_INVALID_ARG, "intrinsics must be finite with fx, fy > 0");
+    if (!(finite(c->bg[0]) && finite(c->bg[1]) && finite(c->bg[2])))
+        return fail(TGS_ERR_INVALID_ARG, "background colour must be finite");
     const float *m = c->world_to_cam;
     for (int i = 0; i < 16; ++i)
         if (!finite(m[i])) return fail(TGS_ERR_INVALID_ARG, "world_to_cam has a non-finite entry");
@@ -304,6 +314,10 @@ struct Profiler {
 };
 Profiler g_prof;
 
+// Set for the duration of an allocation-free call on this thread: no
+// profiling events (creating one allocates).
+thread_local bool t_no_alloc = false;
+
 // Brackets the launches of one stage with events recorded on their stream
 // (detail mode only: each separate event record costs a barrier packet).
 struct ProfScope {
@@ -311,7 +325,8 @@ struct ProfScope {
     hipStream_t st;
     hipEvent_t a = nullptr;
     ProfScope(int stage_, hipStream_t st_) : stage(stage_), st(st_) {
-        if (g_prof.on && g_prof.stages && (a = g_prof.event()) != nullptr) (void)hipEventRecord(a, st);
+        if (!t_no_alloc && g_prof.on && g_prof.stages && (a = g_prof.event()) != nullptr)
+            (void)hipEventRecord(a, st);
     }
     ~ProfScope() {
         if (!a) return;
@@ -331,6 +346,15 @@ struct ProfScope {
 struct tgs_scene {
     int n = 0, deg = 0, ncoef = 1;
     int tile_bound = TGS_TILES_3SIGMA;
+    // how each tile's depth order is produced: 0 = per frame (the per-tile
+    // sort in selective-rendering frames when the longest tile list of a
+    // recent frame fits its LDS bound, else the global depth sort), 1 =
+    // always the global depth sort, 2 = always the per-tile sort
+    int sort_path = TGS_SORT_AUTO;
+    // list length bucket from which the blend splits tiles into quadrants
+    // (0: never), and the most tiles split
+    int split_bucket = tgs::kSplitBucket;
+    int split_max = tgs::kMaxSplit;
     DevBuf data;
     SceneDev view{};
     Workspace ws;
@@ -369,42 +393,39 @@ struct FrameResult {
 };
 
 // Zero the counters and run the per-Gaussian stage.
-tgs_status step_preprocess(tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
+tgs_status step_preprocess(const tgs_scene *sc, Workspace &ws, const CamK &cam, const CullK &cull,
                            hipStream_t st, const FillK *fill = nullptr) {
     ProfScope ps(TGS_PROF_PREPROCESS, st);
     CullK c = cull;
     c.footprint = sc->tile_bound == TGS_TILES_FOOTPRINT ? 1 : 0;
-    launch_preprocess(sc->view, cam, c, ws.records(), ws.cnt.as<Counters>(), fill, st);
+    // the dispatch carries its own timing events (outside the stage mode,
+    // whose scope brackets the stage instead)
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    if (!t_no_alloc && !g_prof.stages) g_prof.kernel_events(TGS_PROF_PREPROCESS, &ev0, &ev1);
+    launch_preprocess(sc->view, cam, c, ws.records(), ws.cnt.as<Counters>(), fill, st, ev0, ev1);
     TGS_LAUNCHED("preprocess");
     return TGS_OK;
 }
 
-// Sort path: 0 = per frame (the per-tile sort in selective-rendering frames
-// when the longest tile list of a recent frame fits its LDS bound, else the
-// global depth sort), 1 = always the global depth sort, 2 = always the
-// per-tile sort.
-int g_sort_path = 0;
-// list length bucket from which the blend splits tiles into quadrants (0:
-// never), and the most tiles split
-int g_split_bucket = kSplitBucket;
-int g_split_max = kMaxSplit;
 constexpr int kSegSmallScene = 131072;
 
 // The Gaussians that have keys and the start of their keys, in the order the
 // keys are emitted: depth order (global depth sort; the last pass publishes
 // the frame's counters to the host, tag ws.seq) or index order (count scan,
 // each tile's list sorted by depth after the tile sort).  Nothing here waits.
-tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipStream_t st,
-                     const uint32_t **sorted_didx) {
+tgs_status step_scan(const tgs_scene *sc, Workspace &ws, const uint32_t *rowpre, int TX,
+                     hipStream_t st, const uint32_t **sorted_didx) {
+    const int n = sc->n;
     // per frame: the per-tile sort pays off in selective-rendering frames
     // (keys only on the selected tiles) whose lists fit its LDS bound; a
     // frame rendering every tile sorts 3-4 times as many keys per tile as
     // the depth sort sorts Gaussians, and takes the global depth sort
     // (and in every frame of a small scene: below kSegSmallScene Gaussians the
     // four depth passes are launch latency, not work)
-    const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0];
-    ws.frame_seg = g_sort_path == 2 ||
-                   (g_sort_path == 0 && (rowpre != nullptr || n < kSegSmallScene) &&
+    const uint32_t maxb = ws.host_maxb ? reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0]
+                                       : 0xffffffffu;
+    ws.frame_seg = sc->sort_path == TGS_SORT_PER_TILE ||
+                   (sc->sort_path == TGS_SORT_AUTO && (rowpre != nullptr || n < kSegSmallScene) &&
                     maxb <= (uint32_t)kSegBucketMax);
     if (ws.frame_seg) {
         ProfScope ps(TGS_PROF_SORT, st);
@@ -440,7 +461,15 @@ tgs_status step_scan(Workspace &ws, int n, const uint32_t *rowpre, int TX, hipSt
 // rest of the frame meanwhile.  *overflow: the frame needed more keys than
 // the buffers hold (it rendered without keys; grow and render it again).
 tgs_status step_wait_counters(Workspace &ws, hipStream_t st, FrameResult &fr, bool *overflow) {
-    volatile HostCounters *h = ws.host_cnt;
+    HostCounters copy{};
+    if (!ws.host_cnt) {
+        // counters in device memory (allocation-free calls): copied back once
+        // the frame has drained
+        TGS_HIP(hipMemcpyAsync(&copy, ws.host_cnt_dev, sizeof(copy), hipMemcpyDeviceToHost, st));
+        TGS_HIP(hipStreamSynchronize(st));
+        if (copy.tag != ws.seq) return fail(TGS_ERR_DEVICE, "frame counters missing after the frame");
+    }
+    volatile HostCounters *h = ws.host_cnt ? ws.host_cnt : &copy;
     for (uint32_t spins = 1; h->tag != ws.seq; ++spins) {
         if ((spins & 4095u) == 0u) {
             const hipError_t q = hipStreamQuery(st);
@@ -480,9 +509,10 @@ int tile_sort_passes(int TX, int TY) {
 
 // Emit the keys in depth order, sort them by tile (stable), find tile ranges;
 // returns the per-tile lists of Gaussian indices.
-tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpre,
+tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const uint32_t *rowpre,
                      const int *sel_cols, const uint32_t *didx, hipStream_t st,
                      const uint32_t **sorted_vals) {
+    const int n = sc->n;
     const int passes = tile_sort_passes(TX, TY);
     const uint32_t cap = (uint32_t)ws.key_cap;
     Counters *cnt = ws.cnt.as<Counters>();
@@ -518,8 +548,8 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     order.tile_out = ws.tile_order.as<int>();
     order.max_bucket = ws.host_maxb_dev + (rowpre ? 1 : 0);
     order.n_split = &cnt->n_split;
-    order.split_bucket = g_split_bucket;
-    order.max_split = g_split_max;
+    order.split_bucket = sc->split_bucket;
+    order.max_split = sc->split_max;
     if (ws.frame_seg) {
         // each tile's list, emitted in index order, by (depth bits, index)
         ProfScope ps(TGS_PROF_SORT, st);
@@ -527,7 +557,8 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
         // frame of the same kind had any (the longest list's bucket, from the
         // host copy)
         // the blend order (below) is computed by one more block of this launch
-        const uint32_t maxb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0];
+        const uint32_t maxb = ws.host_maxb
+            ? reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[rowpre ? 1 : 0] : 0xffffffffu;
         launch_segment_sort(TX * TY, ws.ranges.as<uint2>(), svals,
                             alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
                             ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, &order, st);
@@ -544,8 +575,12 @@ tgs_status step_keys(Workspace &ws, int n, int TX, int TY, const uint32_t *rowpr
     return TGS_OK;
 }
 
-BlendArgs blend_args(const Workspace &ws, int W, int H, const uint32_t *vals) {
+BlendArgs blend_args(const Workspace &ws, const tgs_camera *cam, const uint32_t *vals) {
+    const int W = cam->width, H = cam->height;
     BlendArgs a{};
+    a.bg[0] = cam->bg[0];
+    a.bg[1] = cam->bg[1];
+    a.bg[2] = cam->bg[2];
     a.W = W;
     a.H = H;
     a.TX = (W + 15) / 16;
@@ -590,20 +625,23 @@ extern "C" {
 
 const char *tgs_last_error(void) { return g_err.c_str(); }
 
-tgs_status tgs_set_sort_path(int32_t mode) {
+tgs_status tgs_scene_set_sort_path(tgs_scene *scene, int32_t mode) {
     g_err.clear();
-    if (mode < 0 || mode > 2) return fail(TGS_ERR_INVALID_ARG, "sort path must be 0, 1 or 2");
-    g_sort_path = mode;
+    if (!scene) return fail(TGS_ERR_INVALID_ARG, "scene is NULL");
+    if (mode != TGS_SORT_AUTO && mode != TGS_SORT_DEPTH_FIRST && mode != TGS_SORT_PER_TILE)
+        return fail(TGS_ERR_INVALID_ARG, "sort path must be 0, 1 or 2");
+    scene->sort_path = mode;
     return TGS_OK;
 }
 
-tgs_status tgs_set_blend_split(int32_t log2_min, int32_t max_tiles) {
+tgs_status tgs_scene_set_blend_split(tgs_scene *scene, int32_t log2_min, int32_t max_tiles) {
     g_err.clear();
+    if (!scene) return fail(TGS_ERR_INVALID_ARG, "scene is NULL");
     if (log2_min < -1 || log2_min > 31) return fail(TGS_ERR_INVALID_ARG, "log2_min must be in [-1, 31]");
     if (max_tiles < 0 || max_tiles > kMaxSplit)
         return fail(TGS_ERR_INVALID_ARG, "max_tiles must be in [0, " + std::to_string(kMaxSplit) + "]");
-    g_split_bucket = log2_min + 1;
-    g_split_max = max_tiles;
+    scene->split_bucket = log2_min + 1;
+    scene->split_max = max_tiles;
     return TGS_OK;
 }
 
@@ -807,10 +845,10 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     for (;;) {
         TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
         const uint32_t *didx = nullptr, *vals = nullptr;
-        TGS_TRY(step_scan(ws, sc->n, nullptr, TX, st, &didx));
-        TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, nullptr, didx, st, &vals));
+        TGS_TRY(step_scan(sc, ws, nullptr, TX, st, &didx));
+        TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
-        BlendArgs a = blend_args(ws, W, H, vals);
+        BlendArgs a = blend_args(ws, cam, vals);
         a.tile_list = ws.tile_order.as<int>();
         a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
         a.rgb = out->rgb;
@@ -1009,10 +1047,10 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
                 TGS_LAUNCHED("tile selection");
             }
             const uint32_t *didx = nullptr;
-            TGS_TRY(step_scan(ws, sc->n, ws.rowpre.as<uint32_t>(), TX, st, &didx));
-            TGS_TRY(step_keys(ws, sc->n, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx,
+            TGS_TRY(step_scan(sc, ws, ws.rowpre.as<uint32_t>(), TX, st, &didx));
+            TGS_TRY(step_keys(sc, ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx,
                               st, &vals));
-            BlendArgs a = blend_args(ws, W, H, vals);
+            BlendArgs a = blend_args(ws, cam, vals);
             a.tile_list = ws.tile_order.as<int>();
             a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
             a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
@@ -1041,10 +1079,10 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             cull.clear_flag = s->g_flag.as<uint8_t>();
             TGS_TRY(step_preprocess(sc, ws, ck, cull, st));
             const uint32_t *didx = nullptr;
-            TGS_TRY(step_scan(ws, sc->n, nullptr, TX, st, &didx));
-            TGS_TRY(step_keys(ws, sc->n, TX, TY, nullptr, nullptr, didx, st, &vals));
+            TGS_TRY(step_scan(sc, ws, nullptr, TX, st, &didx));
+            TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
             if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
-            BlendArgs a = blend_args(ws, W, H, vals);
+            BlendArgs a = blend_args(ws, cam, vals);
             a.tile_list = ws.tile_order.as<int>();
             a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
             a.rgb = out->rgb;
@@ -1257,6 +1295,24 @@ tgs_status tgs_debug_dump(const tgs_scene *scene, const tgs_state *state, int32_
         TGS_HIP(hipMemcpy(host, src, size, hipMemcpyDeviceToHost));
     }
     *nbytes = size;
+    return TGS_OK;
+}
+
+tgs_status tgs_debug_dump_range(const tgs_scene *scene, const tgs_state *state, int32_t what,
+                                size_t first, size_t count, void *host) {
+    g_err.clear();
+    if (!scene && !state) return fail(TGS_ERR_INVALID_ARG, "one of scene/state is required");
+    if (what != TGS_DUMP_SORTED_VALUES && what != TGS_DUMP_SORTED_KEYS)
+        return fail(TGS_ERR_INVALID_ARG, "ranges exist for the sorted values and keys only");
+    if (!host && count > 0) return fail(TGS_ERR_INVALID_ARG, "host is NULL");
+    const Workspace &ws = state ? state->ws : scene->ws;
+    if (!ws.has_frame) return fail(TGS_ERR_INVALID_ARG, "no frame has been rendered yet");
+    if (first > (size_t)ws.last_K || count > (size_t)ws.last_K - first)
+        return fail(TGS_ERR_INVALID_ARG, "range past the frame's keys");
+    if (count == 0) return TGS_OK;
+    const uint32_t *src = what == TGS_DUMP_SORTED_VALUES ? ws.last_vals : ws.last_keys;
+    TGS_HIP(hipDeviceSynchronize());
+    TGS_HIP(hipMemcpy(host, src + first, count * sizeof(uint32_t), hipMemcpyDeviceToHost));
     return TGS_OK;
 }
 

@@ -149,9 +149,11 @@ __device__ inline uint32_t masked_count(ushort4 r, const uint32_t *rowpre, int T
 // fill (optional): the depth fill / correspondence query of a TemporalGS
 // frame (full-resolution geometry buffer) run by blocks of the same launch
 // past the Gaussians' (independent work: both read only the forward warp).
+// start / stop (may be NULL): events attached to the preprocess dispatch.
 struct FillK;
 void launch_preprocess(const SceneDev &s, const CamK &cam, const CullK &cull, Records rec,
-                       Counters *cnt, const FillK *fill, hipStream_t st);
+                       Counters *cnt, const FillK *fill, hipStream_t st, hipEvent_t start = nullptr,
+                       hipEvent_t stop = nullptr);
 inline int preprocess_blocks(int n) { return (n + 255) / 256; }
 
 // Keys are emitted in blocks of kKeyBlock consecutive positions; kfirst[B]
@@ -286,7 +288,8 @@ struct BlendArgs {
     const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
     // optional (with tile_list): the first *n_split_dev (<= kMaxSplit) tiles
     // of tile_list are blended as four quadrant blocks each; the launch adds
-    // 3 kMaxSplit + 28 blocks (n_grid: the launch's tile blocks, set by
+    // 3 kMaxSplit + 28 blocks (4 ceil8(n_split) quadrant blocks replace
+    // n_split tile blocks; n_grid: the launch's tile blocks, set by
     // launch_blend)
     const uint32_t *n_split_dev;
     int n_grid;
@@ -304,6 +307,7 @@ struct BlendArgs {
     unsigned long long *pairs;  // optional: count of evaluated pixel-Gaussian pairs
     unsigned long long *hits;   // with pairs: count of pairs with alpha >= 1/255 (composited or stopping)
     float empty_depth;        // depth written where no Gaussian is composited
+    float bg[3];              // background: rgb = sum of w c + T bg
     uint8_t *mark_sel, *mark_mask;   // optional: set to 1 for every blended tile
     // optional (TGS frames): blocks at or past *n_tiles_dev stitch tile
     // stitch_list[block] from the reference image stitch_tab (Eq. 4)
@@ -319,9 +323,9 @@ struct BlendArgs {
     WarpK sw;
 };
 // Longest lists split into quadrant blocks by the blend: at most kMaxSplit
-// tiles (the launch adds 3 kMaxSplit blocks; those without a quadrant exit
-// at once), by default those of kSplitBucket (lists of 2^(kSplitBucket-1)
-// entries) and up.
+// tiles (the launch adds 3 kMaxSplit + 28 blocks, for 4 ceil8(n_split)
+// quadrant blocks; those without a quadrant exit at once), by default those
+// of kSplitBucket (lists of 2^(kSplitBucket-1) entries) and up.
 constexpr int kMaxSplit = TGS_BLEND_SPLIT_MAX;
 constexpr int kSplitBucket = TGS_BLEND_SPLIT_DEFAULT + 1;
 // start/stop (may be NULL) are attached to the dispatch itself

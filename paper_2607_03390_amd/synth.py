@@ -55,6 +55,7 @@ class Camera:
     cy: float
     width: int
     height: int
+    bg: tuple = (0.0, 0.0, 0.0)   # background colour
 
     @property
     def tiles(self) -> tuple[int, int]:
@@ -291,9 +292,10 @@ def scene_city(n, seed, n_buildings=400, extent=100.0, street_half_width=6.0) ->
     n_ground = int(round(0.4 * n))
     n_faces = n - n_ground
     # buildings: footprints placed uniformly, rejecting overlaps and the street
-    boxes = []
+    placed = np.zeros((n_buildings, 5))
+    m = 0
     tries = 0
-    while len(boxes) < n_buildings and tries < 200000:
+    while m < n_buildings and tries < 200000:
         tries += 1
         w, dpt = rng.uniform(4.0, 12.0, 2)
         h = rng.uniform(5.0, 40.0)
@@ -301,11 +303,13 @@ def scene_city(n, seed, n_buildings=400, extent=100.0, street_half_width=6.0) ->
         x0, x1, y0, y1 = cx - w / 2, cx + w / 2, cy - dpt / 2, cy + dpt / 2
         if y0 < street_half_width and y1 > -street_half_width:
             continue
-        if any(x0 < b[1] + 1.0 and x1 > b[0] - 1.0 and y0 < b[3] + 1.0 and y1 > b[2] - 1.0
-               for b in boxes):
+        pb = placed[:m]
+        if np.any((x0 < pb[:, 1] + 1.0) & (x1 > pb[:, 0] - 1.0) & (y0 < pb[:, 3] + 1.0) &
+                  (y1 > pb[:, 2] - 1.0)):
             continue
-        boxes.append((x0, x1, y0, y1, h))
-    boxes = np.array(boxes)
+        placed[m] = (x0, x1, y0, y1, h)
+        m += 1
+    boxes = placed[:m]
     # ground
     g_means = np.stack([rng.uniform(-extent, extent, n_ground),
                         rng.uniform(-extent, extent, n_ground),

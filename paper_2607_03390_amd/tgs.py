@@ -28,12 +28,14 @@ EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_sce
             "tgs_scene_set_tile_bound",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
-            "tgs_profile_start", "tgs_profile_stop", "tgs_set_sort_path", "tgs_set_blend_split",
+            "tgs_debug_dump_range",
+            "tgs_profile_start", "tgs_profile_stop", "tgs_scene_set_sort_path",
+            "tgs_scene_set_blend_split",
             "tgs_last_error"]
 
-# tgs_set_sort_path modes
+# tgs_scene_set_sort_path modes
 SORT_AUTO, SORT_DEPTH_FIRST, SORT_PER_TILE = 0, 1, 2
-# tgs_set_blend_split: default log2 of the list length from which tiles are
+# tgs_scene_set_blend_split: default log2 of the list length from which tiles are
 # split into quadrant blocks, and the most tiles split per frame
 BLEND_SPLIT_DEFAULT, BLEND_SPLIT_MAX = 12, 1024
 
@@ -56,7 +58,8 @@ class tgs_scene_desc(C.Structure):
 
 class tgs_camera(C.Structure):
     _fields_ = [("world_to_cam", C.c_float * 16), ("fx", C.c_float), ("fy", C.c_float),
-                ("cx", C.c_float), ("cy", C.c_float), ("width", C.c_int32), ("height", C.c_int32)]
+                ("cx", C.c_float), ("cy", C.c_float), ("width", C.c_int32), ("height", C.c_int32),
+                ("bg", C.c_float * 3)]
 
 
 class tgs_params(C.Structure):
@@ -113,10 +116,11 @@ def lib():
         L.tgs_state_export.argtypes = [vp, vp, C.POINTER(sz)]
         L.tgs_state_import.argtypes = [vp, vp, sz]
         L.tgs_debug_dump.argtypes = [vp, vp, i32, vp, C.POINTER(sz)]
+        L.tgs_debug_dump_range.argtypes = [vp, vp, i32, sz, sz, vp]
         L.tgs_profile_start.argtypes = [i32]
         L.tgs_profile_stop.argtypes = [C.POINTER(tgs_profile)]
-        L.tgs_set_sort_path.argtypes = [i32]
-        L.tgs_set_blend_split.argtypes = [i32, i32]
+        L.tgs_scene_set_sort_path.argtypes = [vp, i32]
+        L.tgs_scene_set_blend_split.argtypes = [vp, i32, i32]
         for name in EXPORTED:
             if name not in ("tgs_last_error", "tgs_params_default", "tgs_scene_free",
                             "tgs_state_free", "tgs_scene_count"):
@@ -143,13 +147,17 @@ def _ptr(t):
 
 
 def camera(cam) -> tgs_camera:
-    """tgs_camera from any object with w2c, fx, fy, cx, cy, width, height."""
+    """tgs_camera from any object with w2c, fx, fy, cx, cy, width, height
+    (and optionally bg, the background colour; black otherwise)."""
     c = tgs_camera()
     w = np.ascontiguousarray(cam.w2c, np.float32).ravel()
     for k in range(16):
         c.world_to_cam[k] = float(w[k])
     c.fx, c.fy, c.cx, c.cy = float(cam.fx), float(cam.fy), float(cam.cx), float(cam.cy)
     c.width, c.height = int(cam.width), int(cam.height)
+    bg = getattr(cam, "bg", (0.0, 0.0, 0.0))
+    for k in range(3):
+        c.bg[k] = float(bg[k])
     return c
 
 
@@ -279,21 +287,31 @@ def tgs_debug_dump(scene_h, state_h, what) -> np.ndarray:
     return out.view(_DUMP_DTYPE[what])
 
 
+def tgs_debug_dump_range(scene_h, state_h, what, first, count) -> np.ndarray:
+    """Sorted values or keys [first, first + count) of the last frame."""
+    out = np.zeros(max(int(count), 0), np.uint32)
+    _check(lib().tgs_debug_dump_range(scene_h, state_h, int(what), int(first), int(count),
+                                      out.ctypes.data if count else None))
+    return out
+
+
 TGS_PROFILE_COUNT_PAIRS, TGS_PROFILE_STAGES = 1, 2
 
 
-def tgs_set_sort_path(mode):
-    """How per-tile depth order is produced (process-wide): SORT_AUTO,
-    SORT_DEPTH_FIRST (global depth sort, keys emitted in depth order) or
-    SORT_PER_TILE (keys in index order, each tile's list sorted)."""
-    _check(lib().tgs_set_sort_path(int(mode)))
+def tgs_scene_set_sort_path(h, mode):
+    """How per-tile depth order is produced for later renders through the
+    scene: SORT_AUTO, SORT_DEPTH_FIRST (global depth sort, keys emitted in
+    depth order) or SORT_PER_TILE (keys in index order, each tile's list
+    sorted)."""
+    _check(lib().tgs_scene_set_sort_path(h, int(mode)))
 
 
-def tgs_set_blend_split(log2_min=BLEND_SPLIT_DEFAULT, max_tiles=BLEND_SPLIT_MAX):
-    """Tiles with at least 2**log2_min list entries are blended as four
-    quadrant blocks (process-wide; -1: never); if more than max_tiles tiles
-    qualify, the threshold doubles until at most max_tiles do."""
-    _check(lib().tgs_set_blend_split(int(log2_min), int(max_tiles)))
+def tgs_scene_set_blend_split(h, log2_min=BLEND_SPLIT_DEFAULT, max_tiles=BLEND_SPLIT_MAX):
+    """For later renders through the scene, tiles with at least 2**log2_min
+    list entries are blended as four quadrant blocks (-1: never); if more
+    than max_tiles tiles qualify, the threshold doubles until at most
+    max_tiles do."""
+    _check(lib().tgs_scene_set_blend_split(h, int(log2_min), int(max_tiles)))
 
 
 def tgs_profile_start(count_pairs=False, stages=False):

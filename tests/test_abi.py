@@ -122,20 +122,43 @@ def test_tile_bound_rejects_bad_input_on_host():
         assert "tile bound" in L.tgs_last_error().decode()
 
 
-def test_process_wide_settings_reject_bad_values():
+def test_scene_settings_reject_bad_values():
+    """The sort path and blend split are per-scene settings: a NULL scene
+    and out-of-range values are rejected before the scene is touched."""
     L = tgs.lib()
+    dummy = C.c_void_p(1)      # never dereferenced: the values are checked first
+    assert L.tgs_scene_set_sort_path(None, tgs.SORT_AUTO) == tgs.TGS_ERR_INVALID_ARG
+    assert L.tgs_scene_set_blend_split(None, 12, 16) == tgs.TGS_ERR_INVALID_ARG
     for bad in (-1, 3):
-        assert L.tgs_set_sort_path(bad) == tgs.TGS_ERR_INVALID_ARG
+        assert L.tgs_scene_set_sort_path(dummy, bad) == tgs.TGS_ERR_INVALID_ARG
     for bad in (-2, 32):
-        assert L.tgs_set_blend_split(bad, 16) == tgs.TGS_ERR_INVALID_ARG
+        assert L.tgs_scene_set_blend_split(dummy, bad, 16) == tgs.TGS_ERR_INVALID_ARG
         assert "log2_min" in L.tgs_last_error().decode()
     for bad in (-1, tgs.BLEND_SPLIT_MAX + 1):
-        assert L.tgs_set_blend_split(0, bad) == tgs.TGS_ERR_INVALID_ARG
+        assert L.tgs_scene_set_blend_split(dummy, 0, bad) == tgs.TGS_ERR_INVALID_ARG
         assert "max_tiles" in L.tgs_last_error().decode()
-    # valid values only set variables (no GPU work)
-    assert L.tgs_set_blend_split(-1, 0) == 0
-    assert L.tgs_set_blend_split(tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX) == 0
-    assert L.tgs_set_sort_path(tgs.SORT_AUTO) == 0
+
+
+def test_dump_range_rejects_bad_input_on_host():
+    L = tgs.lib()
+    dummy = C.c_void_p(1)      # never dereferenced: the arguments are checked first
+    assert L.tgs_debug_dump_range(None, None, tgs.TGS_DUMP_SORTED_VALUES, 0, 1, dummy) == \
+        tgs.TGS_ERR_INVALID_ARG
+    for bad in (tgs.TGS_DUMP_TILE_RANGES, tgs.TGS_DUMP_RECORDS, 99):
+        assert L.tgs_debug_dump_range(dummy, None, bad, 0, 1, dummy) == tgs.TGS_ERR_INVALID_ARG
+    assert L.tgs_debug_dump_range(dummy, None, tgs.TGS_DUMP_SORTED_KEYS, 0, 4, None) == \
+        tgs.TGS_ERR_INVALID_ARG
+
+
+def test_camera_background_must_be_finite():
+    L = tgs.lib()
+    dummy = C.c_void_p(1)      # rejected before the scene is touched
+    o = tgs.tgs_frame_out()
+    o.rgb = C.c_void_p(1)
+    cam = tgs.camera(synth.make_camera(np.eye(4), 32, 32))
+    cam.bg[1] = float("nan")
+    assert L.tgs_render_full(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    assert "background" in L.tgs_last_error().decode()
 
 
 def test_state_create_rejects_bad_params_on_host():

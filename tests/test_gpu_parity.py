@@ -8,17 +8,19 @@ selected tile masks.  Within tolerance: colour (2e-4), Eq. 1/2 moments,
 alpha, stitched pixels.  Pixels (and occluded tiles) whose blending takes a
 decision within the oracle's margin of a threshold are excluded and counted.
 Temporal frames use state injection: the GPU's priors after frame t are
-imported into the oracle before both render frame t+1.
+imported into the oracle before both render frame t+1, after the GPU's
+exported state has been compared with the oracle's own (schedule counters,
+adaptive frustum, temporal Gaussian buffer, TGB, TAB); the schedule counters
+are never injected, so the oracle's own decide every frame kind.  Margin
+exclusions are bounded per test.
 """
 import numpy as np
 import pytest
 
 from oracle import oracle as O
 from paper_2607_03390_amd import synth, tgs
-from tests.parity_util import (RGB_TOL, STITCH_TOL, check_gaussian_buffer, check_image, check_lists,
-                               check_pooled_tgb,
-                               check_moments, check_records, dumps, gpu_full, import_into_oracle,
-                               log, tile_pixels)
+from tests.parity_util import Uploaded as Up
+from tests.parity_util import full_parity, gpu_full, log, temporal_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -31,59 +33,34 @@ def _device():
     tgs.lib()
 
 
+# Per-scene settings applied by Uploaded: the sort path and the blend split.
+SETTINGS = dict(sort=tgs.SORT_AUTO, split=(tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX))
+
+
 # Every parity case runs with both ways of producing per-tile depth order
 # (global depth sort first; per-tile sort after the tile sort): the lists
 # must be the oracle's either way.
 @pytest.fixture(autouse=True, params=[tgs.SORT_DEPTH_FIRST, tgs.SORT_PER_TILE],
                 ids=["depth_first", "per_tile"])
 def sort_path(request):
-    tgs.tgs_set_sort_path(request.param)
+    SETTINGS["sort"] = request.param
     yield request.param
-    tgs.tgs_set_sort_path(tgs.SORT_AUTO)
+    SETTINGS["sort"] = tgs.SORT_AUTO
 
 
-class Uploaded:
+class Uploaded(Up):
     def __init__(self, scene, bound=tgs.TGS_TILES_3SIGMA):
-        self.scene = scene
-        self.bound = bound
-
-    def __enter__(self):
-        self.h = tgs.tgs_scene_upload(self.scene)
-        tgs.tgs_scene_set_tile_bound(self.h, self.bound)
-        return self.h
-
-    def __exit__(self, *a):
-        tgs.tgs_scene_free(self.h)
+        super().__init__(scene, bound, SETTINGS["sort"], SETTINGS["split"])
 
 
-def _full_parity(scene, cams, sample_tiles=None, label="", bound=tgs.TGS_TILES_3SIGMA):
-    n = scene.n
-    with Uploaded(scene, bound) as h:
-        for k, cam in enumerate(cams):
-            W, H = cam.width, cam.height
-            TX, TY = cam.tiles
-            log(f"[full parity {label}] cam {k} {W}x{H} n={n} tile bound {bound}")
-            res = gpu_full(h, cam, n)
-            d = dumps(h, None, n)
-            g = O.gaussians(scene, cam, tile_bound=bound)
-            ts, items = O.tile_lists(g, TX, TY)
-            check_records(d, g)
-            check_lists(d, ts, items)
-            assert res["n_keys"] == items.size and res["n_survivors"] == g["n_survivors"]
-            assert res["frame_kind"] == tgs.TGS_FRAME_FULL and np.all(res["tile_mask"] == 1)
-            b = O.blend(W, H, ts, items, g, None if sample_tiles is None else np.asarray(sample_tiles, np.int32))
-            rendered = np.ones((TY, TX), bool)
-            if sample_tiles is not None:
-                rendered = np.zeros(TX * TY, bool)
-                rendered[np.asarray(sample_tiles)] = True
-                rendered = rendered.reshape(TY, TX)
-            ok = tile_pixels(rendered, W, H) & (b["margin_pos"] < 0)
-            worst = check_image(res["rgb"], b["rgb"], ok, where=f"cam {k}")
-            check_moments(res, b, ok)
-            if sample_tiles is None:
-                check_gaussian_buffer(res["contrib"][:n] > 0, b)
-            log(f"    keys {items.size} pairs {b['pairs']} max|drgb| {worst:.2e} "
-                f"margin px {(b['margin_pos'] >= 0).sum()}")
+def _full_parity(scene, cams, sample_tiles=None, label="", bound=tgs.TGS_TILES_3SIGMA, **kw):
+    return full_parity(scene, cams, sample_tiles, label, bound, SETTINGS["sort"], SETTINGS["split"],
+                       **kw)
+
+
+def _temporal_parity(scene, cams, W, H, label, bound=tgs.TGS_TILES_3SIGMA, **pkw):
+    return temporal_parity(scene, cams, W, H, label, bound, SETTINGS["sort"], SETTINGS["split"],
+                           **pkw)
 
 
 def test_full_parity_tiny_orbit():
@@ -147,9 +124,9 @@ def split_all(request):
     """Quadrant blocks for every tile with a non-empty list, or (capped) for
     the tiles of the longest length classes that hold at most 40 tiles, the
     other tiles whole."""
-    tgs.tgs_set_blend_split(*request.param)
+    SETTINGS["split"] = request.param
     yield request.param
-    tgs.tgs_set_blend_split(tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX)
+    SETTINGS["split"] = (tgs.BLEND_SPLIT_DEFAULT, tgs.BLEND_SPLIT_MAX)
 
 
 @pytest.mark.parametrize("n,seed,deg,W,H", [(3000, 1, 3, 200, 136), (500, 2, 2, 37, 53),
@@ -250,8 +227,10 @@ def test_key_capacity_growth():
     r = g["rect"][vis]
     K = int(((r[:, 2] - r[:, 0] + 1) * (r[:, 3] - r[:, 1] + 1)).sum())
     assert K > 2 * (4 * sc.n + 65536), K
-    _full_parity(sc, cams, label="capacity growth")
-    st = _temporal_parity(sc, cams, 512, 384, "capacity growth")
+    # pixels here evaluate hundreds of large Gaussians each, so more of them
+    # take a decision within the oracle's margin (1.2e-3 measured)
+    _full_parity(sc, cams, label="capacity growth", margin_px_frac=2e-3)
+    st = _temporal_parity(sc, cams, 512, 384, "capacity growth", margin_px_frac=2e-3)
     assert st["frames"] == 3
 
 
@@ -275,82 +254,6 @@ def test_empty_and_invisible_scenes():
             torch.cuda.synchronize()
             assert info["n_keys"] == 0 and torch.all(out["rgb"] == 0)
         tgs.tgs_state_free(s)
-
-
-def _temporal_parity(scene, cams, W, H, label, bound=tgs.TGS_TILES_3SIGMA, **pkw):
-    import torch
-    n = scene.n
-    stats = dict(frames=0, tgs=0, margin_tiles=0, margin_px=0)
-    with Uploaded(scene, bound) as h:
-        s = tgs.tgs_state_create(h, W, H, tgs.params(**pkw))
-        ora = O.TemporalOracle(scene, W, H, O.Params(tile_bound=bound, **pkw))
-        try:
-            for k, cam in enumerate(cams):
-                blob = tgs.tgs_state_export(s)
-                if k > 0:
-                    import_into_oracle(ora, blob)
-                out = tgs.alloc_frame(W, H, n, depth=True, contrib=True, tile_mask=True)
-                log(f"[temporal parity {label}] frame {k}")
-                info = tgs.tgs_render_temporal(s, cam, **out)
-                torch.cuda.synchronize()
-                res = {kk: v.cpu().numpy() for kk, v in out.items()}
-                ref = ora.render(cam)
-                assert info["frame_kind"] == ref["kind"], (k, info["frame_kind"], ref["kind"])
-                d = dumps(None, s, n)
-                check_records(d, ref["g"])
-                stats["frames"] += 1
-                sel_tiles = res["tile_mask"].astype(bool)
-                if ref["kind"] == O.TGS_FRAME:
-                    stats["tgs"] += 1
-                    TX, TY = cam.tiles
-                    Hg, Wg = ref["dmin"].shape   # the geometry buffer's grid
-                    dm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_DEPTH).reshape(Hg, Wg)
-                    sm = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_WARP_SIGMA).reshape(Hg, Wg)
-                    df = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_FILLED_DEPTH).reshape(Hg, Wg)
-                    uv = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_CORRESPONDENCE).reshape(Hg, Wg, 2)
-                    um = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_UNMATCHED).reshape(TY, TX)
-                    oc = tgs.tgs_debug_dump(None, s, tgs.TGS_DUMP_OCCLUDED).reshape(TY, TX)
-                    assert np.array_equal(dm.view(np.uint32), ref["dmin"].view(np.uint32)), "warped depth"
-                    assert np.array_equal(sm, ref["smax"]), "warped sigma"
-                    assert np.array_equal(df.view(np.uint32), ref["dfill"].view(np.uint32)), "filled depth"
-                    assert np.array_equal(uv.view(np.uint32), ref["uv"].view(np.uint32)), "correspondences"
-                    assert np.array_equal(um, ref["um"]), "unmatched tiles"
-                    differ = oc != ref["oc"]
-                    assert not np.any(differ & (ref["oc_margin"] == 0)), "occluded tiles"
-                    stats["margin_tiles"] += int(differ.sum())
-                    sel_ref = ref["tile_sel"].astype(bool)
-                    if np.array_equal(sel_tiles, sel_ref):
-                        check_lists(d, ref["tile_start"], ref["items"],
-                                    tiles=np.flatnonzero(sel_ref.ravel()))
-                        assert info["n_keys"] == ref["K"]
-                    else:
-                        log(f"    selection differs only at margin tiles {np.flatnonzero(differ.ravel())}")
-                    assert info["n_selected"] == int(sel_tiles.sum())
-                    assert info["n_survivors"] == ref["n_survivors"]
-                    assert info["n_newly_visible"] == int(ref["g"]["newly_visible"].sum())
-                    rend = tile_pixels(sel_tiles & sel_ref, W, H)
-                    stitched = tile_pixels(~sel_tiles & ~sel_ref, W, H)
-                    ok = rend & (ref["margin_pos"] < 0)
-                    check_image(res["rgb"], ref["rgb"], ok, RGB_TOL, f"frame {k} rendered tiles")
-                    check_image(res["rgb"], ref["rgb"], stitched, STITCH_TOL, f"frame {k} stitched tiles")
-                    stats["margin_px"] += int((rend & (ref["margin_pos"] >= 0)).sum())
-                else:
-                    assert np.all(sel_tiles)
-                    check_lists(d, ref["tile_start"], ref["items"])
-                    assert info["n_keys"] == ref["K"] and info["n_survivors"] == ref["n_survivors"]
-                    ok = ref["margin_pos"] < 0
-                    check_image(res["rgb"], ref["rgb"], ok, RGB_TOL, f"frame {k} reference")
-                    check_moments(res, ref, ok)
-                    check_gaussian_buffer(res["contrib"][:n] > 0, ref)
-                    if pkw.get("tgb_downscale", 1) == 2:
-                        check_pooled_tgb(tgs.parse_state(tgs.tgs_state_export(s)), ora, ~ok)
-                    stats["margin_px"] += int((~ok).sum())
-                log(f"    kind {info['frame_kind']} sel {info['n_selected']} keys {info['n_keys']} "
-                    f"surv {info['n_survivors']} newly {info['n_newly_visible']}")
-        finally:
-            tgs.tgs_state_free(s)
-    log(f"[temporal parity {label}] {stats}")
-    return stats
 
 
 def test_temporal_parity_tiny():
@@ -402,6 +305,24 @@ def test_temporal_parity_cube_occlusion():
     cams = synth.orbit_path(10, 3.0, 15.0, 1.0, 144, 120)
     st = _temporal_parity(sc, cams, 144, 120, "cube20k", eta=1.0)
     assert st["tgs"] >= 5
+
+
+def test_temporal_parity_eta_insertion():
+    """A sequence whose pseudo references all come from the eta rule
+    (Sec. III-E adaptive reference insertion): slow orbit steps select
+    under 80 % of the tiles, every fourth step jumps 6 degrees and selects
+    more, and lambda_SR = 10 is never reached.  Frame kinds come from the
+    oracle's own counters."""
+    sc = synth.scene_room(60_000, 2)
+    cams = synth.orbit_path(16, 5.0, 10.0, 0.0, 400, 232, steps=(0.3, 0.3, 0.3, 6.0))
+    st = _temporal_parity(sc, cams, 400, 232, "room60k eta", empty_far=1, lambda_sr=10, eta=0.8)
+    kinds = st["kinds"]
+    assert kinds.count(O.PSEUDO_REF) >= 3 and kinds.count(O.TGS_FRAME) >= 6
+    # a pseudo reference follows a TemporalGS frame before lambda_SR frames
+    # have passed: only the eta rule inserts it
+    assert all(kinds[i - 1] == O.TGS_FRAME for i, kd in enumerate(kinds) if kd == O.PSEUDO_REF)
+    # and the rule does not fire on every TemporalGS frame
+    assert any(kinds[i] == O.TGS_FRAME and kinds[i + 1] == O.TGS_FRAME for i in range(len(kinds) - 1))
 
 
 def test_force_all_dirty_no_cull_equals_full():

@@ -296,6 +296,33 @@ def test_blend_single_gaussian_closed_form():
     assert r["hits"] > 0
 
 
+def test_blend_over_background_closed_form():
+    """With a background colour bg the pixel is c alpha + (1 - alpha) bg for
+    one Gaussian (the transmittance left after it), and bg where nothing is
+    composited."""
+    W, H = 48, 40
+    cam = _cam(np.eye(4), W, H)
+    cam.bg = (0.2, 0.7, 0.05)
+    s, Z, o = 0.05, 3.0, 0.8
+    sc = _scene([[0, 0, Z]], [[s, s, s]], opac=[o], dc=[[0.4, 0.1, -0.3]])
+    r = O.render_full(sc, cam)
+    black = O.render_full(sc, _cam(np.eye(4), W, H))
+    var = (cam.fx * s / Z) ** 2 + 0.3
+    col = np.array([C0 * 0.4 + 0.5, C0 * 0.1 + 0.5, max(0.0, C0 * -0.3 + 0.5)])
+    a = black["alpha"]
+    ok = np.abs(a - 1 / 255) > 1e-6
+    ys, xs = np.mgrid[0:H, 0:W]
+    rho2 = ((xs - cam.cx) ** 2 + (ys - cam.cy) ** 2) / var
+    assert np.allclose(a[a > 0], np.minimum(0.99, o * np.exp(-0.5 * rho2))[a > 0], atol=2e-6)
+    for ch in range(3):
+        want = col[ch] * a + (1 - a) * cam.bg[ch]
+        np.testing.assert_allclose(r["rgb"][ch][ok], want[ok], atol=2e-6)
+        assert np.all(r["rgb"][ch][a == 0] == np.float32(cam.bg[ch]))
+    assert np.array_equal(r["alpha"], black["alpha"]) and np.array_equal(r["D"], black["D"])
+    bf = O.blend_bruteforce(W, H, r["g"], bg=cam.bg)
+    assert np.array_equal(bf["rgb"], r["rgb"])
+
+
 def test_blend_two_gaussians_on_one_ray():
     W = H = 32
     cam = _cam(np.eye(4), W, H)
@@ -337,6 +364,44 @@ def test_bruteforce_equals_tiled(seed, W, H):
     every = O.blend_bruteforce(W, H, r["g"], every_gaussian=True)
     for k in ("rgb", "D", "sigma", "alpha"):
         assert np.array_equal(r[k], every[k]), k
+
+
+def test_sampled_tiles_match_the_full_oracle():
+    """The sampled mode (lists and blend of a tile subset, for images too
+    large to list whole) gives exactly the full oracle's lists and pixels
+    on those tiles, in full frames and in a TemporalGS frame."""
+    w = synth.workload("tiny", n_frames=3)
+    cam = w.cameras[0]
+    TX, TY = cam.tiles
+    sample = np.array([0, 5, 17, 100, 136, 255])
+    full = O.render_full(w.scene, cam)
+    part = O.render_full(w.scene, cam, sample_tiles=sample)
+    counts = O.tile_counts(full["g"], TX, TY)
+    assert np.array_equal(counts, full["tile_start"])
+    m = np.zeros((256, 256), bool)
+    for t in sample:
+        ty, tx = divmod(int(t), TX)
+        m[16 * ty:16 * ty + 16, 16 * tx:16 * tx + 16] = True
+        a = full["items"][full["tile_start"][t]:full["tile_start"][t + 1]]
+        b = part["items"][part["tile_start"][t]:part["tile_start"][t + 1]]
+        assert np.array_equal(a, b)
+    for k in ("rgb", "D", "sigma", "alpha"):
+        assert np.array_equal(full[k][..., m], part[k][..., m]), k
+    T1 = O.TemporalOracle(w.scene, 256, 256)
+    T2 = O.TemporalOracle(w.scene, 256, 256)
+    T1.render(cam)
+    T2.render(cam)
+    a = T1.render(w.cameras[1])
+    b = T2.render(w.cameras[1], sample_tiles=sample)
+    assert a["kind"] == b["kind"] == O.TGS_FRAME and a["n_selected"] == b["n_selected"]
+    sel = a["tile_sel"].ravel().astype(bool)
+    for t in sample:
+        if sel[t]:
+            assert np.array_equal(a["items"][a["tile_start"][t]:a["tile_start"][t + 1]],
+                                  b["items"][b["tile_start"][t]:b["tile_start"][t + 1]])
+    stitched = np.repeat(np.repeat(~a["tile_sel"].astype(bool), 16, 0), 16, 1)
+    assert np.array_equal(a["rgb"][:, stitched], b["rgb"][:, stitched])
+    assert np.array_equal(a["rgb"][:, m], b["rgb"][:, m])
 
 
 def test_lists_sorted_and_complete():
