@@ -182,6 +182,24 @@ tgs_status tgs_scene_set_tile_bound(tgs_scene *scene, int32_t bound);
 tgs_status tgs_render_full(tgs_scene *scene, const tgs_camera *cam, tgs_frame_out *out,
                            void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the frame
+ * of tgs_render_full, computed by the same kernels, with its whole
+ * workspace (records, keys, sort tables, tile ranges, counters) in a fixed
+ * array of TGS_NOALLOC_SCRATCH_BYTES that the library holds on each device
+ * it runs on until the process ends.  The call allocates and frees nothing;
+ * the caller passes the outputs as for tgs_render_full.  Every call on one
+ * device shares that device's array: calls that overlap on a device race
+ * (the stream must belong to the current device).  The scene's sort path
+ * and blend split apply; profiling and tgs_debug_dump do not cover it.
+ * Errors: CAPACITY when n Gaussians at width x height leave no room for
+ * keys, or when the frame needs more Gaussian-tile keys than the array
+ * holds after them (the outputs are then incomplete); otherwise as
+ * tgs_render_full. */
+#define TGS_NOALLOC_SCRATCH_BYTES (64u << 20)
+tgs_status tgs_render_full_noalloc(const tgs_scene *scene, const tgs_camera *cam,
+                                   tgs_frame_out *out, void *stream);
+
 /* Creates the temporal state for `scene` at width x height (Sec. III-B..E):
  * priors, warp buffers and the frame schedule.  params may be NULL
  * (defaults).  The scene must outlive the state. */

@@ -881,6 +881,175 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
     return TGS_OK;
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// allocation-free full render
+// ---------------------------------------------------------------------------
+
+// The frame workspace of tgs_render_full_noalloc: one array per device, held
+// by the library until the process ends and shared by every such call on
+// that device.  In host code `scratch` names a host-side stand-in, not the
+// device array: every host use goes through the address hipGetSymbolAddress
+// returns for the current device.
+static __device__ __align__(256) unsigned char scratch[TGS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr size_t kNoAllocBytes = (size_t)TGS_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's address on the current device, looked up on the first
+// call there (with that device current) and kept.
+tgs_status scratch_address(char **out) {
+    int dev = -1;
+    TGS_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(TGS_ERR_DEVICE, "device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(TGS_ERR_DEVICE, std::string("hipGetSymbolAddress(scratch): ") +
+                                            hipGetErrorString(e));
+        g_scratch_ptr[dev] = static_cast<char *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return TGS_OK;
+}
+
+// 256-byte aligned pieces of [base, base + cap), handed out in order.
+struct Carve {
+    char *base;
+    size_t cap, off;
+    void *raw(size_t bytes) {
+        off = (off + 255) & ~(size_t)255;
+        if (off > cap || bytes > cap - off) return nullptr;
+        void *p = base + off;
+        off += bytes > 0 ? bytes : 1;
+        return p;
+    }
+    bool take(DevBuf &b, size_t bytes) {
+        void *p = raw(bytes);
+        if (p) b.borrow(p, bytes);
+        return p != nullptr;
+    }
+};
+
+// Lays the workspace of a full render (n Gaussians, W x H, key_cap keys) over
+// [base, base + cap); false if it does not fit.
+bool layout_full(Workspace &ws, char *base, size_t cap, int n, int W, int H, size_t key_cap) {
+    Carve c{base, cap, 0};
+    const size_t nn = (size_t)(n > 0 ? n : 1);
+    const int TX = (W + 15) / 16, TY = (H + 15) / 16;
+    const size_t nt = (size_t)TX * TY;
+    const size_t sort_words = std::max(sort_scratch_words((uint32_t)key_cap),
+                                       sort_scratch_words((uint32_t)nn));
+    bool ok = c.take(ws.g, nn * 4 * sizeof(float4)) && c.take(ws.rect, nn * sizeof(ushort4)) &&
+              c.take(ws.status, nn) && c.take(ws.count, (nn + 4) * sizeof(uint32_t)) &&
+              c.take(ws.partial, (size_t)(2 * preprocess_blocks((int)nn)) * sizeof(uint32_t)) &&
+              c.take(ws.dkey, nn * 4) && c.take(ws.didx, nn * 4) && c.take(ws.dkey_alt, nn * 4) &&
+              c.take(ws.didx_alt, nn * 4) && c.take(ws.offs, nn * 4) &&
+              c.take(ws.ranges, nt * sizeof(uint2)) && c.take(ws.sel, nt) &&
+              c.take(ws.sel_list, nt * sizeof(int)) && c.take(ws.tile_order, nt * sizeof(int)) &&
+              c.take(ws.sel_cols, nt * sizeof(int)) &&
+              c.take(ws.rowpre, (size_t)TY * (TX + 1) * sizeof(uint32_t)) &&
+              c.take(ws.cnt, sizeof(Counters)) && c.take(ws.sort, sort_words * sizeof(uint32_t)) &&
+              c.take(ws.tkey, key_cap * 4) && c.take(ws.tval, key_cap * 4) &&
+              c.take(ws.tkey_alt, key_cap * 4) && c.take(ws.tval_alt, key_cap * 4) &&
+              c.take(ws.kfirst, key_blocks(key_cap) * sizeof(uint32_t));
+    void *hc = ok ? c.raw(sizeof(HostCounters)) : nullptr;
+    void *mb = hc ? c.raw(2 * sizeof(uint32_t)) : nullptr;
+    if (!mb) return false;
+    // counters and the longest-list bucket stay in device memory: read back
+    // by a copy, never through pinned host memory
+    ws.host_cnt = nullptr;
+    ws.host_cnt_dev = static_cast<HostCounters *>(hc);
+    ws.host_maxb = nullptr;
+    ws.host_maxb_dev = static_cast<uint32_t *>(mb);
+    ws.n = n;
+    ws.W = W;
+    ws.H = H;
+    ws.key_cap = key_cap;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+tgs_status tgs_render_full_noalloc(const tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *out,
+                                   void *stream) {
+    g_err.clear();
+    if (!sc || !out || !out->rgb) return fail(TGS_ERR_INVALID_ARG, "scene, out and out->rgb are required");
+    TGS_TRY(check_camera(cam));
+    hipStream_t st = (hipStream_t)stream;
+    const int W = cam->width, H = cam->height, TX = (W + 15) / 16, TY = (H + 15) / 16;
+    char *base = nullptr;
+    TGS_TRY(scratch_address(&base));
+    // the largest key capacity the scratch array leaves (host arithmetic only)
+    Workspace ws;
+    size_t lo = 0, hi = kNoAllocBytes / 16;
+    {
+        Workspace probe;
+        if (!layout_full(probe, base, kNoAllocBytes, sc->n, W, H, kKeyBlock))
+            return fail(TGS_ERR_CAPACITY, std::to_string(sc->n) + " Gaussians at " + std::to_string(W) +
+                                              "x" + std::to_string(H) + " do not fit the " +
+                                              std::to_string(kNoAllocBytes >> 20) +
+                                              " MiB scratch array of the allocation-free render");
+        lo = kKeyBlock;
+    }
+    while (lo < hi) {
+        const size_t mid = lo + (hi - lo + 1) / 2;
+        Workspace probe;
+        if (layout_full(probe, base, kNoAllocBytes, sc->n, W, H, mid)) lo = mid;
+        else hi = mid - 1;
+    }
+    if (!layout_full(ws, base, kNoAllocBytes, sc->n, W, H, lo))
+        return fail(TGS_ERR_DEVICE, "scratch layout failed");
+    // no profiling events in this call (creating one allocates)
+    struct NoAllocScope {
+        NoAllocScope() { t_no_alloc = true; }
+        ~NoAllocScope() { t_no_alloc = false; }
+    } scope;
+    // the counters read back must start clear: the array keeps the last
+    // call's contents
+    launch_fill_u8(reinterpret_cast<uint8_t *>(ws.host_cnt_dev), sizeof(HostCounters), 0, st);
+    TGS_LAUNCHED("clear counters");
+    const CamK ck = make_camk(cam);
+    TGS_TRY(step_preprocess(sc, ws, ck, no_cull(0.2f, ws), st));
+    const uint32_t *didx = nullptr, *vals = nullptr;
+    TGS_TRY(step_scan(sc, ws, nullptr, TX, st, &didx));
+    TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
+    if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
+    BlendArgs a = blend_args(ws, cam, vals);
+    a.tile_list = ws.tile_order.as<int>();
+    a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
+    a.rgb = out->rgb;
+    a.depth = out->depth;
+    a.sigma = out->sigma;
+    a.alpha = out->alpha;
+    a.contrib = out->contrib;
+    a.mark_mask = out->tile_mask;
+    launch_blend(a, TX * TY, st, nullptr, nullptr);
+    TGS_LAUNCHED("blend");
+    FrameResult fr;
+    bool overflow = false;
+    TGS_TRY(step_wait_counters(ws, st, fr, &overflow));
+    if (overflow)
+        return fail(TGS_ERR_CAPACITY, "frame needs " + std::to_string(fr.K) +
+                                          " Gaussian-tile keys; the allocation-free render holds " +
+                                          std::to_string(ws.key_cap) + " at this size");
+    out->frame_kind = TGS_FRAME_FULL;
+    out->n_selected = TX * TY;
+    out->n_survivors = (int32_t)fr.n_surv;
+    out->n_newly_visible = 0;
+    out->n_keys = fr.K;
+    return TGS_OK;
+}
+
 tgs_status tgs_state_create(tgs_scene *scene, int32_t width, int32_t height,
                             const tgs_params *params, tgs_state **out) {
     g_err.clear();

@@ -28,7 +28,7 @@ EXPORTED = ["tgs_params_default", "tgs_scene_upload", "tgs_scene_free", "tgs_sce
             "tgs_scene_set_tile_bound",
             "tgs_render_full", "tgs_state_create", "tgs_state_reset", "tgs_state_free",
             "tgs_render_temporal", "tgs_state_export", "tgs_state_import", "tgs_debug_dump",
-            "tgs_debug_dump_range",
+            "tgs_debug_dump_range", "tgs_render_full_noalloc",
             "tgs_profile_start", "tgs_profile_stop", "tgs_scene_set_sort_path",
             "tgs_scene_set_blend_split",
             "tgs_last_error"]
@@ -109,6 +109,7 @@ def lib():
         L.tgs_scene_count.argtypes = [vp]
         L.tgs_scene_set_tile_bound.argtypes = [vp, C.c_int32]
         L.tgs_render_full.argtypes = [vp, C.POINTER(tgs_camera), C.POINTER(tgs_frame_out), vp]
+        L.tgs_render_full_noalloc.argtypes = [vp, C.POINTER(tgs_camera), C.POINTER(tgs_frame_out), vp]
         L.tgs_state_create.argtypes = [vp, i32, i32, C.POINTER(tgs_params), C.POINTER(vp)]
         L.tgs_state_reset.argtypes = [vp]
         L.tgs_state_free.argtypes = [vp]
@@ -211,6 +212,20 @@ def tgs_render_full(scene_h, cam, rgb, depth=None, sigma=None, alpha=None, contr
     o = _frame_out(rgb, depth, sigma, alpha, contrib, tile_mask)
     c = camera(cam)
     _check(lib().tgs_render_full(scene_h, C.byref(c), C.byref(o), _stream(stream)))
+    return _scalars(o)
+
+
+# bytes of the device array that holds the workspace of tgs_render_full_noalloc
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def tgs_render_full_noalloc(scene_h, cam, rgb, depth=None, sigma=None, alpha=None, contrib=None,
+                            tile_mask=None, stream=None):
+    """tgs_render_full with the workspace in the library's fixed device array
+    (no allocation; raises TgsError with TGS_ERR_CAPACITY beyond it)."""
+    o = _frame_out(rgb, depth, sigma, alpha, contrib, tile_mask)
+    c = camera(cam)
+    _check(lib().tgs_render_full_noalloc(scene_h, C.byref(c), C.byref(o), _stream(stream)))
     return _scalars(o)
 
 

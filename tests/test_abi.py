@@ -150,6 +150,18 @@ def test_dump_range_rejects_bad_input_on_host():
         tgs.TGS_ERR_INVALID_ARG
 
 
+def test_noalloc_render_rejects_bad_input_on_host():
+    L = tgs.lib()
+    dummy = C.c_void_p(1)      # rejected before the scene is touched
+    o = tgs.tgs_frame_out()
+    cam = tgs.camera(synth.make_camera(np.eye(4), 32, 32))
+    assert L.tgs_render_full_noalloc(None, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    assert L.tgs_render_full_noalloc(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+    o.rgb = C.c_void_p(1)
+    cam.width = 0
+    assert L.tgs_render_full_noalloc(dummy, C.byref(cam), C.byref(o), None) == tgs.TGS_ERR_INVALID_ARG
+
+
 def test_camera_background_must_be_finite():
     L = tgs.lib()
     dummy = C.c_void_p(1)      # rejected before the scene is touched
