@@ -342,13 +342,19 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
             }
         } else {
             // list slots are read four at a time (one aligned 32-bit LDS load
-            // every fourth entry): three iterations in four wait for one LDS
-            // round trip (the staged record) instead of two
-            uint32_t quad = 0;
-            for (uint32_t e = 0; e < n_run; ++e) {
-                if ((e & 3u) == 0u) quad = *reinterpret_cast<const uint32_t *>(&s.list[my_list][e]);
-                const uint32_t j = (quad >> (8u * (e & 3u))) & 255u;
-                const uint32_t jo = j << 4;   // byte offset into the staged arrays
+            // per four entries, each slot's byte offset taken with constant
+            // shifts): three entries in four wait for one LDS round trip (the
+            // staged record) instead of two.  The walk runs to the wave's
+            // longest list rounded up to four: the slots past every list's
+            // end hold the sentinel (alpha 0)
+            bool stopped = false;
+            for (uint32_t e = 0; e < n_run && !stopped; e += 4) {
+              const uint32_t quad = *reinterpret_cast<const uint32_t *>(&s.list[my_list][e]);
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                // byte offset into the staged arrays (16-byte slots)
+                const uint32_t jo = u == 0 ? (quad << 4) & 0xff0u : (quad >> (8 * u - 4)) & 0xff0u;
+                const uint32_t j = jo >> 4;
                 const float4 g0 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g0) + jo);
                 const float4 g1 = *reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(s.g1) + jo);
                 const float dx = g0.x - fpx, dy = g0.y - fpy;
@@ -398,7 +404,11 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
                                       __float_as_uint(mw));
                     }
                 }
-                if (done == ~0ull) break;
+                if (done == ~0ull) {
+                    stopped = true;
+                    break;
+                }
+              }
             }
         }
         __syncthreads();
@@ -488,13 +498,54 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
             a.tgbh_sigma[(size_t)gy * Wg + gx] = sh;
         }
     }
-    if (!inside || (QUAD && k != 0)) return;
-    const size_t HW = (size_t)a.W * a.H;
-    const size_t o = (size_t)py * a.W + px;
     // the background seen through the remaining transmittance
     cr = __builtin_fmaf(T, a.bg[0], cr);
     cg = __builtin_fmaf(T, a.bg[1], cg);
     cb = __builtin_fmaf(T, a.bg[2], cb);
+    const size_t HW = (size_t)a.W * a.H;
+    if (!QUAD) {
+        // A wave holds an 8x8 quadrant, so its own stores would write the
+        // 32-byte halves of the tile's 64-byte rows.  The outputs go through
+        // LDS instead (the staging arrays are free once every wave has left
+        // the batch loop) and each wave stores four whole rows of 16 pixels
+        // per plane: every store instruction writes whole cache lines.
+        constexpr int kPlanes = CAPTURE ? 6 : 3;
+        float *sv = reinterpret_cast<float *>(s.g0);   // kPlanes x 256 floats
+        __syncthreads();
+        const int lp = (py - ty * kTile) * kTile + (px - tx * kTile);
+        sv[lp] = cr;
+        sv[256 + lp] = cg;
+        sv[512 + lp] = cb;
+        if (CAPTURE) {
+            sv[768 + lp] = D;
+            sv[1024 + lp] = S;
+            sv[1280 + lp] = 1.0f - T;
+        }
+        __syncthreads();
+        const int qx = tx * kTile + (tid & 15), qy = ty * kTile + (tid >> 4);
+        if (qx >= a.W || qy >= a.H) return;
+        const size_t o = (size_t)qy * a.W + qx;
+        const float vr = sv[tid], vg = sv[256 + tid], vb = sv[512 + tid];
+        a.rgb[o] = vr;
+        a.rgb[HW + o] = vg;
+        a.rgb[2 * HW + o] = vb;
+        if (a.tab) {
+            a.tab[o] = vr;
+            a.tab[HW + o] = vg;
+            a.tab[2 * HW + o] = vb;
+        }
+        if (CAPTURE && kPlanes == 6) {
+            const float vd = sv[768 + tid], vs = sv[1024 + tid];
+            if (a.depth) a.depth[o] = vd;
+            if (a.sigma) a.sigma[o] = vs;
+            if (a.alpha) a.alpha[o] = sv[1280 + tid];
+            if (a.tgb_depth) a.tgb_depth[o] = vd;
+            if (a.tgb_sigma) a.tgb_sigma[o] = vs;
+        }
+        return;
+    }
+    if (!inside || k != 0) return;
+    const size_t o = (size_t)py * a.W + px;
     a.rgb[o] = cr;
     a.rgb[HW + o] = cg;
     a.rgb[2 * HW + o] = cb;
