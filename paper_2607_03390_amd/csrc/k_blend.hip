@@ -64,7 +64,8 @@ __device__ inline float quad_sum(float v) {
 }
 
 // LDS of one blend block.  Staged per Gaussian: (u, v, qa, qb) and (qc,
-// opacity, depth, -) where q* = conic coefficients pre-scaled by -log2(e)
+// opacity, depth, f), f set once a pixel composites the Gaussian (the
+// temporal Gaussian buffer, written at the slot's own address), where q* = conic coefficients pre-scaled by -log2(e)
 // (and 1/2 on the squares, by the preprocess) so that log2 of the Gaussian
 // falloff is a three-FMA quadratic form and the opacity is one v_exp_f32.
 // The tile is cut into sixteen 4x4 sub-blocks; sub-block list L (quadrant
@@ -78,7 +79,6 @@ struct BlendLds {
     float4 g1[256];
     float4 col[256];
     int idx[256];
-    uint8_t flag[256];
     __align__(16) uint8_t list[16][256];
     __align__(16) uint32_t cnt[4][16];   // [staging wave][list] entries, then starts
     uint32_t len[16];                    // list lengths
@@ -215,7 +215,6 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
                 if (QUAD) lists &= 0xfu << (4 * q);
             }
         }
-        if (CAPTURE) s.flag[tid] = 0u;
         // order-preserving compaction of each sub-block's Gaussians: counts
         // per staging wave, then each wave's start in every list (s.cnt
         // becomes the exclusive prefix over waves, s.len the totals), then
@@ -326,7 +325,7 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
                     sw += w;
                     s1 = __builtin_fmaf(w, dd, s1);
                     s2 = __builtin_fmaf(w * dd, dd, s2);
-                    if (inc) s.flag[j] = 1u;
+                    if (inc) *reinterpret_cast<float *>(reinterpret_cast<char *>(s.g1) + jo + 12) = 1.0f;
                     if (CONTRIB) {
                         // max weight of this lane's entry over the wave's 16 pixels
                         float mw = w;
@@ -392,8 +391,9 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
                     s1 = __builtin_fmaf(w, dd, s1);
                     s2 = __builtin_fmaf(w * dd, dd, s2);
                     // the pixel composites the Gaussian (w = alpha T > 0); the
-                    // lanes of a group write the same flag
-                    if (inc) s.flag[j] = 1u;
+                    // lanes of a group write the same flag, in the slot's
+                    // staged record (no index to form)
+                    if (inc) *reinterpret_cast<float *>(reinterpret_cast<char *>(s.g1) + jo + 12) = 1.0f;
                     if (CONTRIB) {
                         // max weight over the group's 16 lanes (one Gaussian)
                         float mw = w;
@@ -412,7 +412,7 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
             }
         }
         __syncthreads();
-        if (CAPTURE && a.g_flag && tid < kBatch && kb < range.y && s.flag[tid])
+        if (CAPTURE && a.g_flag && tid < kBatch && kb < range.y && s.g1[tid].w != 0.0f)
             a.g_flag[s.idx[tid]] = 1u;
     }
 
