@@ -12,102 +12,116 @@ namespace tgs {
 
 namespace {
 
-
-// Tile of the r-th key of a Gaussian with tile rectangle rc: row-major over
-// the rectangle, or (rowpre != NULL) over its selected tiles, rows first,
-// O(1) per row from the per-row prefix sums of the tile mask.
-__device__ inline uint32_t key_tile(uint32_t r, ushort4 rc, const uint32_t *rowpre,
-                                    const int *sel_cols, int TX) {
-    int tx, ty;
+// Tile (tx, ty) of the r-th key of a Gaussian with tile rectangle rc:
+// row-major over the rectangle, or (rowpre != NULL) over its selected tiles,
+// rows first, O(1) per row from the per-row prefix sums of the tile mask.
+__device__ inline void key_tile_xy(uint32_t r, ushort4 rc, const uint32_t *rowpre,
+                                   const int *sel_cols, int TX, int &tx, int &ty) {
     if (!rowpre) {
         const uint32_t w = (uint32_t)(rc.z - rc.x + 1);
         ty = rc.y + (int)(r / w);
         tx = rc.x + (int)(r % w);
-    } else {
-        // four rows per step (eight independent loads), then the row
-        // holding the r-th selected tile among them
-        ty = rc.y;
-        const size_t s = (size_t)(TX + 1);
-        const uint32_t *row = rowpre + (size_t)ty * s;
-        for (;;) {
-            if (ty > (int)rc.w) {   // r past the Gaussian's count: cannot happen
-                tx = rc.x;
-                ty = rc.w;
-                break;
-            }
-            uint32_t c[4], b[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const bool in = ty + k <= (int)rc.w;
-                b[k] = in ? row[k * s + rc.x] : 0u;
-                c[k] = in ? row[k * s + rc.z + 1] - b[k] : 0u;
-            }
-            int k = 0;
-            while (k < 3 && r >= c[k]) {
-                r -= c[k];
-                ++k;
-            }
-            if (r < c[k]) {
-                ty += k;
-                tx = sel_cols[(size_t)ty * TX + b[k] + r];
-                break;
-            }
-            r -= c[k];
-            ty += 4;
-            row += 4 * s;
-        }
+        return;
     }
-    return (uint32_t)(ty * TX + tx);
+    // four rows per step (eight independent loads), then the row holding the
+    // r-th selected tile among them
+    ty = rc.y;
+    const size_t s = (size_t)(TX + 1);
+    const uint32_t *row = rowpre + (size_t)ty * s;
+    for (;;) {
+        if (ty > (int)rc.w) {   // r past the Gaussian's count: cannot happen
+            tx = rc.x;
+            ty = rc.w;
+            return;
+        }
+        uint32_t c[4], b[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const bool in = ty + k <= (int)rc.w;
+            b[k] = in ? row[k * s + rc.x] : 0u;
+            c[k] = in ? row[k * s + rc.z + 1] - b[k] : 0u;
+        }
+        int k = 0;
+        while (k < 3 && r >= c[k]) {
+            r -= c[k];
+            ++k;
+        }
+        if (r < c[k]) {
+            ty += k;
+            tx = sel_cols[(size_t)ty * TX + b[k] + r];
+            return;
+        }
+        r -= c[k];
+        ty += 4;
+        row += 4 * s;
+    }
 }
 
-// Block b emits output keys [1024 b, 1024 b + 1024), four per thread at
-// consecutive positions across the block (coalesced stores), whatever the
-// Gaussians' key counts: a Gaussian spanning thousands of tiles is spread
-// over many blocks instead of holding one wave.  The owner of the block's
-// first key comes from the key-block table written with the offsets; the
-// Gaussians starting inside the block mark their first position in LDS and
-// an inclusive max-scan gives every position its owner.  Past the key
-// capacity (cnt->n_sorted == 0 with keys) nothing is emitted: the host grows
-// the buffers and renders the frame again.
-constexpr int kDupKeys = kKeyBlock;
-static_assert(kDupKeys % 256 == 0, "whole keys per thread");
+// Inputs of key generation: the cnt->n_visible Gaussians in emission order
+// (didx), the start of each one's keys (offs, strictly increasing: every
+// emitted Gaussian has keys), the owner of every kKeyBlock-th key (kfirst),
+// and the tile rectangles / selection.
+struct DupIo {
+    const Counters *cnt;
+    const uint32_t *didx;
+    const uint32_t *offs;
+    const uint32_t *kfirst;
+    const ushort4 *rect;
+    const uint32_t *rowpre;
+    const int *sel_cols;
+    int TX;
+    int n_tiles;
+    uint2 *ranges;   // cleared by the first kernel of the emission
+};
 
-__global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
-                                                        const uint32_t *__restrict__ didx,
-                                                        const uint32_t *__restrict__ offs,
-                                                        const uint32_t *__restrict__ kfirst,
-                                                        const ushort4 *__restrict__ rect,
-                                                        const uint32_t *rowpre, const int *sel_cols,
-                                                        int TX, int n_tiles, uint32_t *tkey,
-                                                        uint32_t *tval, uint2 *ranges) {
-    __shared__ int s_owner[kDupKeys];           // window index of each position's owner
-    __shared__ uint32_t s_off[kDupKeys + 1];    // offsets of window Gaussians j0 + k
-    __shared__ uint32_t s_g[kDupKeys + 1];      // their Gaussian indices
-    __shared__ int s_wmax[4];
+// Window of the Gaussians owning output positions [P0, P1) (P0 a multiple
+// of kKeyBlock, P1 - P0 <= KD): from j0, the owner of P0, to the owner of
+// P1 (the next block's first key) or, for the block holding the last key K,
+// to the last Gaussian.  Entry k >= 1 starts at or after P0 + k (strictly
+// increasing offsets), so at most KD entries can start before P1.
+template <int KD>
+__device__ inline void dup_window(const DupIo &io, uint32_t P0, uint32_t P1, uint32_t K,
+                                  uint32_t V, uint32_t &j0, uint32_t &nw) {
+    j0 = io.kfirst[P0 / kKeyBlock];
+    const uint32_t jn = P1 < K ? io.kfirst[P1 / kKeyBlock] + 1u : V;
+    nw = jn - j0 < (uint32_t)KD ? jn - j0 : (uint32_t)KD;
+}
+
+// Owners of the output positions [P0, P1) by a block of NT threads: s_off[k]
+// / s_g[k] = start and Gaussian index of window entry k (those starting
+// before P1), s_owner[i] = the window entry owning position P0 + i.  The
+// window is read in one step (every load in flight at once).  Ends with a
+// barrier.
+template <int KD, int NT>
+__device__ inline void dup_owners(const DupIo &io, uint32_t P0, uint32_t P1, uint32_t K,
+                                  uint32_t V, int *s_owner, uint32_t *s_off, uint32_t *s_g,
+                                  int *s_wmax) {
+    static_assert(KD % NT == 0 && KD % kKeyBlock == 0, "whole steps and key blocks");
+    constexpr int kPer = KD / NT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int t = blockIdx.x * blockDim.x + tid; t < n_tiles; t += gridDim.x * blockDim.x)
-        ranges[t] = make_uint2(0u, 0u);
-    const uint32_t V = cnt->n_visible, K = cnt->n_sorted;
-    const uint32_t P0 = blockIdx.x * (uint32_t)kDupKeys;
-    if (K == 0u || P0 >= K) return;   // block-uniform
-    const uint32_t P1 = K - P0 < (uint32_t)kDupKeys ? K : P0 + kDupKeys;
-    for (int k = tid; k < kDupKeys; k += 256) s_owner[k] = -1;
-    const uint32_t j0 = kfirst[blockIdx.x];   // owner of key P0 (offs[j0] <= P0)
+    uint32_t j0, nw;
+    dup_window<KD>(io, P0, P1, K, V, j0, nw);
+    // clamped indices, no branches: every load is issued before the first wait
+    uint32_t o[kPer], g[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const uint32_t k = (uint32_t)(tid + NT * i), kc = k < nw ? k : nw - 1u;
+        o[i] = io.offs[j0 + kc];
+        g[i] = io.didx[j0 + kc];
+    }
+    for (int k = tid; k < KD; k += NT) s_owner[k] = -1;
     __syncthreads();
-    // at most kDupKeys Gaussians after j0 start inside the block's keys
-    for (int k = tid; k <= kDupKeys; k += 256) {
-        const uint32_t j = j0 + (uint32_t)k;
-        if (j < V) {
-            const uint32_t o = offs[j];
-            s_off[k] = o;
-            s_g[k] = didx[j];
-            if (k == 0) s_owner[0] = 0;
-            else if (o < P1) s_owner[o - P0] = k;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int k = tid + NT * i;
+        if ((uint32_t)k < nw && (k == 0 || o[i] < P1)) {
+            s_off[k] = o[i];
+            s_g[k] = g[i];
+            s_owner[k == 0 ? 0 : (int)(o[i] - P0)] = k;
         }
     }
     __syncthreads();
     // inclusive max-scan of the marks: kPer consecutive entries per thread
-    constexpr int kPer = kDupKeys / 256;
     int v[kPer], m = -1;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
@@ -117,8 +131,8 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
     int inc = m;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(inc, d);
-        if (lane >= d) inc = max(inc, o);
+        const int t = __shfl_up(inc, d);
+        if (lane >= d) inc = max(inc, t);
     }
     int ex = __shfl_up(inc, 1);
     if (lane == 0) ex = -1;
@@ -128,15 +142,53 @@ __global__ __launch_bounds__(256) void duplicate_kernel(const Counters *cnt,
 #pragma unroll
     for (int i = 0; i < kPer; ++i) s_owner[kPer * tid + i] = max(v[i], ex);
     __syncthreads();
+}
+
+
+// Block b emits output keys [1024 b, 1024 b + 1024), four per thread at
+// consecutive positions across the block (coalesced stores), whatever the
+// Gaussians' key counts: a Gaussian spanning thousands of tiles is spread
+// over many blocks instead of holding one wave.  Owners of the positions
+// come from the key-block table and the window of Gaussians starting inside
+// the block (dup_owners).  Past the key capacity (cnt->n_sorted == 0 with
+// keys) nothing is emitted: the host grows the buffers and renders the
+// frame again.
+constexpr int kDupKeys = kKeyBlock;
+
+__global__ __launch_bounds__(256) void duplicate_kernel(DupIo io, uint32_t *tkey, uint32_t *tval) {
+    __shared__ int s_owner[kDupKeys];
+    __shared__ uint32_t s_off[kDupKeys];
+    __shared__ uint32_t s_g[kDupKeys];
+    __shared__ int s_wmax[4];
+    const int tid = threadIdx.x;
+    for (int t = blockIdx.x * blockDim.x + tid; t < io.n_tiles; t += gridDim.x * blockDim.x)
+        io.ranges[t] = make_uint2(0u, 0u);
+    const uint32_t V = io.cnt->n_visible, K = io.cnt->n_sorted;
+    const uint32_t P0 = blockIdx.x * (uint32_t)kDupKeys;
+    if (K == 0u || P0 >= K) return;   // block-uniform
+    const uint32_t P1 = K - P0 < (uint32_t)kDupKeys ? K : P0 + kDupKeys;
+    dup_owners<kDupKeys, 256>(io, P0, P1, K, V, s_owner, s_off, s_g, s_wmax);
+    // positions past the keys take the last key's owner (no branch before
+    // the stores, so every rectangle load is in flight together)
+    constexpr int kPer = kDupKeys / 256;
+    uint32_t g[kPer], r[kPer];
+    ushort4 rc[kPer];
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-        const uint32_t i = (uint32_t)(tid + 256 * k);
-        const uint32_t p = P0 + i;
+        const uint32_t p = P0 + (uint32_t)(tid + 256 * k), pc = p < P1 ? p : P1 - 1u;
+        const int w = s_owner[pc - P0];
+        g[k] = s_g[w];
+        r[k] = pc - s_off[w];
+        rc[k] = io.rect[g[k]];
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const uint32_t p = P0 + (uint32_t)(tid + 256 * k);
+        int tx, ty;
+        key_tile_xy(r[k], rc[k], io.rowpre, io.sel_cols, io.TX, tx, ty);
         if (p < P1) {
-            const int w = s_owner[i];
-            const uint32_t g = s_g[w];
-            tkey[p] = key_tile(p - s_off[w], rect[g], rowpre, sel_cols, TX);
-            tval[p] = g;
+            tkey[p] = (uint32_t)(ty * io.TX + tx);
+            tval[p] = g[k];
         }
     }
 }
@@ -197,8 +249,8 @@ void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *
         return;
     }
     const uint32_t blocks = (cap + kDupKeys - 1) / kDupKeys;
-    duplicate_kernel<<<blocks, 256, 0, st>>>(cnt, didx, offs, kfirst, rect, rowpre, sel_cols, TX,
-                                             n_tiles, tkey, tval, ranges);
+    const DupIo io{cnt, didx, offs, kfirst, rect, rowpre, sel_cols, TX, n_tiles, ranges};
+    duplicate_kernel<<<blocks, 256, 0, st>>>(io, tkey, tval);
 }
 
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,

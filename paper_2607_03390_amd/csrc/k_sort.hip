@@ -91,7 +91,21 @@ struct DepthIo {
     uint32_t tag, cap;
     const uint32_t *pre_partial;   // preprocess per-block survivor / newly-visible counts
     int n_pre;
+    // 1 (fewer than 2^24 Gaussians): the value the passes carry is
+    // index << 8 | min(count, 255), so the last pass reads the key counts
+    // below 255 from it instead of gathering them by index
+    int pack;
 };
+
+// Key count of the Gaussian a carried value stands for, and its index.
+__device__ inline uint32_t carried_count(const DepthIo &io, uint32_t v) {
+    if (!io.pack) return io.count[v];
+    const uint32_t c = v & 255u;
+    return c < 255u ? c : io.count[v >> 8];
+}
+__device__ inline uint32_t carried_index(const DepthIo &io, uint32_t v) {
+    return io.pack ? v >> 8 : v;
+}
 
 // Digit counts of one partition: counts[part * 256 + d] (one coalesced 1 KB
 // row per block); in the last depth pass also the digit weight sums:
@@ -130,7 +144,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
         if (keep) {
             const uint32_t d = (kin[idx] >> shift) & 255u;
             atomicAdd(&s_h[wave][d], 1u);
-            if (MODE == kLast) atomicAdd(&s_w[wave][d], io.count[vin[idx]]);
+            if (MODE == kLast) atomicAdd(&s_w[wave][d], carried_count(io, vin[idx]));
         }
     }
     __syncthreads();
@@ -335,8 +349,9 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         ok[j] = idx < K;
         key[j] = ok[j] ? kin[idx] : 0xffffffffu;
         if (MODE == kFirst) {
-            val[j] = idx;
-            ok[j] = ok[j] && io.count[idx] > 0u;
+            const uint32_t c = ok[j] ? io.count[idx] : 0u;
+            val[j] = io.pack ? idx << 8 | (c < 255u ? c : 255u) : idx;
+            ok[j] = ok[j] && c > 0u;
         } else {
             val[j] = ok[j] ? vin[idx] : 0u;
         }
@@ -345,7 +360,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t woff_mine = MODE == kLast ? offsets[(size_t)np * kRadix + (size_t)part * kRadix + tid] : 0u;
     if (MODE == kLast) {
 #pragma unroll
-        for (int j = 0; j < IPT; ++j) wt[j] = ok[j] ? io.count[val[j]] : 0u;
+        for (int j = 0; j < IPT; ++j) wt[j] = ok[j] ? carried_count(io, val[j]) : 0u;
     }
     for (int k = tid; k < 4 * kRadix; k += kSortThreads) s_wh[k] = 0u;
     // global start of digit tid: digits below it, then partitions before this one
@@ -437,7 +452,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         } else {
             kout[out] = kk;
         }
-        vout[out] = s_vals[i];
+        vout[out] = MODE == kLast ? carried_index(io, s_vals[i]) : s_vals[i];
     }
 }
 
@@ -531,6 +546,7 @@ void launch_depth_sort(int n, uint32_t *count, const ushort4 *rect, const uint32
     io.cap = cap;
     io.pre_partial = pre_partial;
     io.n_pre = n_pre;
+    io.pack = n < (1 << 24) ? 1 : 0;
     const uint32_t nn = (uint32_t)(n > 0 ? n : 0);
     if (ipt_for(nn) == kIptSmall)
         depth_passes<kIptSmall>(nn, dkey, k_a, v_a, k_b, v_b, scratch, io, st);
