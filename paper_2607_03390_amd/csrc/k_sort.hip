@@ -46,6 +46,10 @@ constexpr int kRadix = 256;
 // fill the chip).
 constexpr int kIptLarge = 15;   // 3840-key partitions
 constexpr int kIptSmall = 4;    // 1024-key partitions
+// keys below 2^16 (tile ids of grids up to 65536 tiles) are staged in LDS as
+// 16-bit values, which leaves room for 5120-key partitions at four blocks
+// per CU
+constexpr int kIptLarge16 = 20;
 
 enum { kPlain = 0, kFirst = 1, kLast = 2 };
 
@@ -127,24 +131,32 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
     }
     __syncthreads();
     const uint32_t wbase = part * kTile + (uint32_t)wave * (64u * IPT);
+    // every load first (clamped index, no branch), then the counting
+    uint32_t dg[IPT], wv[MODE == kLast ? IPT : 1];
+    bool keep[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
-        bool keep = idx < K;
-        if (MODE == kFirst && keep) {
+        keep[j] = idx < K;
+        const uint32_t ic = keep[j] ? idx : K - 1u;
+        dg[j] = (kin[ic] >> shift) & 255u;
+        if (MODE == kFirst) {
             uint32_t c;
             if (io.rowpre) {
-                c = masked_count(io.rect[idx], io.rowpre, io.TX);
-                io.count[idx] = c;
+                c = masked_count(io.rect[ic], io.rowpre, io.TX);
+                if (keep[j]) io.count[idx] = c;
             } else {
-                c = io.count[idx];
+                c = io.count[ic];
             }
-            keep = c > 0u;
+            keep[j] = keep[j] && c > 0u;
         }
-        if (keep) {
-            const uint32_t d = (kin[idx] >> shift) & 255u;
-            atomicAdd(&s_h[wave][d], 1u);
-            if (MODE == kLast) atomicAdd(&s_w[wave][d], carried_count(io, vin[idx]));
+        if (MODE == kLast) wv[j] = vin[ic];
+    }
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+        if (keep[j]) {
+            atomicAdd(&s_h[wave][dg[j]], 1u);
+            if (MODE == kLast) atomicAdd(&s_w[wave][dg[j]], carried_count(io, wv[j]));
         }
     }
     __syncthreads();
@@ -290,13 +302,14 @@ __device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s
     __syncthreads();
 }
 
-template <int IPT, int MODE>
+// KT: the type the keys are staged in (uint16_t: every key below 2^16).
+template <int IPT, int MODE, typename KT>
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
     uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
     const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ chunk_sums, DepthIo io) {
     constexpr uint32_t kTile = kSortThreads * IPT;
-    __shared__ uint32_t s_keys[kTile];
+    __shared__ KT s_keys[kTile];
     __shared__ uint32_t s_vals[kTile];
     __shared__ uint32_t s_wt[MODE == kLast ? kTile : 1];   // weights, then their exclusive scan
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
@@ -341,7 +354,9 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     // issue every global load of the block before the first barrier
     const uint32_t wbase = base + (uint32_t)wave * (64u * IPT);
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-    uint32_t key[IPT], val[IPT], rank[IPT], wt[MODE == kLast ? IPT : 1];
+    // 16-bit keys: each item's rank is kept in the upper half of its key
+    constexpr bool kPack = sizeof(KT) == 2;
+    uint32_t key[IPT], val[IPT], rank[kPack ? 1 : IPT], wt[MODE == kLast ? IPT : 1];
     bool ok[IPT];
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
@@ -387,7 +402,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         __builtin_amdgcn_wave_barrier();
         if (valid && below == 0) s_wh[wave * kRadix + d] = before + (uint32_t)__popcll(peers);
         __builtin_amdgcn_wave_barrier();
-        rank[j] = before + below;
+        if constexpr (kPack) key[j] = (key[j] & 0xffffu) | ((before + below) << 16);
+        else rank[j] = before + below;
     }
     __syncthreads();
 
@@ -408,9 +424,17 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         if (ok[j]) {
-            const uint32_t dj = (key[j] >> shift) & 255u;
-            const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rank[j];
-            s_keys[pos] = key[j];
+            uint32_t kj, rk;
+            if constexpr (kPack) {
+                kj = key[j] & 0xffffu;
+                rk = key[j] >> 16;
+            } else {
+                kj = key[j];
+                rk = rank[j];
+            }
+            const uint32_t dj = (kj >> shift) & 255u;
+            const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rk;
+            s_keys[pos] = (KT)kj;
             s_vals[pos] = val[j];
             if (MODE == kLast) s_wt[pos] = wt[j];
         }
@@ -440,7 +464,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     }
 
     for (uint32_t i = tid; i < nv; i += kSortThreads) {
-        const uint32_t kk = s_keys[i];
+        const uint32_t kk = (uint32_t)s_keys[i];
         const uint32_t dj = (kk >> shift) & 255u;
         const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
         if (MODE == kLast) {
@@ -463,7 +487,7 @@ inline uint32_t n_partitions(uint32_t K, int ipt) {
     return np ? np : 1u;
 }
 
-template <int IPT, int MODE>
+template <int IPT, int MODE, typename KT = uint32_t>
 void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *ki,
               const uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, const DepthIo &io,
               hipStream_t st) {
@@ -477,7 +501,7 @@ void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *
         ki, vi, nd, n_max, shift, np, io, table, table + (size_t)np * kRadix);
     sort_colscan_kernel<<<tables * 16 * kChunks, 256, 0, st>>>(nd, n_max, kSortThreads * IPT, np,
                                                                 table, chunk_sums);
-    sort_downsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
+    sort_downsweep_kernel<IPT, MODE, KT><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
                                                                   np, table, chunk_sums, io);
 }
 
@@ -491,12 +515,12 @@ void depth_passes(uint32_t n, const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a
     one_pass<IPT, kLast>(n_vis, n, 24, k_a, v_a, nullptr, v_b, scratch, io, st);
 }
 
-template <int IPT>
+template <int IPT, typename KT = uint32_t>
 void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes, uint32_t *ki,
                   uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, hipStream_t st) {
     const DepthIo none{};
     for (int p = 0; p < passes; ++p) {
-        one_pass<IPT, kPlain>(n_dev, n_max, begin_bit + 8 * p, ki, vi, ko, vo, scratch, none, st);
+        one_pass<IPT, kPlain, KT>(n_dev, n_max, begin_bit + 8 * p, ki, vi, ko, vo, scratch, none, st);
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }
@@ -522,6 +546,9 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int 
     if (ipt_for(n_hint < n_max ? n_hint : n_max) == kIptSmall)
         plain_passes<kIptSmall>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
+    else if (begin_bit + 8 * passes <= 16)
+        plain_passes<kIptLarge16, uint16_t>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt,
+                                            vals_alt, scratch, st);
     else
         plain_passes<kIptLarge>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
