@@ -149,8 +149,16 @@ def parse():
     ap.add_argument("--valu-summary", nargs=2, metavar=("VALU_JSON", "STATS_CSV"),
                     help="VALU issue per kernel from an aggregated SQ_INSTS_VALU run and a "
                          "kernel_stats.csv, to --out-md (no GPU)")
+    ap.add_argument("--workloads-summary", metavar="DIR",
+                    help="table of DIR/<workload>.json (this script's output per workload) for "
+                         "the five workloads, to --out-md (no GPU)")
+    ap.add_argument("--ablation-summary", metavar="JSON",
+                    help="table of the ablation rows of a --ablation run's output, to --out-md "
+                         "(no GPU)")
     ap.add_argument("--out-json")
     ap.add_argument("--out-md")
+    ap.add_argument("--title", default="", help="heading of a summary")
+    ap.add_argument("--note", default="", help="paragraph after a summary's table")
     ap.add_argument("--command", default="", help="the profiled command, quoted in the summary")
     return ap.parse_args()
 
@@ -201,7 +209,73 @@ def _short(name):
     return n.split("(")[0]
 
 
-def trace_summary(stats_csv, out_md, command):
+def _doc(title, body, note):
+    """A summary file: heading, body, closing paragraph."""
+    parts = ([f"# {title}", ""] if title else []) + [body.rstrip("\n")]
+    if note:
+        parts += ["", note]
+    return "\n".join(parts) + "\n"
+
+
+def workloads_summary(d, out_md, command, title, note):
+    names = ["tiny", "object", "room", "city", "stress"]
+    rows, vrows = [], []
+    for w in names:
+        path = os.path.join(d, f"{w}.json")
+        if not os.path.exists(path):
+            continue
+        r = json.loads(open(path).read().strip().splitlines()[-1])
+        c, t, f = r["config"], r["temporal"], r["full"]
+        rows.append(f"| {w} | {c['gaussians']:,} | {c['width']}x{c['height']} (TGB x{c['tgb_downscale']}) | "
+                    f"{t['fps']:.1f} ({t['ms_per_frame']:.3f}) | {f['fps']:.1f} ({f['ms_per_frame']:.3f}) | "
+                    f"{r['speedup_temporal_vs_full']:.3f} | {t['tgsf_pct']:.2f} | {t['sr_tile_pct']:.2f} | "
+                    f"{r['psnr_temporal_vs_full']['mean_db']:.2f} | {r['ssim_temporal_vs_full']['mean']:.4f} | "
+                    f"{r['roofline']['frac']:.3f} | {r['memory']['temporal_over_full']:.3f} |")
+        for k in ("footprint_tile_rule", "empty_far", "tgb_downscale_1", "tgb_downscale_2",
+                  "sort_depth_first", "sort_per_tile"):
+            v = r.get(k)
+            if v:
+                vrows.append(f"| {w} | {v['label']} | {v['temporal_fps']:.1f} | {v['sr_tile_pct']} | "
+                             f"{v['psnr_mean_db']} | {v['ssim_mean']} | {v.get('full_fps', '')} |")
+    body = "\n".join([
+        "Command, from the repository root, per workload:", "", "```", command, "```", "",
+        "Temporal = the TemporalGS schedule over the workload's camera path; full = the 3DGS render "
+        "of every frame of the same path.  Roofline = the benchmark's dominant kernel (the "
+        "preprocess) against HBM.", "",
+        "| workload | Gaussians | image | temporal FPS (ms) | full FPS (ms) | temporal / full | TGSF % | "
+        "SR tile % | PSNR dB | SSIM | roofline frac | memory temporal/full |",
+        "|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"] + rows + [
+        "", "| workload | variant | temporal FPS | SR tile % | PSNR dB | SSIM | full FPS |",
+        "|---|---|---:|---:|---:|---:|---:|"] + vrows)
+    md = _doc(title, body, note)
+    if out_md:
+        open(out_md, "w").write(md)
+    print(md)
+
+
+def ablation_summary(path, out_md, command, title, note):
+    d = json.loads(open(path).read().strip().splitlines()[-1])
+    m = d["memory"]
+    mib = lambda b: b / 2 ** 20
+    rows = [f"| {a['label']} | {a['temporal_fps']:.1f} | {a['tgsf_pct']:.2f} | {a['sr_tile_pct']} | "
+            f"{a['psnr_mean_db']} | {a['ssim_mean']} | {a.get('full_fps', '')} |" for a in d["ablation"]]
+    body = "\n".join([
+        "Command (one MI355X, from the repository root):", "", "```", command, "```", "",
+        f"Headline in the same run: temporal {d['temporal']['fps']:.2f} FPS, full {d['full']['fps']:.2f} "
+        f"FPS (x{d['speedup_temporal_vs_full']:.3f}); SSIM mean {d['ssim_temporal_vs_full']['mean']}, "
+        f"PSNR mean {d['psnr_temporal_vs_full']['mean_db']:.2f} dB.", "",
+        f"Device memory (hipMemGetInfo deltas): scene {mib(m['scene_bytes']):.0f} MiB, full-render "
+        f"path {mib(m['full_render_bytes']):.0f} MiB, temporal path {mib(m['temporal_bytes']):.0f} MiB "
+        f"(x{m['temporal_over_full']:.4f}).", "",
+        "| setting | temporal FPS | TGSF % | SR tile % | PSNR dB | SSIM | full FPS |",
+        "|---|---:|---:|---:|---:|---:|---:|"] + rows)
+    md = _doc(title, body, note)
+    if out_md:
+        open(out_md, "w").write(md)
+    print(md)
+
+
+def trace_summary(stats_csv, out_md, command, title="", note=""):
     rows = sorted(_kernel_stats(stats_csv).items(), key=lambda kv: -kv[1]["total_ns"])
     total = sum(r["total_ns"] for _, r in rows)
     lines = ["| total ms | % | calls | avg us | min us | max us | kernel |",
@@ -210,15 +284,15 @@ def trace_summary(stats_csv, out_md, command):
         lines.append(f"| {r['total_ns'] / 1e6:.2f} | {100 * r['total_ns'] / total:.1f} | {r['calls']} | "
                      f"{r['avg_ns'] / 1e3:.1f} | {r['min_ns'] / 1e3:.1f} | {r['max_ns'] / 1e3:.1f} | "
                      f"`{_short(name)}` |")
-    md = "\n".join(["Command (one MI355X, from the repository root):", "", "```", command, "```", "",
-                    f"{len(rows)} kernels, {total / 1e6:.1f} ms in total, sorted by total time.",
-                    ""] + lines) + "\n"
+    md = _doc(title, "\n".join(["Command (one MI355X, from the repository root):", "", "```", command,
+                                "```", "", f"{len(rows)} kernels, {total / 1e6:.1f} ms in total, sorted "
+                                "by total time.", ""] + lines), note)
     if out_md:
         open(out_md, "w").write(md)
     print(md)
 
 
-def valu_summary(valu_json, stats_csv, out_md, command):
+def valu_summary(valu_json, stats_csv, out_md, command, title="", note=""):
     """VALU issue fraction = wave64 VALU instructions per dispatch / what the
     chip can issue in the kernel's average duration: a wave64 instruction
     holds a 16-lane SIMD for 4 cycles, 4 SIMDs per CU, 256 CUs at 2.4 GHz,
@@ -237,15 +311,17 @@ def valu_summary(valu_json, stats_csv, out_md, command):
     lines = ["| kernel | launches | avg us | VALU wave instr. (M) | VALU issue |",
              "|---|---:|---:|---:|---:|"]
     lines += [f"| `{n}` | {c} | {a:.1f} | {i:.2f} | {f:.3f} |" for _, n, c, a, i, f in rows]
-    md = "\n".join(["Commands (one MI355X, from the repository root):", "", "```", command, "```", "",
-                    "VALU issue = SQ_INSTS_VALU per dispatch / (256 wave instructions per cycle x "
-                    "2.4 GHz x the kernel trace's average duration).", ""] + lines) + "\n"
+    md = _doc(title, "\n".join(["Commands (one MI355X, from the repository root):", "", "```", command,
+                                "```", "", "VALU issue = SQ_INSTS_VALU per dispatch / (256 wave "
+                                "instructions per cycle x 2.4 GHz x the kernel trace's average "
+                                "duration).", ""] + lines), note)
     if out_md:
         open(out_md, "w").write(md)
     print(md)
 
 
-def traffic_summary(fetch_json, write_json, stats_csv, calib_mib, out_json, out_md, command):
+def traffic_summary(fetch_json, write_json, stats_csv, calib_mib, out_json, out_md, command,
+                    title="", note=""):
     """Bytes per launch = counter mean (KiB per dispatch) x the factor that
     maps the copy kernel's reading to the bytes it moved (calib_mib MiB read
     and written); GB/s = bytes per launch / the trace's average duration."""
@@ -288,12 +364,13 @@ def traffic_summary(fetch_json, write_json, stats_csv, calib_mib, out_json, out_
         lines.append(f"| `{name}` | {e.get('calls', e['dispatches'])} | {e.get('avg_us', float('nan')):.1f} | "
                      f"{e['fetch_bytes'] / 1e6:.2f} | {e['write_bytes'] / 1e6:.2f} | "
                      f"{e.get('gbs', float('nan')):.0f} | {e.get('hbm_frac', float('nan')):.3f} |")
-    md = "\n".join(["Commands (one MI355X, from the repository root; one counter per pass):", "", "```",
-                    command, "```", "",
-                    f"Calibration: a {calib_mib} MiB device copy reads FETCH_SIZE x {f_scale:.3f} and "
-                    f"WRITE_SIZE x {w_scale:.3f} of the bytes it moves; every kernel's counters are "
-                    "scaled by those factors.  GB/s = calibrated bytes per launch / the kernel "
-                    "trace's average duration of the same kernel.", ""] + lines) + "\n"
+    md = _doc(title, "\n".join(["Commands (one MI355X, from the repository root; one counter per pass):",
+                                "", "```", command, "```", "",
+                                f"Calibration: a {calib_mib} MiB device copy reads FETCH_SIZE x "
+                                f"{f_scale:.3f} and WRITE_SIZE x {w_scale:.3f} of the bytes it moves; "
+                                "every kernel's counters are scaled by those factors.  GB/s = "
+                                "calibrated bytes per launch / the kernel trace's average duration of "
+                                "the same kernel.", ""] + lines), note)
     if out_md:
         open(out_md, "w").write(md)
     print(md)
@@ -306,13 +383,19 @@ def main():
         return
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary, args.copy_calibration_mb or 256, args.out_json,
-                        args.out_md, args.command)
+                        args.out_md, args.command, args.title, args.note)
         return
     if args.trace_summary:
-        trace_summary(args.trace_summary, args.out_md, args.command)
+        trace_summary(args.trace_summary, args.out_md, args.command, args.title, args.note)
         return
     if args.valu_summary:
-        valu_summary(*args.valu_summary, args.out_md, args.command)
+        valu_summary(*args.valu_summary, args.out_md, args.command, args.title, args.note)
+        return
+    if args.workloads_summary:
+        workloads_summary(args.workloads_summary, args.out_md, args.command, args.title, args.note)
+        return
+    if args.ablation_summary:
+        ablation_summary(args.ablation_summary, args.out_md, args.command, args.title, args.note)
         return
     if args.tgb_downscale is None:
         args.tgb_downscale = 2 if args.workload == "city" else 1
