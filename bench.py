@@ -240,8 +240,8 @@ def workloads_summary(d, out_md, command, title, note):
     body = "\n".join([
         "Command, from the repository root, per workload:", "", "```", command, "```", "",
         "Temporal = the TemporalGS schedule over the workload's camera path; full = the 3DGS render "
-        "of every frame of the same path.  Roofline = the benchmark's dominant kernel (the "
-        "preprocess) against HBM.", "",
+        "of every frame of the same path.  Roofline frac = the benchmark's roofline line: its "
+        "dominant kernel's achieved rate against that kernel's peak.", "",
         "| workload | Gaussians | image | temporal FPS (ms) | full FPS (ms) | temporal / full | TGSF % | "
         "SR tile % | PSNR dB | SSIM | roofline frac | memory temporal/full |",
         "|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"] + rows + [
@@ -698,8 +698,12 @@ def main():
     deg = wl.scene.sh_degree
     stage_ms = {k: prof[k]["ms"] for k in ("preprocess", "blend_ref", "blend_tgs")}
     dom = max(stage_ms, key=lambda k: stage_ms[k])
+    # counter-based traffic: taken on the room workload in the default
+    # settings, with the kernel sources of the hash it records
     traffic_all = None
-    if os.path.exists(TRAFFIC_FILE):
+    profiled = (args.workload == "room" and args.tgb_downscale == 1 and args.sort_path == "auto"
+                and args.blend_split == 12 and args.frames is None)
+    if profiled and os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
         if tr.get("kernel_source_sha") == kernel_source_hash():
             traffic_all = tr["kernels"]
