@@ -8,7 +8,7 @@
 //    full-resolution geometry buffer the preprocess launch runs it);
 //  - occluded tiles of the newly visible Gaussians, one wave per
 //    (Gaussian, tile) pair with a wave ballot over the tile's 256 pixels,
-//    the pairs of 1024 Gaussians dealt out over the waves of a block;
+//    the pairs of 1024 Gaussians dealt out over the four waves of a block;
 //  - tile selection and compaction in one launch, one block per tile row,
 //    including the per-row prefix sums of the mask used by the key counts.
 // (The stitching of the tiles that are not re-rendered, Eq. 4, runs in the
@@ -103,7 +103,9 @@ __device__ inline uint32_t occ_box(int i, const float4 *g, const ushort4 *rect, 
     return (uint32_t)((ex1 - ex0 + 1) * (ey1 - ey0 + 1));
 }
 
-constexpr int kOccThreads = 1024;            // one Gaussian per thread
+constexpr int kOccThreads = 256;
+constexpr int kOccPer = 4;                                 // consecutive Gaussians per thread
+constexpr int kOccBlock = kOccThreads * kOccPer;           // 1024 Gaussians per block
 constexpr int kOccWaves = kOccThreads / 64;
 
 // Exclusive scan across a block of kOccThreads threads, one value each;
@@ -130,36 +132,49 @@ __device__ inline uint32_t occ_block_scan(uint32_t v, uint32_t *s_wave, uint32_t
     return off + inc - v;
 }
 
-// One block per 1024 Gaussians.  The newly visible ones that can reach a
-// tile are compacted in LDS with the start of their (Gaussian, tile) pairs
-// (two block scans).  Wave w takes the pairs p = w (mod 16), 64 at a time: lane
+// One block per 1024 Gaussians, four consecutive ones per thread (a launch
+// of few waves: most blocks find no newly visible Gaussian).  The newly
+// visible ones that can reach a tile are compacted in LDS with the start of
+// their (Gaussian, tile) pairs (two block scans, index order).  Wave w takes
+// the pairs p = w (mod 4), 64 at a time: lane
 // l finds the owner and tile of its pair (the searches run side by side),
 // then the wave tests the pairs one after another with their data broadcast
 // from the lanes: each lane tests four pixel centres and a ballot marks the
 // tile.  Dealing the pairs out one by one spreads a block's pairs, however
-// few Gaussians hold them, evenly over its sixteen waves.  Marks are plain
+// few Gaussians hold them, evenly over its four waves.  Marks are plain
 // byte stores of 1, so concurrent writers agree.
 __global__ __launch_bounds__(kOccThreads) void occluded_kernel(WarpK w, int n,
                                                                const uint8_t *__restrict__ status,
                                                                const float4 *__restrict__ g,
                                                                const ushort4 *__restrict__ rect,
                                                                uint8_t *oc) {
-    __shared__ uint32_t s_idx[kOccThreads];   // compacted Gaussians
-    __shared__ uint32_t s_off[kOccThreads];   // start of their pairs
+    __shared__ uint32_t s_idx[kOccBlock];   // compacted Gaussians
+    __shared__ uint32_t s_off[kOccBlock];   // start of their pairs
     __shared__ uint32_t s_wave[kOccWaves];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int i = blockIdx.x * kOccThreads + tid;
-    uint32_t c = 0u;
-    if (i < n && (status[i] & 2u)) {
-        int3 box;
-        c = occ_box(i, g, rect, &box);
+    const int i0 = blockIdx.x * kOccBlock + tid * kOccPer;
+    uint32_t c[kOccPer], na = 0u, np = 0u;
+#pragma unroll
+    for (int k = 0; k < kOccPer; ++k) {
+        c[k] = 0u;
+        if (i0 + k < n && (status[i0 + k] & 2u)) {
+            int3 box;
+            c[k] = occ_box(i0 + k, g, rect, &box);
+        }
+        na += c[k] ? 1u : 0u;
+        np += c[k];
     }
     uint32_t total, n_act;
-    const uint32_t oa = occ_block_scan(c ? 1u : 0u, s_wave, &n_act);
-    const uint32_t op = occ_block_scan(c, s_wave, &total);
-    if (c) {
-        s_idx[oa] = (uint32_t)i;
-        s_off[oa] = op;
+    uint32_t oa = occ_block_scan(na, s_wave, &n_act);
+    uint32_t op = occ_block_scan(np, s_wave, &total);
+#pragma unroll
+    for (int k = 0; k < kOccPer; ++k) {
+        if (c[k]) {
+            s_idx[oa] = (uint32_t)(i0 + k);
+            s_off[oa] = op;
+            ++oa;
+            op += c[k];
+        }
     }
     __syncthreads();
     const uint32_t mine = total > (uint32_t)wave ? (total - (uint32_t)wave + kOccWaves - 1) / kOccWaves : 0u;
@@ -305,8 +320,8 @@ void launch_fill_query(const FillK &f, hipStream_t st) {
 void launch_occluded(const WarpK &w, int n, const uint8_t *status, const float4 *g,
                      const ushort4 *rect, uint8_t *oc, hipStream_t st) {
     if (n <= 0) return;
-    occluded_kernel<<<(n + kOccThreads - 1) / kOccThreads, kOccThreads, 0, st>>>(w, n, status, g,
-                                                                                rect, oc);
+    occluded_kernel<<<(n + kOccBlock - 1) / kOccBlock, kOccThreads, 0, st>>>(w, n, status, g, rect,
+                                                                            oc);
 }
 
 void launch_select(int TX, int TY, int mode, const uint8_t *oc, const uint8_t *um, uint8_t *sel,
