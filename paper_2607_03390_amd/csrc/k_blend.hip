@@ -687,8 +687,9 @@ void launch_blend(const BlendArgs &a0, int n_blocks, hipStream_t st, hipEvent_t 
     if (n_blocks <= 0) return;
     BlendArgs a = a0;
     a.n_grid = n_blocks;
-    // the quadrant blocks: 4 ceil8(n_split) <= 3 kMaxSplit + 28 more than the tiles
-    if (a.n_split_dev && a.tile_list) n_blocks += 3 * kMaxSplit + 28;
+    // the quadrant blocks: 4 ceil8(n_split) <= 3 split_cap + 28 more than the tiles
+    const int cap = a.split_cap < kMaxSplit ? (a.split_cap > 0 ? a.split_cap : 0) : kMaxSplit;
+    if (a.n_split_dev && a.tile_list && cap > 0) n_blocks += 3 * cap + 28;
     else a.n_split_dev = nullptr;
     if (a.with_next_order) n_blocks += 8;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma ||

@@ -92,7 +92,7 @@ struct Workspace {
     // the next such frame blends with (computed by this frame's blend) and
     // the one this frame blends with
     DevBuf full_order;
-    int full_cur = 0, full_TX = 0, full_TY = 0;
+    int full_cur = 0, full_TX = 0, full_TY = 0, full_split_bucket = 0, full_split_max = 0;
     bool full_ready = false;
     // this frame's blend order, its split count and, in frames that render
     // every tile, the order its blend computes for the next one
@@ -587,7 +587,8 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
         const int nt = TX * TY;
         int *cur = ws.full_order.as<int>() + (size_t)ws.full_cur * nt;
         uint32_t *ns_cur = &cnt->n_split_full[ws.full_cur];
-        if (!(ws.full_ready && ws.full_TX == TX && ws.full_TY == TY)) {
+        if (!(ws.full_ready && ws.full_TX == TX && ws.full_TY == TY &&
+              ws.full_split_bucket == sc->split_bucket && ws.full_split_max == sc->split_max)) {
             ProfScope ps(TGS_PROF_RANGES, st);
             OrderK now = order;
             now.tile_out = cur;
@@ -605,6 +606,8 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
         ws.full_ready = true;
         ws.full_TX = TX;
         ws.full_TY = TY;
+        ws.full_split_bucket = sc->split_bucket;
+        ws.full_split_max = sc->split_max;
     } else {
         ProfScope ps(TGS_PROF_RANGES, st);
         launch_order_tiles(order, st);
@@ -620,10 +623,21 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
     return TGS_OK;
 }
 
-// The blend order step_keys chose for this frame (and the next one's, if any).
-void set_blend_order(BlendArgs &a, const Workspace &ws) {
+// The blend order step_keys chose for this frame (and the next one's, if
+// any).  Splitting long tiles into quadrant blocks is scheduling only: it
+// stays off (and the launch takes no spare blocks for it) when the scene
+// disables it or when the longest list of a recent frame of the same kind
+// (selective or not) was below the split bucket.
+void set_blend_order(BlendArgs &a, const Workspace &ws, const tgs_scene *sc, bool selective) {
     a.tile_list = ws.blend_order;
     a.n_split_dev = ws.blend_nsplit;
+    a.split_cap = sc->split_max;
+    if (sc->split_bucket <= 0 || sc->split_max <= 0) {
+        a.n_split_dev = nullptr;
+    } else if (ws.host_maxb) {
+        const uint32_t mb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[selective ? 1 : 0];
+        if (mb != 0xffffffffu && mb < (uint32_t)sc->split_bucket) a.n_split_dev = nullptr;
+    }
     a.with_next_order = ws.has_next_order ? 1 : 0;
     if (ws.has_next_order) a.next_order = ws.next_order;
 }
@@ -902,7 +916,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, cam, vals);
-        set_blend_order(a, ws);
+        set_blend_order(a, ws, sc, false);
         a.rgb = out->rgb;
         a.depth = out->depth;
         a.sigma = out->sigma;
@@ -1078,7 +1092,7 @@ tgs_status tgs_render_full_noalloc(const tgs_scene *sc, const tgs_camera *cam, t
     TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
     if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
     BlendArgs a = blend_args(ws, cam, vals);
-    set_blend_order(a, ws);
+    set_blend_order(a, ws, sc, false);
     a.rgb = out->rgb;
     a.depth = out->depth;
     a.sigma = out->sigma;
@@ -1272,7 +1286,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             TGS_TRY(step_keys(sc, ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx,
                               st, &vals));
             BlendArgs a = blend_args(ws, cam, vals);
-            set_blend_order(a, ws);
+            set_blend_order(a, ws, sc, true);
             a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
             a.rgb = out->rgb;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
@@ -1303,7 +1317,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
             if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
             BlendArgs a = blend_args(ws, cam, vals);
-            set_blend_order(a, ws);
+            set_blend_order(a, ws, sc, false);
             a.rgb = out->rgb;
             a.tab = s->tab.as<float>();
             a.depth = out->depth;

@@ -287,12 +287,13 @@ struct BlendArgs {
     int W, H, TX, TY;
     const int *tile_list;     // NULL: blockIdx = tile
     const uint32_t *n_tiles_dev;  // optional: blocks at or past *n_tiles_dev do nothing
-    // optional (with tile_list): the first *n_split_dev (<= kMaxSplit) tiles
+    // optional (with tile_list): the first *n_split_dev (<= split_cap) tiles
     // of tile_list are blended as four quadrant blocks each; the launch adds
-    // 3 kMaxSplit + 28 blocks (4 ceil8(n_split) quadrant blocks replace
+    // 3 split_cap + 28 blocks (4 ceil8(n_split) quadrant blocks replace
     // n_split tile blocks; n_grid: the launch's tile blocks, set by
     // launch_blend)
     const uint32_t *n_split_dev;
+    int split_cap;            // with n_split_dev: *n_split_dev <= split_cap <= kMaxSplit
     int n_grid;
     const uint2 *ranges;
     const uint32_t *vals;
@@ -330,9 +331,10 @@ struct BlendArgs {
     int with_next_order;
 };
 // Longest lists split into quadrant blocks by the blend: at most kMaxSplit
-// tiles (the launch adds 3 kMaxSplit + 28 blocks, for 4 ceil8(n_split)
-// quadrant blocks; those without a quadrant exit at once), by default those
-// of kSplitBucket (lists of 2^(kSplitBucket-1) entries) and up.
+// tiles (a scene's cap; the launch adds 3 cap + 28 blocks, for 4 ceil8(n_split)
+// quadrant blocks, those without a quadrant exit at once; none when no
+// split is expected), by default those of kSplitBucket (lists of
+// 2^(kSplitBucket-1) entries) and up.
 constexpr int kMaxSplit = TGS_BLEND_SPLIT_MAX;
 constexpr int kSplitBucket = TGS_BLEND_SPLIT_DEFAULT + 1;
 // start/stop (may be NULL) are attached to the dispatch itself
