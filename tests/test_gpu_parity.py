@@ -96,6 +96,26 @@ def test_full_render_order_reuse_across_sizes():
             assert np.array_equal(got[k], ref[k]), (k, c.width, c.height)
 
 
+def test_full_render_order_after_split_change():
+    """A stored blend order (and its split count) is reused only under the
+    split settings it was computed with: alternating split caps on one scene
+    of long lists give the renders of fresh scenes with each cap."""
+    sc = synth.scene_uniform_cube(24_000, 11, degree=0, log_scale_mean=-2.6)
+    cam = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (0, 0, 0)), 48, 40)
+    caps = ((0, 40), (0, 8), (0, 40), (0, 8))
+    with Uploaded(sc) as h:
+        seq = []
+        for split in caps:
+            tgs.tgs_scene_set_blend_split(h, *split)
+            seq.append(gpu_full(h, cam, sc.n))
+    for split, got in zip(caps, seq):
+        with Uploaded(sc) as h:
+            tgs.tgs_scene_set_blend_split(h, *split)
+            ref = gpu_full(h, cam, sc.n)
+        for k in ("rgb", "depth", "sigma", "alpha", "contrib", "tile_mask"):
+            assert np.array_equal(got[k], ref[k]), (k, split)
+
+
 @pytest.mark.parametrize("n,seed,deg,W,H", [(3000, 1, 3, 200, 136), (2000, 4, 0, 300, 17)])
 def test_full_parity_footprint_tiles(n, seed, deg, W, H):
     sc = synth.small_scene(n, seed, degree=deg)
