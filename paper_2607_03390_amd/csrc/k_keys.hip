@@ -144,7 +144,6 @@ __device__ inline void dup_owners(const DupIo &io, uint32_t P0, uint32_t P1, uin
     __syncthreads();
 }
 
-
 // Block b emits output keys [1024 b, 1024 b + 1024), four per thread at
 // consecutive positions across the block (coalesced stores), whatever the
 // Gaussians' key counts: a Gaussian spanning thousands of tiles is spread
