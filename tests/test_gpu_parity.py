@@ -300,6 +300,18 @@ def test_temporal_parity_tiny():
     assert st["tgs"] >= 1
 
 
+def test_parity_background_colour():
+    """A camera background (rgb = sum of w c + T bg): full renders and a
+    temporal sequence, whose stitched pixels carry the reference's
+    background."""
+    w = synth.workload("tiny", n_frames=6)
+    for c in w.cameras:
+        c.bg = (0.25, 0.5, 0.125)
+    _full_parity(w.scene, w.cameras[:2], label="tiny background")
+    st = _temporal_parity(w.scene, w.cameras, 256, 256, "tiny background")
+    assert st["tgs"] >= 1
+
+
 def test_temporal_parity_tiny_empty_far():
     w = synth.workload("tiny")
     st = _temporal_parity(w.scene, w.cameras, 256, 256, "tiny empty_far", empty_far=1)
