@@ -30,7 +30,6 @@
 #include <hip/hip_ext.h>
 
 #include "stitch.h"
-#include "order.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -575,15 +574,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void b
     // of split tile 8 (b >> 5) + (b & 7): the four blocks of a tile, which
     // stage the same records, share one XCD's L2.
     int blk = (int)blockIdx.x;
-    if (a.with_next_order) {
-        // eight leading blocks, so that the roles below keep their XCDs:
-        // block 0 orders the tiles for the next frame of this kind
-        if (blk < 8) {
-            if (blk == 0) order_tiles_block<256>(a.next_order, &s.cnt[0][0]);
-            return;
-        }
-        blk -= 8;
-    }
     if (a.n_split_dev) {
         const int ns = (int)*a.n_split_dev;
         const int nq = 4 * ((ns + 7) & ~7);
@@ -691,7 +681,6 @@ void launch_blend(const BlendArgs &a0, int n_blocks, hipStream_t st, hipEvent_t 
     const int cap = a.split_cap < kMaxSplit ? (a.split_cap > 0 ? a.split_cap : 0) : kMaxSplit;
     if (a.n_split_dev && a.tile_list && cap > 0) n_blocks += 3 * cap + 28;
     else a.n_split_dev = nullptr;
-    if (a.with_next_order) n_blocks += 8;
     const bool capture = a.depth || a.sigma || a.alpha || a.tgb_depth || a.tgb_sigma ||
                          a.tgbh_depth || a.g_flag || a.contrib;
     if (a.contrib)

@@ -88,18 +88,6 @@ struct Workspace {
     DevBuf dkey, didx, dkey_alt, didx_alt, offs;
     DevBuf tkey, tval, tkey_alt, tval_alt, sort, kfirst;
     DevBuf ranges, sel, sel_list, sel_cols, rowpre, cnt, tile_order;
-    // frames that render every tile: two blend orders [2][TX * TY], the one
-    // the next such frame blends with (computed by this frame's blend) and
-    // the one this frame blends with
-    DevBuf full_order;
-    int full_cur = 0, full_TX = 0, full_TY = 0, full_split_bucket = 0, full_split_max = 0;
-    bool full_ready = false;
-    // this frame's blend order, its split count and, in frames that render
-    // every tile, the order its blend computes for the next one
-    const int *blend_order = nullptr;
-    const uint32_t *blend_nsplit = nullptr;
-    OrderK next_order{};
-    bool has_next_order = false;
     HostCounters *host_cnt = nullptr;     // coherent pinned memory, written by the device
     HostCounters *host_cnt_dev = nullptr; // its device-side address
     // pinned: longest tile list's log2 bucket of some recent frame, [0] of
@@ -159,8 +147,6 @@ struct Workspace {
             TGS_TRY(sel.ensure(nt));
             TGS_TRY(sel_list.ensure(nt * sizeof(int)));
             TGS_TRY(tile_order.ensure(nt * sizeof(int)));
-            TGS_TRY(full_order.ensure(2 * nt * sizeof(int)));
-            full_ready = false;
             TGS_TRY(sel_cols.ensure(nt * sizeof(int)));
             TGS_TRY(rowpre.ensure((size_t)TY * (TX + 1) * sizeof(uint32_t)));
             W = W_;
@@ -577,44 +563,10 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
                             alt ? ws.tval.as<uint32_t>() : ws.tval_alt.as<uint32_t>(),
                             ws.dkey.as<uint32_t>(), maxb >= (uint32_t)kSegLongBucket, &order, st);
         TGS_LAUNCHED("per-tile sort and tile order");
-        ws.blend_order = ws.tile_order.as<int>();
-        ws.blend_nsplit = &cnt->n_split;
-        ws.has_next_order = false;
-    } else if (!rowpre) {
-        // every tile rendered: blend in the order the previous such frame's
-        // blend computed (same tile grid), else one computed now; this
-        // frame's blend computes the next one into the other buffer
-        const int nt = TX * TY;
-        int *cur = ws.full_order.as<int>() + (size_t)ws.full_cur * nt;
-        uint32_t *ns_cur = &cnt->n_split_full[ws.full_cur];
-        if (!(ws.full_ready && ws.full_TX == TX && ws.full_TY == TY &&
-              ws.full_split_bucket == sc->split_bucket && ws.full_split_max == sc->split_max)) {
-            ProfScope ps(TGS_PROF_RANGES, st);
-            OrderK now = order;
-            now.tile_out = cur;
-            now.n_split = ns_cur;
-            launch_order_tiles(now, st);
-            TGS_LAUNCHED("tile order");
-        }
-        ws.blend_order = cur;
-        ws.blend_nsplit = ns_cur;
-        ws.next_order = order;
-        ws.next_order.tile_out = ws.full_order.as<int>() + (size_t)(ws.full_cur ^ 1) * nt;
-        ws.next_order.n_split = &cnt->n_split_full[ws.full_cur ^ 1];
-        ws.has_next_order = true;
-        ws.full_cur ^= 1;
-        ws.full_ready = true;
-        ws.full_TX = TX;
-        ws.full_TY = TY;
-        ws.full_split_bucket = sc->split_bucket;
-        ws.full_split_max = sc->split_max;
     } else {
         ProfScope ps(TGS_PROF_RANGES, st);
         launch_order_tiles(order, st);
         TGS_LAUNCHED("tile order");
-        ws.blend_order = ws.tile_order.as<int>();
-        ws.blend_nsplit = &cnt->n_split;
-        ws.has_next_order = false;
     }
     *sorted_vals = alt ? ws.tval_alt.as<uint32_t>() : ws.tval.as<uint32_t>();
     ws.last_keys = skeys;
@@ -623,23 +575,14 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
     return TGS_OK;
 }
 
-// The blend order step_keys chose for this frame (and the next one's, if
-// any).  Splitting long tiles into quadrant blocks is scheduling only: it
-// stays off (and the launch takes no spare blocks for it) when the scene
-// disables it or when the longest list of a recent frame of the same kind
-// (selective or not) was below the split bucket.
-void set_blend_order(BlendArgs &a, const Workspace &ws, const tgs_scene *sc, bool selective) {
-    a.tile_list = ws.blend_order;
-    a.n_split_dev = ws.blend_nsplit;
+// The blend order of the tiles and the split of the longest ones into
+// quadrant blocks (per frame, from the frame's own lists; off when the scene
+// does not split, and then the launch takes no spare blocks for it).
+void set_blend_order(BlendArgs &a, const Workspace &ws, const tgs_scene *sc) {
+    a.tile_list = ws.tile_order.as<int>();
+    a.n_split_dev = &ws.cnt.as<Counters>()->n_split;
     a.split_cap = sc->split_max;
-    if (sc->split_bucket <= 0 || sc->split_max <= 0) {
-        a.n_split_dev = nullptr;
-    } else if (ws.host_maxb) {
-        const uint32_t mb = reinterpret_cast<volatile uint32_t *>(ws.host_maxb)[selective ? 1 : 0];
-        if (mb != 0xffffffffu && mb < (uint32_t)sc->split_bucket) a.n_split_dev = nullptr;
-    }
-    a.with_next_order = ws.has_next_order ? 1 : 0;
-    if (ws.has_next_order) a.next_order = ws.next_order;
+    if (sc->split_bucket <= 0 || sc->split_max <= 0) a.n_split_dev = nullptr;
 }
 
 BlendArgs blend_args(const Workspace &ws, const tgs_camera *cam, const uint32_t *vals) {
@@ -916,7 +859,7 @@ tgs_status tgs_render_full(tgs_scene *sc, const tgs_camera *cam, tgs_frame_out *
         TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
         if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
         BlendArgs a = blend_args(ws, cam, vals);
-        set_blend_order(a, ws, sc, false);
+        set_blend_order(a, ws, sc);
         a.rgb = out->rgb;
         a.depth = out->depth;
         a.sigma = out->sigma;
@@ -1020,7 +963,6 @@ bool layout_full(Workspace &ws, char *base, size_t cap, int n, int W, int H, siz
               c.take(ws.didx_alt, nn * 4) && c.take(ws.offs, nn * 4) &&
               c.take(ws.ranges, nt * sizeof(uint2)) && c.take(ws.sel, nt) &&
               c.take(ws.sel_list, nt * sizeof(int)) && c.take(ws.tile_order, nt * sizeof(int)) &&
-              c.take(ws.full_order, 2 * nt * sizeof(int)) &&
               c.take(ws.sel_cols, nt * sizeof(int)) &&
               c.take(ws.rowpre, (size_t)TY * (TX + 1) * sizeof(uint32_t)) &&
               c.take(ws.cnt, sizeof(Counters)) && c.take(ws.sort, sort_words * sizeof(uint32_t)) &&
@@ -1092,7 +1034,7 @@ tgs_status tgs_render_full_noalloc(const tgs_scene *sc, const tgs_camera *cam, t
     TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
     if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
     BlendArgs a = blend_args(ws, cam, vals);
-    set_blend_order(a, ws, sc, false);
+    set_blend_order(a, ws, sc);
     a.rgb = out->rgb;
     a.depth = out->depth;
     a.sigma = out->sigma;
@@ -1286,7 +1228,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             TGS_TRY(step_keys(sc, ws, TX, TY, ws.rowpre.as<uint32_t>(), ws.sel_cols.as<int>(), didx,
                               st, &vals));
             BlendArgs a = blend_args(ws, cam, vals);
-            set_blend_order(a, ws, sc, true);
+            set_blend_order(a, ws, sc);
             a.n_tiles_dev = &ws.cnt.as<Counters>()->n_selected;
             a.rgb = out->rgb;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_TGS);
@@ -1317,7 +1259,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             TGS_TRY(step_keys(sc, ws, TX, TY, nullptr, nullptr, didx, st, &vals));
             if (out->contrib) launch_fill_f32(out->contrib, (size_t)sc->n, 0.0f, st);
             BlendArgs a = blend_args(ws, cam, vals);
-            set_blend_order(a, ws, sc, false);
+            set_blend_order(a, ws, sc);
             a.rgb = out->rgb;
             a.tab = s->tab.as<float>();
             a.depth = out->depth;

@@ -83,8 +83,7 @@ struct Counters {
     uint32_t n_visible;       // Gaussians with at least one key
     uint32_t n_sorted;        // keys emitted and sorted: n_keys, or 0 past the key capacity
     uint32_t n_split;         // tiles the blend splits into quadrants (the blend order's first)
-    uint32_t n_split_full[2]; // the same for the two orders of frames that render every tile
-    uint32_t pad[3];
+    uint32_t pad;
 };
 
 // The frame's counters as the host reads them: written by the last counting
@@ -323,17 +322,11 @@ struct BlendArgs {
     const float2 *stitch_uv;
     const float *stitch_dfill;
     WarpK sw;
-    // optional (with_next_order): block 0 of eight extra leading blocks
-    // computes the blend order of the next frame of the same kind from this
-    // frame's ranges (the order only schedules tiles, so a frame may take
-    // the previous one's)
-    OrderK next_order;
-    int with_next_order;
 };
 // Longest lists split into quadrant blocks by the blend: at most kMaxSplit
 // tiles (a scene's cap; the launch adds 3 cap + 28 blocks, for 4 ceil8(n_split)
-// quadrant blocks, those without a quadrant exit at once; none when no
-// split is expected), by default those of kSplitBucket (lists of
+// quadrant blocks, those without a quadrant exit at once; none when the
+// scene does not split), by default those of kSplitBucket (lists of
 // 2^(kSplitBucket-1) entries) and up.
 constexpr int kMaxSplit = TGS_BLEND_SPLIT_MAX;
 constexpr int kSplitBucket = TGS_BLEND_SPLIT_DEFAULT + 1;
