@@ -303,11 +303,14 @@ __device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s
 }
 
 // KT: the type the keys are staged in (uint16_t: every key below 2^16).
+// nbits: the digit bits a kept key can have set (1..8; the higher digit bits
+// are zero for every kept key, so the match skips them).
 template <int IPT, int MODE, typename KT>
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
-    uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, uint32_t np,
-    const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ chunk_sums, DepthIo io) {
+    uint32_t *__restrict__ vout, const uint32_t *n_dev, uint32_t n_host, int shift, int nbits,
+    uint32_t np, const uint32_t *__restrict__ offsets, const uint32_t *__restrict__ chunk_sums,
+    DepthIo io) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ KT s_keys[kTile];
     __shared__ uint32_t s_vals[kTile];
@@ -392,9 +395,11 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t m = __ballot(bit);
-            peers &= bit ? m : ~m;
+            if (b < nbits) {   // uniform
+                const bool bit = (d >> b) & 1u;
+                const uint64_t m = __ballot(bit);
+                peers &= bit ? m : ~m;
+            }
         }
         const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
         uint32_t before = 0;
@@ -488,7 +493,7 @@ inline uint32_t n_partitions(uint32_t K, int ipt) {
 }
 
 template <int IPT, int MODE, typename KT = uint32_t>
-void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *ki,
+void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, int nbits, const uint32_t *ki,
               const uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, const DepthIo &io,
               hipStream_t st) {
     // at least one block: the last depth pass always publishes the counters
@@ -502,25 +507,29 @@ void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, const uint32_t *
     sort_colscan_kernel<<<tables * 16 * kChunks, 256, 0, st>>>(nd, n_max, kSortThreads * IPT, np,
                                                                 table, chunk_sums);
     sort_downsweep_kernel<IPT, MODE, KT><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
-                                                                  np, table, chunk_sums, io);
+                                                                  nbits, np, table, chunk_sums, io);
 }
 
 template <int IPT>
 void depth_passes(uint32_t n, const uint32_t *dkey, uint32_t *k_a, uint32_t *v_a, uint32_t *k_b,
                   uint32_t *v_b, uint32_t *scratch, const DepthIo &io, hipStream_t st) {
     const uint32_t *n_vis = &io.cnt->n_visible;
-    one_pass<IPT, kFirst>(nullptr, n, 0, dkey, nullptr, k_a, v_a, scratch, io, st);
-    one_pass<IPT, kPlain>(n_vis, n, 8, k_a, v_a, k_b, v_b, scratch, io, st);
-    one_pass<IPT, kPlain>(n_vis, n, 16, k_b, v_b, k_a, v_a, scratch, io, st);
-    one_pass<IPT, kLast>(n_vis, n, 24, k_a, v_a, nullptr, v_b, scratch, io, st);
+    one_pass<IPT, kFirst>(nullptr, n, 0, 8, dkey, nullptr, k_a, v_a, scratch, io, st);
+    one_pass<IPT, kPlain>(n_vis, n, 8, 8, k_a, v_a, k_b, v_b, scratch, io, st);
+    one_pass<IPT, kPlain>(n_vis, n, 16, 8, k_b, v_b, k_a, v_a, scratch, io, st);
+    // kept depths are positive (above the near plane): the sign bit is zero
+    one_pass<IPT, kLast>(n_vis, n, 24, 7, k_a, v_a, nullptr, v_b, scratch, io, st);
 }
 
 template <int IPT, typename KT = uint32_t>
-void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int passes, uint32_t *ki,
+void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int bits, uint32_t *ki,
                   uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, hipStream_t st) {
     const DepthIo none{};
+    const int passes = sort_passes_for_bits(bits);
     for (int p = 0; p < passes; ++p) {
-        one_pass<IPT, kPlain, KT>(n_dev, n_max, begin_bit + 8 * p, ki, vi, ko, vo, scratch, none, st);
+        const int nb = bits - 8 * p < 8 ? bits - 8 * p : 8;
+        one_pass<IPT, kPlain, KT>(n_dev, n_max, begin_bit + 8 * p, nb, ki, vi, ko, vo, scratch, none,
+                                  st);
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }
@@ -539,18 +548,19 @@ size_t sort_scratch_words(uint32_t max_keys) {
 }
 
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int begin_bit,
-                    int passes, uint32_t *keys, uint32_t *vals, uint32_t *keys_alt,
+                    int bits, uint32_t *keys, uint32_t *vals, uint32_t *keys_alt,
                     uint32_t *vals_alt, uint32_t *scratch, hipStream_t st) {
+    const int passes = sort_passes_for_bits(bits);
     if (n_max <= 1 || passes <= 0) return 0;
     // partition size from the expected count (the grid covers n_max either way)
     if (ipt_for(n_hint < n_max ? n_hint : n_max) == kIptSmall)
-        plain_passes<kIptSmall>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
+        plain_passes<kIptSmall>(n_dev, n_max, begin_bit, bits, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
     else if (begin_bit + 8 * passes <= 16)
-        plain_passes<kIptLarge16, uint16_t>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt,
+        plain_passes<kIptLarge16, uint16_t>(n_dev, n_max, begin_bit, bits, keys, vals, keys_alt,
                                             vals_alt, scratch, st);
     else
-        plain_passes<kIptLarge>(n_dev, n_max, begin_bit, passes, keys, vals, keys_alt, vals_alt,
+        plain_passes<kIptLarge>(n_dev, n_max, begin_bit, bits, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
     return passes & 1;
 }

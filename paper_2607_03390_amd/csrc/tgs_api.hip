@@ -501,11 +501,14 @@ tgs_status grow_after_overflow(Workspace &ws, const FrameResult &fr, int passes,
     return ws.ensure_keys(want, passes);
 }
 
-int tile_sort_passes(int TX, int TY) {
+// Key bits of a tile id on a TX x TY grid.
+int tile_id_bits(int TX, int TY) {
     int bits = 0;
     while ((1 << bits) < TX * TY) ++bits;
-    return sort_passes_for_bits(bits);
+    return bits;
 }
+
+int tile_sort_passes(int TX, int TY) { return sort_passes_for_bits(tile_id_bits(TX, TY)); }
 
 // Emit the keys in depth order, sort them by tile (stable), find tile ranges;
 // returns the per-tile lists of Gaussian indices.
@@ -513,7 +516,6 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
                      const int *sel_cols, const uint32_t *didx, hipStream_t st,
                      const uint32_t **sorted_vals) {
     const int n = sc->n;
-    const int passes = tile_sort_passes(TX, TY);
     const uint32_t cap = (uint32_t)ws.key_cap;
     Counters *cnt = ws.cnt.as<Counters>();
     {
@@ -526,7 +528,8 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
     int alt = 0;
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        alt = launch_sort_u32(&cnt->n_sorted, cap, ws.recent_K[rowpre ? 1 : 0], 0, passes,
+        alt = launch_sort_u32(&cnt->n_sorted, cap, ws.recent_K[rowpre ? 1 : 0], 0,
+                              tile_id_bits(TX, TY),
                               ws.tkey.as<uint32_t>(),
                               ws.tval.as<uint32_t>(), ws.tkey_alt.as<uint32_t>(),
                               ws.tval_alt.as<uint32_t>(), ws.sort.as<uint32_t>(), st);
@@ -1279,7 +1282,7 @@ tgs_status tgs_render_temporal(tgs_state *s, const tgs_camera *cam, tgs_frame_ou
             a.mark_sel = ws.sel.as<uint8_t>();
             a.mark_mask = out->tile_mask;
             a.pairs = g_prof.pairs(TGS_PROF_BLEND_REF);
-        a.hits = g_prof.hits(TGS_PROF_BLEND_REF);
+            a.hits = g_prof.hits(TGS_PROF_BLEND_REF);
             {
                 hipEvent_t ev0, ev1;
                 g_prof.kernel_events(TGS_PROF_BLEND_REF, &ev0, &ev1);
