@@ -117,7 +117,8 @@ __device__ inline uint32_t carried_index(const DepthIo &io, uint32_t v) {
 template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint32_t *n_dev,
-    uint32_t n_host, int shift, uint32_t np, DepthIo io, uint32_t *counts, uint32_t *weights) {
+    uint32_t n_host, int shift, int nbits, uint32_t np, DepthIo io, uint32_t *counts,
+    uint32_t *weights) {
     constexpr uint32_t kTile = kSortThreads * IPT;
     __shared__ uint32_t s_h[4][kRadix];
     __shared__ uint32_t s_w[MODE == kLast ? 4 : 1][kRadix];
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
         keep[j] = idx < K;
         const uint32_t ic = keep[j] ? idx : K - 1u;
-        dg[j] = (kin[ic] >> shift) & 255u;
+        dg[j] = (kin[ic] >> shift) & ((1u << nbits) - 1u);
         if (MODE == kFirst) {
             uint32_t c;
             if (io.rowpre) {
@@ -303,8 +304,8 @@ __device__ void publish_counters(const DepthIo &io, uint64_t n_keys, uint32_t *s
 }
 
 // KT: the type the keys are staged in (uint16_t: every key below 2^16).
-// nbits: the digit bits a kept key can have set (1..8; the higher digit bits
-// are zero for every kept key, so the match skips them).
+// nbits: the pass's digit width (1..8): the digit is key bits [shift,
+// shift + nbits).
 template <int IPT, int MODE, typename KT>
 __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
@@ -357,6 +358,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     // issue every global load of the block before the first barrier
     const uint32_t wbase = base + (uint32_t)wave * (64u * IPT);
     const uint64_t lt_mask = (1ull << lane) - 1ull;
+    const uint32_t dmask = (1u << nbits) - 1u;
     // 16-bit keys: each item's rank is kept in the upper half of its key
     constexpr bool kPack = sizeof(KT) == 2;
     uint32_t key[IPT], val[IPT], rank[kPack ? 1 : IPT], wt[MODE == kLast ? IPT : 1];
@@ -391,7 +393,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const bool valid = ok[j];
-        const uint32_t d = (key[j] >> shift) & 255u;
+        const uint32_t d = (key[j] >> shift) & dmask;
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
                 kj = key[j];
                 rk = rank[j];
             }
-            const uint32_t dj = (kj >> shift) & 255u;
+            const uint32_t dj = (kj >> shift) & dmask;
             const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rk;
             s_keys[pos] = (KT)kj;
             s_vals[pos] = val[j];
@@ -470,7 +472,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
 
     for (uint32_t i = tid; i < nv; i += kSortThreads) {
         const uint32_t kk = (uint32_t)s_keys[i];
-        const uint32_t dj = (kk >> shift) & 255u;
+        const uint32_t dj = (kk >> shift) & dmask;
         const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
         if (MODE == kLast) {
             const uint32_t o = s_wbase[dj] + (s_wt[i] - s_wt[s_dstart[dj]]);
@@ -503,7 +505,7 @@ void one_pass(const uint32_t *n_dev, uint32_t n_max, int shift, int nbits, const
     const uint32_t *nd = MODE == kFirst ? nullptr : n_dev;
     const int tables = MODE == kLast ? 2 : 1;
     sort_upsweep_kernel<IPT, MODE><<<np, kSortThreads, 0, st>>>(
-        ki, vi, nd, n_max, shift, np, io, table, table + (size_t)np * kRadix);
+        ki, vi, nd, n_max, shift, nbits, np, io, table, table + (size_t)np * kRadix);
     sort_colscan_kernel<<<tables * 16 * kChunks, 256, 0, st>>>(nd, n_max, kSortThreads * IPT, np,
                                                                 table, chunk_sums);
     sort_downsweep_kernel<IPT, MODE, KT><<<np, kSortThreads, 0, st>>>(ki, vi, ko, vo, nd, n_max, shift,
@@ -525,11 +527,14 @@ template <int IPT, typename KT = uint32_t>
 void plain_passes(const uint32_t *n_dev, uint32_t n_max, int begin_bit, int bits, uint32_t *ki,
                   uint32_t *vi, uint32_t *ko, uint32_t *vo, uint32_t *scratch, hipStream_t st) {
     const DepthIo none{};
+    // digits of (nearly) equal width: fewer runs per partition in the widest
+    // pass, so its scattered writes come in longer pieces
     const int passes = sort_passes_for_bits(bits);
+    int shift = begin_bit;
     for (int p = 0; p < passes; ++p) {
-        const int nb = bits - 8 * p < 8 ? bits - 8 * p : 8;
-        one_pass<IPT, kPlain, KT>(n_dev, n_max, begin_bit + 8 * p, nb, ki, vi, ko, vo, scratch, none,
-                                  st);
+        const int nb = bits / passes + (p < bits % passes ? 1 : 0);
+        one_pass<IPT, kPlain, KT>(n_dev, n_max, shift, nb, ki, vi, ko, vo, scratch, none, st);
+        shift += nb;
         uint32_t *t = ki; ki = ko; ko = t;
         t = vi; vi = vo; vo = t;
     }
@@ -556,7 +561,7 @@ int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int 
     if (ipt_for(n_hint < n_max ? n_hint : n_max) == kIptSmall)
         plain_passes<kIptSmall>(n_dev, n_max, begin_bit, bits, keys, vals, keys_alt, vals_alt,
                                 scratch, st);
-    else if (begin_bit + 8 * passes <= 16)
+    else if (begin_bit + bits <= 16)
         plain_passes<kIptLarge16, uint16_t>(n_dev, n_max, begin_bit, bits, keys, vals, keys_alt,
                                             vals_alt, scratch, st);
     else
