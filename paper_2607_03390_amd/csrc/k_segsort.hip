@@ -19,6 +19,7 @@
 // The per-tile lists are identical to those of the depth-ordered path.  One
 // more block of the short-list launch computes the blend order of the tiles
 // (order.h).
+#include "match.h"
 #include "order.h"
 #include "tgs_internal.h"
 
@@ -259,13 +260,10 @@ __device__ void segment_lsd(uint32_t *vals, uint32_t *tmp, uint32_t L, const uin
             const bool ok = i < L;
             const uint32_t v = ok ? src[i] : 0u;
             const uint32_t d = ok ? (dkey[v] >> shift) & 255u : 0u;
-            uint64_t peers = __ballot(ok);
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const bool bit = (d >> b) & 1u;
-                const uint64_t m = __ballot(bit);
-                peers &= bit ? m : ~m;
-            }
+            const uint32_t dg[1] = {d};
+            uint64_t pm[1] = {__ballot(ok)};
+            match_digits<1>(dg, 8, pm);
+            const uint64_t peers = pm[0];
             for (int k = tid; k < kWaves * 256; k += kSegThreads) s_wcnt[k] = 0u;
             __syncthreads();
             if (ok && (peers & lt) == 0) s_wcnt[wave * 256 + d] = (uint32_t)__popcll(peers);
@@ -318,24 +316,33 @@ __device__ void seg_sort_lds(uint32_t *vals, uint32_t L, const uint32_t *dkey, u
         for (int k = tid; k < kWaves * 256; k += NT) s_wh[k] = 0u;
         __syncthreads();
         uint32_t rank[IPT];
+        // depths are positive: the top digit has 7 bits
+        const int nbits = pass == 3 ? 7 : 8;
+        constexpr int kG = IPT < 4 ? IPT : 4;
 #pragma unroll
-        for (int j = 0; j < IPT; ++j) {
-            const bool valid = ok[j];
-            const uint32_t d = (key[j] >> shift) & 255u;
-            uint64_t peers = __ballot(valid);
+        for (int j0 = 0; j0 < IPT; j0 += kG) {
+            uint32_t dg[kG];
+            uint64_t pm[kG];
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const bool bit = (d >> b) & 1u;
-                const uint64_t m = __ballot(bit);
-                peers &= bit ? m : ~m;
+            for (int g = 0; g < kG; ++g) {
+                dg[g] = (key[j0 + g] >> shift) & 255u;
+                pm[g] = __ballot(ok[j0 + g]);
             }
-            const uint32_t below = (uint32_t)__popcll(peers & lt);
-            uint32_t before = 0;
-            if (valid) before = s_wh[wave * 256 + d];
-            __builtin_amdgcn_wave_barrier();
-            if (valid && below == 0) s_wh[wave * 256 + d] = before + (uint32_t)__popcll(peers);
-            __builtin_amdgcn_wave_barrier();
-            rank[j] = before + below;
+            match_digits<kG>(dg, nbits, pm);
+#pragma unroll
+            for (int g = 0; g < kG; ++g) {
+                const int j = j0 + g;
+                const bool valid = ok[j];
+                const uint32_t d = dg[g];
+                const uint64_t peers = pm[g];
+                const uint32_t below = (uint32_t)__popcll(peers & lt);
+                uint32_t before = 0;
+                if (valid) before = s_wh[wave * 256 + d];
+                __builtin_amdgcn_wave_barrier();
+                if (valid && below == 0) s_wh[wave * 256 + d] = before + (uint32_t)__popcll(peers);
+                __builtin_amdgcn_wave_barrier();
+                rank[j] = before + below;
+            }
         }
         __syncthreads();
         {

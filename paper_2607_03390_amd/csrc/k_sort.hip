@@ -33,6 +33,7 @@
 //    writes, at each sorted position, the exclusive prefix of the weights:
 //    where the Gaussian's tile keys start, and the owner of every 1024-key
 //    block of the emission.  It publishes the frame's counters to the host.
+#include "match.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -367,13 +368,16 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     for (int j = 0; j < IPT; ++j) {
         const uint32_t idx = wbase + (uint32_t)(j * 64 + lane);
         ok[j] = idx < K;
-        key[j] = ok[j] ? kin[idx] : 0xffffffffu;
+        // clamped index: every load is issued, none behind a branch (the
+        // values of lanes past the end are never used)
+        const uint32_t ic = ok[j] ? idx : K - 1u;
+        key[j] = kin[ic];
         if (MODE == kFirst) {
-            const uint32_t c = ok[j] ? io.count[idx] : 0u;
+            const uint32_t c = io.count[ic];
             val[j] = io.pack ? idx << 8 | (c < 255u ? c : 255u) : idx;
             ok[j] = ok[j] && c > 0u;
         } else {
-            val[j] = ok[j] ? vin[idx] : 0u;
+            val[j] = vin[ic];
         }
     }
     const uint32_t off_mine = offsets[(size_t)part * kRadix + tid];
@@ -390,27 +394,35 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         s_wbase[tid] = sat32(wb + wpre + woff_mine);
     }
     __syncthreads();
+    // Rank: the lanes holding the same digit (matched over a group of items
+    // at once), then the per-wave digit counters in input order.
+    constexpr int kG = IPT % 5 == 0 ? 5 : 4;
+    static_assert(IPT % kG == 0, "items per thread must be a multiple of the group");
 #pragma unroll
-    for (int j = 0; j < IPT; ++j) {
-        const bool valid = ok[j];
-        const uint32_t d = (key[j] >> shift) & dmask;
-        uint64_t peers = __ballot(valid);
+    for (int j0 = 0; j0 < IPT; j0 += kG) {
+        uint32_t dg[kG];
+        uint64_t pm[kG];
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            if (b < nbits) {   // uniform
-                const bool bit = (d >> b) & 1u;
-                const uint64_t m = __ballot(bit);
-                peers &= bit ? m : ~m;
-            }
+        for (int g = 0; g < kG; ++g) {
+            dg[g] = (key[j0 + g] >> shift) & dmask;
+            pm[g] = __ballot(ok[j0 + g]);
         }
-        const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
-        uint32_t before = 0;
-        if (valid) before = s_wh[wave * kRadix + d];
-        __builtin_amdgcn_wave_barrier();
-        if (valid && below == 0) s_wh[wave * kRadix + d] = before + (uint32_t)__popcll(peers);
-        __builtin_amdgcn_wave_barrier();
-        if constexpr (kPack) key[j] = (key[j] & 0xffffu) | ((before + below) << 16);
-        else rank[j] = before + below;
+        match_digits<kG>(dg, nbits, pm);
+#pragma unroll
+        for (int g = 0; g < kG; ++g) {
+            const int j = j0 + g;
+            const bool valid = ok[j];
+            const uint32_t d = dg[g];
+            const uint64_t peers = pm[g];
+            const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
+            uint32_t before = 0;
+            if (valid) before = s_wh[wave * kRadix + d];
+            __builtin_amdgcn_wave_barrier();
+            if (valid && below == 0) s_wh[wave * kRadix + d] = before + (uint32_t)__popcll(peers);
+            __builtin_amdgcn_wave_barrier();
+            if constexpr (kPack) key[j] = (key[j] & 0xffffu) | ((before + below) << 16);
+            else rank[j] = before + below;
+        }
     }
     __syncthreads();
 

@@ -2,6 +2,7 @@
 // or, in frames with a per-tile sort, by the first block of that launch.
 #pragma once
 
+#include "match.h"
 #include "tgs_internal.h"
 
 namespace tgs {
@@ -19,24 +20,31 @@ __device__ inline uint32_t length_bucket(const uint2 *ranges, int t) {
     return len ? 32u - (uint32_t)__clz(len) : 0u;
 }
 
-// Wave-aggregated LDS atomic without a loop: lanes with equal buckets are
-// matched over the six bucket bits; the lowest lane of each group adds the
-// group's size (one LDS atomic instruction for all groups) and the others
-// take consecutive slots after its old value.
-__device__ inline uint32_t wave_bucket_add(uint32_t *s_cnt, uint32_t b, bool active) {
+// Wave-aggregated LDS atomics without a loop, for N items per lane: lanes
+// with equal buckets are matched over the six bucket bits; the lowest lane
+// of each group adds the group's size (one LDS atomic instruction per item
+// for all groups) and the others take consecutive slots after its old
+// value.  Items are counted in order (item k before item k + 1), and every
+// match and atomic of the N items is issued before the first result is used.
+template <int N>
+__device__ inline void wave_bucket_add(uint32_t *s_cnt, const uint32_t (&b)[N], const bool (&active)[N],
+                                       uint32_t (&slot)[N]) {
     const int lane = threadIdx.x & 63;
-    uint64_t peers = __ballot(active);
+    uint64_t pm[N];
 #pragma unroll
-    for (int bit = 0; bit < 6; ++bit) {
-        const bool x = (b >> bit) & 1u;
-        const uint64_t m = __ballot(x);
-        peers &= x ? m : ~m;
+    for (int k = 0; k < N; ++k) pm[k] = __ballot(active[k]);
+    match_digits<N>(b, 6, pm);
+    int leader[N];
+    uint32_t base[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        leader[k] = pm[k] ? __ffsll((long long)pm[k]) - 1 : lane;
+        base[k] = 0u;
+        if (active[k] && lane == leader[k]) base[k] = atomicAdd(&s_cnt[b[k]], (uint32_t)__popcll(pm[k]));
     }
-    const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
-    uint32_t base = 0;
-    if (active && lane == leader) base = atomicAdd(&s_cnt[b], (uint32_t)__popcll(peers));
-    base = __shfl(base, leader);
-    return base + (uint32_t)__popcll(peers & ((1ull << lane) - 1ull));
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+        slot[k] = __shfl(base[k], leader[k]) + (uint32_t)__popcll(pm[k] & ((1ull << lane) - 1ull));
 }
 
 // One block of NT threads orders the tiles (s_cnt: 33 words of LDS).
@@ -72,16 +80,14 @@ __device__ void order_tiles_block(const OrderK &o, uint32_t *s_cnt) {
 #pragma unroll
                 for (int k = 0; k < kPer; ++k) bk[k] = act[k] ? length_bucket(ranges, t[k]) : 0u;
             }
+            // one LDS atomic per bucket present in the wave and item (lists
+            // fall into a dozen buckets: per-lane atomics contend)
+            uint32_t slot[kPer];
+            wave_bucket_add<kPer>(s_cnt, bk, act, slot);
+            if (pass == 1) {
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                if (pass == 0) {
-                    // one LDS atomic per bucket present in the wave (lists
-                    // fall into a dozen buckets: per-lane atomics contend)
-                    (void)wave_bucket_add(s_cnt, bk[k], act[k]);
-                } else {
-                    const uint32_t slot = wave_bucket_add(s_cnt, bk[k], act[k]);
-                    if (act[k]) tile_out[slot] = t[k];
-                }
+                for (int k = 0; k < kPer; ++k)
+                    if (act[k]) tile_out[slot[k]] = t[k];
             }
         }
         __syncthreads();
