@@ -319,7 +319,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     __shared__ uint32_t s_wt[MODE == kLast ? kTile : 1];   // weights, then their exclusive scan
     __shared__ uint32_t s_wh[4 * kRadix];     // per-wave digit counters, then wave prefixes
     __shared__ uint32_t s_dstart[kRadix];     // block-local start of each digit
-    __shared__ uint32_t s_gbase[kRadix];      // global start of this block's digit run
+    __shared__ uint32_t s_gbase[kRadix];      // global start of this block's digit run,
+                                              // then that minus the block-local start
     __shared__ uint32_t s_wbase[MODE == kLast ? kRadix : 1];   // global weight prefix of the run
     __shared__ uint32_t s_scan[4];
     __shared__ uint64_t s_scan64[4];
@@ -430,29 +431,35 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
     const uint32_t c0 = s_wh[d], c1 = s_wh[kRadix + d], c2 = s_wh[2 * kRadix + d],
                    c3 = s_wh[3 * kRadix + d];
     const uint32_t total = c0 + c1 + c2 + c3;
-    __syncthreads();
-    s_wh[d] = 0u;
-    s_wh[kRadix + d] = c0;
-    s_wh[2 * kRadix + d] = c0 + c1;
-    s_wh[3 * kRadix + d] = c0 + c1 + c2;
     uint32_t n_valid;
-    s_dstart[d] = block_exclusive_scan256<uint32_t>(total, s_scan, &n_valid);
+    // the scan's barriers also order the counter reads above before the
+    // writes below
+    const uint32_t dstart = block_exclusive_scan256<uint32_t>(total, s_scan, &n_valid);
+    // per wave: where its items of digit d start in the block's staging
+    s_wh[d] = dstart;
+    s_wh[kRadix + d] = dstart + c0;
+    s_wh[2 * kRadix + d] = dstart + c0 + c1;
+    s_wh[3 * kRadix + d] = dstart + c0 + c1 + c2;
+    s_dstart[d] = dstart;
+    s_gbase[d] -= dstart;
     if (tid == 0) s_nvalid = n_valid;
     __syncthreads();
 
+    // staging reads first (a digit of any item is in range), then the writes
+    // of the kept items
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
+        uint32_t kj, rk;
+        if constexpr (kPack) {
+            kj = key[j] & 0xffffu;
+            rk = key[j] >> 16;
+        } else {
+            kj = key[j];
+            rk = rank[j];
+        }
+        const uint32_t dj = (kj >> shift) & dmask;
+        const uint32_t pos = s_wh[wave * kRadix + dj] + rk;
         if (ok[j]) {
-            uint32_t kj, rk;
-            if constexpr (kPack) {
-                kj = key[j] & 0xffffu;
-                rk = key[j] >> 16;
-            } else {
-                kj = key[j];
-                rk = rank[j];
-            }
-            const uint32_t dj = (kj >> shift) & dmask;
-            const uint32_t pos = s_dstart[dj] + s_wh[wave * kRadix + dj] + rk;
             s_keys[pos] = (KT)kj;
             s_vals[pos] = val[j];
             if (MODE == kLast) s_wt[pos] = wt[j];
@@ -482,10 +489,33 @@ __global__ __launch_bounds__(kSortThreads) void sort_downsweep_kernel(
         __syncthreads();
     }
 
+    if (MODE != kLast) {
+        // every staged slot is read (in bounds; slots past nv are unused),
+        // then the kept items are stored: all LDS reads of the thread in
+        // flight at once
+        uint32_t sk[IPT], sv[IPT], od[IPT];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            const uint32_t i = (uint32_t)(j * kSortThreads + tid);
+            sk[j] = (uint32_t)s_keys[i];
+            sv[j] = s_vals[i];
+        }
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) od[j] = s_gbase[(sk[j] >> shift) & dmask];
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+            const uint32_t i = (uint32_t)(j * kSortThreads + tid);
+            if (i < nv) {
+                kout[od[j] + i] = sk[j];
+                vout[od[j] + i] = sv[j];
+            }
+        }
+        return;
+    }
     for (uint32_t i = tid; i < nv; i += kSortThreads) {
         const uint32_t kk = (uint32_t)s_keys[i];
         const uint32_t dj = (kk >> shift) & dmask;
-        const uint32_t out = s_gbase[dj] + (i - s_dstart[dj]);
+        const uint32_t out = s_gbase[dj] + i;
         if (MODE == kLast) {
             const uint32_t o = s_wbase[dj] + (s_wt[i] - s_wt[s_dstart[dj]]);
             io.offs[out] = o;
