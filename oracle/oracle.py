@@ -468,7 +468,8 @@ class TemporalOracle:
             self.since_true += 1
             self.since_ref += 1
             if self.p.enable_sr:
-                # adaptive reference insertion: "exceeds" eta of all tiles.
+                # adaptive reference insertion: strictly more selected tiles
+                # than eta times all tiles.
                 # eta is a float32 parameter of the interface, so the product
                 # is taken with that float32 value, widened exactly
                 eta = float(np.float32(self.p.eta))
