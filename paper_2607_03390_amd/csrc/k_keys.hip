@@ -233,8 +233,8 @@ __global__ __launch_bounds__(256) void ranges_kernel(const Counters *cnt, const 
 }
 
 __global__ __launch_bounds__(1024) void order_tiles_kernel(OrderK o) {
-    __shared__ uint32_t s_cnt[33];
-    order_tiles_block<1024>(o, s_cnt);
+    __shared__ uint32_t s_cnt[order_lds_words(1024)];
+    order_tiles_block<1024, true>(o, s_cnt);
 }
 
 }  // namespace

@@ -405,11 +405,11 @@ __global__ __launch_bounds__(kShortThreads) void segment_sort_short_kernel(const
     __shared__ uint32_t s_wh[(kShortThreads / 64) * 256];
     __shared__ uint32_t s_dstart[256];
     __shared__ uint32_t s_scan[kShortThreads / 64];
-    __shared__ uint32_t s_ocnt[33];
+    __shared__ uint32_t s_ocnt[order_lds_words(kShortThreads)];
     int tile = (int)blockIdx.x;
     if (with_order) {
         if (tile == 0) {   // block-uniform
-            order_tiles_block<kShortThreads>(order, s_ocnt);
+            order_tiles_block<kShortThreads, false>(order, s_ocnt);
             return;
         }
         tile -= 1;

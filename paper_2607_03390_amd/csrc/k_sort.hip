@@ -114,24 +114,29 @@ __device__ inline uint32_t carried_index(const DepthIo &io, uint32_t v) {
 
 // Digit counts of one partition: counts[part * 256 + d] (one coalesced 1 KB
 // row per block); in the last depth pass also the digit weight sums:
-// weights[part * 256 + d].
+// weights[part * 256 + d].  The LDS counters are per wave and, in the last
+// depth pass, per lane & 3 as well: its digits (the top bits of depths)
+// take a handful of values, and lanes adding to one address serialise.
 template <int IPT, int MODE>
 __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
     const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint32_t *n_dev,
     uint32_t n_host, int shift, int nbits, uint32_t np, DepthIo io, uint32_t *counts,
     uint32_t *weights) {
     constexpr uint32_t kTile = kSortThreads * IPT;
-    __shared__ uint32_t s_h[4][kRadix];
-    __shared__ uint32_t s_w[MODE == kLast ? 4 : 1][kRadix];
+    constexpr int kCopies = MODE == kLast ? 4 : 1;
+    constexpr int kRows = 4 * kCopies;
+    __shared__ uint32_t s_h[kRows][kRadix];
+    __shared__ uint32_t s_w[MODE == kLast ? kRows : 1][kRadix];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t K = MODE == kFirst ? n_host : key_count(n_dev, n_host);
     const uint32_t part = blockIdx.x;
     if (part * kTile >= K) return;   // block-uniform: beyond the keys
-    for (int k = tid; k < 4 * kRadix; k += kSortThreads) {
+    for (int k = tid; k < kRows * kRadix; k += kSortThreads) {
         (&s_h[0][0])[k] = 0u;
         if (MODE == kLast) (&s_w[0][0])[k] = 0u;
     }
     __syncthreads();
+    const int row = wave * kCopies + (lane & (kCopies - 1));
     const uint32_t wbase = part * kTile + (uint32_t)wave * (64u * IPT);
     // every load first (clamped index, no branch), then the counting
     uint32_t dg[IPT], wv[MODE == kLast ? IPT : 1];
@@ -157,14 +162,21 @@ __global__ __launch_bounds__(kSortThreads) void sort_upsweep_kernel(
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         if (keep[j]) {
-            atomicAdd(&s_h[wave][dg[j]], 1u);
-            if (MODE == kLast) atomicAdd(&s_w[wave][dg[j]], carried_count(io, wv[j]));
+            atomicAdd(&s_h[row][dg[j]], 1u);
+            if (MODE == kLast) atomicAdd(&s_w[row][dg[j]], carried_count(io, wv[j]));
         }
     }
     __syncthreads();
-    counts[(size_t)part * kRadix + tid] = s_h[0][tid] + s_h[1][tid] + s_h[2][tid] + s_h[3][tid];
-    if (MODE == kLast)
-        weights[(size_t)part * kRadix + tid] = s_w[0][tid] + s_w[1][tid] + s_w[2][tid] + s_w[3][tid];
+    uint32_t hc = 0;
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) hc += s_h[r][tid];
+    counts[(size_t)part * kRadix + tid] = hc;
+    if (MODE == kLast) {
+        uint32_t wc = 0;
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) wc += s_w[r][tid];
+        weights[(size_t)part * kRadix + tid] = wc;
+    }
 }
 
 // The partitions holding keys are cut into kChunks chunks of L consecutive
