@@ -237,10 +237,11 @@ def test_split_blend_pair_count(split_all):
 @pytest.mark.parametrize("W,H,log_scale", [(3840, 2160, -3.6), (7680, 4320, -3.6),
                                            (3840, 2160, -2.2)])
 def test_full_parity_large_grids(W, H, log_scale):
-    """Tile grids of 240 x 135 and 480 x 270 (two and three 8-bit tile-sort
-    passes over 15- and 17-bit tile ids), and 35M keys on the first (the
-    radix column scan's long-table path, key buffers grown after an
-    overflow): lists bit-exact, colour on sampled tiles."""
+    """Tile grids of 240 x 135 and 480 x 270 (tile-sort passes of 8 + 7 and
+    6 + 6 + 5 bits over 15- and 17-bit tile ids; the tile order in several
+    rounds), and 35M keys on the first (the radix column scan's long-table
+    path, key buffers grown after an overflow): lists bit-exact, colour on
+    sampled tiles."""
     sc = synth.small_scene(20_000, 13, degree=1, log_scale_mean=log_scale)
     cam = synth.make_camera(synth.look_at((0.0, -3.0, 1.0), (0, 0, 0)), W, H)
     TX, TY = cam.tiles
