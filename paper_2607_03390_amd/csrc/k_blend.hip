@@ -54,6 +54,20 @@ __device__ inline uint32_t quad_bcast_u(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, K | (K << 2) | (K << 4) | (K << 6), 0xf,
                                               0xf, false);
 }
+// Inclusive prefix sum over the wave's lanes, in lane order, of four byte
+// fields at once (no field's total may exceed 255): within rows of 16 lanes
+// by shifts of 1, 2, 4 and 8, then the rows' totals by the row broadcasts of
+// lanes 15 and 31.
+__device__ inline uint32_t wave_incl_sum_bytes(uint32_t x) {
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return x;
+}
+
 // Sum over each group of four lanes (quad_perm [1,0,3,2], then [2,3,0,1]).
 __device__ inline float quad_sum(float v) {
     v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xb1,
@@ -80,8 +94,7 @@ struct BlendLds {
     float4 col[256];
     int idx[256];
     __align__(16) uint8_t list[16][256];
-    __align__(16) uint32_t cnt[4][16];   // [staging wave][list] entries, then starts
-    uint32_t len[16];                    // list lengths
+    __align__(16) uint16_t mask[256];   // sub-blocks each staged Gaussian meets
 };
 
 // One 16x16 tile, or (QUAD) one 8x8 quadrant q of it.
@@ -215,51 +228,46 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
                 if (QUAD) lists &= 0xfu << (4 * q);
             }
         }
-        // order-preserving compaction of each sub-block's Gaussians: counts
-        // per staging wave, then each wave's start in every list (s.cnt
-        // becomes the exclusive prefix over waves, s.len the totals), then
-        // the entries (the votes are taken again rather than kept live)
-#pragma unroll
-        for (int L = 0; L < 16; ++L) {
-            if (QUAD && (L >> 2) != q) continue;
-            const uint64_t bal = __ballot((lists >> L) & 1u);
-            if (lane == 0) s.cnt[wave][L] = (uint32_t)__popcll(bal);
-        }
+        // Order-preserving compaction: every staged Gaussian's sub-block
+        // bits go to LDS, then each wave builds the lists it walks (tile:
+        // its four sub-blocks; quadrant: its one) from all the staged
+        // Gaussians.  Lane l takes slots 4l .. 4l + 3; its entries' offsets
+        // are one wave-wide prefix sum of its per-list counts, four lists
+        // packed one byte each (a list holds at most 255 entries).
+        s.mask[tid] = (uint16_t)lists;
         __syncthreads();
-        if (QUAD ? (tid >= 4 * q && tid < 4 * q + 4) : tid < 16) {
-            uint32_t run = 0;
+        constexpr int kNL = QUAD ? 1 : 4;
+        const int L0 = QUAD ? my_list : 4 * wave;
+        const uint2 m4 = reinterpret_cast<const uint2 *>(s.mask)[lane];
+        uint32_t own[kNL], packed = 0;
 #pragma unroll
-            for (int w2 = 0; w2 < 4; ++w2) {
-                const uint32_t c = s.cnt[w2][tid];
-                s.cnt[w2][tid] = run;
-                run += c;
+        for (int gl = 0; gl < kNL; ++gl) {
+            const uint32_t L = (uint32_t)(L0 + gl);
+            // bit k: slot 4 lane + k meets sub-block L
+            own[gl] = __builtin_amdgcn_ubfe(m4.x, L, 1) | __builtin_amdgcn_ubfe(m4.x, 16 + L, 1) << 1 |
+                      __builtin_amdgcn_ubfe(m4.y, L, 1) << 2 | __builtin_amdgcn_ubfe(m4.y, 16 + L, 1) << 3;
+            packed |= (uint32_t)__popc(own[gl]) << (8 * gl);
+        }
+        const uint32_t incl = wave_incl_sum_bytes(packed);
+        const uint32_t excl = incl - packed;
+        const uint32_t tot = __builtin_amdgcn_readlane(incl, 63);
+        uint32_t n_long = 0;
+#pragma unroll
+        for (int gl = 0; gl < kNL; ++gl) {
+            uint8_t *dst = &s.list[L0 + gl][0];
+            uint32_t o = (excl >> (8 * gl)) & 255u;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if ((own[gl] >> k) & 1u) dst[o] = (uint8_t)(4 * lane + k);
+                o += (own[gl] >> k) & 1u;
             }
-            s.len[tid] = run;
+            n_long = max(n_long, (tot >> (8 * gl)) & 255u);
         }
-        __syncthreads();
-        // an empty constraint (no code): the bits are extracted again here
-        // instead of sixteen of them living across the barriers
-        __asm__ volatile("" : "+v"(lists));
-        // the wave's 16 list starts in four 16-byte LDS loads
-        uint4 st4[4];
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) st4[qq] = reinterpret_cast<const uint4 *>(&s.cnt[wave][0])[qq];
-#pragma unroll
-        for (int L = 0; L < 16; ++L) {
-            if (QUAD && (L >> 2) != q) continue;
-            const uint64_t bal = __ballot((lists >> L) & 1u);
-            const uint4 v4 = st4[L >> 2];
-            const uint32_t st = (L & 3) == 0 ? v4.x : (L & 3) == 1 ? v4.y : (L & 3) == 2 ? v4.z : v4.w;
-            if ((lists >> L) & 1u) s.list[L][(uint32_t)__popcll(bal & lt_mask) + st] = (uint8_t)tid;
-        }
-        // the wave's trip count, the same for every lane (kept on scalar
+        // the wave's trip count, the same for every lane (on scalar
         // registers): its longest list (tile; shorter lists are padded), or
-        // its list's length rounded up to whole groups of four (quadrant)
-        const uint32_t n_long = QUAD
-            ? (__builtin_amdgcn_readfirstlane(s.len[my_list]) + 3u) & ~3u
-            : __builtin_amdgcn_readfirstlane(max(max(s.len[4 * wave], s.len[4 * wave + 1]),
-                                                 max(s.len[4 * wave + 2], s.len[4 * wave + 3])));
-        __syncthreads();
+        // its list's length rounded up to whole groups of four (quadrant).
+        // The wave reads only the lists it wrote: no barrier before the walk.
+        if (QUAD) n_long = (n_long + 3u) & ~3u;
         {
             const uint32_t kn = b + kBatch + tid;
             nidx = (tid < kBatch && kn < range.y) ? (int)a.vals[kn] : 0;
