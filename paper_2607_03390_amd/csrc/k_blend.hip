@@ -571,8 +571,11 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
     }
 }
 
+// Eight waves per SIMD (64 VGPRs); the capture variants, which carry the
+// Eq. 1/2 sums as well, at seven (72 VGPRs) so that nothing spills to
+// scratch.
 template <bool CAPTURE, bool CONTRIB, bool COUNT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void blend_kernel(BlendArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAPTURE ? 7 : 8))) void blend_kernel(BlendArgs a) {
     __shared__ BlendLds s;
     // block roles (block-uniform): with a split count ns, the first
     // nq = 4 ceil8(ns) blocks take the quadrants of the first ns tiles of the
