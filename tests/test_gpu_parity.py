@@ -78,11 +78,11 @@ def test_full_parity_ragged(n, seed, deg, W, H):
     _full_parity(sc, cams, label=f"ragged {W}x{H}")
 
 
-def test_full_render_order_reuse_across_sizes():
-    """Frames that render every tile blend in the order the previous such
-    frame's blend launch computed on the same tile grid (the first frame on a
-    grid computes its own): renders at changing sizes on one scene equal, bit
-    for bit, the renders of a scene that sees each camera once."""
+def test_full_render_independent_of_earlier_sizes():
+    """A render depends on its inputs only, not on the frames before it (the
+    scene's workspace, blend order and split set are the frame's own):
+    renders at changing sizes on one scene equal, bit for bit, the renders
+    of a scene that sees each camera once."""
     sc = synth.small_scene(3000, 1, degree=3)
     eyes = ((0.2, -3.0, 0.7), (2.5, 1.0, -0.4), (0.0, -1.2, 0.1), (1.0, 2.0, 0.3), (-2.0, 0.5, 0.2))
     sizes = ((200, 136), (64, 64), (200, 136), (200, 136), (37, 53))
@@ -96,10 +96,10 @@ def test_full_render_order_reuse_across_sizes():
             assert np.array_equal(got[k], ref[k]), (k, c.width, c.height)
 
 
-def test_full_render_order_after_split_change():
-    """A stored blend order (and its split count) is reused only under the
-    split settings it was computed with: alternating split caps on one scene
-    of long lists give the renders of fresh scenes with each cap."""
+def test_full_render_after_split_change():
+    """The quadrant split follows the scene's current setting: alternating
+    split caps on one scene of long lists give the renders of fresh scenes
+    with each cap."""
     sc = synth.scene_uniform_cube(24_000, 11, degree=0, log_scale_mean=-2.6)
     cam = synth.make_camera(synth.look_at((0.0, -7.0, 0.5), (0, 0, 0)), 48, 40)
     caps = ((0, 40), (0, 8), (0, 40), (0, 8))
