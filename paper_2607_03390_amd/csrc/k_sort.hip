@@ -1,5 +1,5 @@
-// LSD radix sort of (uint32 key, uint32 value) pairs, 8-bit digits, for the
-// two sorts of a frame (Sec. III-A, per-tile depth order):
+// LSD radix sort of (uint32 key, uint32 value) pairs, digits of up to 8
+// bits, for the two sorts of a frame (Sec. III-A, per-tile depth order):
 //  1. the Gaussians that have keys, by depth (float bits of a positive depth
 //     are ordered like the depths), input in Gaussian index order;
 //  2. the Gaussian-tile keys by tile id, input in depth order.
@@ -8,9 +8,9 @@
 // of the 64-bit (tile, depth) keys, at a third of the HBM traffic (the depth
 // passes run over the Gaussians, not over their tile copies).
 //
-// Structure for gfx950, per 8-bit pass: an upsweep kernel counts each
-// partition's digits (1024 keys per partition for an expected count up to 2M
-// keys, 3840 above) into
+// Structure for gfx950, per pass: an upsweep kernel counts each partition's
+// digits (1024 keys per partition for an expected count up to 2M keys, 3840
+// above, 5120 for 16-bit keys) into
 // a partition-major table, a column scan turns those counts into offsets
 // within 16 chunks of partitions plus per-chunk digit sums, and a downsweep
 // kernel ranks each partition in LDS and scatters it (the digit bases are a
@@ -19,6 +19,9 @@
 // atomics serialise across the eight XCDs), so the sort is deterministic and
 // needs no forward-progress assumption.  Ranking is stable (a wave's 64-lane
 // match over the digit bits plus per-wave digit counters in input order).
+// A pass sorts only the bits its keys can have: the tile sort spreads the
+// tile id's bits evenly over its passes, and the top depth digit has 7 bits
+// (depths are positive).
 // Keys are staged in LDS in digit order before the scatter so that writes of
 // one digit run are contiguous.  Key counts live on the device (grids sized
 // for an upper bound; partitions past the count do no work and are not
