@@ -322,7 +322,7 @@ tgs_status tgs_profile_stop(tgs_profile *out);
  * and the temporal states bound to it).  Both ways give identical per-tile
  * lists (depth bits, then Gaussian index):
  *   TGS_SORT_DEPTH_FIRST: the Gaussians with keys are radix-sorted by depth
- *     (four 8-bit passes over them), keys are emitted in that order and
+ *     (four passes of at most 8 bits over them), keys are emitted in that order and
  *     stably radix-sorted by tile;
  *   TGS_SORT_PER_TILE: key counts are scanned in index order, keys emitted
  *     in index order and stably sorted by tile, then one block per tile

@@ -10,9 +10,10 @@
 //     duplication and tile-sort kernels as the depth-ordered path), so each
 //     tile's list comes out in index order.
 //  3. One block per tile sorts its list by (depth bits, Gaussian index): a
-//     stable LSD radix sort on the depth bits (four 8-bit passes, the list
-//     in index order stays in index order among equal depths) with the
-//     (depth key, index) pairs in LDS and 1-8 entries per thread, for lists
+//     stable LSD radix sort on the depth bits (passes of 8, 8, 8 and 7 bits,
+//     depths being positive; the list in index order stays in index order
+//     among equal depths) with the (depth key, index) pairs in LDS and 1-8
+//     entries per thread, for lists
 //     of up to 4096 entries; the same sort over global memory for longer
 //     ones (correct for any length, meant for the rare list that outgrows
 //     the bound).

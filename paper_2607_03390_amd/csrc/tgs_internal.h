@@ -209,8 +209,9 @@ int sort_passes_for_bits(int bits);
 // Scratch words of a sort of at most max_keys keys (either kind below).
 size_t sort_scratch_words(uint32_t max_keys);
 // Stable LSD sort of (key, value) pairs on key bits [begin_bit, begin_bit +
-// bits), in passes of 8 bits; every key must be below 2^(begin_bit + bits).  The key count is *n_dev if n_dev is not NULL (n_max bounds it),
-// else n_max.  Returns 1 if the result is in the alt buffers.
+// bits), in ceil(bits / 8) passes of (nearly) equal width; every key must be
+// below 2^(begin_bit + bits).  The key count is *n_dev if n_dev is not NULL
+// (n_max bounds it), else n_max.  Returns 1 if the result is in the alt buffers.
 // n_hint: the expected key count (e.g. a recent frame's); it picks the
 // partition size (small partitions fill the chip for small sorts).
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int begin_bit,
