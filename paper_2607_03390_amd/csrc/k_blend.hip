@@ -138,7 +138,6 @@ __device__ __attribute__((always_inline)) inline void blend_block(const BlendArg
     __asm__ volatile("" : "+v"(fpx), "+v"(fpy));
     const float tile_x0 = (float)(tx * kTile), tile_y0 = (float)(ty * kTile);
     const uint2 range = a.ranges[tile];
-    const uint64_t lt_mask = (1ull << lane) - 1ull;
 
     float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
     float sw = 0.0f, s1 = 0.0f, s2 = 0.0f, d0 = 0.0f;

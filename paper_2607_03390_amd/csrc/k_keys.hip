@@ -72,6 +72,8 @@ struct DupIo {
     int TX;
     int n_tiles;
     uint2 *ranges;   // cleared by the first kernel of the emission
+    uint32_t *rows;  // optional: digit counts of each block's keys for the tile sort
+    int row_bits;    // width of that digit (key bits [0, row_bits))
 };
 
 // Window of the Gaussians owning output positions [P0, P1) (P0 a multiple
@@ -151,7 +153,9 @@ __device__ inline void dup_owners(const DupIo &io, uint32_t P0, uint32_t P1, uin
 // come from the key-block table and the window of Gaussians starting inside
 // the block (dup_owners).  Past the key capacity (cnt->n_sorted == 0 with
 // keys) nothing is emitted: the host grows the buffers and renders the
-// frame again.
+// frame again.  With io.rows, the block also counts its keys' first
+// tile-sort digit into row blockIdx.x (LDS counters per wave), so that the
+// sort's first pass needs no counting launch of its own.
 constexpr int kDupKeys = kKeyBlock;
 
 __global__ __launch_bounds__(256) void duplicate_kernel(DupIo io, uint32_t *tkey, uint32_t *tval) {
@@ -159,12 +163,17 @@ __global__ __launch_bounds__(256) void duplicate_kernel(DupIo io, uint32_t *tkey
     __shared__ uint32_t s_off[kDupKeys];
     __shared__ uint32_t s_g[kDupKeys];
     __shared__ int s_wmax[4];
+    __shared__ uint32_t s_hist[4][256];
     const int tid = threadIdx.x;
     for (int t = blockIdx.x * blockDim.x + tid; t < io.n_tiles; t += gridDim.x * blockDim.x)
         io.ranges[t] = make_uint2(0u, 0u);
     const uint32_t V = io.cnt->n_visible, K = io.cnt->n_sorted;
     const uint32_t P0 = blockIdx.x * (uint32_t)kDupKeys;
     if (K == 0u || P0 >= K) return;   // block-uniform
+    if (io.rows) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) s_hist[w][tid] = 0u;   // ordered by dup_owners' barriers
+    }
     const uint32_t P1 = K - P0 < (uint32_t)kDupKeys ? K : P0 + kDupKeys;
     dup_owners<kDupKeys, 256>(io, P0, P1, K, V, s_owner, s_off, s_g, s_wmax);
     // positions past the keys take the last key's owner (no branch before
@@ -186,9 +195,16 @@ __global__ __launch_bounds__(256) void duplicate_kernel(DupIo io, uint32_t *tkey
         int tx, ty;
         key_tile_xy(r[k], rc[k], io.rowpre, io.sel_cols, io.TX, tx, ty);
         if (p < P1) {
-            tkey[p] = (uint32_t)(ty * io.TX + tx);
+            const uint32_t key = (uint32_t)(ty * io.TX + tx);
+            tkey[p] = key;
             tval[p] = g[k];
+            if (io.rows) atomicAdd(&s_hist[tid >> 6][key & ((1u << io.row_bits) - 1u)], 1u);
         }
+    }
+    if (io.rows) {
+        __syncthreads();
+        io.rows[(size_t)blockIdx.x * 256 + tid] = s_hist[0][tid] + s_hist[1][tid] + s_hist[2][tid] +
+                                                  s_hist[3][tid];
     }
 }
 
@@ -242,13 +258,15 @@ __global__ __launch_bounds__(1024) void order_tiles_kernel(OrderK o) {
 void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
                       const uint32_t *offs, const uint32_t *kfirst, const ushort4 *rect,
                       const uint32_t *rowpre, const int *sel_cols, int TX, int n_tiles,
-                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st) {
+                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, uint32_t *rows, int row_bits,
+                      hipStream_t st) {
     if (n <= 0 || cap == 0) {
         ranges_zero_kernel<<<(n_tiles + 255) / 256, 256, 0, st>>>(n_tiles, ranges);
         return;
     }
     const uint32_t blocks = (cap + kDupKeys - 1) / kDupKeys;
-    const DupIo io{cnt, didx, offs, kfirst, rect, rowpre, sel_cols, TX, n_tiles, ranges};
+    const DupIo io{cnt, didx, offs, kfirst, rect, rowpre, sel_cols, TX, n_tiles, ranges,
+                   row_bits > 0 ? rows : nullptr, row_bits};
     duplicate_kernel<<<blocks, 256, 0, st>>>(io, tkey, tval);
 }
 

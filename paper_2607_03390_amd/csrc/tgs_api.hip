@@ -518,21 +518,27 @@ tgs_status step_keys(const tgs_scene *sc, Workspace &ws, int TX, int TY, const u
     const int n = sc->n;
     const uint32_t cap = (uint32_t)ws.key_cap;
     Counters *cnt = ws.cnt.as<Counters>();
+    const int bits = tile_id_bits(TX, TY);
+    const uint32_t hint = ws.recent_K[rowpre ? 1 : 0];
+    // the emission counts the tile sort's first digit per block of keys
+    // (where the sort's partitions are whole blocks), in place of that
+    // pass's counting launch
+    const bool counted = sort_takes_rows(cap, hint, 0, bits);
     {
         ProfScope ps(TGS_PROF_DUPLICATE, st);
         launch_duplicate(n, cap, cnt, didx, ws.offs.as<uint32_t>(), ws.kfirst.as<uint32_t>(),
                          ws.rect.as<ushort4>(), rowpre, sel_cols, TX, TX * TY,
-                         ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(), ws.ranges.as<uint2>(), st);
+                         ws.tkey.as<uint32_t>(), ws.tval.as<uint32_t>(), ws.ranges.as<uint2>(),
+                         sort_count_rows(ws.sort.as<uint32_t>()),
+                         counted ? sort_first_digit_bits(bits) : 0, st);
         TGS_LAUNCHED("duplicate");
     }
     int alt = 0;
     {
         ProfScope ps(TGS_PROF_SORT, st);
-        alt = launch_sort_u32(&cnt->n_sorted, cap, ws.recent_K[rowpre ? 1 : 0], 0,
-                              tile_id_bits(TX, TY),
-                              ws.tkey.as<uint32_t>(),
+        alt = launch_sort_u32(&cnt->n_sorted, cap, hint, 0, bits, ws.tkey.as<uint32_t>(),
                               ws.tval.as<uint32_t>(), ws.tkey_alt.as<uint32_t>(),
-                              ws.tval_alt.as<uint32_t>(), ws.sort.as<uint32_t>(), st);
+                              ws.tval_alt.as<uint32_t>(), ws.sort.as<uint32_t>(), counted, st);
         TGS_LAUNCHED("tile sort");
     }
     const uint32_t *skeys = alt ? ws.tkey_alt.as<uint32_t>() : ws.tkey.as<uint32_t>();

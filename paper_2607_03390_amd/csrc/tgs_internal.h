@@ -175,10 +175,14 @@ __device__ inline void mark_key_blocks(uint32_t *kfirst, uint32_t nb, uint32_t s
 // (cap bounds n_sorted for the grid; nothing is emitted past the key
 // capacity) and clears the tile ranges (filled by launch_ranges after the
 // tile sort).  rowpre / sel_cols are NULL in frames that render every tile.
+// rows (optional): per block of kKeyBlock keys, the counts of the tile
+// sort's first digit (key bits [0, row_bits)) in row b of rows[b][256] (see
+// launch_sort_u32).
 void launch_duplicate(int n, uint32_t cap, const Counters *cnt, const uint32_t *didx,
                       const uint32_t *offs, const uint32_t *kfirst, const ushort4 *rect,
                       const uint32_t *rowpre, const int *sel_cols, int TX, int n_tiles,
-                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, hipStream_t st);
+                      uint32_t *tkey, uint32_t *tval, uint2 *ranges, uint32_t *rows,
+                      int row_bits, hipStream_t st);
 // Ranges of the cnt->n_sorted tile-sorted keys; cap bounds n_sorted for the grid.
 void launch_ranges(uint32_t cap, const Counters *cnt, const uint32_t *keys, uint2 *ranges,
                    hipStream_t st);
@@ -214,9 +218,17 @@ size_t sort_scratch_words(uint32_t max_keys);
 // (n_max bounds it), else n_max.  Returns 1 if the result is in the alt buffers.
 // n_hint: the expected key count (e.g. a recent frame's); it picks the
 // partition size (small partitions fill the chip for small sorts).
+// counted: the first pass's digit counts of every kKeyBlock keys are
+// already in sort_count_rows(scratch) (written by the key emission), so that
+// pass has no counting launch; allowed only where sort_takes_rows says so.
 int launch_sort_u32(const uint32_t *n_dev, uint32_t n_max, uint32_t n_hint, int begin_bit,
                     int bits, uint32_t *keys, uint32_t *vals, uint32_t *keys_alt,
-                    uint32_t *vals_alt, uint32_t *scratch, hipStream_t st);
+                    uint32_t *vals_alt, uint32_t *scratch, bool counted, hipStream_t st);
+// Whether launch_sort_u32 with these sizes can take counted rows, and the
+// width of its first digit; where the rows go in its scratch.
+bool sort_takes_rows(uint32_t n_max, uint32_t n_hint, int begin_bit, int bits);
+int sort_first_digit_bits(int bits);
+uint32_t *sort_count_rows(uint32_t *scratch);
 // Depth order of the Gaussians with count[i] > 0 among i < n, stable by index
 // (keys dkey[i], the depth's float bits): four passes (dkey -> a -> b -> a ->
 // v_b; k_b may alias dkey).  With rowpre (a selective-rendering frame) the
