@@ -260,6 +260,30 @@ def test_sh_matches_textbook_real_harmonics():
             used.add(hit[0])
 
 
+def test_sh_basis_signs_and_order():
+    """The basis, sign for sign: function l^2 + l + m (m = -l .. l) is the
+    real harmonic built from scipy's complex harmonics, which carry the
+    Condon-Shortley phase: sqrt(2) Im Y_l^|m| for m < 0, Y_l^0, sqrt(2) Re
+    Y_l^m for m > 0 (the convention of the cited 3DGS renderer's colour
+    model, e.g. function 1 = -sqrt(3 / 4 pi) y).  A flipped sign or a swapped
+    pair of functions fails here, which the orthonormality and +/- checks
+    above would let through."""
+    from scipy.special import sph_harm_y
+    dirs, _ = _sphere_quadrature(8, 16)
+    theta = np.arccos(np.clip(dirs[:, 2], -1, 1))
+    phi = np.arctan2(dirs[:, 1], dirs[:, 0])
+    Y = np.array([O.sh_basis(3, d) for d in dirs])
+    for l in range(4):
+        for m in range(-l, l + 1):
+            c = sph_harm_y(l, abs(m), theta, phi)
+            ref = math.sqrt(2) * c.imag if m < 0 else (c.real if m == 0 else math.sqrt(2) * c.real)
+            np.testing.assert_allclose(Y[:, l * l + l + m], ref, atol=1e-10, err_msg=f"l={l} m={m}")
+    # the first-degree functions in closed form
+    d = np.array([0.36, -0.48, 0.8])
+    c1 = math.sqrt(3.0 / (4.0 * math.pi))
+    np.testing.assert_allclose(O.sh_basis(1, d)[1:4], [-c1 * d[1], c1 * d[2], -c1 * d[0]], rtol=1e-12)
+
+
 # --------------------------------------------------------------------------
 # blending (Sec. III-A), depth moments (Eq. 1, Eq. 2)
 # --------------------------------------------------------------------------
